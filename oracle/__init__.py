@@ -1,0 +1,155 @@
+"""Sequential fp64 CPU oracle of the block-diffusion Gated Delta Rule.
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the CPU-baseline
+leg of the benchmark may import this package; the product library never does.
+
+The arithmetic lives in ``bdgdn_oracle.c`` (plain C, fp64, OpenMP over
+independent (sequence, v-head) units).  This module only marshals numpy arrays
+to it.  Each entry point follows the paper (FLARE, arXiv 2606.01774):
+
+* ``fwd_train``  -- two-stream training forward: clean causal recurrence
+  (eq. gdn-recurrence in its per-step form, eq. per-step-fwd) and noisy blocks
+  seeded from the clean boundary state with block-end readout (eq.
+  flare-gdn-schedule, eq. noisy-block-fwd); document packing per the
+  "Document-packed training" appendix.
+* ``denoise``    -- Diffusion-Trust denoise pass: reads the cached state, never
+  writes it (appendix "Differences between the denoise pass and the
+  state-update pass").
+* ``commit``     -- token-causal state-update pass that writes the state back.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "bdgdn_oracle.c")
+_LIB = os.path.join(_HERE, "libbdgdn_oracle.so")
+# The mutation tests point this at a deliberately broken copy of the oracle to show
+# that the pins catch it; nothing else sets it.
+_LIB_OVERRIDE = os.environ.get("BDGDN_ORACLE_LIB")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (IEEE fp64, no fast-math)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.run(["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-Wall",
+                        "-o", tmp, _SRC, "-lm"], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        path = _LIB_OVERRIDE or _LIB
+        if not _LIB_OVERRIDE and not os.path.exists(_LIB):
+            build(force=True)
+        lib = ctypes.CDLL(path)
+        P = ctypes.c_void_p
+        I = ctypes.c_int
+        D = ctypes.c_double
+        lib.oracle_fwd_train.argtypes = [I, I, I, P, I, I, I, I, I, D] + [P] * 14
+        lib.oracle_fwd_train.restype = I
+        lib.oracle_denoise.argtypes = [I, I, I, I, I, I, D, P, P] + [P] * 6
+        lib.oracle_denoise.restype = I
+        lib.oracle_commit.argtypes = [I, I, I, I, I, I, D, P, P] + [P] * 6
+        lib.oracle_commit.restype = I
+        lib.oracle_set_threads.argtypes = [I]
+        lib.oracle_max_threads.restype = I
+        _lib = lib
+    return _lib
+
+
+def set_threads(n: int) -> None:
+    _load().oracle_set_threads(int(n))
+
+
+def max_threads() -> int:
+    return int(_load().oracle_max_threads())
+
+
+def _f64(x):
+    if x is None:
+        return None
+    if hasattr(x, "detach"):  # torch tensor
+        x = x.detach().cpu().double().numpy()
+    return np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def fwd_train(q, k, v, g, beta, qn, kn, vn, gn, betan, *, block, scale,
+              cu_seqlens=None, h0=None, want_ht=True):
+    """Two-stream forward.
+
+    Shapes (non-packed): q,k [B,T,Hqk,dk]; v [B,T,Hv,dv]; g,beta [B,T,Hv].
+    Packed: the same with B == 1 and ``cu_seqlens`` [N+1] int offsets.
+    Returns (o, on, ht) as fp64 arrays; ht is [B or N, Hv, dk, dv] or None.
+    """
+    q, k, v, g, beta = map(_f64, (q, k, v, g, beta))
+    qn, kn, vn, gn, betan = map(_f64, (qn, kn, vn, gn, betan))
+    B, T, Hqk, dk = q.shape
+    Hv, dv = v.shape[2], v.shape[3]
+    cu = None
+    nseq = B
+    if cu_seqlens is not None:
+        cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+        nseq = cu.shape[0] - 1
+        assert B == 1 and int(cu[-1]) <= T
+    h0a = _f64(h0)
+    o = np.zeros((B, T, Hv, dv))
+    on = np.zeros((B, T, Hv, dv))
+    ht = np.zeros((nseq, Hv, dk, dv)) if want_ht else None
+    rc = _load().oracle_fwd_train(
+        B, T, nseq, _ptr(cu), Hqk, Hv, dk, dv, int(block), float(scale),
+        _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+        _ptr(qn), _ptr(kn), _ptr(vn), _ptr(gn), _ptr(betan),
+        _ptr(h0a), _ptr(o), _ptr(on), _ptr(ht))
+    if rc != 0:
+        raise RuntimeError(f"oracle_fwd_train failed: {rc}")
+    return o, on, ht
+
+
+def denoise(pool, q, k, v, g, beta, *, scale, slot=None):
+    """Block-end readout of R blocks seeded from pool[slot[r]].
+
+    pool [n_slots,Hv,dk,dv]; q,k [R,L,Hqk,dk]; v [R,L,Hv,dv]; g,beta [R,L,Hv].
+    Returns o [R,L,Hv,dv] (fp64).  The pool is not modified.
+    """
+    pool = _f64(pool)
+    q, k, v, g, beta = map(_f64, (q, k, v, g, beta))
+    R, L, Hqk, dk = q.shape
+    Hv, dv = v.shape[2], v.shape[3]
+    sl = None if slot is None else np.ascontiguousarray(np.asarray(slot, dtype=np.int32))
+    o = np.zeros((R, L, Hv, dv))
+    rc = _load().oracle_denoise(R, Hqk, Hv, dk, dv, L, float(scale), _ptr(pool), _ptr(sl),
+                                _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(o))
+    if rc != 0:
+        raise RuntimeError(f"oracle_denoise failed: {rc}")
+    return o
+
+
+def commit(pool, q, k, v, g, beta, *, scale, slot=None, want_o=True):
+    """Token-causal pass over R blocks; returns (new_pool, o or None) in fp64.
+
+    The input pool is copied; the returned pool holds the advanced states.
+    """
+    pool = _f64(pool).copy()
+    q, k, v, g, beta = map(_f64, (q, k, v, g, beta))
+    R, L, Hqk, dk = q.shape
+    Hv, dv = v.shape[2], v.shape[3]
+    sl = None if slot is None else np.ascontiguousarray(np.asarray(slot, dtype=np.int32))
+    o = np.zeros((R, L, Hv, dv)) if want_o else None
+    rc = _load().oracle_commit(R, Hqk, Hv, dk, dv, L, float(scale), _ptr(pool), _ptr(sl),
+                               _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(o))
+    if rc != 0:
+        raise RuntimeError(f"oracle_commit failed: {rc}")
+    return pool, o

@@ -1,0 +1,80 @@
+"""The oracle pins must catch plausible mistakes.
+
+Each case plants one mistake in a private copy of the oracle's C source (a
+dropped term, a wrong sign or index, a wrong seed, a wrong readout order, ...),
+compiles it, and runs the pin suite against it in a subprocess.  The suite must
+fail for every mutant.  Nothing here touches the product library or a GPU.
+"""
+import os
+import subprocess
+import sys
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "bdgdn_oracle.c")
+
+NOISY_LOOPS = """        for (long l = p0; l < p1; ++l)
+            gdr_step(Sn, d->dk, d->dv, row_qk(kn, d, l, h), row_v(vn, d, l, h),
+                     gate_at(gn, d, l, h), gate_at(betan, d, l, h), u);
+        for (long l = p0; l < p1; ++l)       /* block-end readout */
+            readout(Sn, d->dk, d->dv, row_qk(qn, d, l, h), d->scale, row_o(on, d, l, h));"""
+NOISY_PER_POSITION = """        for (long l = p0; l < p1; ++l) {
+            gdr_step(Sn, d->dk, d->dv, row_qk(kn, d, l, h), row_v(vn, d, l, h),
+                     gate_at(gn, d, l, h), gate_at(betan, d, l, h), u);
+            readout(Sn, d->dk, d->dv, row_qk(qn, d, l, h), d->scale, row_o(on, d, l, h));
+        }"""
+CLEAN_STEP = """            gdr_step(S, d->dk, d->dv, row_qk(k, d, t, h), row_v(v, d, t, h),
+                     gate_at(g, d, t, h), gate_at(beta, d, t, h), u);
+            readout(S, d->dk, d->dv, row_qk(q, d, t, h), d->scale, row_o(o, d, t, h));"""
+CLEAN_READ_FIRST = """            readout(S, d->dk, d->dv, row_qk(q, d, t, h), d->scale, row_o(o, d, t, h));
+            gdr_step(S, d->dk, d->dv, row_qk(k, d, t, h), row_v(v, d, t, h),
+                     gate_at(g, d, t, h), gate_at(beta, d, t, h), u);"""
+
+MUTANTS = {
+    "no_gating_decay": ("for (int i = 0; i < dk * dv; ++i) S[i] *= alpha;", ";"),
+    "alpha_sign": ("const double alpha = exp(g);", "const double alpha = exp(-g);"),
+    "prediction_sign": ("u[j] = beta * (v[j] - acc);", "u[j] = beta * (v[j] + acc);"),
+    "dropped_beta": ("u[j] = beta * (v[j] - acc);", "u[j] = (v[j] - acc);"),
+    "write_factor": ("S[i * dv + j] += k[i] * u[j];", "S[i * dv + j] += 0.5 * k[i] * u[j];"),
+    "readout_index": ("acc += S[i * dv + j] * q[i];", "acc += S[i * dv + j] * q[(i + 1) % dk];"),
+    "prediction_index": ("acc += S[i * dv + j] * k[i];", "acc += S[i * dv + j] * k[(i + 1) % dk];"),
+    "noisy_seed_zero": ("        memcpy(Sn, S, ssz * sizeof(double));",
+                        "        memset(Sn, 0, ssz * sizeof(double));"),
+    "noisy_not_reset": ("        memcpy(Sn, S, ssz * sizeof(double));",
+                        "        if (p0 == r0) memcpy(Sn, S, ssz * sizeof(double));"),
+    "noisy_per_position_readout": (NOISY_LOOPS, NOISY_PER_POSITION),
+    "clean_read_before_write": (CLEAN_STEP, CLEAN_READ_FIRST),
+    "noisy_uses_clean_keys": ("row_qk(kn, d, l, h), row_v(vn, d, l, h)",
+                              "row_qk(k, d, l, h), row_v(vn, d, l, h)"),
+    "clean_uses_noisy_gates": ("gate_at(g, d, t, h), gate_at(beta, d, t, h)",
+                               "gate_at(gn, d, t, h), gate_at(beta, d, t, h)"),
+    "gva_mapping": ("int hq = h / (d->h_v / d->h_qk);", "int hq = h % d->h_qk;"),
+    "doc_state_not_reset": ("                else memset(S, 0, ssz * sizeof(double));",
+                            "                else if (n == 0) memset(S, 0, ssz * sizeof(double));"),
+    "denoise_writes_pool": (
+        "                readout(Sn, dk, dv, row_qk(q, &d, l, h), scale, row_o(o, &d, l, h));",
+        "                readout(Sn, dk, dv, row_qk(q, &d, l, h), scale, row_o(o, &d, l, h));\n"
+        "            memcpy((double *)pool + ((size_t)s * h_v + h) * ssz, Sn, ssz * sizeof(double));"),
+    "commit_skips_last_token": ("for (long t = (long)r * L; t < (long)r * L + L; ++t) {",
+                                "for (long t = (long)r * L; t < (long)r * L + L - 1; ++t) {"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique"
+    with tempfile.TemporaryDirectory() as td:
+        path = os.path.join(td, "mutant.c")
+        lib = os.path.join(td, "libmutant.so")
+        open(path, "w").write(src.replace(old, new))
+        subprocess.run(["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-o", lib, path, "-lm"],
+                       check=True, capture_output=True)
+        env = dict(os.environ, BDGDN_ORACLE_LIB=lib, OMP_NUM_THREADS="2")
+        r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                            os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                           cwd=ROOT, env=env, capture_output=True, text=True, timeout=300)
+        assert r.returncode != 0, f"mutant {name} passed every pin:\n{r.stdout[-2000:]}"

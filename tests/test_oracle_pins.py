@@ -1,0 +1,402 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these compares the oracle with itself: each check is a closed form, an
+invariant stated by the paper, a special case that reduces to a textbook
+formula, or a brute-force evaluation in a different formulation (the unrolled
+product of transition matrices, in floating point and in exact rationals).
+
+Paper references (FLARE, arXiv 2606.01774): eq. gdn-recurrence (Sec. 3.1), the
+per-step expanded form eq. per-step-fwd, the two-stream schedule eq.
+flare-gdn-schedule (Sec. 3.2), eq. noisy-block-fwd and the block-end readout,
+the document-packing appendix, and the serving passes (Diffusion-Trust appendix).
+"""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+
+
+def _unit(rng, shape):
+    x = rng.standard_normal(shape)
+    return x / np.linalg.norm(x, axis=-1, keepdims=True)
+
+
+def _stream(rng, B, T, hqk, hv, dk, dv):
+    return dict(
+        q=_unit(rng, (B, T, hqk, dk)), k=_unit(rng, (B, T, hqk, dk)),
+        v=rng.standard_normal((B, T, hv, dv)),
+        g=-np.log1p(np.exp(rng.uniform(-6, -2, (B, T, hv)))),
+        beta=1.0 / (1.0 + np.exp(-rng.uniform(-2, 2, (B, T, hv)))))
+
+
+def _two(rng, B, T, hqk, hv, dk, dv):
+    c = _stream(rng, B, T, hqk, hv, dk, dv)
+    n = _stream(rng, B, T, hqk, hv, dk, dv)
+    return c, n
+
+
+def _run(c, n, L, scale=1.0, **kw):
+    return oracle.fwd_train(c["q"], c["k"], c["v"], c["g"], c["beta"],
+                            n["q"], n["k"], n["v"], n["g"], n["beta"],
+                            block=L, scale=scale, **kw)
+
+
+# ---------------------------------------------------------------------------
+# Brute force: the unrolled product of eq. gdn-recurrence,
+#   S_t = (M_t ... M_1) S_0 + sum_i (M_t ... M_{i+1}) beta_i k_i v_i^T,
+#   M_t = alpha_t (I - beta_t k_t k_t^T).
+# ---------------------------------------------------------------------------
+def _unrolled_states(k, v, alpha, beta, S0):
+    T, dk = k.shape
+    M = [alpha[t] * (np.eye(dk) - beta[t] * np.outer(k[t], k[t])) for t in range(T)]
+    states = []
+    for t in range(T):
+        P = np.eye(dk)
+        for j in range(t, -1, -1):
+            P = P @ M[j]
+        acc = P @ S0
+        for i in range(t + 1):
+            Q = np.eye(dk)
+            for j in range(t, i, -1):
+                Q = Q @ M[j]
+            acc = acc + Q @ np.outer(beta[i] * k[i], v[i])
+        states.append(acc)
+    return states
+
+
+def _brute_two_stream(c, n, L, scale, b, h, S0, hv_per_qk=1):
+    """Brute-force clean and noisy outputs of sequence b, v-head h."""
+    hq = h // hv_per_qk
+    k, q, v = c["k"][b, :, hq], c["q"][b, :, hq], c["v"][b, :, h]
+    al, be = np.exp(c["g"][b, :, h]), c["beta"][b, :, h]
+    kn, qn, vn = n["k"][b, :, hq], n["q"][b, :, hq], n["v"][b, :, h]
+    aln, ben = np.exp(n["g"][b, :, h]), n["beta"][b, :, h]
+    T = k.shape[0]
+    Sc = _unrolled_states(k, v, al, be, S0)
+    o = np.stack([scale * Sc[t].T @ q[t] for t in range(T)])
+    on = np.zeros_like(o)
+    for p0 in range(0, T, L):
+        p1 = min(p0 + L, T)
+        seed = S0 if p0 == 0 else Sc[p0 - 1]
+        Sn = _unrolled_states(kn[p0:p1], vn[p0:p1], aln[p0:p1], ben[p0:p1], seed)[-1]
+        for l in range(p0, p1):
+            on[l] = scale * Sn.T @ qn[l]
+    return o, on, Sc[-1]
+
+
+@pytest.mark.parametrize("L", [1, 2, 3, 4])
+def test_pin_bruteforce_unrolled_product(L):
+    rng = np.random.default_rng(100 + L)
+    B, T, hqk, hv, dk, dv = 2, 7, 1, 2, 4, 3
+    c, n = _two(rng, B, T, hqk, hv, dk, dv)
+    h0 = rng.standard_normal((B, hv, dk, dv)) * 0.5
+    o, on, ht = _run(c, n, L, scale=0.7, h0=h0)
+    for b in range(B):
+        for h in range(hv):
+            bo, bon, bS = _brute_two_stream(c, n, L, 0.7, b, h, h0[b, h], hv_per_qk=hv // hqk)
+            np.testing.assert_allclose(o[b, :, h], bo, rtol=1e-12, atol=1e-12)
+            np.testing.assert_allclose(on[b, :, h], bon, rtol=1e-12, atol=1e-12)
+            np.testing.assert_allclose(ht[b, h], bS, rtol=1e-12, atol=1e-12)
+
+
+def test_pin_exact_rational_unrolled_product():
+    """Exact rational arithmetic (fractions) of the unrolled product; the oracle
+    receives g = log(alpha) and must agree to fp64 rounding."""
+    rng = np.random.default_rng(7)
+    T, dk, dv, L = 6, 3, 2, 2
+    fr = lambda x: Fraction(int(round(x * 16)), 16)
+    k = [[fr(x) for x in row] for row in rng.uniform(-1, 1, (T, dk))]
+    v = [[fr(x) for x in row] for row in rng.uniform(-1, 1, (T, dv))]
+    q = [[fr(x) for x in row] for row in rng.uniform(-1, 1, (T, dk))]
+    kn = [[fr(x) for x in row] for row in rng.uniform(-1, 1, (T, dk))]
+    vn = [[fr(x) for x in row] for row in rng.uniform(-1, 1, (T, dv))]
+    qn = [[fr(x) for x in row] for row in rng.uniform(-1, 1, (T, dk))]
+    al = [Fraction(int(n), 16) for n in rng.integers(12, 16, T)]
+    aln = [Fraction(int(n), 16) for n in rng.integers(12, 16, T)]
+    be = [Fraction(int(n), 8) for n in rng.integers(1, 8, T)]
+    ben = [Fraction(int(n), 8) for n in rng.integers(1, 8, T)]
+
+    def step(S, kk, vv, a, b):
+        # S = a (I - b k k^T) S + b k v^T, exactly
+        kS = [sum(kk[i] * S[i][j] for i in range(dk)) for j in range(dv)]
+        return [[a * (S[i][j] - b * kk[i] * kS[j]) + b * kk[i] * vv[j] for j in range(dv)]
+                for i in range(dk)]
+
+    def read(S, qq):
+        return [sum(S[i][j] * qq[i] for i in range(dk)) for j in range(dv)]
+
+    S = [[Fraction(0)] * dv for _ in range(dk)]
+    o_ex, on_ex = [], [None] * T
+    for p0 in range(0, T, L):
+        Sn = [row[:] for row in S]
+        for l in range(p0, p0 + L):
+            Sn = step(Sn, kn[l], vn[l], aln[l], ben[l])
+        for l in range(p0, p0 + L):
+            on_ex[l] = read(Sn, qn[l])
+        for t in range(p0, p0 + L):
+            S = step(S, k[t], v[t], al[t], be[t])
+            o_ex.append(read(S, q[t]))
+    arr = lambda x: np.array([[float(e) for e in r] for r in x])[None, :, None, :]
+    garr = lambda x: np.log(np.array([float(e) for e in x]))[None, :, None]
+    barr = lambda x: np.array([float(e) for e in x])[None, :, None]
+    c = dict(q=arr(q), k=arr(k), v=arr(v), g=garr(al), beta=barr(be))
+    n = dict(q=arr(qn), k=arr(kn), v=arr(vn), g=garr(aln), beta=barr(ben))
+    o, on, ht = _run(c, n, L)
+    np.testing.assert_allclose(o[0, :, 0], np.array([[float(e) for e in r] for r in o_ex]),
+                               rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(on[0, :, 0], np.array([[float(e) for e in r] for r in on_ex]),
+                               rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(ht[0, 0], np.array([[float(e) for e in r] for r in S]),
+                               rtol=1e-12, atol=1e-13)
+
+
+def test_pin_exact_overwrite():
+    """beta = 1 and ||k|| = 1 make the write an exact overwrite: S_t^T k_t = v_t.
+    With q_t = k_t the clean readout is s v_t; with q~ = k~ the last position of
+    each noisy block reads s v~ of that position (the block-end state holds it)."""
+    rng = np.random.default_rng(1)
+    B, T, dk, dv, L = 2, 12, 8, 5, 4
+    c, n = _two(rng, B, T, 1, 1, dk, dv)
+    for s in (c, n):
+        s["q"] = s["k"].copy()
+        s["beta"] = np.ones_like(s["beta"])
+    h0 = rng.standard_normal((B, 1, dk, dv))
+    o, on, _ = _run(c, n, L, scale=0.5, h0=h0)
+    np.testing.assert_allclose(o, 0.5 * c["v"], atol=1e-13)
+    np.testing.assert_allclose(on[:, L - 1::L], 0.5 * n["v"][:, L - 1::L], atol=1e-13)
+    o1, on1, _ = _run(c, n, 1, scale=0.5, h0=h0)
+    np.testing.assert_allclose(on1, 0.5 * n["v"], atol=1e-13)
+
+
+def test_pin_frozen_state():
+    """beta = 0 never writes: S_t = exp(sum g) h0, so o_t = s exp(G_t) h0^T q_t,
+    and a noisy block read decays by the clean prefix and its own gates."""
+    rng = np.random.default_rng(2)
+    B, T, hqk, hv, dk, dv, L = 1, 10, 1, 2, 6, 4, 4
+    c, n = _two(rng, B, T, hqk, hv, dk, dv)
+    c["beta"][:] = 0.0
+    n["beta"][:] = 0.0
+    h0 = rng.standard_normal((B, hv, dk, dv))
+    o, on, ht = _run(c, n, L, scale=0.3, h0=h0)
+    for h in range(hv):
+        G = np.cumsum(c["g"][0, :, h])
+        for t in range(T):
+            np.testing.assert_allclose(o[0, t, h], 0.3 * np.exp(G[t]) * h0[0, h].T @ c["q"][0, t, 0],
+                                       rtol=1e-12, atol=1e-14)
+        for p0 in range(0, T, L):
+            p1 = min(p0 + L, T)
+            dec = (G[p0 - 1] if p0 else 0.0) + n["g"][0, p0:p1, h].sum()
+            for l in range(p0, p1):
+                np.testing.assert_allclose(on[0, l, h], 0.3 * np.exp(dec) * h0[0, h].T @ n["q"][0, l, 0],
+                                           rtol=1e-12, atol=1e-14)
+        np.testing.assert_allclose(ht[0, h], np.exp(G[-1]) * h0[0, h], rtol=1e-12)
+    # g = 0 as well: the state is exactly h0
+    c["g"][:] = 0.0
+    o, _, ht = _run(c, n, L, scale=1.0, h0=h0)
+    np.testing.assert_array_equal(ht, h0)
+
+
+def test_pin_orthonormal_keys_is_linear_attention():
+    """With alpha = 1, h0 = 0 and mutually orthonormal keys across both streams the
+    prediction error is u = v, so the GDR reduces to linear attention:
+    o_t = s sum_{i<=t} beta_i (q_t.k_i) v_i, and a noisy block reads the clean
+    prefix plus its own writes."""
+    rng = np.random.default_rng(3)
+    T, dk, dv, L = 6, 16, 5, 3
+    Qm, _ = np.linalg.qr(rng.standard_normal((dk, dk)))
+    c, n = _two(rng, 1, T, 1, 1, dk, dv)
+    c["k"][0, :, 0] = Qm[:T]
+    n["k"][0, :, 0] = Qm[T:2 * T]
+    for s in (c, n):
+        s["g"][:] = 0.0
+    o, on, _ = _run(c, n, L, scale=0.9)
+    q, k, v, be = c["q"][0, :, 0], c["k"][0, :, 0], c["v"][0, :, 0], c["beta"][0, :, 0]
+    qn, kn, vn, ben = n["q"][0, :, 0], n["k"][0, :, 0], n["v"][0, :, 0], n["beta"][0, :, 0]
+    for t in range(T):
+        ref = sum(be[i] * (q[t] @ k[i]) * v[i] for i in range(t + 1))
+        np.testing.assert_allclose(o[0, t, 0], 0.9 * ref, atol=1e-13)
+    for p0 in range(0, T, L):
+        for l in range(p0, p0 + L):
+            ref = sum(be[i] * (qn[l] @ k[i]) * v[i] for i in range(p0))
+            ref = ref + sum(ben[j] * (qn[l] @ kn[j]) * vn[j] for j in range(p0, p0 + L))
+            np.testing.assert_allclose(on[0, l, 0], 0.9 * ref, atol=1e-13)
+
+
+def test_pin_single_token_from_zero():
+    rng = np.random.default_rng(4)
+    c, n = _two(rng, 1, 1, 1, 1, 7, 3)
+    o, on, ht = _run(c, n, 1, scale=0.25)
+    q, k, v, be = c["q"][0, 0, 0], c["k"][0, 0, 0], c["v"][0, 0, 0], c["beta"][0, 0, 0]
+    np.testing.assert_allclose(o[0, 0, 0], 0.25 * be * (q @ k) * v, rtol=1e-13)
+    np.testing.assert_allclose(ht[0, 0], be * np.outer(k, v), rtol=1e-13)
+
+
+def test_pin_block_one_reduces_to_causal_recurrence():
+    """L = 1 and identical noisy/clean inputs: each noisy block is one causal step
+    from the clean prefix, so the noisy output equals the clean output exactly."""
+    rng = np.random.default_rng(5)
+    c, _ = _two(rng, 2, 9, 1, 2, 5, 4)
+    n = {key: val.copy() for key, val in c.items()}
+    o, on, _ = _run(c, n, 1, scale=0.4)
+    np.testing.assert_array_equal(on, o)
+
+
+@pytest.mark.parametrize("L", [2, 3, 5])
+def test_pin_identical_streams_read_block_end_clean_state(L):
+    """Identical streams: the noisy block ending at p1 reads the clean state S_{p1},
+    so each position reads s S_{p1}^T q_l and the last position equals o there."""
+    rng = np.random.default_rng(6 + L)
+    T = 11
+    c, _ = _two(rng, 1, T, 1, 1, 4, 3)
+    n = {key: val.copy() for key, val in c.items()}
+    o, on, _ = _run(c, n, L)
+    for p0 in range(0, T, L):
+        p1 = min(p0 + L, T)
+        np.testing.assert_array_equal(on[0, p1 - 1], o[0, p1 - 1])
+        trunc = {key: val[:, :p1].copy() for key, val in c.items()}
+        _, _, ht = _run(trunc, trunc, L)
+        for l in range(p0, p1):
+            np.testing.assert_allclose(on[0, l, 0], ht[0, 0].T @ c["q"][0, l, 0], rtol=1e-12,
+                                       atol=1e-14)
+
+
+def test_pin_block_independence_and_clean_isolation():
+    """Perturbing the noisy inputs of one block changes only that block's noisy
+    outputs; the clean outputs and final state are untouched (Sec. 3.2: all
+    block-to-block flow passes through the clean stream)."""
+    rng = np.random.default_rng(8)
+    B, T, L = 1, 16, 4
+    c, n = _two(rng, B, T, 1, 1, 6, 4)
+    o, on, ht = _run(c, n, L)
+    n2 = {key: val.copy() for key, val in n.items()}
+    blk = slice(4, 8)
+    for key in ("q", "k", "v"):
+        n2[key][:, blk] += rng.standard_normal(n2[key][:, blk].shape)
+    n2["g"][:, blk] *= 0.5
+    n2["beta"][:, blk] *= 0.9
+    o2, on2, ht2 = _run(c, n2, L)
+    np.testing.assert_array_equal(o2, o)
+    np.testing.assert_array_equal(ht2, ht)
+    mask = np.zeros(T, bool)
+    mask[blk] = True
+    np.testing.assert_array_equal(on2[:, ~mask], on[:, ~mask])
+    assert np.abs(on2[:, mask] - on[:, mask]).min() > 0
+
+
+def test_pin_packed_equals_separate_documents():
+    """Packing: each document behaves as an independent sequence whose clean and
+    noisy states start from zero; the last document ends with a partial block."""
+    rng = np.random.default_rng(9)
+    L = 4
+    lengths = [8, 12, 4, 7]
+    Ttot = sum(lengths)
+    c, n = _two(rng, 1, Ttot, 1, 2, 5, 3)
+    cu = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+    o, on, ht = _run(c, n, L, scale=0.6, cu_seqlens=cu)
+    assert ht.shape[0] == len(lengths)
+    for d, (a, b) in enumerate(zip(cu[:-1], cu[1:])):
+        cs = {key: val[:, a:b].copy() for key, val in c.items()}
+        ns = {key: val[:, a:b].copy() for key, val in n.items()}
+        od, ond, htd = _run(cs, ns, L, scale=0.6)
+        np.testing.assert_array_equal(o[:, a:b], od)
+        np.testing.assert_array_equal(on[:, a:b], ond)
+        np.testing.assert_array_equal(ht[d], htd[0])
+
+
+def test_pin_partial_tail_equals_identity_padding():
+    """A partial last block behaves as if zero-padded with identity tokens
+    (k = 0, g = 0, beta = 0), the reading of the packed-tail rule."""
+    rng = np.random.default_rng(10)
+    T, L = 10, 4
+    c, n = _two(rng, 1, T, 1, 1, 5, 3)
+    o, on, ht = _run(c, n, L)
+    pad = 12 - T
+
+    def padded(s):
+        out = {}
+        for key, val in s.items():
+            z = np.zeros((1, pad) + val.shape[2:])
+            out[key] = np.concatenate([val, z], axis=1)
+        return out
+    o2, on2, ht2 = _run(padded(c), padded(n), L)
+    np.testing.assert_allclose(o2[:, :T], o, rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(on2[:, :T], on, rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(ht2, ht, rtol=1e-14, atol=1e-15)
+
+
+def test_pin_grouped_value_heads_map_consecutively():
+    """h_v = 2 h_qk: v-head h uses q/k head h // 2, i.e. the same result as
+    repeating each q/k head twice."""
+    rng = np.random.default_rng(11)
+    c, n = _two(rng, 1, 8, 2, 4, 4, 3)
+    o, on, ht = _run(c, n, 4)
+    rep = lambda s: {**s, "q": np.repeat(s["q"], 2, axis=2), "k": np.repeat(s["k"], 2, axis=2)}
+    o2, on2, ht2 = _run(rep(c), rep(n), 4)
+    np.testing.assert_array_equal(o, o2)
+    np.testing.assert_array_equal(on, on2)
+    np.testing.assert_array_equal(ht, ht2)
+
+
+# ----------------------------- serving passes -----------------------------
+def _serve_block(rng, R, L, hqk, hv, dk, dv):
+    s = _stream(rng, R, L, hqk, hv, dk, dv)
+    return s["q"], s["k"], s["v"], s["g"], s["beta"]
+
+
+def test_pin_denoise_is_noisy_block_of_training_schedule():
+    """A denoise pass from a cached prefix state equals the training schedule's
+    noisy output for the block that follows that prefix."""
+    rng = np.random.default_rng(12)
+    R, L, hv, dk, dv = 3, 4, 2, 5, 3
+    pool = rng.standard_normal((R, hv, dk, dv))
+    q, k, v, g, b = _serve_block(rng, R, L, 1, hv, dk, dv)
+    pool0 = pool.copy()
+    o = oracle.denoise(pool, q, k, v, g, b, scale=0.5)
+    np.testing.assert_array_equal(pool, pool0)
+    for r in range(R):
+        # the same block as the first block of a training sequence seeded by h0
+        n = dict(q=q[r:r + 1], k=k[r:r + 1], v=v[r:r + 1], g=g[r:r + 1], beta=b[r:r + 1])
+        _, on, _ = _run(n, n, L, scale=0.5, h0=pool[r:r + 1])
+        np.testing.assert_array_equal(o[r:r + 1], on)
+        # and the brute-force block-end state
+        for h in range(hv):
+            Sn = _unrolled_states(k[r, :, 0], v[r, :, h], np.exp(g[r, :, h]), b[r, :, h], pool[r, h])[-1]
+            np.testing.assert_allclose(o[r, :, h], 0.5 * (q[r, :, 0] @ Sn), rtol=1e-12, atol=1e-13)
+
+
+def test_pin_commit_is_causal_pass_and_writes_state():
+    rng = np.random.default_rng(13)
+    R, L, hv, dk, dv = 2, 5, 2, 4, 4
+    pool = rng.standard_normal((R + 1, hv, dk, dv))
+    slot = np.array([2, 0], np.int32)
+    q, k, v, g, b = _serve_block(rng, R, L, 1, hv, dk, dv)
+    newpool, o = oracle.commit(pool, q, k, v, g, b, scale=0.8, slot=slot)
+    np.testing.assert_array_equal(newpool[1], pool[1])        # untouched slot
+    for r, s in enumerate(slot):
+        for h in range(hv):
+            st = _unrolled_states(k[r, :, 0], v[r, :, h], np.exp(g[r, :, h]), b[r, :, h], pool[s, h])
+            np.testing.assert_allclose(newpool[s, h], st[-1], rtol=1e-12, atol=1e-13)
+            for t in range(L):
+                np.testing.assert_allclose(o[r, t, h], 0.8 * st[t].T @ q[r, t, 0], rtol=1e-12, atol=1e-13)
+
+
+def test_pin_denoise_after_commit_equals_training_schedule():
+    """denoise(commit(S, blk1), blk2) equals the training schedule's noisy output of
+    blk2 for the clean sequence [blk1] seeded with S."""
+    rng = np.random.default_rng(14)
+    L, hv, dk, dv = 4, 1, 4, 3
+    S = rng.standard_normal((1, hv, dk, dv))
+    b1 = _serve_block(rng, 1, L, 1, hv, dk, dv)
+    b2 = _serve_block(rng, 1, L, 1, hv, dk, dv)
+    S1, _ = oracle.commit(S, *b1, scale=1.0)
+    o2 = oracle.denoise(S1, *b2, scale=1.0)
+    # the clean stream is [blk1, anything]; the noisy stream's second block is blk2
+    junk = _serve_block(rng, 1, L, 1, hv, dk, dv)
+    cat = lambda a, b, i: np.concatenate([a[i], b[i]], axis=1)
+    keys = ("q", "k", "v", "g", "beta")
+    c = {key: cat(b1, junk, i) for i, key in enumerate(keys)}
+    n = {key: cat(junk, b2, i) for i, key in enumerate(keys)}
+    _, on, _ = _run(c, n, L, scale=1.0, h0=S)
+    np.testing.assert_array_equal(on[:, L:], o2)
