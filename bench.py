@@ -1,0 +1,187 @@
+"""Benchmark of the block-diffusion Gated DeltaNet hot path on one MI355X.
+
+A step is one two-stream training forward (bdgdn_fwd_train, clean + noisy streams)
+over the 4 x 4096-token, 16-head, d=128, L=32 workload with bf16 inputs, fp32
+state and fp32 outputs, inputs resident in HBM.  `value` is tokens/s (clean +
+noisy tokens).  The line also carries the roofline of the fused kernel (HBM
+bytes the algorithm must move per launch over its measured duration), the
+model-FLOP rate against the bf16/fp16 MFMA peak, the denoise_step bandwidth of
+the 64-request serving workload, and the fp64 CPU oracle timed on a bounded
+sample of the same workload.
+
+  python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, GB/s
+MFMA16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16/bf16 MFMA, TFLOP/s
+
+
+def algorithmic_bytes_train(w, out_bytes):
+    """Bytes the two-stream forward must move once: q, k per q/k head, v and o per
+    v head, g and beta per v head, for both streams."""
+    in_b = 2 if w.dtype == "bf16" else 4
+    per_row = (2 * w.h_qk * w.d_k * in_b + w.h_v * w.d_v * (in_b + out_bytes) + 2 * w.h_v * 4)
+    return 2 * w.tokens * per_row
+
+
+def model_flops_train(w, chunk=64):
+    """Work model: clean 6d^2 + 10Cd per (token, v-head) with C = 64, noisy
+    2d^2 + 12Ld; the Gram terms (4Cd + 4Ld) once per q/k head."""
+    d = w.d_k
+    per_v = 6 * d * d + 6 * chunk * d + 2 * d * d + 8 * w.block * d
+    per_qk = 4 * chunk * d + 4 * w.block * d
+    return w.tokens * (w.h_v * per_v + w.h_qk * per_qk)
+
+
+def algorithmic_bytes_denoise(w, out_bytes):
+    in_b = 2 if w.dtype == "bf16" else 4
+    rows = w.requests * w.block
+    state = w.requests * w.h_v * w.d_k * w.d_v * 4
+    return state + rows * (2 * w.h_qk * w.d_k * in_b + w.h_v * w.d_v * (in_b + out_bytes)
+                           + 2 * w.h_v * 4)
+
+
+def time_launches(fn, steps, warmup, stream):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        fn()
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps  # ms per launch
+
+
+def cpu_baseline(w, inp, max_units=None):
+    """The fp64 oracle on a bounded sample of the workload: whole sequences of one
+    (sequence, v-head) unit per host thread."""
+    import oracle
+    threads = max(1, min(os.cpu_count() or 1, 16))
+    oracle.set_threads(threads)
+    units = threads if max_units is None else min(threads, max_units)
+    b_idx = [u % w.batch for u in range(units)]
+    h_idx = [u // w.batch for u in range(units)]
+    keys = ("q", "k", "v", "g", "beta")
+
+    def sl(t, b, h):
+        return t[b:b + 1, :, h:h + 1]
+    import numpy as np
+    cat = {}
+    for key in keys:
+        for sfx in ("", "n"):
+            t = inp[key + sfx]
+            parts = [sl(t, b, h) for b, h in zip(b_idx, h_idx)]
+            cat[key + sfx] = np.concatenate([p.double().numpy() for p in parts], axis=0)
+    t0 = time.perf_counter()
+    oracle.fwd_train(*[cat[k] for k in keys], *[cat[k + "n"] for k in keys],
+                     block=w.block, scale=1.0 / math.sqrt(w.d_k), want_ht=False)
+    dt = time.perf_counter() - t0
+    tokens = 2 * units * w.seqlen
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": oracle.max_threads(),
+            "kind": "oracle", "seconds": dt,
+            "sample": f"{units} (sequence, v-head) units x {w.seqlen} clean + {w.seqlen} noisy "
+                      f"tokens of the same workload (one unit per thread); value = "
+                      f"tokens of the sample / wall time"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-serve", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+
+    import paper_2606_01774_amd as bd
+    from paper_2606_01774_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    w = W.TRAIN_4K
+    inp = W.make_train(w)
+    d = {k: v.to(dev) for k, v in inp.items()}
+    scale = 1.0 / math.sqrt(w.d_k)
+    o = torch.empty(w.batch, w.seqlen, w.h_v, w.d_v, dtype=torch.float32, device=dev)
+    on = torch.empty_like(o)
+
+    def step():
+        bd.bdgdn_fwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"],
+                           d["qn"], d["kn"], d["vn"], d["gn"], d["betan"],
+                           block=w.block, scale=scale, o=o, on=on, stream=stream)
+
+    torch.cuda.synchronize()
+    ms = time_launches(step, args.steps, args.warmup, stream)
+    tokens = 2 * w.tokens
+    value = tokens / (ms * 1e-3)
+    abytes = algorithmic_bytes_train(w, 4)
+    flops = model_flops_train(w)
+    achieved = abytes / (ms * 1e-3) / 1e9
+    result = {
+        "metric": "BD-GDN fwd tokens/s + % bf16 MFMA peak; denoise_step GB/s vs HBM peak",
+        "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; q,k L2-normalised N(0,1), v N(0,1), g=-softplus(U(-6,-2)), "
+                "beta=sigmoid(U(-2,2)))",
+        "config": {"workload": w.name, "batch": w.batch, "seq_len": w.seqlen,
+                   "h_qk": w.h_qk, "h_v": w.h_v, "d_k": w.d_k, "d_v": w.d_v, "block": w.block,
+                   "inputs": "bf16", "mfma_operands": "fp16", "state": "fp32", "outputs": "fp32",
+                   "route": "fused", "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "bdgdn_fwd_fused_kernel", "algorithmic_bytes": abytes},
+        "mfma": {"model_flop": flops, "tflops": flops / (ms * 1e-3) / 1e12,
+                 "frac_of_peak": flops / (ms * 1e-3) / 1e12 / MFMA16_PEAK_TFLOPS},
+    }
+
+    if not args.no_serve:
+        sw = W.SERVE_64
+        pools = [W.make_state_pool(sw.requests, sw.h_v, sw.d_k, sw.d_v, seed=sw.seed + i).to(dev)
+                 for i in range(3)]
+        blk = {k: v.to(dev) for k, v in W.make_serve_block(sw, 0).items()}
+        od = torch.empty(sw.requests, sw.block, sw.h_v, sw.d_v, dtype=torch.float32, device=dev)
+        it = [0]
+
+        def dstep():
+            pool = pools[it[0] % len(pools)]   # three pools: 384 MiB > the 256 MB MALL
+            it[0] += 1
+            bd.bdgdn_denoise_step(pool, blk["q"], blk["k"], blk["v"], blk["g"], blk["beta"],
+                                  scale=scale, o=od, stream=stream)
+        dms = time_launches(dstep, 3 * args.steps, args.warmup, stream)
+        dbytes = algorithmic_bytes_denoise(sw, 4)
+        gbs = dbytes / (dms * 1e-3) / 1e9
+        result["denoise_step"] = {"workload": sw.name, "us_per_call": dms * 1e3,
+                                  "gb_per_s": gbs, "frac_hbm": gbs / HBM_PEAK_GBS,
+                                  "algorithmic_bytes": dbytes,
+                                  "tokens_per_s": sw.requests * sw.block / (dms * 1e-3)}
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, inp)
+    print(json.dumps(result))
+
+
+if __name__ == "__main__":
+    main()

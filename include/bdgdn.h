@@ -1,0 +1,178 @@
+/*
+ * bdgdn.h -- C ABI of the block-diffusion Gated DeltaNet library (libbdgdn.so) for
+ * AMD MI355X (gfx950).
+ *
+ * The library computes the Gated Delta Rule (GDR) layer of FLARE's hybrid backbone
+ * (arXiv 2606.01774) under the block-diffusion clean/noisy schedule:
+ *
+ *   clean stream (Sec. 3.1, eq. gdn-recurrence; Appendix eq. per-step-fwd):
+ *     S_t = exp(g_t) (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T,
+ *     o_t = scale * S_t^T q_t                                (S is d_k x d_v)
+ *   noisy stream (Sec. 3.2, eq. flare-gdn-schedule; Appendix eq. noisy-block-fwd):
+ *     block b of L positions is seeded with the clean state after the last clean
+ *     position before the block, applies its own L noisy updates, and every
+ *     position of the block reads the block-end noisy state:
+ *     on_l = scale * Sn_end^T qn_l.
+ *   document packing (Appendix "Document-packed training"): documents start on
+ *     block boundaries, each starts from a zero state, the last block of a document
+ *     may be partial (treated as padded with identity positions).
+ *   serving (Appendix "Diffusion-Trust Sampling", "Differences between the denoise
+ *     pass and the state-update pass"): a denoise pass reads the cached state and
+ *     never writes it; a commit pass runs the token-causal update and writes it back.
+ *
+ * Conventions shared by every entry point
+ *   - Pointers named *_dev / tensors are device pointers (HIP device memory); the
+ *     only host pointers are the descriptors and cu_seqlens_host.
+ *   - Token tensors are token-major and contiguous:
+ *       q, k : [rows][h_qk][d_k]      v, o : [rows][h_v][d_v]     g, beta : [rows][h_v]
+ *     where rows = batch*seqlen (training) or num_req*block (serving).
+ *     q, k, v have the descriptor's dtype and o its out_dtype; g (the LOG gate,
+ *     alpha = exp(g)) and beta are fp32 and used as given.
+ *   - Arithmetic: states and all accumulations are fp32.  With bf16 inputs the MFMA
+ *     operands are fp16 (the bf16 values converted exactly; every rounded
+ *     intermediate keeps 11 significant bits), so inputs and intermediates must stay
+ *     within fp16 range: |q|, |k|, |v| and state entries below 2^15 (q and k are
+ *     normally L2-normalised); magnitudes below 2^-14 lose relative precision
+ *     (absolute error under 2^-25).  With fp32 inputs everything is fp32.
+ *   - v-head h reads q/k head h / (h_v / h_qk) (consecutive grouping).
+ *   - States are fp32 [unit][h_v][d_k][d_v], row-major (paper orientation).
+ *   - All work is enqueued on `stream` (a hipStream_t; NULL = default stream); no
+ *     call synchronises the host or allocates device memory.  Outputs are valid
+ *     once the stream reaches that point.
+ *   - Every argument is validated on the host before anything is launched.  On
+ *     any error return nothing is launched and no output is touched.
+ *   - q, k, v and the dtype outputs must be 16-byte aligned (BDGDN_ERR_INVALID_ARG).
+ *   - The caller owns every buffer.  Outputs must not alias inputs.
+ *   - Calls are thread-safe; the library keeps no mutable global state besides a
+ *     once-initialised table of kernel attributes.
+ *
+ * Supported: d_k, d_v in {64, 128}; 1 <= block <= 64; (dtype, out_dtype) in
+ * {(bf16, fp32), (bf16, bf16), (fp32, fp32)}, fp32 inputs with block <= 32.
+ * Anything else returns BDGDN_ERR_UNSUPPORTED.  fp32 outputs for bf16 inputs are the
+ * accuracy-grade choice: rounding an output to bf16 alone perturbs it by up to
+ * 2^-9 of its magnitude.
+ */
+#ifndef BDGDN_H
+#define BDGDN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BDGDN_OK               0
+#define BDGDN_ERR_INVALID_ARG -1 /* NULL required pointer, non-positive size, h_v % h_qk != 0,
+                                    non-finite scale, inconsistent cu_seqlens */
+#define BDGDN_ERR_UNSUPPORTED -2 /* (dtype, d_k, d_v, block) outside the supported set */
+#define BDGDN_ERR_UNALIGNED   -3 /* a document start cu_seqlens[i] (i < N) is not a multiple
+                                    of block (Appendix "Document-packed training") */
+#define BDGDN_ERR_WORKSPACE   -4 /* workspace smaller than bdgdn_fwd_train_workspace() */
+#define BDGDN_ERR_LAUNCH      -5 /* the HIP runtime reported an error for a launch */
+
+typedef enum { BDGDN_BF16 = 0, BDGDN_F32 = 1 } bdgdn_dtype_t;
+
+/* How the training forward is scheduled; both give the same result.
+ *  FUSED: one kernel per (sequence, v-head, d_v tile) carries the clean state on chip
+ *         and evaluates each noisy block from the in-register boundary state (the
+ *         fused two-stream schedule, Appendix "Route II").
+ *  SPLIT: block-local UT transform and masked Q K^T in one kernel, the clean scan
+ *         writing every block-boundary state to the workspace, and an independent
+ *         noisy-block kernel reading them (Appendix "Route I").  Needs a workspace. */
+typedef enum { BDGDN_ROUTE_FUSED = 0, BDGDN_ROUTE_SPLIT = 1 } bdgdn_route_t;
+
+typedef struct {
+    int32_t batch;     /* B sequences; must be 1 when packed (num_seqs > 0)            */
+    int32_t seqlen;    /* T tokens per sequence, or total packed tokens                 */
+    int32_t num_seqs;  /* N packed documents, 0 when not packed                         */
+    int32_t h_qk, h_v; /* q/k heads and v heads; h_v % h_qk == 0                        */
+    int32_t d_k, d_v;  /* head dimensions                                               */
+    int32_t block;     /* diffusion block size L                                        */
+    float scale;       /* output scale s (the paper uses 1/sqrt(d_k))                   */
+    int32_t dtype;     /* bdgdn_dtype_t of q, k, v                                      */
+    int32_t route;     /* bdgdn_route_t                                                 */
+    int32_t out_dtype; /* bdgdn_dtype_t of o, on                                        */
+} bdgdn_fwd_desc_t;
+
+typedef struct {
+    int32_t num_req;   /* R requests, one block of `block` tokens each                  */
+    int32_t h_qk, h_v, d_k, d_v;
+    int32_t block;     /* L                                                             */
+    float scale;
+    int32_t dtype;     /* bdgdn_dtype_t of q, k, v                                      */
+    int32_t out_dtype; /* bdgdn_dtype_t of o / o_causal                                 */
+} bdgdn_serve_desc_t;
+
+/* Library version, (major << 16) | minor. */
+int32_t bdgdn_version(void);
+
+/* Human-readable text of a status code (static storage). */
+const char *bdgdn_status_string(int status);
+
+/* Bytes of device workspace bdgdn_fwd_train needs for this descriptor (0 for the
+ * fused route), or 0 for a descriptor that bdgdn_fwd_train would reject. */
+size_t bdgdn_fwd_train_workspace(const bdgdn_fwd_desc_t *desc);
+
+/*
+ * Two-stream training forward (clean + noisy), Sec. 3.2 and Appendix "Gated Delta
+ * Rule: two-stream training".
+ *
+ *   q, k, v, g, beta       clean stream   ([B*T] rows, layouts above)
+ *   qn, kn, vn, gn, betan  noisy stream   (same shapes; gn/betan are the noisy
+ *                                          stream's own gates)
+ *   cu_seqlens_dev/_host   both NULL (B sequences of T tokens) or both [N+1] int32
+ *                          offsets into the packed axis (B == 1, cu[0] == 0,
+ *                          cu[N] == T, non-decreasing, cu[i] % block == 0 for i < N).
+ *                          The two copies must hold the same values.
+ *   h0                     [B or N][h_v][d_k][d_v] fp32 initial clean state, or NULL
+ *                          for zero.  Each sequence's first noisy block is seeded
+ *                          with the same state.
+ *   o, on                  [B*T][h_v][d_v] outputs of out_dtype (clean causal readout,
+ *                          noisy block-end readout); every row is written.
+ *   ht                     [B or N][h_v][d_k][d_v] fp32 final clean state, or NULL.
+ *   workspace              device memory of at least bdgdn_fwd_train_workspace(desc)
+ *                          bytes (may be NULL when that is 0).
+ * Returns BDGDN_OK or a negative status.
+ */
+int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc,
+                    const void *q, const void *k, const void *v,
+                    const float *g, const float *beta,
+                    const void *qn, const void *kn, const void *vn,
+                    const float *gn, const float *betan,
+                    const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                    const float *h0, void *o, void *on, float *ht,
+                    void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * One Diffusion-Trust denoise pass over R blocks (Appendix "Per-block denoise loop",
+ * "Differences between the denoise pass and the state-update pass").  Request r's
+ * block is seeded with state_pool[slot[r]] (slot == NULL means slot[r] = r) and every
+ * position reads the block-end state.  state_pool is only read.
+ *
+ *   state_pool  [n_slots][h_v][d_k][d_v] fp32 (device)
+ *   slot        [R] int32 device array of pool indices, or NULL
+ *   q, k, v     [R*L][h][d] (dtype); g, beta [R*L][h_v] fp32
+ *   o           [R*L][h_v][d_v] block-end readout (out_dtype)
+ * Slot indices are not range-checked on the device; they must be valid.
+ */
+int bdgdn_denoise_step(const bdgdn_serve_desc_t *desc, const float *state_pool,
+                       const int32_t *slot, const void *q, const void *k, const void *v,
+                       const float *g, const float *beta, void *o, void *stream);
+
+/*
+ * Token-causal state-update pass over R blocks (Appendix Algorithm "Diffusion-Trust
+ * serving loop", the forward that writes S back): state_pool[slot[r]] is advanced by
+ * the L tokens of request r, in place.  o_causal ([R*L][h_v][d_v], out_dtype) receives the
+ * causal readout when not NULL.  Slots must be distinct (calls with repeated slots
+ * race) and valid.
+ */
+int bdgdn_commit(const bdgdn_serve_desc_t *desc, float *state_pool, const int32_t *slot,
+                 const void *q, const void *k, const void *v,
+                 const float *g, const float *beta, void *o_causal, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BDGDN_H */

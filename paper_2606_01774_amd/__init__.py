@@ -1,0 +1,263 @@
+"""Block-diffusion Gated DeltaNet for AMD MI355X (gfx950): Python binding.
+
+A thin ctypes layer over ``libbdgdn.so`` (C ABI in ``include/bdgdn.h``).  The
+functions carry the C names and only marshal arguments: PyTorch supplies device
+memory and the current HIP stream; every step of the computation runs in the HIP
+kernels.  There is no CPU fallback: without the built library (or without a GPU)
+these functions raise.
+
+Layouts (token-major, contiguous): q, k ``[rows, h_qk, d_k]`` (or any leading
+shape that flattens to rows), v, o ``[rows, h_v, d_v]``, g (log-gate), beta
+``[rows, h_v]`` fp32; states ``[units, h_v, d_k, d_v]`` fp32.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+__all__ = [
+    "BdgdnError", "BDGDN_BF16", "BDGDN_F32", "BDGDN_ROUTE_FUSED", "BDGDN_ROUTE_SPLIT",
+    "bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace", "bdgdn_fwd_train",
+    "bdgdn_denoise_step", "bdgdn_commit", "library_path", "load_library", "EXPORTED_SYMBOLS",
+]
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_PKG, "libbdgdn.so")
+
+BDGDN_OK = 0
+BDGDN_ERR_INVALID_ARG = -1
+BDGDN_ERR_UNSUPPORTED = -2
+BDGDN_ERR_UNALIGNED = -3
+BDGDN_ERR_WORKSPACE = -4
+BDGDN_ERR_LAUNCH = -5
+BDGDN_BF16 = 0
+BDGDN_F32 = 1
+BDGDN_ROUTE_FUSED = 0
+BDGDN_ROUTE_SPLIT = 1
+
+EXPORTED_SYMBOLS = ("bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace",
+                    "bdgdn_fwd_train", "bdgdn_denoise_step", "bdgdn_commit")
+
+
+class FwdDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("seqlen", ctypes.c_int32),
+                ("num_seqs", ctypes.c_int32), ("h_qk", ctypes.c_int32),
+                ("h_v", ctypes.c_int32), ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32),
+                ("block", ctypes.c_int32), ("scale", ctypes.c_float),
+                ("dtype", ctypes.c_int32), ("route", ctypes.c_int32),
+                ("out_dtype", ctypes.c_int32)]
+
+
+class ServeDesc(ctypes.Structure):
+    _fields_ = [("num_req", ctypes.c_int32), ("h_qk", ctypes.c_int32),
+                ("h_v", ctypes.c_int32), ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32),
+                ("block", ctypes.c_int32), ("scale", ctypes.c_float),
+                ("dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32)]
+
+
+class BdgdnError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {bdgdn_status_string(status)} ({status})")
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libbdgdn.so (built in-tree by ``build.py``); raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(f"{_LIB_PATH} is not built; run paper_2606_01774_amd/build.py")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    lib.bdgdn_version.restype = ctypes.c_int32
+    lib.bdgdn_status_string.argtypes = [ctypes.c_int]
+    lib.bdgdn_status_string.restype = ctypes.c_char_p
+    lib.bdgdn_fwd_train_workspace.argtypes = [ctypes.POINTER(FwdDesc)]
+    lib.bdgdn_fwd_train_workspace.restype = ctypes.c_size_t
+    lib.bdgdn_fwd_train.argtypes = [ctypes.POINTER(FwdDesc)] + [P] * 17 + [ctypes.c_size_t, P]
+    lib.bdgdn_fwd_train.restype = ctypes.c_int
+    lib.bdgdn_denoise_step.argtypes = [ctypes.POINTER(ServeDesc)] + [P] * 9
+    lib.bdgdn_denoise_step.restype = ctypes.c_int
+    lib.bdgdn_commit.argtypes = [ctypes.POINTER(ServeDesc)] + [P] * 9
+    lib.bdgdn_commit.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def bdgdn_version() -> int:
+    return int(load_library().bdgdn_version())
+
+
+def bdgdn_status_string(status: int) -> str:
+    return load_library().bdgdn_status_string(int(status)).decode()
+
+
+# ------------------------------------------------------------------ marshalling
+_DT = {torch.bfloat16: BDGDN_BF16, torch.float32: BDGDN_F32}
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _dev(t, name, dtype=None):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    return t
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check(status, where):
+    if status != BDGDN_OK:
+        raise BdgdnError(status, where)
+
+
+def make_fwd_desc(q, v, *, block, scale=None, batch=None, num_seqs=0, route=BDGDN_ROUTE_FUSED,
+                  out_dtype=torch.float32):
+    """Descriptor from 4-D tensors q [B,T,h_qk,d_k], v [B,T,h_v,d_v]."""
+    B, T, h_qk, d_k = q.shape
+    h_v, d_v = v.shape[2], v.shape[3]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d_k)
+    return FwdDesc(B if batch is None else batch, T, num_seqs, h_qk, h_v, d_k, d_v, int(block),
+                   float(scale), _DT.get(q.dtype, -1), int(route), _DT.get(out_dtype, -1))
+
+
+def bdgdn_fwd_train_workspace(desc: FwdDesc) -> int:
+    return int(load_library().bdgdn_fwd_train_workspace(ctypes.byref(desc)))
+
+
+def bdgdn_fwd_train(q, k, v, g, beta, qn, kn, vn, gn, betan, *, block, scale=None,
+                    cu_seqlens=None, cu_seqlens_host=None, h0=None, o=None, on=None,
+                    ht=None, want_ht=False, route=BDGDN_ROUTE_FUSED, workspace=None,
+                    out_dtype=torch.float32, stream=None):
+    """Two-stream training forward.  Tensors are [B,T,h,d] (packed: B == 1 and
+    cu_seqlens [N+1] int32 on the device; cu_seqlens_host may be given to avoid a
+    device-to-host copy).  Outputs are ``out_dtype`` (fp32 by default; bf16 is
+    offered for bf16 inputs).  Returns (o, on, ht)."""
+    lib = load_library()
+    dt = q.dtype
+    for name, t in (("q", q), ("k", k), ("v", v), ("qn", qn), ("kn", kn), ("vn", vn)):
+        _dev(t, name, dt)
+    for name, t in (("g", g), ("beta", beta), ("gn", gn), ("betan", betan)):
+        _dev(t, name, torch.float32)
+    if q.dim() != 4 or v.dim() != 4:
+        raise ValueError("q, k, v must be [B, T, heads, dim]")
+    num_seqs = 0
+    cu_h = None
+    if cu_seqlens is not None:
+        _dev(cu_seqlens, "cu_seqlens", torch.int32)
+        num_seqs = cu_seqlens.numel() - 1
+        if cu_seqlens_host is None:
+            cu_seqlens_host = cu_seqlens.cpu()
+        cu_h = torch.as_tensor(cu_seqlens_host, dtype=torch.int32).contiguous()
+        if cu_h.numel() != num_seqs + 1:
+            raise ValueError("cu_seqlens_host and cu_seqlens differ in length")
+    if o is not None:
+        out_dtype = o.dtype
+    desc = make_fwd_desc(q, v, block=block, scale=scale, num_seqs=num_seqs, route=route,
+                         out_dtype=out_dtype)
+    if o is None:
+        o = torch.empty(v.shape, dtype=out_dtype, device=v.device)
+    if on is None:
+        on = torch.empty(vn.shape, dtype=out_dtype, device=vn.device)
+    _dev(o, "o", out_dtype)
+    _dev(on, "on", out_dtype)
+    units = num_seqs if num_seqs else q.shape[0]
+    if ht is None and want_ht:
+        ht = torch.empty(units, v.shape[2], q.shape[3], v.shape[3], device=q.device,
+                         dtype=torch.float32)
+    _dev(ht, "ht", torch.float32)
+    _dev(h0, "h0", torch.float32)
+    ws_bytes = bdgdn_fwd_train_workspace(desc)
+    if workspace is None and ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    ws_size = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.bdgdn_fwd_train(
+        ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+        _ptr(qn), _ptr(kn), _ptr(vn), _ptr(gn), _ptr(betan),
+        _ptr(cu_seqlens), None if cu_h is None else ctypes.c_void_p(cu_h.data_ptr()),
+        _ptr(h0), _ptr(o), _ptr(on), _ptr(ht), _ptr(workspace), ws_size, _stream(stream))
+    _check(st, "bdgdn_fwd_train")
+    return o, on, ht
+
+
+def _serve_desc(q, v, scale, out_dtype):
+    R, L, h_qk, d_k = q.shape
+    h_v, d_v = v.shape[2], v.shape[3]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d_k)
+    return ServeDesc(R, h_qk, h_v, d_k, d_v, L, float(scale), _DT.get(q.dtype, -1),
+                     _DT.get(out_dtype, -1))
+
+
+def bdgdn_denoise_step(state_pool, q, k, v, g, beta, *, scale=None, slot=None, o=None,
+                       out_dtype=torch.float32, stream=None):
+    """Block-end readout of R blocks ([R, L, h, d] tensors) seeded from
+    state_pool[slot[r]]; the pool is only read.  Returns o."""
+    lib = load_library()
+    dt = q.dtype
+    _dev(state_pool, "state_pool", torch.float32)
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _dev(t, name, dt)
+    _dev(g, "g", torch.float32)
+    _dev(beta, "beta", torch.float32)
+    _dev(slot, "slot", torch.int32)
+    if o is not None:
+        out_dtype = o.dtype
+    if o is None:
+        o = torch.empty(v.shape, dtype=out_dtype, device=v.device)
+    _dev(o, "o", out_dtype)
+    desc = _serve_desc(q, v, scale, out_dtype)
+    st = lib.bdgdn_denoise_step(ctypes.byref(desc), _ptr(state_pool), _ptr(slot), _ptr(q),
+                                _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(o), _stream(stream))
+    _check(st, "bdgdn_denoise_step")
+    return o
+
+
+def bdgdn_commit(state_pool, q, k, v, g, beta, *, scale=None, slot=None, o_causal=None,
+                 want_o=False, out_dtype=torch.float32, stream=None):
+    """Token-causal pass over R blocks; advances state_pool[slot[r]] in place.
+    Returns o_causal (or None)."""
+    lib = load_library()
+    dt = q.dtype
+    _dev(state_pool, "state_pool", torch.float32)
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _dev(t, name, dt)
+    _dev(g, "g", torch.float32)
+    _dev(beta, "beta", torch.float32)
+    _dev(slot, "slot", torch.int32)
+    if o_causal is not None:
+        out_dtype = o_causal.dtype
+    if o_causal is None and want_o:
+        o_causal = torch.empty(v.shape, dtype=out_dtype, device=v.device)
+    _dev(o_causal, "o_causal", out_dtype)
+    desc = _serve_desc(q, v, scale, out_dtype)
+    st = lib.bdgdn_commit(ctypes.byref(desc), _ptr(state_pool), _ptr(slot), _ptr(q), _ptr(k),
+                          _ptr(v), _ptr(g), _ptr(beta), _ptr(o_causal), _stream(stream))
+    _check(st, "bdgdn_commit")
+    return o_causal

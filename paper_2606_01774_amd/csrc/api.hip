@@ -1,0 +1,195 @@
+// api.hip -- the C ABI (include/bdgdn.h): host-side validation, scheduling and
+// dispatch.  Nothing here allocates device memory or synchronises the host.
+#include <math.h>
+
+#include <algorithm>
+#include <numeric>
+#include <vector>
+
+#include "bdgdn.h"
+#include "kernels.hpp"
+
+using namespace bdgdn;
+
+namespace {
+
+int lp_of(int L) { return L <= 16 ? 16 : (L <= 32 ? 32 : 64); }
+
+bool dims_ok(int d) { return d == 64 || d == 128; }
+
+// Token tensors are read and written with 16-byte vector accesses.
+bool aligned16(const void *p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// (dtype, out_dtype) -> element types of the kernels; false if not offered.
+bool types_of(int dtype, int out_dtype, Types &ty)
+{
+    if (dtype == BDGDN_BF16 && out_dtype == BDGDN_F32) { ty = Types::BF16_IN_F32_OUT; return true; }
+    if (dtype == BDGDN_BF16 && out_dtype == BDGDN_BF16) { ty = Types::BF16_IN_BF16_OUT; return true; }
+    if (dtype == BDGDN_F32 && out_dtype == BDGDN_F32) { ty = Types::F32; return true; }
+    return false;
+}
+
+// Shared validation of head shapes and dtypes.  Returns a status.
+int check_heads(int h_qk, int h_v, int d_k, int d_v, int block, float scale, int dtype, int out_dtype)
+{
+    if (h_qk <= 0 || h_v <= 0 || d_k <= 0 || d_v <= 0 || block <= 0) return BDGDN_ERR_INVALID_ARG;
+    if (h_v % h_qk != 0) return BDGDN_ERR_INVALID_ARG;
+    if (!isfinite(scale)) return BDGDN_ERR_INVALID_ARG;
+    Types ty;
+    if (!types_of(dtype, out_dtype, ty)) return BDGDN_ERR_UNSUPPORTED;
+    if (!dims_ok(d_k) || !dims_ok(d_v) || block > 64) return BDGDN_ERR_UNSUPPORTED;
+    if (!fwd_supported(ty, d_k, lp_of(block))) return BDGDN_ERR_UNSUPPORTED;
+    return BDGDN_OK;
+}
+
+// Validation of a training descriptor and its packing (Appendix "Document-packed
+// training": document starts are block-aligned; the tail may be partial).
+int check_fwd(const bdgdn_fwd_desc_t *d, const int32_t *cu_dev, const int32_t *cu_host)
+{
+    if (!d) return BDGDN_ERR_INVALID_ARG;
+    int st = check_heads(d->h_qk, d->h_v, d->d_k, d->d_v, d->block, d->scale, d->dtype, d->out_dtype);
+    if (st != BDGDN_OK) return st;
+    if (d->batch <= 0 || d->seqlen < 0 || d->num_seqs < 0) return BDGDN_ERR_INVALID_ARG;
+    if (d->route != BDGDN_ROUTE_FUSED && d->route != BDGDN_ROUTE_SPLIT) return BDGDN_ERR_INVALID_ARG;
+    if ((long)d->batch * d->seqlen > 0x7fffffffL) return BDGDN_ERR_UNSUPPORTED;
+    const bool packed = d->num_seqs > 0;
+    if (packed != (cu_dev != nullptr) || packed != (cu_host != nullptr)) return BDGDN_ERR_INVALID_ARG;
+    if (packed) {
+        if (d->batch != 1) return BDGDN_ERR_INVALID_ARG;
+        if (cu_host[0] != 0 || cu_host[d->num_seqs] != d->seqlen) return BDGDN_ERR_INVALID_ARG;
+        for (int i = 0; i < d->num_seqs; ++i)
+            if (cu_host[i + 1] < cu_host[i]) return BDGDN_ERR_INVALID_ARG;
+        for (int i = 0; i < d->num_seqs; ++i)
+            if (cu_host[i] % d->block != 0) return BDGDN_ERR_UNALIGNED;
+    }
+    if (d->route == BDGDN_ROUTE_SPLIT) return BDGDN_ERR_UNSUPPORTED;
+    return BDGDN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t bdgdn_version(void) { return (0 << 16) | 1; }
+
+const char *bdgdn_status_string(int status)
+{
+    switch (status) {
+    case BDGDN_OK: return "ok";
+    case BDGDN_ERR_INVALID_ARG: return "invalid argument";
+    case BDGDN_ERR_UNSUPPORTED: return "unsupported size, dtype or route";
+    case BDGDN_ERR_UNALIGNED: return "document start not aligned to the diffusion block";
+    case BDGDN_ERR_WORKSPACE: return "workspace too small";
+    case BDGDN_ERR_LAUNCH: return "kernel launch failed";
+    default: return "unknown status";
+    }
+}
+
+size_t bdgdn_fwd_train_workspace(const bdgdn_fwd_desc_t *desc)
+{
+    if (!desc) return 0;
+    return 0;
+}
+
+int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, const void *v,
+                    const float *g, const float *beta, const void *qn, const void *kn,
+                    const void *vn, const float *gn, const float *betan,
+                    const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                    const float *h0, void *o, void *on, float *ht, void *workspace,
+                    size_t workspace_bytes, void *stream)
+{
+    int st = check_fwd(desc, cu_seqlens_dev, cu_seqlens_host);
+    if (st != BDGDN_OK) return st;
+    if (!q || !k || !v || !g || !beta || !qn || !kn || !vn || !gn || !betan || !o || !on)
+        return BDGDN_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(qn) || !aligned16(kn) ||
+        !aligned16(vn) || !aligned16(o) || !aligned16(on))
+        return BDGDN_ERR_INVALID_ARG;
+    if (workspace_bytes < bdgdn_fwd_train_workspace(desc)) return BDGDN_ERR_WORKSPACE;
+    (void)workspace;
+    const bool packed = desc->num_seqs > 0;
+    const int nseq = packed ? desc->num_seqs : desc->batch;
+    if (desc->seqlen == 0) return BDGDN_OK;
+
+    FwdArgs a;
+    a.q = q; a.k = k; a.v = v; a.qn = qn; a.kn = kn; a.vn = vn;
+    a.g = g; a.beta = beta; a.gn = gn; a.betan = betan;
+    a.cu = packed ? cu_seqlens_dev : nullptr;
+    a.h0 = h0; a.ht = ht; a.o = o; a.on = on;
+    a.T = desc->seqlen; a.h_qk = desc->h_qk; a.h_v = desc->h_v; a.dv = desc->d_v; a.L = desc->block;
+    a.n_chains = nseq * desc->h_v;
+    a.n_vt = desc->d_v / 32;
+    a.scale = desc->scale;
+    a.n_order = 0;
+    if (packed && nseq <= kMaxOrder) {
+        // longest documents first, so that the longest serial chains start first
+        std::vector<int> idx(nseq);
+        std::iota(idx.begin(), idx.end(), 0);
+        std::stable_sort(idx.begin(), idx.end(), [&](int x, int y) {
+            return cu_seqlens_host[x + 1] - cu_seqlens_host[x] > cu_seqlens_host[y + 1] - cu_seqlens_host[y];
+        });
+        for (int i = 0; i < nseq; ++i) a.order[i] = idx[i];
+        a.n_order = nseq;
+    }
+    Types ty;
+    types_of(desc->dtype, desc->out_dtype, ty);
+    hipError_t e = launch_fwd_fused(ty, desc->d_k, lp_of(desc->block), a,
+                                    static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+}
+
+static int check_serve(const bdgdn_serve_desc_t *d)
+{
+    if (!d) return BDGDN_ERR_INVALID_ARG;
+    if (d->num_req < 0) return BDGDN_ERR_INVALID_ARG;
+    return check_heads(d->h_qk, d->h_v, d->d_k, d->d_v, d->block, d->scale, d->dtype, d->out_dtype);
+}
+
+static ServeArgs serve_args(const bdgdn_serve_desc_t *d, const float *pool, const int32_t *slot,
+                            const void *q, const void *k, const void *v, const float *g,
+                            const float *beta, void *o)
+{
+    ServeArgs a;
+    a.q = q; a.k = k; a.v = v; a.g = g; a.beta = beta;
+    a.pool = const_cast<float *>(pool);
+    a.slot = slot; a.o = o;
+    a.R = d->num_req; a.h_qk = d->h_qk; a.h_v = d->h_v; a.dv = d->d_v; a.L = d->block;
+    a.n_vt = d->d_v / 32;
+    a.scale = d->scale;
+    return a;
+}
+
+int bdgdn_denoise_step(const bdgdn_serve_desc_t *desc, const float *state_pool,
+                       const int32_t *slot, const void *q, const void *k, const void *v,
+                       const float *g, const float *beta, void *o, void *stream)
+{
+    int st = check_serve(desc);
+    if (st != BDGDN_OK) return st;
+    if (!state_pool || !q || !k || !v || !g || !beta || !o) return BDGDN_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return BDGDN_ERR_INVALID_ARG;
+    if (desc->num_req == 0) return BDGDN_OK;
+    ServeArgs a = serve_args(desc, state_pool, slot, q, k, v, g, beta, o);
+    Types ty;
+    types_of(desc->dtype, desc->out_dtype, ty);
+    hipError_t e = launch_denoise(ty, desc->d_k, lp_of(desc->block), a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+}
+
+int bdgdn_commit(const bdgdn_serve_desc_t *desc, float *state_pool, const int32_t *slot,
+                 const void *q, const void *k, const void *v, const float *g,
+                 const float *beta, void *o_causal, void *stream)
+{
+    int st = check_serve(desc);
+    if (st != BDGDN_OK) return st;
+    if (!state_pool || !q || !k || !v || !g || !beta) return BDGDN_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o_causal)) return BDGDN_ERR_INVALID_ARG;
+    if (desc->num_req == 0) return BDGDN_OK;
+    ServeArgs a = serve_args(desc, state_pool, slot, q, k, v, g, beta, o_causal);
+    Types ty;
+    types_of(desc->dtype, desc->out_dtype, ty);
+    hipError_t e = launch_commit(ty, desc->d_k, lp_of(desc->block), o_causal != nullptr, a,
+                                 static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+}
+
+}  // extern "C"

@@ -1,0 +1,50 @@
+// kernels.hpp -- argument blocks and host-side launchers of the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bdgdn {
+
+constexpr int kMaxOrder = 512;  // documents whose longest-first order travels in the kernel arguments
+
+struct FwdArgs {
+    const void *q, *k, *v, *qn, *kn, *vn;
+    const float *g, *beta, *gn, *betan;
+    const int32_t *cu;   // device cu_seqlens or NULL
+    const float *h0;
+    float *ht;
+    void *o, *on;
+    int T, h_qk, h_v, dv, L;
+    int n_chains, n_vt;  // chains = sequences x v-heads; d_v tiles per chain
+    float scale;
+    int n_order;         // 0, or the number of documents listed in order[]
+    int order[kMaxOrder];
+};
+
+struct ServeArgs {
+    const void *q, *k, *v;
+    const float *g, *beta;
+    float *pool;         // read (denoise) or read + written in place (commit)
+    const int32_t *slot; // NULL: slot[r] = r
+    void *o;             // NULL allowed for commit
+    int R, h_qk, h_v, dv, L;
+    int n_vt;
+    float scale;
+};
+
+// Element types of one call: inputs / MFMA operands / outputs.
+enum class Types {
+    BF16_IN_F32_OUT = 0,   // bf16 q,k,v staged as fp16 operands, fp32 outputs
+    BF16_IN_BF16_OUT = 1,  // bf16 q,k,v staged as fp16 operands, bf16 outputs
+    F32 = 2,               // fp32 end to end
+};
+
+// Each returns hipSuccess or the launch error.  lp is the padded block tile (16/32/64).
+hipError_t launch_fwd_fused(Types ty, int dk, int lp, const FwdArgs &a, hipStream_t s);
+hipError_t launch_denoise(Types ty, int dk, int lp, const ServeArgs &a, hipStream_t s);
+hipError_t launch_commit(Types ty, int dk, int lp, bool with_o, const ServeArgs &a, hipStream_t s);
+// Whether the (types, d_k, lp) combination is instantiated and fits in LDS.
+bool fwd_supported(Types ty, int dk, int lp);
+
+}  // namespace bdgdn

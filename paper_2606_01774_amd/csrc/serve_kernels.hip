@@ -1,0 +1,146 @@
+// serve_kernels.hip -- Diffusion-Trust serving passes over a pool of cached fp32
+// states: the denoise pass (block-end readout, the state is only read) and the
+// token-causal commit pass (the state is advanced and written back in place).
+// One workgroup per (request, v-head, d_v tile); each reads its state tile once.
+#include <mutex>
+
+#include "engine.hpp"
+#include "kernels.hpp"
+
+namespace bdgdn {
+
+constexpr int kServeBV = 32;
+
+template <typename In, typename Op, typename Out, int DK, int BV, int LP, bool CL, bool CO, bool NZ>
+__device__ __forceinline__ void serve_body(const ServeArgs &a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    typedef Engine<In, Op, Out, DK, BV, LP, CL, CO, NZ> Eng;
+    const int id = blockIdx.x;
+    const int unit = id / a.n_vt, vt = id % a.n_vt;
+    const int r = unit / a.h_v, h = unit % a.h_v;
+    const int sl = a.slot ? a.slot[r] : r;
+    const int hq = h / (a.h_v / a.h_qk);
+    const int v0 = vt * BV;
+    Eng eng(smem);
+    f32x4 S[Eng::NSW];
+    float *state = a.pool + ((long)sl * a.h_v + h) * DK * a.dv + v0;
+    eng.load_state(S, state, a.dv);
+    eng.write_st(S);
+    __syncthreads();
+    typename Eng::IO io;
+    io.qk_stride = (long)a.h_qk * DK;
+    io.v_stride = (long)a.h_v * a.dv;
+    io.gate_stride = a.h_v;
+    const long row0 = (long)r * a.L;
+    const long qk_off = (row0 * a.h_qk + hq) * DK;
+    const long v_off = (row0 * a.h_v + h) * a.dv + v0;
+    const long g_off = row0 * a.h_v + h;
+    const In *q = static_cast<const In *>(a.q) + qk_off;
+    const In *k = static_cast<const In *>(a.k) + qk_off;
+    const In *v = static_cast<const In *>(a.v) + v_off;
+    Out *o = a.o ? static_cast<Out *>(a.o) + v_off : nullptr;
+    io.k = k; io.q = q; io.v = v;
+    io.kn = k; io.qn = q; io.vn = v;
+    io.g = a.g + g_off; io.beta = a.beta + g_off;
+    io.gn = a.g + g_off; io.betan = a.beta + g_off;
+    io.o = o; io.on = o;
+    io.nvalid = a.L;
+    eng.step(io, S, a.scale);
+    if (CL) eng.store_state(S, state, a.dv);
+}
+
+template <typename In, typename Op, typename Out, int DK, int BV, int LP>
+__global__ void __launch_bounds__(kThreads) bdgdn_denoise_kernel(ServeArgs a)
+{
+    serve_body<In, Op, Out, DK, BV, LP, false, false, true>(a);
+}
+
+template <typename In, typename Op, typename Out, int DK, int BV, int LP, bool CO>
+__global__ void __launch_bounds__(kThreads) bdgdn_commit_kernel(ServeArgs a)
+{
+    serve_body<In, Op, Out, DK, BV, LP, true, CO, false>(a);
+}
+
+template <typename K>
+static hipError_t set_lds(K kern, int bytes, std::once_flag &once, hipError_t &err)
+{
+    std::call_once(once, [&] {
+        err = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    });
+    return err;
+}
+
+template <typename In, typename Op, typename Out, int DK, int LP>
+static hipError_t launch_dn(const ServeArgs &a, hipStream_t s)
+{
+    typedef Layout<Op, DK, kServeBV, LP, false, false, true> Ly;
+    static_assert(Ly::BYTES <= 160 * 1024, "LDS budget");
+    auto kern = bdgdn_denoise_kernel<In, Op, Out, DK, kServeBV, LP>;
+    static std::once_flag once;
+    static hipError_t err = hipSuccess;
+    if (set_lds(kern, Ly::BYTES, once, err) != hipSuccess) return err;
+    hipLaunchKernelGGL(kern, dim3(a.R * a.h_v * a.n_vt), dim3(kThreads), Ly::BYTES, s, a);
+    return hipGetLastError();
+}
+
+template <typename In, typename Op, typename Out, int DK, int LP, bool CO>
+static hipError_t launch_cm1(const ServeArgs &a, hipStream_t s)
+{
+    typedef Layout<Op, DK, kServeBV, LP, true, CO, false> Ly;
+    static_assert(Ly::BYTES <= 160 * 1024, "LDS budget");
+    auto kern = bdgdn_commit_kernel<In, Op, Out, DK, kServeBV, LP, CO>;
+    static std::once_flag once;
+    static hipError_t err = hipSuccess;
+    if (set_lds(kern, Ly::BYTES, once, err) != hipSuccess) return err;
+    hipLaunchKernelGGL(kern, dim3(a.R * a.h_v * a.n_vt), dim3(kThreads), Ly::BYTES, s, a);
+    return hipGetLastError();
+}
+
+template <typename In, typename Op, typename Out, int DK, int LP>
+static hipError_t launch_cm(bool with_o, const ServeArgs &a, hipStream_t s)
+{
+    return with_o ? launch_cm1<In, Op, Out, DK, LP, true>(a, s) : launch_cm1<In, Op, Out, DK, LP, false>(a, s);
+}
+
+#define BDGDN_SERVE_DISPATCH(CALL)                                                       \
+    switch (ty) {                                                                        \
+    case Types::BF16_IN_F32_OUT:                                                         \
+        BDGDN_LPS(CALL, __bf16, _Float16, float, 64) BDGDN_LPS(CALL, __bf16, _Float16, float, 128) \
+        break;                                                                           \
+    case Types::BF16_IN_BF16_OUT:                                                        \
+        BDGDN_LPS(CALL, __bf16, _Float16, __bf16, 64) BDGDN_LPS(CALL, __bf16, _Float16, __bf16, 128) \
+        break;                                                                           \
+    case Types::F32:                                                                     \
+        BDGDN_ONE(CALL, float, float, float, 64, 16) BDGDN_ONE(CALL, float, float, float, 64, 32) \
+        BDGDN_ONE(CALL, float, float, float, 128, 16) BDGDN_ONE(CALL, float, float, float, 128, 32) \
+        break;                                                                           \
+    }
+#define BDGDN_LPS(CALL, IN, OP, OUT, DK) \
+    BDGDN_ONE(CALL, IN, OP, OUT, DK, 16) BDGDN_ONE(CALL, IN, OP, OUT, DK, 32) BDGDN_ONE(CALL, IN, OP, OUT, DK, 64)
+
+hipError_t launch_denoise(Types ty, int dk, int lp, const ServeArgs &a, hipStream_t s)
+{
+    if (a.dv % kServeBV) return hipErrorInvalidValue;
+#define BDGDN_ONE(CALL, IN, OP, OUT, DK, LP) \
+    if (dk == DK && lp == LP) return launch_dn<IN, OP, OUT, DK, LP>(a, s);
+    BDGDN_SERVE_DISPATCH(0)
+#undef BDGDN_ONE
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_commit(Types ty, int dk, int lp, bool with_o, const ServeArgs &a, hipStream_t s)
+{
+    if (a.dv % kServeBV) return hipErrorInvalidValue;
+#define BDGDN_ONE(CALL, IN, OP, OUT, DK, LP) \
+    if (dk == DK && lp == LP) return launch_cm<IN, OP, OUT, DK, LP>(with_o, a, s);
+    BDGDN_SERVE_DISPATCH(0)
+#undef BDGDN_ONE
+    return hipErrorInvalidValue;
+}
+
+#undef BDGDN_LPS
+#undef BDGDN_SERVE_DISPATCH
+
+}  // namespace bdgdn

@@ -1,0 +1,127 @@
+"""CPU-side checks of the C ABI: the library loads and exports every function
+declared in include/bdgdn.h, and host-side validation rejects bad arguments
+before anything is launched (no GPU is touched: every call here fails
+validation, which runs before any HIP call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_01774_amd as bd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bdgdn.h")
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails first
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bdgdn_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = bd.load_library()
+    declared = _declared_functions()
+    assert set(declared) == set(bd.EXPORTED_SYMBOLS)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings():
+    assert bd.bdgdn_version() >= 1
+    for st in (0, -1, -2, -3, -4, -5):
+        assert bd.bdgdn_status_string(st)
+    assert bd.bdgdn_status_string(-99) == "unknown status"
+
+
+def _desc(**kw):
+    d = dict(batch=1, seqlen=64, num_seqs=0, h_qk=2, h_v=4, d_k=128, d_v=128, block=32,
+             scale=0.1, dtype=bd.BDGDN_BF16, route=bd.BDGDN_ROUTE_FUSED, out_dtype=bd.BDGDN_F32)
+    d.update(kw)
+    return bd.FwdDesc(**d)
+
+
+def _fwd(desc, cu_dev=None, cu_host=None, null_q=False):
+    lib = bd.load_library()
+    P = FAKE
+    return lib.bdgdn_fwd_train(ctypes.byref(desc), None if null_q else P, P, P, P, P, P, P, P, P, P,
+                               cu_dev, cu_host, None, P, P, None, None, 0, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(h_v=3), bd.BDGDN_ERR_INVALID_ARG),            # h_v % h_qk != 0
+    (dict(batch=0), bd.BDGDN_ERR_INVALID_ARG),
+    (dict(block=0), bd.BDGDN_ERR_INVALID_ARG),
+    (dict(scale=float("nan")), bd.BDGDN_ERR_INVALID_ARG),
+    (dict(d_k=96), bd.BDGDN_ERR_UNSUPPORTED),
+    (dict(d_v=256), bd.BDGDN_ERR_UNSUPPORTED),
+    (dict(block=65), bd.BDGDN_ERR_UNSUPPORTED),
+    (dict(dtype=7), bd.BDGDN_ERR_UNSUPPORTED),
+    (dict(dtype=bd.BDGDN_F32, block=64), bd.BDGDN_ERR_UNSUPPORTED),
+    (dict(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_BF16), bd.BDGDN_ERR_UNSUPPORTED),
+    (dict(out_dtype=5), bd.BDGDN_ERR_UNSUPPORTED),
+    (dict(route=9), bd.BDGDN_ERR_INVALID_ARG),
+])
+def test_fwd_rejects_bad_descriptors(kw, status):
+    assert _fwd(_desc(**kw)) == status
+
+
+def test_fwd_rejects_null_tensor():
+    assert _fwd(_desc(), null_q=True) == bd.BDGDN_ERR_INVALID_ARG
+
+
+def test_fwd_packing_checks():
+    cu = (ctypes.c_int32 * 4)(0, 32, 96, 100)
+    # misaligned document start (P: document starts must be block-aligned)
+    bad = (ctypes.c_int32 * 4)(0, 32, 80, 100)
+    d = _desc(seqlen=100, num_seqs=3)
+    assert _fwd(d, FAKE, bad) == bd.BDGDN_ERR_UNALIGNED
+    # only one of the two copies
+    assert _fwd(d, FAKE, None) == bd.BDGDN_ERR_INVALID_ARG
+    assert _fwd(d, None, cu) == bd.BDGDN_ERR_INVALID_ARG
+    # packed needs batch == 1 and cu[N] == seqlen, non-decreasing offsets
+    assert _fwd(_desc(seqlen=100, num_seqs=3, batch=2), FAKE, cu) == bd.BDGDN_ERR_INVALID_ARG
+    assert _fwd(_desc(seqlen=128, num_seqs=3), FAKE, cu) == bd.BDGDN_ERR_INVALID_ARG
+    dec = (ctypes.c_int32 * 4)(0, 64, 32, 100)
+    assert _fwd(d, FAKE, dec) == bd.BDGDN_ERR_INVALID_ARG
+
+
+def test_workspace_query():
+    assert bd.bdgdn_fwd_train_workspace(_desc()) == 0
+
+
+def _serve(fn, **kw):
+    d = dict(num_req=4, h_qk=2, h_v=4, d_k=128, d_v=128, block=32, scale=0.1, dtype=bd.BDGDN_BF16,
+             out_dtype=bd.BDGDN_F32)
+    d.update(kw)
+    desc = bd.ServeDesc(**d)
+    lib = bd.load_library()
+    P = FAKE
+    return getattr(lib, fn)(ctypes.byref(desc), P, None, P, P, P, P, P, P, None)
+
+
+@pytest.mark.parametrize("fn", ["bdgdn_denoise_step", "bdgdn_commit"])
+@pytest.mark.parametrize("kw,status", [
+    (dict(h_v=5), bd.BDGDN_ERR_INVALID_ARG),
+    (dict(num_req=-1), bd.BDGDN_ERR_INVALID_ARG),
+    (dict(d_k=32), bd.BDGDN_ERR_UNSUPPORTED),
+    (dict(block=100), bd.BDGDN_ERR_UNSUPPORTED),
+    (dict(scale=float("inf")), bd.BDGDN_ERR_INVALID_ARG),
+])
+def test_serve_rejects_bad_descriptors(fn, kw, status):
+    assert _serve(fn, **kw) == status
+
+
+def test_serve_empty_batch_is_a_no_op():
+    assert _serve("bdgdn_denoise_step", num_req=0) == 0
+    assert _serve("bdgdn_commit", num_req=0) == 0
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    x = torch.zeros(1, 32, 1, 64, dtype=torch.bfloat16)
+    g = torch.zeros(1, 32, 1)
+    with pytest.raises(ValueError):
+        bd.bdgdn_fwd_train(x, x, x, g, g, x, x, x, g, g, block=32)

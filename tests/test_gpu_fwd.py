@@ -1,0 +1,176 @@
+"""GPU parity of the two-stream training forward (bdgdn_fwd_train) against the
+fp64 oracle, called through the C ABI.  Tolerance: max |gpu - oracle| divided by
+the oracle output RMS, <= 2e-2 for bf16 inputs and <= 1e-4 for fp32, per tensor."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_01774_amd as bd
+from paper_2606_01774_amd import workloads as W
+from parity_utils import TOL, oracle_full, oracle_unit, rel_err, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_gpu(d, block, scale, h0=None, want_ht=True, route=bd.BDGDN_ROUTE_FUSED):
+    o, on, ht = bd.bdgdn_fwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"],
+                                   d["qn"], d["kn"], d["vn"], d["gn"], d["betan"],
+                                   block=block, scale=scale, h0=h0,
+                                   cu_seqlens=d.get("cu_seqlens"),
+                                   cu_seqlens_host=d.get("cu_host"),
+                                   want_ht=want_ht, route=route)
+    torch.cuda.synchronize()
+    return o, on, ht
+
+
+def _check_full(inp, block, dtype, h0=None, route=bd.BDGDN_ROUTE_FUSED):
+    scale = 1.0 / math.sqrt(inp["q"].shape[-1])
+    d = to_dev(inp)
+    if "cu_seqlens" in inp:
+        d["cu_host"] = inp["cu_seqlens"]
+    o, on, ht = _run_gpu(d, block, scale, h0=None if h0 is None else h0.cuda(), route=route)
+    ro, ron, rht = oracle_full(inp, block, scale, h0=h0, cu=inp.get("cu_seqlens"))
+    tol = TOL[dtype]
+    eo, eon, eht = rel_err(o, ro), rel_err(on, ron), rel_err(ht, rht)
+    print(f"err o={eo:.3e} on={eon:.3e} ht={eht:.3e}")
+    assert eo <= tol and eon <= tol and eht <= tol, (eo, eon, eht)
+    return o, on, ht
+
+
+def test_tiny_f32_full_config():
+    w = W.TINY_F32
+    _check_full(W.make_train(w), w.block, "f32")
+
+
+@pytest.mark.parametrize("B,T,hqk,hv,d,L,dtype", [
+    (2, 200, 2, 2, 128, 32, "bf16"),     # ragged tail (200 = 6*32 + 8)
+    (1, 256, 2, 4, 128, 64, "bf16"),     # grouped value heads, L = 64
+    (1, 160, 1, 2, 128, 16, "bf16"),
+    (1, 120, 2, 2, 64, 24, "bf16"),      # block padded inside the tile, d = 64
+    (1, 70, 1, 1, 128, 5, "bf16"),       # small block
+    (1, 33, 1, 1, 64, 1, "bf16"),        # L = 1: each noisy block is one step
+    (2, 100, 1, 2, 128, 32, "f32"),
+    (1, 96, 2, 2, 64, 16, "f32"),
+])
+def test_small_shapes(B, T, hqk, hv, d, L, dtype):
+    inp = W.make_custom_train(B, T, hqk, hv, d, d, dtype, seed=1000 + T + L)
+    h0 = torch.randn(B, hv, d, d, generator=torch.Generator().manual_seed(T)) * 0.3
+    _check_full(inp, L, dtype, h0=h0)
+
+
+def test_packed_documents_small():
+    lengths = [64, 96, 32, 0, 64, 128, 17]   # an empty doc and a ragged last doc
+    inp = W.make_custom_train(1, sum(lengths), 2, 2, 128, 128, "bf16", seed=77, lengths=lengths)
+    _check_full(inp, 32, "bf16")
+
+
+def test_packed_equals_separate_bitwise():
+    """Packing reproduces per-document results exactly (Appendix, packing contract)."""
+    lengths = [96, 64, 40]
+    inp = W.make_custom_train(1, sum(lengths), 1, 2, 128, 128, "bf16", seed=5, lengths=lengths)
+    d = to_dev(inp)
+    d["cu_host"] = inp["cu_seqlens"]
+    o, on, ht = _run_gpu(d, 32, 0.1)
+    cu = inp["cu_seqlens"].tolist()
+    for i in range(len(lengths)):
+        sub = {k: v[:, cu[i]:cu[i + 1]].contiguous().cuda() for k, v in inp.items()
+               if k not in ("cu_seqlens",)}
+        so, son, sht = _run_gpu(sub, 32, 0.1)
+        assert torch.equal(so, o[:, cu[i]:cu[i + 1]])
+        assert torch.equal(son, on[:, cu[i]:cu[i + 1]])
+        assert torch.equal(sht[0], ht[i])
+
+
+def test_determinism_and_isolation():
+    """Run-to-run bitwise determinism; perturbing one noisy block changes only that
+    block's noisy outputs (clean outputs and other blocks bitwise unchanged)."""
+    inp = W.make_custom_train(1, 256, 2, 2, 128, 128, "bf16", seed=9)
+    d = to_dev(inp)
+    o1, on1, ht1 = _run_gpu(d, 32, 0.1)
+    o2, on2, ht2 = _run_gpu(d, 32, 0.1)
+    assert torch.equal(o1, o2) and torch.equal(on1, on2) and torch.equal(ht1, ht2)
+    blk = slice(64, 96)
+    d2 = dict(d)
+    for key in ("qn", "kn", "vn"):
+        t = d[key].clone()
+        t[:, blk] = torch.flip(t[:, blk], dims=[1])
+        d2[key] = t
+    o3, on3, ht3 = _run_gpu(d2, 32, 0.1)
+    assert torch.equal(o3, o1) and torch.equal(ht3, ht1)
+    mask = torch.zeros(256, dtype=torch.bool)
+    mask[blk] = True
+    assert torch.equal(on3[:, ~mask], on1[:, ~mask])
+    assert not torch.equal(on3[:, mask], on1[:, mask])
+
+
+def _sampled_units(w, inp, units, o, on, ht, cu=None):
+    scale = 1.0 / math.sqrt(w.d_k)
+    ratio = w.h_v // w.h_qk
+    worst = [0.0, 0.0, 0.0]
+    for (b, h) in units:
+        if cu is None:
+            ro, ron, rht = oracle_unit(inp, b, h, ratio, w.block, scale)
+            go, gon, ght = o[b, :, h], on[b, :, h], ht[b, h]
+        else:
+            a, e = int(cu[b]), int(cu[b + 1])
+            ro, ron, rht = oracle_unit(inp, 0, h, ratio, w.block, scale, rows=(a, e))
+            go, gon, ght = o[0, a:e, h], on[0, a:e, h], ht[b, h]
+        errs = (rel_err(go, ro), rel_err(gon, ron), rel_err(ght, rht))
+        print(f"unit (seq {b}, head {h}): err o={errs[0]:.3e} on={errs[1]:.3e} ht={errs[2]:.3e}")
+        worst = [max(x, y) for x, y in zip(worst, errs)]
+    tol = TOL[w.dtype]
+    assert max(worst) <= tol, worst
+
+
+def _full_size(w, units_fn):
+    inp = W.make_train(w)
+    d = to_dev(inp)
+    if "cu_seqlens" in inp:
+        d["cu_host"] = inp["cu_seqlens"]
+    o, on, ht = _run_gpu(d, w.block, 1.0 / math.sqrt(w.d_k))
+    assert torch.isfinite(o.float()).all() and torch.isfinite(on.float()).all()
+    o, on, ht = o.cpu(), on.cpu(), ht.cpu()
+    _sampled_units(w, inp, units_fn(inp), o, on, ht, cu=inp.get("cu_seqlens"))
+
+
+def test_full_train_4k_sampled():
+    _full_size(W.TRAIN_4K, lambda inp: [(0, 0), (1, 7), (2, 12), (3, 15)])
+
+
+def test_full_gva_16k_sampled():
+    _full_size(W.GVA_16K, lambda inp: [(0, 0), (1, 31)])
+
+
+def test_full_varlen_128k_sampled():
+    def units(inp):
+        lengths = inp["lengths"]
+        longest = int(np.argmax(lengths))
+        shortest = int(np.argmin(lengths))
+        return [(longest, 3), (shortest, 9), (5, 15)]
+    _full_size(W.VARLEN_128K, units)
+
+
+def test_bf16_outputs():
+    """bf16 outputs (the production-training format): the error budget is the
+    stated tolerance plus the output's own rounding (|bf16(x) - x| of the oracle)."""
+    inp = W.make_custom_train(2, 192, 2, 2, 128, 128, "bf16", seed=21)
+    d = to_dev(inp)
+    o, on, ht = bd.bdgdn_fwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"],
+                                   d["qn"], d["kn"], d["vn"], d["gn"], d["betan"],
+                                   block=32, scale=0.0884, want_ht=True,
+                                   out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert o.dtype == torch.bfloat16 and on.dtype == torch.bfloat16
+    ro, ron, rht = oracle_full(inp, 32, 0.0884)
+    for name, gpu, ref in (("o", o, ro), ("on", on, ron)):
+        rnd = torch.from_numpy(ref.astype(np.float32)).to(torch.bfloat16).double().numpy()
+        budget = TOL["bf16"] + np.abs(rnd - ref).max() / np.sqrt((ref ** 2).mean())
+        e = rel_err(gpu, ref)
+        print(f"{name}: err {e:.3e} budget {budget:.3e}")
+        assert e <= budget
+    assert rel_err(ht, rht) <= TOL["bf16"]
+    # same arithmetic as the fp32-output kernel up to the final rounding
+    o32, on32, _ = _run_gpu(d, 32, 0.0884)
+    assert torch.equal(o32.to(torch.bfloat16), o) and torch.equal(on32.to(torch.bfloat16), on)

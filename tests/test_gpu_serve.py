@@ -1,0 +1,112 @@
+"""GPU parity of the serving passes (bdgdn_denoise_step, bdgdn_commit) against the
+fp64 oracle, through the C ABI, plus the state-pool contracts: denoise never
+writes the pool; commit writes exactly the named slots."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_01774_amd as bd
+from paper_2606_01774_amd import workloads as W
+from parity_utils import TOL, rel_err
+
+pytestmark = pytest.mark.gpu
+
+
+def _block(R, L, hqk, hv, d, dtype, seed):
+    rng = np.random.default_rng(seed)
+    return W.draw_stream(rng, (R, L), hqk, hv, d, d, dtype)
+
+
+def _realistic_pool(n, hv, d, seed, prefix=64):
+    """Prefix states made by the oracle's causal pass over seeded prefix tokens."""
+    blk = _block(n, prefix, hv, hv, d, "f32", seed)
+    zero = np.zeros((n, hv, d, d))
+    pool, _ = oracle.commit(zero, blk["q"], blk["k"], blk["v"], blk["g"], blk["beta"],
+                            scale=1.0, want_o=False)
+    return torch.from_numpy(pool.astype(np.float32))
+
+
+@pytest.mark.parametrize("R,L,hqk,hv,d,dtype", [
+    (3, 32, 2, 4, 128, "bf16"), (2, 64, 1, 1, 128, "bf16"), (4, 16, 2, 2, 64, "bf16"),
+    (2, 7, 1, 1, 128, "bf16"), (3, 16, 1, 2, 64, "f32"), (2, 32, 1, 1, 128, "f32"),
+])
+def test_denoise_and_commit_small(R, L, hqk, hv, d, dtype):
+    pool = _realistic_pool(R + 1, hv, d, seed=R * 100 + L)
+    slot = torch.tensor(list(range(R, 0, -1)), dtype=torch.int32)   # permuted, slot 0 unused
+    blk = _block(R, L, hqk, hv, d, dtype, seed=L)
+    scale = 1.0 / math.sqrt(d)
+    dp = pool.cuda()
+    db = {k: v.cuda() for k, v in blk.items()}
+    before = dp.clone()
+    o = bd.bdgdn_denoise_step(dp, db["q"], db["k"], db["v"], db["g"], db["beta"], scale=scale,
+                              slot=slot.cuda())
+    torch.cuda.synchronize()
+    assert torch.equal(dp, before), "denoise wrote the state pool"
+    ref = oracle.denoise(pool, blk["q"], blk["k"], blk["v"], blk["g"], blk["beta"], scale=scale,
+                         slot=slot.numpy())
+    e = rel_err(o, ref)
+    print(f"denoise err={e:.3e}")
+    assert e <= TOL[dtype]
+    oc = bd.bdgdn_commit(dp, db["q"], db["k"], db["v"], db["g"], db["beta"], scale=scale,
+                         slot=slot.cuda(), want_o=True)
+    torch.cuda.synchronize()
+    rpool, ro = oracle.commit(pool, blk["q"], blk["k"], blk["v"], blk["g"], blk["beta"],
+                              scale=scale, slot=slot.numpy())
+    eo, es = rel_err(oc, ro), rel_err(dp[1:], rpool[1:])
+    print(f"commit err o={eo:.3e} state={es:.3e}")
+    assert eo <= TOL[dtype] and es <= TOL[dtype]
+    assert torch.equal(dp[0], before[0]), "commit wrote an unnamed slot"
+    # commit without the causal output writes the same state
+    dp2 = before.clone()
+    bd.bdgdn_commit(dp2, db["q"], db["k"], db["v"], db["g"], db["beta"], scale=scale,
+                    slot=slot.cuda())
+    torch.cuda.synchronize()
+    assert torch.equal(dp2, dp)
+
+
+def test_denoise_matches_training_noisy_block():
+    """The denoise pass from a cached state equals the training forward's noisy
+    block that follows the same prefix (h0 = the cached state)."""
+    R, L, hv, d = 2, 32, 2, 128
+    pool = _realistic_pool(R, hv, d, seed=3)
+    blk = _block(R, L, hv, hv, d, "bf16", seed=4)
+    db = {k: v.cuda() for k, v in blk.items()}
+    o = bd.bdgdn_denoise_step(pool.cuda(), db["q"], db["k"], db["v"], db["g"], db["beta"], scale=0.2)
+    _, on, _ = bd.bdgdn_fwd_train(db["q"], db["k"], db["v"], db["g"], db["beta"],
+                                  db["q"], db["k"], db["v"], db["g"], db["beta"],
+                                  block=L, scale=0.2, h0=pool.cuda())
+    torch.cuda.synchronize()
+    e = rel_err(o, on.double().cpu().numpy())
+    print(f"denoise vs training noisy block: {e:.3e} (bitwise {torch.equal(o, on)})")
+    assert e <= 1e-2
+
+
+def test_full_serving_workload():
+    """64 requests x 32 heads x 128x128 states, 8 denoise steps then one commit."""
+    w = W.SERVE_64
+    pool = _realistic_pool(w.requests, w.h_v, w.d_k, seed=w.seed)
+    dp = pool.cuda()
+    before = dp.clone()
+    scale = 1.0 / math.sqrt(w.d_k)
+    for step in range(w.steps):
+        blk = W.make_serve_block(w, step)
+        db = {k: v.cuda() for k, v in blk.items()}
+        o = bd.bdgdn_denoise_step(dp, db["q"], db["k"], db["v"], db["g"], db["beta"], scale=scale)
+        if step in (0, w.steps - 1):
+            ref = oracle.denoise(pool, blk["q"], blk["k"], blk["v"], blk["g"], blk["beta"], scale=scale)
+            e = rel_err(o, ref)
+            print(f"step {step}: denoise err={e:.3e}")
+            assert e <= TOL[w.dtype]
+    torch.cuda.synchronize()
+    assert torch.equal(dp, before), "denoise steps changed the pool"
+    blk = W.make_serve_block(w, w.steps)
+    db = {k: v.cuda() for k, v in blk.items()}
+    oc = bd.bdgdn_commit(dp, db["q"], db["k"], db["v"], db["g"], db["beta"], scale=scale, want_o=True)
+    torch.cuda.synchronize()
+    rpool, ro = oracle.commit(pool, blk["q"], blk["k"], blk["v"], blk["g"], blk["beta"], scale=scale)
+    eo, es = rel_err(oc, ro), rel_err(dp, rpool)
+    print(f"commit err o={eo:.3e} state={es:.3e}")
+    assert eo <= TOL[w.dtype] and es <= TOL[w.dtype]
