@@ -126,11 +126,13 @@ def main():
     scale = 1.0 / math.sqrt(w.d_k)
     o = torch.empty(w.batch, w.seqlen, w.h_v, w.d_v, dtype=torch.float32, device=dev)
     on = torch.empty_like(o)
+    desc = bd.make_fwd_desc(d["q"], d["v"], block=w.block, scale=scale)
+    ws = torch.empty(max(256, bd.bdgdn_fwd_train_workspace(desc)), dtype=torch.uint8, device=dev)
 
     def step():
         bd.bdgdn_fwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"],
                            d["qn"], d["kn"], d["vn"], d["gn"], d["betan"],
-                           block=w.block, scale=scale, o=o, on=on, stream=stream)
+                           block=w.block, scale=scale, o=o, on=on, workspace=ws, stream=stream)
 
     torch.cuda.synchronize()
     ms = time_launches(step, args.steps, args.warmup, stream)
@@ -149,10 +151,11 @@ def main():
         "config": {"workload": w.name, "batch": w.batch, "seq_len": w.seqlen,
                    "h_qk": w.h_qk, "h_v": w.h_v, "d_k": w.d_k, "d_v": w.d_v, "block": w.block,
                    "inputs": "bf16", "mfma_operands": "fp16", "state": "fp32", "outputs": "fp32",
-                   "route": "fused", "parallelism": "none (1 GPU)"},
+                   "route": "fused (UT records + scan)", "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "bdgdn_fwd_fused_kernel", "algorithmic_bytes": abytes},
+                     "kernel": "bdgdn_fwd_train step = bdgdn_k1_intra_kernel + bdgdn_k2_scan_kernel",
+                     "algorithmic_bytes": abytes},
         "mfma": {"model_flop": flops, "tflops": flops / (ms * 1e-3) / 1e12,
                  "frac_of_peak": flops / (ms * 1e-3) / 1e12 / MFMA16_PEAK_TFLOPS},
     }

@@ -73,14 +73,19 @@ extern "C" {
 
 typedef enum { BDGDN_BF16 = 0, BDGDN_F32 = 1 } bdgdn_dtype_t;
 
-/* How the training forward is scheduled; both give the same result.
- *  FUSED: one kernel per (sequence, v-head, d_v tile) carries the clean state on chip
- *         and evaluates each noisy block from the in-register boundary state (the
- *         fused two-stream schedule, Appendix "Route II").
- *  SPLIT: block-local UT transform and masked Q K^T in one kernel, the clean scan
- *         writing every block-boundary state to the workspace, and an independent
- *         noisy-block kernel reading them (Appendix "Route I").  Needs a workspace. */
-typedef enum { BDGDN_ROUTE_FUSED = 0, BDGDN_ROUTE_SPLIT = 1 } bdgdn_route_t;
+/* How the training forward is scheduled; every route gives the same result up to
+ * floating-point summation order.
+ *  FUSED:   two kernels.  The block-local UT transform and masked Q K^T of every
+ *           (block, v-head) are computed in parallel into the workspace; then one
+ *           workgroup per (sequence, v-head, d_v tile) scans the blocks in order with
+ *           the clean state on chip and evaluates each noisy block from the in-register
+ *           boundary state (the fused two-stream schedule, Appendix "Route II").  Needs
+ *           a workspace.
+ *  SPLIT:   boundary states through HBM and a separate noisy-block kernel (Appendix
+ *           "Route I").  Not available in this version (BDGDN_ERR_UNSUPPORTED).
+ *  ONEPASS: one kernel per (sequence, v-head, d_v tile) that recomputes the UT
+ *           transform of each block itself.  No workspace. */
+typedef enum { BDGDN_ROUTE_FUSED = 0, BDGDN_ROUTE_SPLIT = 1, BDGDN_ROUTE_ONEPASS = 2 } bdgdn_route_t;
 
 typedef struct {
     int32_t batch;     /* B sequences; must be 1 when packed (num_seqs > 0)            */
@@ -132,7 +137,9 @@ size_t bdgdn_fwd_train_workspace(const bdgdn_fwd_desc_t *desc);
  *                          noisy block-end readout); every row is written.
  *   ht                     [B or N][h_v][d_k][d_v] fp32 final clean state, or NULL.
  *   workspace              device memory of at least bdgdn_fwd_train_workspace(desc)
- *                          bytes (may be NULL when that is 0).
+ *                          bytes, 256-byte aligned (may be NULL when that is 0); its
+ *                          contents are scratch owned by the call until the stream
+ *                          passes it.
  * Returns BDGDN_OK or a negative status.
  */
 int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc,

@@ -50,7 +50,8 @@ int check_fwd(const bdgdn_fwd_desc_t *d, const int32_t *cu_dev, const int32_t *c
     int st = check_heads(d->h_qk, d->h_v, d->d_k, d->d_v, d->block, d->scale, d->dtype, d->out_dtype);
     if (st != BDGDN_OK) return st;
     if (d->batch <= 0 || d->seqlen < 0 || d->num_seqs < 0) return BDGDN_ERR_INVALID_ARG;
-    if (d->route != BDGDN_ROUTE_FUSED && d->route != BDGDN_ROUTE_SPLIT) return BDGDN_ERR_INVALID_ARG;
+    if (d->route != BDGDN_ROUTE_FUSED && d->route != BDGDN_ROUTE_SPLIT && d->route != BDGDN_ROUTE_ONEPASS)
+        return BDGDN_ERR_INVALID_ARG;
     if ((long)d->batch * d->seqlen > 0x7fffffffL) return BDGDN_ERR_UNSUPPORTED;
     const bool packed = d->num_seqs > 0;
     if (packed != (cu_dev != nullptr) || packed != (cu_host != nullptr)) return BDGDN_ERR_INVALID_ARG;
@@ -62,7 +63,7 @@ int check_fwd(const bdgdn_fwd_desc_t *d, const int32_t *cu_dev, const int32_t *c
         for (int i = 0; i < d->num_seqs; ++i)
             if (cu_host[i] % d->block != 0) return BDGDN_ERR_UNALIGNED;
     }
-    if (d->route == BDGDN_ROUTE_SPLIT) return BDGDN_ERR_UNSUPPORTED;
+    if (d->route == BDGDN_ROUTE_SPLIT) return BDGDN_ERR_UNSUPPORTED;   // not built yet
     return BDGDN_OK;
 }
 
@@ -85,10 +86,31 @@ const char *bdgdn_status_string(int status)
     }
 }
 
+// Blocks of the packed axis (packed) or of all sequences: the UT records are indexed by
+// (block, v-head); document starts are block-aligned, so blocks never straddle documents.
+static long total_blocks(const bdgdn_fwd_desc_t *d)
+{
+    const long nblk = (d->seqlen + d->block - 1) / d->block;
+    return d->num_seqs > 0 ? nblk : nblk * d->batch;
+}
+
+static size_t workspace_bytes_of(const bdgdn_fwd_desc_t *d)
+{
+    if (d->route != BDGDN_ROUTE_FUSED) return 0;
+    Types ty;
+    types_of(d->dtype, d->out_dtype, ty);
+    return (size_t)total_blocks(d) * d->h_v * scan_record_bytes(ty, lp_of(d->block));
+}
+
 size_t bdgdn_fwd_train_workspace(const bdgdn_fwd_desc_t *desc)
 {
     if (!desc) return 0;
-    return 0;
+    // size only descriptors whose shapes and types are valid (packing is checked per call)
+    if (check_heads(desc->h_qk, desc->h_v, desc->d_k, desc->d_v, desc->block, desc->scale, desc->dtype,
+                    desc->out_dtype) != BDGDN_OK)
+        return 0;
+    if (desc->batch <= 0 || desc->seqlen < 0) return 0;
+    return workspace_bytes_of(desc);
 }
 
 int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, const void *v,
@@ -105,36 +127,65 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(qn) || !aligned16(kn) ||
         !aligned16(vn) || !aligned16(o) || !aligned16(on))
         return BDGDN_ERR_INVALID_ARG;
-    if (workspace_bytes < bdgdn_fwd_train_workspace(desc)) return BDGDN_ERR_WORKSPACE;
-    (void)workspace;
+    const size_t need = workspace_bytes_of(desc);
+    if (need > 0 && (workspace_bytes < need || !workspace)) return BDGDN_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return BDGDN_ERR_WORKSPACE;
     const bool packed = desc->num_seqs > 0;
     const int nseq = packed ? desc->num_seqs : desc->batch;
     if (desc->seqlen == 0) return BDGDN_OK;
-
-    FwdArgs a;
-    a.q = q; a.k = k; a.v = v; a.qn = qn; a.kn = kn; a.vn = vn;
-    a.g = g; a.beta = beta; a.gn = gn; a.betan = betan;
-    a.cu = packed ? cu_seqlens_dev : nullptr;
-    a.h0 = h0; a.ht = ht; a.o = o; a.on = on;
-    a.T = desc->seqlen; a.h_qk = desc->h_qk; a.h_v = desc->h_v; a.dv = desc->d_v; a.L = desc->block;
-    a.n_chains = nseq * desc->h_v;
-    a.n_vt = desc->d_v / 32;
-    a.scale = desc->scale;
-    a.n_order = 0;
+    Types ty;
+    types_of(desc->dtype, desc->out_dtype, ty);
+    const int lp = lp_of(desc->block);
+    const hipStream_t strm = static_cast<hipStream_t>(stream);
+    // longest documents first, so that the longest serial chains start first
+    int order[kMaxOrder];
+    int n_order = 0;
     if (packed && nseq <= kMaxOrder) {
-        // longest documents first, so that the longest serial chains start first
         std::vector<int> idx(nseq);
         std::iota(idx.begin(), idx.end(), 0);
         std::stable_sort(idx.begin(), idx.end(), [&](int x, int y) {
             return cu_seqlens_host[x + 1] - cu_seqlens_host[x] > cu_seqlens_host[y + 1] - cu_seqlens_host[y];
         });
-        for (int i = 0; i < nseq; ++i) a.order[i] = idx[i];
-        a.n_order = nseq;
+        for (int i = 0; i < nseq; ++i) order[i] = idx[i];
+        n_order = nseq;
     }
-    Types ty;
-    types_of(desc->dtype, desc->out_dtype, ty);
-    hipError_t e = launch_fwd_fused(ty, desc->d_k, lp_of(desc->block), a,
-                                    static_cast<hipStream_t>(stream));
+    hipError_t e;
+    if (desc->route == BDGDN_ROUTE_FUSED) {
+        IntraArgs ia;
+        ia.q = q; ia.k = k; ia.qn = qn; ia.kn = kn;
+        ia.g = g; ia.beta = beta; ia.gn = gn; ia.betan = betan;
+        ia.ws = static_cast<unsigned char *>(workspace);
+        ia.T = desc->seqlen; ia.L = desc->block;
+        ia.nblk = (desc->seqlen + desc->block - 1) / desc->block;
+        ia.total_blocks = total_blocks(desc);
+        ia.h_qk = desc->h_qk; ia.h_v = desc->h_v;
+        ScanArgs sa;
+        sa.q = q; sa.k = k; sa.v = v; sa.qn = qn; sa.kn = kn; sa.vn = vn;
+        sa.cu = packed ? cu_seqlens_dev : nullptr;
+        sa.h0 = h0; sa.ht = ht; sa.o = o; sa.on = on;
+        sa.ws = static_cast<const unsigned char *>(workspace);
+        sa.T = desc->seqlen; sa.L = desc->block; sa.nblk = ia.nblk;
+        sa.h_qk = desc->h_qk; sa.h_v = desc->h_v; sa.dv = desc->d_v;
+        sa.n_chains = nseq * desc->h_v;
+        sa.n_vt = desc->d_v / scan_tile_v();
+        sa.scale = desc->scale;
+        sa.n_order = n_order;
+        for (int i = 0; i < n_order; ++i) sa.order[i] = order[i];
+        e = launch_fwd_scan(ty, desc->d_k, lp, ia, sa, strm);
+    } else {
+        FwdArgs a;
+        a.q = q; a.k = k; a.v = v; a.qn = qn; a.kn = kn; a.vn = vn;
+        a.g = g; a.beta = beta; a.gn = gn; a.betan = betan;
+        a.cu = packed ? cu_seqlens_dev : nullptr;
+        a.h0 = h0; a.ht = ht; a.o = o; a.on = on;
+        a.T = desc->seqlen; a.h_qk = desc->h_qk; a.h_v = desc->h_v; a.dv = desc->d_v; a.L = desc->block;
+        a.n_chains = nseq * desc->h_v;
+        a.n_vt = desc->d_v / fwd_tile_v();
+        a.scale = desc->scale;
+        a.n_order = n_order;
+        for (int i = 0; i < n_order; ++i) a.order[i] = order[i];
+        e = launch_fwd_fused(ty, desc->d_k, lp, a, strm);
+    }
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
 }
 
@@ -154,7 +205,7 @@ static ServeArgs serve_args(const bdgdn_serve_desc_t *d, const float *pool, cons
     a.pool = const_cast<float *>(pool);
     a.slot = slot; a.o = o;
     a.R = d->num_req; a.h_qk = d->h_qk; a.h_v = d->h_v; a.dv = d->d_v; a.L = d->block;
-    a.n_vt = d->d_v / 32;
+    a.n_vt = d->d_v / serve_tile_v();
     a.scale = d->scale;
     return a;
 }

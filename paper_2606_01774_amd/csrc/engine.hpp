@@ -17,147 +17,11 @@
 // S_r = gamma_r S0 + sum_{i<=r} (gamma_r/gamma_i) k_i delta_i^T); only
 // exponentials of block-local differences are ever formed.
 //
-// MFMA operand convention: a 16x16 output tile C += A * B where A is 16 x K and B is
-// given transposed (16 x K); both live in LDS with K contiguous.  Lane l holds
-// C[4*(l>>4) + i][l & 15] in accumulator element i.
 #pragma once
 
-#include <hip/hip_runtime.h>
-#include <stdint.h>
+#include "common.hpp"
 
 namespace bdgdn {
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
-
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
-constexpr float kLog2e = 1.4426950408889634f;
-
-template <typename E> struct Mma;
-
-// fp16 operands, fp32 accumulate: v_mfma_f32_16x16x32_f16 (8 operands per lane).  The
-// bf16 inputs are staged as fp16 (exact for |x| in [2^-14, 2^15]); every rounded
-// intermediate operand (state, T, masked Q K^T, Delta) then carries 11 significant
-// bits instead of bf16's 8, at the same MFMA rate.
-template <> struct Mma<_Float16> {
-    static constexpr int kStep = 32;
-    static constexpr int kPerLane = 8;
-    static constexpr int kPad = 8;  // LDS row padding in elements (16 bytes)
-    typedef f16x8 frag;
-    static __device__ __forceinline__ frag load(const _Float16 *p)
-    {
-        return *reinterpret_cast<const f16x8 *>(p);
-    }
-    static __device__ __forceinline__ f32x4 mma(frag a, frag b, f32x4 c)
-    {
-        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-    }
-};
-
-// fp32 operands: v_mfma_f32_16x16x4_f32 (one operand per lane).
-template <> struct Mma<float> {
-    static constexpr int kStep = 4;
-    static constexpr int kPerLane = 1;
-    static constexpr int kPad = 4;
-    typedef float frag;
-    static __device__ __forceinline__ frag load(const float *p) { return *p; }
-    static __device__ __forceinline__ f32x4 mma(frag a, frag b, f32x4 c)
-    {
-        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-    }
-};
-
-template <typename E> __device__ __forceinline__ E to_e(float x);
-template <> __device__ __forceinline__ __bf16 to_e<__bf16>(float x) { return (__bf16)x; }
-template <> __device__ __forceinline__ _Float16 to_e<_Float16>(float x) { return (_Float16)x; }
-template <> __device__ __forceinline__ float to_e<float>(float x) { return x; }
-__device__ __forceinline__ float to_f(__bf16 x) { return (float)x; }
-__device__ __forceinline__ float to_f(_Float16 x) { return (float)x; }
-__device__ __forceinline__ float to_f(float x) { return x; }
-
-// A 16-byte chunk of input elements re-encoded as operand elements of the same size.
-template <typename In, typename Op> __device__ __forceinline__ uint4 to_operand(uint4 raw)
-{
-    static_assert(sizeof(In) == sizeof(Op), "same element size");
-    if constexpr (__is_same(In, Op)) {
-        return raw;
-    } else {
-        constexpr int N = 16 / sizeof(In);
-        In src[N];
-        Op dst[N];
-        __builtin_memcpy(src, &raw, 16);
-#pragma unroll
-        for (int e = 0; e < N; ++e) dst[e] = to_e<Op>(to_f(src[e]));
-        uint4 out;
-        __builtin_memcpy(&out, dst, 16);
-        return out;
-    }
-}
-
-// Four consecutive elements to LDS (8-byte store for 16-bit types, 16-byte for fp32).
-__device__ __forceinline__ void st4(_Float16 *p, float a, float b, float c, float d)
-{
-    f16x4 v = {(_Float16)a, (_Float16)b, (_Float16)c, (_Float16)d};
-    *reinterpret_cast<f16x4 *>(p) = v;
-}
-__device__ __forceinline__ void st4(float *p, float a, float b, float c, float d)
-{
-    f32x4 v = {a, b, c, d};
-    *reinterpret_cast<f32x4 *>(p) = v;
-}
-
-// C(16x16) += A(16 x K) * Bt(16 x K)^T, operands in LDS with K contiguous.  For fp16
-// a K that is not a multiple of 32 ends with one v_mfma_f32_16x16x16_f16 step
-// (4 operands per lane) so no operand is read past K.
-template <typename E, int K>
-__device__ __forceinline__ f32x4 tile_mma(f32x4 acc, const E *A, int lda, const E *Bt, int ldb,
-                                          int lane)
-{
-    constexpr int KS = Mma<E>::kStep;
-    constexpr int KMAIN = K - K % KS;
-    const int r = lane & 15, ko = (lane >> 4) * Mma<E>::kPerLane;
-    const E *a = A + r * lda + ko;
-    const E *b = Bt + r * ldb + ko;
-#pragma unroll
-    for (int k0 = 0; k0 < KMAIN; k0 += KS)
-        acc = Mma<E>::mma(Mma<E>::load(a + k0), Mma<E>::load(b + k0), acc);
-    if constexpr (KMAIN != K) {
-        static_assert(sizeof(E) == 2 && K - KMAIN == 16, "fp16 tail of 16");
-        const int k4 = (lane >> 4) * 4;
-        const f16x4 a4 = *reinterpret_cast<const f16x4 *>(A + r * lda + KMAIN + k4);
-        const f16x4 b4 = *reinterpret_cast<const f16x4 *>(Bt + r * ldb + KMAIN + k4);
-        acc = __builtin_amdgcn_mfma_f32_16x16x16f16(a4, b4, acc, 0, 0, 0);
-    }
-    return acc;
-}
-
-// C(16x16) += A(16 x K) * B(K x 16), fp32, both row-major in LDS (used by the solve).
-__device__ __forceinline__ f32x4 tile_mma_rr(f32x4 acc, const float *A, int lda, const float *B,
-                                             int ldb, int K, int lane)
-{
-    const int m = lane & 15, kk = lane >> 4;
-    for (int k0 = 0; k0 < K; k0 += 4)
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A[m * lda + k0 + kk], B[(k0 + kk) * ldb + m],
-                                                   acc, 0, 0, 0);
-    return acc;
-}
-
-__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
-
-// Lower-triangular tile index -> (bi, bj), bi >= bj, row-major over bi.
-__device__ __forceinline__ void tri_decode(int l, int &bi, int &bj)
-{
-    bi = 0;
-    while (l > bi) {
-        l -= bi + 1;
-        ++bi;
-    }
-    bj = l;
-}
 
 // ---------------------------------------------------------------------------------
 // Shared-memory layout of one workgroup.  Buffers whose lifetimes do not overlap
@@ -181,11 +45,13 @@ struct Layout {
     static constexpr int NVB = BV / 16;
     static constexpr int NSOLVE = (CL ? 1 : 0) + (NZ ? 1 : 0);
     static constexpr int NROWS = (CL ? 1 : 0) + (CO ? 1 : 0) + (NZ ? 2 : 0);
-    // row-buffer slots
+    // row-buffer slots; slot 0 is the clean K, which lives outside U because the
+    // state update at the end of the block reads it
     static constexpr int SLOT_K = 0;
     static constexpr int SLOT_Q = 1;
     static constexpr int SLOT_KN = CL ? (CO ? 2 : 1) : 0;
     static constexpr int SLOT_QN = SLOT_KN + 1;
+    static constexpr int NROWS_U = NROWS - (CL ? 1 : 0);   // row sets inside U
 
     static constexpr int al(int x) { return (x + 15) & ~15; }
     static constexpr int mx(int a, int b) { return a > b ? a : b; }
@@ -201,12 +67,12 @@ struct Layout {
     static constexpr int OFF_POST = 0;                               // over A after the solve
     static constexpr int OFF_T = al(mx(OFF_Y + Y_B, NPOST * DT_B));
     static constexpr int OFF_D = OFF_T + NSOLVE * TM_B;
-    static constexpr int U_B = al(mx(NROWS * ROWS_B, OFF_D + NSOLVE * DT_B));
+    static constexpr int U_B = al(mx(NROWS_U * ROWS_B, OFF_D + NSOLVE * DT_B));
 
-    static constexpr int OFF_U = 0;
-    static constexpr int OFF_KT = OFF_U + U_B;
-    static constexpr int KT_B = CL ? al(DK * TS * SZ) : 0;
-    static constexpr int OFF_ST = OFF_KT + KT_B;
+    static constexpr int OFF_K = 0;                     // clean K rows (CL only)
+    static constexpr int K_B = CL ? ROWS_B : 0;
+    static constexpr int OFF_U = OFF_K + K_B;
+    static constexpr int OFF_ST = OFF_U + U_B;
     static constexpr int ST_B = al(BV * RS * SZ);
     static constexpr int OFF_V = OFF_ST + ST_B;
     static constexpr int V_B = al(LP * VS * SZ);
@@ -230,8 +96,11 @@ template <typename In, typename Out> struct BlockIO {
 
 // In: element type of q, k, v in global memory; E: MFMA operand type in LDS (same size
 // as In); Out: element type of the outputs.
-template <typename In, typename E, typename Out, int DK, int BV, int LP, bool CL, bool CO, bool NZ>
+template <typename In, typename E, typename Out, int DK, int BV, int LP, bool CL, bool CO, bool NZ,
+          int NW = 4>
 struct Engine {
+    static constexpr int kWaves = NW;
+    static constexpr int kThreads = 64 * NW;
     static_assert(sizeof(In) == sizeof(E), "inputs are staged chunk for chunk");
     typedef Layout<E, DK, BV, LP, CL, CO, NZ> Ly;
     typedef BlockIO<In, Out> IO;
@@ -264,19 +133,22 @@ struct Engine {
     unsigned char *smem;
     int tid, lane, wave;
 
-    __device__ E *rows(int slot) const { return reinterpret_cast<E *>(smem + Ly::OFF_U + slot * Ly::ROWS_B); }
-    __device__ float *amat(int m) const { return reinterpret_cast<float *>(smem + Ly::OFF_U + Ly::OFF_A + m * Ly::A_B); }
-    __device__ float *ytmp(int p) const { return reinterpret_cast<float *>(smem + Ly::OFF_U + Ly::OFF_Y) + p * 256; }
-    __device__ E *tmat(int m) const { return reinterpret_cast<E *>(smem + Ly::OFF_U + Ly::OFF_T + m * Ly::TM_B); }
-    __device__ E *dmat(int m) const { return reinterpret_cast<E *>(smem + Ly::OFF_U + Ly::OFF_D + m * Ly::DT_B); }
+    __device__ __forceinline__ E *rows(int slot) const
+    {
+        if (CL && slot == Ly::SLOT_K) return reinterpret_cast<E *>(smem + Ly::OFF_K);
+        return reinterpret_cast<E *>(smem + Ly::OFF_U + (slot - (CL ? 1 : 0)) * Ly::ROWS_B);
+    }
+    __device__ __forceinline__ float *amat(int m) const { return reinterpret_cast<float *>(smem + Ly::OFF_U + Ly::OFF_A + m * Ly::A_B); }
+    __device__ __forceinline__ float *ytmp(int p) const { return reinterpret_cast<float *>(smem + Ly::OFF_U + Ly::OFF_Y) + p * 256; }
+    __device__ __forceinline__ E *tmat(int m) const { return reinterpret_cast<E *>(smem + Ly::OFF_U + Ly::OFF_T + m * Ly::TM_B); }
+    __device__ __forceinline__ E *dmat(int m) const { return reinterpret_cast<E *>(smem + Ly::OFF_U + Ly::OFF_D + m * Ly::DT_B); }
     // post-solve [v][token] buffers: 0 = Delta, 1 = decayed Delta (clean), 2 or 0 = Delta~
-    __device__ E *post(int i) const { return reinterpret_cast<E *>(smem + Ly::OFF_U + Ly::OFF_POST + i * Ly::DT_B); }
-    __device__ E *kt() const { return reinterpret_cast<E *>(smem + Ly::OFF_KT); }
-    __device__ E *st() const { return reinterpret_cast<E *>(smem + Ly::OFF_ST); }
-    __device__ E *vs(int m) const { return reinterpret_cast<E *>(smem + Ly::OFF_V + m * Ly::V_B); }
-    __device__ E *pm() const { return reinterpret_cast<E *>(smem + Ly::OFF_PR); }
-    __device__ E *rm() const { return reinterpret_cast<E *>(smem + Ly::OFF_PR + (CO ? Ly::TM_B : 0)); }
-    __device__ float *gates(int s) const { return reinterpret_cast<float *>(smem + Ly::OFF_GATES) + s * 64; }
+    __device__ __forceinline__ E *post(int i) const { return reinterpret_cast<E *>(smem + Ly::OFF_U + Ly::OFF_POST + i * Ly::DT_B); }
+    __device__ __forceinline__ E *st() const { return reinterpret_cast<E *>(smem + Ly::OFF_ST); }
+    __device__ __forceinline__ E *vs(int m) const { return reinterpret_cast<E *>(smem + Ly::OFF_V + m * Ly::V_B); }
+    __device__ __forceinline__ E *pm() const { return reinterpret_cast<E *>(smem + Ly::OFF_PR); }
+    __device__ __forceinline__ E *rm() const { return reinterpret_cast<E *>(smem + Ly::OFF_PR + (CO ? Ly::TM_B : 0)); }
+    __device__ __forceinline__ float *gates(int s) const { return reinterpret_cast<float *>(smem + Ly::OFF_GATES) + s * 64; }
 
     static constexpr int SOLVE_N = Ly::NSOLVE;   // solve matrix index: 0 = clean (if CL), last = noisy
     static constexpr int MAT_C = 0;
@@ -293,7 +165,7 @@ struct Engine {
     // ----------------------------------------------------------------- state I/O
     // Load fp32 state tile [d_k][v0..v0+BV) of row stride dv into accumulator layout
     // (tile t = (bk, bc) holds S[16bk + 4(l>>4) + i][16bc + (l&15)]).  src == NULL -> 0.
-    __device__ void load_state(f32x4 (&S)[NSW], const float *src, int dv) const
+    __device__ __forceinline__ void load_state(f32x4 (&S)[NSW], const float *src, int dv) const
     {
 #pragma unroll
         for (int s = 0; s < NSW; ++s) {
@@ -310,7 +182,7 @@ struct Engine {
             S[s] = acc;
         }
     }
-    __device__ void store_state(const f32x4 (&S)[NSW], float *dst, int dv) const
+    __device__ __forceinline__ void store_state(const f32x4 (&S)[NSW], float *dst, int dv) const
     {
 #pragma unroll
         for (int s = 0; s < NSW; ++s) {
@@ -326,7 +198,7 @@ struct Engine {
         }
     }
     // S^T (MFMA operand, dtype E) into LDS: ST[v][d_k].
-    __device__ void write_st(const f32x4 (&S)[NSW]) const
+    __device__ __forceinline__ void write_st(const f32x4 (&S)[NSW]) const
     {
 #pragma unroll
         for (int s = 0; s < NSW; ++s) {
@@ -340,53 +212,73 @@ struct Engine {
     }
 
     // ----------------------------------------------------------------- phase L
-    // Global -> LDS for one block: q/k rows (and K transposed), the V tiles, gates.
-    // Rows at or past nvalid are zero: identity positions (k = 0, g = 0, beta = 0).
-    __device__ void load_block(const IO &io) const
+    // Global -> registers (fetch) and registers -> LDS (stage) for one block: q/k rows
+    // (and K transposed), the V tiles, gates.  Rows at or past nvalid are zero:
+    // identity positions (k = 0, g = 0, beta = 0).  The fetch of block b+1 is issued
+    // right after block b is staged so its latency hides behind block b's work.
+    struct Fetched {
+        u32x4 rb[Ly::NROWS][RPT];
+        u32x4 vb[Ly::NSOLVE][VPT];
+        float gv;
+    };
+
+    // Source of row set rs (a compile-time index after unrolling).
+    __device__ __forceinline__ const In *row_src(const IO &io, int rs) const
+    {
+        if (CL && rs == Ly::SLOT_K) return io.k;
+        if (CO && rs == Ly::SLOT_Q) return io.q;
+        if (NZ && rs == Ly::SLOT_KN) return io.kn;
+        return io.qn;
+    }
+
+    // Rows at or past nvalid are read from the last valid row (always in bounds: a
+    // block has at least one row) and replaced by zero, so every load is an
+    // unconditional 16-byte global load.  Wave w < 4 reads gate slot w (one row per
+    // lane), so the gate pointer is uniform across the wave.
+    __device__ __forceinline__ void fetch(const IO &io, Fetched &f) const
     {
         constexpr int NR = Ly::NROWS;
-        const In *src[4] = {nullptr, nullptr, nullptr, nullptr};
-        if (CL) src[Ly::SLOT_K] = io.k;
-        if (CO) src[Ly::SLOT_Q] = io.q;
-        if (NZ) {
-            src[Ly::SLOT_KN] = io.kn;
-            src[Ly::SLOT_QN] = io.qn;
-        }
-        uint4 rb[NR][RPT];
-        const uint4 zero = {0u, 0u, 0u, 0u};
+        static_assert(NW >= 4, "gate slots are loaded by waves 0..3");
+        const u32x4 zero = {0u, 0u, 0u, 0u};
+        const int last = io.nvalid - 1;
 #pragma unroll
-        for (int rs = 0; rs < NR; ++rs)
+        for (int s = 0; s < RPT; ++s) {
+            const int c = tid + s * kThreads;
+            const int cr = c < RCH ? c : RCH - 1;
+            const int t = cr / CPR, cc = cr % CPR;
+            const bool ok = c < RCH && t <= last;
+            const long off = (long)(t <= last ? t : last) * io.qk_stride + cc * EPC;
 #pragma unroll
-            for (int s = 0; s < RPT; ++s) {
-                const int c = tid + s * kThreads;
-                const int t = c / CPR, cc = c % CPR;
-                rb[rs][s] = (c < RCH && t < io.nvalid)
-                                ? to_operand<In, E>(*reinterpret_cast<const uint4 *>(src[rs] + t * io.qk_stride + cc * EPC))
-                                : zero;
+            for (int rs = 0; rs < NR; ++rs) {
+                const u32x4 x = *reinterpret_cast<const u32x4 *>(row_src(io, rs) + off);
+                f.rb[rs][s] = ok ? x : zero;
             }
-        const In *vsrc[2] = {CL ? io.v : io.vn, io.vn};
-        uint4 vb[Ly::NSOLVE][VPT];
-#pragma unroll
-        for (int m = 0; m < Ly::NSOLVE; ++m)
-#pragma unroll
-            for (int s = 0; s < VPT; ++s) {
-                const int c = tid + s * kThreads;
-                const int t = c / VCPR, cc = c % VCPR;
-                vb[m][s] = (c < VCH && t < io.nvalid)
-                               ? to_operand<In, E>(*reinterpret_cast<const uint4 *>(vsrc[m] + t * io.v_stride + cc * EPC))
-                               : zero;
-            }
-        float gv = 0.f;
-        {
-            const int which = tid / LP, t = tid % LP;
-            const float *gp = nullptr;
-            if (which == GS_G && CL) gp = io.g;
-            if (which == GS_B && CL) gp = io.beta;
-            if (which == GS_GN && NZ) gp = io.gn;
-            if (which == GS_BN && NZ) gp = io.betan;
-            if (which < 4 && gp && t < io.nvalid) gv = gp[t * io.gate_stride];
         }
-        // LDS writes
+#pragma unroll
+        for (int s = 0; s < VPT; ++s) {
+            const int c = tid + s * kThreads;
+            const int cr = c < VCH ? c : VCH - 1;
+            const int t = cr / VCPR, cc = cr % VCPR;
+            const bool ok = c < VCH && t <= last;
+            const long off = (long)(t <= last ? t : last) * io.v_stride + cc * EPC;
+#pragma unroll
+            for (int m = 0; m < Ly::NSOLVE; ++m) {
+                const u32x4 x = *reinterpret_cast<const u32x4 *>(((CL && m == 0) ? io.v : io.vn) + off);
+                f.vb[m][s] = ok ? x : zero;
+            }
+        }
+        f.gv = 0.f;
+        const bool want = (wave < 2 && CL) || (wave >= 2 && wave < 4 && NZ);
+        if (want) {
+            const float *gp = wave == GS_G ? io.g : wave == GS_B ? io.beta : wave == GS_GN ? io.gn : io.betan;
+            const float x = gp[(long)(lane <= last ? lane : last) * io.gate_stride];
+            f.gv = lane <= last ? x : 0.f;
+        }
+    }
+
+    __device__ __forceinline__ void stage(const Fetched &f) const
+    {
+        constexpr int NR = Ly::NROWS;
 #pragma unroll
         for (int rs = 0; rs < NR; ++rs)
 #pragma unroll
@@ -394,22 +286,9 @@ struct Engine {
                 const int c = tid + s * kThreads;
                 if (c < RCH) {
                     const int t = c / CPR, cc = c % CPR;
-                    *reinterpret_cast<uint4 *>(rows(rs) + t * Ly::RS + cc * EPC) = rb[rs][s];
+                    *reinterpret_cast<u32x4 *>(rows(rs) + t * Ly::RS + cc * EPC) = to_operand<In, E>(f.rb[rs][s]);
                 }
             }
-        if (CL) {
-#pragma unroll
-            for (int s = 0; s < RPT; ++s) {
-                const int c = tid + s * kThreads;
-                if (c < RCH) {
-                    const int t = c / CPR, cc = c % CPR;
-                    E tmp[EPC];
-                    __builtin_memcpy(tmp, &rb[Ly::SLOT_K][s], 16);
-#pragma unroll
-                    for (int e = 0; e < EPC; ++e) kt()[(cc * EPC + e) * Ly::TS + t] = tmp[e];
-                }
-            }
-        }
 #pragma unroll
         for (int m = 0; m < Ly::NSOLVE; ++m)
 #pragma unroll
@@ -417,14 +296,14 @@ struct Engine {
                 const int c = tid + s * kThreads;
                 if (c < VCH) {
                     const int t = c / VCPR, cc = c % VCPR;
-                    *reinterpret_cast<uint4 *>(vs(m) + t * Ly::VS + cc * EPC) = vb[m][s];
+                    *reinterpret_cast<u32x4 *>(vs(m) + t * Ly::VS + cc * EPC) = to_operand<In, E>(f.vb[m][s]);
                 }
             }
-        if (tid < 4 * LP) gates(tid / LP)[tid % LP] = gv;
+        if (wave < 4 && lane < LP) gates(wave)[lane] = f.gv;
     }
 
     // In-place inclusive scan of a gate slot (times log2 e), by one wave.
-    __device__ void scan_gates(int slot) const
+    __device__ __forceinline__ void scan_gates(int slot) const
     {
         float *gp = gates(slot);
         float x = lane < LP ? gp[lane] * kLog2e : 0.f;
@@ -438,7 +317,7 @@ struct Engine {
 
     // ----------------------------------------------------------------- phase G
     // Which operands a phase-G list entry multiplies; K = DK for all of them.
-    __device__ void g_decode(int idx, int &kind, int &bi, int &bj, const E *&A, const E *&B) const
+    __device__ __forceinline__ void g_decode(int idx, int &kind, int &bi, int &bj, const E *&A, const E *&B) const
     {
         int l = idx;
         kind = 0;
@@ -456,7 +335,7 @@ struct Engine {
     }
 
     // All Gram products, K S0 products and (owned) Q S0 products of the block.
-    __device__ void gram_and_x(f32x4 (&gacc)[NGW], f32x4 (&x2)[NXW], f32x4 (&x4)[NXW]) const
+    __device__ __forceinline__ void gram_and_x(f32x4 (&gacc)[NGW], f32x4 (&x2)[NXW], f32x4 (&x4)[NXW]) const
     {
         const f32x4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -484,7 +363,7 @@ struct Engine {
     }
 
     // Masks, decays and beta applied to the phase-G results, written to LDS.
-    __device__ void epilogue(const f32x4 (&gacc)[NGW], f32x4 (&x2)[NXW], f32x4 (&x4)[NXW]) const
+    __device__ __forceinline__ void epilogue(const f32x4 (&gacc)[NGW], f32x4 (&x2)[NXW], f32x4 (&x4)[NXW]) const
     {
         const float *G = gates(GS_G), *Bt = gates(GS_B), *Gn = gates(GS_GN), *Bn = gates(GS_BN);
         const int r0 = 4 * (lane >> 4), cl = lane & 15;
@@ -505,7 +384,7 @@ struct Engine {
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const int r = 16 * bi + r0 + i;
-                        Am[r * Ly::FS + c] = c < r ? BB[r] * exp2f(GG[r] - gc) * a[i] : 0.f;
+                        Am[r * Ly::FS + c] = c < r ? BB[r] * fexp2(GG[r] - gc) * a[i] : 0.f;
                     }
                 } else if (kind == 1) {        // P_rc = exp(G_r - G_c) (q_r . k_c), c <= r
                     const int c = 16 * bj + cl;
@@ -513,11 +392,11 @@ struct Engine {
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const int r = 16 * bi + r0 + i;
-                        pm()[r * Ly::TS + c] = to_e<E>(c <= r ? exp2f(G[r] - gc) * a[i] : 0.f);
+                        pm()[r * Ly::TS + c] = to_e<E>(c <= r ? fexp2(G[r] - gc) * a[i] : 0.f);
                     }
                 } else if (kind == 3) {        // R_rc = exp(Gn_end - Gn_c) (qn_r . kn_c)
                     const int c = 16 * bj + cl;
-                    const float dc = exp2f(Gn[LP - 1] - Gn[c]);
+                    const float dc = fexp2(Gn[LP - 1] - Gn[c]);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const int r = 16 * bi + r0 + i;
@@ -531,7 +410,7 @@ struct Engine {
                     const int r = 16 * bi + r0;
                     float d[4];
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) d[i] = to_f(V[(r + i) * Ly::VS + vc]) - exp2f(GG[r + i]) * a[i];
+                    for (int i = 0; i < 4; ++i) d[i] = to_f(V[(r + i) * Ly::VS + vc]) - fexp2(GG[r + i]) * a[i];
                     st4(dmat(noisy ? MAT_N : MAT_C) + vc * Ly::TS + r, d[0], d[1], d[2], d[3]);
                 }
             }
@@ -543,10 +422,10 @@ struct Engine {
                 const int r = 16 * (t / NVB) + r0;
                 if (CO) {
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) x2[s][i] *= exp2f(G[r + i]);
+                    for (int i = 0; i < 4; ++i) x2[s][i] *= fexp2(G[r + i]);
                 }
                 if (NZ) {
-                    const float e = exp2f(Gn[LP - 1]);
+                    const float e = fexp2(Gn[LP - 1]);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) x4[s][i] *= e;
                 }
@@ -559,7 +438,7 @@ struct Engine {
     // T = (I + A)^{-1} diag(beta) as MFMA operands.  Diagonal 16x16 blocks by forward
     // substitution (one column per lane), off-diagonal blocks row-block by row-block:
     //   X_ij = -X_ii * sum_{k=j}^{i-1} A_ik X_kj.
-    __device__ void solve() const
+    __device__ __forceinline__ void solve() const
     {
         if (wave < Ly::NSOLVE) {
             const int g = lane >> 4, j = lane & 15;
@@ -577,7 +456,7 @@ struct Engine {
                 for (int r = 0; r < 16; ++r) Ab[r * Ly::FS + j] = x[r];
             }
         }
-        __syncthreads();
+        lds_barrier();
         for (int i = 1; i < NB; ++i) {
             const int npairs = Ly::NSOLVE * i;
             for (int p = wave; p < npairs; p += kWaves) {
@@ -590,7 +469,7 @@ struct Engine {
 #pragma unroll
                 for (int q = 0; q < 4; ++q) Y[(4 * (lane >> 4) + q) * 16 + (lane & 15)] = acc[q];
             }
-            __syncthreads();
+            lds_barrier();
             for (int p = wave; p < npairs; p += kWaves) {
                 const int m = p / i, j = p % i;
                 float *Am = amat(m);
@@ -600,7 +479,7 @@ struct Engine {
                 for (int q = 0; q < 4; ++q)
                     Am[(16 * i + 4 * (lane >> 4) + q) * Ly::FS + 16 * j + (lane & 15)] = -acc[q];
             }
-            __syncthreads();
+            lds_barrier();
         }
         // T = X diag(beta): lower triangle, zero above.
         for (int e = tid; e < Ly::NSOLVE * LP * LP; e += kThreads) {
@@ -611,7 +490,7 @@ struct Engine {
     }
 
     // ----------------------------------------------------------------- phase Delta
-    __device__ void deltas() const
+    __device__ __forceinline__ void deltas() const
     {
         const float *G = gates(GS_G);
         const int r0 = 4 * (lane >> 4), cl = lane & 15;
@@ -631,15 +510,15 @@ struct Engine {
                 } else {
                     st4(post(0) + vc * Ly::TS + r, acc[0], acc[1], acc[2], acc[3]);
                     const float ge = G[LP - 1];
-                    st4(post(1) + vc * Ly::TS + r, exp2f(ge - G[r]) * acc[0], exp2f(ge - G[r + 1]) * acc[1],
-                        exp2f(ge - G[r + 2]) * acc[2], exp2f(ge - G[r + 3]) * acc[3]);
+                    st4(post(1) + vc * Ly::TS + r, fexp2(ge - G[r]) * acc[0], fexp2(ge - G[r + 1]) * acc[1],
+                        fexp2(ge - G[r + 2]) * acc[2], fexp2(ge - G[r + 3]) * acc[3]);
                 }
             }
         }
     }
 
     // ----------------------------------------------------------------- outputs
-    __device__ void store_rows(Out *dst, long stride, int nvalid, int bi, int bc, f32x4 acc, float scale) const
+    __device__ __forceinline__ void store_rows(Out *dst, long stride, int nvalid, int bi, int bc, f32x4 acc, float scale) const
     {
         const int r = 16 * bi + 4 * (lane >> 4), vc = 16 * bc + (lane & 15);
 #pragma unroll
@@ -647,7 +526,7 @@ struct Engine {
             if (r + i < nvalid) dst[(long)(r + i) * stride + vc] = to_e<Out>(acc[i] * scale);
     }
 
-    __device__ void outputs(const IO &io, const f32x4 (&x2)[NXW], const f32x4 (&x4)[NXW], float scale) const
+    __device__ __forceinline__ void outputs(const IO &io, const f32x4 (&x2)[NXW], const f32x4 (&x4)[NXW], float scale) const
     {
 #pragma unroll
         for (int s = 0; s < NXW; ++s) {
@@ -667,40 +546,44 @@ struct Engine {
     }
 
     // S <- gamma_n S + K^T diag(gamma_n / gamma) Delta, then refresh the S^T operand.
-    __device__ void update_state(f32x4 (&S)[NSW]) const
+    __device__ __forceinline__ void update_state(f32x4 (&S)[NSW]) const
     {
-        const float decay = exp2f(gates(GS_G)[LP - 1]);
+        const float decay = fexp2(gates(GS_G)[LP - 1]);
 #pragma unroll
         for (int s = 0; s < NSW; ++s) {
             const int t = wave + s * kWaves;
             if (t < NS) {
                 const int bk = t / NVB, bc = t % NVB;
                 f32x4 acc = S[s] * decay;
-                S[s] = tile_mma<E, LP>(acc, kt() + 16 * bk * Ly::TS, Ly::TS, post(1) + 16 * bc * Ly::TS, Ly::TS, lane);
+                S[s] = tile_mma_at<E, LP>(acc, rows(Ly::SLOT_K) + 16 * bk, Ly::RS, post(1) + 16 * bc * Ly::TS, Ly::TS, lane);
             }
         }
         write_st(S);
     }
 
     // One block of the two-stream schedule from the state whose S^T operand is in LDS.
-    __device__ void step(const IO &io, f32x4 (&S)[NSW], float scale) const
+    // f holds this block's fetched inputs on entry; when has_next is set the inputs of
+    // `next` are fetched into f while this block computes.
+    __device__ __forceinline__ void step(const IO &io, bool has_next, const IO &next, Fetched &f,
+                                         f32x4 (&S)[NSW], float scale) const
     {
-        load_block(io);
-        __syncthreads();
+        stage(f);
+        lds_barrier();
+        if (has_next) fetch(next, f);
         if (CL && wave == 0) scan_gates(GS_G);
         if (NZ && wave == (CL ? 1 : 0)) scan_gates(GS_GN);
         f32x4 gacc[NGW], x2[NXW], x4[NXW];
         gram_and_x(gacc, x2, x4);
-        __syncthreads();                 // row buffers are dead from here on
+        lds_barrier();                 // row buffers are dead from here on
         epilogue(gacc, x2, x4);
-        __syncthreads();
+        lds_barrier();
         solve();
-        __syncthreads();
+        lds_barrier();
         deltas();
-        __syncthreads();
+        lds_barrier();
         outputs(io, x2, x4, scale);
         if (CL) update_state(S);
-        __syncthreads();
+        lds_barrier();
     }
 };
 

@@ -11,13 +11,21 @@
 
 namespace bdgdn {
 
-constexpr int kFwdBV = 32;
+#ifndef BDGDN_FWD_BV
+#define BDGDN_FWD_BV 32
+#endif
+#ifndef BDGDN_FWD_NW
+#define BDGDN_FWD_NW 8
+#endif
+constexpr int kFwdBV = BDGDN_FWD_BV;  // d_v columns per workgroup
+constexpr int kFwdNW = BDGDN_FWD_NW;  // waves per workgroup
+constexpr int kFwdThreads = 64 * kFwdNW;
 
 template <typename In, typename Op, typename Out, int DK, int BV, int LP>
-__global__ void __launch_bounds__(kThreads) bdgdn_fwd_fused_kernel(FwdArgs a)
+__global__ void __launch_bounds__(kFwdThreads) bdgdn_fwd_fused_kernel(FwdArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    typedef Engine<In, Op, Out, DK, BV, LP, true, true, true> Eng;
+    typedef Engine<In, Op, Out, DK, BV, LP, true, true, true, kFwdNW> Eng;
     // Workgroup ids are dealt round-robin over the 8 XCDs; ids i, i+8, i+16, ... of a
     // group carry the d_v tiles of one chain so they share that XCD's L2 for q/k.
     const int id = blockIdx.x;
@@ -44,29 +52,37 @@ __global__ void __launch_bounds__(kThreads) bdgdn_fwd_fused_kernel(FwdArgs a)
     eng.load_state(S, a.h0 ? a.h0 + state_off : nullptr, a.dv);
     eng.write_st(S);
     __syncthreads();
-    typename Eng::IO io;
-    io.qk_stride = (long)a.h_qk * DK;
-    io.v_stride = (long)a.h_v * a.dv;
-    io.gate_stride = a.h_v;
-    for (long j0 = 0; j0 < len; j0 += a.L) {
+    // Block descriptors are rebuilt by value each iteration (scalar arithmetic); an
+    // array of them indexed at run time would live in scratch memory.
+    auto make_io = [&](long j0) {
+        typename Eng::IO x;
         const long row0 = base + j0;
         const long qk_off = (row0 * a.h_qk + hq) * DK;
         const long v_off = (row0 * a.h_v + h) * a.dv + v0;
         const long g_off = row0 * a.h_v + h;
-        io.k = static_cast<const In *>(a.k) + qk_off;
-        io.q = static_cast<const In *>(a.q) + qk_off;
-        io.v = static_cast<const In *>(a.v) + v_off;
-        io.kn = static_cast<const In *>(a.kn) + qk_off;
-        io.qn = static_cast<const In *>(a.qn) + qk_off;
-        io.vn = static_cast<const In *>(a.vn) + v_off;
-        io.g = a.g + g_off;
-        io.beta = a.beta + g_off;
-        io.gn = a.gn + g_off;
-        io.betan = a.betan + g_off;
-        io.o = static_cast<Out *>(a.o) + v_off;
-        io.on = static_cast<Out *>(a.on) + v_off;
-        io.nvalid = (int)(len - j0 < a.L ? len - j0 : a.L);
-        eng.step(io, S, a.scale);
+        x.qk_stride = (long)a.h_qk * DK;
+        x.v_stride = (long)a.h_v * a.dv;
+        x.gate_stride = a.h_v;
+        x.k = static_cast<const In *>(a.k) + qk_off;
+        x.q = static_cast<const In *>(a.q) + qk_off;
+        x.v = static_cast<const In *>(a.v) + v_off;
+        x.kn = static_cast<const In *>(a.kn) + qk_off;
+        x.qn = static_cast<const In *>(a.qn) + qk_off;
+        x.vn = static_cast<const In *>(a.vn) + v_off;
+        x.g = a.g + g_off;
+        x.beta = a.beta + g_off;
+        x.gn = a.gn + g_off;
+        x.betan = a.betan + g_off;
+        x.o = static_cast<Out *>(a.o) + v_off;
+        x.on = static_cast<Out *>(a.on) + v_off;
+        x.nvalid = (int)(len - j0 < a.L ? len - j0 : a.L);
+        return x;
+    };
+    typename Eng::Fetched f;
+    if (len > 0) eng.fetch(make_io(0), f);
+    for (long j0 = 0; j0 < len; j0 += a.L) {
+        const bool more = j0 + a.L < len;
+        eng.step(make_io(j0), more, make_io(more ? j0 + a.L : j0), f, S, a.scale);
     }
     if (a.ht) eng.store_state(S, a.ht + state_off, a.dv);
 }
@@ -86,9 +102,11 @@ static hipError_t launch_one(const FwdArgs &a, hipStream_t s)
     if (attr_err != hipSuccess) return attr_err;
     const int groups = (a.n_chains + 7) / 8;
     const int grid = groups * 8 * a.n_vt;
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), Ly::BYTES, s, a);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(kFwdThreads), Ly::BYTES, s, a);
     return hipGetLastError();
 }
+
+int fwd_tile_v() { return kFwdBV; }
 
 bool fwd_supported(Types ty, int dk, int lp)
 {
@@ -98,7 +116,7 @@ bool fwd_supported(Types ty, int dk, int lp)
 
 hipError_t launch_fwd_fused(Types ty, int dk, int lp, const FwdArgs &a, hipStream_t s)
 {
-    if (a.dv % kFwdBV) return hipErrorInvalidValue;
+    if (a.dv % kFwdBV || a.n_vt * kFwdBV != a.dv) return hipErrorInvalidValue;
 #define BDGDN_CASE(IN, OP, OUT, DK, LP) \
     if (dk == DK && lp == LP) return launch_one<IN, OP, OUT, DK, LP>(a, s);
 #define BDGDN_LPS(IN, OP, OUT, DK) \

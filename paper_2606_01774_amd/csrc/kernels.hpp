@@ -22,6 +22,31 @@ struct FwdArgs {
     int order[kMaxOrder];
 };
 
+// Block-local UT transform (one workgroup per (block, v-head)).
+struct IntraArgs {
+    const void *q, *k, *qn, *kn;
+    const float *g, *beta, *gn, *betan;
+    unsigned char *ws;   // records, ((block * h_v) + h) * record bytes
+    int T, L, nblk;      // tokens per sequence (packed: total), block, blocks per sequence
+    long total_blocks;   // sequences * nblk
+    int h_qk, h_v;
+};
+
+// Sequential scan (one workgroup per (chain, d_v tile)).
+struct ScanArgs {
+    const void *q, *k, *v, *qn, *kn, *vn;
+    const int32_t *cu;
+    const float *h0;
+    float *ht;
+    void *o, *on;
+    const unsigned char *ws;
+    int T, L, nblk, h_qk, h_v, dv;
+    int n_chains, n_vt;
+    float scale;
+    int n_order;
+    int order[kMaxOrder];
+};
+
 struct ServeArgs {
     const void *q, *k, *v;
     const float *g, *beta;
@@ -44,6 +69,13 @@ enum class Types {
 hipError_t launch_fwd_fused(Types ty, int dk, int lp, const FwdArgs &a, hipStream_t s);
 hipError_t launch_denoise(Types ty, int dk, int lp, const ServeArgs &a, hipStream_t s);
 hipError_t launch_commit(Types ty, int dk, int lp, bool with_o, const ServeArgs &a, hipStream_t s);
+// Two-kernel training forward (UT transform records, then the scan).
+hipError_t launch_fwd_scan(Types ty, int dk, int lp, const IntraArgs &ia, const ScanArgs &sa, hipStream_t s);
+size_t scan_record_bytes(Types ty, int lp);
+int scan_tile_v();
+// d_v columns handled by one workgroup of the training / serving kernels.
+int fwd_tile_v();
+int serve_tile_v();
 // Whether the (types, d_k, lp) combination is instantiated and fits in LDS.
 bool fwd_supported(Types ty, int dk, int lp);
 

@@ -9,13 +9,21 @@
 
 namespace bdgdn {
 
-constexpr int kServeBV = 32;
+#ifndef BDGDN_SERVE_BV
+#define BDGDN_SERVE_BV 64
+#endif
+#ifndef BDGDN_SERVE_NW
+#define BDGDN_SERVE_NW 8
+#endif
+constexpr int kServeBV = BDGDN_SERVE_BV;  // d_v columns per workgroup
+constexpr int kServeNW = BDGDN_SERVE_NW;  // waves per workgroup
+constexpr int kServeThreads = 64 * kServeNW;
 
 template <typename In, typename Op, typename Out, int DK, int BV, int LP, bool CL, bool CO, bool NZ>
 __device__ __forceinline__ void serve_body(const ServeArgs &a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    typedef Engine<In, Op, Out, DK, BV, LP, CL, CO, NZ> Eng;
+    typedef Engine<In, Op, Out, DK, BV, LP, CL, CO, NZ, kServeNW> Eng;
     const int id = blockIdx.x;
     const int unit = id / a.n_vt, vt = id % a.n_vt;
     const int r = unit / a.h_v, h = unit % a.h_v;
@@ -46,18 +54,20 @@ __device__ __forceinline__ void serve_body(const ServeArgs &a)
     io.gn = a.g + g_off; io.betan = a.beta + g_off;
     io.o = o; io.on = o;
     io.nvalid = a.L;
-    eng.step(io, S, a.scale);
+    typename Eng::Fetched f;
+    eng.fetch(io, f);
+    eng.step(io, false, io, f, S, a.scale);
     if (CL) eng.store_state(S, state, a.dv);
 }
 
 template <typename In, typename Op, typename Out, int DK, int BV, int LP>
-__global__ void __launch_bounds__(kThreads) bdgdn_denoise_kernel(ServeArgs a)
+__global__ void __launch_bounds__(kServeThreads) bdgdn_denoise_kernel(ServeArgs a)
 {
     serve_body<In, Op, Out, DK, BV, LP, false, false, true>(a);
 }
 
 template <typename In, typename Op, typename Out, int DK, int BV, int LP, bool CO>
-__global__ void __launch_bounds__(kThreads) bdgdn_commit_kernel(ServeArgs a)
+__global__ void __launch_bounds__(kServeThreads) bdgdn_commit_kernel(ServeArgs a)
 {
     serve_body<In, Op, Out, DK, BV, LP, true, CO, false>(a);
 }
@@ -81,7 +91,7 @@ static hipError_t launch_dn(const ServeArgs &a, hipStream_t s)
     static std::once_flag once;
     static hipError_t err = hipSuccess;
     if (set_lds(kern, Ly::BYTES, once, err) != hipSuccess) return err;
-    hipLaunchKernelGGL(kern, dim3(a.R * a.h_v * a.n_vt), dim3(kThreads), Ly::BYTES, s, a);
+    hipLaunchKernelGGL(kern, dim3(a.R * a.h_v * a.n_vt), dim3(kServeThreads), Ly::BYTES, s, a);
     return hipGetLastError();
 }
 
@@ -94,7 +104,7 @@ static hipError_t launch_cm1(const ServeArgs &a, hipStream_t s)
     static std::once_flag once;
     static hipError_t err = hipSuccess;
     if (set_lds(kern, Ly::BYTES, once, err) != hipSuccess) return err;
-    hipLaunchKernelGGL(kern, dim3(a.R * a.h_v * a.n_vt), dim3(kThreads), Ly::BYTES, s, a);
+    hipLaunchKernelGGL(kern, dim3(a.R * a.h_v * a.n_vt), dim3(kServeThreads), Ly::BYTES, s, a);
     return hipGetLastError();
 }
 
@@ -120,9 +130,11 @@ static hipError_t launch_cm(bool with_o, const ServeArgs &a, hipStream_t s)
 #define BDGDN_LPS(CALL, IN, OP, OUT, DK) \
     BDGDN_ONE(CALL, IN, OP, OUT, DK, 16) BDGDN_ONE(CALL, IN, OP, OUT, DK, 32) BDGDN_ONE(CALL, IN, OP, OUT, DK, 64)
 
+int serve_tile_v() { return kServeBV; }
+
 hipError_t launch_denoise(Types ty, int dk, int lp, const ServeArgs &a, hipStream_t s)
 {
-    if (a.dv % kServeBV) return hipErrorInvalidValue;
+    if (a.dv % kServeBV || a.n_vt * kServeBV != a.dv) return hipErrorInvalidValue;
 #define BDGDN_ONE(CALL, IN, OP, OUT, DK, LP) \
     if (dk == DK && lp == LP) return launch_dn<IN, OP, OUT, DK, LP>(a, s);
     BDGDN_SERVE_DISPATCH(0)
@@ -132,7 +144,7 @@ hipError_t launch_denoise(Types ty, int dk, int lp, const ServeArgs &a, hipStrea
 
 hipError_t launch_commit(Types ty, int dk, int lp, bool with_o, const ServeArgs &a, hipStream_t s)
 {
-    if (a.dv % kServeBV) return hipErrorInvalidValue;
+    if (a.dv % kServeBV || a.n_vt * kServeBV != a.dv) return hipErrorInvalidValue;
 #define BDGDN_ONE(CALL, IN, OP, OUT, DK, LP) \
     if (dk == DK && lp == LP) return launch_cm<IN, OP, OUT, DK, LP>(with_o, a, s);
     BDGDN_SERVE_DISPATCH(0)

@@ -89,7 +89,13 @@ def test_fwd_packing_checks():
 
 
 def test_workspace_query():
-    assert bd.bdgdn_fwd_train_workspace(_desc()) == 0
+    # one record per (block, v-head): 64 tokens / 32 = 2 blocks x 4 v-heads
+    ws = bd.bdgdn_fwd_train_workspace(_desc())
+    assert ws > 0 and ws % (2 * 4) == 0 and (ws // 8) % 256 == 0
+    assert bd.bdgdn_fwd_train_workspace(_desc(route=bd.BDGDN_ROUTE_ONEPASS)) == 0
+    assert bd.bdgdn_fwd_train_workspace(_desc(h_v=3)) == 0
+    # too small a workspace is refused before any launch
+    assert _fwd(_desc()) == bd.BDGDN_ERR_WORKSPACE
 
 
 def _serve(fn, **kw):

@@ -44,6 +44,10 @@ def test_tiny_f32_full_config():
     _check_full(W.make_train(w), w.block, "f32")
 
 
+ROUTES = [bd.BDGDN_ROUTE_FUSED, bd.BDGDN_ROUTE_ONEPASS]
+
+
+@pytest.mark.parametrize("route", ROUTES)
 @pytest.mark.parametrize("B,T,hqk,hv,d,L,dtype", [
     (2, 200, 2, 2, 128, 32, "bf16"),     # ragged tail (200 = 6*32 + 8)
     (1, 256, 2, 4, 128, 64, "bf16"),     # grouped value heads, L = 64
@@ -54,16 +58,31 @@ def test_tiny_f32_full_config():
     (2, 100, 1, 2, 128, 32, "f32"),
     (1, 96, 2, 2, 64, 16, "f32"),
 ])
-def test_small_shapes(B, T, hqk, hv, d, L, dtype):
+def test_small_shapes(B, T, hqk, hv, d, L, dtype, route):
     inp = W.make_custom_train(B, T, hqk, hv, d, d, dtype, seed=1000 + T + L)
     h0 = torch.randn(B, hv, d, d, generator=torch.Generator().manual_seed(T)) * 0.3
-    _check_full(inp, L, dtype, h0=h0)
+    _check_full(inp, L, dtype, h0=h0, route=route)
 
 
-def test_packed_documents_small():
+@pytest.mark.parametrize("route", ROUTES)
+def test_packed_documents_small(route):
     lengths = [64, 96, 32, 0, 64, 128, 17]   # an empty doc and a ragged last doc
     inp = W.make_custom_train(1, sum(lengths), 2, 2, 128, 128, "bf16", seed=77, lengths=lengths)
-    _check_full(inp, 32, "bf16")
+    _check_full(inp, 32, "bf16", route=route)
+
+
+@pytest.mark.parametrize("L", [16, 32, 64])
+def test_routes_agree(L):
+    """The two schedules compute the same function: the two-kernel route and the
+    single-kernel route agree to rounding (both against each other and the oracle)."""
+    inp = W.make_custom_train(2, 4 * L + 5, 2, 4, 128, 128, "bf16", seed=L)
+    d = to_dev(inp)
+    a = _run_gpu(d, L, 0.1, route=bd.BDGDN_ROUTE_FUSED)
+    b = _run_gpu(d, L, 0.1, route=bd.BDGDN_ROUTE_ONEPASS)
+    for x, y in zip(a, b):
+        e = rel_err(x, y.double().cpu().numpy())
+        print(f"route difference {e:.3e}")
+        assert e <= TOL["bf16"]
 
 
 def test_packed_equals_separate_bitwise():
