@@ -269,6 +269,12 @@ __device__ __forceinline__ void lds_barrier()
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Wait until all of this wave's global loads have returned (s_waitcnt vmcnt(0) on
+// gfx9-family encodings: vmcnt = 0, expcnt and lgkmcnt left at their maxima).  Used
+// once after loads issued before a loop, so the loop's own waits only ever count the
+// loop's loads.
+__device__ __forceinline__ void wait_global_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // 2^x with the hardware v_exp_f32 (arguments here are block-local gate differences,
 // within [-12, 0]).
 __device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }

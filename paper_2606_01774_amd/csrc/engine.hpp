@@ -181,6 +181,7 @@ struct Engine {
             }
             S[s] = acc;
         }
+        wait_global_loads();
     }
     __device__ __forceinline__ void store_state(const f32x4 (&S)[NSW], float *dst, int dv) const
     {
@@ -216,10 +217,13 @@ struct Engine {
     // (and K transposed), the V tiles, gates.  Rows at or past nvalid are zero:
     // identity positions (k = 0, g = 0, beta = 0).  The fetch of block b+1 is issued
     // right after block b is staged so its latency hides behind block b's work.
+    // Raw loaded data (rows past the block end are zeroed when staged, so nothing here
+    // waits for the loads to arrive).
     struct Fetched {
         u32x4 rb[Ly::NROWS][RPT];
         u32x4 vb[Ly::NSOLVE][VPT];
         float gv;
+        int last;
     };
 
     // Source of row set rs (a compile-time index after unrolling).
@@ -239,46 +243,39 @@ struct Engine {
     {
         constexpr int NR = Ly::NROWS;
         static_assert(NW >= 4, "gate slots are loaded by waves 0..3");
-        const u32x4 zero = {0u, 0u, 0u, 0u};
         const int last = io.nvalid - 1;
+        f.last = last;
 #pragma unroll
         for (int s = 0; s < RPT; ++s) {
             const int c = tid + s * kThreads;
             const int cr = c < RCH ? c : RCH - 1;
             const int t = cr / CPR, cc = cr % CPR;
-            const bool ok = c < RCH && t <= last;
             const long off = (long)(t <= last ? t : last) * io.qk_stride + cc * EPC;
 #pragma unroll
-            for (int rs = 0; rs < NR; ++rs) {
-                const u32x4 x = *reinterpret_cast<const u32x4 *>(row_src(io, rs) + off);
-                f.rb[rs][s] = ok ? x : zero;
-            }
+            for (int rs = 0; rs < NR; ++rs) f.rb[rs][s] = *reinterpret_cast<const u32x4 *>(row_src(io, rs) + off);
         }
 #pragma unroll
         for (int s = 0; s < VPT; ++s) {
             const int c = tid + s * kThreads;
             const int cr = c < VCH ? c : VCH - 1;
             const int t = cr / VCPR, cc = cr % VCPR;
-            const bool ok = c < VCH && t <= last;
             const long off = (long)(t <= last ? t : last) * io.v_stride + cc * EPC;
 #pragma unroll
-            for (int m = 0; m < Ly::NSOLVE; ++m) {
-                const u32x4 x = *reinterpret_cast<const u32x4 *>(((CL && m == 0) ? io.v : io.vn) + off);
-                f.vb[m][s] = ok ? x : zero;
-            }
+            for (int m = 0; m < Ly::NSOLVE; ++m)
+                f.vb[m][s] = *reinterpret_cast<const u32x4 *>(((CL && m == 0) ? io.v : io.vn) + off);
         }
         f.gv = 0.f;
         const bool want = (wave < 2 && CL) || (wave >= 2 && wave < 4 && NZ);
         if (want) {
             const float *gp = wave == GS_G ? io.g : wave == GS_B ? io.beta : wave == GS_GN ? io.gn : io.betan;
-            const float x = gp[(long)(lane <= last ? lane : last) * io.gate_stride];
-            f.gv = lane <= last ? x : 0.f;
+            f.gv = gp[(long)(lane <= last ? lane : last) * io.gate_stride];
         }
     }
 
     __device__ __forceinline__ void stage(const Fetched &f) const
     {
         constexpr int NR = Ly::NROWS;
+        const u32x4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int rs = 0; rs < NR; ++rs)
 #pragma unroll
@@ -286,7 +283,8 @@ struct Engine {
                 const int c = tid + s * kThreads;
                 if (c < RCH) {
                     const int t = c / CPR, cc = c % CPR;
-                    *reinterpret_cast<u32x4 *>(rows(rs) + t * Ly::RS + cc * EPC) = to_operand<In, E>(f.rb[rs][s]);
+                    *reinterpret_cast<u32x4 *>(rows(rs) + t * Ly::RS + cc * EPC) =
+                        t <= f.last ? to_operand<In, E>(f.rb[rs][s]) : zero;
                 }
             }
 #pragma unroll
@@ -296,10 +294,11 @@ struct Engine {
                 const int c = tid + s * kThreads;
                 if (c < VCH) {
                     const int t = c / VCPR, cc = c % VCPR;
-                    *reinterpret_cast<u32x4 *>(vs(m) + t * Ly::VS + cc * EPC) = to_operand<In, E>(f.vb[m][s]);
+                    *reinterpret_cast<u32x4 *>(vs(m) + t * Ly::VS + cc * EPC) =
+                        t <= f.last ? to_operand<In, E>(f.vb[m][s]) : zero;
                 }
             }
-        if (wave < 4 && lane < LP) gates(wave)[lane] = f.gv;
+        if (wave < 4 && lane < LP) gates(wave)[lane] = lane <= f.last ? f.gv : 0.f;
     }
 
     // In-place inclusive scan of a gate slot (times log2 e), by one wave.

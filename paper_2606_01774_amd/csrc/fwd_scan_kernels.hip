@@ -18,12 +18,16 @@ namespace bdgdn {
 #ifndef BDGDN_SCAN_NW
 #define BDGDN_SCAN_NW 8
 #endif
+#ifndef BDGDN_SCAN_F16X
+#define BDGDN_SCAN_F16X 0
+#endif
 #ifndef BDGDN_INTRA_NW
 #define BDGDN_INTRA_NW 4
 #endif
 constexpr int kScanBV = BDGDN_SCAN_BV;
 constexpr int kScanNW = BDGDN_SCAN_NW;
 constexpr int kIntraNW = BDGDN_INTRA_NW;
+constexpr bool kScanF16X = BDGDN_SCAN_F16X != 0;
 
 template <typename In, int DK, int LP>
 __global__ void __launch_bounds__(64 * kIntraNW) bdgdn_k1_intra_kernel(IntraArgs a)
@@ -51,7 +55,7 @@ template <typename In, typename Out, int DK, int BV, int LP>
 __global__ void __launch_bounds__(64 * kScanNW) bdgdn_k2_scan_kernel(ScanArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    typedef Scan<In, Out, DK, BV, LP, kScanNW> K2;
+    typedef Scan<In, Out, DK, BV, LP, kScanNW, kScanF16X> K2;
     // ids i, i+8, i+16, ... of a group carry the d_v tiles of one chain, so they land
     // on one XCD and share its L2 for the q/k rows and the records.
     const int id = blockIdx.x;
@@ -124,7 +128,7 @@ template <typename In, typename Out, int DK, int LP>
 static hipError_t launch_pair(const IntraArgs &ia, const ScanArgs &sa, hipStream_t s)
 {
     typedef Intra<In, DK, LP, kIntraNW> K1;
-    typedef Scan<In, Out, DK, kScanBV, LP, kScanNW> K2;
+    typedef Scan<In, Out, DK, kScanBV, LP, kScanNW, kScanF16X> K2;
     static_assert(K1::BYTES <= 160 * 1024 && K2::BYTES <= 160 * 1024, "LDS budget");
     auto k1 = bdgdn_k1_intra_kernel<In, DK, LP>;
     auto k2 = bdgdn_k2_scan_kernel<In, Out, DK, kScanBV, LP>;

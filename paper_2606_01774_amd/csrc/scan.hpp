@@ -15,6 +15,8 @@
 // blocks in order; the next block's inputs are fetched while the current one computes.
 #pragma once
 
+#include <type_traits>
+
 #include "intra.hpp"
 
 namespace bdgdn {
@@ -29,11 +31,14 @@ template <typename In, typename Out> struct ScanIO {
     int nvalid;
 };
 
-template <typename In, typename Out, int DK, int BV, int LP, int NW>
+// F16X: with bf16 inputs, stage the q/k rows as fp16 and carry the state operand and
+// the decayed Delta as single fp16 operands instead of bf16 hi + lo pairs.
+template <typename In, typename Out, int DK, int BV, int LP, int NW, bool F16X = false>
 struct Scan {
-    typedef typename Prec<In>::Row Row;
+    static constexpr bool USE_F16 = F16X && __is_same(In, __bf16);
+    typedef typename std::conditional<USE_F16, _Float16, typename Prec<In>::Row>::type Row;
     typedef typename Prec<In>::Mid Mid;
-    static constexpr bool SPLIT = Prec<In>::kSplit;
+    static constexpr bool SPLIT = USE_F16 ? false : Prec<In>::kSplit;
     typedef Rec<Mid, LP> Rc;
     typedef ScanIO<In, Out> IO;
     static constexpr int kThreads = 64 * NW;
@@ -53,6 +58,7 @@ struct Scan {
     static constexpr int EPC = 16 / SR;
     // LDS layout
     static constexpr int ROWS_B = al16(LP * RS * SR);
+    static_assert(sizeof(In) == SR, "inputs are staged chunk for chunk");
     static constexpr int DT_B = al16(BV * TS * SM);
     static constexpr int NPOST = SPLIT ? 4 : 3;   // Delta, decayed Delta (hi, lo), Delta~
     static constexpr int OFF_K = 0;
@@ -75,6 +81,8 @@ struct Scan {
     static constexpr int FCH = Rc::FACT_BYTES / 16;
     static_assert(FCH <= kThreads, "factor chunks");
     static_assert(RCH % kThreads == 0 || RPT == 1, "row chunks");
+    // a tile index w + s*NW is in range for every wave when the count divides evenly
+    static constexpr bool S_EVEN = NS % NW == 0;
 
     unsigned char *smem;
     int tid, lane, wave;
@@ -86,7 +94,7 @@ struct Scan {
         wave = wave_id();
     }
     __device__ __forceinline__ Row *rows(int i) const { return reinterpret_cast<Row *>(smem + i * ROWS_B); }
-    __device__ __forceinline__ Row *vs(int m) const { return reinterpret_cast<Row *>(smem + OFF_V + m * V_B); }
+    __device__ __forceinline__ In *vs(int m) const { return reinterpret_cast<In *>(smem + OFF_V + m * V_B); }
     __device__ __forceinline__ Mid *tm(int m) const { return reinterpret_cast<Mid *>(smem + OFF_T + m * TM_B); }
     __device__ __forceinline__ float *fac(int m) const { return reinterpret_cast<float *>(smem + OFF_F) + m * 64; }
     __device__ __forceinline__ Row *st(int h) const { return reinterpret_cast<Row *>(smem + OFF_ST + h * ST_B); }
@@ -103,7 +111,7 @@ struct Scan {
         for (int s = 0; s < NSW; ++s) {
             const int t = wave + s * NW;
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-            if (t < NS && src) {
+            if ((S_EVEN || t < NS) && src) {
                 const int bk = t / NVB, bc = t % NVB;
                 const float *p = src + (long)(16 * bk + 4 * (lane >> 4)) * dv + 16 * bc + (lane & 15);
                 acc[0] = p[0];
@@ -113,13 +121,14 @@ struct Scan {
             }
             S[s] = acc;
         }
+        wait_global_loads();
     }
     __device__ __forceinline__ void store_state(const f32x4 (&S)[NSW], float *dst, int dv) const
     {
 #pragma unroll
         for (int s = 0; s < NSW; ++s) {
             const int t = wave + s * NW;
-            if (t < NS) {
+            if (S_EVEN || t < NS) {
                 const int bk = t / NVB, bc = t % NVB;
                 float *p = dst + (long)(16 * bk + 4 * (lane >> 4)) * dv + 16 * bc + (lane & 15);
                 p[0] = S[s][0];
@@ -135,7 +144,7 @@ struct Scan {
 #pragma unroll
         for (int s = 0; s < NSW; ++s) {
             const int t = wave + s * NW;
-            if (t < NS) {
+            if (S_EVEN || t < NS) {
                 const int bk = t / NVB, bc = t % NVB;
                 const int off = (16 * bc + (lane & 15)) * RS + 16 * bk + 4 * (lane >> 4);
                 if constexpr (SPLIT) {
@@ -155,11 +164,14 @@ struct Scan {
     }
 
     // ------------------------------------------------------------------ loads
+    // Raw loaded data; rows past the block end are zeroed when staged, so nothing
+    // here waits for the loads to arrive.
     struct Fetched {
         u32x4 rb[4][RPT];
         u32x4 vb[2][VPT];
         u32x4 mb[MPT];
         u32x4 fb;
+        int last;
     };
 
     __device__ __forceinline__ const In *row_src(const IO &io, int i) const
@@ -167,35 +179,29 @@ struct Scan {
         return i == 0 ? io.k : i == 1 ? io.q : i == 2 ? io.kn : io.qn;
     }
 
-    // Rows at or past nvalid are read from the last valid row and replaced by zero.
+    // Rows at or past nvalid are read from the last valid row (in bounds); stage()
+    // replaces them by zero.
     __device__ __forceinline__ void fetch(const IO &io, Fetched &f) const
     {
-        const u32x4 zero = {0u, 0u, 0u, 0u};
         const int last = io.nvalid - 1;
+        f.last = last;
 #pragma unroll
         for (int s = 0; s < RPT; ++s) {
             const int c = tid + s * kThreads;
             const int cr = c < RCH ? c : RCH - 1;
             const int t = cr / CPR, cc = cr % CPR;
-            const bool ok = c < RCH && t <= last;
             const long off = (long)(t <= last ? t : last) * io.qk_stride + cc * EPC;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const u32x4 x = *reinterpret_cast<const u32x4 *>(row_src(io, i) + off);
-                f.rb[i][s] = ok ? x : zero;
-            }
+            for (int i = 0; i < 4; ++i) f.rb[i][s] = *reinterpret_cast<const u32x4 *>(row_src(io, i) + off);
         }
 #pragma unroll
         for (int s = 0; s < VPT; ++s) {
             const int c = tid + s * kThreads;
             const int cr = c < VCH ? c : VCH - 1;
             const int t = cr / VCPR, cc = cr % VCPR;
-            const bool ok = c < VCH && t <= last;
             const long off = (long)(t <= last ? t : last) * io.v_stride + cc * EPC;
-            const u32x4 x0 = *reinterpret_cast<const u32x4 *>(io.v + off);
-            const u32x4 x1 = *reinterpret_cast<const u32x4 *>(io.vn + off);
-            f.vb[0][s] = ok ? x0 : zero;
-            f.vb[1][s] = ok ? x1 : zero;
+            f.vb[0][s] = *reinterpret_cast<const u32x4 *>(io.v + off);
+            f.vb[1][s] = *reinterpret_cast<const u32x4 *>(io.vn + off);
         }
         const u32x4 *rec = reinterpret_cast<const u32x4 *>(io.rec);
 #pragma unroll
@@ -208,13 +214,16 @@ struct Scan {
 
     __device__ __forceinline__ void stage(const Fetched &f) const
     {
+        const u32x4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int s = 0; s < RPT; ++s) {
             const int c = tid + s * kThreads;
             if (c < RCH) {
                 const int t = c / CPR, cc = c % CPR;
+                const bool ok = t <= f.last;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4 *>(rows(i) + t * RS + cc * EPC) = f.rb[i][s];
+                for (int i = 0; i < 4; ++i)
+                    *reinterpret_cast<u32x4 *>(rows(i) + t * RS + cc * EPC) = ok ? to_operand<In, Row>(f.rb[i][s]) : zero;
             }
         }
 #pragma unroll
@@ -222,8 +231,9 @@ struct Scan {
             const int c = tid + s * kThreads;
             if (c < VCH) {
                 const int t = c / VCPR, cc = c % VCPR;
-                *reinterpret_cast<u32x4 *>(vs(0) + t * VS + cc * EPC) = f.vb[0][s];
-                *reinterpret_cast<u32x4 *>(vs(1) + t * VS + cc * EPC) = f.vb[1][s];
+                const bool ok = t <= f.last;
+                *reinterpret_cast<u32x4 *>(vs(0) + t * VS + cc * EPC) = ok ? f.vb[0][s] : zero;
+                *reinterpret_cast<u32x4 *>(vs(1) + t * VS + cc * EPC) = ok ? f.vb[1][s] : zero;
             }
         }
 #pragma unroll
@@ -277,7 +287,7 @@ struct Scan {
                 const int t = noisy ? idx - NX : idx, bi = t / NVB, bc = t % NVB;
                 const f32x4 a = x_tile(rows(noisy ? 2 : 0) + 16 * bi * RS, bc);
                 const float *E = noisy ? eGn : eG;
-                const Row *V = vs(noisy ? 1 : 0);
+                const In *V = vs(noisy ? 1 : 0);
                 const int r = 16 * bi + r0, vc = 16 * bc + cl;
                 float d[4];
 #pragma unroll
@@ -360,7 +370,7 @@ struct Scan {
 #pragma unroll
         for (int s = 0; s < NSW; ++s) {
             const int t = wave + s * NW;
-            if (t < NS) {
+            if (S_EVEN || t < NS) {
                 const int bk = t / NVB, bc = t % NVB;
                 const f32x4 acc = S[s] * decay;
                 if constexpr (SPLIT)
