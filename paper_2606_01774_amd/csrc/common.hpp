@@ -246,6 +246,66 @@ __device__ __forceinline__ f32x4 tile_mma_at2(f32x4 acc, const E *R, int ldr, co
     return acc;
 }
 
+// ------------------------------------------------------------------ quad operands
+// Lane (g = lane >> 4, r = lane & 15) of a 16x16 MFMA tile can hold, for operand row r
+// (a row of A, a column of B), the four values at k = 4g .. 4g+3 of a 16-wide k-block:
+// a "quad".  An accumulator tile is held the same way (lane (g, n) has C[4g + i][n]), so
+// an accumulator feeds the next product straight from registers: as a B operand whose
+// k runs over its rows, or as the A operand of its transpose.  A product over
+// K = 16 NKB takes NKB quads per operand and lane; since any fixed assignment of the
+// k values to MFMA operand slots yields the same sum, two k-blocks fill one 16x16x32
+// step (16-bit types) and a k-block is four 16x16x4 steps (fp32).
+template <typename E> struct QuadOf;
+template <> struct QuadOf<_Float16> { typedef f16x4 type; };
+template <> struct QuadOf<float> { typedef f32x4 type; };
+template <typename E> using Quad = typename QuadOf<E>::type;
+
+template <typename E> __device__ __forceinline__ Quad<E> ld_quad(const E *p)
+{
+    return *reinterpret_cast<const Quad<E> *>(p);
+}
+template <typename E> __device__ __forceinline__ void st_quad(E *p, Quad<E> q)
+{
+    *reinterpret_cast<Quad<E> *>(p) = q;
+}
+template <typename E> __device__ __forceinline__ Quad<E> quad_of(f32x4 a);
+template <> __device__ __forceinline__ f16x4 quad_of<_Float16>(f32x4 a)
+{
+    return f16x4{(_Float16)a[0], (_Float16)a[1], (_Float16)a[2], (_Float16)a[3]};
+}
+template <> __device__ __forceinline__ f32x4 quad_of<float>(f32x4 a) { return a; }
+
+// Quads of row (lane & 15) of the row-major LDS matrix M (row stride ld), k-blocks
+// 0 .. NKB-1 starting at M's first column.
+template <typename E, int NKB>
+__device__ __forceinline__ void ld_quads(Quad<E> (&q)[NKB], const E *M, int ld, int lane)
+{
+    const E *p = M + (lane & 15) * ld + 4 * (lane >> 4);
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) q[kb] = ld_quad(p + 16 * kb);
+}
+
+// acc += sum over k-blocks kb of A_kb B_kb.
+template <typename E, int NKB>
+__device__ __forceinline__ f32x4 mma_q(f32x4 acc, const Quad<E> (&a)[NKB], const Quad<E> (&b)[NKB])
+{
+    if constexpr (sizeof(E) == 2) {
+#pragma unroll
+        for (int u = 0; u + 1 < NKB; u += 2) {
+            const f16x8 a8 = __builtin_shufflevector(a[u], a[u + 1], 0, 1, 2, 3, 4, 5, 6, 7);
+            const f16x8 b8 = __builtin_shufflevector(b[u], b[u + 1], 0, 1, 2, 3, 4, 5, 6, 7);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a8, b8, acc, 0, 0, 0);
+        }
+        if constexpr (NKB % 2) acc = __builtin_amdgcn_mfma_f32_16x16x16f16(a[NKB - 1], b[NKB - 1], acc, 0, 0, 0);
+    } else {
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[kb][i], b[kb][i], acc, 0, 0, 0);
+    }
+    return acc;
+}
+
 // C(16x16) += A(16 x K) * B(K x 16), fp32, both row-major in LDS (used by the solve).
 __device__ __forceinline__ f32x4 tile_mma_rr(f32x4 acc, const float *A, int lda, const float *B,
                                              int ldb, int K, int lane)

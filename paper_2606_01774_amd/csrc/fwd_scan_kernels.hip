@@ -12,22 +12,11 @@
 
 namespace bdgdn {
 
-#ifndef BDGDN_SCAN_BV
-#define BDGDN_SCAN_BV 32
-#endif
-#ifndef BDGDN_SCAN_NW
-#define BDGDN_SCAN_NW 8
-#endif
-#ifndef BDGDN_SCAN_F16X
-#define BDGDN_SCAN_F16X 0
-#endif
 #ifndef BDGDN_INTRA_NW
 #define BDGDN_INTRA_NW 4
 #endif
-constexpr int kScanBV = BDGDN_SCAN_BV;
-constexpr int kScanNW = BDGDN_SCAN_NW;
+constexpr int kScanBV = 32;
 constexpr int kIntraNW = BDGDN_INTRA_NW;
-constexpr bool kScanF16X = BDGDN_SCAN_F16X != 0;
 
 template <typename In, int DK, int LP>
 __global__ void __launch_bounds__(64 * kIntraNW) bdgdn_k1_intra_kernel(IntraArgs a)
@@ -52,10 +41,11 @@ __global__ void __launch_bounds__(64 * kIntraNW) bdgdn_k1_intra_kernel(IntraArgs
 }
 
 template <typename In, typename Out, int DK, int BV, int LP>
-__global__ void __launch_bounds__(64 * kScanNW) bdgdn_k2_scan_kernel(ScanArgs a)
+__global__ void __launch_bounds__(512) bdgdn_k2_scan_kernel(ScanArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    typedef Scan<In, Out, DK, BV, LP, kScanNW, kScanF16X> K2;
+    typedef Scan<In, Out, DK, BV, LP> K2;
+    static_assert(K2::kThreads == 512, "launch bounds");
     // ids i, i+8, i+16, ... of a group carry the d_v tiles of one chain, so they land
     // on one XCD and share its L2 for the q/k rows and the records.
     const int id = blockIdx.x;
@@ -78,40 +68,32 @@ __global__ void __launch_bounds__(64 * kScanNW) bdgdn_k2_scan_kernel(ScanArgs a)
     }
     const int hq = h / (a.h_v / a.h_qk);
     const int v0 = vt * BV;
-    K2 k2(smem);
-    f32x4 S[K2::NSW];
+    typename K2::Chain c;
+    const long qk_off = (base * a.h_qk + hq) * DK;
+    const long v_off = (base * a.h_v + h) * a.dv + v0;
+    c.p0.k = static_cast<const In *>(a.k) + qk_off;
+    c.p0.q = static_cast<const In *>(a.q) + qk_off;
+    c.p0.kn = static_cast<const In *>(a.kn) + qk_off;
+    c.p0.qn = static_cast<const In *>(a.qn) + qk_off;
+    c.p0.v = static_cast<const In *>(a.v) + v_off;
+    c.p0.vn = static_cast<const In *>(a.vn) + v_off;
+    c.p0.rec = a.ws + (gb0 * a.h_v + h) * (long)K2::Rc::BYTES;
+    c.p0.o = static_cast<Out *>(a.o) + v_off;
+    c.p0.on = static_cast<Out *>(a.on) + v_off;
+    c.qks = a.h_qk * DK;
+    c.vst = a.h_v * a.dv;
+    c.qk_blk = (long)a.L * c.qks;
+    c.v_blk = (long)a.L * c.vst;
+    c.rec_blk = (long)a.h_v * K2::Rc::BYTES;
+    c.len = len;
+    c.L = a.L;
     const long state_off = ((long)seq * a.h_v + h) * DK * a.dv + v0;
-    k2.load_state(S, a.h0 ? a.h0 + state_off : nullptr, a.dv);
-    k2.write_st(S);
-    __syncthreads();
-    auto make_io = [&](long j) {
-        typename K2::IO x;
-        const long j0 = j * a.L;
-        const long row0 = base + j0;
-        const long qk_off = (row0 * a.h_qk + hq) * DK;
-        const long v_off = (row0 * a.h_v + h) * a.dv + v0;
-        x.qk_stride = (long)a.h_qk * DK;
-        x.v_stride = (long)a.h_v * a.dv;
-        x.k = static_cast<const In *>(a.k) + qk_off;
-        x.q = static_cast<const In *>(a.q) + qk_off;
-        x.kn = static_cast<const In *>(a.kn) + qk_off;
-        x.qn = static_cast<const In *>(a.qn) + qk_off;
-        x.v = static_cast<const In *>(a.v) + v_off;
-        x.vn = static_cast<const In *>(a.vn) + v_off;
-        x.rec = a.ws + ((gb0 + j) * a.h_v + h) * (long)K2::Rc::BYTES;
-        x.o = static_cast<Out *>(a.o) + v_off;
-        x.on = static_cast<Out *>(a.on) + v_off;
-        x.nvalid = (int)(len - j0 < a.L ? len - j0 : a.L);
-        return x;
-    };
-    const long nb = (len + a.L - 1) / a.L;
-    typename K2::Fetched f;
-    if (nb > 0) k2.fetch(make_io(0), f);
-    for (long j = 0; j < nb; ++j) {
-        const bool more = j + 1 < nb;
-        k2.step(make_io(j), more, make_io(more ? j + 1 : j), f, S, a.scale);
-    }
-    if (a.ht) k2.store_state(S, a.ht + state_off, a.dv);
+    c.h0 = a.h0 ? a.h0 + state_off : nullptr;
+    c.ht = a.ht ? a.ht + state_off : nullptr;
+    c.dv = a.dv;
+    c.scale = a.scale;
+    K2 k2(smem);
+    k2.run(c);
 }
 
 template <typename K>
@@ -128,7 +110,7 @@ template <typename In, typename Out, int DK, int LP>
 static hipError_t launch_pair(const IntraArgs &ia, const ScanArgs &sa, hipStream_t s)
 {
     typedef Intra<In, DK, LP, kIntraNW> K1;
-    typedef Scan<In, Out, DK, kScanBV, LP, kScanNW, kScanF16X> K2;
+    typedef Scan<In, Out, DK, kScanBV, LP> K2;
     static_assert(K1::BYTES <= 160 * 1024 && K2::BYTES <= 160 * 1024, "LDS budget");
     auto k1 = bdgdn_k1_intra_kernel<In, DK, LP>;
     auto k2 = bdgdn_k2_scan_kernel<In, Out, DK, kScanBV, LP>;
@@ -140,7 +122,7 @@ static hipError_t launch_pair(const IntraArgs &ia, const ScanArgs &sa, hipStream
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int grid = (sa.n_chains + 7) / 8 * 8 * sa.n_vt;
-    hipLaunchKernelGGL(k2, dim3(grid), dim3(64 * kScanNW), K2::BYTES, s, sa);
+    hipLaunchKernelGGL(k2, dim3(grid), dim3(K2::kThreads), K2::BYTES, s, sa);
     return hipGetLastError();
 }
 

@@ -3,86 +3,94 @@
 // the fused two-stream schedule of "Route II": each noisy block is evaluated from the
 // clean boundary state held on chip, never written out).
 //
-// Per block, from the clean state S0 (d_k x b_v tile of the d_k x d_v state) and the
-// block's record (T, T~, P, R and the decay factors; see intra.hpp):
+// Per block, from the clean state S0 (the d_k x 32 column tile of the d_k x d_v state
+// this workgroup owns) and the block's record (T, T~, P, R and the decay factors; see
+// intra.hpp):
 //   X1 = K S0, X2 = Q S0, X3 = K~ S0, X4 = Q~ S0
 //   D  = V  - diag(eG)  X1,      Delta  = T  D
 //   D~ = V~ - diag(eGn) X3,      Delta~ = T~ D~
 //   O  = s [ diag(eG) X2 + P Delta ]
 //   O~ = s [ gamma~_n X4 + R Delta~ ]
 //   S  = gamma_n S0 + K^T diag(dG) Delta
-// One workgroup owns one (sequence or document, v-head, d_v tile) chain and walks its
-// blocks in order; the next block's inputs are fetched while the current one computes.
+//
+// One workgroup of eight waves owns one (sequence or document, v-head, 32-column tile)
+// chain and walks its blocks in order.  The waves split by role, two per role, one per
+// 16-column half (bc) of the tile:
+//   C (waves 0, 1)  the recurrence: X1, D, Delta and the state update, with the state
+//                   kept in registers (fp32, plus its operand copy) and every
+//                   intermediate passed from accumulator to operand in registers;
+//                   publishes Delta and the new state's operand copy through LDS;
+//   N (waves 2, 3)  the noisy block: X3, X4, D~, Delta~, O~ from the published state;
+//   O (waves 4, 5)  the clean outputs, one block behind: X2 while C works on a
+//                   block, P Delta once C has published Delta;
+//   L (waves 6, 7)  the next block's loads: global loads one block ahead, converted
+//                   and staged into the other half of a double-buffered LDS set,
+//                   with K also staged transposed for the update.
+// One workgroup barrier per block.  When two staging sets do not fit in LDS (64-position
+// blocks with bf16 inputs, 32-position blocks with fp32 inputs) all eight waves stage
+// each block in a phase of its own, behind a second barrier.
 #pragma once
-
-#include <type_traits>
 
 #include "intra.hpp"
 
 namespace bdgdn {
 
-// Pointers of one block of one chain (row r of a tensor is base + r * stride).
-template <typename In, typename Out> struct ScanIO {
-    const In *k, *q, *kn, *qn;   // first row, q/k head
-    const In *v, *vn;            // first row, v head, column v0
-    const unsigned char *rec;    // this (block, v-head) record
-    Out *o, *on;                 // first row, v head, column v0
-    long qk_stride, v_stride;
-    int nvalid;
-};
+// Operand type of the scan's MFMA products by input type: fp16 for bf16 inputs (the
+// bf16 q / k rows convert exactly in fp16's normal range; the state operand, D and
+// Delta keep 11 significant bits), fp32 for fp32 inputs.
+template <typename In> struct ScanOp;
+template <> struct ScanOp<__bf16> { typedef _Float16 type; };
+template <> struct ScanOp<float> { typedef float type; };
 
-// F16X: with bf16 inputs, stage the q/k rows as fp16 and carry the state operand and
-// the decayed Delta as single fp16 operands instead of bf16 hi + lo pairs.
-template <typename In, typename Out, int DK, int BV, int LP, int NW, bool F16X = false>
+template <typename In, typename Out, int DK, int BV, int LP>
 struct Scan {
-    static constexpr bool USE_F16 = F16X && __is_same(In, __bf16);
-    typedef typename std::conditional<USE_F16, _Float16, typename Prec<In>::Row>::type Row;
-    typedef typename Prec<In>::Mid Mid;
-    static constexpr bool SPLIT = USE_F16 ? false : Prec<In>::kSplit;
-    typedef Rec<Mid, LP> Rc;
-    typedef ScanIO<In, Out> IO;
-    static constexpr int kThreads = 64 * NW;
-    static constexpr int NB = LP / 16, NVB = BV / 16;
-    static constexpr int NX = NB * NVB;          // tiles of an LP x BV product
-    static constexpr int NS = (DK / 16) * NVB;   // tiles of the d_k x BV state
-    static constexpr int NXW = (NX + NW - 1) / NW;
-    static constexpr int NSW = (NS + NW - 1) / NW;
-    static constexpr int N13 = 2 * NX, N13W = (N13 + NW - 1) / NW;   // X1 and X3 tiles
-    static constexpr int ND = 2 * NX, NDW = (ND + NW - 1) / NW;      // Delta and Delta~ tiles
-    static constexpr int SR = (int)sizeof(Row), SM = (int)sizeof(Mid);
-    static_assert(SR == SM, "row and intermediate operands share strides");
-    static constexpr int PE = Mma<Row>::kPad;
-    static constexpr int RS = DK + PE;   // [token][d_k] rows and ST [v][d_k]
-    static constexpr int TS = LP + PE;   // [*][token] buffers
-    static constexpr int VS = BV + PE;   // staged V [token][v]
-    static constexpr int EPC = 16 / SR;
-    // LDS layout
-    static constexpr int ROWS_B = al16(LP * RS * SR);
-    static_assert(sizeof(In) == SR, "inputs are staged chunk for chunk");
-    static constexpr int DT_B = al16(BV * TS * SM);
-    static constexpr int NPOST = SPLIT ? 4 : 3;   // Delta, decayed Delta (hi, lo), Delta~
-    static constexpr int OFF_K = 0;
-    static constexpr int OFF_Y = ROWS_B;          // q, kn, qn rows; later the post buffers
-    static constexpr int Y_B = al16(imax(3 * ROWS_B, NPOST * DT_B));
-    static constexpr int OFF_V = OFF_Y + Y_B;
-    static constexpr int V_B = al16(LP * VS * SR);
-    static constexpr int OFF_T = OFF_V + 2 * V_B;  // T, T~, P, R
-    static constexpr int TM_B = al16(LP * TS * SM);
-    static constexpr int OFF_F = OFF_T + 4 * TM_B; // eG, dG, eGn
-    static constexpr int OFF_ST = OFF_F + 3 * 64 * 4;
-    static constexpr int ST_B = al16(BV * RS * SR);
-    static constexpr int OFF_D = OFF_ST + (SPLIT ? 2 : 1) * ST_B;
-    static constexpr int BYTES = OFF_D + 2 * DT_B;
-    // fetch geometry (16-byte chunks)
-    static constexpr int CPR = DK / EPC, RCH = LP * CPR, RPT = (RCH + kThreads - 1) / kThreads;
-    static constexpr int VCPR = BV / EPC, VCH = LP * VCPR, VPT = (VCH + kThreads - 1) / kThreads;
-    static constexpr int MCPR = LP * SM / 16;   // chunks per record matrix row
-    static constexpr int MCH = 4 * LP * MCPR, MPT = (MCH + kThreads - 1) / kThreads;
+    typedef typename ScanOp<In>::type E;
+    static_assert(__is_same(E, typename Prec<In>::Mid), "records hold scan operands");
+    typedef Rec<E, LP> Rc;
+    typedef Quad<E> QE;
+    static constexpr int NW = 8, kThreads = 64 * NW;
+    static constexpr int NB = LP / 16, DKB = DK / 16;
+    static_assert(BV == 32, "two 16-column halves per workgroup");
+    static constexpr int SE = (int)sizeof(E);
+    static_assert(SE == (int)sizeof(In), "inputs are staged chunk for chunk");
+    static constexpr int EPC = 16 / SE;   // elements per 16-byte chunk
+    static constexpr int PE = EPC;        // row padding: 16 bytes
+    static constexpr int RS = DK + PE;    // [token][d_k] rows, ST [v][d_k]
+    static constexpr int TS = LP + PE;    // [*][token]: T, T~, P, R, K^T, Delta^T
+    static constexpr int VS = BV + PE;    // V [token][v]
+    // one staging set
+    static constexpr int ROWS_B = al16(LP * RS * SE);
+    // 16-bit operands read K^T straight from the K rows with LDS transpose loads; fp32
+    // operands keep a staged transposed copy
+    static constexpr bool TR = SE == 2;
+    static constexpr int KT_B = TR ? 0 : al16(DK * TS * SE);
+    static constexpr int V_B = al16(LP * VS * SE);
+    static constexpr int TM_B = al16(LP * TS * SE);
+    static constexpr int OFF_KT = 4 * ROWS_B;
+    static constexpr int OFF_V = OFF_KT + KT_B;
+    static constexpr int OFF_TM = OFF_V + 2 * V_B;
+    static constexpr int OFF_FAC = OFF_TM + 4 * TM_B;
+    static constexpr int SET_B = OFF_FAC + 3 * 64 * 4;
+    static constexpr int ST_B = al16(BV * RS * SE);
+    static constexpr int DT_B = al16(BV * TS * SE);
+    static constexpr int kLds = 160 * 1024;
+    static constexpr bool DBUF = 2 * SET_B + 2 * ST_B + 2 * DT_B <= kLds;
+    static constexpr int NSET = DBUF ? 2 : 1;
+    static constexpr int OFF_ST = NSET * SET_B;
+    static constexpr int OFF_DT = OFF_ST + NSET * ST_B;
+    static constexpr int BYTES = OFF_DT + 2 * DT_B;
+    static_assert(BYTES <= kLds, "LDS budget");
+    // the team of waves that loads and stages: L, or everyone in the single-set schedule
+    static constexpr int TW = DBUF ? 2 : NW, TW0 = DBUF ? 6 : 0, TT = 64 * TW;
+    static constexpr int CPR = DK / EPC;                  // chunks per q / k row
+    static constexpr int KPL = 16 * CPR / 64;             // K chunks per lane and t-block
+    static constexpr int NTBW = (NB + TW - 1) / TW;       // K t-blocks per team wave
+    static constexpr int OPS = LP * CPR / TT;             // q, k~, q~ chunks per thread and set
+    static_assert((LP * CPR) % TT == 0, "row chunks split evenly over the team");
+    static constexpr int VCPR = BV / EPC;
+    static constexpr int MCPR = LP / EPC, MCH = 4 * LP * MCPR;
     static constexpr int FCH = Rc::FACT_BYTES / 16;
-    static_assert(FCH <= kThreads, "factor chunks");
-    static_assert(RCH % kThreads == 0 || RPT == 1, "row chunks");
-    // a tile index w + s*NW is in range for every wave when the count divides evenly
-    static constexpr bool S_EVEN = NS % NW == 0;
+    static_assert(FCH <= TT, "factor chunks");
 
     unsigned char *smem;
     int tid, lane, wave;
@@ -93,295 +101,522 @@ struct Scan {
         lane = tid & 63;
         wave = wave_id();
     }
-    __device__ __forceinline__ Row *rows(int i) const { return reinterpret_cast<Row *>(smem + i * ROWS_B); }
-    __device__ __forceinline__ In *vs(int m) const { return reinterpret_cast<In *>(smem + OFF_V + m * V_B); }
-    __device__ __forceinline__ Mid *tm(int m) const { return reinterpret_cast<Mid *>(smem + OFF_T + m * TM_B); }
-    __device__ __forceinline__ float *fac(int m) const { return reinterpret_cast<float *>(smem + OFF_F) + m * 64; }
-    __device__ __forceinline__ Row *st(int h) const { return reinterpret_cast<Row *>(smem + OFF_ST + h * ST_B); }
-    __device__ __forceinline__ Mid *dm(int m) const { return reinterpret_cast<Mid *>(smem + OFF_D + m * DT_B); }
-    // post buffers over the dead q / kn / qn rows
-    __device__ __forceinline__ Mid *dl() const { return reinterpret_cast<Mid *>(smem + OFF_Y); }
-    __device__ __forceinline__ Mid *dn() const { return reinterpret_cast<Mid *>(smem + OFF_Y + DT_B); }
-    __device__ __forceinline__ Row *dd(int h) const { return reinterpret_cast<Row *>(smem + OFF_Y + (2 + h) * DT_B); }
+    __device__ __forceinline__ unsigned char *set(int p) const { return smem + p * SET_B; }
+    __device__ __forceinline__ E *rows(int p, int i) const { return reinterpret_cast<E *>(set(p) + i * ROWS_B); }
+    __device__ __forceinline__ E *kt(int p) const { return reinterpret_cast<E *>(set(p) + OFF_KT); }
+    __device__ __forceinline__ In *vs(int p, int m) const { return reinterpret_cast<In *>(set(p) + OFF_V + m * V_B); }
+    __device__ __forceinline__ E *tm(int p, int m) const { return reinterpret_cast<E *>(set(p) + OFF_TM + m * TM_B); }
+    __device__ __forceinline__ float *fac(int p, int m) const
+    {
+        return reinterpret_cast<float *>(set(p) + OFF_FAC) + m * 64;
+    }
+    __device__ __forceinline__ E *st(int b) const { return reinterpret_cast<E *>(smem + OFF_ST + b * ST_B); }
+    __device__ __forceinline__ E *dt(int b) const { return reinterpret_cast<E *>(smem + OFF_DT + b * DT_B); }
 
-    // ------------------------------------------------------------------ state
-    __device__ __forceinline__ void load_state(f32x4 (&S)[NSW], const float *src, int dv) const
+    // ------------------------------------------------------------------ chain
+    struct Ptrs {
+        const In *k, *q, *kn, *qn, *v, *vn;   // first row of the block (v, vn: column tile)
+        const unsigned char *rec;              // the block's record
+        Out *o, *on;
+    };
+    struct Chain {
+        Ptrs p0;                      // block 0
+        long qk_blk, v_blk, rec_blk;  // per-block advance (elements, elements, bytes)
+        int qks, vst;                 // row strides (elements)
+        long len;                     // tokens
+        int L;
+        const float *h0;              // initial state tile (row stride dv) or null
+        float *ht;                    // final state tile or null
+        int dv;
+        float scale;
+    };
+    __device__ __forceinline__ static void advance(Ptrs &p, const Chain &c)
     {
-#pragma unroll
-        for (int s = 0; s < NSW; ++s) {
-            const int t = wave + s * NW;
-            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-            if ((S_EVEN || t < NS) && src) {
-                const int bk = t / NVB, bc = t % NVB;
-                const float *p = src + (long)(16 * bk + 4 * (lane >> 4)) * dv + 16 * bc + (lane & 15);
-                acc[0] = p[0];
-                acc[1] = p[dv];
-                acc[2] = p[2 * dv];
-                acc[3] = p[3 * dv];
-            }
-            S[s] = acc;
-        }
-        wait_global_loads();
+        p.k += c.qk_blk;
+        p.q += c.qk_blk;
+        p.kn += c.qk_blk;
+        p.qn += c.qk_blk;
+        p.v += c.v_blk;
+        p.vn += c.v_blk;
+        p.rec += c.rec_blk;
+        p.o += c.v_blk;
+        p.on += c.v_blk;
     }
-    __device__ __forceinline__ void store_state(const f32x4 (&S)[NSW], float *dst, int dv) const
+    __device__ __forceinline__ static int nvalid_of(const Chain &c, int j)
     {
-#pragma unroll
-        for (int s = 0; s < NSW; ++s) {
-            const int t = wave + s * NW;
-            if (S_EVEN || t < NS) {
-                const int bk = t / NVB, bc = t % NVB;
-                float *p = dst + (long)(16 * bk + 4 * (lane >> 4)) * dv + 16 * bc + (lane & 15);
-                p[0] = S[s][0];
-                p[dv] = S[s][1];
-                p[2 * dv] = S[s][2];
-                p[3 * dv] = S[s][3];
-            }
-        }
-    }
-    // S^T operand(s) in LDS: ST[v][d_k]; with bf16 inputs as hi = bf16(S), lo = bf16(S - hi).
-    __device__ __forceinline__ void write_st(const f32x4 (&S)[NSW]) const
-    {
-#pragma unroll
-        for (int s = 0; s < NSW; ++s) {
-            const int t = wave + s * NW;
-            if (S_EVEN || t < NS) {
-                const int bk = t / NVB, bc = t % NVB;
-                const int off = (16 * bc + (lane & 15)) * RS + 16 * bk + 4 * (lane >> 4);
-                if constexpr (SPLIT) {
-                    float hi[4], lo[4];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        hi[i] = to_f(to_e<Row>(S[s][i]));
-                        lo[i] = S[s][i] - hi[i];
-                    }
-                    st4(st(0) + off, hi[0], hi[1], hi[2], hi[3]);
-                    st4(st(1) + off, lo[0], lo[1], lo[2], lo[3]);
-                } else {
-                    st4(st(0) + off, S[s][0], S[s][1], S[s][2], S[s][3]);
-                }
-            }
-        }
+        const long rem = c.len - (long)j * c.L;
+        return rem < c.L ? (int)rem : c.L;
     }
 
     // ------------------------------------------------------------------ loads
-    // Raw loaded data; rows past the block end are zeroed when staged, so nothing
-    // here waits for the loads to arrive.
+    // Buffer loads whose resource covers exactly the block's valid rows: rows at or
+    // past the block end read as zero (identity padding), with no clamps or branches.
+    // Per-lane byte offsets are fixed for the whole chain; the resources move with the
+    // block.
+    static constexpr int KCH = 16 * CPR;                  // K chunks per t-block
+    static constexpr int VPS = LP * VCPR;                 // V chunks per stream
+    static constexpr int VPL = (VPS + TT - 1) / TT;
+    static_assert(MCH % TT == 0, "record chunks split evenly over the team");
+    static constexpr int MPL = MCH / TT;
+    struct Offs {
+        unsigned k[NTBW][KPL];   // K rows of this wave's t-blocks
+        unsigned o[OPS];         // q, k~, q~ rows
+        unsigned v[VPL];
+    };
+    __device__ __forceinline__ void make_offs(const Chain &c, Offs &of) const
+    {
+        const int lt = tid - 64 * TW0, tw = wave - TW0;
+#pragma unroll
+        for (int s = 0; s < NTBW; ++s)
+#pragma unroll
+            for (int u = 0; u < KPL; ++u) {
+                const int ch = lane + 64 * u, t = 16 * (tw + TW * s) + ch / CPR, cc = ch % CPR;
+                of.k[s][u] = (unsigned)(t * c.qks * SE + cc * 16);
+            }
+#pragma unroll
+        for (int u = 0; u < OPS; ++u) {
+            const int ch = lt + TT * u, t = ch / CPR, cc = ch % CPR;
+            of.o[u] = (unsigned)(t * c.qks * SE + cc * 16);
+        }
+#pragma unroll
+        for (int u = 0; u < VPL; ++u) {
+            const int ch = lt + TT * u, t = ch / VCPR, cc = ch % VCPR;
+            of.v[u] = (unsigned)(t * c.vst * SE + cc * 16);
+        }
+    }
+
     struct Fetched {
-        u32x4 rb[4][RPT];
-        u32x4 vb[2][VPT];
-        u32x4 mb[MPT];
+        u32x4 kb[NTBW][KPL];
+        u32x4 ob[3][OPS];
+        u32x4 vb[2][VPL];
+        u32x4 mb[MPL];
         u32x4 fb;
-        int last;
     };
 
-    __device__ __forceinline__ const In *row_src(const IO &io, int i) const
+    __device__ __forceinline__ static __amdgpu_buffer_rsrc_t rsrc(const void *base, unsigned bytes)
     {
-        return i == 0 ? io.k : i == 1 ? io.q : i == 2 ? io.kn : io.qn;
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+    }
+    __device__ __forceinline__ static u32x4 bload(__amdgpu_buffer_rsrc_t r, unsigned off)
+    {
+        return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
     }
 
-    // Rows at or past nvalid are read from the last valid row (in bounds); stage()
-    // replaces them by zero.
-    __device__ __forceinline__ void fetch(const IO &io, Fetched &f) const
+    __device__ __forceinline__ void fetch(const Ptrs &P, const Chain &c, int nvalid, const Offs &of, Fetched &f) const
     {
-        const int last = io.nvalid - 1;
-        f.last = last;
+        const int lt = tid - 64 * TW0, tw = wave - TW0;
+        const unsigned rb = (unsigned)(nvalid * c.qks * SE), vb = (unsigned)(nvalid * c.vst * SE);
+        const __amdgpu_buffer_rsrc_t rk = rsrc(P.k, rb), rq = rsrc(P.q, rb), rkn = rsrc(P.kn, rb),
+                                     rqn = rsrc(P.qn, rb), rv = rsrc(P.v, vb), rvn = rsrc(P.vn, vb),
+                                     rr = rsrc(P.rec, (unsigned)Rc::BYTES);
 #pragma unroll
-        for (int s = 0; s < RPT; ++s) {
-            const int c = tid + s * kThreads;
-            const int cr = c < RCH ? c : RCH - 1;
-            const int t = cr / CPR, cc = cr % CPR;
-            const long off = (long)(t <= last ? t : last) * io.qk_stride + cc * EPC;
+        for (int s = 0; s < NTBW; ++s)
+            if (tw + TW * s < NB) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) f.rb[i][s] = *reinterpret_cast<const u32x4 *>(row_src(io, i) + off);
+                for (int u = 0; u < KPL; ++u) f.kb[s][u] = bload(rk, of.k[s][u]);
+            }
+#pragma unroll
+        for (int u = 0; u < OPS; ++u) {
+            f.ob[0][u] = bload(rq, of.o[u]);
+            f.ob[1][u] = bload(rkn, of.o[u]);
+            f.ob[2][u] = bload(rqn, of.o[u]);
         }
 #pragma unroll
-        for (int s = 0; s < VPT; ++s) {
-            const int c = tid + s * kThreads;
-            const int cr = c < VCH ? c : VCH - 1;
-            const int t = cr / VCPR, cc = cr % VCPR;
-            const long off = (long)(t <= last ? t : last) * io.v_stride + cc * EPC;
-            f.vb[0][s] = *reinterpret_cast<const u32x4 *>(io.v + off);
-            f.vb[1][s] = *reinterpret_cast<const u32x4 *>(io.vn + off);
-        }
-        const u32x4 *rec = reinterpret_cast<const u32x4 *>(io.rec);
+        for (int u = 0; u < VPL; ++u)
+            if (VPS % TT == 0 || lt + TT * u < VPS) {
+                f.vb[0][u] = bload(rv, of.v[u]);
+                f.vb[1][u] = bload(rvn, of.v[u]);
+            }
 #pragma unroll
-        for (int s = 0; s < MPT; ++s) {
-            const int c = tid + s * kThreads;
-            f.mb[s] = rec[c < MCH ? c : MCH - 1];
-        }
-        f.fb = rec[Rc::OFF_EG / 16 + (tid < FCH ? tid : FCH - 1)];
+        for (int u = 0; u < MPL; ++u) f.mb[u] = bload(rr, (unsigned)(16 * (lt + TT * u)));
+        f.fb = bload(rr, (unsigned)(Rc::OFF_EG + 16 * (lt < FCH ? lt : 0)));
     }
 
-    __device__ __forceinline__ void stage(const Fetched &f) const
+    // Stage the fetched block into set p.  With NEXT, each register is refilled with the
+    // matching chunk of the block at Pn right after it is written, so the next block's
+    // loads are in flight for a whole block step; nvalid_n = 0 makes them read nothing.
+    template <bool NEXT>
+    __device__ __forceinline__ void stage_impl(int p, Fetched &f, const Ptrs &Pn, int nvalid_n, const Chain &c,
+                                               const Offs &of) const
     {
-        const u32x4 zero = {0u, 0u, 0u, 0u};
+        const int lt = tid - 64 * TW0, tw = wave - TW0;
+        const unsigned rbn = (unsigned)(nvalid_n * c.qks * SE), vbn = (unsigned)(nvalid_n * c.vst * SE);
+        const __amdgpu_buffer_rsrc_t rk = rsrc(Pn.k, rbn), rq = rsrc(Pn.q, rbn), rkn = rsrc(Pn.kn, rbn),
+                                     rqn = rsrc(Pn.qn, rbn), rv = rsrc(Pn.v, vbn), rvn = rsrc(Pn.vn, vbn),
+                                     rr = rsrc(Pn.rec, nvalid_n > 0 ? (unsigned)Rc::BYTES : 0u);
 #pragma unroll
-        for (int s = 0; s < RPT; ++s) {
-            const int c = tid + s * kThreads;
-            if (c < RCH) {
-                const int t = c / CPR, cc = c % CPR;
-                const bool ok = t <= f.last;
+        for (int s = 0; s < NTBW; ++s) {
+            const int tb = tw + TW * s;
+            if (tb < NB) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    *reinterpret_cast<u32x4 *>(rows(i) + t * RS + cc * EPC) = ok ? to_operand<In, Row>(f.rb[i][s]) : zero;
-            }
-        }
-#pragma unroll
-        for (int s = 0; s < VPT; ++s) {
-            const int c = tid + s * kThreads;
-            if (c < VCH) {
-                const int t = c / VCPR, cc = c % VCPR;
-                const bool ok = t <= f.last;
-                *reinterpret_cast<u32x4 *>(vs(0) + t * VS + cc * EPC) = ok ? f.vb[0][s] : zero;
-                *reinterpret_cast<u32x4 *>(vs(1) + t * VS + cc * EPC) = ok ? f.vb[1][s] : zero;
-            }
-        }
-#pragma unroll
-        for (int s = 0; s < MPT; ++s) {
-            const int c = tid + s * kThreads;
-            if (c < MCH) {
-                const int m = c / (LP * MCPR), rr = (c / MCPR) % LP, cc = c % MCPR;
-                *reinterpret_cast<u32x4 *>(tm(m) + rr * TS + cc * (16 / SM)) = f.mb[s];
-            }
-        }
-        if (tid < FCH) {
-            // factor chunk tid covers floats 4*tid .. 4*tid+3 of [eG | dG | eGn]
-            const int e = 4 * tid, m = e / LP, i = e % LP;
-            *reinterpret_cast<u32x4 *>(fac(m) + i) = f.fb;
-        }
-    }
-
-    // ------------------------------------------------------------------ block step
-    __device__ __forceinline__ f32x4 x_tile(const Row *A, int bc) const
-    {
-        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (SPLIT)
-            return tile_mma2<Row, DK>(z, A, RS, st(0) + 16 * bc * RS, st(1) + 16 * bc * RS, RS, lane);
-        else
-            return tile_mma<Row, DK>(z, A, RS, st(0) + 16 * bc * RS, RS, lane);
-    }
-
-    __device__ __forceinline__ void store_rows(Out *dst, long stride, int nvalid, int bi, int bc, f32x4 acc,
-                                               float scale) const
-    {
-        const int r = 16 * bi + 4 * (lane >> 4), vc = 16 * bc + (lane & 15);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            if (r + i < nvalid) dst[(long)(r + i) * stride + vc] = to_e<Out>(acc[i] * scale);
-    }
-
-    __device__ __forceinline__ void step(const IO &io, bool has_next, const IO &next, Fetched &f,
-                                         f32x4 (&S)[NSW], float scale) const
-    {
-        stage(f);
-        lds_barrier();
-        if (has_next) fetch(next, f);
-        const int r0 = 4 * (lane >> 4), cl = lane & 15;
-        const float *eG = fac(0), *dG = fac(1), *eGn = fac(2);
-        // X1, X3 -> D, D~ (any wave); X2, X4 kept by their owners
-#pragma unroll
-        for (int s = 0; s < N13W; ++s) {
-            const int idx = wave + s * NW;
-            if (idx < N13) {
-                const bool noisy = idx >= NX;
-                const int t = noisy ? idx - NX : idx, bi = t / NVB, bc = t % NVB;
-                const f32x4 a = x_tile(rows(noisy ? 2 : 0) + 16 * bi * RS, bc);
-                const float *E = noisy ? eGn : eG;
-                const In *V = vs(noisy ? 1 : 0);
-                const int r = 16 * bi + r0, vc = 16 * bc + cl;
-                float d[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) d[i] = to_f(V[(r + i) * VS + vc]) - E[r + i] * a[i];
-                st4(dm(noisy ? 1 : 0) + vc * TS + r, d[0], d[1], d[2], d[3]);
-            }
-        }
-        f32x4 x2[NXW], x4[NXW];
-        const float gn_end = eGn[LP - 1];
-#pragma unroll
-        for (int s = 0; s < NXW; ++s) {
-            const int t2 = wave + s * NW;
-            if (t2 < NX) {
-                x2[s] = x_tile(rows(1) + 16 * (t2 / NVB) * RS, t2 % NVB);
-                const int r = 16 * (t2 / NVB) + r0;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) x2[s][i] *= eG[r + i];
-            }
-            // X4 tile t is owned by wave (t + NX) % NW
-            const int t4 = ((wave - NX % NW) + NW) % NW + s * NW;
-            if (t4 < NX) {
-                x4[s] = x_tile(rows(3) + 16 * (t4 / NVB) * RS, t4 % NVB);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) x4[s][i] *= gn_end;
-            }
-        }
-        lds_barrier();   // q / kn / qn rows and V are dead from here on
-        // Delta = T D, Delta~ = T~ D~
-#pragma unroll
-        for (int s = 0; s < NDW; ++s) {
-            const int idx = wave + s * NW;
-            if (idx < ND) {
-                const bool noisy = idx >= NX;
-                const int t = noisy ? idx - NX : idx, bi = t / NVB, bc = t % NVB;
-                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-                acc = tile_mma<Mid, LP>(acc, tm(noisy ? 1 : 0) + 16 * bi * TS, TS, dm(noisy ? 1 : 0) + 16 * bc * TS, TS,
-                                        lane);
-                const int vc = 16 * bc + cl, r = 16 * bi + r0;
-                if (noisy) {
-                    st4(dn() + vc * TS + r, acc[0], acc[1], acc[2], acc[3]);
-                } else {
-                    st4(dl() + vc * TS + r, acc[0], acc[1], acc[2], acc[3]);
-                    float e[4];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) e[i] = dG[r + i] * acc[i];
-                    if constexpr (SPLIT) {
-                        float hi[4], lo[4];
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            hi[i] = to_f(to_e<Row>(e[i]));
-                            lo[i] = e[i] - hi[i];
-                        }
-                        st4(dd(0) + vc * TS + r, hi[0], hi[1], hi[2], hi[3]);
-                        st4(dd(1) + vc * TS + r, lo[0], lo[1], lo[2], lo[3]);
-                    } else {
-                        st4(dd(0) + vc * TS + r, e[0], e[1], e[2], e[3]);
-                    }
+                for (int u = 0; u < KPL; ++u) {
+                    const int ch = lane + 64 * u, t = 16 * tb + ch / CPR, cc = ch % CPR;
+                    *reinterpret_cast<u32x4 *>(rows(p, 0) + t * RS + cc * EPC) = to_operand<In, E>(f.kb[s][u]);
+                    if (NEXT) f.kb[s][u] = bload(rk, of.k[s][u]);
                 }
             }
         }
-        lds_barrier();
-        // outputs
 #pragma unroll
-        for (int s = 0; s < NXW; ++s) {
-            const int t2 = wave + s * NW;
-            if (t2 < NX) {
-                const int bi = t2 / NVB, bc = t2 % NVB;
-                const f32x4 acc = tile_mma<Mid, LP>(x2[s], tm(2) + 16 * bi * TS, TS, dl() + 16 * bc * TS, TS, lane);
-                store_rows(io.o, io.v_stride, io.nvalid, bi, bc, acc, scale);
-            }
-            const int t4 = ((wave - NX % NW) + NW) % NW + s * NW;
-            if (t4 < NX) {
-                const int bi = t4 / NVB, bc = t4 % NVB;
-                const f32x4 acc = tile_mma<Mid, LP>(x4[s], tm(3) + 16 * bi * TS, TS, dn() + 16 * bc * TS, TS, lane);
-                store_rows(io.on, io.v_stride, io.nvalid, bi, bc, acc, scale);
+        for (int u = 0; u < OPS; ++u) {
+            const int ch = lt + TT * u, t = ch / CPR, cc = ch % CPR;
+#pragma unroll
+            for (int si = 0; si < 3; ++si) {
+                *reinterpret_cast<u32x4 *>(rows(p, 1 + si) + t * RS + cc * EPC) = to_operand<In, E>(f.ob[si][u]);
+                if (NEXT) f.ob[si][u] = bload(si == 0 ? rq : si == 1 ? rkn : rqn, of.o[u]);
             }
         }
-        // S <- gamma_n S + K^T diag(dG) Delta
-        const float decay = eG[LP - 1];
 #pragma unroll
-        for (int s = 0; s < NSW; ++s) {
-            const int t = wave + s * NW;
-            if (S_EVEN || t < NS) {
-                const int bk = t / NVB, bc = t % NVB;
-                const f32x4 acc = S[s] * decay;
-                if constexpr (SPLIT)
-                    S[s] = tile_mma_at2<Row, LP>(acc, rows(0) + 16 * bk, RS, dd(0) + 16 * bc * TS, dd(1) + 16 * bc * TS,
-                                                 TS, lane);
-                else
-                    S[s] = tile_mma_at<Row, LP>(acc, rows(0) + 16 * bk, RS, dd(0) + 16 * bc * TS, TS, lane);
+        for (int u = 0; u < VPL; ++u) {
+            const int ch = lt + TT * u;
+            if (VPS % TT == 0 || ch < VPS) {
+                const int t = ch / VCPR, cc = ch % VCPR;
+                *reinterpret_cast<u32x4 *>(vs(p, 0) + t * VS + cc * EPC) = f.vb[0][u];
+                *reinterpret_cast<u32x4 *>(vs(p, 1) + t * VS + cc * EPC) = f.vb[1][u];
+                if (NEXT) {
+                    f.vb[0][u] = bload(rv, of.v[u]);
+                    f.vb[1][u] = bload(rvn, of.v[u]);
+                }
             }
         }
-        write_st(S);
-        lds_barrier();
+#pragma unroll
+        for (int u = 0; u < MPL; ++u) {
+            const int ch = lt + TT * u;
+            const int m = ch / (LP * MCPR), rr2 = (ch / MCPR) % LP, cc = ch % MCPR;
+            *reinterpret_cast<u32x4 *>(tm(p, m) + rr2 * TS + cc * EPC) = f.mb[u];
+            if (NEXT) f.mb[u] = bload(rr, (unsigned)(16 * ch));
+        }
+        if (lt < FCH) {
+            // chunk lt holds floats 4 lt .. 4 lt + 3 of [eG | dG | eGn]
+            const int e = 4 * lt, m = e / LP, i = e % LP;
+            *reinterpret_cast<u32x4 *>(fac(p, m) + i) = f.fb;
+        }
+        if (NEXT) f.fb = bload(rr, (unsigned)(Rc::OFF_EG + 16 * (lt < FCH ? lt : 0)));
+        // fp32 operands: K^T of this wave's t-blocks, from the rows it has just written
+        // (LDS operations of one wave complete in order, so no barrier is needed)
+#pragma unroll
+        for (int s = 0; s < NTBW; ++s) {
+            const int tb = tw + TW * s;
+            if (!TR && tb < NB) {
+#pragma unroll
+                for (int u = 0; u < DK / 16; ++u) {
+                    const int qd = lane + 64 * u, kk = qd % DK, g4 = qd / DK;
+                    const E *src = rows(p, 0) + (16 * tb + 4 * g4) * RS + kk;
+                    QE v;
+                    v[0] = src[0];
+                    v[1] = src[RS];
+                    v[2] = src[2 * RS];
+                    v[3] = src[3 * RS];
+                    st_quad(kt(p) + kk * TS + 16 * tb + 4 * g4, v);
+                }
+            }
+        }
+    }
+    __device__ __forceinline__ void stage(int p, Fetched &f, const Chain &c, const Offs &of) const
+    {
+        stage_impl<false>(p, f, c.p0, 0, c, of);
+    }
+
+    // ------------------------------------------------------------------ helpers
+    __device__ __forceinline__ f32x4 ld4f(const float *p) const { return *reinterpret_cast<const f32x4 *>(p); }
+
+    // X = R S for the NB row tiles of row set R (rows(p, i)), state operand quads sq.
+    __device__ __forceinline__ void x_rows(f32x4 (&x)[NB], const E *R, const QE (&sq)[DKB]) const
+    {
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            QE a[DKB];
+            ld_quads<E, DKB>(a, R + 16 * rb * RS, RS, lane);
+            x[rb] = mma_q<E, DKB>(f32x4{0.f, 0.f, 0.f, 0.f}, a, sq);
+        }
+    }
+
+    // D = V - diag(G) X (column half bc), as B-operand quads.
+    __device__ __forceinline__ void d_quads(QE (&dq)[NB], const f32x4 (&x)[NB], const In *V, const float *G,
+                                            int bc) const
+    {
+        const int g = lane >> 4, n = lane & 15;
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            const int r = 16 * rb + 4 * g;
+            const f32x4 gq = ld4f(G + r);
+            const In *vp = V + r * VS + 16 * bc + n;
+            f32x4 d;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) d[i] = to_f(vp[i * VS]) - gq[i] * x[rb][i];
+            dq[rb] = quad_of<E>(d);
+        }
+    }
+
+    // Y = M Z for a record matrix M (LP x LP, rows(p)) and B-operand quads zq.
+    __device__ __forceinline__ void m_times(f32x4 (&y)[NB], const E *M, const QE (&zq)[NB], const f32x4 (&init)[NB]) const
+    {
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            QE a[NB];
+            ld_quads<E, NB>(a, M + 16 * rb * TS, TS, lane);
+            y[rb] = mma_q<E, NB>(init[rb], a, zq);
+        }
+    }
+
+    __device__ __forceinline__ void store_out(Out *dst, int stride, int nvalid, int bc, const f32x4 (&acc)[NB],
+                                              float scale) const
+    {
+        const int g = lane >> 4, n = lane & 15;
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            const int r = 16 * rb + 4 * g;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (r + i < nvalid) dst[(r + i) * stride + 16 * bc + n] = to_e<Out>(acc[rb][i] * scale);
+        }
+    }
+
+    __device__ __forceinline__ void write_st(int b, const QE (&sq)[DKB], int bc) const
+    {
+        const int g = lane >> 4, n = lane & 15;
+        E *dst = st(b) + (16 * bc + n) * RS + 4 * g;
+#pragma unroll
+        for (int kb = 0; kb < DKB; ++kb) st_quad(dst + 16 * kb, sq[kb]);
+    }
+
+    // A-operand quads of K^T (rows 16 kb .. 16 kb + 15 of K^T, all NB t-blocks): lane
+    // (g, r) gets K[16 rb + 4 g + i][16 kb + r], i = 0..3.  A 16-bit transpose load hands
+    // lane i of each 16-lane group element (i & 3) of the 4-element segment addressed by
+    // lane 4 j + (i >> 2) of the group, as element j; so lane 16 g + 4 j + q addresses
+    // row 16 rb + 4 g + j, columns 16 kb + 4 q .. + 3 of K.
+    __device__ __forceinline__ void kt_quads(QE (&a)[NB], int p, int kb) const
+    {
+        if constexpr (TR) {
+            const E *base = rows(p, 0) + (4 * (lane >> 4) + ((lane >> 2) & 3)) * RS + 16 * kb + 4 * (lane & 3);
+#pragma unroll
+            for (int rb = 0; rb < NB; ++rb)
+                a[rb] = __builtin_bit_cast(QE, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                                   (__attribute__((address_space(3))) s16x4 *)(base + 16 * rb * RS)));
+        } else {
+            ld_quads<E, NB>(a, kt(p) + 16 * kb * TS, TS, lane);
+        }
+    }
+
+    // ------------------------------------------------------------------ roles
+    // C: one block of the recurrence for column half bc.  S (fp32) and sq (its operand
+    // copy) are the state on entry and on exit; Delta^T goes to dt(db).
+    __device__ __forceinline__ void c_block(int p, int db, int bc, f32x4 (&S)[DKB], QE (&sq)[DKB]) const
+    {
+        const int g = lane >> 4, n = lane & 15;
+        const f32x4 z[NB] = {};
+        f32x4 x[NB];
+        x_rows(x, rows(p, 0), sq);
+        QE dq[NB];
+        d_quads(dq, x, vs(p, 0), fac(p, 0), bc);
+        f32x4 dl[NB];
+        m_times(dl, tm(p, 0), dq, z);
+        QE uq[NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            st_quad(dt(db) + (16 * bc + n) * TS + 16 * rb + 4 * g, quad_of<E>(dl[rb]));
+            uq[rb] = quad_of<E>(dl[rb] * ld4f(fac(p, 1) + 16 * rb + 4 * g));
+        }
+        const float decay = fac(p, 0)[LP - 1];
+#pragma unroll
+        for (int kb = 0; kb < DKB; ++kb) {
+            QE a[NB];
+            kt_quads(a, p, kb);
+            S[kb] = mma_q<E, NB>(S[kb] * decay, a, uq);
+            sq[kb] = quad_of<E>(S[kb]);
+        }
+    }
+
+    // N: the noisy block for column half bc, from the state operand in st(sb).
+    __device__ __forceinline__ void n_block(int p, int sb, int bc, Out *on, int stride, int nvalid,
+                                            float scale) const
+    {
+        const f32x4 z[NB] = {};
+        QE sq[DKB];
+        ld_quads<E, DKB>(sq, st(sb) + 16 * bc * RS, RS, lane);
+        f32x4 x3[NB], x4[NB];
+        x_rows(x3, rows(p, 2), sq);
+        x_rows(x4, rows(p, 3), sq);
+        QE dq[NB];
+        d_quads(dq, x3, vs(p, 1), fac(p, 2), bc);
+        f32x4 dn[NB];
+        m_times(dn, tm(p, 1), dq, z);
+        QE nq[NB];
+        const float gn_end = fac(p, 2)[LP - 1];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            nq[rb] = quad_of<E>(dn[rb]);
+            x4[rb] *= gn_end;
+        }
+        f32x4 o[NB];
+        m_times(o, tm(p, 3), nq, x4);
+        store_out(on, stride, nvalid, bc, o, scale);
+    }
+
+    // O, first half: X2 scaled by eG and the P quads of the current block, kept until
+    // Delta is published.
+    __device__ __forceinline__ void o_begin(int p, int sb, int bc, f32x4 (&x2)[NB], QE (&pq)[NB][NB]) const
+    {
+        const int g = lane >> 4;
+        QE sq[DKB];
+        ld_quads<E, DKB>(sq, st(sb) + 16 * bc * RS, RS, lane);
+        x_rows(x2, rows(p, 1), sq);
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            x2[rb] *= ld4f(fac(p, 0) + 16 * rb + 4 * g);
+            ld_quads<E, NB>(pq[rb], tm(p, 2) + 16 * rb * TS, TS, lane);
+        }
+    }
+
+    // O, second half: O = s (X2 + P Delta) with Delta^T from dt(db).
+    __device__ __forceinline__ void o_end(int db, int bc, const f32x4 (&x2)[NB], const QE (&pq)[NB][NB], Out *o,
+                                          int stride, int nvalid, float scale) const
+    {
+        QE dq[NB];
+        ld_quads<E, NB>(dq, dt(db) + 16 * bc * TS, TS, lane);
+        f32x4 acc[NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) acc[rb] = mma_q<E, NB>(x2[rb], pq[rb], dq);
+        store_out(o, stride, nvalid, bc, acc, scale);
+    }
+
+    // ------------------------------------------------------------------ the chain
+    __device__ void run(const Chain &c) const
+    {
+        const int nb = (int)((c.len + c.L - 1) / c.L);
+        const int g = lane >> 4, n = lane & 15;
+        if (wave < 2) {
+            // ---- C
+            const int bc = wave;
+            f32x4 S[DKB];
+            QE sq[DKB];
+#pragma unroll
+            for (int kb = 0; kb < DKB; ++kb) {
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                if (c.h0) {
+                    const float *src = c.h0 + (long)(16 * kb + 4 * g) * c.dv + 16 * bc + n;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[i] = src[i * c.dv];
+                }
+                S[kb] = acc;
+                sq[kb] = quad_of<E>(acc);
+            }
+            wait_global_loads();
+            Fetched f;
+            Offs of;
+            if (!DBUF || wave >= TW0) make_offs(c, of);
+            Ptrs pf = c.p0;
+            if (DBUF)
+                write_st(0, sq, bc);
+            else if (nb > 0)
+                fetch(pf, c, nvalid_of(c, 0), of, f);
+            lds_barrier();
+            for (int j = 0; j < nb; ++j) {
+                const int p = DBUF ? (j & 1) : 0;
+                if (!DBUF) {
+                    stage(0, f, c, of);
+                    write_st(0, sq, bc);
+                    lds_barrier();
+                    if (j + 1 < nb) {
+                        advance(pf, c);
+                        fetch(pf, c, nvalid_of(c, j + 1), of, f);
+                    }
+                }
+                c_block(p, j & 1, bc, S, sq);
+                if (DBUF) write_st((j + 1) & 1, sq, bc);
+                lds_barrier();
+            }
+            if (c.ht) {
+#pragma unroll
+                for (int kb = 0; kb < DKB; ++kb) {
+                    float *dst = c.ht + (long)(16 * kb + 4 * g) * c.dv + 16 * bc + n;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) dst[i * c.dv] = S[kb][i];
+                }
+            }
+        } else if (wave < 4) {
+            // ---- N
+            const int bc = wave - 2;
+            Fetched f;
+            Offs of;
+            if (!DBUF || wave >= TW0) make_offs(c, of);
+            Ptrs pf = c.p0, pc = c.p0;
+            if (!DBUF && nb > 0) fetch(pf, c, nvalid_of(c, 0), of, f);
+            lds_barrier();
+            for (int j = 0; j < nb; ++j) {
+                const int p = DBUF ? (j & 1) : 0;
+                if (!DBUF) {
+                    stage(0, f, c, of);
+                    lds_barrier();
+                    if (j + 1 < nb) {
+                        advance(pf, c);
+                        fetch(pf, c, nvalid_of(c, j + 1), of, f);
+                    }
+                }
+                n_block(p, DBUF ? (j & 1) : 0, bc, pc.on, c.vst, nvalid_of(c, j), c.scale);
+                advance(pc, c);
+                lds_barrier();
+            }
+        } else if (wave < 6) {
+            // ---- O
+            const int bc = wave - 4;
+            Fetched f;
+            Offs of;
+            if (!DBUF || wave >= TW0) make_offs(c, of);
+            Ptrs pf = c.p0, pc = c.p0;
+            f32x4 x2[NB];
+            QE pq[NB][NB];
+            if (!DBUF && nb > 0) fetch(pf, c, nvalid_of(c, 0), of, f);
+            lds_barrier();
+            for (int j = 0; j < nb; ++j) {
+                const int p = DBUF ? (j & 1) : 0;
+                if (!DBUF) {
+                    stage(0, f, c, of);
+                    lds_barrier();
+                    if (j + 1 < nb) {
+                        advance(pf, c);
+                        fetch(pf, c, nvalid_of(c, j + 1), of, f);
+                    }
+                }
+                if (j > 0) {
+                    o_end((j - 1) & 1, bc, x2, pq, pc.o, c.vst, nvalid_of(c, j - 1), c.scale);
+                    advance(pc, c);
+                }
+                o_begin(p, DBUF ? (j & 1) : 0, bc, x2, pq);
+                lds_barrier();
+            }
+            if (nb > 0) o_end((nb - 1) & 1, bc, x2, pq, pc.o, c.vst, nvalid_of(c, nb - 1), c.scale);
+        } else {
+            // ---- L
+            Fetched f;
+            Offs of;
+            if (!DBUF || wave >= TW0) make_offs(c, of);
+            Ptrs pf = c.p0;
+            if (nb > 0) {
+                fetch(pf, c, nvalid_of(c, 0), of, f);
+                if (DBUF) {
+                    stage(0, f, c, of);
+                    advance(pf, c);
+                    if (nb > 1) fetch(pf, c, nvalid_of(c, 1), of, f);
+                    advance(pf, c);
+                }
+            }
+            lds_barrier();
+            for (int j = 0; j < nb; ++j) {
+                if (DBUF) {
+                    // stage block j + 1, load block j + 2 (pf)
+                    if (j + 1 < nb) stage_impl<true>((j + 1) & 1, f, pf, j + 2 < nb ? nvalid_of(c, j + 2) : 0, c, of);
+                    advance(pf, c);
+                } else {
+                    stage(0, f, c, of);
+                    lds_barrier();
+                    if (j + 1 < nb) {
+                        advance(pf, c);
+                        fetch(pf, c, nvalid_of(c, j + 1), of, f);
+                    }
+                }
+                lds_barrier();
+            }
+        }
     }
 };
 
