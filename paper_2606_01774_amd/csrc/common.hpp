@@ -276,13 +276,17 @@ template <> __device__ __forceinline__ f16x4 quad_of<_Float16>(f32x4 a)
 template <> __device__ __forceinline__ f32x4 quad_of<float>(f32x4 a) { return a; }
 
 // Quads of row (lane & 15) of the row-major LDS matrix M (row stride ld), k-blocks
-// 0 .. NKB-1 starting at M's first column.
+// 0 .. NKB-1 starting at M's first column.  Each quad is its own 8-byte LDS read: with
+// rows 16 bytes past a multiple of 256 bytes these are free of bank conflicts, while the
+// paired two-address reads the compiler would otherwise form from them are not (8
+// conflict cycles per pair on gfx950); the volatile access keeps them unpaired.
 template <typename E, int NKB>
 __device__ __forceinline__ void ld_quads(Quad<E> (&q)[NKB], const E *M, int ld, int lane)
 {
+    typedef const __attribute__((address_space(3))) volatile Quad<E> *LQ;
     const E *p = M + (lane & 15) * ld + 4 * (lane >> 4);
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) q[kb] = ld_quad(p + 16 * kb);
+    for (int kb = 0; kb < NKB; ++kb) q[kb] = *(LQ)(p + 16 * kb);
 }
 
 // acc += sum over k-blocks kb of A_kb B_kb.

@@ -41,11 +41,11 @@ __global__ void __launch_bounds__(64 * kIntraNW) bdgdn_k1_intra_kernel(IntraArgs
 }
 
 template <typename In, typename Out, int DK, int BV, int LP>
-__global__ void __launch_bounds__(512) bdgdn_k2_scan_kernel(ScanArgs a)
+__global__ void __launch_bounds__(640) bdgdn_k2_scan_kernel(ScanArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     typedef Scan<In, Out, DK, BV, LP> K2;
-    static_assert(K2::kThreads == 512, "launch bounds");
+    static_assert(K2::kThreads == 640, "launch bounds");
     // ids i, i+8, i+16, ... of a group carry the d_v tiles of one chain, so they land
     // on one XCD and share its L2 for the q/k rows and the records.
     const int id = blockIdx.x;

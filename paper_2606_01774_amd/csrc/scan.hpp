@@ -33,6 +33,10 @@
 
 #include "intra.hpp"
 
+#ifndef BDGDN_SCAN_LAYOUT
+#define BDGDN_SCAN_LAYOUT 0x3333221100ull
+#endif
+
 namespace bdgdn {
 
 // Operand type of the scan's MFMA products by input type: fp16 for bf16 inputs (the
@@ -48,8 +52,8 @@ struct Scan {
     static_assert(__is_same(E, typename Prec<In>::Mid), "records hold scan operands");
     typedef Rec<E, LP> Rc;
     typedef Quad<E> QE;
-    static constexpr int NW = 8, kThreads = 64 * NW;
-    static constexpr int NB = LP / 16, DKB = DK / 16;
+    static constexpr int NW = 10, kThreads = 64 * NW;
+    static constexpr int NB = LP / 16, DKB = DK / 16, NVB = BV / 16;
     static_assert(BV == 32, "two 16-column halves per workgroup");
     static constexpr int SE = (int)sizeof(E);
     static_assert(SE == (int)sizeof(In), "inputs are staged chunk for chunk");
@@ -60,50 +64,77 @@ struct Scan {
     static constexpr int VS = BV + PE;    // V [token][v]
     // one staging set
     static constexpr int ROWS_B = al16(LP * RS * SE);
-    // 16-bit operands read K^T straight from the K rows with LDS transpose loads; fp32
-    // operands keep a staged transposed copy
+    // K^T for the state update is read straight from the K rows: with LDS transpose
+    // loads for 16-bit operands, element by element for fp32
     static constexpr bool TR = SE == 2;
-    static constexpr int KT_B = TR ? 0 : al16(DK * TS * SE);
     static constexpr int V_B = al16(LP * VS * SE);
     static constexpr int TM_B = al16(LP * TS * SE);
-    static constexpr int OFF_KT = 4 * ROWS_B;
-    static constexpr int OFF_V = OFF_KT + KT_B;
+    static constexpr int OFF_V = 4 * ROWS_B;
     static constexpr int OFF_TM = OFF_V + 2 * V_B;
     static constexpr int OFF_FAC = OFF_TM + 4 * TM_B;
     static constexpr int SET_B = OFF_FAC + 3 * 64 * 4;
     static constexpr int ST_B = al16(BV * RS * SE);
     static constexpr int DT_B = al16(BV * TS * SE);
     static constexpr int kLds = 160 * 1024;
-    static constexpr bool DBUF = 2 * SET_B + 2 * ST_B + 2 * DT_B <= kLds;
+    static constexpr bool DBUF = 2 * SET_B + 2 * ST_B + 2 * DT_B + 1024 <= kLds;
     static constexpr int NSET = DBUF ? 2 : 1;
     static constexpr int OFF_ST = NSET * SET_B;
     static constexpr int OFF_DT = OFF_ST + NSET * ST_B;
-    static constexpr int BYTES = OFF_DT + 2 * DT_B;
+    static constexpr int OFF_DUMMY = OFF_DT + 2 * DT_B;   // sink for unassigned staging slots
+    static constexpr int BYTES = OFF_DUMMY + 64 * 16;
     static_assert(BYTES <= kLds, "LDS budget");
-    // the team of waves that loads and stages: L, or everyone in the single-set schedule
-    static constexpr int TW = DBUF ? 2 : NW, TW0 = DBUF ? 6 : 0, TT = 64 * TW;
+    // Roles by wave: nibble w of kLayout (w = 0..9) is the role of wave w: 0 C, 1 N,
+    // 2 O, 3 L.  Waves w, w + 4 and w + 8 share a SIMD.  The two waves of a compute role
+    // take column halves 0 and 1 in wave order; L waves form the staging team in wave
+    // order.
+    enum { R_C = 0, R_N = 1, R_O = 2, R_L = 3 };
+    static constexpr unsigned long long kLayout = BDGDN_SCAN_LAYOUT;
+    static constexpr int role_of(int w) { return (int)((kLayout >> (4 * w)) & 15); }
+    static constexpr int rank_of(int w)
+    {
+        int r = 0;
+        for (int i = 0; i < w; ++i) r += role_of(i) == role_of(w);
+        return r;
+    }
+    static constexpr int count_of(int role)
+    {
+        int n = 0;
+        for (int i = 0; i < 10; ++i) n += role_of(i) == role;
+        return n;
+    }
+    static_assert(count_of(R_C) == 2 && count_of(R_N) == 2 && count_of(R_O) == 2 && count_of(R_L) == 4, "layout");
+    // the team of waves that loads and stages: the L waves
+    static constexpr int TW = 4, TT = 64 * TW;
     static constexpr int CPR = DK / EPC;                  // chunks per q / k row
-    static constexpr int KPL = 16 * CPR / 64;             // K chunks per lane and t-block
-    static constexpr int NTBW = (NB + TW - 1) / TW;       // K t-blocks per team wave
-    static constexpr int OPS = LP * CPR / TT;             // q, k~, q~ chunks per thread and set
-    static_assert((LP * CPR) % TT == 0, "row chunks split evenly over the team");
+    static constexpr int OCH = LP * CPR;                  // chunks per row set
+    static constexpr int OPS = (OCH + TT - 1) / TT;       // row slots per thread (x 4 sets)
     static constexpr int VCPR = BV / EPC;
+    static constexpr int VPS = LP * VCPR;                 // V chunks per stream
+    static_assert(VPS % 64 == 0, "a wave's V slot lies in one stream");
+    static constexpr int VPL = (2 * VPS + TT - 1) / TT;   // V slots per thread (both streams)
     static constexpr int MCPR = LP / EPC, MCH = 4 * LP * MCPR;
     static constexpr int FCH = Rc::FACT_BYTES / 16;
-    static_assert(FCH <= TT, "factor chunks");
+    static constexpr int RPL = (MCH + TT - 1) / TT;       // record matrix slots per thread
+    static_assert(FCH <= TT, "one factor slot");
+    static_assert(Rc::OFF_EG == 16 * MCH, "factors follow the matrices");
 
     unsigned char *smem;
     int tid, lane, wave;
+
+    int role, rank;   // this wave's role and its index among the waves of that role
 
     __device__ Scan(unsigned char *s) : smem(s)
     {
         tid = threadIdx.x;
         lane = tid & 63;
         wave = wave_id();
+        role = (int)((kLayout >> (4 * wave)) & 15);
+        rank = 0;
+#pragma unroll
+        for (int i = 0; i < 10; ++i) rank += (i < wave && role_of(i) == role) ? 1 : 0;
     }
     __device__ __forceinline__ unsigned char *set(int p) const { return smem + p * SET_B; }
     __device__ __forceinline__ E *rows(int p, int i) const { return reinterpret_cast<E *>(set(p) + i * ROWS_B); }
-    __device__ __forceinline__ E *kt(int p) const { return reinterpret_cast<E *>(set(p) + OFF_KT); }
     __device__ __forceinline__ In *vs(int p, int m) const { return reinterpret_cast<In *>(set(p) + OFF_V + m * V_B); }
     __device__ __forceinline__ E *tm(int p, int m) const { return reinterpret_cast<E *>(set(p) + OFF_TM + m * TM_B); }
     __device__ __forceinline__ float *fac(int p, int m) const
@@ -149,47 +180,60 @@ struct Scan {
     }
 
     // ------------------------------------------------------------------ loads
-    // Buffer loads whose resource covers exactly the block's valid rows: rows at or
-    // past the block end read as zero (identity padding), with no clamps or branches.
-    // Per-lane byte offsets are fixed for the whole chain; the resources move with the
-    // block.
-    static constexpr int KCH = 16 * CPR;                  // K chunks per t-block
-    static constexpr int VPS = LP * VCPR;                 // V chunks per stream
-    static constexpr int VPL = (VPS + TT - 1) / TT;
-    static_assert(MCH % TT == 0, "record chunks split evenly over the team");
-    static constexpr int MPL = MCH / TT;
+    // The L team moves one block: 4 row sets, V and V~ (the column tile), and the
+    // record.  Every thread runs the same straight-line sequence of slots (no branches,
+    // so the compiler's load counters stay exact and a wait never covers loads of the
+    // next block): an unassigned slot reloads the block's first chunk (a cache hit) and
+    // stores it into a per-lane sink in LDS.  Resources cover exactly the block's valid
+    // rows, so rows past the block end read as zero.
     struct Offs {
-        unsigned k[NTBW][KPL];   // K rows of this wave's t-blocks
-        unsigned o[OPS];         // q, k~, q~ rows
-        unsigned v[VPL];
+        unsigned rg[OPS], rl[OPS];   // row slots: global byte offset, LDS byte offset in a row set
+        unsigned vg[VPL], vl[VPL];   // V slots (stream and validity are per wave)
+        unsigned mg[RPL], ml[RPL];   // record matrix slots (LDS offset relative to the set)
+        unsigned fg, fl;             // factor slot
     };
+    // V slot u of team wave tw: stream m, or none
+    __device__ __forceinline__ static int v_base(int tw, int u) { return tw * 64 + TT * u; }
     __device__ __forceinline__ void make_offs(const Chain &c, Offs &of) const
     {
-        const int lt = tid - 64 * TW0, tw = wave - TW0;
-#pragma unroll
-        for (int s = 0; s < NTBW; ++s)
-#pragma unroll
-            for (int u = 0; u < KPL; ++u) {
-                const int ch = lane + 64 * u, t = 16 * (tw + TW * s) + ch / CPR, cc = ch % CPR;
-                of.k[s][u] = (unsigned)(t * c.qks * SE + cc * 16);
-            }
+        const int tw = rank, lt = 64 * tw + lane;
+        const unsigned sink = (unsigned)(OFF_DUMMY + 16 * lane);
 #pragma unroll
         for (int u = 0; u < OPS; ++u) {
             const int ch = lt + TT * u, t = ch / CPR, cc = ch % CPR;
-            of.o[u] = (unsigned)(t * c.qks * SE + cc * 16);
+            const bool ok = ch < OCH;
+            of.rg[u] = ok ? (unsigned)(t * c.qks * SE + cc * 16) : 0u;
+            of.rl[u] = ok ? (unsigned)((t * RS + cc * EPC) * SE) : sink;
         }
 #pragma unroll
         for (int u = 0; u < VPL; ++u) {
-            const int ch = lt + TT * u, t = ch / VCPR, cc = ch % VCPR;
-            of.v[u] = (unsigned)(t * c.vst * SE + cc * 16);
+            const int vb = v_base(tw, u);
+            const bool ok = vb < 2 * VPS;
+            const int ch = (ok ? vb % VPS : 0) + lane, t = ch / VCPR, cc = ch % VCPR;
+            of.vg[u] = ok ? (unsigned)(t * c.vst * SE + cc * 16) : 0u;
+            of.vl[u] = ok ? (unsigned)(OFF_V + (vb / VPS) * V_B + (t * VS + cc * EPC) * SE) : sink;
+        }
+#pragma unroll
+        for (int u = 0; u < RPL; ++u) {
+            const int ch = lt + TT * u;
+            const bool ok = ch < MCH;
+            const int m = ch / (LP * MCPR), rr = (ch / MCPR) % LP, cc = ch % MCPR;
+            of.mg[u] = ok ? (unsigned)(16 * ch) : 0u;
+            of.ml[u] = ok ? (unsigned)(OFF_TM + m * TM_B + (rr * TS + cc * EPC) * SE) : sink;
+        }
+        {
+            // factor chunk e holds floats 4 e .. 4 e + 3 of [eG | dG | eGn]
+            const bool ok = lt < FCH;
+            const int e = 4 * lt, m = e / LP, i = e % LP;
+            of.fg = ok ? (unsigned)(Rc::OFF_EG + 16 * lt) : 0u;
+            of.fl = ok ? (unsigned)(OFF_FAC + (m * 64 + i) * 4) : sink;
         }
     }
 
     struct Fetched {
-        u32x4 kb[NTBW][KPL];
-        u32x4 ob[3][OPS];
-        u32x4 vb[2][VPL];
-        u32x4 mb[MPL];
+        u32x4 rb[4][OPS];
+        u32x4 vb[VPL];
+        u32x4 mb[RPL];
         u32x4 fb;
     };
 
@@ -201,174 +245,148 @@ struct Scan {
     {
         return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
     }
+    __device__ __forceinline__ void st16(int p, unsigned off, u32x4 v) const
+    {
+        // offsets below OFF_DUMMY are inside the staging set; the sink is absolute
+        unsigned char *base = off >= (unsigned)OFF_DUMMY ? smem : set(p);
+        *reinterpret_cast<u32x4 *>(base + off) = v;
+    }
+
+    struct Rsrcs {
+        __amdgpu_buffer_rsrc_t r[4], v[2], m;
+    };
+    __device__ __forceinline__ Rsrcs rsrcs(const Ptrs &P, const Chain &c, int nvalid) const
+    {
+        const unsigned rb = (unsigned)(nvalid * c.qks * SE), vb = (unsigned)(nvalid * c.vst * SE);
+        Rsrcs r;
+        r.r[0] = rsrc(P.k, rb);
+        r.r[1] = rsrc(P.q, rb);
+        r.r[2] = rsrc(P.kn, rb);
+        r.r[3] = rsrc(P.qn, rb);
+        r.v[0] = rsrc(P.v, vb);
+        r.v[1] = rsrc(P.vn, vb);
+        r.m = rsrc(P.rec, nvalid > 0 ? (unsigned)Rc::BYTES : 0u);
+        return r;
+    }
 
     __device__ __forceinline__ void fetch(const Ptrs &P, const Chain &c, int nvalid, const Offs &of, Fetched &f) const
     {
-        const int lt = tid - 64 * TW0, tw = wave - TW0;
-        const unsigned rb = (unsigned)(nvalid * c.qks * SE), vb = (unsigned)(nvalid * c.vst * SE);
-        const __amdgpu_buffer_rsrc_t rk = rsrc(P.k, rb), rq = rsrc(P.q, rb), rkn = rsrc(P.kn, rb),
-                                     rqn = rsrc(P.qn, rb), rv = rsrc(P.v, vb), rvn = rsrc(P.vn, vb),
-                                     rr = rsrc(P.rec, (unsigned)Rc::BYTES);
+        const int tw = rank;
+        const Rsrcs r = rsrcs(P, c, nvalid);
 #pragma unroll
-        for (int s = 0; s < NTBW; ++s)
-            if (tw + TW * s < NB) {
+        for (int u = 0; u < OPS; ++u)
 #pragma unroll
-                for (int u = 0; u < KPL; ++u) f.kb[s][u] = bload(rk, of.k[s][u]);
-            }
+            for (int si = 0; si < 4; ++si) f.rb[si][u] = bload(r.r[si], of.rg[u]);
 #pragma unroll
-        for (int u = 0; u < OPS; ++u) {
-            f.ob[0][u] = bload(rq, of.o[u]);
-            f.ob[1][u] = bload(rkn, of.o[u]);
-            f.ob[2][u] = bload(rqn, of.o[u]);
-        }
+        for (int u = 0; u < VPL; ++u) f.vb[u] = bload(v_base(tw, u) >= VPS ? r.v[1] : r.v[0], of.vg[u]);
 #pragma unroll
-        for (int u = 0; u < VPL; ++u)
-            if (VPS % TT == 0 || lt + TT * u < VPS) {
-                f.vb[0][u] = bload(rv, of.v[u]);
-                f.vb[1][u] = bload(rvn, of.v[u]);
-            }
-#pragma unroll
-        for (int u = 0; u < MPL; ++u) f.mb[u] = bload(rr, (unsigned)(16 * (lt + TT * u)));
-        f.fb = bload(rr, (unsigned)(Rc::OFF_EG + 16 * (lt < FCH ? lt : 0)));
+        for (int u = 0; u < RPL; ++u) f.mb[u] = bload(r.m, of.mg[u]);
+        f.fb = bload(r.m, of.fg);
     }
 
-    // Stage the fetched block into set p.  With NEXT, each register is refilled with the
-    // matching chunk of the block at Pn right after it is written, so the next block's
-    // loads are in flight for a whole block step; nvalid_n = 0 makes them read nothing.
-    template <bool NEXT>
-    __device__ __forceinline__ void stage_impl(int p, Fetched &f, const Ptrs &Pn, int nvalid_n, const Chain &c,
+    // Stage the fetched block into set p, refilling each register with the matching
+    // chunk of the block at Pn right after it is written (nvalid_n = 0: nothing), so
+    // the next block's loads are in flight while the current ones are consumed.
+    __device__ __forceinline__ void stage_next(int p, Fetched &f, const Ptrs &Pn, int nvalid_n, const Chain &c,
                                                const Offs &of) const
     {
-        const int lt = tid - 64 * TW0, tw = wave - TW0;
-        const unsigned rbn = (unsigned)(nvalid_n * c.qks * SE), vbn = (unsigned)(nvalid_n * c.vst * SE);
-        const __amdgpu_buffer_rsrc_t rk = rsrc(Pn.k, rbn), rq = rsrc(Pn.q, rbn), rkn = rsrc(Pn.kn, rbn),
-                                     rqn = rsrc(Pn.qn, rbn), rv = rsrc(Pn.v, vbn), rvn = rsrc(Pn.vn, vbn),
-                                     rr = rsrc(Pn.rec, nvalid_n > 0 ? (unsigned)Rc::BYTES : 0u);
+        const int tw = rank;
+        const Rsrcs r = rsrcs(Pn, c, nvalid_n);
+        const unsigned rset = (unsigned)ROWS_B;
 #pragma unroll
-        for (int s = 0; s < NTBW; ++s) {
-            const int tb = tw + TW * s;
-            if (tb < NB) {
+        for (int u = 0; u < OPS; ++u)
 #pragma unroll
-                for (int u = 0; u < KPL; ++u) {
-                    const int ch = lane + 64 * u, t = 16 * tb + ch / CPR, cc = ch % CPR;
-                    *reinterpret_cast<u32x4 *>(rows(p, 0) + t * RS + cc * EPC) = to_operand<In, E>(f.kb[s][u]);
-                    if (NEXT) f.kb[s][u] = bload(rk, of.k[s][u]);
-                }
+            for (int si = 0; si < 4; ++si) {
+                st16(p, of.rl[u] + (of.rl[u] >= (unsigned)OFF_DUMMY ? 0u : si * rset), to_operand<In, E>(f.rb[si][u]));
+                f.rb[si][u] = bload(r.r[si], of.rg[u]);
             }
-        }
-#pragma unroll
-        for (int u = 0; u < OPS; ++u) {
-            const int ch = lt + TT * u, t = ch / CPR, cc = ch % CPR;
-#pragma unroll
-            for (int si = 0; si < 3; ++si) {
-                *reinterpret_cast<u32x4 *>(rows(p, 1 + si) + t * RS + cc * EPC) = to_operand<In, E>(f.ob[si][u]);
-                if (NEXT) f.ob[si][u] = bload(si == 0 ? rq : si == 1 ? rkn : rqn, of.o[u]);
-            }
-        }
 #pragma unroll
         for (int u = 0; u < VPL; ++u) {
-            const int ch = lt + TT * u;
-            if (VPS % TT == 0 || ch < VPS) {
-                const int t = ch / VCPR, cc = ch % VCPR;
-                *reinterpret_cast<u32x4 *>(vs(p, 0) + t * VS + cc * EPC) = f.vb[0][u];
-                *reinterpret_cast<u32x4 *>(vs(p, 1) + t * VS + cc * EPC) = f.vb[1][u];
-                if (NEXT) {
-                    f.vb[0][u] = bload(rv, of.v[u]);
-                    f.vb[1][u] = bload(rvn, of.v[u]);
-                }
-            }
+            st16(p, of.vl[u], f.vb[u]);
+            f.vb[u] = bload(v_base(tw, u) >= VPS ? r.v[1] : r.v[0], of.vg[u]);
         }
 #pragma unroll
-        for (int u = 0; u < MPL; ++u) {
-            const int ch = lt + TT * u;
-            const int m = ch / (LP * MCPR), rr2 = (ch / MCPR) % LP, cc = ch % MCPR;
-            *reinterpret_cast<u32x4 *>(tm(p, m) + rr2 * TS + cc * EPC) = f.mb[u];
-            if (NEXT) f.mb[u] = bload(rr, (unsigned)(16 * ch));
+        for (int u = 0; u < RPL; ++u) {
+            st16(p, of.ml[u], f.mb[u]);
+            f.mb[u] = bload(r.m, of.mg[u]);
         }
-        if (lt < FCH) {
-            // chunk lt holds floats 4 lt .. 4 lt + 3 of [eG | dG | eGn]
-            const int e = 4 * lt, m = e / LP, i = e % LP;
-            *reinterpret_cast<u32x4 *>(fac(p, m) + i) = f.fb;
-        }
-        if (NEXT) f.fb = bload(rr, (unsigned)(Rc::OFF_EG + 16 * (lt < FCH ? lt : 0)));
-        // fp32 operands: K^T of this wave's t-blocks, from the rows it has just written
-        // (LDS operations of one wave complete in order, so no barrier is needed)
-#pragma unroll
-        for (int s = 0; s < NTBW; ++s) {
-            const int tb = tw + TW * s;
-            if (!TR && tb < NB) {
-#pragma unroll
-                for (int u = 0; u < DK / 16; ++u) {
-                    const int qd = lane + 64 * u, kk = qd % DK, g4 = qd / DK;
-                    const E *src = rows(p, 0) + (16 * tb + 4 * g4) * RS + kk;
-                    QE v;
-                    v[0] = src[0];
-                    v[1] = src[RS];
-                    v[2] = src[2 * RS];
-                    v[3] = src[3 * RS];
-                    st_quad(kt(p) + kk * TS + 16 * tb + 4 * g4, v);
-                }
-            }
-        }
-    }
-    __device__ __forceinline__ void stage(int p, Fetched &f, const Chain &c, const Offs &of) const
-    {
-        stage_impl<false>(p, f, c.p0, 0, c, of);
+        st16(p, of.fl, f.fb);
+        f.fb = bload(r.m, of.fg);
     }
 
     // ------------------------------------------------------------------ helpers
     __device__ __forceinline__ f32x4 ld4f(const float *p) const { return *reinterpret_cast<const f32x4 *>(p); }
 
-    // X = R S for the NB row tiles of row set R (rows(p, i)), state operand quads sq.
-    __device__ __forceinline__ void x_rows(f32x4 (&x)[NB], const E *R, const QE (&sq)[DKB]) const
+    // X = R S for the NB row tiles of row set R and NC column halves (state operand
+    // quads sq[c]); each A quad is read once for all halves.
+    template <int NC>
+    __device__ __forceinline__ void x_rows(f32x4 (&x)[NB][NC], const E *R, const QE (&sq)[NC][DKB]) const
     {
 #pragma unroll
         for (int rb = 0; rb < NB; ++rb) {
             QE a[DKB];
             ld_quads<E, DKB>(a, R + 16 * rb * RS, RS, lane);
-            x[rb] = mma_q<E, DKB>(f32x4{0.f, 0.f, 0.f, 0.f}, a, sq);
+#pragma unroll
+            for (int c = 0; c < NC; ++c) x[rb][c] = mma_q<E, DKB>(f32x4{0.f, 0.f, 0.f, 0.f}, a, sq[c]);
         }
     }
 
-    // D = V - diag(G) X (column half bc), as B-operand quads.
-    __device__ __forceinline__ void d_quads(QE (&dq)[NB], const f32x4 (&x)[NB], const In *V, const float *G,
-                                            int bc) const
+    // D = V - diag(G) X (column halves bc0 .. bc0 + NC - 1), as B-operand quads.
+    template <int NC>
+    __device__ __forceinline__ void d_quads(QE (&dq)[NC][NB], const f32x4 (&x)[NB][NC], const In *V, const float *G,
+                                            int bc0) const
     {
         const int g = lane >> 4, n = lane & 15;
 #pragma unroll
         for (int rb = 0; rb < NB; ++rb) {
             const int r = 16 * rb + 4 * g;
             const f32x4 gq = ld4f(G + r);
-            const In *vp = V + r * VS + 16 * bc + n;
-            f32x4 d;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) d[i] = to_f(vp[i * VS]) - gq[i] * x[rb][i];
-            dq[rb] = quad_of<E>(d);
+            for (int c = 0; c < NC; ++c) {
+                const In *vp = V + r * VS + 16 * (bc0 + c) + n;
+                f32x4 d;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) d[i] = to_f(vp[i * VS]) - gq[i] * x[rb][c][i];
+                dq[c][rb] = quad_of<E>(d);
+            }
         }
     }
 
-    // Y = M Z for a record matrix M (LP x LP, rows(p)) and B-operand quads zq.
-    __device__ __forceinline__ void m_times(f32x4 (&y)[NB], const E *M, const QE (&zq)[NB], const f32x4 (&init)[NB]) const
+    // Y = M Z + init for a record matrix M (LP x LP) and B-operand quads zq[c].
+    template <int NC>
+    __device__ __forceinline__ void m_times(f32x4 (&y)[NB][NC], const E *M, const QE (&zq)[NC][NB],
+                                            const f32x4 (&init)[NB][NC]) const
     {
 #pragma unroll
         for (int rb = 0; rb < NB; ++rb) {
             QE a[NB];
             ld_quads<E, NB>(a, M + 16 * rb * TS, TS, lane);
-            y[rb] = mma_q<E, NB>(init[rb], a, zq);
+#pragma unroll
+            for (int c = 0; c < NC; ++c) y[rb][c] = mma_q<E, NB>(init[rb][c], a, zq[c]);
         }
     }
 
-    __device__ __forceinline__ void store_out(Out *dst, int stride, int nvalid, int bc, const f32x4 (&acc)[NB],
+    // Rows at or past nvalid fall outside the store resource and are dropped.
+    template <int NC>
+    __device__ __forceinline__ void store_out(Out *dst, int stride, int nvalid, int bc0, const f32x4 (&acc)[NB][NC],
                                               float scale) const
     {
+        constexpr int SO = (int)sizeof(Out);
+        const __amdgpu_buffer_rsrc_t r = rsrc(dst, (unsigned)(nvalid * stride * SO));
         const int g = lane >> 4, n = lane & 15;
 #pragma unroll
-        for (int rb = 0; rb < NB; ++rb) {
-            const int r = 16 * rb + 4 * g;
+        for (int rb = 0; rb < NB; ++rb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                if (r + i < nvalid) dst[(r + i) * stride + 16 * bc + n] = to_e<Out>(acc[rb][i] * scale);
-        }
+            for (int c = 0; c < NC; ++c)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int off = ((16 * rb + 4 * g + i) * stride + 16 * (bc0 + c) + n) * SO;
+                    const Out v = to_e<Out>(acc[rb][c][i] * scale);
+                    if constexpr (SO == 4)
+                        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, off, 0, 0);
+                    else
+                        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, v), r, off, 0, 0);
+                }
     }
 
     __device__ __forceinline__ void write_st(int b, const QE (&sq)[DKB], int bc) const
@@ -393,7 +411,11 @@ struct Scan {
                 a[rb] = __builtin_bit_cast(QE, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                                                    (__attribute__((address_space(3))) s16x4 *)(base + 16 * rb * RS)));
         } else {
-            ld_quads<E, NB>(a, kt(p) + 16 * kb * TS, TS, lane);
+            const E *src = rows(p, 0) + 4 * (lane >> 4) * RS + 16 * kb + (lane & 15);
+#pragma unroll
+            for (int rb = 0; rb < NB; ++rb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) a[rb][i] = src[(16 * rb + i) * RS];
         }
     }
 
@@ -403,18 +425,19 @@ struct Scan {
     __device__ __forceinline__ void c_block(int p, int db, int bc, f32x4 (&S)[DKB], QE (&sq)[DKB]) const
     {
         const int g = lane >> 4, n = lane & 15;
-        const f32x4 z[NB] = {};
-        f32x4 x[NB];
-        x_rows(x, rows(p, 0), sq);
-        QE dq[NB];
-        d_quads(dq, x, vs(p, 0), fac(p, 0), bc);
-        f32x4 dl[NB];
-        m_times(dl, tm(p, 0), dq, z);
+        const f32x4 z[NB][1] = {};
+        const QE(&sq1)[1][DKB] = *reinterpret_cast<const QE(*)[1][DKB]>(&sq);
+        f32x4 x[NB][1];
+        x_rows<1>(x, rows(p, 0), sq1);
+        QE dq[1][NB];
+        d_quads<1>(dq, x, vs(p, 0), fac(p, 0), bc);
+        f32x4 dl[NB][1];
+        m_times<1>(dl, tm(p, 0), dq, z);
         QE uq[NB];
 #pragma unroll
         for (int rb = 0; rb < NB; ++rb) {
-            st_quad(dt(db) + (16 * bc + n) * TS + 16 * rb + 4 * g, quad_of<E>(dl[rb]));
-            uq[rb] = quad_of<E>(dl[rb] * ld4f(fac(p, 1) + 16 * rb + 4 * g));
+            st_quad(dt(db) + (16 * bc + n) * TS + 16 * rb + 4 * g, quad_of<E>(dl[rb][0]));
+            uq[rb] = quad_of<E>(dl[rb][0] * ld4f(fac(p, 1) + 16 * rb + 4 * g));
         }
         const float decay = fac(p, 0)[LP - 1];
 #pragma unroll
@@ -426,67 +449,75 @@ struct Scan {
         }
     }
 
-    // N: the noisy block for column half bc, from the state operand in st(sb).
-    __device__ __forceinline__ void n_block(int p, int sb, int bc, Out *on, int stride, int nvalid,
-                                            float scale) const
+    // N and O: one wave per column half
+    static constexpr int NCP = 1;
+
+    // N: the noisy block for column half C0 from the state operand in st(sb).
+    __device__ __forceinline__ void n_block(int p, int sb, int C0, Out *on, int stride, int nvalid, float scale) const
     {
-        const f32x4 z[NB] = {};
-        QE sq[DKB];
-        ld_quads<E, DKB>(sq, st(sb) + 16 * bc * RS, RS, lane);
-        f32x4 x3[NB], x4[NB];
-        x_rows(x3, rows(p, 2), sq);
-        x_rows(x4, rows(p, 3), sq);
-        QE dq[NB];
-        d_quads(dq, x3, vs(p, 1), fac(p, 2), bc);
-        f32x4 dn[NB];
-        m_times(dn, tm(p, 1), dq, z);
-        QE nq[NB];
+        const f32x4 z[NB][NCP] = {};
+        QE sq[NCP][DKB];
+#pragma unroll
+        for (int c = 0; c < NCP; ++c) ld_quads<E, DKB>(sq[c], st(sb) + 16 * (C0 + c) * RS, RS, lane);
+        f32x4 x3[NB][NCP], x4[NB][NCP];
+        x_rows<NCP>(x3, rows(p, 2), sq);
+        x_rows<NCP>(x4, rows(p, 3), sq);
+        QE dq[NCP][NB];
+        d_quads<NCP>(dq, x3, vs(p, 1), fac(p, 2), C0);
+        f32x4 dn[NB][NCP];
+        m_times<NCP>(dn, tm(p, 1), dq, z);
+        QE nq[NCP][NB];
         const float gn_end = fac(p, 2)[LP - 1];
 #pragma unroll
-        for (int rb = 0; rb < NB; ++rb) {
-            nq[rb] = quad_of<E>(dn[rb]);
-            x4[rb] *= gn_end;
-        }
-        f32x4 o[NB];
-        m_times(o, tm(p, 3), nq, x4);
-        store_out(on, stride, nvalid, bc, o, scale);
+        for (int rb = 0; rb < NB; ++rb)
+#pragma unroll
+            for (int c = 0; c < NCP; ++c) {
+                nq[c][rb] = quad_of<E>(dn[rb][c]);
+                x4[rb][c] *= gn_end;
+            }
+        f32x4 o[NB][NCP];
+        m_times<NCP>(o, tm(p, 3), nq, x4);
+        store_out<NCP>(on, stride, nvalid, C0, o, scale);
     }
 
-    // O, first half: X2 scaled by eG and the P quads of the current block, kept until
+    // O, first half: X2 scaled by eG for column half bc, and the P quads, kept until
     // Delta is published.
-    __device__ __forceinline__ void o_begin(int p, int sb, int bc, f32x4 (&x2)[NB], QE (&pq)[NB][NB]) const
+    __device__ __forceinline__ void o_begin(int p, int sb, int bc, f32x4 (&x2)[NB][1], QE (&pq)[NB][NB]) const
     {
         const int g = lane >> 4;
-        QE sq[DKB];
-        ld_quads<E, DKB>(sq, st(sb) + 16 * bc * RS, RS, lane);
-        x_rows(x2, rows(p, 1), sq);
+        QE sq[1][DKB];
+        ld_quads<E, DKB>(sq[0], st(sb) + 16 * bc * RS, RS, lane);
+        x_rows<1>(x2, rows(p, 1), sq);
 #pragma unroll
         for (int rb = 0; rb < NB; ++rb) {
-            x2[rb] *= ld4f(fac(p, 0) + 16 * rb + 4 * g);
+            x2[rb][0] *= ld4f(fac(p, 0) + 16 * rb + 4 * g);
             ld_quads<E, NB>(pq[rb], tm(p, 2) + 16 * rb * TS, TS, lane);
         }
     }
 
     // O, second half: O = s (X2 + P Delta) with Delta^T from dt(db).
-    __device__ __forceinline__ void o_end(int db, int bc, const f32x4 (&x2)[NB], const QE (&pq)[NB][NB], Out *o,
+    __device__ __forceinline__ void o_end(int db, int bc, const f32x4 (&x2)[NB][1], const QE (&pq)[NB][NB], Out *o,
                                           int stride, int nvalid, float scale) const
     {
-        QE dq[NB];
-        ld_quads<E, NB>(dq, dt(db) + 16 * bc * TS, TS, lane);
-        f32x4 acc[NB];
+        QE dq[1][NB];
+        ld_quads<E, NB>(dq[0], dt(db) + 16 * bc * TS, TS, lane);
+        f32x4 acc[NB][1];
 #pragma unroll
-        for (int rb = 0; rb < NB; ++rb) acc[rb] = mma_q<E, NB>(x2[rb], pq[rb], dq);
-        store_out(o, stride, nvalid, bc, acc, scale);
+        for (int rb = 0; rb < NB; ++rb) acc[rb][0] = mma_q<E, NB>(x2[rb][0], pq[rb], dq[0]);
+        store_out<1>(o, stride, nvalid, bc, acc, scale);
     }
 
     // ------------------------------------------------------------------ the chain
+    // Waves by the layout table: C, N, O (column half = rank), L.  With one
+    // staging set, L stages each block in a phase of its own (the other waves wait at
+    // a barrier) and C publishes the state operand in that phase.
     __device__ void run(const Chain &c) const
     {
         const int nb = (int)((c.len + c.L - 1) / c.L);
         const int g = lane >> 4, n = lane & 15;
-        if (wave < 2) {
+        if (role == R_C) {
             // ---- C
-            const int bc = wave;
+            const int bc = rank;
             f32x4 S[DKB];
             QE sq[DKB];
 #pragma unroll
@@ -501,27 +532,14 @@ struct Scan {
                 sq[kb] = quad_of<E>(acc);
             }
             wait_global_loads();
-            Fetched f;
-            Offs of;
-            if (!DBUF || wave >= TW0) make_offs(c, of);
-            Ptrs pf = c.p0;
-            if (DBUF)
-                write_st(0, sq, bc);
-            else if (nb > 0)
-                fetch(pf, c, nvalid_of(c, 0), of, f);
+            if (DBUF) write_st(0, sq, bc);
             lds_barrier();
             for (int j = 0; j < nb; ++j) {
-                const int p = DBUF ? (j & 1) : 0;
                 if (!DBUF) {
-                    stage(0, f, c, of);
                     write_st(0, sq, bc);
                     lds_barrier();
-                    if (j + 1 < nb) {
-                        advance(pf, c);
-                        fetch(pf, c, nvalid_of(c, j + 1), of, f);
-                    }
                 }
-                c_block(p, j & 1, bc, S, sq);
+                c_block(DBUF ? (j & 1) : 0, j & 1, bc, S, sq);
                 if (DBUF) write_st((j + 1) & 1, sq, bc);
                 lds_barrier();
             }
@@ -533,88 +551,86 @@ struct Scan {
                     for (int i = 0; i < 4; ++i) dst[i * c.dv] = S[kb][i];
                 }
             }
-        } else if (wave < 4) {
+        } else if (role == R_N) {
             // ---- N
-            const int bc = wave - 2;
-            Fetched f;
-            Offs of;
-            if (!DBUF || wave >= TW0) make_offs(c, of);
-            Ptrs pf = c.p0, pc = c.p0;
-            if (!DBUF && nb > 0) fetch(pf, c, nvalid_of(c, 0), of, f);
+            const int bc = rank;
+            Ptrs pc = c.p0;
             lds_barrier();
             for (int j = 0; j < nb; ++j) {
-                const int p = DBUF ? (j & 1) : 0;
-                if (!DBUF) {
-                    stage(0, f, c, of);
-                    lds_barrier();
-                    if (j + 1 < nb) {
-                        advance(pf, c);
-                        fetch(pf, c, nvalid_of(c, j + 1), of, f);
-                    }
-                }
-                n_block(p, DBUF ? (j & 1) : 0, bc, pc.on, c.vst, nvalid_of(c, j), c.scale);
+                if (!DBUF) lds_barrier();
+                n_block(DBUF ? (j & 1) : 0, DBUF ? (j & 1) : 0, bc, pc.on, c.vst, nvalid_of(c, j), c.scale);
                 advance(pc, c);
                 lds_barrier();
             }
-        } else if (wave < 6) {
+        } else if (role == R_O) {
             // ---- O
-            const int bc = wave - 4;
-            Fetched f;
-            Offs of;
-            if (!DBUF || wave >= TW0) make_offs(c, of);
-            Ptrs pf = c.p0, pc = c.p0;
-            f32x4 x2[NB];
+            const int bc = rank;
+            Ptrs pc = c.p0;
+            f32x4 x2[NB][1];
             QE pq[NB][NB];
-            if (!DBUF && nb > 0) fetch(pf, c, nvalid_of(c, 0), of, f);
             lds_barrier();
             for (int j = 0; j < nb; ++j) {
-                const int p = DBUF ? (j & 1) : 0;
-                if (!DBUF) {
-                    stage(0, f, c, of);
-                    lds_barrier();
-                    if (j + 1 < nb) {
-                        advance(pf, c);
-                        fetch(pf, c, nvalid_of(c, j + 1), of, f);
-                    }
-                }
+                if (!DBUF) lds_barrier();
                 if (j > 0) {
                     o_end((j - 1) & 1, bc, x2, pq, pc.o, c.vst, nvalid_of(c, j - 1), c.scale);
                     advance(pc, c);
                 }
-                o_begin(p, DBUF ? (j & 1) : 0, bc, x2, pq);
+                o_begin(DBUF ? (j & 1) : 0, DBUF ? (j & 1) : 0, bc, x2, pq);
                 lds_barrier();
             }
             if (nb > 0) o_end((nb - 1) & 1, bc, x2, pq, pc.o, c.vst, nvalid_of(c, nb - 1), c.scale);
         } else {
             // ---- L
-            Fetched f;
             Offs of;
-            if (!DBUF || wave >= TW0) make_offs(c, of);
-            Ptrs pf = c.p0;
-            if (nb > 0) {
-                fetch(pf, c, nvalid_of(c, 0), of, f);
-                if (DBUF) {
-                    stage(0, f, c, of);
+            make_offs(c, of);
+            Ptrs pf = c.p0;   // next block to load
+            auto nv = [&](int jj) { return jj < nb ? nvalid_of(c, jj) : 0; };
+            if constexpr (DBUF && SE == 4) {
+                // fp32: step j stages block j + 1 and loads block j + 2
+                Fetched f;
+                fetch(pf, c, nv(0), of, f);
+                advance(pf, c);
+                if (nb > 0) stage_next(0, f, pf, nv(1), c, of);
+                advance(pf, c);
+                lds_barrier();
+                for (int j = 0; j < nb; ++j) {
+                    if (j + 1 < nb) stage_next((j + 1) & 1, f, pf, nv(j + 2), c, of);
                     advance(pf, c);
-                    if (nb > 1) fetch(pf, c, nvalid_of(c, 1), of, f);
-                    advance(pf, c);
+                    lds_barrier();
                 }
-            }
-            lds_barrier();
-            for (int j = 0; j < nb; ++j) {
-                if (DBUF) {
-                    // stage block j + 1, load block j + 2 (pf)
-                    if (j + 1 < nb) stage_impl<true>((j + 1) & 1, f, pf, j + 2 < nb ? nvalid_of(c, j + 2) : 0, c, of);
+            } else if constexpr (DBUF) {
+                // step j stages block j + 1 from f[(j + 1) & 1] and loads block j + 3 into it:
+                // two blocks of loads in flight
+                Fetched f0, f1;
+                fetch(pf, c, nv(0), of, f0);
+                advance(pf, c);
+                fetch(pf, c, nv(1), of, f1);
+                advance(pf, c);
+                if (nb > 0) stage_next(0, f0, pf, nv(2), c, of);   // block 0; f0 <- block 2
+                advance(pf, c);
+                lds_barrier();
+                for (int j = 0; j < nb; j += 2) {
+                    if (j + 1 < nb) stage_next(1, f1, pf, nv(j + 3), c, of);
                     advance(pf, c);
-                } else {
-                    stage(0, f, c, of);
                     lds_barrier();
                     if (j + 1 < nb) {
+                        if (j + 2 < nb) stage_next(0, f0, pf, nv(j + 4), c, of);
                         advance(pf, c);
-                        fetch(pf, c, nvalid_of(c, j + 1), of, f);
+                        lds_barrier();
                     }
                 }
+            } else {
+                // one set: step j stages block j in a phase of its own, loading block j + 1
+                Fetched f;
+                fetch(pf, c, nv(0), of, f);
+                advance(pf, c);
                 lds_barrier();
+                for (int j = 0; j < nb; ++j) {
+                    stage_next(0, f, pf, nv(j + 1), c, of);
+                    advance(pf, c);
+                    lds_barrier();
+                    lds_barrier();
+                }
             }
         }
     }
