@@ -67,36 +67,63 @@ def time_launches(fn, steps, warmup, stream):
     return start.elapsed_time(end) / steps  # ms per launch
 
 
-def cpu_baseline(w, inp, max_units=None):
-    """The fp64 oracle on a bounded sample of the workload: whole sequences of one
-    (sequence, v-head) unit per host thread."""
+def cpu_baseline(w, inp):
+    """The fp64 oracle over the whole workload (every (sequence, v-head) unit, clean and
+    noisy streams), its units spread over up to 16 host threads."""
     import oracle
     threads = max(1, min(os.cpu_count() or 1, 16))
     oracle.set_threads(threads)
-    units = threads if max_units is None else min(threads, max_units)
-    b_idx = [u % w.batch for u in range(units)]
-    h_idx = [u // w.batch for u in range(units)]
     keys = ("q", "k", "v", "g", "beta")
-
-    def sl(t, b, h):
-        return t[b:b + 1, :, h:h + 1]
-    import numpy as np
-    cat = {}
-    for key in keys:
-        for sfx in ("", "n"):
-            t = inp[key + sfx]
-            parts = [sl(t, b, h) for b, h in zip(b_idx, h_idx)]
-            cat[key + sfx] = np.concatenate([p.double().numpy() for p in parts], axis=0)
+    arr = {k: inp[k].double().numpy() for k in inp}
     t0 = time.perf_counter()
-    oracle.fwd_train(*[cat[k] for k in keys], *[cat[k + "n"] for k in keys],
+    oracle.fwd_train(*[arr[k] for k in keys], *[arr[k + "n"] for k in keys],
                      block=w.block, scale=1.0 / math.sqrt(w.d_k), want_ht=False)
     dt = time.perf_counter() - t0
-    tokens = 2 * units * w.seqlen
+    tokens = 2 * w.tokens
     return {"value": tokens / dt, "unit": "tokens/s", "cores": oracle.max_threads(),
             "kind": "oracle", "seconds": dt,
-            "sample": f"{units} (sequence, v-head) units x {w.seqlen} clean + {w.seqlen} noisy "
-                      f"tokens of the same workload (one unit per thread); value = "
-                      f"tokens of the sample / wall time"}
+            "sample": f"the whole workload: {w.batch} sequences x {w.h_v} v-heads x "
+                      f"({w.seqlen} clean + {w.seqlen} noisy) tokens in fp64; value = tokens / wall time"}
+
+
+def kernel_source_hash():
+    """Hash of the HIP sources, to tell whether a recorded counter measurement still
+    describes the kernels being timed."""
+    import hashlib
+    h = hashlib.sha256()
+    src = os.path.join(ROOT, "paper_2606_01774_amd", "csrc")
+    for name in sorted(os.listdir(src)):
+        if name.endswith((".hip", ".hpp")):
+            with open(os.path.join(src, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic():
+    """HBM bytes per forward step from the FETCH_SIZE / WRITE_SIZE counter runs recorded
+    under profiles/ (copy-calibrated), or None when the kernels have changed since."""
+    path = os.path.join(ROOT, "profiles", "traffic_train_bf16_b4_t4096_h16_d128_l32.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except OSError:
+        return None
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    return rec.get("bytes_per_step")
+
+
+def copy_probe(steps):
+    """A plain device-to-device copy of 256 MiB, the reference for scaling the byte
+    counters (its true traffic is 256 MiB read + 256 MiB written per launch)."""
+    import torch
+    n = 256 * 1024 * 1024 // 4
+    x = torch.ones(n, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(steps):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n * 4, "launches": steps}))
 
 
 def main():
@@ -106,11 +133,17 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-serve", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run only a 256 MiB device copy (byte-counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
+
+    if args.copy_probe:
+        copy_probe(args.steps)
+        return
 
     import torch
 
@@ -153,9 +186,9 @@ def main():
                    "inputs": "bf16", "mfma_operands": "fp16", "state": "fp32", "outputs": "fp32",
                    "route": "fused (UT records + scan)", "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": recorded_traffic(),
                      "kernel": "bdgdn_fwd_train step = bdgdn_k1_intra_kernel + bdgdn_k2_scan_kernel",
-                     "algorithmic_bytes": abytes},
+                     "algorithmic_bytes": abytes, "kernel_source_hash": kernel_source_hash()},
         "mfma": {"model_flop": flops, "tflops": flops / (ms * 1e-3) / 1e12,
                  "frac_of_peak": flops / (ms * 1e-3) / 1e12 / MFMA16_PEAK_TFLOPS},
     }
