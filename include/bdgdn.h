@@ -75,17 +75,25 @@ typedef enum { BDGDN_BF16 = 0, BDGDN_F32 = 1 } bdgdn_dtype_t;
 
 /* How the training forward is scheduled; every route gives the same result up to
  * floating-point summation order.
- *  FUSED:   two kernels.  The block-local UT transform and masked Q K^T of every
- *           (block, v-head) are computed in parallel into the workspace; then one
- *           workgroup per (sequence, v-head, d_v tile) scans the blocks in order with
- *           the clean state on chip and evaluates each noisy block from the in-register
- *           boundary state (the fused two-stream schedule, Appendix "Route II").  Needs
- *           a workspace.
+ *  FUSED:   the fused two-stream schedule (Appendix "Route II"): one workgroup per
+ *           (sequence, v-head, d_v tile) scans the blocks in order with the clean state
+ *           on chip and evaluates each noisy block from the in-register boundary state.
+ *           With bf16 inputs and blocks of at most 32 positions this is one kernel whose
+ *           workgroups also compute each block's UT transform and masked Q K^T a block
+ *           ahead (no workspace); otherwise it is the RECORDS schedule.
  *  SPLIT:   boundary states through HBM and a separate noisy-block kernel (Appendix
  *           "Route I").  Not available in this version (BDGDN_ERR_UNSUPPORTED).
  *  ONEPASS: one kernel per (sequence, v-head, d_v tile) that recomputes the UT
- *           transform of each block itself.  No workspace. */
-typedef enum { BDGDN_ROUTE_FUSED = 0, BDGDN_ROUTE_SPLIT = 1, BDGDN_ROUTE_ONEPASS = 2 } bdgdn_route_t;
+ *           transform of each block itself, without overlap.  No workspace.
+ *  RECORDS: two kernels: the UT transform and masked Q K^T of every (block, v-head)
+ *           in parallel into the workspace, then the scan of FUSED reading them.
+ *           Needs a workspace (bdgdn_fwd_train_workspace). */
+typedef enum {
+    BDGDN_ROUTE_FUSED = 0,
+    BDGDN_ROUTE_SPLIT = 1,
+    BDGDN_ROUTE_ONEPASS = 2,
+    BDGDN_ROUTE_RECORDS = 3
+} bdgdn_route_t;
 
 typedef struct {
     int32_t batch;     /* B sequences; must be 1 when packed (num_seqs > 0)            */
@@ -115,8 +123,8 @@ int32_t bdgdn_version(void);
 /* Human-readable text of a status code (static storage). */
 const char *bdgdn_status_string(int status);
 
-/* Bytes of device workspace bdgdn_fwd_train needs for this descriptor (0 for the
- * fused route), or 0 for a descriptor that bdgdn_fwd_train would reject. */
+/* Bytes of device workspace bdgdn_fwd_train needs for this descriptor (0 when the
+ * route runs without one), or 0 for a descriptor that bdgdn_fwd_train would reject. */
 size_t bdgdn_fwd_train_workspace(const bdgdn_fwd_desc_t *desc);
 
 /*

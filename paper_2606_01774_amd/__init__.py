@@ -20,7 +20,7 @@ import torch
 
 __all__ = [
     "BdgdnError", "BDGDN_BF16", "BDGDN_F32", "BDGDN_ROUTE_FUSED", "BDGDN_ROUTE_SPLIT",
-    "BDGDN_ROUTE_ONEPASS",
+    "BDGDN_ROUTE_ONEPASS", "BDGDN_ROUTE_RECORDS",
     "bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace", "bdgdn_fwd_train",
     "bdgdn_denoise_step", "bdgdn_commit", "library_path", "load_library", "EXPORTED_SYMBOLS",
 ]
@@ -39,6 +39,7 @@ BDGDN_F32 = 1
 BDGDN_ROUTE_FUSED = 0
 BDGDN_ROUTE_SPLIT = 1
 BDGDN_ROUTE_ONEPASS = 2
+BDGDN_ROUTE_RECORDS = 3
 
 EXPORTED_SYMBOLS = ("bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace",
                     "bdgdn_fwd_train", "bdgdn_denoise_step", "bdgdn_commit")

@@ -50,7 +50,8 @@ int check_fwd(const bdgdn_fwd_desc_t *d, const int32_t *cu_dev, const int32_t *c
     int st = check_heads(d->h_qk, d->h_v, d->d_k, d->d_v, d->block, d->scale, d->dtype, d->out_dtype);
     if (st != BDGDN_OK) return st;
     if (d->batch <= 0 || d->seqlen < 0 || d->num_seqs < 0) return BDGDN_ERR_INVALID_ARG;
-    if (d->route != BDGDN_ROUTE_FUSED && d->route != BDGDN_ROUTE_SPLIT && d->route != BDGDN_ROUTE_ONEPASS)
+    if (d->route != BDGDN_ROUTE_FUSED && d->route != BDGDN_ROUTE_SPLIT && d->route != BDGDN_ROUTE_ONEPASS &&
+        d->route != BDGDN_ROUTE_RECORDS)
         return BDGDN_ERR_INVALID_ARG;
     if ((long)d->batch * d->seqlen > 0x7fffffffL) return BDGDN_ERR_UNSUPPORTED;
     const bool packed = d->num_seqs > 0;
@@ -94,11 +95,18 @@ static long total_blocks(const bdgdn_fwd_desc_t *d)
     return d->num_seqs > 0 ? nblk : nblk * d->batch;
 }
 
+// The fused route runs as one kernel where it can, else through the UT records.
+static bool one_kernel(const bdgdn_fwd_desc_t *d, Types ty)
+{
+    return d->route == BDGDN_ROUTE_FUSED && pipelined_supported(ty, d->d_k, lp_of(d->block));
+}
+
 static size_t workspace_bytes_of(const bdgdn_fwd_desc_t *d)
 {
-    if (d->route != BDGDN_ROUTE_FUSED) return 0;
+    if (d->route != BDGDN_ROUTE_FUSED && d->route != BDGDN_ROUTE_RECORDS) return 0;
     Types ty;
     types_of(d->dtype, d->out_dtype, ty);
+    if (one_kernel(d, ty)) return 0;
     return (size_t)total_blocks(d) * d->h_v * scan_record_bytes(ty, lp_of(d->block));
 }
 
@@ -150,7 +158,7 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         n_order = nseq;
     }
     hipError_t e;
-    if (desc->route == BDGDN_ROUTE_FUSED) {
+    if (desc->route == BDGDN_ROUTE_FUSED || desc->route == BDGDN_ROUTE_RECORDS) {
         IntraArgs ia;
         ia.q = q; ia.k = k; ia.qn = qn; ia.kn = kn;
         ia.g = g; ia.beta = beta; ia.gn = gn; ia.betan = betan;
@@ -161,6 +169,7 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         ia.h_qk = desc->h_qk; ia.h_v = desc->h_v;
         ScanArgs sa;
         sa.q = q; sa.k = k; sa.v = v; sa.qn = qn; sa.kn = kn; sa.vn = vn;
+        sa.g = g; sa.beta = beta; sa.gn = gn; sa.betan = betan;
         sa.cu = packed ? cu_seqlens_dev : nullptr;
         sa.h0 = h0; sa.ht = ht; sa.o = o; sa.on = on;
         sa.ws = static_cast<const unsigned char *>(workspace);
@@ -171,7 +180,8 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         sa.scale = desc->scale;
         sa.n_order = n_order;
         for (int i = 0; i < n_order; ++i) sa.order[i] = order[i];
-        e = launch_fwd_scan(ty, desc->d_k, lp, ia, sa, strm);
+        e = one_kernel(desc, ty) ? launch_fwd_pipelined(ty, desc->d_k, lp, sa, strm)
+                                 : launch_fwd_scan(ty, desc->d_k, lp, ia, sa, strm);
     } else {
         FwdArgs a;
         a.q = q; a.k = k; a.v = v; a.qn = qn; a.kn = kn; a.vn = vn;

@@ -1,0 +1,781 @@
+// fused.hpp -- the two-stream training forward of the block-diffusion Gated Delta Rule in
+// one kernel: the block-local UT transform (Appendix "Chunk-corrected values", eq. f-blk)
+// and the sequential state scan with the noisy blocks evaluated from the on-chip clean
+// boundary state (Appendix eq. chunk-state, eq. noisy-block-fwd; the fused schedule of
+// "Route II"), pipelined block by block inside one workgroup per (sequence or document,
+// v-head, 32-column tile of d_v).
+//
+// Per block (see scan.hpp for the scan's arithmetic):
+//   record:  G = cumulative log-gates, A_ri = beta_r 2^(G_r - G_i) (k_r . k_i) (i < r),
+//            T = (I + A)^(-1) diag(beta), and the noisy T~ from the noisy rows and gates;
+//   scan:    X = rows S0, D = V - diag(eG) X1, Delta = T D, O = diag(eG) Q S0 + P Delta with
+//            P_ri = 2^(G_r - G_i) (q_r . k_i) (i <= r), O~ from Delta~ and
+//            R_ri = 2^(G~_n - G~_i) (q~_r . k~_i), S <- gamma_n S0 + K^T diag(dG) Delta.
+//
+// Twelve waves in five roles; in step j of the chain
+//   C (waves 0, 1)   the recurrence of block j, one 16-column half each (state in registers)
+//   N (waves 2, 3)   the noisy block j, R included
+//   O (waves 4, 5)   the clean outputs of block j - 1; X2 and P of block j
+//   U (waves 6, 7)   the record of block j + 1: U0 the clean T and factors, U1 the noisy ones
+//   L (waves 8-11)   stage the rows of block j + 2 and the V tile of block j + 1
+// so nothing waits inside a step: one workgroup barrier per block.  Rows of a block live in
+// a three-slot ring (used by U one step before the scan); V, the record and the factors
+// in a two-slot set.  Rows are stored unpadded with their 16-byte chunks XOR-swizzled by
+// row, which keeps every LDS access pattern here free of bank conflicts in 3 x 32 KB.
+// The waves on the recurrence's critical path (C, U) run at a raised issue priority.
+#pragma once
+
+#include "intra.hpp"
+
+namespace bdgdn {
+
+#ifndef BDGDN_PRIO_C
+#define BDGDN_PRIO_C 3
+#endif
+#ifndef BDGDN_PRIO_N
+#define BDGDN_PRIO_N 1
+#endif
+#ifndef BDGDN_PRIO_O
+#define BDGDN_PRIO_O 1
+#endif
+#ifndef BDGDN_PRIO_U
+#define BDGDN_PRIO_U 3
+#endif
+#ifndef BDGDN_PRIO_L
+#define BDGDN_PRIO_L 2
+#endif
+
+template <typename Out, int DK, int LP>
+struct Fused {
+    typedef __bf16 In;
+    typedef _Float16 E;
+    typedef Quad<E> QE;
+    static constexpr int NW = 12, kThreads = 64 * NW;
+    static constexpr int BV = 32, NVB = 2;
+    static constexpr int NB = LP / 16, DKB = DK / 16;
+    static_assert(LP == 16 || LP == 32, "blocks of 16 or 32 positions");
+    static_assert(DK == 64 || DK == 128, "d_k of 64 or 128");
+    static constexpr int CPR = DK / 8;           // 16-byte chunks per row
+    static constexpr int RPB = 256 / (2 * DK);   // rows per 256 bytes (1 or 2)
+    static constexpr int TS = LP + 8;            // record matrices, Delta^T: [*][token] rows
+    static constexpr int VS = BV + 8;            // V [token][v]
+    // LDS layout
+    static constexpr int ROWS_B = LP * DK * 2;   // one row set (k, q, k~ or q~)
+    static constexpr int RING_B = 4 * ROWS_B;    // one ring slot
+    static constexpr int V_B = LP * VS * 2;
+    static constexpr int TM_B = al16(LP * TS * 2);
+    static constexpr int OFF_TM = 2 * V_B;
+    static constexpr int OFF_FAC = OFF_TM + 2 * TM_B;
+    static constexpr int NFAC = 5;
+    static constexpr int SET_B = OFF_FAC + NFAC * 64 * 4;
+    static constexpr int ST_B = BV * DK * 2;     // state operand [v][d_k], swizzled like rows
+    static constexpr int DT_B = al16(BV * TS * 2);
+    static constexpr int US_B = 2 * 64 * 4;      // per U wave: cumulative gates, beta
+    static constexpr int OFF_SET = 3 * RING_B;
+    static constexpr int OFF_ST = OFF_SET + 2 * SET_B;
+    static constexpr int OFF_DT = OFF_ST + 2 * ST_B;
+    static constexpr int OFF_US = OFF_DT + 2 * DT_B;
+    static constexpr int OFF_SINK = OFF_US + 2 * US_B;
+    static constexpr int BYTES = OFF_SINK + 64 * 16;
+    static_assert(BYTES <= 160 * 1024, "LDS budget");
+    // staging team
+    static constexpr int TT = 256;
+    static constexpr int OCH = LP * CPR;                  // chunks per row set
+    static constexpr int OPS = (OCH + TT - 1) / TT;
+    static constexpr int VCPR = BV / 8, VPS = LP * VCPR;  // V chunks per stream
+    static constexpr int VPL = (2 * VPS + TT - 1) / TT;
+    static_assert(VPS % 64 == 0, "a wave's V slot lies in one stream");
+
+    unsigned char *smem;
+    int tid, lane, wave;
+
+    __device__ Fused(unsigned char *s) : smem(s)
+    {
+        tid = threadIdx.x;
+        lane = tid & 63;
+        wave = wave_id();
+    }
+
+    // ------------------------------------------------------------------ layout
+    __device__ __forceinline__ E *rows(int slot, int i) const
+    {
+        return reinterpret_cast<E *>(smem + slot * RING_B + i * ROWS_B);
+    }
+    __device__ __forceinline__ unsigned char *set(int p) const { return smem + OFF_SET + p * SET_B; }
+    __device__ __forceinline__ In *vs(int p, int m) const { return reinterpret_cast<In *>(set(p) + m * V_B); }
+    __device__ __forceinline__ E *tm(int p, int m) const { return reinterpret_cast<E *>(set(p) + OFF_TM + m * TM_B); }
+    __device__ __forceinline__ float *fac(int p, int m) const
+    {
+        return reinterpret_cast<float *>(set(p) + OFF_FAC) + m * 64;
+    }
+    __device__ __forceinline__ E *st(int b) const { return reinterpret_cast<E *>(smem + OFF_ST + b * ST_B); }
+    __device__ __forceinline__ E *dt(int b) const { return reinterpret_cast<E *>(smem + OFF_DT + b * DT_B); }
+    __device__ __forceinline__ float *us(int u) const { return reinterpret_cast<float *>(smem + OFF_US + u * US_B); }
+
+    // Element offset of (row, k) in a swizzled [rows][DK] matrix: chunk k/8 of a row is
+    // stored at chunk (k/8) ^ (row / RPB mod CPR).
+    __device__ __forceinline__ static int swz(int row) { return (row / RPB) & (CPR - 1); }
+    __device__ __forceinline__ static int rofs(int row, int k)
+    {
+        return row * DK + ((((k >> 3) ^ swz(row)) << 3) | (k & 7));
+    }
+
+    // Per-lane offsets of the operand quads of a 16-row block (row lane & 15, k-block kb):
+    // the swizzle depends on the row within the block only, so one set serves every row
+    // block, row set and the state operand.
+    struct QOffs {
+        int q[DKB];    // quads: row lane & 15, k = 16 kb + 4 (lane >> 4)
+        int t[DKB];    // transpose-load segments (see kt_quads)
+    };
+    __device__ __forceinline__ void make_qoffs(QOffs &o) const
+    {
+        const int r = lane & 15, g = lane >> 4;
+        const int tr = 4 * g + ((lane >> 2) & 3), tq = lane & 3;
+#pragma unroll
+        for (int kb = 0; kb < DKB; ++kb) {
+            o.q[kb] = rofs(r, 16 * kb + 4 * g);
+            o.t[kb] = rofs(tr, 16 * kb + 4 * tq);
+        }
+    }
+    template <int NKB>
+    __device__ __forceinline__ void ld_q(QE (&q)[NKB], const E *M, const int (&off)[DKB]) const
+    {
+        typedef const __attribute__((address_space(3))) volatile QE *LQ;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) q[kb] = *(LQ)(M + off[kb]);
+    }
+
+    // ------------------------------------------------------------------ chain
+    struct Ptrs {
+        const In *k, *q, *kn, *qn, *v, *vn;
+        const float *g, *beta, *gn, *betan;
+        Out *o, *on;
+    };
+    struct Chain {
+        Ptrs p0;
+        long qk_blk, v_blk, g_blk;   // per-block advance (elements)
+        int qks, vst, gst;           // row strides (elements)
+        long len;
+        int L;
+        const float *h0;
+        float *ht;
+        int dv;
+        float scale;
+    };
+    __device__ __forceinline__ static void advance(Ptrs &p, const Chain &c)
+    {
+        p.k += c.qk_blk;
+        p.q += c.qk_blk;
+        p.kn += c.qk_blk;
+        p.qn += c.qk_blk;
+        p.v += c.v_blk;
+        p.vn += c.v_blk;
+        p.g += c.g_blk;
+        p.beta += c.g_blk;
+        p.gn += c.g_blk;
+        p.betan += c.g_blk;
+        p.o += c.v_blk;
+        p.on += c.v_blk;
+    }
+    __device__ __forceinline__ static int nvalid_of(const Chain &c, int j)
+    {
+        const long rem = c.len - (long)j * c.L;
+        return rem <= 0 ? 0 : rem < c.L ? (int)rem : c.L;
+    }
+    __device__ __forceinline__ static __amdgpu_buffer_rsrc_t rsrc(const void *base, unsigned bytes)
+    {
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+    }
+
+    // ------------------------------------------------------------------ L: staging
+    // Every team thread runs the same straight-line sequence of slots (no branches, so
+    // the compiler's load counters stay exact); an unassigned slot reloads the block's
+    // first chunk and stores into a per-lane sink.  Resources cover exactly the block's
+    // valid rows: rows past the block end read as zero.
+    struct LOffs {
+        unsigned rg[OPS], rl[OPS];   // rows: global byte offset, LDS byte offset in a row set
+        unsigned vg[VPL], vl[VPL];   // V: global byte offset, LDS byte offset in a set
+    };
+    struct RowsF {
+        u32x4 c[4][OPS];
+    };
+    struct VF {
+        u32x4 c[VPL];
+    };
+    __device__ __forceinline__ int v_base(int tw, int u) const { return tw * 64 + TT * u; }
+    __device__ __forceinline__ void make_loffs(const Chain &c, int tw, LOffs &o) const
+    {
+        const int lt = 64 * tw + lane;
+        const unsigned sink = (unsigned)(OFF_SINK + 16 * lane);
+#pragma unroll
+        for (int u = 0; u < OPS; ++u) {
+            const int ch = lt + TT * u, t = ch / CPR, cc = ch % CPR;
+            const bool ok = ch < OCH;
+            o.rg[u] = ok ? (unsigned)(t * c.qks * 2 + cc * 16) : 0u;
+            o.rl[u] = ok ? (unsigned)(2 * rofs(t, 8 * cc)) : sink;
+        }
+#pragma unroll
+        for (int u = 0; u < VPL; ++u) {
+            // slot u of team wave tw covers chunks vb .. vb + 63 of [V | V~]
+            const int vb = v_base(tw, u);
+            const bool ok = vb < 2 * VPS;
+            const int m = vb / VPS, ch = (ok ? vb % VPS : 0) + lane, t = ch / VCPR, cc = ch % VCPR;
+            o.vg[u] = ok ? (unsigned)(t * c.vst * 2 + cc * 16) : 0u;
+            o.vl[u] = ok ? (unsigned)(m * V_B + (t * VS + cc * 8) * 2) : sink;
+        }
+    }
+    struct RowRs {
+        __amdgpu_buffer_rsrc_t r[4];
+    };
+    __device__ __forceinline__ RowRs row_rsrcs(const Ptrs &P, const Chain &c, int nvalid) const
+    {
+        const unsigned b = (unsigned)(nvalid * c.qks * 2);
+        RowRs r;
+        r.r[0] = rsrc(P.k, b);
+        r.r[1] = rsrc(P.q, b);
+        r.r[2] = rsrc(P.kn, b);
+        r.r[3] = rsrc(P.qn, b);
+        return r;
+    }
+    // The V stream of a slot is fixed per wave (a stream spans whole waves).
+    __device__ __forceinline__ __amdgpu_buffer_rsrc_t v_rsrc(const Ptrs &P, const Chain &c, int nvalid, int tw,
+                                                            int u) const
+    {
+        return rsrc(v_base(tw, u) >= VPS ? (const void *)P.vn : (const void *)P.v, (unsigned)(nvalid * c.vst * 2));
+    }
+    __device__ __forceinline__ static u32x4 bload(__amdgpu_buffer_rsrc_t r, unsigned off)
+    {
+        return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+    }
+    __device__ __forceinline__ void st16(unsigned char *base, unsigned off, u32x4 v) const
+    {
+        unsigned char *b = off >= (unsigned)OFF_SINK ? smem : base;
+        *reinterpret_cast<u32x4 *>(b + off) = v;
+    }
+    __device__ __forceinline__ void fetch_rows(const Ptrs &P, const Chain &c, int nvalid, const LOffs &o, RowsF &f) const
+    {
+        const RowRs r = row_rsrcs(P, c, nvalid);
+#pragma unroll
+        for (int u = 0; u < OPS; ++u)
+#pragma unroll
+            for (int si = 0; si < 4; ++si) f.c[si][u] = bload(r.r[si], o.rg[u]);
+    }
+    __device__ __forceinline__ void fetch_v(const Ptrs &P, const Chain &c, int nvalid, int tw, const LOffs &o, VF &f) const
+    {
+#pragma unroll
+        for (int u = 0; u < VPL; ++u) f.c[u] = bload(v_rsrc(P, c, nvalid, tw, u), o.vg[u]);
+    }
+    // Stage rows into ring slot `slot` (converted to fp16), refilling from the block at Pn.
+    __device__ __forceinline__ void stage_rows(int slot, RowsF &f, const Ptrs &Pn, const Chain &c, int nvalid_n,
+                                               const LOffs &o) const
+    {
+        const RowRs r = row_rsrcs(Pn, c, nvalid_n);
+#pragma unroll
+        for (int u = 0; u < OPS; ++u)
+#pragma unroll
+            for (int si = 0; si < 4; ++si) {
+                st16(smem + slot * RING_B + si * ROWS_B, o.rl[u], to_operand<In, E>(f.c[si][u]));
+                f.c[si][u] = bload(r.r[si], o.rg[u]);
+            }
+    }
+    __device__ __forceinline__ void stage_v(int p, VF &f, const Ptrs &Pn, const Chain &c, int nvalid_n, int tw,
+                                            const LOffs &o) const
+    {
+#pragma unroll
+        for (int u = 0; u < VPL; ++u) {
+            st16(set(p), o.vl[u], f.c[u]);
+            f.c[u] = bload(v_rsrc(Pn, c, nvalid_n, tw, u), o.vg[u]);
+        }
+    }
+
+    __device__ __forceinline__ f32x4 ld4f(const float *p) const { return *reinterpret_cast<const f32x4 *>(p); }
+
+    // ------------------------------------------------------------------ U: the record
+    template <int CTRL> __device__ __forceinline__ static float dpp(float v)
+    {
+        return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, true));
+    }
+    __device__ __forceinline__ static float lane_value(float v, int l)
+    {
+        return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+    }
+    // Inclusive prefix sum over lanes 0 .. 31: shifts by 1, 2, 4, 8 inside each 16-lane row,
+    // then the total of row 0 carried into row 1.
+    __device__ __forceinline__ float scan32(float x) const
+    {
+        x += dpp<0x111>(x);
+        x += dpp<0x112>(x);
+        x += dpp<0x114>(x);
+        x += dpp<0x118>(x);
+        const float r0 = lane_value(x, 15);
+        return lane >= 16 && lane < 32 ? x + r0 : x;
+    }
+    __device__ __forceinline__ static f32x4 mfma16(f16x4 a, f16x4 b, f32x4 c)
+    {
+        return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0);
+    }
+
+    // One U wave builds the clean (STREAM 0: T, P, eG, dG) or noisy (STREAM 1: T~, R,
+    // eGn) half of the record of one block from the rows in ring slot `slot` and the
+    // block's gates (gv, bv: lane t < LP holds position t; zero past the block end).
+    //
+    // Everything after the gates stays in registers.  With mfma16(q(X), q(Y)) = X^T Y for
+    // accumulator tiles X, Y (lane (g, n) holding rows 4g .. 4g + 3 of column n), a product
+    // needs its left factor as the accumulator of its transpose; so the solve carries each
+    // matrix together with its transpose.  (I + A)^(-1) is built by doubling the size of
+    // the inverted diagonal blocks: with D_b the inverse restricted to blocks of size b and
+    // M_b the part of A between the two b-halves of each 2b block,
+    //     D_2b = D_b - D_b M_b D_b,    D_2 = I - M_1,
+    // which is the block lower-triangular inverse formula, so no intermediate exceeds the
+    // entries of the inverse itself; the last level joins the two 16 x 16 diagonal blocks:
+    // X10 = -X11 A10 X00.  Products take fp16 operands and accumulate in fp32.  T, P and R
+    // are produced transposed, so each lane writes four consecutive entries of a row.
+    // Masked entries are selected, not branched on; exponents are clamped at 0 so that
+    // masked-out entries stay finite.
+    template <int STREAM>
+    __device__ __forceinline__ void u_record(int slot, int p, float gv, float bv, const QOffs &qo) const
+    {
+        const int g = lane >> 4, n = lane & 15;
+        float *Gs = us(STREAM), *Bs = Gs + 64;   // cumulative log2-gates, beta
+        const float x = scan32(lane < LP ? gv * kLog2e : 0.f);
+        const float gl = lane_value(x, LP - 1);
+        Gs[lane] = x;
+        Bs[lane] = bv;
+        if (lane < LP) {
+            if (STREAM == 0) {
+                fac(p, 0)[lane] = fexp2(x);
+                fac(p, 1)[lane] = fexp2(gl - x);
+                fac(p, 3)[lane] = x;
+            } else {
+                fac(p, 2)[lane] = fexp2(x);
+                fac(p, 4)[lane] = fexp2(gl - x);
+            }
+        }
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        const E *K = rows(slot, STREAM == 0 ? 0 : 2);
+        QE kq[NB][DKB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) ld_q<DKB>(kq[rb], K + 16 * rb * DK, qo.q);
+        // kk[bi][bj]: lane (g, n) = k_(16 bi + 4g + i) . k_(16 bj + n)   (tile (1, 0) unused)
+        f32x4 kk[NB][NB];
+#pragma unroll
+        for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+            for (int bj = bi; bj < NB; ++bj) kk[bi][bj] = mma_q<E, DKB>(z, kq[bi], kq[bj]);
+        // per-lane gates: rows 4g + i and column n of each 16-block
+        f32x4 gr[NB], br[NB];
+        float gc[NB], bc[NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            gr[rb] = ld4f(Gs + 16 * rb + 4 * g);
+            br[rb] = ld4f(Bs + 16 * rb + 4 * g);
+            gc[rb] = Gs[16 * rb + n];
+            bc[rb] = Bs[16 * rb + n];
+        }
+        // diagonal tiles of A (below the diagonal) and A^T (above): one exponent serves both
+        f32x4 D[NB], Dt[NB], At[NB];
+#pragma unroll
+        for (int t = 0; t < NB; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = 4 * g + i, xr = r ^ n;
+                const float d = gr[t][i] - gc[t];
+                const float e = fexp2(fminf(r > n ? d : -d, 0.f)) * kk[t][t][i];
+                const float a = r > n ? br[t][i] * e : 0.f;
+                At[t][i] = n > r ? bc[t] * e : 0.f;
+                D[t][i] = (xr == 0 ? 1.f : 0.f) - (xr == 1 ? a : 0.f);
+                Dt[t][i] = (xr == 0 ? 1.f : 0.f) - (xr == 1 ? At[t][i] : 0.f);
+            }
+#pragma unroll
+        for (int b = 2; b < 16; b *= 2)
+#pragma unroll
+            for (int t = 0; t < NB; ++t) {
+                f32x4 mt;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int xr = (4 * g + i) ^ n;
+                    mt[i] = xr >= b && xr < 2 * b ? At[t][i] : 0.f;
+                }
+                const f32x4 y = mfma16(quad_of<E>(mt), quad_of<E>(D[t]), z);   // M_b D_b
+                const f16x4 ny = quad_of<E>(-y), dtq = quad_of<E>(Dt[t]);
+                D[t] = mfma16(dtq, ny, D[t]);                                   // D_b - D_b M_b D_b
+                Dt[t] = mfma16(ny, dtq, Dt[t]);                                 // and its transpose
+            }
+        // T = X diag(beta), written as rows of T from the transposed tiles
+        E *T = tm(p, STREAM == 0 ? 0 : 1);
+#pragma unroll
+        for (int t = 0; t < NB; ++t) {
+            f32x4 v;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = 4 * g + i <= n ? Dt[t][i] * br[t][i] : 0.f;
+            st_quad(T + (16 * t + n) * TS + 16 * t + 4 * g, quad_of<E>(v));
+        }
+        if constexpr (NB == 2) {
+            // A10^T from k_(4g + i) . k_(16 + n); Y = A10 X00; X10^T = -Y^T X11^T
+            f32x4 a01;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) a01[i] = bc[1] * fexp2(fminf(gc[1] - gr[0][i], 0.f)) * kk[0][1][i];
+            const f32x4 y = mfma16(quad_of<E>(a01), quad_of<E>(D[0]), z);
+            const f32x4 x10t = mfma16(quad_of<E>(-y), quad_of<E>(Dt[1]), z);
+            f32x4 v;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = x10t[i] * br[0][i];
+            st_quad(T + (16 + n) * TS + 4 * g, quad_of<E>(v));
+            st_quad(T + n * TS + 16 + 4 * g, quad_of<E>(z));
+        }
+    }
+
+    // ------------------------------------------------------------------ scan helpers
+
+    template <int NC>
+    __device__ __forceinline__ void x_rows(f32x4 (&x)[NB][NC], const E *R, const QE (&sq)[NC][DKB],
+                                           const QOffs &qo) const
+    {
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            QE a[DKB];
+            ld_q<DKB>(a, R + 16 * rb * DK, qo.q);
+#pragma unroll
+            for (int c = 0; c < NC; ++c) x[rb][c] = mma_q<E, DKB>(f32x4{0.f, 0.f, 0.f, 0.f}, a, sq[c]);
+        }
+    }
+    __device__ __forceinline__ void d_quads(QE (&dq)[NB], const f32x4 (&x)[NB], const In *V, const float *G,
+                                            int bc) const
+    {
+        const int g = lane >> 4, n = lane & 15;
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            const int r = 16 * rb + 4 * g;
+            const f32x4 gq = ld4f(G + r);
+            const In *vp = V + r * VS + 16 * bc + n;
+            f32x4 d;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) d[i] = to_f(vp[i * VS]) - gq[i] * x[rb][i];
+            dq[rb] = quad_of<E>(d);
+        }
+    }
+    // Y = M Z + init for a record matrix M (LP x LP, padded rows) and B-operand quads zq.
+    __device__ __forceinline__ void m_times(f32x4 (&y)[NB], const E *M, const QE (&zq)[NB], const f32x4 (&init)[NB]) const
+    {
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            QE a[NB];
+            ld_quads<E, NB>(a, M + 16 * rb * TS, TS, lane);
+            y[rb] = mma_q<E, NB>(init[rb], a, zq);
+        }
+    }
+    __device__ __forceinline__ void store_out(Out *dst, int stride, int nvalid, int bc, const f32x4 (&acc)[NB],
+                                              float scale) const
+    {
+        constexpr int SO = (int)sizeof(Out);
+        const __amdgpu_buffer_rsrc_t r = rsrc(dst, (unsigned)(nvalid * stride * SO));
+        const int g = lane >> 4, n = lane & 15;
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int off = ((16 * rb + 4 * g + i) * stride + 16 * bc + n) * SO;
+                const Out v = to_e<Out>(acc[rb][i] * scale);
+                if constexpr (SO == 4)
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, off, 0, 0);
+                else
+                    __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, v), r, off, 0, 0);
+            }
+    }
+    __device__ __forceinline__ void write_st(int b, const QE (&sq)[DKB], int bc, const QOffs &qo) const
+    {
+        E *dst = st(b) + 16 * bc * DK;
+#pragma unroll
+        for (int kb = 0; kb < DKB; ++kb) st_quad(dst + qo.q[kb], sq[kb]);
+    }
+    // A-operand quads of K^T rows 16 kb .. 16 kb + 15 from the swizzled K rows with
+    // transpose loads: lane 16 g + 4 j + q addresses row 16 rb + 4 g + j, columns
+    // 16 kb + 4 q .. + 3, and lane (g, r) receives K[16 rb + 4 g + i][16 kb + r], i = 0..3.
+    __device__ __forceinline__ void kt_quads(QE (&a)[NB], const E *K, int kb, const QOffs &qo) const
+    {
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb)
+            a[rb] = __builtin_bit_cast(QE, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                               (__attribute__((address_space(3))) s16x4 *)(K + 16 * rb * DK + qo.t[kb])));
+    }
+
+    // ------------------------------------------------------------------ scan roles
+    __device__ __forceinline__ void c_block(int slot, int p, int db, int bc, f32x4 (&S)[DKB], QE (&sq)[DKB],
+                                            const QOffs &qo) const
+    {
+        const int g = lane >> 4, n = lane & 15;
+        const f32x4 z[NB] = {};
+        const QE(&sq1)[1][DKB] = *reinterpret_cast<const QE(*)[1][DKB]>(&sq);
+        const E *K = rows(slot, 0);
+        f32x4 x1[NB][1];
+        x_rows<1>(x1, K, sq1, qo);
+        f32x4 x[NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) x[rb] = x1[rb][0];
+        QE dq[NB];
+        d_quads(dq, x, vs(p, 0), fac(p, 0), bc);
+        f32x4 dl[NB];
+        m_times(dl, tm(p, 0), dq, z);
+        QE uq[NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            st_quad(dt(db) + (16 * bc + n) * TS + 16 * rb + 4 * g, quad_of<E>(dl[rb]));
+            uq[rb] = quad_of<E>(dl[rb] * ld4f(fac(p, 1) + 16 * rb + 4 * g));
+        }
+        const float decay = fac(p, 0)[LP - 1];
+#pragma unroll
+        for (int kb = 0; kb < DKB; ++kb) {
+            QE a[NB];
+            kt_quads(a, K, kb, qo);
+            S[kb] = mma_q<E, NB>(S[kb] * decay, a, uq);
+            sq[kb] = quad_of<E>(S[kb]);
+        }
+    }
+    // N: the noisy block.  R_rc = 2^(G~_n - G~_c) (q~_r . k~_c) is formed here from the rows
+    // it already holds: with the key rows as the left operand the accumulator is R^T, which
+    // is the A-operand layout of R.
+    __device__ __forceinline__ void n_block(int slot, int p, int sb, int bc, Out *on, int stride, int nvalid,
+                                            float scale, const QOffs &qo) const
+    {
+        const int g = lane >> 4;
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        const f32x4 zs[NB] = {};
+        QE sq[DKB];
+        ld_q<DKB>(sq, st(sb) + 16 * bc * DK, qo.q);
+        QE kq[NB][DKB];
+        f32x4 x3[NB], x4[NB];
+        QE rq[NB][NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            ld_q<DKB>(kq[rb], rows(slot, 2) + 16 * rb * DK, qo.q);
+            x3[rb] = mma_q<E, DKB>(z, kq[rb], sq);
+        }
+        const float gn_end = fac(p, 2)[LP - 1];
+#pragma unroll
+        for (int bi = 0; bi < NB; ++bi) {
+            QE qq[DKB];
+            ld_q<DKB>(qq, rows(slot, 3) + 16 * bi * DK, qo.q);
+            x4[bi] = mma_q<E, DKB>(z, qq, sq) * gn_end;
+#pragma unroll
+            for (int bj = 0; bj < NB; ++bj)
+                rq[bi][bj] = quad_of<E>(mma_q<E, DKB>(z, kq[bj], qq) * ld4f(fac(p, 4) + 16 * bj + 4 * g));
+        }
+        QE dq[NB];
+        d_quads(dq, x3, vs(p, 1), fac(p, 2), bc);
+        f32x4 dn[NB];
+        m_times(dn, tm(p, 1), dq, zs);
+        QE nq[NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) nq[rb] = quad_of<E>(dn[rb]);
+        f32x4 o[NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) o[rb] = mma_q<E, NB>(x4[rb], rq[rb], nq);
+        store_out(on, stride, nvalid, bc, o, scale);
+    }
+    // O, first half: X2 = diag(eG) Q S0 and P_rc = 2^(G_r - G_c) (q_r . k_c), c <= r, of
+    // block j in registers (P in the A-operand layout, as for R above).
+    __device__ __forceinline__ void o_begin(int slot, int p, int sb, int bc, f32x4 (&x2)[NB], QE (&pq)[NB][NB],
+                                            const QOffs &qo) const
+    {
+        const int g = lane >> 4, n = lane & 15;
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        QE sq[DKB];
+        ld_q<DKB>(sq, st(sb) + 16 * bc * DK, qo.q);
+        QE kq[NB][DKB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) ld_q<DKB>(kq[rb], rows(slot, 0) + 16 * rb * DK, qo.q);
+        const float *G = fac(p, 3);
+        f32x4 gr[NB];
+        float gc[NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            gr[rb] = ld4f(G + 16 * rb + 4 * g);
+            gc[rb] = G[16 * rb + n];
+        }
+#pragma unroll
+        for (int bi = 0; bi < NB; ++bi) {
+            QE qq[DKB];
+            ld_q<DKB>(qq, rows(slot, 1) + 16 * bi * DK, qo.q);
+            x2[bi] = mma_q<E, DKB>(z, qq, sq) * ld4f(fac(p, 0) + 16 * bi + 4 * g);
+#pragma unroll
+            for (int bj = 0; bj < NB; ++bj) {
+                f32x4 v = z;
+                if (bj <= bi) {
+                    const f32x4 qk = mma_q<E, DKB>(z, kq[bj], qq);   // row 16 bi + n, cols 16 bj + 4g + i
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const bool on = bj < bi || 4 * g + i <= n;
+                        v[i] = on ? fexp2(fminf(gc[bi] - gr[bj][i], 0.f)) * qk[i] : 0.f;
+                    }
+                }
+                pq[bi][bj] = quad_of<E>(v);
+            }
+        }
+    }
+    __device__ __forceinline__ void o_end(int db, int bc, const f32x4 (&x2)[NB], const QE (&pq)[NB][NB], Out *o,
+                                          int stride, int nvalid, float scale) const
+    {
+        QE dq[NB];
+        ld_quads<E, NB>(dq, dt(db) + 16 * bc * TS, TS, lane);
+        f32x4 acc[NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) acc[rb] = mma_q<E, NB>(x2[rb], pq[rb], dq);
+        store_out(o, stride, nvalid, bc, acc, scale);
+    }
+
+    // U: the record of block j + 1 in step j (block 0 before the loop); each block's gates
+    // are loaded at the start of the step before the one that uses them.
+    template <int STREAM>
+    __device__ __forceinline__ void u_loop(const Chain &c, int nb, const QOffs &qo) const
+    {
+        Ptrs pg = c.p0;
+        auto load_gates = [&](int jj, float &gx, float &bx) {
+            const unsigned bytes = (unsigned)(nvalid_of(c, jj) * c.gst * 4);
+            const __amdgpu_buffer_rsrc_t rg = rsrc(STREAM == 0 ? pg.g : pg.gn, bytes);
+            const __amdgpu_buffer_rsrc_t rb = rsrc(STREAM == 0 ? pg.beta : pg.betan, bytes);
+            const int off = (lane < LP ? lane : 0) * c.gst * 4;
+            gx = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rg, off, 0, 0));
+            bx = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, off, 0, 0));
+            advance(pg, c);
+        };
+        float gx, bx, gy, by;
+        load_gates(0, gx, bx);
+        load_gates(1, gy, by);
+        lds_barrier();
+        u_record<STREAM>(0, 0, lane < LP ? gx : 0.f, lane < LP ? bx : 0.f, qo);
+        lds_barrier();
+        for (int j = 0; j < nb; ++j) {
+            load_gates(j + 2, gx, bx);
+            u_record<STREAM>((j + 1) % 3, (j + 1) & 1, lane < LP ? gy : 0.f, lane < LP ? by : 0.f, qo);
+            gy = gx;
+            by = bx;
+            lds_barrier();
+        }
+    }
+
+    // ------------------------------------------------------------------ the chain
+    // Barriers: two before the loop (rows and V of the first blocks staged; record of
+    // block 0 built), then one per block.
+    __device__ void run(const Chain &c) const
+    {
+        const int nb = (int)((c.len + c.L - 1) / c.L);
+        const int g = lane >> 4, n = lane & 15;
+        auto nv = [&](int jj) { return nvalid_of(c, jj); };
+        QOffs qo;
+        make_qoffs(qo);
+        if (wave < 2) {
+            // ---- C
+            __builtin_amdgcn_s_setprio(BDGDN_PRIO_C);
+            const int bc = wave;
+            f32x4 S[DKB];
+            QE sq[DKB];
+#pragma unroll
+            for (int kb = 0; kb < DKB; ++kb) {
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                if (c.h0) {
+                    const float *src = c.h0 + (long)(16 * kb + 4 * g) * c.dv + 16 * bc + n;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[i] = src[i * c.dv];
+                }
+                S[kb] = acc;
+                sq[kb] = quad_of<E>(acc);
+            }
+            wait_global_loads();
+            write_st(0, sq, bc, qo);
+            lds_barrier();
+            lds_barrier();
+            for (int j = 0; j < nb; ++j) {
+                c_block(j % 3, j & 1, j & 1, bc, S, sq, qo);
+                write_st((j + 1) & 1, sq, bc, qo);
+                lds_barrier();
+            }
+            if (c.ht) {
+#pragma unroll
+                for (int kb = 0; kb < DKB; ++kb) {
+                    float *dst = c.ht + (long)(16 * kb + 4 * g) * c.dv + 16 * bc + n;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) dst[i * c.dv] = S[kb][i];
+                }
+            }
+        } else if (wave < 4) {
+            // ---- N
+            __builtin_amdgcn_s_setprio(BDGDN_PRIO_N);
+            const int bc = wave - 2;
+            Ptrs pc = c.p0;
+            lds_barrier();
+            lds_barrier();
+            for (int j = 0; j < nb; ++j) {
+                n_block(j % 3, j & 1, j & 1, bc, pc.on, c.vst, nv(j), c.scale, qo);
+                advance(pc, c);
+                lds_barrier();
+            }
+        } else if (wave < 6) {
+            // ---- O
+            __builtin_amdgcn_s_setprio(BDGDN_PRIO_O);
+            const int bc = wave - 4;
+            Ptrs pc = c.p0;
+            f32x4 x2[NB];
+            QE pq[NB][NB];
+            lds_barrier();
+            lds_barrier();
+            for (int j = 0; j < nb; ++j) {
+                if (j > 0) {
+                    o_end((j - 1) & 1, bc, x2, pq, pc.o, c.vst, nv(j - 1), c.scale);
+                    advance(pc, c);
+                }
+                o_begin(j % 3, j & 1, j & 1, bc, x2, pq, qo);
+                lds_barrier();
+            }
+            if (nb > 0) o_end((nb - 1) & 1, bc, x2, pq, pc.o, c.vst, nv(nb - 1), c.scale);
+        } else if (wave == 6) {
+            __builtin_amdgcn_s_setprio(BDGDN_PRIO_U);
+            u_loop<0>(c, nb, qo);
+        } else if (wave == 7) {
+            __builtin_amdgcn_s_setprio(BDGDN_PRIO_U);
+            u_loop<1>(c, nb, qo);
+        } else {
+            // ---- L: step j stages the rows of block j + 2 and the V tile of block j + 1,
+            // each refilled from two blocks further on
+            __builtin_amdgcn_s_setprio(BDGDN_PRIO_L);
+            const int tw = wave - 8;
+            LOffs o;
+            make_loffs(c, tw, o);
+            Ptrs pr = c.p0, pv = c.p0;   // next rows / V block to load
+            RowsF r0, r1;
+            VF v0, v1;
+            fetch_rows(pr, c, nv(0), o, r0);
+            advance(pr, c);
+            fetch_rows(pr, c, nv(1), o, r1);
+            advance(pr, c);
+            fetch_v(pv, c, nv(0), tw, o, v0);
+            advance(pv, c);
+            fetch_v(pv, c, nv(1), tw, o, v1);
+            advance(pv, c);
+            stage_rows(0, r0, pr, c, nv(2), o);   // rows 0; r0 <- rows 2
+            advance(pr, c);
+            stage_rows(1, r1, pr, c, nv(3), o);   // rows 1; r1 <- rows 3
+            advance(pr, c);
+            stage_v(0, v0, pv, c, nv(2), tw, o);   // V 0; v0 <- V 2
+            advance(pv, c);
+            lds_barrier();
+            lds_barrier();
+            for (int j = 0; j < nb; j += 2) {
+                // step j: rows j + 2 (r0) into slot (j + 2) % 3, V j + 1 (v1) into set 1
+                stage_rows((j + 2) % 3, r0, pr, c, nv(j + 4), o);
+                advance(pr, c);
+                stage_v(1, v1, pv, c, nv(j + 3), tw, o);
+                advance(pv, c);
+                lds_barrier();
+                if (j + 1 < nb) {
+                    stage_rows((j + 3) % 3, r1, pr, c, nv(j + 5), o);
+                    advance(pr, c);
+                    stage_v(0, v0, pv, c, nv(j + 4), tw, o);
+                    advance(pv, c);
+                    lds_barrier();
+                }
+            }
+        }
+    }
+};
+
+}  // namespace bdgdn

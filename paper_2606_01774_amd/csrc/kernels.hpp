@@ -35,6 +35,7 @@ struct IntraArgs {
 // Sequential scan (one workgroup per (chain, d_v tile)).
 struct ScanArgs {
     const void *q, *k, *v, *qn, *kn, *vn;
+    const float *g, *beta, *gn, *betan;   // read by the one-kernel schedule only
     const int32_t *cu;
     const float *h0;
     float *ht;
@@ -71,6 +72,10 @@ hipError_t launch_denoise(Types ty, int dk, int lp, const ServeArgs &a, hipStrea
 hipError_t launch_commit(Types ty, int dk, int lp, bool with_o, const ServeArgs &a, hipStream_t s);
 // Two-kernel training forward (UT transform records, then the scan).
 hipError_t launch_fwd_scan(Types ty, int dk, int lp, const IntraArgs &ia, const ScanArgs &sa, hipStream_t s);
+// The one-kernel pipelined schedule (UT transform inside the scan workgroups): bf16
+// inputs, blocks of at most 32 positions.
+bool pipelined_supported(Types ty, int dk, int lp);
+hipError_t launch_fwd_pipelined(Types ty, int dk, int lp, const ScanArgs &a, hipStream_t s);
 size_t scan_record_bytes(Types ty, int lp);
 int scan_tile_v();
 // d_v columns handled by one workgroup of the training / serving kernels.

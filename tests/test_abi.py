@@ -89,13 +89,21 @@ def test_fwd_packing_checks():
 
 
 def test_workspace_query():
-    # one record per (block, v-head): 64 tokens / 32 = 2 blocks x 4 v-heads
-    ws = bd.bdgdn_fwd_train_workspace(_desc())
+    # RECORDS: one record per (block, v-head): 64 tokens / 32 = 2 blocks x 4 v-heads
+    rec = _desc(route=bd.BDGDN_ROUTE_RECORDS)
+    ws = bd.bdgdn_fwd_train_workspace(rec)
     assert ws > 0 and ws % (2 * 4) == 0 and (ws // 8) % 256 == 0
+    # FUSED runs as one kernel without a workspace for bf16 inputs and blocks up to 32 ...
+    assert bd.bdgdn_fwd_train_workspace(_desc()) == 0
+    assert bd.bdgdn_fwd_train_workspace(_desc(block=16, d_k=64, d_v=64)) == 0
+    # ... and through the records otherwise (64-position blocks, fp32 inputs)
+    assert bd.bdgdn_fwd_train_workspace(_desc(block=64)) > 0
+    assert bd.bdgdn_fwd_train_workspace(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32)) > 0
     assert bd.bdgdn_fwd_train_workspace(_desc(route=bd.BDGDN_ROUTE_ONEPASS)) == 0
     assert bd.bdgdn_fwd_train_workspace(_desc(h_v=3)) == 0
     # too small a workspace is refused before any launch
-    assert _fwd(_desc()) == bd.BDGDN_ERR_WORKSPACE
+    assert _fwd(rec) == bd.BDGDN_ERR_WORKSPACE
+    assert _fwd(_desc(block=64)) == bd.BDGDN_ERR_WORKSPACE
 
 
 def _serve(fn, **kw):

@@ -44,7 +44,7 @@ def test_tiny_f32_full_config():
     _check_full(W.make_train(w), w.block, "f32")
 
 
-ROUTES = [bd.BDGDN_ROUTE_FUSED, bd.BDGDN_ROUTE_ONEPASS]
+ROUTES = [bd.BDGDN_ROUTE_FUSED, bd.BDGDN_ROUTE_ONEPASS, bd.BDGDN_ROUTE_RECORDS]
 
 
 @pytest.mark.parametrize("route", ROUTES)
@@ -73,16 +73,17 @@ def test_packed_documents_small(route):
 
 @pytest.mark.parametrize("L", [16, 32, 64])
 def test_routes_agree(L):
-    """The two schedules compute the same function: the two-kernel route and the
-    single-kernel route agree to rounding (both against each other and the oracle)."""
+    """The schedules compute the same function: the fused route (one kernel up to
+    32-position blocks), the records route and the one-pass route agree to rounding."""
     inp = W.make_custom_train(2, 4 * L + 5, 2, 4, 128, 128, "bf16", seed=L)
     d = to_dev(inp)
     a = _run_gpu(d, L, 0.1, route=bd.BDGDN_ROUTE_FUSED)
-    b = _run_gpu(d, L, 0.1, route=bd.BDGDN_ROUTE_ONEPASS)
-    for x, y in zip(a, b):
-        e = rel_err(x, y.double().cpu().numpy())
-        print(f"route difference {e:.3e}")
-        assert e <= TOL["bf16"]
+    for other in (bd.BDGDN_ROUTE_ONEPASS, bd.BDGDN_ROUTE_RECORDS):
+        b = _run_gpu(d, L, 0.1, route=other)
+        for x, y in zip(a, b):
+            e = rel_err(x, y.double().cpu().numpy())
+            print(f"route {other} difference {e:.3e}")
+            assert e <= TOL["bf16"]
 
 
 def test_packed_equals_separate_bitwise():
