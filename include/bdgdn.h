@@ -27,7 +27,9 @@
  *       q, k : [rows][h_qk][d_k]      v, o : [rows][h_v][d_v]     g, beta : [rows][h_v]
  *     where rows = batch*seqlen (training) or num_req*block (serving).
  *     q, k, v have the descriptor's dtype and o its out_dtype; g (the LOG gate,
- *     alpha = exp(g)) and beta are fp32 and used as given.
+ *     alpha = exp(g)) and beta are fp32 and used as given.  g must be <= 0 (alpha in
+ *     (0, 1], a decay): the bf16 kernels evaluate every decay exponent as non-positive,
+ *     and a positive g gives unspecified (finite) results there.
  *   - Arithmetic: states and all accumulations are fp32.  With bf16 inputs the MFMA
  *     operands are fp16 (the bf16 values converted exactly; every rounded
  *     intermediate keeps 11 significant bits), so inputs and intermediates must stay

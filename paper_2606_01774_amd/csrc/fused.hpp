@@ -22,28 +22,11 @@
 // a three-slot ring (used by U one step before the scan); V, the record and the factors
 // in a two-slot set.  Rows are stored unpadded with their 16-byte chunks XOR-swizzled by
 // row, which keeps every LDS access pattern here free of bank conflicts in 3 x 32 KB.
-// The waves on the recurrence's critical path (C, U) run at a raised issue priority.
 #pragma once
 
 #include "intra.hpp"
 
 namespace bdgdn {
-
-#ifndef BDGDN_PRIO_C
-#define BDGDN_PRIO_C 3
-#endif
-#ifndef BDGDN_PRIO_N
-#define BDGDN_PRIO_N 1
-#endif
-#ifndef BDGDN_PRIO_O
-#define BDGDN_PRIO_O 1
-#endif
-#ifndef BDGDN_PRIO_U
-#define BDGDN_PRIO_U 3
-#endif
-#ifndef BDGDN_PRIO_L
-#define BDGDN_PRIO_L 2
-#endif
 
 template <typename Out, int DK, int LP>
 struct Fused {
@@ -315,6 +298,48 @@ struct Fused {
         return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0);
     }
 
+    // Per-lane constants of the solve, element i of a 16 x 16 tile at row r = 4g + i,
+    // column n: the identity, the level-1 entries of A and A^T, and for
+    // the levels b = 2, 4, 8 an AND mask over the fp16 quad that keeps the entries of
+    // M_b^T (those above the diagonal whose row and column differ first in bit log2 b).
+    struct USolve {
+        f32x4 one, m1lo, m1up;
+        unsigned mk[3][2];
+    };
+    __device__ __forceinline__ void make_usolve(USolve &u) const
+    {
+        const int g = lane >> 4, n = lane & 15;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = 4 * g + i, xr = r ^ n;
+            u.one[i] = xr == 0 ? 1.f : 0.f;
+            u.m1lo[i] = xr == 1 && r > n ? 1.f : 0.f;
+            u.m1up[i] = xr == 1 && n > r ? 1.f : 0.f;
+        }
+#pragma unroll
+        for (int l = 0; l < 3; ++l) {
+            const int b = 2 << l;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                unsigned m = 0;
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    const int r = 4 * g + 2 * h + e, xr = r ^ n;
+                    if (n > r && xr >= b && xr < 2 * b) m |= 0xffffu << (16 * e);
+                }
+                u.mk[l][h] = m;
+            }
+        }
+    }
+    __device__ __forceinline__ static f16x4 and_mask(f16x4 q, const unsigned (&m)[2])
+    {
+        typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+        u32x2 w = __builtin_bit_cast(u32x2, q);
+        w[0] &= m[0];
+        w[1] &= m[1];
+        return __builtin_bit_cast(f16x4, w);
+    }
+
     // One U wave builds the clean (STREAM 0: T, P, eG, dG) or noisy (STREAM 1: T~, R,
     // eGn) half of the record of one block from the rows in ring slot `slot` and the
     // block's gates (gv, bv: lane t < LP holds position t; zero past the block end).
@@ -330,10 +355,12 @@ struct Fused {
     // entries of the inverse itself; the last level joins the two 16 x 16 diagonal blocks:
     // X10 = -X11 A10 X00.  Products take fp16 operands and accumulate in fp32.  T, P and R
     // are produced transposed, so each lane writes four consecutive entries of a row.
-    // Masked entries are selected, not branched on; exponents are clamped at 0 so that
-    // masked-out entries stay finite.
+    // Masked entries are selected, not branched on.  With log-gates g <= 0 the cumulative
+    // G is non-increasing, so every decay exponent kept (G_r - G_c, r >= c) is <= 0 and is
+    // evaluated as -|G_r - G_c|, which also keeps the discarded entries finite.
     template <int STREAM>
-    __device__ __forceinline__ void u_record(int slot, int p, float gv, float bv, const QOffs &qo) const
+    __device__ __forceinline__ void u_record(int slot, int p, float gv, float bv, const QOffs &qo,
+                                             const USolve &us_) const
     {
         const int g = lane >> 4, n = lane & 15;
         float *Gs = us(STREAM), *Bs = Gs + 64;   // cumulative log2-gates, beta
@@ -373,48 +400,39 @@ struct Fused {
             bc[rb] = Bs[16 * rb + n];
         }
         // diagonal tiles of A (below the diagonal) and A^T (above): one exponent serves both
-        f32x4 D[NB], Dt[NB], At[NB];
-#pragma unroll
-        for (int t = 0; t < NB; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int r = 4 * g + i, xr = r ^ n;
-                const float d = gr[t][i] - gc[t];
-                const float e = fexp2(fminf(r > n ? d : -d, 0.f)) * kk[t][t][i];
-                const float a = r > n ? br[t][i] * e : 0.f;
-                At[t][i] = n > r ? bc[t] * e : 0.f;
-                D[t][i] = (xr == 0 ? 1.f : 0.f) - (xr == 1 ? a : 0.f);
-                Dt[t][i] = (xr == 0 ? 1.f : 0.f) - (xr == 1 ? At[t][i] : 0.f);
-            }
-#pragma unroll
-        for (int b = 2; b < 16; b *= 2)
-#pragma unroll
-            for (int t = 0; t < NB; ++t) {
-                f32x4 mt;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int xr = (4 * g + i) ^ n;
-                    mt[i] = xr >= b && xr < 2 * b ? At[t][i] : 0.f;
-                }
-                const f32x4 y = mfma16(quad_of<E>(mt), quad_of<E>(D[t]), z);   // M_b D_b
-                const f16x4 ny = quad_of<E>(-y), dtq = quad_of<E>(Dt[t]);
-                D[t] = mfma16(dtq, ny, D[t]);                                   // D_b - D_b M_b D_b
-                Dt[t] = mfma16(ny, dtq, Dt[t]);                                 // and its transpose
-            }
-        // T = X diag(beta), written as rows of T from the transposed tiles
-        E *T = tm(p, STREAM == 0 ? 0 : 1);
+        f32x4 D[NB], Dt[NB];
+        f16x4 atq[NB];
 #pragma unroll
         for (int t = 0; t < NB; ++t) {
-            f32x4 v;
+            f32x4 at;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) v[i] = 4 * g + i <= n ? Dt[t][i] * br[t][i] : 0.f;
-            st_quad(T + (16 * t + n) * TS + 16 * t + 4 * g, quad_of<E>(v));
+            for (int i = 0; i < 4; ++i) {
+                const float e = fexp2(-fabsf(gr[t][i] - gc[t])) * kk[t][t][i];
+                at[i] = bc[t] * e;
+                D[t][i] = fmaf(-us_.m1lo[i], br[t][i] * e, us_.one[i]);
+                Dt[t][i] = fmaf(-us_.m1up[i], at[i], us_.one[i]);
+            }
+            atq[t] = quad_of<E>(at);
         }
+#pragma unroll
+        for (int l = 0; l < 3; ++l)
+#pragma unroll
+            for (int t = 0; t < NB; ++t) {
+                const f32x4 y = mfma16(and_mask(atq[t], us_.mk[l]), quad_of<E>(D[t]), z);   // M_b D_b
+                const f16x4 ny = quad_of<E>(-y), dtq = quad_of<E>(Dt[t]);
+                D[t] = mfma16(dtq, ny, D[t]);                                             // D_b - D_b M_b D_b
+                Dt[t] = mfma16(ny, dtq, Dt[t]);                                           // and its transpose
+            }
+        // T = X diag(beta), written as rows of T from the transposed tiles (whose entries
+        // below the diagonal are exact zeros: every product there has a zero factor)
+        E *T = tm(p, STREAM == 0 ? 0 : 1);
+#pragma unroll
+        for (int t = 0; t < NB; ++t) st_quad(T + (16 * t + n) * TS + 16 * t + 4 * g, quad_of<E>(Dt[t] * br[t]));
         if constexpr (NB == 2) {
             // A10^T from k_(4g + i) . k_(16 + n); Y = A10 X00; X10^T = -Y^T X11^T
             f32x4 a01;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) a01[i] = bc[1] * fexp2(fminf(gc[1] - gr[0][i], 0.f)) * kk[0][1][i];
+            for (int i = 0; i < 4; ++i) a01[i] = bc[1] * fexp2(-fabsf(gc[1] - gr[0][i])) * kk[0][1][i];
             const f32x4 y = mfma16(quad_of<E>(a01), quad_of<E>(D[0]), z);
             const f32x4 x10t = mfma16(quad_of<E>(-y), quad_of<E>(Dt[1]), z);
             f32x4 v;
@@ -605,7 +623,7 @@ struct Fused {
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const bool on = bj < bi || 4 * g + i <= n;
-                        v[i] = on ? fexp2(fminf(gc[bi] - gr[bj][i], 0.f)) * qk[i] : 0.f;
+                        v[i] = on ? fexp2(-fabsf(gc[bi] - gr[bj][i])) * qk[i] : 0.f;
                     }
                 }
                 pq[bi][bj] = quad_of<E>(v);
@@ -638,15 +656,17 @@ struct Fused {
             bx = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rb, off, 0, 0));
             advance(pg, c);
         };
+        USolve usv;
+        make_usolve(usv);
         float gx, bx, gy, by;
         load_gates(0, gx, bx);
         load_gates(1, gy, by);
         lds_barrier();
-        u_record<STREAM>(0, 0, lane < LP ? gx : 0.f, lane < LP ? bx : 0.f, qo);
+        u_record<STREAM>(0, 0, lane < LP ? gx : 0.f, lane < LP ? bx : 0.f, qo, usv);
         lds_barrier();
         for (int j = 0; j < nb; ++j) {
             load_gates(j + 2, gx, bx);
-            u_record<STREAM>((j + 1) % 3, (j + 1) & 1, lane < LP ? gy : 0.f, lane < LP ? by : 0.f, qo);
+            u_record<STREAM>((j + 1) % 3, (j + 1) & 1, lane < LP ? gy : 0.f, lane < LP ? by : 0.f, qo, usv);
             gy = gx;
             by = bx;
             lds_barrier();
@@ -665,7 +685,6 @@ struct Fused {
         make_qoffs(qo);
         if (wave < 2) {
             // ---- C
-            __builtin_amdgcn_s_setprio(BDGDN_PRIO_C);
             const int bc = wave;
             f32x4 S[DKB];
             QE sq[DKB];
@@ -699,7 +718,6 @@ struct Fused {
             }
         } else if (wave < 4) {
             // ---- N
-            __builtin_amdgcn_s_setprio(BDGDN_PRIO_N);
             const int bc = wave - 2;
             Ptrs pc = c.p0;
             lds_barrier();
@@ -711,7 +729,6 @@ struct Fused {
             }
         } else if (wave < 6) {
             // ---- O
-            __builtin_amdgcn_s_setprio(BDGDN_PRIO_O);
             const int bc = wave - 4;
             Ptrs pc = c.p0;
             f32x4 x2[NB];
@@ -728,15 +745,12 @@ struct Fused {
             }
             if (nb > 0) o_end((nb - 1) & 1, bc, x2, pq, pc.o, c.vst, nv(nb - 1), c.scale);
         } else if (wave == 6) {
-            __builtin_amdgcn_s_setprio(BDGDN_PRIO_U);
             u_loop<0>(c, nb, qo);
         } else if (wave == 7) {
-            __builtin_amdgcn_s_setprio(BDGDN_PRIO_U);
             u_loop<1>(c, nb, qo);
         } else {
             // ---- L: step j stages the rows of block j + 2 and the V tile of block j + 1,
             // each refilled from two blocks further on
-            __builtin_amdgcn_s_setprio(BDGDN_PRIO_L);
             const int tw = wave - 8;
             LOffs o;
             make_loffs(c, tw, o);
@@ -759,20 +773,27 @@ struct Fused {
             advance(pv, c);
             lds_barrier();
             lds_barrier();
-            for (int j = 0; j < nb; j += 2) {
+            // Steps in pairs with a straight-line body (a branch inside it would make the
+            // compiler's load counters at the loop head wait for the newest loads); an odd
+            // last step follows the loop.
+            int j = 0;
+            for (; j + 1 < nb; j += 2) {
                 // step j: rows j + 2 (r0) into slot (j + 2) % 3, V j + 1 (v1) into set 1
                 stage_rows((j + 2) % 3, r0, pr, c, nv(j + 4), o);
                 advance(pr, c);
                 stage_v(1, v1, pv, c, nv(j + 3), tw, o);
                 advance(pv, c);
                 lds_barrier();
-                if (j + 1 < nb) {
-                    stage_rows((j + 3) % 3, r1, pr, c, nv(j + 5), o);
-                    advance(pr, c);
-                    stage_v(0, v0, pv, c, nv(j + 4), tw, o);
-                    advance(pv, c);
-                    lds_barrier();
-                }
+                stage_rows((j + 3) % 3, r1, pr, c, nv(j + 5), o);
+                advance(pr, c);
+                stage_v(0, v0, pv, c, nv(j + 4), tw, o);
+                advance(pv, c);
+                lds_barrier();
+            }
+            if (j < nb) {
+                stage_rows((j + 2) % 3, r0, pr, c, 0, o);
+                stage_v(1, v1, pv, c, 0, tw, o);
+                lds_barrier();
             }
         }
     }
