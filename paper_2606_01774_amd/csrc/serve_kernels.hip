@@ -1,11 +1,15 @@
 // serve_kernels.hip -- Diffusion-Trust serving passes over a pool of cached fp32
 // states: the denoise pass (block-end readout, the state is only read) and the
 // token-causal commit pass (the state is advanced and written back in place).
-// One workgroup per (request, v-head, d_v tile); each reads its state tile once.
+// bf16 inputs with d_k = d_v = 128 and blocks of up to 32 positions run the streaming
+// kernels of serve.hpp (one workgroup per (request, v-head), state straight to
+// registers); every other shape runs the general engine, one workgroup per (request,
+// v-head, d_v tile).  Each workgroup reads its state tile once.
 #include <mutex>
 
 #include "engine.hpp"
 #include "kernels.hpp"
+#include "serve.hpp"
 
 namespace bdgdn {
 
@@ -72,6 +76,49 @@ __global__ void __launch_bounds__(kServeThreads) bdgdn_commit_kernel(ServeArgs a
     serve_body<In, Op, Out, DK, BV, LP, true, CO, false>(a);
 }
 
+// ---- streaming kernels (serve.hpp)
+template <typename Out, int LP, bool COMMIT, bool CO>
+__device__ __forceinline__ void stream_body(const ServeArgs &a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    typedef Serve<Out, 128, LP, COMMIT, CO> K;
+    typedef typename K::In In;
+    const int unit = blockIdx.x;
+    const int r = unit / a.h_v, h = unit % a.h_v;
+    const int sl = a.slot ? a.slot[r] : r;
+    const int hq = h / (a.h_v / a.h_qk);
+    typename K::Unit u;
+    const long row0 = (long)r * a.L;
+    const long qk_off = (row0 * a.h_qk + hq) * 128;
+    const long v_off = (row0 * a.h_v + h) * 128;
+    u.k = static_cast<const In *>(a.k) + qk_off;
+    u.q = static_cast<const In *>(a.q) + qk_off;
+    u.v = static_cast<const In *>(a.v) + v_off;
+    u.g = a.g + row0 * a.h_v + h;
+    u.beta = a.beta + row0 * a.h_v + h;
+    u.state = a.pool + ((long)sl * a.h_v + h) * 128 * 128;
+    u.o = a.o ? static_cast<Out *>(a.o) + v_off : nullptr;
+    u.qks = a.h_qk * 128;
+    u.vst = a.h_v * 128;
+    u.gst = a.h_v;
+    u.nvalid = a.L;
+    u.scale = a.scale;
+    K k(smem);
+    k.run(u);
+}
+
+template <typename Out, int LP>
+__global__ void __launch_bounds__(256) bdgdn_k4_denoise_kernel(ServeArgs a)
+{
+    stream_body<Out, LP, false, false>(a);
+}
+
+template <typename Out, int LP, bool CO>
+__global__ void __launch_bounds__(256) bdgdn_k4_commit_kernel(ServeArgs a)
+{
+    stream_body<Out, LP, true, CO>(a);
+}
+
 template <typename K>
 static hipError_t set_lds(K kern, int bytes, std::once_flag &once, hipError_t &err)
 {
@@ -132,8 +179,36 @@ static hipError_t launch_cm(bool with_o, const ServeArgs &a, hipStream_t s)
 
 int serve_tile_v() { return kServeBV; }
 
+static bool stream_ok(Types ty, int dk, int lp, const ServeArgs &a)
+{
+    return ty != Types::F32 && dk == 128 && a.dv == 128 && (lp == 16 || lp == 32);
+}
+
+template <typename Out, int LP, bool COMMIT, bool CO>
+static hipError_t launch_stream(const ServeArgs &a, hipStream_t s)
+{
+    typedef Serve<Out, 128, LP, COMMIT, CO> K;
+    static_assert(K::BYTES <= 64 * 1024, "LDS budget");
+    void (*kern)(ServeArgs);
+    if constexpr (COMMIT)
+        kern = bdgdn_k4_commit_kernel<Out, LP, CO>;
+    else
+        kern = bdgdn_k4_denoise_kernel<Out, LP>;
+    hipLaunchKernelGGL(kern, dim3(a.R * a.h_v), dim3(K::kThreads), K::BYTES, s, a);
+    return hipGetLastError();
+}
+
+template <bool COMMIT, bool CO>
+static hipError_t dispatch_stream(Types ty, int lp, const ServeArgs &a, hipStream_t s)
+{
+    if (ty == Types::BF16_IN_F32_OUT)
+        return lp == 16 ? launch_stream<float, 16, COMMIT, CO>(a, s) : launch_stream<float, 32, COMMIT, CO>(a, s);
+    return lp == 16 ? launch_stream<__bf16, 16, COMMIT, CO>(a, s) : launch_stream<__bf16, 32, COMMIT, CO>(a, s);
+}
+
 hipError_t launch_denoise(Types ty, int dk, int lp, const ServeArgs &a, hipStream_t s)
 {
+    if (stream_ok(ty, dk, lp, a)) return dispatch_stream<false, false>(ty, lp, a, s);
     if (a.dv % kServeBV || a.n_vt * kServeBV != a.dv) return hipErrorInvalidValue;
 #define BDGDN_ONE(CALL, IN, OP, OUT, DK, LP) \
     if (dk == DK && lp == LP) return launch_dn<IN, OP, OUT, DK, LP>(a, s);
@@ -144,6 +219,8 @@ hipError_t launch_denoise(Types ty, int dk, int lp, const ServeArgs &a, hipStrea
 
 hipError_t launch_commit(Types ty, int dk, int lp, bool with_o, const ServeArgs &a, hipStream_t s)
 {
+    if (stream_ok(ty, dk, lp, a))
+        return with_o ? dispatch_stream<true, true>(ty, lp, a, s) : dispatch_stream<true, false>(ty, lp, a, s);
     if (a.dv % kServeBV || a.n_vt * kServeBV != a.dv) return hipErrorInvalidValue;
 #define BDGDN_ONE(CALL, IN, OP, OUT, DK, LP) \
     if (dk == DK && lp == LP) return launch_cm<IN, OP, OUT, DK, LP>(with_o, a, s);

@@ -1,0 +1,173 @@
+// ut.hpp -- the block-local UT transform of the Gated Delta Rule held in one wave's
+// registers (Appendix "Chunk-corrected values", eq. f-blk): the cumulative gates of a
+// block by a cross-lane scan, the Gram tiles of its keys on MFMA, and
+// T = (I + A)^(-1) diag(beta) with
+//     A_ri = beta_r 2^(G_r - G_i) (k_r . k_i)   (i < r),  G = cumulative log2-gates,
+// for blocks of 16 or 32 positions.  Shared by the one-kernel training forward and the
+// serving kernels.
+#pragma once
+
+#include "common.hpp"
+
+namespace bdgdn {
+
+namespace ut {
+
+typedef _Float16 E;
+typedef f16x4 QE;
+
+template <int CTRL> __device__ __forceinline__ float dpp(float v)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, true));
+}
+__device__ __forceinline__ float lane_value(float v, int l)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+// Inclusive prefix sum over lanes 0 .. 31: shifts by 1, 2, 4, 8 inside each 16-lane row,
+// then the total of row 0 carried into row 1.
+__device__ __forceinline__ float scan32(float x, int lane)
+{
+    x += dpp<0x111>(x);
+    x += dpp<0x112>(x);
+    x += dpp<0x114>(x);
+    x += dpp<0x118>(x);
+    const float r0 = lane_value(x, 15);
+    return lane >= 16 && lane < 32 ? x + r0 : x;
+}
+__device__ __forceinline__ f32x4 mfma16(f16x4 a, f16x4 b, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 ld4f(const float *p) { return *reinterpret_cast<const f32x4 *>(p); }
+
+// Per-lane constants of the solve, element i of a 16 x 16 tile at row r = 4g + i,
+// column n: the identity, the level-1 entries of A and A^T, and for the levels
+// b = 2, 4, 8 an AND mask over the fp16 quad that keeps the entries of M_b^T (those above
+// the diagonal whose row and column differ first in bit log2 b).
+struct Consts {
+    f32x4 one, m1lo, m1up;
+    unsigned mk[3][2];
+};
+__device__ __forceinline__ void make_consts(Consts &u, int lane)
+{
+    const int g = lane >> 4, n = lane & 15;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r = 4 * g + i, xr = r ^ n;
+        u.one[i] = xr == 0 ? 1.f : 0.f;
+        u.m1lo[i] = xr == 1 && r > n ? 1.f : 0.f;
+        u.m1up[i] = xr == 1 && n > r ? 1.f : 0.f;
+    }
+#pragma unroll
+    for (int l = 0; l < 3; ++l) {
+        const int b = 2 << l;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            unsigned m = 0;
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                const int r = 4 * g + 2 * h + e, xr = r ^ n;
+                if (n > r && xr >= b && xr < 2 * b) m |= 0xffffu << (16 * e);
+            }
+            u.mk[l][h] = m;
+        }
+    }
+}
+__device__ __forceinline__ f16x4 and_mask(f16x4 q, const unsigned (&m)[2])
+{
+    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+    u32x2 w = __builtin_bit_cast(u32x2, q);
+    w[0] &= m[0];
+    w[1] &= m[1];
+    return __builtin_bit_cast(f16x4, w);
+}
+
+// T = (I + A)^(-1) diag(beta) of one block of NB x 16 positions, written row-major to
+// LDS (T, row stride ts, fp16), from the key-row quads kq[rb][kb] (lane (g, r): row
+// 16 rb + r, columns 16 kb + 4g .. + 3) and the block's cumulative log2-gates Gs and step
+// sizes Bs (LDS, one per position).
+//
+// Everything stays in registers.  With mfma16(q(X), q(Y)) = X^T Y for accumulator tiles
+// X, Y (lane (g, n) holding rows 4g .. 4g + 3 of column n), a product needs its left
+// factor as the accumulator of its transpose; so the solve carries each matrix together
+// with its transpose.  (I + A)^(-1) is built by doubling the size of the inverted
+// diagonal blocks: with D_b the inverse restricted to blocks of size b and M_b the part
+// of A between the two b-halves of each 2b block,
+//     D_2b = D_b - D_b M_b D_b,    D_2 = I - M_1,
+// which is the block lower-triangular inverse formula, so no intermediate exceeds the
+// entries of the inverse itself; the last level joins the two 16 x 16 diagonal blocks:
+// X10 = -X11 A10 X00.  Products take fp16 operands and accumulate in fp32.  T is produced
+// transposed, so each lane writes four consecutive entries of a row.  Masked entries are
+// selected, not branched on.  With log-gates g <= 0 the cumulative G is non-increasing,
+// so every decay exponent kept (G_r - G_c, r >= c) is <= 0 and is evaluated as
+// -|G_r - G_c|, which also keeps the discarded entries finite.
+template <int NB, int DKB>
+__device__ __forceinline__ void solve_t(const QE (&kq)[NB][DKB], const float *Gs, const float *Bs, E *T, int ts,
+                                        const Consts &us_, int lane)
+{
+    static_assert(NB == 1 || NB == 2, "blocks of 16 or 32 positions");
+    const int g = lane >> 4, n = lane & 15;
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    // kk[bi][bj]: lane (g, n) = k_(16 bi + 4g + i) . k_(16 bj + n)   (tile (1, 0) unused)
+    f32x4 kk[NB][NB];
+#pragma unroll
+    for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+        for (int bj = bi; bj < NB; ++bj) kk[bi][bj] = mma_q<E, DKB>(z, kq[bi], kq[bj]);
+    // per-lane gates: rows 4g + i and column n of each 16-block
+    f32x4 gr[NB], br[NB];
+    float gc[NB], bc[NB];
+#pragma unroll
+    for (int rb = 0; rb < NB; ++rb) {
+        gr[rb] = ld4f(Gs + 16 * rb + 4 * g);
+        br[rb] = ld4f(Bs + 16 * rb + 4 * g);
+        gc[rb] = Gs[16 * rb + n];
+        bc[rb] = Bs[16 * rb + n];
+    }
+    // diagonal tiles of A (below the diagonal) and A^T (above): one exponent serves both
+    f32x4 D[NB], Dt[NB];
+    f16x4 atq[NB];
+#pragma unroll
+    for (int t = 0; t < NB; ++t) {
+        f32x4 at;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float e = fexp2(-fabsf(gr[t][i] - gc[t])) * kk[t][t][i];
+            at[i] = bc[t] * e;
+            D[t][i] = fmaf(-us_.m1lo[i], br[t][i] * e, us_.one[i]);
+            Dt[t][i] = fmaf(-us_.m1up[i], at[i], us_.one[i]);
+        }
+        atq[t] = quad_of<E>(at);
+    }
+#pragma unroll
+    for (int l = 0; l < 3; ++l)
+#pragma unroll
+        for (int t = 0; t < NB; ++t) {
+            const f32x4 y = mfma16(and_mask(atq[t], us_.mk[l]), quad_of<E>(D[t]), z);   // M_b D_b
+            const f16x4 ny = quad_of<E>(-y), dtq = quad_of<E>(Dt[t]);
+            D[t] = mfma16(dtq, ny, D[t]);                                             // D_b - D_b M_b D_b
+            Dt[t] = mfma16(ny, dtq, Dt[t]);                                           // and its transpose
+        }
+    // T = X diag(beta), written as rows of T from the transposed tiles (whose entries
+    // below the diagonal are exact zeros: every product there has a zero factor)
+#pragma unroll
+    for (int t = 0; t < NB; ++t) st_quad(T + (16 * t + n) * ts + 16 * t + 4 * g, quad_of<E>(Dt[t] * br[t]));
+    if constexpr (NB == 2) {
+        // A10^T from k_(4g + i) . k_(16 + n); Y = A10 X00; X10^T = -Y^T X11^T
+        f32x4 a01;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a01[i] = bc[1] * fexp2(-fabsf(gc[1] - gr[0][i])) * kk[0][1][i];
+        const f32x4 y = mfma16(quad_of<E>(a01), quad_of<E>(D[0]), z);
+        const f32x4 x10t = mfma16(quad_of<E>(-y), quad_of<E>(Dt[1]), z);
+        f32x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = x10t[i] * br[0][i];
+        st_quad(T + (16 + n) * ts + 4 * g, quad_of<E>(v));
+        st_quad(T + n * ts + 16 + 4 * g, quad_of<E>(z));
+    }
+}
+
+}  // namespace ut
+
+}  // namespace bdgdn
