@@ -23,6 +23,9 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+ROUTES = {"fused": "fused (one kernel: per-block UT transform inside the state scan)",
+          "split": "split (clean scan writing fp32 seed states, then the noisy-block kernel)",
+          "records": "records (UT-transform kernel, then the scan)"}
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, GB/s
 MFMA16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16/bf16 MFMA, TFLOP/s
 
@@ -133,6 +136,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-serve", action="store_true")
+    ap.add_argument("--route", choices=sorted(ROUTES), default="fused",
+                    help="schedule of the training forward (fused is the performance mode; split and "
+                         "records attribute its parts to separate kernels)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run only a 256 MiB device copy (byte-counter calibration)")
     args = ap.parse_args()
@@ -159,13 +165,15 @@ def main():
     scale = 1.0 / math.sqrt(w.d_k)
     o = torch.empty(w.batch, w.seqlen, w.h_v, w.d_v, dtype=torch.float32, device=dev)
     on = torch.empty_like(o)
-    desc = bd.make_fwd_desc(d["q"], d["v"], block=w.block, scale=scale)
+    route = {"fused": bd.BDGDN_ROUTE_FUSED, "split": bd.BDGDN_ROUTE_SPLIT,
+             "records": bd.BDGDN_ROUTE_RECORDS}[args.route]
+    desc = bd.make_fwd_desc(d["q"], d["v"], block=w.block, scale=scale, route=route)
     ws = torch.empty(max(256, bd.bdgdn_fwd_train_workspace(desc)), dtype=torch.uint8, device=dev)
 
     def step():
         bd.bdgdn_fwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"],
                            d["qn"], d["kn"], d["vn"], d["gn"], d["betan"],
-                           block=w.block, scale=scale, o=o, on=on, workspace=ws, stream=stream)
+                           block=w.block, scale=scale, o=o, on=on, workspace=ws, stream=stream, route=route)
 
     torch.cuda.synchronize()
     ms = time_launches(step, args.steps, args.warmup, stream)
@@ -184,10 +192,11 @@ def main():
         "config": {"workload": w.name, "batch": w.batch, "seq_len": w.seqlen,
                    "h_qk": w.h_qk, "h_v": w.h_v, "d_k": w.d_k, "d_v": w.d_v, "block": w.block,
                    "inputs": "bf16", "mfma_operands": "fp16", "state": "fp32", "outputs": "fp32",
-                   "route": "fused (one kernel: per-block UT transform inside the state scan)", "parallelism": "none (1 GPU)"},
+                   "route": ROUTES[args.route], "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": recorded_traffic(),
-                     "kernel": "bdgdn_fwd_pipelined_kernel (the whole bdgdn_fwd_train step)",
+                     "kernel": ("bdgdn_fwd_pipelined_kernel (the whole bdgdn_fwd_train step)" if args.route == "fused"
+                                else f"the {args.route} schedule (all of its kernels)"),
                      "algorithmic_bytes": abytes, "kernel_source_hash": kernel_source_hash()},
         "mfma": {"model_flop": flops, "tflops": flops / (ms * 1e-3) / 1e12,
                  "frac_of_peak": flops / (ms * 1e-3) / 1e12 / MFMA16_PEAK_TFLOPS},

@@ -84,7 +84,12 @@ typedef enum { BDGDN_BF16 = 0, BDGDN_F32 = 1 } bdgdn_dtype_t;
  *           workgroups also compute each block's UT transform and masked Q K^T a block
  *           ahead (no workspace); otherwise it is the RECORDS schedule.
  *  SPLIT:   boundary states through HBM and a separate noisy-block kernel (Appendix
- *           "Route I").  Not available in this version (BDGDN_ERR_UNSUPPORTED).
+ *           "Route I"): the clean scan writes the clean state before every block (the
+ *           seed of that noisy block) into the workspace, fp32 [block][h_v][d_k][d_v]
+ *           (blocks of all sequences, or of the packed axis, in order), then every
+ *           noisy block is evaluated in parallel from its seed.  The clean outputs and
+ *           ht equal FUSED's bit for bit.  bf16 inputs, d_k = d_v = 128 and blocks of at
+ *           most 32 positions only (else BDGDN_ERR_UNSUPPORTED).
  *  ONEPASS: one kernel per (sequence, v-head, d_v tile) that recomputes the UT
  *           transform of each block itself, without overlap.  No workspace.
  *  RECORDS: two kernels: the UT transform and masked Q K^T of every (block, v-head)

@@ -64,7 +64,11 @@ int check_fwd(const bdgdn_fwd_desc_t *d, const int32_t *cu_dev, const int32_t *c
         for (int i = 0; i < d->num_seqs; ++i)
             if (cu_host[i] % d->block != 0) return BDGDN_ERR_UNALIGNED;
     }
-    if (d->route == BDGDN_ROUTE_SPLIT) return BDGDN_ERR_UNSUPPORTED;   // not built yet
+    if (d->route == BDGDN_ROUTE_SPLIT) {
+        Types ty;
+        types_of(d->dtype, d->out_dtype, ty);
+        if (!split_supported(ty, d->d_k, d->d_v, lp_of(d->block))) return BDGDN_ERR_UNSUPPORTED;
+    }
     return BDGDN_OK;
 }
 
@@ -103,9 +107,13 @@ static bool one_kernel(const bdgdn_fwd_desc_t *d, Types ty)
 
 static size_t workspace_bytes_of(const bdgdn_fwd_desc_t *d)
 {
-    if (d->route != BDGDN_ROUTE_FUSED && d->route != BDGDN_ROUTE_RECORDS) return 0;
     Types ty;
     types_of(d->dtype, d->out_dtype, ty);
+    if (d->route == BDGDN_ROUTE_SPLIT) {
+        if (!split_supported(ty, d->d_k, d->d_v, lp_of(d->block))) return 0;
+        return (size_t)total_blocks(d) * d->h_v * d->d_k * d->d_v * sizeof(float);   // seed states
+    }
+    if (d->route != BDGDN_ROUTE_FUSED && d->route != BDGDN_ROUTE_RECORDS) return 0;
     if (one_kernel(d, ty)) return 0;
     return (size_t)total_blocks(d) * d->h_v * scan_record_bytes(ty, lp_of(d->block));
 }
@@ -158,7 +166,7 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         n_order = nseq;
     }
     hipError_t e;
-    if (desc->route == BDGDN_ROUTE_FUSED || desc->route == BDGDN_ROUTE_RECORDS) {
+    if (desc->route != BDGDN_ROUTE_ONEPASS) {
         IntraArgs ia;
         ia.q = q; ia.k = k; ia.qn = qn; ia.kn = kn;
         ia.g = g; ia.beta = beta; ia.gn = gn; ia.betan = betan;
@@ -173,6 +181,7 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         sa.cu = packed ? cu_seqlens_dev : nullptr;
         sa.h0 = h0; sa.ht = ht; sa.o = o; sa.on = on;
         sa.ws = static_cast<const unsigned char *>(workspace);
+        sa.bs = desc->route == BDGDN_ROUTE_SPLIT ? static_cast<float *>(workspace) : nullptr;
         sa.T = desc->seqlen; sa.L = desc->block; sa.nblk = ia.nblk;
         sa.h_qk = desc->h_qk; sa.h_v = desc->h_v; sa.dv = desc->d_v;
         sa.n_chains = nseq * desc->h_v;
@@ -180,8 +189,22 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         sa.scale = desc->scale;
         sa.n_order = n_order;
         for (int i = 0; i < n_order; ++i) sa.order[i] = order[i];
-        e = one_kernel(desc, ty) ? launch_fwd_pipelined(ty, desc->d_k, lp, sa, strm)
-                                 : launch_fwd_scan(ty, desc->d_k, lp, ia, sa, strm);
+        if (desc->route == BDGDN_ROUTE_SPLIT) {
+            NoisyArgs na;
+            na.qn = qn; na.kn = kn; na.vn = vn; na.gn = gn; na.betan = betan;
+            na.bs = sa.bs;
+            na.cu = sa.cu;
+            na.on = on;
+            na.T = desc->seqlen; na.L = desc->block; na.nblk = ia.nblk;
+            na.n_docs = packed ? nseq : 0;
+            na.total_blocks = ia.total_blocks;
+            na.h_qk = desc->h_qk; na.h_v = desc->h_v;
+            na.scale = desc->scale;
+            e = launch_fwd_split(ty, lp, sa, na, strm);
+        } else {
+            e = one_kernel(desc, ty) ? launch_fwd_pipelined(ty, desc->d_k, lp, sa, strm)
+                                     : launch_fwd_scan(ty, desc->d_k, lp, ia, sa, strm);
+        }
     } else {
         FwdArgs a;
         a.q = q; a.k = k; a.v = v; a.qn = qn; a.kn = kn; a.vn = vn;

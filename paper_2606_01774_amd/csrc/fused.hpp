@@ -25,15 +25,23 @@
 #pragma once
 
 #include "intra.hpp"
+#include "kernels.hpp"
 #include "ut.hpp"
 
 namespace bdgdn {
 
-template <typename Out, int DK, int LP>
+// SPLIT: the clean scan alone (the first kernel of the split schedule, Appendix "Route
+// I"): the noisy waves and the noisy half of the record stand idle, the noisy rows are not
+// staged, and the C waves write each block's seed state (the clean state before the
+// block) to HBM for a separate noisy-block kernel.
+template <typename Out, int DK, int LP, bool SPLIT = false>
 struct Fused {
     typedef __bf16 In;
     typedef _Float16 E;
     typedef Quad<E> QE;
+    typedef Out OutT;
+    static constexpr int DKC = DK;
+    static constexpr bool kSplit = SPLIT;
     static constexpr int NW = 12, kThreads = 64 * NW;
     static constexpr int BV = 32, NVB = 2;
     static constexpr int NB = LP / 16, DKB = DK / 16;
@@ -64,6 +72,7 @@ struct Fused {
     static_assert(BYTES <= 160 * 1024, "LDS budget");
     // staging team
     static constexpr int TT = 256;
+    static constexpr int NSETS = SPLIT ? 2 : 4;           // row sets staged per block
     static constexpr int OCH = LP * CPR;                  // chunks per row set
     static constexpr int OPS = (OCH + TT - 1) / TT;
     static constexpr int VCPR = BV / 8, VPS = LP * VCPR;  // V chunks per stream
@@ -141,6 +150,8 @@ struct Fused {
         int qks, vst, gst;           // row strides (elements)
         long len;
         int L;
+        float *bs;     // SPLIT: seed state of the chain's first block (column v0), or null
+        long bs_blk;   // per-block advance of bs (elements)
         const float *h0;
         float *ht;
         int dv;
@@ -181,7 +192,7 @@ struct Fused {
         unsigned vg[VPL], vl[VPL];   // V: global byte offset, LDS byte offset in a set
     };
     struct RowsF {
-        u32x4 c[4][OPS];
+        u32x4 c[NSETS][OPS];
     };
     struct VF {
         u32x4 c[VPL];
@@ -202,7 +213,7 @@ struct Fused {
         for (int u = 0; u < VPL; ++u) {
             // slot u of team wave tw covers chunks vb .. vb + 63 of [V | V~]
             const int vb = v_base(tw, u);
-            const bool ok = vb < 2 * VPS;
+            const bool ok = vb < (SPLIT ? 1 : 2) * VPS;
             const int m = vb / VPS, ch = (ok ? vb % VPS : 0) + lane, t = ch / VCPR, cc = ch % VCPR;
             o.vg[u] = ok ? (unsigned)(t * c.vst * 2 + cc * 16) : 0u;
             o.vl[u] = ok ? (unsigned)(m * V_B + (t * VS + cc * 8) * 2) : sink;
@@ -242,7 +253,7 @@ struct Fused {
 #pragma unroll
         for (int u = 0; u < OPS; ++u)
 #pragma unroll
-            for (int si = 0; si < 4; ++si) f.c[si][u] = bload(r.r[si], o.rg[u]);
+            for (int si = 0; si < NSETS; ++si) f.c[si][u] = bload(r.r[si], o.rg[u]);
     }
     __device__ __forceinline__ void fetch_v(const Ptrs &P, const Chain &c, int nvalid, int tw, const LOffs &o, VF &f) const
     {
@@ -257,7 +268,7 @@ struct Fused {
 #pragma unroll
         for (int u = 0; u < OPS; ++u)
 #pragma unroll
-            for (int si = 0; si < 4; ++si) {
+            for (int si = 0; si < NSETS; ++si) {
                 st16(smem + slot * RING_B + si * ROWS_B, o.rl[u], to_operand<In, E>(f.c[si][u]));
                 f.c[si][u] = bload(r.r[si], o.rg[u]);
             }
@@ -565,7 +576,16 @@ struct Fused {
             write_st(0, sq, bc, qo);
             lds_barrier();
             lds_barrier();
+            float *bs = c.bs;
             for (int j = 0; j < nb; ++j) {
+                if constexpr (SPLIT) {
+                    // the seed of noisy block j: the clean state before block j
+#pragma unroll
+                    for (int kb = 0; kb < DKB; ++kb)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) bs[(long)(16 * kb + 4 * g + i) * c.dv + 16 * bc + n] = S[kb][i];
+                    bs += c.bs_blk;
+                }
                 c_block(j % 3, j & 1, j & 1, bc, S, sq, qo);
                 write_st((j + 1) & 1, sq, bc, qo);
                 lds_barrier();
@@ -578,6 +598,11 @@ struct Fused {
                     for (int i = 0; i < 4; ++i) dst[i * c.dv] = S[kb][i];
                 }
             }
+        } else if (SPLIT && (wave < 4 || wave == 7)) {
+            // ---- idle in the split schedule: keep the barrier count
+            lds_barrier();
+            lds_barrier();
+            for (int j = 0; j < nb; ++j) lds_barrier();
         } else if (wave < 4) {
             // ---- N
             const int bc = wave - 2;
@@ -660,5 +685,76 @@ struct Fused {
         }
     }
 };
+
+// One workgroup's chain: (sequence or document, v-head, d_v tile) from the block id.  Ids
+// i, i+8, i+16, ... of a group carry the d_v tiles of one chain, so they land on one XCD
+// and share its L2 for the q/k rows and gates.
+template <typename K>
+__device__ __forceinline__ void run_chain(const ScanArgs &a, unsigned char *smem)
+{
+    static_assert(K::kThreads == 768, "launch bounds");
+    typedef typename K::In In;
+    typedef typename K::OutT Out;
+    constexpr int DK = K::DKC;
+    const int id = blockIdx.x;
+    const int per = 8 * a.n_vt;
+    const int chain = (id / per) * 8 + (id % 8);
+    const int vt = (id % per) / 8;
+    if (chain >= a.n_chains) return;
+    int seq = chain / a.h_v;
+    const int h = chain % a.h_v;
+    if (a.n_order > 0) seq = a.order[seq];
+    long base, len;
+    if (a.cu) {
+        base = a.cu[seq];
+        len = (long)a.cu[seq + 1] - base;
+    } else {
+        base = (long)seq * a.T;
+        len = a.T;
+    }
+    const int hq = h / (a.h_v / a.h_qk);
+    const int v0 = vt * K::BV;
+    typename K::Chain c;
+    const long qk_off = (base * a.h_qk + hq) * DK;
+    const long v_off = (base * a.h_v + h) * a.dv + v0;
+    const long g_off = base * a.h_v + h;
+    c.p0.k = static_cast<const In *>(a.k) + qk_off;
+    c.p0.q = static_cast<const In *>(a.q) + qk_off;
+    c.p0.kn = static_cast<const In *>(a.kn) + qk_off;
+    c.p0.qn = static_cast<const In *>(a.qn) + qk_off;
+    c.p0.v = static_cast<const In *>(a.v) + v_off;
+    c.p0.vn = static_cast<const In *>(a.vn) + v_off;
+    c.p0.g = a.g + g_off;
+    c.p0.beta = a.beta + g_off;
+    c.p0.gn = a.gn + g_off;
+    c.p0.betan = a.betan + g_off;
+    c.p0.o = static_cast<Out *>(a.o) + v_off;
+    c.p0.on = static_cast<Out *>(a.on) + v_off;
+    c.qks = a.h_qk * DK;
+    c.vst = a.h_v * a.dv;
+    c.gst = a.h_v;
+    c.qk_blk = (long)a.L * c.qks;
+    c.v_blk = (long)a.L * c.vst;
+    c.g_blk = (long)a.L * c.gst;
+    c.len = len;
+    c.L = a.L;
+    const long state_off = ((long)seq * a.h_v + h) * DK * a.dv + v0;
+    c.h0 = a.h0 ? a.h0 + state_off : nullptr;
+    if constexpr (K::kSplit) {
+        // seed states by global block: documents start on block boundaries, sequences
+        // own ceil(T / L) blocks each
+        const long gblk0 = a.cu ? base / a.L : (long)seq * a.nblk;
+        c.bs = a.bs + (gblk0 * a.h_v + h) * DK * a.dv + v0;
+        c.bs_blk = (long)a.h_v * DK * a.dv;
+    } else {
+        c.bs = nullptr;
+        c.bs_blk = 0;
+    }
+    c.ht = a.ht ? a.ht + state_off : nullptr;
+    c.dv = a.dv;
+    c.scale = a.scale;
+    K k(smem);
+    k.run(c);
+}
 
 }  // namespace bdgdn

@@ -12,60 +12,7 @@ template <typename Out, int DK, int LP>
 __global__ void __launch_bounds__(768) bdgdn_fwd_pipelined_kernel(ScanArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    typedef Fused<Out, DK, LP> K;
-    static_assert(K::kThreads == 768, "launch bounds");
-    typedef typename K::In In;
-    // ids i, i+8, i+16, ... of a group carry the d_v tiles of one chain, so they land
-    // on one XCD and share its L2 for the q/k rows and gates.
-    const int id = blockIdx.x;
-    const int per = 8 * a.n_vt;
-    const int chain = (id / per) * 8 + (id % 8);
-    const int vt = (id % per) / 8;
-    if (chain >= a.n_chains) return;
-    int seq = chain / a.h_v;
-    const int h = chain % a.h_v;
-    if (a.n_order > 0) seq = a.order[seq];
-    long base, len;
-    if (a.cu) {
-        base = a.cu[seq];
-        len = (long)a.cu[seq + 1] - base;
-    } else {
-        base = (long)seq * a.T;
-        len = a.T;
-    }
-    const int hq = h / (a.h_v / a.h_qk);
-    const int v0 = vt * K::BV;
-    typename K::Chain c;
-    const long qk_off = (base * a.h_qk + hq) * DK;
-    const long v_off = (base * a.h_v + h) * a.dv + v0;
-    const long g_off = base * a.h_v + h;
-    c.p0.k = static_cast<const In *>(a.k) + qk_off;
-    c.p0.q = static_cast<const In *>(a.q) + qk_off;
-    c.p0.kn = static_cast<const In *>(a.kn) + qk_off;
-    c.p0.qn = static_cast<const In *>(a.qn) + qk_off;
-    c.p0.v = static_cast<const In *>(a.v) + v_off;
-    c.p0.vn = static_cast<const In *>(a.vn) + v_off;
-    c.p0.g = a.g + g_off;
-    c.p0.beta = a.beta + g_off;
-    c.p0.gn = a.gn + g_off;
-    c.p0.betan = a.betan + g_off;
-    c.p0.o = static_cast<Out *>(a.o) + v_off;
-    c.p0.on = static_cast<Out *>(a.on) + v_off;
-    c.qks = a.h_qk * DK;
-    c.vst = a.h_v * a.dv;
-    c.gst = a.h_v;
-    c.qk_blk = (long)a.L * c.qks;
-    c.v_blk = (long)a.L * c.vst;
-    c.g_blk = (long)a.L * c.gst;
-    c.len = len;
-    c.L = a.L;
-    const long state_off = ((long)seq * a.h_v + h) * DK * a.dv + v0;
-    c.h0 = a.h0 ? a.h0 + state_off : nullptr;
-    c.ht = a.ht ? a.ht + state_off : nullptr;
-    c.dv = a.dv;
-    c.scale = a.scale;
-    K k(smem);
-    k.run(c);
+    run_chain<Fused<Out, DK, LP>>(a, smem);
 }
 
 template <typename Out, int DK, int LP>

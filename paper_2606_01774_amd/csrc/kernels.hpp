@@ -41,11 +41,25 @@ struct ScanArgs {
     float *ht;
     void *o, *on;
     const unsigned char *ws;
+    float *bs;           // split schedule: seed states by (global block, v-head), or null
     int T, L, nblk, h_qk, h_v, dv;
     int n_chains, n_vt;
     float scale;
     int n_order;
     int order[kMaxOrder];
+};
+
+// Noisy-block pass of the split schedule (one workgroup per (global block, v-head)).
+struct NoisyArgs {
+    const void *qn, *kn, *vn;
+    const float *gn, *betan;
+    const float *bs;     // seed states [global block][h_v][d_k][d_v]
+    const int32_t *cu;   // device cu_seqlens or NULL
+    void *on;
+    int T, L, nblk, n_docs;   // tokens per sequence (packed: total), block, blocks per sequence
+    long total_blocks;
+    int h_qk, h_v;
+    float scale;
 };
 
 struct ServeArgs {
@@ -76,6 +90,10 @@ hipError_t launch_fwd_scan(Types ty, int dk, int lp, const IntraArgs &ia, const 
 // inputs, blocks of at most 32 positions.
 bool pipelined_supported(Types ty, int dk, int lp);
 hipError_t launch_fwd_pipelined(Types ty, int dk, int lp, const ScanArgs &a, hipStream_t s);
+// The split schedule (clean scan exposing the seed states, then the noisy-block pass):
+// bf16 inputs, d_k = d_v = 128, blocks of at most 32 positions.
+bool split_supported(Types ty, int dk, int dv, int lp);
+hipError_t launch_fwd_split(Types ty, int lp, const ScanArgs &sa, const NoisyArgs &na, hipStream_t s);
 size_t scan_record_bytes(Types ty, int lp);
 int scan_tile_v();
 // d_v columns handled by one workgroup of the training / serving kernels.

@@ -106,6 +106,20 @@ def test_workspace_query():
     assert _fwd(_desc(block=64)) == bd.BDGDN_ERR_WORKSPACE
 
 
+def test_split_route_limits_and_workspace():
+    """The split schedule runs bf16 inputs with d_k = d_v = 128 and blocks up to 32; its
+    workspace holds one fp32 seed state per (block, v-head)."""
+    split = dict(route=bd.BDGDN_ROUTE_SPLIT)
+    for kw in (dict(d_k=64, d_v=64), dict(d_v=64), dict(block=64),
+               dict(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32)):
+        assert _fwd(_desc(**split, **kw)) == bd.BDGDN_ERR_UNSUPPORTED, kw
+        assert bd.bdgdn_fwd_train_workspace(_desc(**split, **kw)) == 0
+    # 64 tokens in blocks of 32 -> 2 blocks; 100 tokens in blocks of 16 -> 7 blocks
+    assert bd.bdgdn_fwd_train_workspace(_desc(**split)) == 2 * 4 * 128 * 128 * 4
+    assert bd.bdgdn_fwd_train_workspace(_desc(**split, seqlen=100, block=16, batch=3)) == 3 * 7 * 4 * 128 * 128 * 4
+    assert _fwd(_desc(**split)) == bd.BDGDN_ERR_WORKSPACE
+
+
 def _serve(fn, **kw):
     d = dict(num_req=4, h_qk=2, h_v=4, d_k=128, d_v=128, block=32, scale=0.1, dtype=bd.BDGDN_BF16,
              out_dtype=bd.BDGDN_F32)

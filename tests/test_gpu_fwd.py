@@ -86,6 +86,30 @@ def test_routes_agree(L):
             assert e <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("B,T,hqk,hv,L,lengths", [
+    (2, 200, 2, 2, 32, None),           # ragged tail
+    (1, 256, 2, 4, 32, None),           # grouped value heads
+    (1, 150, 1, 2, 16, None),
+    (1, 70, 1, 1, 5, None),             # small block, padded to 16
+    (1, 401, 2, 2, 32, [64, 96, 0, 32, 192, 17]),   # packed, an empty and a ragged doc
+])
+def test_split_route(B, T, hqk, hv, L, lengths):
+    """The split schedule (clean scan writing the seed states, then the noisy-block kernel)
+    against the oracle, and against the fused schedule: the same clean arithmetic, and
+    noisy outputs within rounding of each other."""
+    inp = W.make_custom_train(B, T, hqk, hv, 128, 128, "bf16", seed=500 + T + L, lengths=lengths)
+    h0 = None if lengths else torch.randn(B, hv, 128, 128, generator=torch.Generator().manual_seed(L)) * 0.3
+    o, on, ht = _check_full(inp, L, "bf16", h0=h0, route=bd.BDGDN_ROUTE_SPLIT)
+    d = to_dev(inp)
+    if lengths:
+        d["cu_host"] = inp["cu_seqlens"]
+    fo, fon, fht = _run_gpu(d, L, 1.0 / math.sqrt(128), h0=None if h0 is None else h0.cuda())
+    assert torch.equal(o, fo) and torch.equal(ht, fht)
+    e = rel_err(on, fon.double().cpu().numpy())
+    print(f"split vs fused noisy difference {e:.3e}")
+    assert e <= TOL["bf16"]
+
+
 def test_packed_equals_separate_bitwise():
     """Packing reproduces per-document results exactly (Appendix, packing contract)."""
     lengths = [96, 64, 40]
