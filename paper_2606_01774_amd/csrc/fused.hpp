@@ -82,11 +82,20 @@ struct Fused {
     unsigned char *smem;
     int tid, lane, wave;
 
+    // Role of each hardware wave.  Wave w of the workgroup runs on SIMD w mod 4, and the
+    // roles are placed so that the three waves of each SIMD carry similar work (measured
+    // per-role busy cycles): SIMD 0 and 1 hold C, N and O; SIMD 2 and 3 hold U and two L.
+    // `wave` below is the role index: 0-1 C, 2-3 N, 4-5 O, 6-7 U, 8-11 L.
+    __device__ __forceinline__ static int role_of(int w)
+    {
+        return w < 2 ? w : w < 4 ? w + 6 : w < 6 ? w - 2 : w < 8 ? w : w < 10 ? w - 4 : w;
+    }
+
     __device__ Fused(unsigned char *s) : smem(s)
     {
         tid = threadIdx.x;
         lane = tid & 63;
-        wave = wave_id();
+        wave = role_of(wave_id());
     }
 
     // ------------------------------------------------------------------ layout
