@@ -5,9 +5,9 @@ over the 4 x 4096-token, 16-head, d=128, L=32 workload with bf16 inputs, fp32
 state and fp32 outputs, inputs resident in HBM.  `value` is tokens/s (clean +
 noisy tokens).  The line also carries the roofline of the fused kernel (HBM
 bytes the algorithm must move per launch over its measured duration), the
-model-FLOP rate against the bf16/fp16 MFMA peak, the denoise_step bandwidth of
-the 64-request serving workload, and the fp64 CPU oracle timed on a bounded
-sample of the same workload.
+model-FLOP rate against the bf16/fp16 MFMA peak, the denoise_step and commit
+bandwidths of the 64-request serving workload, and the fp64 CPU oracle timed on
+the same workload.
 
   python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
 """
@@ -55,6 +55,15 @@ def algorithmic_bytes_denoise(w, out_bytes):
                            + 2 * w.h_v * 4)
 
 
+def algorithmic_bytes_commit(w):
+    """The state pass without outputs: the fp32 state read and written back, and the
+    block's k, v, g, beta read once (q is not needed without outputs)."""
+    in_b = 2 if w.dtype == "bf16" else 4
+    rows = w.requests * w.block
+    state = w.requests * w.h_v * w.d_k * w.d_v * 4
+    return 2 * state + rows * (w.h_qk * w.d_k * in_b + w.h_v * w.d_v * in_b + 2 * w.h_v * 4)
+
+
 def time_launches(fn, steps, warmup, stream):
     import torch
     for _ in range(warmup):
@@ -89,16 +98,19 @@ def cpu_baseline(w, inp):
                       f"({w.seqlen} clean + {w.seqlen} noisy) tokens in fp64; value = tokens / wall time"}
 
 
+# The sources the one-kernel forward is built from (its translation unit and headers).
+FUSED_SOURCES = ("common.hpp", "fused.hpp", "fused_kernels.hip", "intra.hpp", "kernels.hpp", "ut.hpp")
+
+
 def kernel_source_hash():
-    """Hash of the HIP sources, to tell whether a recorded counter measurement still
-    describes the kernels being timed."""
+    """Hash of the one-kernel forward's sources, to tell whether a recorded counter
+    measurement still describes the kernel being timed."""
     import hashlib
     h = hashlib.sha256()
     src = os.path.join(ROOT, "paper_2606_01774_amd", "csrc")
-    for name in sorted(os.listdir(src)):
-        if name.endswith((".hip", ".hpp")):
-            with open(os.path.join(src, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+    for name in FUSED_SOURCES:
+        with open(os.path.join(src, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()[:16]
 
 
@@ -221,7 +233,20 @@ def main():
         result["denoise_step"] = {"workload": sw.name, "us_per_call": dms * 1e3,
                                   "gb_per_s": gbs, "frac_hbm": gbs / HBM_PEAK_GBS,
                                   "algorithmic_bytes": dbytes,
-                                  "tokens_per_s": sw.requests * sw.block / (dms * 1e-3)}
+                                  "tokens_per_s": sw.requests * sw.block / (dms * 1e-3),
+                                  "kernel": "bdgdn_k4_denoise_kernel"}
+
+        def cstep():
+            pool = pools[it[0] % len(pools)]
+            it[0] += 1
+            bd.bdgdn_commit(pool, blk["q"], blk["k"], blk["v"], blk["g"], blk["beta"],
+                            scale=scale, stream=stream)
+        cms = time_launches(cstep, 3 * args.steps, args.warmup, stream)
+        cbytes = algorithmic_bytes_commit(sw)
+        cgbs = cbytes / (cms * 1e-3) / 1e9
+        result["commit"] = {"workload": sw.name, "us_per_call": cms * 1e3, "gb_per_s": cgbs,
+                            "frac_hbm": cgbs / HBM_PEAK_GBS, "algorithmic_bytes": cbytes,
+                            "kernel": "bdgdn_k4_commit_kernel (state written back, no outputs)"}
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, inp)
