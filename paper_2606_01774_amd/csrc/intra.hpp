@@ -17,6 +17,7 @@
 #pragma once
 
 #include "common.hpp"
+#include "ut.hpp"
 
 namespace bdgdn {
 
@@ -60,7 +61,10 @@ struct Intra {
     static constexpr int NB = LP / 16;
     static constexpr int NL = NB * (NB + 1) / 2;
     static constexpr int NF = NB * NB;
-    static constexpr int NG = 2 * NL + 2 * NF;   // KK lower, QK full, KnKn lower, QnKn full
+    // bf16 inputs: T by the register-resident doubling solve (ut::solve_t, fp16 operands),
+    // which forms K K^T itself; fp32 inputs: fp32 forward substitution from A in LDS.
+    static constexpr bool REG = sizeof(Mid) == 2;
+    static constexpr int NG = REG ? 2 * NF : 2 * NL + 2 * NF;   // [KK lower] QK full [KnKn lower] QnKn full
     static constexpr int NGW = (NG + NW - 1) / NW;
     static constexpr int RS = DK + Mma<Row>::kPad;
     static constexpr int FS = LP + 4;
@@ -154,6 +158,13 @@ struct Intra {
     __device__ __forceinline__ void decode(int idx, int &kind, int &bi, int &bj) const
     {
         int l = idx;
+        if constexpr (REG) {
+            kind = l < NF ? 1 : 3;
+            l %= NF;
+            bi = l / NB;
+            bj = l % NB;
+            return;
+        }
         if (l < NL) { kind = 0; tri_decode(l, bi, bj); return; }
         l -= NL;
         if (l < NF) { kind = 1; bi = l / NB; bj = l % NB; return; }
@@ -222,7 +233,33 @@ struct Intra {
         }
     }
 
-    // (I + A)^{-1} in place for the clean (m = 0) and noisy (m = 1) blocks, then
+    // bf16 inputs: the key rows of the wave's stream (wave 0 clean, wave 1 noisy) as fp16
+    // quads (bf16 -> fp16 is exact in range), read while the row buffers are alive; then
+    // T = (I + A)^(-1) diag(beta) in registers (ut::solve_t), written to the stage.
+    static constexpr int DKB = DK / 16;
+    typedef ut::QE QE;
+    __device__ __forceinline__ void key_quads(QE (&kq)[NB][DKB]) const
+    {
+        const Row *K = rows(wave == 0 ? 0 : 2);
+        const int r = lane & 15, c4 = 4 * (lane >> 4);
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb)
+#pragma unroll
+            for (int kb = 0; kb < DKB; ++kb) {
+                const Row *src = K + (16 * rb + r) * RS + 16 * kb + c4;
+                kq[rb][kb] = QE{(_Float16)to_f(src[0]), (_Float16)to_f(src[1]), (_Float16)to_f(src[2]),
+                                (_Float16)to_f(src[3])};
+            }
+    }
+    __device__ __forceinline__ void solve_reg(const QE (&kq)[NB][DKB]) const
+    {
+        ut::Consts cs;
+        ut::make_consts(cs, lane);
+        ut::solve_t<NB, DKB>(kq, gates(wave == 0 ? 0 : 2), gates(wave == 0 ? 1 : 3),
+                             reinterpret_cast<_Float16 *>(stg(wave)), LP, cs, lane);
+    }
+
+    // fp32 inputs: (I + A)^{-1} in place for the clean (m = 0) and noisy (m = 1) blocks, then
     // T = (I + A)^{-1} diag(beta) staged as Mid.  Diagonal 16x16 blocks by forward
     // substitution (one column per lane), then row-block by row-block:
     //   X_ij = -X_ii sum_{k=j}^{i-1} A_ik X_kj.
@@ -302,10 +339,18 @@ struct Intra {
         if (wave == 1) scan_gates(2);
         f32x4 acc[NGW];
         gram(acc);
-        lds_barrier();   // row buffers are dead from here on
-        epilogue(acc);
-        lds_barrier();
-        solve();
+        if constexpr (REG) {
+            QE kq[NB][DKB];
+            if (wave < 2) key_quads(kq);
+            lds_barrier();   // row buffers are dead from here on
+            epilogue(acc);   // P, R to the stage
+            if (wave < 2) solve_reg(kq);   // T, T~ to the stage
+        } else {
+            lds_barrier();   // row buffers are dead from here on
+            epilogue(acc);
+            lds_barrier();
+            solve();
+        }
         lds_barrier();
         store(rec);
     }

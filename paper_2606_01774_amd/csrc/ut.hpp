@@ -3,8 +3,8 @@
 // block by a cross-lane scan, the Gram tiles of its keys on MFMA, and
 // T = (I + A)^(-1) diag(beta) with
 //     A_ri = beta_r 2^(G_r - G_i) (k_r . k_i)   (i < r),  G = cumulative log2-gates,
-// for blocks of 16 or 32 positions.  Shared by the one-kernel training forward and the
-// serving kernels.
+// for blocks of 16, 32 or 64 positions.  Shared by the one-kernel training forward, the
+// serving kernels and the UT-transform kernel of the two-kernel schedule.
 #pragma once
 
 #include "common.hpp"
@@ -83,10 +83,11 @@ __device__ __forceinline__ f16x4 and_mask(f16x4 q, const unsigned (&m)[2])
     return __builtin_bit_cast(f16x4, w);
 }
 
-// T = (I + A)^(-1) diag(beta) of one block of NB x 16 positions, written row-major to
-// LDS (T, row stride ts, fp16), from the key-row quads kq[rb][kb] (lane (g, r): row
-// 16 rb + r, columns 16 kb + 4g .. + 3) and the block's cumulative log2-gates Gs and step
-// sizes Bs (LDS, one per position).
+// T = (I + A)^(-1) diag(beta) of one block of NB x 16 positions (NB = 1, 2 or 4), written
+// row-major to LDS (T, row stride ts, fp16, every entry including the zeros above the
+// diagonal), from the key-row quads kq[rb][kb] (lane (g, r): row 16 rb + r, columns
+// 16 kb + 4g .. + 3) and the block's cumulative log2-gates Gs and step sizes Bs (LDS, one
+// per position).
 //
 // Everything stays in registers.  With mfma16(q(X), q(Y)) = X^T Y for accumulator tiles
 // X, Y (lane (g, n) holding rows 4g .. 4g + 3 of column n), a product needs its left
@@ -96,20 +97,22 @@ __device__ __forceinline__ f16x4 and_mask(f16x4 q, const unsigned (&m)[2])
 // of A between the two b-halves of each 2b block,
 //     D_2b = D_b - D_b M_b D_b,    D_2 = I - M_1,
 // which is the block lower-triangular inverse formula, so no intermediate exceeds the
-// entries of the inverse itself; the last level joins the two 16 x 16 diagonal blocks:
-// X10 = -X11 A10 X00.  Products take fp16 operands and accumulate in fp32.  T is produced
-// transposed, so each lane writes four consecutive entries of a row.  Masked entries are
-// selected, not branched on.  With log-gates g <= 0 the cumulative G is non-increasing,
-// so every decay exponent kept (G_r - G_c, r >= c) is <= 0 and is evaluated as
-// -|G_r - G_c|, which also keeps the discarded entries finite.
+// entries of the inverse itself.  Inside a 16 x 16 tile the levels b = 1 .. 8 run on all
+// diagonal tiles at once; the 16 -> 32 level joins pairs of tiles (X10 = -X11 A10 X00) and
+// the 32 -> 64 level the two 32-blocks (X_hl = -X_hh A_hl X_ll, 2 x 2 tiles each).
+// Products take fp16 operands and accumulate in fp32.  T is written from transposed tiles,
+// so each lane writes four consecutive entries of a row.  Masked entries are selected, not
+// branched on.  With log-gates g <= 0 the cumulative G is non-increasing, so every decay
+// exponent kept (G_r - G_c, r >= c) is <= 0 and is evaluated as -|G_r - G_c|, which also
+// keeps the discarded entries finite.
 template <int NB, int DKB>
 __device__ __forceinline__ void solve_t(const QE (&kq)[NB][DKB], const float *Gs, const float *Bs, E *T, int ts,
                                         const Consts &us_, int lane)
 {
-    static_assert(NB == 1 || NB == 2, "blocks of 16 or 32 positions");
+    static_assert(NB == 1 || NB == 2 || NB == 4, "blocks of 16, 32 or 64 positions");
     const int g = lane >> 4, n = lane & 15;
     const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-    // kk[bi][bj]: lane (g, n) = k_(16 bi + 4g + i) . k_(16 bj + n)   (tile (1, 0) unused)
+    // kk[bi][bj]: lane (g, n) = k_(16 bi + 4g + i) . k_(16 bj + n)   (bi <= bj only)
     f32x4 kk[NB][NB];
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi)
@@ -125,6 +128,18 @@ __device__ __forceinline__ void solve_t(const QE (&kq)[NB][DKB], const float *Gs
         gc[rb] = Gs[16 * rb + n];
         bc[rb] = Bs[16 * rb + n];
     }
+    // (A_(bj, bi))^T for bi < bj: lane (g, n) = A[16 bj + n][16 bi + 4g + i]
+    auto a_t = [&](int bi, int bj) {
+        f32x4 a;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a[i] = bc[bj] * fexp2(-fabsf(gc[bj] - gr[bi][i])) * kk[bi][bj][i];
+        return a;
+    };
+    // T tile (bi, bj) from the accumulator of its transpose X_(bi, bj)^T (times beta of the
+    // columns)
+    auto put = [&](int bi, int bj, f32x4 xt) {
+        st_quad(T + (16 * bi + n) * ts + 16 * bj + 4 * g, quad_of<E>(xt * br[bj]));
+    };
     // diagonal tiles of A (below the diagonal) and A^T (above): one exponent serves both
     f32x4 D[NB], Dt[NB];
     f16x4 atq[NB];
@@ -149,22 +164,43 @@ __device__ __forceinline__ void solve_t(const QE (&kq)[NB][DKB], const float *Gs
             D[t] = mfma16(dtq, ny, D[t]);                                             // D_b - D_b M_b D_b
             Dt[t] = mfma16(ny, dtq, Dt[t]);                                           // and its transpose
         }
-    // T = X diag(beta), written as rows of T from the transposed tiles (whose entries
-    // below the diagonal are exact zeros: every product there has a zero factor)
+    // the diagonal tiles of T (their entries above the diagonal are exact zeros: every
+    // product there has a zero factor)
 #pragma unroll
-    for (int t = 0; t < NB; ++t) st_quad(T + (16 * t + n) * ts + 16 * t + 4 * g, quad_of<E>(Dt[t] * br[t]));
-    if constexpr (NB == 2) {
-        // A10^T from k_(4g + i) . k_(16 + n); Y = A10 X00; X10^T = -Y^T X11^T
-        f32x4 a01;
+    for (int t = 0; t < NB; ++t) put(t, t, Dt[t]);
+    if constexpr (NB >= 2) {
+        // 16 -> 32: per pair (2p, 2p + 1), Y = A10 X00, X10 = -X11 Y (and its transpose)
+        f32x4 x10[NB / 2], x10t[NB / 2];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) a01[i] = bc[1] * fexp2(-fabsf(gc[1] - gr[0][i])) * kk[0][1][i];
-        const f32x4 y = mfma16(quad_of<E>(a01), quad_of<E>(D[0]), z);
-        const f32x4 x10t = mfma16(quad_of<E>(-y), quad_of<E>(Dt[1]), z);
-        f32x4 v;
+        for (int pr = 0; pr < NB / 2; ++pr) {
+            const int lo = 2 * pr, hi = 2 * pr + 1;
+            const f32x4 y = mfma16(quad_of<E>(a_t(lo, hi)), quad_of<E>(D[lo]), z);
+            const f16x4 ny = quad_of<E>(-y);
+            x10t[pr] = mfma16(ny, quad_of<E>(Dt[hi]), z);
+            x10[pr] = mfma16(quad_of<E>(Dt[hi]), ny, z);
+            put(hi, lo, x10t[pr]);
+            st_quad(T + (16 * lo + n) * ts + 16 * hi + 4 * g, quad_of<E>(z));
+        }
+        if constexpr (NB == 4) {
+            // 32 -> 64: Y = A_hl X_ll (tiles Y_bj,bl for bj in {2, 3}, bl in {0, 1}), then
+            // X_hl = -X_hh Y, produced transposed
+            const f16x4 a02 = quad_of<E>(a_t(0, 2)), a12 = quad_of<E>(a_t(1, 2));
+            const f16x4 a03 = quad_of<E>(a_t(0, 3)), a13 = quad_of<E>(a_t(1, 3));
+            const f16x4 d0 = quad_of<E>(D[0]), d1 = quad_of<E>(D[1]), x10q = quad_of<E>(x10[0]);
+            const f16x4 ny20 = quad_of<E>(-mfma16(a12, x10q, mfma16(a02, d0, z)));   // -(A20 X00 + A21 X10)
+            const f16x4 ny21 = quad_of<E>(-mfma16(a12, d1, z));                      // -A21 X11
+            const f16x4 ny30 = quad_of<E>(-mfma16(a13, x10q, mfma16(a03, d0, z)));   // -(A30 X00 + A31 X10)
+            const f16x4 ny31 = quad_of<E>(-mfma16(a13, d1, z));                      // -A31 X11
+            const f16x4 dt2 = quad_of<E>(Dt[2]), dt3 = quad_of<E>(Dt[3]), x32t = quad_of<E>(x10t[1]);
+            put(2, 0, mfma16(ny20, dt2, z));                                 // (X22 Y20)^T, negated
+            put(2, 1, mfma16(ny21, dt2, z));
+            put(3, 0, mfma16(ny30, dt3, mfma16(ny20, x32t, z)));             // (X32 Y20 + X33 Y30)^T
+            put(3, 1, mfma16(ny31, dt3, mfma16(ny21, x32t, z)));
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = x10t[i] * br[0][i];
-        st_quad(T + (16 + n) * ts + 4 * g, quad_of<E>(v));
-        st_quad(T + n * ts + 16 + 4 * g, quad_of<E>(z));
+            for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+                for (int bj = 2; bj < 4; ++bj) st_quad(T + (16 * bi + n) * ts + 16 * bj + 4 * g, quad_of<E>(z));
+        }
     }
 }
 
