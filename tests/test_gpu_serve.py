@@ -110,3 +110,55 @@ def test_full_serving_workload():
     eo, es = rel_err(oc, ro), rel_err(dp, rpool)
     print(f"commit err o={eo:.3e} state={es:.3e}")
     assert eo <= TOL[w.dtype] and es <= TOL[w.dtype]
+
+
+@pytest.mark.parametrize("R,L,hqk,hv", [(3, 20, 1, 4), (2, 1, 2, 2), (1, 32, 1, 1), (5, 16, 2, 4)])
+def test_streaming_kernels_ragged_blocks(R, L, hqk, hv):
+    """The streaming denoise/commit kernels (bf16, d = 128) on blocks that pad to 16 or 32
+    positions, grouped value heads up to 4 per q/k head, and two commits in a row (the
+    second starting from the state the first wrote)."""
+    d = 128
+    pool = _realistic_pool(R, hv, d, seed=7 * R + L)
+    b1 = _block(R, L, hqk, hv, d, "bf16", seed=100 + L)
+    b2 = _block(R, L, hqk, hv, d, "bf16", seed=200 + L)
+    scale = 1.0 / math.sqrt(d)
+    dp = pool.cuda()
+    d1 = {k: v.cuda() for k, v in b1.items()}
+    d2 = {k: v.cuda() for k, v in b2.items()}
+    o = bd.bdgdn_denoise_step(dp, d1["q"], d1["k"], d1["v"], d1["g"], d1["beta"], scale=scale)
+    oc1 = bd.bdgdn_commit(dp, d1["q"], d1["k"], d1["v"], d1["g"], d1["beta"], scale=scale, want_o=True)
+    oc2 = bd.bdgdn_commit(dp, d2["q"], d2["k"], d2["v"], d2["g"], d2["beta"], scale=scale, want_o=True)
+    torch.cuda.synchronize()
+    ref = oracle.denoise(pool, b1["q"], b1["k"], b1["v"], b1["g"], b1["beta"], scale=scale)
+    p1, r1 = oracle.commit(pool, b1["q"], b1["k"], b1["v"], b1["g"], b1["beta"], scale=scale)
+    p2, r2 = oracle.commit(p1, b2["q"], b2["k"], b2["v"], b2["g"], b2["beta"], scale=scale)
+    errs = (rel_err(o, ref), rel_err(oc1, r1), rel_err(oc2, r2), rel_err(dp, p2))
+    print("denoise, commit 1, commit 2, state:", ["%.3e" % e for e in errs])
+    assert max(errs) <= TOL["bf16"]
+
+
+def test_streaming_kernels_bf16_outputs():
+    """bf16 outputs: the same arithmetic as the fp32-output kernels up to the final rounding,
+    and within the tolerance plus the output's own rounding of the oracle."""
+    R, L, h, d = 4, 32, 4, 128
+    pool = _realistic_pool(R, h, d, seed=11)
+    blk = _block(R, L, h, h, d, "bf16", seed=12)
+    db = {k: v.cuda() for k, v in blk.items()}
+    scale = 1.0 / math.sqrt(d)
+    o32 = bd.bdgdn_denoise_step(pool.cuda(), db["q"], db["k"], db["v"], db["g"], db["beta"], scale=scale)
+    o16 = bd.bdgdn_denoise_step(pool.cuda(), db["q"], db["k"], db["v"], db["g"], db["beta"], scale=scale,
+                                out_dtype=torch.bfloat16)
+    pa, pb = pool.cuda(), pool.cuda()
+    c32 = bd.bdgdn_commit(pa, db["q"], db["k"], db["v"], db["g"], db["beta"], scale=scale, want_o=True)
+    c16 = bd.bdgdn_commit(pb, db["q"], db["k"], db["v"], db["g"], db["beta"], scale=scale, want_o=True,
+                          out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert o16.dtype == torch.bfloat16 and c16.dtype == torch.bfloat16
+    assert torch.equal(o32.to(torch.bfloat16), o16) and torch.equal(c32.to(torch.bfloat16), c16)
+    assert torch.equal(pa, pb)
+    ref = oracle.denoise(pool, blk["q"], blk["k"], blk["v"], blk["g"], blk["beta"], scale=scale)
+    rnd = torch.from_numpy(ref.astype(np.float32)).to(torch.bfloat16).double().numpy()
+    budget = TOL["bf16"] + np.abs(rnd - ref).max() / np.sqrt((ref ** 2).mean())
+    e = rel_err(o16, ref)
+    print(f"bf16 denoise err {e:.3e} budget {budget:.3e}")
+    assert e <= budget
