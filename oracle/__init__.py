@@ -60,6 +60,10 @@ def _load():
         lib.oracle_denoise.restype = I
         lib.oracle_commit.argtypes = [I, I, I, I, I, I, D, P, P] + [P] * 6
         lib.oracle_commit.restype = I
+        lib.oracle_commit_record.argtypes = [I, I, I, I, I, I, I, D, P, P] + [P] * 7
+        lib.oracle_commit_record.restype = I
+        lib.oracle_accept_states.argtypes = [I, I, I, I, I, P, P, P, P]
+        lib.oracle_accept_states.restype = I
         lib.oracle_set_threads.argtypes = [I]
         lib.oracle_max_threads.restype = I
         _lib = lib
@@ -153,3 +157,36 @@ def commit(pool, q, k, v, g, beta, *, scale, slot=None, want_o=True):
     if rc != 0:
         raise RuntimeError(f"oracle_commit failed: {rc}")
     return pool, o
+
+
+def commit_record(pool, q, k, v, g, beta, *, scale, n_record, slot=None, want_o=True):
+    """The commit pass that also keeps the verify-position states: states[r, i] is the
+    state before block position L - n_record + i.  Returns (new_pool, o or None,
+    states [R, n_record, Hv, dk, dv]) in fp64; the input pool is copied."""
+    pool = _f64(pool).copy()
+    q, k, v, g, beta = map(_f64, (q, k, v, g, beta))
+    R, L, Hqk, dk = q.shape
+    Hv, dv = v.shape[2], v.shape[3]
+    sl = None if slot is None else np.ascontiguousarray(np.asarray(slot, dtype=np.int32))
+    o = np.zeros((R, L, Hv, dv)) if want_o else None
+    states = np.zeros((R, n_record, Hv, dk, dv))
+    rc = _load().oracle_commit_record(R, Hqk, Hv, dk, dv, L, int(n_record), float(scale), _ptr(pool),
+                                      _ptr(sl), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(o),
+                                      _ptr(states))
+    if rc != 0:
+        raise RuntimeError(f"oracle_commit_record failed: {rc}")
+    return pool, o, states
+
+
+def accept_states(pool, states, accept, *, slot=None):
+    """Pool after the verify decision: request r keeps states[r, accept[r]] (or the pool's
+    state when accept[r] == n_record).  Returns the new pool (fp64 copy)."""
+    pool = _f64(pool).copy()
+    states = _f64(states)
+    R, n_rec, Hv, dk, dv = states.shape
+    acc = np.ascontiguousarray(np.asarray(accept, dtype=np.int32))
+    sl = None if slot is None else np.ascontiguousarray(np.asarray(slot, dtype=np.int32))
+    rc = _load().oracle_accept_states(R, Hv, dk, dv, n_rec, _ptr(pool), _ptr(sl), _ptr(states), _ptr(acc))
+    if rc != 0:
+        raise RuntimeError(f"oracle_accept_states failed: {rc}")
+    return pool

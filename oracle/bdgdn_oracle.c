@@ -20,7 +20,10 @@
  *     each document start; the last block of a document may be partial.
  *   - serving passes (Appendix "Diffusion-Trust Sampling", "Differences between the
  *     denoise pass and the state-update pass"): denoise reads the cached state and
- *     never writes it; commit runs the token-causal pass and writes the state back.
+ *     never writes it; commit runs the token-causal pass and writes the state back;
+ *     the AR-Trust verify pass also keeps the states at the verify positions, and the
+ *     accept step writes the state at each request's accepted offset back to the pool
+ *     (Appendix "Serving-system machinery", cache-and-scatter).
  *
  * Layouts (row = token index in the flattened [B*T] or packed token axis):
  *   q,k  [row][h_qk][d_k]    v,o [row][h_v][d_v]    g,beta [row][h_v]
@@ -240,6 +243,75 @@ int oracle_commit(int R, int h_qk, int h_v, int dk, int dv, int L, double scale,
         free(u);
     }
     return err;
+}
+
+/*
+ * oracle_commit_record: the commit pass that also keeps the verify-position states
+ * (Appendix "Serving-system machinery for the hybrid backbone", cache-and-scatter, and
+ * Algorithm "AR-Trust serving round"): before the update of block position
+ * p = L - n_rec + i (i = 0 .. n_rec-1) the current state is copied to
+ * states[r][i][h] (layout [R][n_rec][h_v][dk][dv]); the pool then holds the state after
+ * all L positions, as after oracle_commit.
+ */
+int oracle_commit_record(int R, int h_qk, int h_v, int dk, int dv, int L, int n_rec, double scale,
+                         double *pool, const int32_t *slot,
+                         const double *q, const double *k, const double *v,
+                         const double *g, const double *beta, double *o, double *states)
+{
+    if (L < 1 || h_qk < 1 || h_v < 1 || h_v % h_qk || n_rec < 1 || n_rec > L) return -1;
+    dims_t d = {h_qk, h_v, dk, dv, scale};
+    const size_t ssz = (size_t)dk * dv;
+    const long nunits = (long)R * h_v;
+    int err = 0;
+#pragma omp parallel
+    {
+        double *u = malloc((size_t)dv * sizeof(double));
+        const int ok = u != NULL;
+        if (!ok) {
+#pragma omp atomic write
+            err = -2;
+        }
+#pragma omp for schedule(dynamic, 1)
+        for (long unit = 0; unit < nunits; ++unit) {
+            if (!ok) continue;
+            int r = (int)(unit / h_v), h = (int)(unit % h_v);
+            int s = slot ? slot[r] : r;
+            double *S = pool + ((size_t)s * h_v + h) * ssz;
+            for (int p = 0; p < L; ++p) {
+                const long t = (long)r * L + p;
+                const int i = p - (L - n_rec);
+                if (i >= 0)   /* the state before position p */
+                    memcpy(states + (((size_t)r * n_rec + i) * h_v + h) * ssz, S, ssz * sizeof(double));
+                gdr_step(S, dk, dv, row_qk(k, &d, t, h), row_v(v, &d, t, h),
+                         gate_at(g, &d, t, h), gate_at(beta, &d, t, h), u);
+                if (o) readout(S, dk, dv, row_qk(q, &d, t, h), scale, row_o(o, &d, t, h));
+            }
+        }
+        free(u);
+    }
+    return err;
+}
+
+/*
+ * oracle_accept_states: the gather-scatter after a verify decision.  Request r keeps
+ * the state at its accepted offset: pool[slot[r]][h] = states[r][accept[r]][h] for
+ * accept[r] < n_rec; accept[r] == n_rec keeps the state already in the pool.
+ */
+int oracle_accept_states(int R, int h_v, int dk, int dv, int n_rec, double *pool, const int32_t *slot,
+                         const double *states, const int32_t *accept)
+{
+    if (h_v < 1 || n_rec < 1) return -1;
+    for (int r = 0; r < R; ++r)
+        if (accept[r] < 0 || accept[r] > n_rec) return -1;
+    const size_t ssz = (size_t)dk * dv;
+    for (int r = 0; r < R; ++r) {
+        if (accept[r] == n_rec) continue;
+        const int s = slot ? slot[r] : r;
+        for (int h = 0; h < h_v; ++h)
+            memcpy(pool + ((size_t)s * h_v + h) * ssz,
+                   states + (((size_t)r * n_rec + accept[r]) * h_v + h) * ssz, ssz * sizeof(double));
+    }
+    return 0;
 }
 
 void oracle_set_threads(int n)

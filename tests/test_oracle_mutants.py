@@ -57,6 +57,17 @@ MUTANTS = {
         "                readout(Sn, dk, dv, row_qk(q, &d, l, h), scale, row_o(o, &d, l, h));",
         "                readout(Sn, dk, dv, row_qk(q, &d, l, h), scale, row_o(o, &d, l, h));\n"
         "            memcpy((double *)pool + ((size_t)s * h_v + h) * ssz, Sn, ssz * sizeof(double));"),
+    "record_after_update": (
+        "                if (i >= 0)   /* the state before position p */\n"
+        "                    memcpy(states + (((size_t)r * n_rec + i) * h_v + h) * ssz, S, ssz * sizeof(double));\n"
+        "                gdr_step(S, dk, dv, row_qk(k, &d, t, h), row_v(v, &d, t, h),\n"
+        "                         gate_at(g, &d, t, h), gate_at(beta, &d, t, h), u);\n",
+        "                gdr_step(S, dk, dv, row_qk(k, &d, t, h), row_v(v, &d, t, h),\n"
+        "                         gate_at(g, &d, t, h), gate_at(beta, &d, t, h), u);\n"
+        "                if (i >= 0)\n"
+        "                    memcpy(states + (((size_t)r * n_rec + i) * h_v + h) * ssz, S, ssz * sizeof(double));\n"),
+    "accept_offset_shift": ("states + (((size_t)r * n_rec + accept[r]) * h_v + h) * ssz",
+                            "states + (((size_t)r * n_rec + (accept[r] + 1) % n_rec) * h_v + h) * ssz"),
     "commit_skips_last_token": ("for (long t = (long)r * L; t < (long)r * L + L; ++t) {",
                                 "for (long t = (long)r * L; t < (long)r * L + L - 1; ++t) {"),
 }

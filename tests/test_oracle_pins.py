@@ -400,3 +400,49 @@ def test_pin_denoise_after_commit_equals_training_schedule():
     n = {key: cat(junk, b2, i) for i, key in enumerate(keys)}
     _, on, _ = _run(c, n, L, scale=1.0, h0=S)
     np.testing.assert_array_equal(on[:, L:], o2)
+
+
+# ------------------- AR-Trust verify-position states (cache-and-scatter) -------------------
+def test_pin_commit_record_keeps_prefix_states():
+    """The verify pass keeps, for the last n_record positions p of the block, the state
+    before position p: the brute-force unrolled state after the first p tokens (the
+    cached state itself for p = 0).  Its pool and outputs are those of the commit pass."""
+    rng = np.random.default_rng(15)
+    R, L, hv, dk, dv = 2, 5, 2, 4, 3
+    pool = rng.standard_normal((R + 1, hv, dk, dv))
+    slot = np.array([1, 2], np.int32)
+    q, k, v, g, b = _serve_block(rng, R, L, 1, hv, dk, dv)
+    for n_rec in (1, 3, L):
+        newpool, o, states = oracle.commit_record(pool, q, k, v, g, b, scale=0.7, n_record=n_rec, slot=slot)
+        cpool, co = oracle.commit(pool, q, k, v, g, b, scale=0.7, slot=slot)
+        np.testing.assert_array_equal(newpool, cpool)
+        np.testing.assert_array_equal(o, co)
+        assert states.shape == (R, n_rec, hv, dk, dv)
+        for r, s in enumerate(slot):
+            for h in range(hv):
+                st = _unrolled_states(k[r, :, 0], v[r, :, h], np.exp(g[r, :, h]), b[r, :, h], pool[s, h])
+                for i in range(n_rec):
+                    p = L - n_rec + i
+                    want = pool[s, h] if p == 0 else st[p - 1]
+                    np.testing.assert_allclose(states[r, i, h], want, rtol=1e-12, atol=1e-13)
+
+
+def test_pin_accept_states_rewinds_to_accepted_offset():
+    """After a verify pass over [anchor, d_0 .. d_(K-1)] (L = K + 1 positions, K recorded),
+    accepting a drafts leaves the state after the anchor and a drafts: the commit pass over
+    the first 1 + a tokens; accepting all K keeps the verify pass's final state."""
+    rng = np.random.default_rng(16)
+    R, K, hv, dk, dv = 4, 3, 2, 4, 4
+    L = K + 1
+    pool = rng.standard_normal((R, hv, dk, dv))
+    q, k, v, g, b = _serve_block(rng, R, L, 1, hv, dk, dv)
+    vpool, _, states = oracle.commit_record(pool, q, k, v, g, b, scale=1.0, n_record=K)
+    accept = np.array([0, 1, K - 1, K], np.int32)
+    out = oracle.accept_states(vpool, states, accept)
+    for r in range(R):
+        a = int(accept[r])
+        blk = [x[r:r + 1, :1 + a] for x in (q, k, v, g, b)]
+        want, _ = oracle.commit(pool[r:r + 1], *blk, scale=1.0)
+        np.testing.assert_array_equal(out[r], want[0])
+    with pytest.raises(RuntimeError):
+        oracle.accept_states(vpool, states, np.array([0, 1, K + 1, 0], np.int32))
