@@ -193,6 +193,41 @@ int bdgdn_commit(const bdgdn_serve_desc_t *desc, float *state_pool, const int32_
                  const void *q, const void *k, const void *v,
                  const float *g, const float *beta, void *o_causal, void *stream);
 
+/*
+ * The AR-Trust verify pass with its state cache (Appendix "Serving-system machinery for
+ * the hybrid backbone", cache-and-scatter; Algorithm "AR-Trust serving round"): the
+ * commit pass of bdgdn_commit over each request's block of L = desc->block positions
+ * (e.g. the anchor and K draft tokens, L = K + 1), which also writes, for the block's
+ * last n_record positions p = L - n_record + i (i = 0 .. n_record-1), the state before
+ * position p:
+ *
+ *   states      [R][n_record][h_v][d_k][d_v] fp32 (device, 16-byte aligned), written
+ *               whole; states[r][i] is the state after the first L - n_record + i
+ *               positions of request r (the cached state itself when that is 0).
+ *
+ * The pool then holds the state after all L positions, exactly as after bdgdn_commit
+ * (o_causal as there).  1 <= n_record <= block.  Available for bf16 inputs with
+ * d_k = d_v = 128 and blocks of at most 32 positions (else BDGDN_ERR_UNSUPPORTED).
+ */
+int bdgdn_commit_record(const bdgdn_serve_desc_t *desc, float *state_pool, const int32_t *slot,
+                        const void *q, const void *k, const void *v,
+                        const float *g, const float *beta, void *o_causal,
+                        int32_t n_record, float *states, void *stream);
+
+/*
+ * The accept step after a verify decision: request r keeps the state at its accepted
+ * offset, state_pool[slot[r]][h] = states[r][accept[r]][h] for every v-head h, in one
+ * launch (one workgroup per (request, v-head)).
+ *
+ *   accept      [R] int32 device array; accept[r] == n_record keeps the state already in
+ *               the pool (the verify pass's final state); values outside [0, n_record]
+ *               also leave the slot untouched (they are not checked on the host).
+ *   states      as written by bdgdn_commit_record with the same n_record and desc.
+ * state_pool and states must be 16-byte aligned.  Any supported (d_k, d_v).
+ */
+int bdgdn_accept_states(const bdgdn_serve_desc_t *desc, float *state_pool, const int32_t *slot,
+                        const float *states, int32_t n_record, const int32_t *accept, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

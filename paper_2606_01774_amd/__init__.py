@@ -22,6 +22,7 @@ __all__ = [
     "BdgdnError", "BDGDN_BF16", "BDGDN_F32", "BDGDN_ROUTE_FUSED", "BDGDN_ROUTE_SPLIT",
     "BDGDN_ROUTE_ONEPASS", "BDGDN_ROUTE_RECORDS",
     "bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace", "bdgdn_fwd_train",
+    "bdgdn_commit_record", "bdgdn_accept_states",
     "bdgdn_denoise_step", "bdgdn_commit", "library_path", "load_library", "EXPORTED_SYMBOLS",
 ]
 
@@ -42,7 +43,8 @@ BDGDN_ROUTE_ONEPASS = 2
 BDGDN_ROUTE_RECORDS = 3
 
 EXPORTED_SYMBOLS = ("bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace",
-                    "bdgdn_fwd_train", "bdgdn_denoise_step", "bdgdn_commit")
+                    "bdgdn_fwd_train", "bdgdn_denoise_step", "bdgdn_commit", "bdgdn_commit_record",
+                    "bdgdn_accept_states")
 
 
 class FwdDesc(ctypes.Structure):
@@ -94,6 +96,10 @@ def load_library():
     lib.bdgdn_denoise_step.restype = ctypes.c_int
     lib.bdgdn_commit.argtypes = [ctypes.POINTER(ServeDesc)] + [P] * 9
     lib.bdgdn_commit.restype = ctypes.c_int
+    lib.bdgdn_commit_record.argtypes = [ctypes.POINTER(ServeDesc)] + [P] * 8 + [ctypes.c_int32, P, P]
+    lib.bdgdn_commit_record.restype = ctypes.c_int
+    lib.bdgdn_accept_states.argtypes = [ctypes.POINTER(ServeDesc), P, P, P, ctypes.c_int32, P, P]
+    lib.bdgdn_accept_states.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -264,3 +270,50 @@ def bdgdn_commit(state_pool, q, k, v, g, beta, *, scale=None, slot=None, o_causa
                           _ptr(v), _ptr(g), _ptr(beta), _ptr(o_causal), _stream(stream))
     _check(st, "bdgdn_commit")
     return o_causal
+
+
+def bdgdn_commit_record(state_pool, q, k, v, g, beta, *, n_record, scale=None, slot=None, states=None,
+                        o_causal=None, want_o=False, out_dtype=torch.float32, stream=None):
+    """The AR-Trust verify pass: bdgdn_commit over R blocks of L positions that also writes
+    states[r, i] = the state before block position L - n_record + i.
+    Returns (states [R, n_record, Hv, dk, dv] fp32, o_causal or None)."""
+    lib = load_library()
+    dt = q.dtype
+    _dev(state_pool, "state_pool", torch.float32)
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _dev(t, name, dt)
+    _dev(g, "g", torch.float32)
+    _dev(beta, "beta", torch.float32)
+    _dev(slot, "slot", torch.int32)
+    R, L, _, dk = q.shape
+    Hv, dv = v.shape[2], v.shape[3]
+    if states is None:
+        states = torch.empty(R, int(n_record), Hv, dk, dv, dtype=torch.float32, device=q.device)
+    _dev(states, "states", torch.float32)
+    if o_causal is not None:
+        out_dtype = o_causal.dtype
+    if o_causal is None and want_o:
+        o_causal = torch.empty(v.shape, dtype=out_dtype, device=v.device)
+    _dev(o_causal, "o_causal", out_dtype)
+    desc = _serve_desc(q, v, scale, out_dtype)
+    st = lib.bdgdn_commit_record(ctypes.byref(desc), _ptr(state_pool), _ptr(slot), _ptr(q), _ptr(k),
+                                 _ptr(v), _ptr(g), _ptr(beta), _ptr(o_causal), int(n_record), _ptr(states),
+                                 _stream(stream))
+    _check(st, "bdgdn_commit_record")
+    return states, o_causal
+
+
+def bdgdn_accept_states(state_pool, states, accept, *, block, h_qk=None, slot=None, stream=None):
+    """The accept step: state_pool[slot[r]] <- states[r, accept[r]] where accept[r] <
+    n_record (states [R, n_record, Hv, dk, dv] from bdgdn_commit_record; block = its L)."""
+    lib = load_library()
+    _dev(state_pool, "state_pool", torch.float32)
+    _dev(states, "states", torch.float32)
+    _dev(accept, "accept", torch.int32)
+    _dev(slot, "slot", torch.int32)
+    R, n_record, Hv, dk, dv = states.shape
+    desc = ServeDesc(R, Hv if h_qk is None else int(h_qk), Hv, dk, dv, int(block), 1.0, BDGDN_BF16,
+                     _DT[torch.float32])
+    st = lib.bdgdn_accept_states(ctypes.byref(desc), _ptr(state_pool), _ptr(slot), _ptr(states),
+                                 int(n_record), _ptr(accept), _stream(stream))
+    _check(st, "bdgdn_accept_states")

@@ -240,6 +240,9 @@ static ServeArgs serve_args(const bdgdn_serve_desc_t *d, const float *pool, cons
     a.R = d->num_req; a.h_qk = d->h_qk; a.h_v = d->h_v; a.dv = d->d_v; a.L = d->block;
     a.n_vt = d->d_v / serve_tile_v();
     a.scale = d->scale;
+    a.states = nullptr;
+    a.n_rec = 0;
+    a.accept = nullptr;
     return a;
 }
 
@@ -273,6 +276,46 @@ int bdgdn_commit(const bdgdn_serve_desc_t *desc, float *state_pool, const int32_
     types_of(desc->dtype, desc->out_dtype, ty);
     hipError_t e = launch_commit(ty, desc->d_k, lp_of(desc->block), o_causal != nullptr, a,
                                  static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+}
+
+int bdgdn_commit_record(const bdgdn_serve_desc_t *desc, float *state_pool, const int32_t *slot,
+                        const void *q, const void *k, const void *v, const float *g,
+                        const float *beta, void *o_causal, int32_t n_record, float *states,
+                        void *stream)
+{
+    int st = check_serve(desc);
+    if (st != BDGDN_OK) return st;
+    if (!state_pool || !q || !k || !v || !g || !beta || !states) return BDGDN_ERR_INVALID_ARG;
+    if (n_record < 1 || n_record > desc->block) return BDGDN_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o_causal) || !aligned16(states))
+        return BDGDN_ERR_INVALID_ARG;
+    Types ty;
+    types_of(desc->dtype, desc->out_dtype, ty);
+    if (!record_supported(ty, desc->d_k, desc->d_v, lp_of(desc->block))) return BDGDN_ERR_UNSUPPORTED;
+    if (desc->num_req == 0) return BDGDN_OK;
+    ServeArgs a = serve_args(desc, state_pool, slot, q, k, v, g, beta, o_causal);
+    a.states = states;
+    a.n_rec = n_record;
+    hipError_t e = launch_commit_record(ty, lp_of(desc->block), o_causal != nullptr, a,
+                                        static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+}
+
+int bdgdn_accept_states(const bdgdn_serve_desc_t *desc, float *state_pool, const int32_t *slot,
+                        const float *states, int32_t n_record, const int32_t *accept, void *stream)
+{
+    int st = check_serve(desc);
+    if (st != BDGDN_OK) return st;
+    if (!state_pool || !states || !accept) return BDGDN_ERR_INVALID_ARG;
+    if (n_record < 1 || n_record > desc->block) return BDGDN_ERR_INVALID_ARG;
+    if (!aligned16(state_pool) || !aligned16(states)) return BDGDN_ERR_INVALID_ARG;
+    if (desc->num_req == 0) return BDGDN_OK;
+    ServeArgs a = serve_args(desc, state_pool, slot, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+    a.states = const_cast<float *>(states);
+    a.n_rec = n_record;
+    a.accept = accept;
+    hipError_t e = launch_accept_states(a, desc->d_k, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
 }
 

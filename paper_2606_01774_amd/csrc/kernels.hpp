@@ -71,6 +71,9 @@ struct ServeArgs {
     int R, h_qk, h_v, dv, L;
     int n_vt;
     float scale;
+    float *states;       // recorded states [R][n_rec][h_v][d_k][d_v] (commit_record, accept), or NULL
+    int n_rec;           // recorded positions: the block's last n_rec
+    const int32_t *accept;   // accepted offsets [R] (accept)
 };
 
 // Element types of one call: inputs / MFMA operands / outputs.
@@ -84,6 +87,12 @@ enum class Types {
 hipError_t launch_fwd_fused(Types ty, int dk, int lp, const FwdArgs &a, hipStream_t s);
 hipError_t launch_denoise(Types ty, int dk, int lp, const ServeArgs &a, hipStream_t s);
 hipError_t launch_commit(Types ty, int dk, int lp, bool with_o, const ServeArgs &a, hipStream_t s);
+// The commit pass that also writes the states before the block's last n_rec positions
+// (streaming kernels: bf16 inputs, d_k = d_v = 128, blocks of at most 32 positions).
+bool record_supported(Types ty, int dk, int dv, int lp);
+hipError_t launch_commit_record(Types ty, int lp, bool with_o, const ServeArgs &a, hipStream_t s);
+// pool[slot[r]] <- states[r][accept[r]] for every head where accept[r] < n_rec.
+hipError_t launch_accept_states(const ServeArgs &a, int dk, hipStream_t s);
 // Two-kernel training forward (UT transform records, then the scan).
 hipError_t launch_fwd_scan(Types ty, int dk, int lp, const IntraArgs &ia, const ScanArgs &sa, hipStream_t s);
 // The one-kernel pipelined schedule (UT transform inside the scan workgroups): bf16

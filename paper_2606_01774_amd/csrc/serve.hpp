@@ -13,6 +13,10 @@
 //   commit (token-causal; the state is advanced and written back in place):
 //     O  = s [ diag(gamma) Q S0 + P Delta ],       P_ri = (gamma_r / gamma_i) (q_r . k_i), i <= r
 //     S0 <- gamma_n S0 + K^T diag(gamma_n / gamma) Delta
+//   commit with recorded states (the AR-Trust verify pass, Appendix "Serving-system
+//   machinery", cache-and-scatter): before that, the state before each recorded position p,
+//     S^(p) = gamma_(p-1) S0 + K^T diag(m_p) Delta,  m_p,j = gamma_(p-1) / gamma_j (j < p), 0 else
+//   (S^(0) = S0), is written to the states buffer.
 //
 // Workgroup of four waves.  Each wave owns 32 columns of the state, as two 16-column
 // MFMA strips interleaved by column parity: lane (g, n) holds rows 16 kb + 4g + i of
@@ -27,8 +31,9 @@
 
 namespace bdgdn {
 
-template <typename Out, int DK, int LP, bool COMMIT, bool CO>
+template <typename Out, int DK, int LP, bool COMMIT, bool CO, bool REC = false>
 struct Serve {
+    static_assert(!REC || COMMIT, "states are recorded by the commit pass");
     typedef __bf16 In;
     typedef _Float16 E;
     typedef f16x4 QE;
@@ -96,7 +101,68 @@ struct Serve {
         int qks, vst, gst;         // row strides (elements); the state rows are BV apart
         int nvalid;                // positions of the block (<= LP)
         float scale;
+        float *states;             // REC: state before position nvalid - n_rec (column v0)
+        int n_rec;                 // REC: recorded positions (the block's last n_rec)
+        long rec_step;             // REC: elements between consecutive recorded states
     };
+
+    // A-operand quads of K^T rows 16 kb .. 16 kb + 15 by transpose reads: lane (g, r)
+    // receives K[16 rb + 4g + i][16 kb + r], i = 0..3 (the transposed-read offsets are those
+    // of rofs for row 4g + (lane >> 2 & 3), columns 16 kb + 4 (lane & 3))
+    __device__ __forceinline__ void kt_quads(QE (&a)[NB], int kb) const
+    {
+        const int g = lane >> 4;
+        const int off = rofs(4 * g + ((lane >> 2) & 3), 16 * kb + 4 * (lane & 3));
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb)
+            a[rb] = __builtin_bit_cast(QE, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                               (__attribute__((address_space(3))) s16x4 *)(rows(0) + 16 * rb * DK + off)));
+    }
+
+    // The states before the block's last n_rec positions (see the header), from the rows'
+    // Delta (dl) and the cached state S of this wave's two strips; written with the same
+    // 8-byte column-pair accesses as the state itself.
+    __device__ void record_states(const Unit &u, const f32x4 (&S)[2][DKB], const f32x4 (&dl)[2][NB]) const
+    {
+        const int g = lane >> 4, n = lane & 15;
+        const int c0 = 32 * wave + 2 * n;
+        const float *Gs = us(0);   // cumulative log2-gates of the block (wave 0's scratch)
+        QE kt[DKB][NB];
+#pragma unroll
+        for (int kb = 0; kb < DKB; ++kb) kt_quads(kt[kb], kb);
+        f32x4 xj[NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) xj[rb] = ut::ld4f(Gs + 16 * rb + 4 * g);
+        const int soff = (4 * g * BV + c0) * 4;
+        for (int i = 0; i < u.n_rec; ++i) {
+            const int p = u.nvalid - u.n_rec + i;
+            const __amdgpu_buffer_rsrc_t rs = rsrc(u.states + (long)i * u.rec_step, (unsigned)(DK * BV * 4));
+            const float xp = p > 0 ? Gs[p - 1] : 0.f;
+            const float gp = p > 0 ? fexp2(xp) : 1.f;
+            QE uq[2][NB];
+#pragma unroll
+            for (int rb = 0; rb < NB; ++rb) {
+                f32x4 m;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int j = 16 * rb + 4 * g + e;
+                    m[e] = j < p ? fexp2(-fabsf(xp - xj[rb][e])) : 0.f;
+                }
+                uq[0][rb] = quad_of<E>(dl[0][rb] * m);
+                uq[1][rb] = quad_of<E>(dl[1][rb] * m);
+            }
+#pragma unroll
+            for (int kb = 0; kb < DKB; ++kb) {
+                const f32x4 a = mma_q<E, NB>(S[0][kb] * gp, kt[kb], uq[0]);
+                const f32x4 b = mma_q<E, NB>(S[1][kb] * gp, kt[kb], uq[1]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const u32x2 w = {u_of(a[e]), u_of(b[e])};
+                    __builtin_amdgcn_raw_buffer_store_b64(w, rs, soff, (16 * kb + e) * BV * 4, 0);
+                }
+            }
+        }
+    }
 
     __device__ void run(const Unit &u) const
     {
@@ -151,16 +217,10 @@ struct Serve {
         }
         lds_barrier();
 
-        // per-lane quad offsets (row lane & 15; transposes: see kt below)
-        int qo[DKB], to[DKB];
-        {
-            const int tr = 4 * g + ((lane >> 2) & 3), tq = lane & 3;
+        // per-lane quad offsets (row lane & 15)
+        int qo[DKB];
 #pragma unroll
-            for (int kb = 0; kb < DKB; ++kb) {
-                qo[kb] = rofs(n, 16 * kb + 4 * g);
-                to[kb] = rofs(tr, 16 * kb + 4 * tq);
-            }
-        }
+        for (int kb = 0; kb < DKB; ++kb) qo[kb] = rofs(n, 16 * kb + 4 * g);
         auto ld_rows = [&](QE (&q)[DKB], const E *M) {
 #pragma unroll
             for (int kb = 0; kb < DKB; ++kb) q[kb] = *(LQ)(M + qo[kb]);
@@ -318,6 +378,7 @@ struct Serve {
         // ---- commit: S0 <- gamma_n S0 + K^T diag(gamma_n / gamma) Delta, written in place
         if constexpr (COMMIT) {
             const float gn = fac(0)[LP - 1];
+            if constexpr (REC) record_states(u, S, dl);
             QE uq[2][NB];
 #pragma unroll
             for (int rb = 0; rb < NB; ++rb) {
@@ -327,13 +388,8 @@ struct Serve {
             }
 #pragma unroll
             for (int kb = 0; kb < DKB; ++kb) {
-                // A-operand quads of K^T rows 16 kb .. 16 kb + 15 by transpose reads: lane
-                // (g, r) receives K[16 rb + 4g + i][16 kb + r], i = 0..3
                 QE a[NB];
-#pragma unroll
-                for (int rb = 0; rb < NB; ++rb)
-                    a[rb] = __builtin_bit_cast(QE, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                                                       (__attribute__((address_space(3))) s16x4 *)(rows(0) + 16 * rb * DK + to[kb])));
+                kt_quads(a, kb);
                 S[0][kb] = mma_q<E, NB>(S[0][kb] * gn, a, uq[0]);
                 S[1][kb] = mma_q<E, NB>(S[1][kb] * gn, a, uq[1]);
             }

@@ -77,11 +77,11 @@ __global__ void __launch_bounds__(kServeThreads) bdgdn_commit_kernel(ServeArgs a
 }
 
 // ---- streaming kernels (serve.hpp)
-template <typename Out, int LP, bool COMMIT, bool CO>
+template <typename Out, int LP, bool COMMIT, bool CO, bool REC = false>
 __device__ __forceinline__ void stream_body(const ServeArgs &a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    typedef Serve<Out, 128, LP, COMMIT, CO> K;
+    typedef Serve<Out, 128, LP, COMMIT, CO, REC> K;
     typedef typename K::In In;
     const int unit = blockIdx.x;
     const int r = unit / a.h_v, h = unit % a.h_v;
@@ -103,6 +103,9 @@ __device__ __forceinline__ void stream_body(const ServeArgs &a)
     u.gst = a.h_v;
     u.nvalid = a.L;
     u.scale = a.scale;
+    u.states = REC ? a.states + ((long)r * a.n_rec * a.h_v + h) * 128 * 128 : nullptr;
+    u.n_rec = REC ? a.n_rec : 0;
+    u.rec_step = (long)a.h_v * 128 * 128;
     K k(smem);
     k.run(u);
 }
@@ -117,6 +120,27 @@ template <typename Out, int LP, bool CO>
 __global__ void __launch_bounds__(256) bdgdn_k4_commit_kernel(ServeArgs a)
 {
     stream_body<Out, LP, true, CO>(a);
+}
+
+template <typename Out, int LP, bool CO>
+__global__ void __launch_bounds__(256) bdgdn_k4_commit_record_kernel(ServeArgs a)
+{
+    stream_body<Out, LP, true, CO, true>(a);
+}
+
+// The accept step of the verify-state cache: one workgroup per (request, v-head) copies
+// the recorded state at the request's accepted offset into its pool slot (16-byte
+// accesses, each thread strided by the workgroup); offsets at or past n_rec (the pool
+// already holds the pass's final state) and negative ones leave the slot untouched.
+__global__ void __launch_bounds__(256) bdgdn_accept_states_kernel(ServeArgs a, int ssz4)
+{
+    const int r = blockIdx.x / a.h_v, h = blockIdx.x % a.h_v;
+    const int acc = a.accept[r];
+    if (acc < 0 || acc >= a.n_rec) return;
+    const int sl = a.slot ? a.slot[r] : r;
+    const f32x4 *src = reinterpret_cast<const f32x4 *>(a.states) + (((long)r * a.n_rec + acc) * a.h_v + h) * ssz4;
+    f32x4 *dst = reinterpret_cast<f32x4 *>(a.pool) + ((long)sl * a.h_v + h) * ssz4;
+    for (int i = threadIdx.x; i < ssz4; i += 256) dst[i] = src[i];
 }
 
 template <typename K>
@@ -195,6 +219,40 @@ static hipError_t launch_stream(const ServeArgs &a, hipStream_t s)
     else
         kern = bdgdn_k4_denoise_kernel<Out, LP>;
     hipLaunchKernelGGL(kern, dim3(a.R * a.h_v), dim3(K::kThreads), K::BYTES, s, a);
+    return hipGetLastError();
+}
+
+template <typename Out, int LP, bool CO>
+static hipError_t launch_record(const ServeArgs &a, hipStream_t s)
+{
+    typedef Serve<Out, 128, LP, true, CO, true> K;
+    hipLaunchKernelGGL((bdgdn_k4_commit_record_kernel<Out, LP, CO>), dim3(a.R * a.h_v), dim3(K::kThreads), K::BYTES,
+                       s, a);
+    return hipGetLastError();
+}
+
+bool record_supported(Types ty, int dk, int dv, int lp)
+{
+    return ty != Types::F32 && dk == 128 && dv == 128 && (lp == 16 || lp == 32);
+}
+
+hipError_t launch_commit_record(Types ty, int lp, bool with_o, const ServeArgs &a, hipStream_t s)
+{
+    if (!record_supported(ty, 128, a.dv, lp) || !a.states || a.n_rec < 1 || a.n_rec > a.L) return hipErrorInvalidValue;
+#define BDGDN_REC(OUT) \
+    return with_o ? (lp == 16 ? launch_record<OUT, 16, true>(a, s) : launch_record<OUT, 32, true>(a, s)) \
+                  : (lp == 16 ? launch_record<OUT, 16, false>(a, s) : launch_record<OUT, 32, false>(a, s));
+    if (ty == Types::BF16_IN_F32_OUT) {
+        BDGDN_REC(float)
+    }
+    BDGDN_REC(__bf16)
+#undef BDGDN_REC
+}
+
+hipError_t launch_accept_states(const ServeArgs &a, int dk, hipStream_t s)
+{
+    if (!a.states || !a.accept || a.n_rec < 1 || (dk * a.dv) % 4) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(bdgdn_accept_states_kernel, dim3(a.R * a.h_v), dim3(256), 0, s, a, dk * a.dv / 4);
     return hipGetLastError();
 }
 

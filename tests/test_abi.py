@@ -153,3 +153,39 @@ def test_binding_refuses_host_tensors():
     g = torch.zeros(1, 32, 1)
     with pytest.raises(ValueError):
         bd.bdgdn_fwd_train(x, x, x, g, g, x, x, x, g, g, block=32)
+
+
+def _record(**kw):
+    n_record = kw.pop("n_record", 4)
+    states = kw.pop("states", FAKE)
+    d = dict(num_req=4, h_qk=2, h_v=4, d_k=128, d_v=128, block=8, scale=0.1, dtype=bd.BDGDN_BF16,
+             out_dtype=bd.BDGDN_F32)
+    d.update(kw)
+    P = FAKE
+    return bd.load_library().bdgdn_commit_record(ctypes.byref(bd.ServeDesc(**d)), P, None, P, P, P, P, P, None,
+                                                 n_record, states, None)
+
+
+def _accept(**kw):
+    n_record = kw.pop("n_record", 4)
+    accept = kw.pop("accept", FAKE)
+    d = dict(num_req=4, h_qk=2, h_v=4, d_k=128, d_v=128, block=8, scale=0.1, dtype=bd.BDGDN_BF16,
+             out_dtype=bd.BDGDN_F32)
+    d.update(kw)
+    P = FAKE
+    return bd.load_library().bdgdn_accept_states(ctypes.byref(bd.ServeDesc(**d)), P, None, P, n_record, accept,
+                                                 None)
+
+
+def test_verify_state_cache_validation():
+    assert _record(n_record=0) == bd.BDGDN_ERR_INVALID_ARG
+    assert _record(n_record=9) == bd.BDGDN_ERR_INVALID_ARG            # more than the block
+    assert _record(states=None) == bd.BDGDN_ERR_INVALID_ARG
+    assert _record(d_k=64, d_v=64) == bd.BDGDN_ERR_UNSUPPORTED
+    assert _record(block=48, n_record=4) == bd.BDGDN_ERR_UNSUPPORTED  # blocks of up to 32 only
+    assert _record(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32) == bd.BDGDN_ERR_UNSUPPORTED
+    assert _record(num_req=0) == bd.BDGDN_OK
+    assert _accept(n_record=0) == bd.BDGDN_ERR_INVALID_ARG
+    assert _accept(accept=None) == bd.BDGDN_ERR_INVALID_ARG
+    assert _accept(h_v=5) == bd.BDGDN_ERR_INVALID_ARG
+    assert _accept(num_req=0) == bd.BDGDN_OK

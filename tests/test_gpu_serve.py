@@ -162,3 +162,49 @@ def test_streaming_kernels_bf16_outputs():
     e = rel_err(o16, ref)
     print(f"bf16 denoise err {e:.3e} budget {budget:.3e}")
     assert e <= budget
+
+
+@pytest.mark.parametrize("R,K,hqk,hv,dtype_out", [(3, 4, 1, 2, torch.float32), (2, 15, 2, 2, torch.float32),
+                                                   (4, 31, 1, 1, torch.bfloat16), (2, 1, 1, 1, torch.float32)])
+def test_verify_state_cache(R, K, hqk, hv, dtype_out):
+    """The AR-Trust verify pass over [anchor, d_0 .. d_(K-1)] (L = K + 1 positions) keeps
+    the states before the K draft positions; the accept step rewinds each request to its
+    accepted offset (all offsets 0 .. K exercised), against the oracle."""
+    d, L = 128, K + 1
+    pool = _realistic_pool(R + 1, hv, d, seed=K + 31)
+    slot = torch.tensor(list(range(R, 0, -1)), dtype=torch.int32)
+    blk = _block(R, L, hqk, hv, d, "bf16", seed=K + 7)
+    scale = 1.0 / math.sqrt(d)
+    db = {k: v.cuda() for k, v in blk.items()}
+    dp = pool.cuda()
+    states, o = bd.bdgdn_commit_record(dp, db["q"], db["k"], db["v"], db["g"], db["beta"], n_record=K,
+                                       scale=scale, slot=slot.cuda(), want_o=True, out_dtype=dtype_out)
+    torch.cuda.synchronize()
+    rpool, ro, rstates = oracle.commit_record(pool, blk["q"], blk["k"], blk["v"], blk["g"], blk["beta"],
+                                              scale=scale, n_record=K, slot=slot.numpy())
+    tol = TOL["bf16"]
+    if dtype_out == torch.bfloat16:
+        rnd = torch.from_numpy(ro.astype(np.float32)).to(torch.bfloat16).double().numpy()
+        tol += np.abs(rnd - ro).max() / np.sqrt((ro ** 2).mean())
+    es, eo, ep = rel_err(states, rstates), rel_err(o, ro), rel_err(dp[1:], rpool[1:])
+    print(f"states err={es:.3e} o err={eo:.3e} pool err={ep:.3e}")
+    assert es <= TOL["bf16"] and eo <= tol and ep <= TOL["bf16"]
+    # the same pool as the plain commit pass, bit for bit
+    dp2 = pool.cuda()
+    bd.bdgdn_commit(dp2, db["q"], db["k"], db["v"], db["g"], db["beta"], scale=scale, slot=slot.cuda())
+    torch.cuda.synchronize()
+    assert torch.equal(dp2, dp)
+    # accept: every offset 0 .. K once across the requests (cycled)
+    accept = torch.tensor([(r * 7) % (K + 1) for r in range(R)], dtype=torch.int32)
+    before = dp.clone()
+    bd.bdgdn_accept_states(dp, states, accept.cuda(), block=L, slot=slot.cuda())
+    torch.cuda.synchronize()
+    want = oracle.accept_states(rpool, rstates, accept.numpy(), slot=slot.numpy())
+    assert rel_err(dp[1:], want[1:]) <= TOL["bf16"]
+    assert torch.equal(dp[0], before[0])
+    for r in range(R):
+        s = int(slot[r])
+        if int(accept[r]) == K:
+            assert torch.equal(dp[s], before[s])
+        else:
+            assert torch.equal(dp[s], states[r, int(accept[r])])
