@@ -64,6 +64,15 @@ def algorithmic_bytes_commit(w):
     return 2 * state + rows * (w.h_qk * w.d_k * in_b + w.h_v * w.d_v * in_b + 2 * w.h_v * 4)
 
 
+def algorithmic_bytes_verify(w, n_record):
+    """The verify pass (no outputs): the state read and written back, n_record recorded
+    states written, the block's k, v, g, beta read."""
+    in_b = 2 if w.dtype == "bf16" else 4
+    rows = w.requests * w.block
+    state = w.requests * w.h_v * w.d_k * w.d_v * 4
+    return (2 + n_record) * state + rows * (w.h_qk * w.d_k * in_b + w.h_v * w.d_v * in_b + 2 * w.h_v * 4)
+
+
 def time_launches(fn, steps, warmup, stream):
     import torch
     for _ in range(warmup):
@@ -247,6 +256,37 @@ def main():
         result["commit"] = {"workload": sw.name, "us_per_call": cms * 1e3, "gb_per_s": cgbs,
                             "frac_hbm": cgbs / HBM_PEAK_GBS, "algorithmic_bytes": cbytes,
                             "kernel": "bdgdn_k4_commit_kernel (state written back, no outputs)"}
+
+        # AR-Trust verify round: the verify pass keeping the states before the draft
+        # positions, then the accept step (offsets drawn below the horizon, so every
+        # request copies one state back)
+        vw = W.VERIFY_64
+        n_rec = vw.block - 1
+        vblk = {k: v.to(dev) for k, v in W.make_serve_block(vw, 0).items()}
+        states = torch.empty(vw.requests, n_rec, vw.h_v, vw.d_k, vw.d_v, dtype=torch.float32, device=dev)
+        gen = torch.Generator().manual_seed(vw.seed)
+        accept = torch.randint(0, n_rec, (vw.requests,), generator=gen, dtype=torch.int32).to(dev)
+
+        def vstep():
+            pool = pools[it[0] % len(pools)]
+            it[0] += 1
+            bd.bdgdn_commit_record(pool, vblk["q"], vblk["k"], vblk["v"], vblk["g"], vblk["beta"],
+                                   n_record=n_rec, scale=scale, states=states, stream=stream)
+        vms = time_launches(vstep, 3 * args.steps, args.warmup, stream)
+        vbytes = algorithmic_bytes_verify(vw, n_rec)
+
+        def astep():
+            pool = pools[it[0] % len(pools)]
+            it[0] += 1
+            bd.bdgdn_accept_states(pool, states, accept, block=vw.block, stream=stream)
+        ams = time_launches(astep, 3 * args.steps, args.warmup, stream)
+        abytes_acc = 2 * vw.requests * vw.h_v * vw.d_k * vw.d_v * 4
+        result["verify"] = {"workload": vw.name, "us_per_call": vms * 1e3,
+                            "gb_per_s": vbytes / (vms * 1e-3) / 1e9,
+                            "frac_hbm": vbytes / (vms * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": vbytes,
+                            "kernel": "bdgdn_k4_commit_record_kernel (7 recorded states, no outputs)",
+                            "accept_us_per_call": ams * 1e3,
+                            "accept_gb_per_s": abytes_acc / (ams * 1e-3) / 1e9}
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, inp)

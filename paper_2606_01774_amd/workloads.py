@@ -69,6 +69,9 @@ TRAIN_4K = TrainWorkload("train_bf16_b4_t4096_h16_d128_l32", 4, 4096, 16, 16, 12
 GVA_16K = TrainWorkload("gva_bf16_b2_t16384_hqk16_hv32_d128_l64", 2, 16384, 16, 32, 128, 128,
                         64, "bf16", 2)
 SERVE_64 = ServeWorkload("serve_bf16_r64_h32_d128_l32_x8", 64, 32, 32, 128, 128, 32, 8, "bf16", 3)
+# AR-Trust verify round: the anchor and 7 draft tokens per request (the verify pass keeps
+# the states before the 7 draft positions)
+VERIFY_64 = ServeWorkload("verify_bf16_r64_h32_d128_l8_rec7", 64, 32, 32, 128, 128, 8, 1, "bf16", 5)
 VARLEN_128K = TrainWorkload("varlen_bf16_n32_t131072_h16_d128_l32", 1, 131072, 16, 16, 128, 128,
                             32, "bf16", 4, n_docs=32, doc_min=512, doc_max=8192)
 
