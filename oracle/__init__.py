@@ -64,6 +64,10 @@ def _load():
         lib.oracle_commit_record.restype = I
         lib.oracle_accept_states.argtypes = [I, I, I, I, I, P, P, P, P]
         lib.oracle_accept_states.restype = I
+        lib.oracle_shortconv_fwd.argtypes = [I, P, I, I, I, I] + [P] * 6
+        lib.oracle_shortconv_fwd.restype = I
+        lib.oracle_shortconv_bwd.argtypes = [I, P, I, I, I, I] + [P] * 10
+        lib.oracle_shortconv_bwd.restype = I
         lib.oracle_set_threads.argtypes = [I]
         lib.oracle_max_threads.restype = I
         _lib = lib
@@ -190,3 +194,40 @@ def accept_states(pool, states, accept, *, slot=None):
     if rc != 0:
         raise RuntimeError(f"oracle_accept_states failed: {rc}")
     return pool
+
+
+def _conv_cu(rows, cu_seqlens):
+    cu = np.array([0, rows], np.int32) if cu_seqlens is None else np.asarray(cu_seqlens, np.int32)
+    return np.ascontiguousarray(cu), len(cu) - 1
+
+
+def shortconv_fwd(x, xn, w, bias=None, *, block, act=1, cu_seqlens=None):
+    """Two-stream ShortConv forward on one packed axis: x, xn [rows, D], w [D, W] (lag-i
+    weight in column i), bias [D] or None.  Returns (y, yn) in fp64."""
+    x, xn, w = _f64(x), _f64(xn), _f64(w)
+    b = None if bias is None else _f64(bias)
+    rows, D = x.shape
+    W = w.shape[1]
+    cu, n = _conv_cu(rows, cu_seqlens)
+    y, yn = np.zeros((rows, D)), np.zeros((rows, D))
+    rc = _load().oracle_shortconv_fwd(n, _ptr(cu), D, W, int(block), int(act), _ptr(x), _ptr(xn), _ptr(w),
+                                      _ptr(b), _ptr(y), _ptr(yn))
+    if rc != 0:
+        raise RuntimeError(f"oracle_shortconv_fwd failed: {rc}")
+    return y, yn
+
+
+def shortconv_bwd(x, xn, w, bias, dy, dyn, *, block, act=1, cu_seqlens=None):
+    """Backward of shortconv_fwd: returns (dx, dxn, dw, dbias or None) in fp64."""
+    x, xn, w, dy, dyn = map(_f64, (x, xn, w, dy, dyn))
+    b = None if bias is None else _f64(bias)
+    rows, D = x.shape
+    W = w.shape[1]
+    cu, n = _conv_cu(rows, cu_seqlens)
+    dx, dxn, dw = np.zeros((rows, D)), np.zeros((rows, D)), np.zeros((D, W))
+    db = None if bias is None else np.zeros(D)
+    rc = _load().oracle_shortconv_bwd(n, _ptr(cu), D, W, int(block), int(act), _ptr(x), _ptr(xn), _ptr(w),
+                                      _ptr(b), _ptr(dy), _ptr(dyn), _ptr(dx), _ptr(dxn), _ptr(dw), _ptr(db))
+    if rc != 0:
+        raise RuntimeError(f"oracle_shortconv_bwd failed: {rc}")
+    return dx, dxn, dw, db

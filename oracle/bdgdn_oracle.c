@@ -24,6 +24,8 @@
  *     the AR-Trust verify pass also keeps the states at the verify positions, and the
  *     accept step writes the state at each request's accepted offset back to the pool
  *     (Appendix "Serving-system machinery", cache-and-scatter).
+ *   - the two-stream 1D causal ShortConv feeding the GDR, forward and backward
+ *     (Appendix "ShortConv under two-stream training").
  *
  * Layouts (row = token index in the flattened [B*T] or packed token axis):
  *   q,k  [row][h_qk][d_k]    v,o [row][h_v][d_v]    g,beta [row][h_v]
@@ -310,6 +312,103 @@ int oracle_accept_states(int R, int h_v, int dk, int dv, int n_rec, double *pool
         for (int h = 0; h < h_v; ++h)
             memcpy(pool + ((size_t)s * h_v + h) * ssz,
                    states + (((size_t)r * n_rec + accept[r]) * h_v + h) * ssz, ssz * sizeof(double));
+    }
+    return 0;
+}
+
+/*
+ * The two-stream 1D causal ShortConv (Appendix "ShortConv under two-stream training",
+ * eq. short-conv-clean and eq. short-conv-noisy) for one packed axis of rows:
+ *   clean  pre_t  = bias + sum_i w_i * xc_(t-i)
+ *   noisy  pre~_l = bias + sum_i w_i * z_(l,i),  z_(l,i) = xn_(l-i) if l-i >= the start of
+ *          l's diffusion block, else xc_(l-i)
+ *   y = act(pre): act 0 = identity, 1 = silu (x / (1 + exp(-x)))
+ * depthwise over D channels (w [D][W], w[c][i] = the lag-i weight), every read outside the
+ * current document (before its start) contributing zero; documents and blocks as in the
+ * training schedule (blocks counted from each document start).  x, xn, y, yn: [rows][D].
+ */
+static double act_of(double p, int act) { return act ? p / (1.0 + exp(-p)) : p; }
+static double act_grad(double p, int act)
+{
+    if (!act) return 1.0;
+    const double sg = 1.0 / (1.0 + exp(-p));
+    return sg * (1.0 + p * (1.0 - sg));
+}
+
+/* pre-activations of one position of both streams (doc starts at row a) */
+static void conv_pre(long t, long a, int L, int D, int W, int c, const double *x, const double *xn,
+                     const double *w, const double *bias, double *pc, double *pn)
+{
+    const long blk = a + ((t - a) / L) * L;   /* start of t's diffusion block */
+    double sc = bias ? bias[c] : 0.0, sn = sc;
+    for (int i = 0; i < W; ++i) {
+        const long src = t - i;
+        if (src < a) break;
+        sc += w[c * W + i] * x[src * D + c];
+        sn += w[c * W + i] * (src >= blk ? xn[src * D + c] : x[src * D + c]);
+    }
+    *pc = sc;
+    *pn = sn;
+}
+
+int oracle_shortconv_fwd(int n_docs, const int32_t *cu, int D, int W, int L, int act,
+                         const double *x, const double *xn, const double *w, const double *bias,
+                         double *y, double *yn)
+{
+    if (n_docs < 1 || D < 1 || W < 1 || L < 1) return -1;
+    for (int d = 0; d < n_docs; ++d)
+        for (long t = cu[d]; t < cu[d + 1]; ++t)
+            for (int c = 0; c < D; ++c) {
+                double pc, pn;
+                conv_pre(t, cu[d], L, D, W, c, x, xn, w, bias, &pc, &pn);
+                y[t * D + c] = act_of(pc, act);
+                yn[t * D + c] = act_of(pn, act);
+            }
+    return 0;
+}
+
+/*
+ * Backward of oracle_shortconv_fwd: given dy, dyn, the gradients of the loss with respect
+ * to x, xn, w and bias (dx, dxn, dw [D][W], dbias [D], all overwritten), by the chain rule
+ * through every read of the forward: each output's pre-activation gradient
+ * dpre = dy act'(pre) is sent to the input it read at each lag (the clean or the noisy
+ * stream, as chosen in the forward) times that lag's weight, and to w and bias.
+ */
+int oracle_shortconv_bwd(int n_docs, const int32_t *cu, int D, int W, int L, int act,
+                         const double *x, const double *xn, const double *w, const double *bias,
+                         const double *dy, const double *dyn, double *dx, double *dxn, double *dw,
+                         double *dbias)
+{
+    if (n_docs < 1 || D < 1 || W < 1 || L < 1) return -1;
+    const long rows = cu[n_docs];
+    memset(dx, 0, (size_t)rows * D * sizeof(double));
+    memset(dxn, 0, (size_t)rows * D * sizeof(double));
+    memset(dw, 0, (size_t)D * W * sizeof(double));
+    if (dbias) memset(dbias, 0, (size_t)D * sizeof(double));
+    for (int d = 0; d < n_docs; ++d) {
+        const long a = cu[d];
+        for (long t = a; t < cu[d + 1]; ++t)
+            for (int c = 0; c < D; ++c) {
+                double pc, pn;
+                conv_pre(t, a, L, D, W, c, x, xn, w, bias, &pc, &pn);
+                const double gc = dy[t * D + c] * act_grad(pc, act);
+                const double gn = dyn[t * D + c] * act_grad(pn, act);
+                if (dbias) dbias[c] += gc + gn;
+                const long blk = a + ((t - a) / L) * L;
+                for (int i = 0; i < W; ++i) {
+                    const long src = t - i;
+                    if (src < a) break;
+                    dx[src * D + c] += w[c * W + i] * gc;
+                    dw[c * W + i] += gc * x[src * D + c];
+                    if (src >= blk) {
+                        dxn[src * D + c] += w[c * W + i] * gn;
+                        dw[c * W + i] += gn * xn[src * D + c];
+                    } else {
+                        dx[src * D + c] += w[c * W + i] * gn;
+                        dw[c * W + i] += gn * x[src * D + c];
+                    }
+                }
+            }
     }
     return 0;
 }

@@ -68,6 +68,13 @@ MUTANTS = {
         "                    memcpy(states + (((size_t)r * n_rec + i) * h_v + h) * ssz, S, ssz * sizeof(double));\n"),
     "accept_offset_shift": ("states + (((size_t)r * n_rec + accept[r]) * h_v + h) * ssz",
                             "states + (((size_t)r * n_rec + (accept[r] + 1) % n_rec) * h_v + h) * ssz"),
+    "conv_noisy_block_rule": ("sn += w[c * W + i] * (src >= blk ? xn[src * D + c] : x[src * D + c]);",
+                              "sn += w[c * W + i] * (src > blk ? xn[src * D + c] : x[src * D + c]);"),
+    "conv_reads_across_documents": ("        if (src < a) break;\n        sc += w[c * W + i] * x[src * D + c];",
+                                    "        if (src < 0) break;\n        sc += w[c * W + i] * x[src * D + c];"),
+    "conv_silu_grad": ("return sg * (1.0 + p * (1.0 - sg));", "return sg;"),
+    "conv_dw_misses_noisy": ("                        dw[c * W + i] += gn * xn[src * D + c];",
+                             "                        dw[c * W + i] += 0.0 * gn * xn[src * D + c];"),
     "commit_skips_last_token": ("for (long t = (long)r * L; t < (long)r * L + L; ++t) {",
                                 "for (long t = (long)r * L; t < (long)r * L + L - 1; ++t) {"),
 }

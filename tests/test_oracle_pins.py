@@ -446,3 +446,80 @@ def test_pin_accept_states_rewinds_to_accepted_offset():
         np.testing.assert_array_equal(out[r], want[0])
     with pytest.raises(RuntimeError):
         oracle.accept_states(vpool, states, np.array([0, 1, K + 1, 0], np.int32))
+
+
+# ------------------------- two-stream 1D causal ShortConv -------------------------
+def _silu(p):
+    return p / (1.0 + np.exp(-p))
+
+
+def _conv_inputs(rng, rows, D, W):
+    x = rng.standard_normal((rows, D))
+    xn = rng.standard_normal((rows, D))
+    w = rng.standard_normal((D, W)) * 0.5
+    b = rng.standard_normal(D) * 0.1
+    return x, xn, w, b
+
+
+@pytest.mark.parametrize("act", [0, 1])
+def test_pin_shortconv_clean_is_causal_convolution(act):
+    """The clean output is the standard causal depthwise convolution of each document
+    (numpy's full convolution, first T terms), plus bias, through the activation."""
+    rng = np.random.default_rng(40)
+    cu = np.array([0, 7, 7, 19, 24], np.int32)   # an empty document
+    x, xn, w, b = _conv_inputs(rng, 24, 3, 4)
+    y, _ = oracle.shortconv_fwd(x, xn, w, b, block=3, act=act, cu_seqlens=cu)
+    f = _silu if act else (lambda p: p)
+    for d in range(len(cu) - 1):
+        a, e = cu[d], cu[d + 1]
+        if e == a:
+            continue
+        for c in range(3):
+            ref = np.convolve(x[a:e, c], w[c])[: e - a] + b[c]
+            np.testing.assert_allclose(y[a:e, c], f(ref), rtol=1e-13, atol=1e-14)
+
+
+def test_pin_shortconv_noisy_block_rules():
+    """Noisy outputs: one block covering the document is the convolution of the noisy
+    stream alone; identical streams give the clean output for any block; blocks of one
+    position read the noisy input at lag 0 and the clean inputs at every other lag."""
+    rng = np.random.default_rng(41)
+    rows, D, W = 11, 2, 4
+    x, xn, w, b = _conv_inputs(rng, rows, D, W)
+    _, yn = oracle.shortconv_fwd(x, xn, w, b, block=64, act=0)
+    for c in range(D):
+        np.testing.assert_allclose(yn[:, c], np.convolve(xn[:, c], w[c])[:rows] + b[c], rtol=1e-13, atol=1e-14)
+    for L in (1, 2, 3, 5):
+        y, yn = oracle.shortconv_fwd(x, x, w, b, block=L, act=1)
+        np.testing.assert_array_equal(y, yn)
+    _, yn = oracle.shortconv_fwd(x, xn, w, b, block=1, act=0)
+    for t in range(rows):
+        want = b + w[:, 0] * xn[t] + sum(w[:, i] * x[t - i] for i in range(1, W) if t - i >= 0)
+        np.testing.assert_allclose(yn[t], want, rtol=1e-13, atol=1e-14)
+
+
+@pytest.mark.parametrize("act", [0, 1])
+def test_pin_shortconv_backward_is_gradient(act):
+    """The backward equals central finite differences of the (pinned) forward for a
+    random linear functional of both outputs, with documents and several blocks."""
+    rng = np.random.default_rng(42 + act)
+    cu = np.array([0, 5, 12], np.int32)
+    rows, D, W, L = 12, 2, 4, 3
+    x, xn, w, b = _conv_inputs(rng, rows, D, W)
+    gy, gyn = rng.standard_normal((rows, D)), rng.standard_normal((rows, D))
+    loss = lambda x_, xn_, w_, b_: float(np.sum(gy * oracle.shortconv_fwd(x_, xn_, w_, b_, block=L, act=act,
+                                                                           cu_seqlens=cu)[0])
+                                         + np.sum(gyn * oracle.shortconv_fwd(x_, xn_, w_, b_, block=L, act=act,
+                                                                              cu_seqlens=cu)[1]))
+    dx, dxn, dw, db = oracle.shortconv_bwd(x, xn, w, b, gy, gyn, block=L, act=act, cu_seqlens=cu)
+    h = 1e-6
+    for name, arr, grad in (("x", x, dx), ("xn", xn, dxn), ("w", w, dw), ("b", b, db)):
+        fd = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            args = {"x": x, "xn": xn, "w": w, "b": b}
+            hi = {k: v.copy() for k, v in args.items()}
+            lo = {k: v.copy() for k, v in args.items()}
+            hi[name][idx] += h
+            lo[name][idx] -= h
+            fd[idx] = (loss(hi["x"], hi["xn"], hi["w"], hi["b"]) - loss(lo["x"], lo["xn"], lo["w"], lo["b"])) / (2 * h)
+        np.testing.assert_allclose(grad, fd, rtol=1e-6, atol=1e-7, err_msg=name)
