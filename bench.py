@@ -6,7 +6,8 @@ state and fp32 outputs, inputs resident in HBM.  `value` is tokens/s (clean +
 noisy tokens).  The line also carries the roofline of the fused kernel (HBM
 bytes the algorithm must move per launch over its measured duration), the
 model-FLOP rate against the bf16/fp16 MFMA peak, the denoise_step and commit
-bandwidths of the 64-request serving workload, and the fp64 CPU oracle timed on
+bandwidths of the 64-request serving workload, the two-stream ShortConv forward and
+backward bandwidths at the training token shape, and the fp64 CPU oracle timed on
 the same workload.
 
   python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
@@ -71,6 +72,13 @@ def algorithmic_bytes_verify(w, n_record):
     rows = w.requests * w.block
     state = w.requests * w.h_v * w.d_k * w.d_v * 4
     return (2 + n_record) * state + rows * (w.h_qk * w.d_k * in_b + w.h_v * w.d_v * in_b + 2 * w.h_v * 4)
+
+
+def algorithmic_bytes_conv(w, backward):
+    """ShortConv: the forward reads x, xn and writes y, yn; the backward reads x, xn, dy,
+    dyn and writes dx, dxn (the filter, bias and their gradients are negligible)."""
+    es = 2 if w.dtype == "bf16" else 4
+    return (6 if backward else 4) * w.batch * w.seqlen * w.channels * es
 
 
 def time_launches(fn, steps, warmup, stream):
@@ -157,6 +165,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-serve", action="store_true")
+    ap.add_argument("--no-conv", action="store_true")
     ap.add_argument("--route", choices=sorted(ROUTES), default="fused",
                     help="schedule of the training forward (fused is the performance mode; split and "
                          "records attribute its parts to separate kernels)")
@@ -287,6 +296,37 @@ def main():
                             "kernel": "bdgdn_k4_commit_record_kernel (7 recorded states, no outputs)",
                             "accept_us_per_call": ams * 1e3,
                             "accept_gb_per_s": abytes_acc / (ams * 1e-3) / 1e9}
+
+    if not args.no_conv:
+        # the GDN layer's two-stream ShortConv at the same token shape (channels = the q, k
+        # and v projections side by side), forward and backward
+        cw = W.CONV_TRAIN
+        cin = {k: (None if v is None else v.to(dev)) for k, v in W.make_conv(cw).items()}
+        y, yn = torch.empty_like(cin["x"]), torch.empty_like(cin["x"])
+        dx, dxn = torch.empty_like(cin["x"]), torch.empty_like(cin["x"])
+        dw, db = torch.empty_like(cin["w"]), torch.empty_like(cin["bias"])
+        cdesc = bd.make_conv_desc(cin["x"], cin["w"], block=cw.block, activation=cw.act)
+        cws = torch.empty(max(256, bd.bdgdn_shortconv_bwd_workspace(cdesc)), dtype=torch.uint8, device=dev)
+
+        def fstep():
+            bd.bdgdn_shortconv_fwd(cin["x"], cin["xn"], cin["w"], cin["bias"], block=cw.block, activation=cw.act,
+                                   y=y, yn=yn, stream=stream)
+
+        def bstep():
+            bd.bdgdn_shortconv_bwd(cin["x"], cin["xn"], cin["w"], cin["bias"], cin["dy"], cin["dyn"],
+                                   block=cw.block, activation=cw.act, dx=dx, dxn=dxn, dw=dw, dbias=db,
+                                   workspace=cws, stream=stream)
+        fms = time_launches(fstep, args.steps, args.warmup, stream)
+        bms = time_launches(bstep, args.steps, args.warmup, stream)
+        fbytes, bbytes = algorithmic_bytes_conv(cw, backward=False), algorithmic_bytes_conv(cw, backward=True)
+        result["shortconv"] = {
+            "workload": cw.name,
+            "fwd": {"us_per_call": fms * 1e3, "gb_per_s": fbytes / (fms * 1e-3) / 1e9,
+                    "frac_hbm": fbytes / (fms * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": fbytes,
+                    "kernel": "bdgdn_shortconv_fwd_kernel"},
+            "bwd": {"us_per_call": bms * 1e3, "gb_per_s": bbytes / (bms * 1e-3) / 1e9,
+                    "frac_hbm": bbytes / (bms * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": bbytes,
+                    "kernel": "bdgdn_shortconv_bwd_kernel + bdgdn_shortconv_reduce_kernel"}}
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, inp)

@@ -228,6 +228,64 @@ int bdgdn_commit_record(const bdgdn_serve_desc_t *desc, float *state_pool, const
 int bdgdn_accept_states(const bdgdn_serve_desc_t *desc, float *state_pool, const int32_t *slot,
                         const float *states, int32_t n_record, const int32_t *accept, void *stream);
 
+/*
+ * The two-stream 1D causal ShortConv in front of the GDR inputs (Appendix "ShortConv under
+ * two-stream training", eq. short-conv-clean and eq. short-conv-noisy, computed in the fused
+ * form that picks each lag's stream in place), per channel c with filter w[c][0..W-1]:
+ *
+ *   y[t]   = act(bias[c] + sum_i w[c][i] x[t-i])
+ *   yn[t]  = act(bias[c] + sum_i w[c][i] z(t, t-i)),  z(t, s) = xn[s] if s lies in t's
+ *            diffusion block, else x[s]
+ *
+ * with diffusion blocks of `block` rows counted from each sequence's (or document's) start,
+ * and rows before that start read as zero (Appendix "Document-packed training", the
+ * ShortConv lag mask).  act is the identity or silu.
+ *
+ *   x, xn, y, yn   [B*T][channels] of dtype (the clean and noisy streams), 8-byte aligned
+ *   w              [channels][width] fp32, w[c][i] the weight of lag i
+ *   bias           [channels] fp32, or NULL for none
+ *   cu_seqlens_*   both NULL (B sequences of T rows) or both [N+1] int32 offsets into the
+ *                  packed rows (B == 1, cu[0] == 0, cu[N] == T, non-decreasing; any
+ *                  document lengths).  The two copies must hold the same values.
+ * Supported: dtype bf16 or fp32, 1 <= width <= 4, channels a multiple of 4 (bf16) or 2
+ * (fp32); else BDGDN_ERR_UNSUPPORTED.  The token tensors may be NULL when B*T == 0.
+ * Results are deterministic.
+ */
+typedef enum { BDGDN_ACT_NONE = 0, BDGDN_ACT_SILU = 1 } bdgdn_act_t;
+
+typedef struct {
+    int32_t batch;      /* B sequences; must be 1 when packed (num_seqs > 0)           */
+    int32_t seqlen;     /* T rows per sequence, or total packed rows                    */
+    int32_t num_seqs;   /* N packed documents, 0 when not packed                        */
+    int32_t channels;   /* D, the row length of every token tensor                      */
+    int32_t width;      /* W filter taps                                                */
+    int32_t block;      /* diffusion block size L                                       */
+    int32_t activation; /* bdgdn_act_t                                                  */
+    int32_t dtype;      /* bdgdn_dtype_t of x, xn, y, yn, dy, dyn, dx, dxn              */
+} bdgdn_conv_desc_t;
+
+/* Forward: writes every row of y and yn. */
+int bdgdn_shortconv_fwd(const bdgdn_conv_desc_t *desc, const void *x, const void *xn, const float *w,
+                        const float *bias, const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                        void *y, void *yn, void *stream);
+
+/* Bytes of device workspace bdgdn_shortconv_bwd needs (0 when there are no rows, or for a
+ * descriptor it would reject). */
+size_t bdgdn_shortconv_bwd_workspace(const bdgdn_conv_desc_t *desc);
+
+/*
+ * Backward of bdgdn_shortconv_fwd for the upstream gradients dy, dyn ([B*T][channels],
+ * dtype): writes dx, dxn (dtype, every row), dw ([channels][width] fp32) and, when not
+ * NULL, dbias ([channels] fp32); all are overwritten, not accumulated into.  Each noisy
+ * output's gradient flows to the stream it read at each lag.  workspace: device memory
+ * of at least bdgdn_shortconv_bwd_workspace(desc) bytes, 256-byte aligned, scratch owned
+ * by the call until the stream passes it.
+ */
+int bdgdn_shortconv_bwd(const bdgdn_conv_desc_t *desc, const void *x, const void *xn, const float *w,
+                        const float *bias, const void *dy, const void *dyn, const int32_t *cu_seqlens_dev,
+                        const int32_t *cu_seqlens_host, void *dx, void *dxn, float *dw, float *dbias,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -22,7 +22,8 @@ __all__ = [
     "BdgdnError", "BDGDN_BF16", "BDGDN_F32", "BDGDN_ROUTE_FUSED", "BDGDN_ROUTE_SPLIT",
     "BDGDN_ROUTE_ONEPASS", "BDGDN_ROUTE_RECORDS",
     "bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace", "bdgdn_fwd_train",
-    "bdgdn_commit_record", "bdgdn_accept_states",
+    "bdgdn_commit_record", "bdgdn_accept_states", "BDGDN_ACT_NONE", "BDGDN_ACT_SILU",
+    "bdgdn_shortconv_fwd", "bdgdn_shortconv_bwd_workspace", "bdgdn_shortconv_bwd",
     "bdgdn_denoise_step", "bdgdn_commit", "library_path", "load_library", "EXPORTED_SYMBOLS",
 ]
 
@@ -41,10 +42,13 @@ BDGDN_ROUTE_FUSED = 0
 BDGDN_ROUTE_SPLIT = 1
 BDGDN_ROUTE_ONEPASS = 2
 BDGDN_ROUTE_RECORDS = 3
+BDGDN_ACT_NONE = 0
+BDGDN_ACT_SILU = 1
 
 EXPORTED_SYMBOLS = ("bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace",
                     "bdgdn_fwd_train", "bdgdn_denoise_step", "bdgdn_commit", "bdgdn_commit_record",
-                    "bdgdn_accept_states")
+                    "bdgdn_accept_states", "bdgdn_shortconv_fwd", "bdgdn_shortconv_bwd_workspace",
+                    "bdgdn_shortconv_bwd")
 
 
 class FwdDesc(ctypes.Structure):
@@ -61,6 +65,13 @@ class ServeDesc(ctypes.Structure):
                 ("h_v", ctypes.c_int32), ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32),
                 ("block", ctypes.c_int32), ("scale", ctypes.c_float),
                 ("dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32)]
+
+
+class ConvDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("seqlen", ctypes.c_int32),
+                ("num_seqs", ctypes.c_int32), ("channels", ctypes.c_int32),
+                ("width", ctypes.c_int32), ("block", ctypes.c_int32),
+                ("activation", ctypes.c_int32), ("dtype", ctypes.c_int32)]
 
 
 class BdgdnError(RuntimeError):
@@ -100,6 +111,12 @@ def load_library():
     lib.bdgdn_commit_record.restype = ctypes.c_int
     lib.bdgdn_accept_states.argtypes = [ctypes.POINTER(ServeDesc), P, P, P, ctypes.c_int32, P, P]
     lib.bdgdn_accept_states.restype = ctypes.c_int
+    lib.bdgdn_shortconv_fwd.argtypes = [ctypes.POINTER(ConvDesc)] + [P] * 9
+    lib.bdgdn_shortconv_fwd.restype = ctypes.c_int
+    lib.bdgdn_shortconv_bwd_workspace.argtypes = [ctypes.POINTER(ConvDesc)]
+    lib.bdgdn_shortconv_bwd_workspace.restype = ctypes.c_size_t
+    lib.bdgdn_shortconv_bwd.argtypes = [ctypes.POINTER(ConvDesc)] + [P] * 13 + [ctypes.c_size_t, P]
+    lib.bdgdn_shortconv_bwd.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -317,3 +334,91 @@ def bdgdn_accept_states(state_pool, states, accept, *, block, h_qk=None, slot=No
     st = lib.bdgdn_accept_states(ctypes.byref(desc), _ptr(state_pool), _ptr(slot), _ptr(states),
                                  int(n_record), _ptr(accept), _stream(stream))
     _check(st, "bdgdn_accept_states")
+
+
+# ------------------------------------------------------------------ ShortConv
+def _conv_packing(x, cu_seqlens, cu_seqlens_host):
+    if x.dim() != 3:
+        raise ValueError("x must be [B, T, channels]")
+    if cu_seqlens is None:
+        return 0, None
+    _dev(cu_seqlens, "cu_seqlens", torch.int32)
+    n = cu_seqlens.numel() - 1
+    if cu_seqlens_host is None:
+        cu_seqlens_host = cu_seqlens.cpu()
+    cu_h = torch.as_tensor(cu_seqlens_host, dtype=torch.int32).contiguous()
+    if cu_h.numel() != n + 1:
+        raise ValueError("cu_seqlens_host and cu_seqlens differ in length")
+    return n, cu_h
+
+
+def make_conv_desc(x, w, *, block, activation=BDGDN_ACT_SILU, num_seqs=0):
+    """Descriptor from x [B, T, channels] and w [channels, width]."""
+    B, T, D = x.shape
+    return ConvDesc(B, T, num_seqs, D, int(w.shape[1]), int(block), int(activation), _DT.get(x.dtype, -1))
+
+
+def bdgdn_shortconv_fwd(x, xn, w, bias=None, *, block, activation=BDGDN_ACT_SILU, cu_seqlens=None,
+                        cu_seqlens_host=None, y=None, yn=None, stream=None):
+    """Two-stream ShortConv forward.  x, xn [B, T, channels] (bf16 or fp32; packed: B == 1
+    and cu_seqlens [N+1] int32 on the device), w [channels, width] fp32 (lag-i weight in
+    column i), bias [channels] fp32 or None.  Returns (y, yn) of x's dtype."""
+    lib = load_library()
+    _dev(x, "x")
+    _dev(xn, "xn", x.dtype)
+    _dev(w, "w", torch.float32)
+    _dev(bias, "bias", torch.float32)
+    n, cu_h = _conv_packing(x, cu_seqlens, cu_seqlens_host)
+    if xn.shape != x.shape or w.dim() != 2 or w.shape[0] != x.shape[2]:
+        raise ValueError("xn must match x and w must be [channels, width]")
+    desc = make_conv_desc(x, w, block=block, activation=activation, num_seqs=n)
+    if y is None:
+        y = torch.empty_like(x)
+    if yn is None:
+        yn = torch.empty_like(x)
+    _dev(y, "y", x.dtype)
+    _dev(yn, "yn", x.dtype)
+    st = lib.bdgdn_shortconv_fwd(ctypes.byref(desc), _ptr(x), _ptr(xn), _ptr(w), _ptr(bias), _ptr(cu_seqlens),
+                                 None if cu_h is None else ctypes.c_void_p(cu_h.data_ptr()), _ptr(y), _ptr(yn),
+                                 _stream(stream))
+    _check(st, "bdgdn_shortconv_fwd")
+    return y, yn
+
+
+def bdgdn_shortconv_bwd_workspace(desc: ConvDesc) -> int:
+    return int(load_library().bdgdn_shortconv_bwd_workspace(ctypes.byref(desc)))
+
+
+def bdgdn_shortconv_bwd(x, xn, w, bias, dy, dyn, *, block, activation=BDGDN_ACT_SILU, cu_seqlens=None,
+                        cu_seqlens_host=None, dx=None, dxn=None, dw=None, dbias=None, workspace=None,
+                        stream=None):
+    """Backward of bdgdn_shortconv_fwd for upstream gradients dy, dyn (x's shape and dtype).
+    Returns (dx, dxn, dw, dbias); dbias is None when bias is None."""
+    lib = load_library()
+    _dev(x, "x")
+    for name, t in (("xn", xn), ("dy", dy), ("dyn", dyn)):
+        _dev(t, name, x.dtype)
+        if t.shape != x.shape:
+            raise ValueError(f"{name} must match x")
+    _dev(w, "w", torch.float32)
+    _dev(bias, "bias", torch.float32)
+    n, cu_h = _conv_packing(x, cu_seqlens, cu_seqlens_host)
+    desc = make_conv_desc(x, w, block=block, activation=activation, num_seqs=n)
+    dx = torch.empty_like(x) if dx is None else dx
+    dxn = torch.empty_like(x) if dxn is None else dxn
+    dw = torch.empty_like(w) if dw is None else dw
+    if dbias is None and bias is not None:
+        dbias = torch.empty_like(bias)
+    for name, t, dt in (("dx", dx, x.dtype), ("dxn", dxn, x.dtype), ("dw", dw, torch.float32),
+                        ("dbias", dbias, torch.float32)):
+        _dev(t, name, dt)
+    ws_bytes = bdgdn_shortconv_bwd_workspace(desc)
+    if workspace is None and ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=x.device)
+    ws_size = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.bdgdn_shortconv_bwd(ctypes.byref(desc), _ptr(x), _ptr(xn), _ptr(w), _ptr(bias), _ptr(dy), _ptr(dyn),
+                                 _ptr(cu_seqlens), None if cu_h is None else ctypes.c_void_p(cu_h.data_ptr()),
+                                 _ptr(dx), _ptr(dxn), _ptr(dw), _ptr(dbias), _ptr(workspace), ws_size,
+                                 _stream(stream))
+    _check(st, "bdgdn_shortconv_bwd")
+    return dx, dxn, dw, dbias

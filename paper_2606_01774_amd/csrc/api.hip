@@ -72,6 +72,43 @@ int check_fwd(const bdgdn_fwd_desc_t *d, const int32_t *cu_dev, const int32_t *c
     return BDGDN_OK;
 }
 
+// Validation of a ShortConv descriptor and its packing.  Blocks are counted from each
+// document start, so document starts need no alignment.
+int check_conv(const bdgdn_conv_desc_t *d, const int32_t *cu_dev, const int32_t *cu_host)
+{
+    if (!d) return BDGDN_ERR_INVALID_ARG;
+    if (d->batch <= 0 || d->seqlen < 0 || d->num_seqs < 0 || d->channels <= 0 || d->block <= 0)
+        return BDGDN_ERR_INVALID_ARG;
+    if (d->activation != BDGDN_ACT_NONE && d->activation != BDGDN_ACT_SILU) return BDGDN_ERR_INVALID_ARG;
+    if (d->dtype != BDGDN_BF16 && d->dtype != BDGDN_F32) return BDGDN_ERR_UNSUPPORTED;
+    if (d->width < 1 || d->width > 4) return BDGDN_ERR_UNSUPPORTED;
+    if (d->channels % (d->dtype == BDGDN_BF16 ? 4 : 2) != 0) return BDGDN_ERR_UNSUPPORTED;
+    if ((long)d->batch * d->seqlen > 0x7fffffffL) return BDGDN_ERR_UNSUPPORTED;
+    const bool packed = d->num_seqs > 0;
+    if (packed != (cu_dev != nullptr) || packed != (cu_host != nullptr)) return BDGDN_ERR_INVALID_ARG;
+    if (packed) {
+        if (d->batch != 1) return BDGDN_ERR_INVALID_ARG;
+        if (cu_host[0] != 0 || cu_host[d->num_seqs] != d->seqlen) return BDGDN_ERR_INVALID_ARG;
+        for (int i = 0; i < d->num_seqs; ++i)
+            if (cu_host[i + 1] < cu_host[i]) return BDGDN_ERR_INVALID_ARG;
+    }
+    return BDGDN_OK;
+}
+
+bool aligned8(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 7) == 0; }
+
+ConvArgs conv_args(const bdgdn_conv_desc_t *d, const int32_t *cu_dev, const void *x, const void *xn,
+                   const float *w, const float *bias, void *y, void *yn)
+{
+    ConvArgs a = {};
+    a.x = x; a.xn = xn; a.w = w; a.bias = bias; a.y = y; a.yn = yn;
+    a.cu = d->num_seqs > 0 ? cu_dev : nullptr;
+    a.rows = (long)d->batch * d->seqlen;
+    a.D = d->channels; a.L = d->block; a.act = d->activation;
+    a.n_docs = d->num_seqs; a.seqlen = d->seqlen;
+    return a;
+}
+
 }  // namespace
 
 extern "C" {
@@ -316,6 +353,50 @@ int bdgdn_accept_states(const bdgdn_serve_desc_t *desc, float *state_pool, const
     a.n_rec = n_record;
     a.accept = accept;
     hipError_t e = launch_accept_states(a, desc->d_k, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+}
+
+size_t bdgdn_shortconv_bwd_workspace(const bdgdn_conv_desc_t *desc)
+{
+    if (!desc || desc->batch <= 0 || desc->seqlen < 0 || desc->channels <= 0 || desc->width < 1 || desc->width > 4)
+        return 0;
+    return conv_part_floats((long)desc->batch * desc->seqlen, desc->channels, desc->width) * sizeof(float);
+}
+
+int bdgdn_shortconv_fwd(const bdgdn_conv_desc_t *desc, const void *x, const void *xn, const float *w,
+                        const float *bias, const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                        void *y, void *yn, void *stream)
+{
+    int st = check_conv(desc, cu_seqlens_dev, cu_seqlens_host);
+    if (st != BDGDN_OK) return st;
+    const bool any = (long)desc->batch * desc->seqlen > 0;   // token tensors may be NULL without rows
+    if (!w || (any && (!x || !xn || !y || !yn))) return BDGDN_ERR_INVALID_ARG;
+    if (!aligned8(x) || !aligned8(xn) || !aligned8(y) || !aligned8(yn)) return BDGDN_ERR_INVALID_ARG;
+    const ConvArgs a = conv_args(desc, cu_seqlens_dev, x, xn, w, bias, y, yn);
+    hipError_t e = launch_shortconv_fwd(desc->dtype == BDGDN_BF16, desc->width, a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+}
+
+int bdgdn_shortconv_bwd(const bdgdn_conv_desc_t *desc, const void *x, const void *xn, const float *w,
+                        const float *bias, const void *dy, const void *dyn, const int32_t *cu_seqlens_dev,
+                        const int32_t *cu_seqlens_host, void *dx, void *dxn, float *dw, float *dbias,
+                        void *workspace, size_t workspace_bytes, void *stream)
+{
+    int st = check_conv(desc, cu_seqlens_dev, cu_seqlens_host);
+    if (st != BDGDN_OK) return st;
+    const bool any = (long)desc->batch * desc->seqlen > 0;
+    if (!w || !dw || (any && (!x || !xn || !dy || !dyn || !dx || !dxn))) return BDGDN_ERR_INVALID_ARG;
+    if (!aligned8(x) || !aligned8(xn) || !aligned8(dy) || !aligned8(dyn) || !aligned8(dx) || !aligned8(dxn))
+        return BDGDN_ERR_INVALID_ARG;
+    const size_t need = bdgdn_shortconv_bwd_workspace(desc);
+    if (need > 0 && (workspace_bytes < need || !workspace)) return BDGDN_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return BDGDN_ERR_WORKSPACE;
+    ConvArgs a = conv_args(desc, cu_seqlens_dev, x, xn, w, bias, dx, dxn);
+    a.dy = dy; a.dyn = dyn;
+    a.part = static_cast<float *>(workspace);
+    a.dw = dw;
+    a.dbias = dbias;
+    hipError_t e = launch_shortconv_bwd(desc->dtype == BDGDN_BF16, desc->width, a, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
 }
 

@@ -111,4 +111,20 @@ int serve_tile_v();
 // Whether the (types, d_k, lp) combination is instantiated and fits in LDS.
 bool fwd_supported(Types ty, int dk, int lp);
 
+// The two-stream ShortConv (conv_kernels.hip).  x, xn, y, yn, dy, dyn are [rows][D] of the
+// conv dtype; w [D][W] and bias [D] fp32; part [row groups][W + 1][D] fp32 partials of the
+// backward; n_rg is set by the launchers.
+struct ConvArgs {
+    const void *x, *xn, *dy, *dyn;
+    const float *w, *bias;
+    const int32_t *cu;   // [n_docs + 1] device offsets, or NULL for sequences of seqlen rows
+    void *y, *yn;        // forward outputs, or dx, dxn in the backward
+    float *part, *dw, *dbias;
+    long rows;
+    int D, L, act, n_docs, seqlen, n_rg;
+};
+size_t conv_part_floats(long rows, int D, int width);
+hipError_t launch_shortconv_fwd(bool bf16, int width, const ConvArgs &a, hipStream_t s);
+hipError_t launch_shortconv_bwd(bool bf16, int width, const ConvArgs &a, hipStream_t s);
+
 }  // namespace bdgdn

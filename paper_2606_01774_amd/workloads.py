@@ -63,6 +63,22 @@ class ServeWorkload:
     seed: int
 
 
+@dataclass(frozen=True)
+class ConvWorkload:
+    """Two-stream ShortConv: ``batch`` sequences of ``seqlen`` clean and ``seqlen`` noisy
+    rows of ``channels`` (the q, k, v projections side by side), a depthwise causal
+    filter of ``width`` taps, diffusion blocks of ``block`` rows."""
+    name: str
+    batch: int
+    seqlen: int
+    channels: int
+    width: int
+    block: int
+    act: int
+    dtype: str
+    seed: int
+
+
 TINY_F32 = TrainWorkload("tiny_f32_b1_t256_h2_d64_l16", 1, 256, 2, 2, 64, 64, 16, "f32", 0)
 TRAIN_4K = TrainWorkload("train_bf16_b4_t4096_h16_d128_l32", 4, 4096, 16, 16, 128, 128, 32,
                          "bf16", 1)
@@ -75,7 +91,12 @@ VERIFY_64 = ServeWorkload("verify_bf16_r64_h32_d128_l8_rec7", 64, 32, 32, 128, 1
 VARLEN_128K = TrainWorkload("varlen_bf16_n32_t131072_h16_d128_l32", 1, 131072, 16, 16, 128, 128,
                             32, "bf16", 4, n_docs=32, doc_min=512, doc_max=8192)
 
-WORKLOADS = {w.name: w for w in (TINY_F32, TRAIN_4K, GVA_16K, SERVE_64, VARLEN_128K)}
+# The GDN layer's ShortConv at the 16-head, d = 128 shape (channels 3 x 16 x 128): 4096
+# clean + 4096 noisy rows, width 4, silu
+CONV_4K = ConvWorkload("shortconv_bf16_b1_t4096_d6144_w4_l32", 1, 4096, 6144, 4, 32, 1, "bf16", 6)
+CONV_TRAIN = ConvWorkload("shortconv_bf16_b4_t4096_d6144_w4_l32", 4, 4096, 6144, 4, 32, 1, "bf16", 7)
+
+WORKLOADS = {w.name: w for w in (TINY_F32, TRAIN_4K, GVA_16K, SERVE_64, VARLEN_128K, CONV_4K, CONV_TRAIN)}
 
 _TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32}
 
@@ -185,3 +206,24 @@ def make_state_pool(n_slots, h_v, d_k, d_v, seed, sigma=0.3):
     rng = np.random.default_rng(seed)
     x = rng.standard_normal((n_slots, h_v, d_k, d_v), dtype=np.float32) * np.float32(sigma)
     return torch.from_numpy(x)
+
+
+def draw_conv(rng, batch, seqlen, channels, width, dtype, bias=True):
+    """ShortConv inputs: x, xn, dy, dyn ~ N(0, 1) of shape [batch, seqlen, channels]
+    rounded to ``dtype``; w [channels, width] and bias [channels] ~ U(-1/sqrt(width),
+    1/sqrt(width)) (a depthwise filter's default fan-in scaling), fp32."""
+    fdt = np.float64 if dtype == "f32" else np.float32
+    tdt = torch_dtype(dtype)
+    out = {}
+    for key in ("x", "xn", "dy", "dyn"):
+        a = rng.standard_normal((batch, seqlen, channels), dtype=fdt)
+        out[key] = torch.from_numpy(a).to(tdt)
+    bound = 1.0 / np.sqrt(width)
+    out["w"] = torch.from_numpy(rng.uniform(-bound, bound, (channels, width)).astype(np.float32))
+    out["bias"] = torch.from_numpy(rng.uniform(-bound, bound, channels).astype(np.float32)) if bias else None
+    return out
+
+
+def make_conv(w: ConvWorkload, seed: int | None = None):
+    rng = np.random.default_rng(w.seed if seed is None else seed)
+    return draw_conv(rng, w.batch, w.seqlen, w.channels, w.width, w.dtype)

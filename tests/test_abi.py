@@ -189,3 +189,64 @@ def test_verify_state_cache_validation():
     assert _accept(accept=None) == bd.BDGDN_ERR_INVALID_ARG
     assert _accept(h_v=5) == bd.BDGDN_ERR_INVALID_ARG
     assert _accept(num_req=0) == bd.BDGDN_OK
+
+
+def _conv(fn="fwd", cu_dev=None, cu_host=None, null_x=False, ws=None, ws_bytes=0, **kw):
+    d = dict(batch=2, seqlen=64, num_seqs=0, channels=256, width=4, block=8, activation=bd.BDGDN_ACT_SILU,
+             dtype=bd.BDGDN_BF16)
+    d.update(kw)
+    desc = bd.ConvDesc(**d)
+    lib = bd.load_library()
+    P = FAKE
+    x = None if null_x else P
+    if fn == "fwd":
+        return lib.bdgdn_shortconv_fwd(ctypes.byref(desc), x, P, P, None, cu_dev, cu_host, P, P, None)
+    return lib.bdgdn_shortconv_bwd(ctypes.byref(desc), x, P, P, None, P, P, cu_dev, cu_host, P, P, P, None,
+                                   ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("fn", ["fwd", "bwd"])
+@pytest.mark.parametrize("kw,status", [
+    (dict(width=0), bd.BDGDN_ERR_UNSUPPORTED),
+    (dict(width=5), bd.BDGDN_ERR_UNSUPPORTED),
+    (dict(channels=258), bd.BDGDN_ERR_UNSUPPORTED),          # bf16 needs multiples of 4
+    (dict(channels=0), bd.BDGDN_ERR_INVALID_ARG),
+    (dict(block=0), bd.BDGDN_ERR_INVALID_ARG),
+    (dict(batch=0), bd.BDGDN_ERR_INVALID_ARG),
+    (dict(activation=2), bd.BDGDN_ERR_INVALID_ARG),
+    (dict(dtype=7), bd.BDGDN_ERR_UNSUPPORTED),
+    (dict(null_x=True), bd.BDGDN_ERR_INVALID_ARG),
+])
+def test_shortconv_rejects_bad_descriptors(fn, kw, status):
+    assert _conv(fn, **kw) == status
+
+
+def test_shortconv_fp32_channel_rule_and_packing():
+    assert _conv(dtype=bd.BDGDN_F32, channels=258, null_x=True) == bd.BDGDN_ERR_INVALID_ARG  # 258 is fine
+    cu = (ctypes.c_int32 * 4)(0, 10, 10, 64)
+    assert _conv(batch=1, num_seqs=3, cu_dev=FAKE, cu_host=None) == bd.BDGDN_ERR_INVALID_ARG
+    assert _conv(batch=2, num_seqs=3, cu_dev=FAKE, cu_host=cu) == bd.BDGDN_ERR_INVALID_ARG
+    bad = (ctypes.c_int32 * 4)(0, 20, 10, 64)                     # decreasing
+    assert _conv(batch=1, num_seqs=3, cu_dev=FAKE, cu_host=bad, null_x=True) == bd.BDGDN_ERR_INVALID_ARG
+    short = (ctypes.c_int32 * 4)(0, 10, 20, 60)                   # does not end at seqlen
+    assert _conv(batch=1, num_seqs=3, cu_dev=FAKE, cu_host=short) == bd.BDGDN_ERR_INVALID_ARG
+
+
+def test_shortconv_workspace():
+    lib = bd.load_library()
+
+    def ws(**kw):
+        d = dict(batch=2, seqlen=64, num_seqs=0, channels=256, width=4, block=8, activation=1, dtype=0)
+        d.update(kw)
+        return lib.bdgdn_shortconv_bwd_workspace(ctypes.byref(bd.ConvDesc(**d)))
+
+    # whole (width + 1) x channels fp32 partials, one per group of rows, growing with the rows
+    unit = 5 * 256 * 4
+    assert ws() > 0 and ws() % unit == 0
+    assert ws(seqlen=4096) % unit == 0 and ws(seqlen=4096) > ws()
+    assert ws(width=2) % (3 * 256 * 4) == 0
+    assert ws(seqlen=0) == 0
+    assert ws(width=9) == 0
+    assert _conv("bwd", ws=None, ws_bytes=0) == bd.BDGDN_ERR_WORKSPACE
+    assert _conv("bwd", ws=FAKE, ws_bytes=ws() - 4) == bd.BDGDN_ERR_WORKSPACE
+    assert _conv("bwd", ws=ctypes.c_void_p(0x1004), ws_bytes=ws()) == bd.BDGDN_ERR_WORKSPACE   # misaligned
