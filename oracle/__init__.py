@@ -16,6 +16,10 @@ to it.  Each entry point follows the paper (FLARE, arXiv 2606.01774):
   writes it (appendix "Differences between the denoise pass and the
   state-update pass").
 * ``commit``     -- token-causal state-update pass that writes the state back.
+* ``bwd_train``  -- gradients of the two-stream training forward (appendix
+  "Backward primitives": the per-step backward, eq. per-step-bwd; the noisy
+  block-end readout backward, eq. noisy-readout-bwd; the block-level chain rule,
+  eq. dh-block-recursion).
 """
 from __future__ import annotations
 
@@ -56,6 +60,8 @@ def _load():
         D = ctypes.c_double
         lib.oracle_fwd_train.argtypes = [I, I, I, P, I, I, I, I, I, D] + [P] * 14
         lib.oracle_fwd_train.restype = I
+        lib.oracle_bwd_train.argtypes = [I, I, I, P, I, I, I, I, I, D] + [P] * 25
+        lib.oracle_bwd_train.restype = I
         lib.oracle_denoise.argtypes = [I, I, I, I, I, I, D, P, P] + [P] * 6
         lib.oracle_denoise.restype = I
         lib.oracle_commit.argtypes = [I, I, I, I, I, I, D, P, P] + [P] * 6
@@ -124,6 +130,42 @@ def fwd_train(q, k, v, g, beta, qn, kn, vn, gn, betan, *, block, scale,
     if rc != 0:
         raise RuntimeError(f"oracle_fwd_train failed: {rc}")
     return o, on, ht
+
+
+def bwd_train(q, k, v, g, beta, qn, kn, vn, gn, betan, do, don, *, block, scale,
+              cu_seqlens=None, h0=None, dht=None, want_dh0=True):
+    """Gradients of  sum(do * o) + sum(don * on) + sum(dht * ht)  for fwd_train's inputs.
+
+    Same shapes as fwd_train; do, don like v; dht like ht (or None for zero).  Returns a
+    dict with dq, dk, dv, dg, dbeta (clean), dqn, dkn, dvn, dgn, dbetan (noisy) and dh0
+    ([B or N, Hv, dk, dv], or None), all fp64.  dq, dk of a q/k head sum over its v-heads.
+    """
+    q, k, v, g, beta = map(_f64, (q, k, v, g, beta))
+    qn, kn, vn, gn, betan = map(_f64, (qn, kn, vn, gn, betan))
+    do, don = _f64(do), _f64(don)
+    B, T, Hqk, dk = q.shape
+    Hv, dv = v.shape[2], v.shape[3]
+    cu = None
+    nseq = B
+    if cu_seqlens is not None:
+        cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+        nseq = cu.shape[0] - 1
+        assert B == 1 and int(cu[-1]) <= T
+    h0a, dhta = _f64(h0), _f64(dht)
+    out = {name: np.zeros(ref.shape) for name, ref in
+           (("dq", q), ("dk", k), ("dv", v), ("dg", g), ("dbeta", beta),
+            ("dqn", qn), ("dkn", kn), ("dvn", vn), ("dgn", gn), ("dbetan", betan))}
+    out["dh0"] = np.zeros((nseq, Hv, dk, dv)) if want_dh0 else None
+    rc = _load().oracle_bwd_train(
+        B, T, nseq, _ptr(cu), Hqk, Hv, dk, dv, int(block), float(scale),
+        _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+        _ptr(qn), _ptr(kn), _ptr(vn), _ptr(gn), _ptr(betan),
+        _ptr(h0a), _ptr(do), _ptr(don), _ptr(dhta),
+        *[_ptr(out[n]) for n in ("dq", "dk", "dv", "dg", "dbeta", "dqn", "dkn", "dvn", "dgn", "dbetan")],
+        _ptr(out["dh0"]))
+    if rc != 0:
+        raise RuntimeError(f"oracle_bwd_train failed: {rc}")
+    return out
 
 
 def denoise(pool, q, k, v, g, beta, *, scale, slot=None):

@@ -26,6 +26,12 @@
  *     (Appendix "Serving-system machinery", cache-and-scatter).
  *   - the two-stream 1D causal ShortConv feeding the GDR, forward and backward
  *     (Appendix "ShortConv under two-stream training").
+ *   - the backward of the two-stream training forward (Appendix "Backward primitives":
+ *     the per-step backward, eq. per-step-bwd, applied token by token in reverse; the
+ *     noisy block's block-end readout, eq. noisy-readout-bwd, followed by its reverse sweep
+ *     with zero per-step output gradient; and the block-level chain rule,
+ *     eq. dh-block-recursion: the gradient at a noisy block's seed is added to the clean
+ *     state gradient at the end of the previous block).
  *
  * Layouts (row = token index in the flattened [B*T] or packed token axis):
  *   q,k  [row][h_qk][d_k]    v,o [row][h_v][d_v]    g,beta [row][h_v]
@@ -163,6 +169,230 @@ int oracle_fwd_train(int B, int T, int n_seqs, const int32_t *cu,
             }
         }
         free(S); free(Sn); free(u);
+    }
+    return err;
+}
+
+/*
+ * Forward of one block from state S_in over rows [p0, p1) (clean or noisy inputs),
+ * keeping what the per-step backward needs: Sst[i] = the state after step i (Sst[-1] is
+ * S_in, passed separately), Spre[i] = exp(g) times the state before step i, uu[i] = the
+ * prediction error v - S_pre^T k (before the step size).
+ */
+static void block_states(const dims_t *d, long p0, long p1, int h, const double *S_in,
+                         const double *k, const double *v, const double *g, const double *beta,
+                         double *Spre, double *Sst, double *uu)
+{
+    const size_t ssz = (size_t)d->dk * d->dv;
+    for (long t = p0; t < p1; ++t) {
+        const long i = t - p0;
+        const double *prev = i == 0 ? S_in : Sst + (i - 1) * ssz;
+        const double alpha = exp(gate_at(g, d, t, h)), b = gate_at(beta, d, t, h);
+        const double *kt = row_qk(k, d, t, h), *vt = row_v(v, d, t, h);
+        double *sp = Spre + i * ssz, *st = Sst + i * ssz, *ut = uu + i * d->dv;
+        for (size_t e = 0; e < ssz; ++e) sp[e] = alpha * prev[e];
+        for (int j = 0; j < d->dv; ++j) {
+            double acc = 0.0;
+            for (int a = 0; a < d->dk; ++a) acc += sp[a * d->dv + j] * kt[a];
+            ut[j] = vt[j] - acc;
+        }
+        for (int a = 0; a < d->dk; ++a)
+            for (int j = 0; j < d->dv; ++j) st[a * d->dv + j] = sp[a * d->dv + j] + kt[a] * b * ut[j];
+    }
+}
+
+/*
+ * Eq. per-step-bwd for one token: dS holds dL/dS_t on entry and dL/dS_(t-1) on exit.
+ * do_ may be NULL (a noisy step: its output gradient entered through the block-end
+ * readout).  Gradients are added into dq, dk (d_k vectors), dv (d_v) and *dg, *db.
+ */
+static void per_step_bwd(const dims_t *d, double *dS, const double *do_, const double *q, const double *k,
+                         double g, double beta, const double *Spre, const double *St, const double *u,
+                         double *dq, double *dk, double *dv, double *dg, double *db, double *ddelta)
+{
+    const int dkk = d->dk, dvv = d->dv;
+    if (do_) {
+        for (int a = 0; a < dkk; ++a) {              /* dq = s S_t do */
+            double acc = 0.0;
+            for (int j = 0; j < dvv; ++j) acc += St[a * dvv + j] * do_[j];
+            dq[a] += d->scale * acc;
+        }
+        for (int a = 0; a < dkk; ++a)                /* dS_t += s q do^T */
+            for (int j = 0; j < dvv; ++j) dS[a * dvv + j] += d->scale * q[a] * do_[j];
+    }
+    for (int j = 0; j < dvv; ++j) {                  /* d delta = dS_t^T k */
+        double acc = 0.0;
+        for (int a = 0; a < dkk; ++a) acc += dS[a * dvv + j] * k[a];
+        ddelta[j] = acc;
+    }
+    for (int a = 0; a < dkk; ++a) {                  /* dk_write = dS_t delta, delta = beta u */
+        double acc = 0.0;
+        for (int j = 0; j < dvv; ++j) acc += dS[a * dvv + j] * beta * u[j];
+        dk[a] += acc;
+    }
+    double dbeta = 0.0;
+    for (int j = 0; j < dvv; ++j) {                  /* du = beta d delta; dv = du; dbeta = d delta . u */
+        dbeta += ddelta[j] * u[j];
+        ddelta[j] *= beta;                           /* ddelta now holds du */
+        dv[j] += ddelta[j];
+    }
+    *db += dbeta;
+    for (int a = 0; a < dkk; ++a) {                  /* dk_pred = -S_pre du */
+        double acc = 0.0;
+        for (int j = 0; j < dvv; ++j) acc += Spre[a * dvv + j] * ddelta[j];
+        dk[a] -= acc;
+    }
+    double dgate = 0.0;
+    const double alpha = exp(g);
+    for (int a = 0; a < dkk; ++a)                    /* dS_pre = dS_t - k du^T; dg = <dS_pre, S_pre> */
+        for (int j = 0; j < dvv; ++j) {
+            const double dsp = dS[a * dvv + j] - k[a] * ddelta[j];
+            dgate += dsp * Spre[a * dvv + j];
+            dS[a * dvv + j] = alpha * dsp;           /* dS_(t-1) = exp(g) dS_pre */
+        }
+    *dg += dgate;
+}
+
+typedef struct {
+    double *dq, *dk, *dv, *dg, *db;
+} grads_t;
+
+static double *grow_qk(double *base, const dims_t *d, long row, int h)
+{
+    return base + ((size_t)row * d->h_qk + h / (d->h_v / d->h_qk)) * d->dk;
+}
+
+/*
+ * Backward of two_stream_unit over rows [r0, r1), one v-head.  dS holds dL/d(final clean
+ * state) on entry (dht or zero) and dL/d(initial state) on exit (dh0).  ck: clean states
+ * before every block (filled here by a forward pass from S_init).
+ */
+static void two_stream_unit_bwd(const dims_t *d, int L, long r0, long r1, int h, const double *S_init,
+                                const double *q, const double *k, const double *v, const double *g,
+                                const double *beta, const double *qn, const double *kn, const double *vn,
+                                const double *gn, const double *betan, const double *do_, const double *don,
+                                grads_t gc, grads_t gnz, double *dS, double *ck, double *Spre, double *Sst,
+                                double *uu, double *dSn, double *tmp)
+{
+    const size_t ssz = (size_t)d->dk * d->dv;
+    const long nblk = (r1 - r0 + L - 1) / L;
+    /* checkpoints: the clean state before each block */
+    memcpy(ck, S_init, ssz * sizeof(double));
+    for (long b = 0; b + 1 < nblk; ++b) {
+        const long p0 = r0 + b * L, p1 = p0 + L;
+        block_states(d, p0, p1, h, ck + b * ssz, k, v, g, beta, Spre, Sst, uu);
+        memcpy(ck + (b + 1) * ssz, Sst + (p1 - p0 - 1) * ssz, ssz * sizeof(double));
+    }
+    for (long b = nblk - 1; b >= 0; --b) {
+        const long p0 = r0 + b * L, p1 = p0 + L < r1 ? p0 + L : r1;
+        const double *seed = ck + b * ssz;
+        /* clean block, tokens in reverse */
+        block_states(d, p0, p1, h, seed, k, v, g, beta, Spre, Sst, uu);
+        for (long t = p1 - 1; t >= p0; --t) {
+            const long i = t - p0;
+            per_step_bwd(d, dS, row_v(do_, d, t, h), row_qk(q, d, t, h), row_qk(k, d, t, h), gate_at(g, d, t, h),
+                         gate_at(beta, d, t, h), Spre + i * ssz, Sst + i * ssz, uu + i * d->dv,
+                         grow_qk(gc.dq, d, t, h), grow_qk(gc.dk, d, t, h), gc.dv + ((size_t)t * d->h_v + h) * d->dv,
+                         gc.dg + (size_t)t * d->h_v + h, gc.db + (size_t)t * d->h_v + h, tmp);
+        }
+        /* noisy block b from the same seed: block-end readout, then the reverse sweep */
+        block_states(d, p0, p1, h, seed, kn, vn, gn, betan, Spre, Sst, uu);
+        const double *Send = Sst + (p1 - p0 - 1) * ssz;
+        memset(dSn, 0, ssz * sizeof(double));
+        for (long l = p0; l < p1; ++l) {
+            const double *ql = row_qk(qn, d, l, h), *dol = row_v(don, d, l, h);
+            double *dql = grow_qk(gnz.dq, d, l, h);
+            for (int a = 0; a < d->dk; ++a) {
+                double acc = 0.0;
+                for (int j = 0; j < d->dv; ++j) {
+                    acc += Send[a * d->dv + j] * dol[j];             /* dq~ = s S~_end do~ */
+                    dSn[a * d->dv + j] += d->scale * ql[a] * dol[j]; /* dS~_end = s sum q~ do~^T */
+                }
+                dql[a] += d->scale * acc;
+            }
+        }
+        for (long l = p1 - 1; l >= p0; --l) {
+            const long i = l - p0;
+            per_step_bwd(d, dSn, NULL, NULL, row_qk(kn, d, l, h), gate_at(gn, d, l, h), gate_at(betan, d, l, h),
+                         Spre + i * ssz, Sst + i * ssz, uu + i * d->dv, NULL, grow_qk(gnz.dk, d, l, h),
+                         gnz.dv + ((size_t)l * d->h_v + h) * d->dv, gnz.dg + (size_t)l * d->h_v + h,
+                         gnz.db + (size_t)l * d->h_v + h, tmp);
+        }
+        /* eq. dh-block-recursion: the seed is the clean state at the end of block b - 1 */
+        for (size_t e = 0; e < ssz; ++e) dS[e] += dSn[e];
+    }
+}
+
+/*
+ * oracle_bwd_train: gradients of  sum <do, o> + sum <don, on> + <dht, ht>  with respect to
+ * every input of oracle_fwd_train (same layouts; dq, dk, dqn, dkn per q/k head summed over
+ * its v-heads).  dht and dh0 may be NULL (zero / not wanted); h0 NULL means zero.
+ * Work is split over (sequence, q/k head) units so that grouped v-heads accumulate into
+ * their q/k head's gradients in one thread.
+ */
+int oracle_bwd_train(int B, int T, int n_seqs, const int32_t *cu,
+                     int h_qk, int h_v, int dk, int dv, int L, double scale,
+                     const double *q, const double *k, const double *v, const double *g, const double *beta,
+                     const double *qn, const double *kn, const double *vn, const double *gn, const double *betan,
+                     const double *h0, const double *do_, const double *don, const double *dht,
+                     double *dq, double *dkk, double *dvv, double *dg, double *db,
+                     double *dqn, double *dkn, double *dvn, double *dgn, double *dbn, double *dh0)
+{
+    if (L < 1 || h_qk < 1 || h_v < 1 || h_v % h_qk || dk < 1 || dv < 1) return -1;
+    dims_t d = {h_qk, h_v, dk, dv, scale};
+    const int nseq = cu ? n_seqs : B;
+    const long rows = cu ? cu[n_seqs] : (long)B * T;
+    const size_t ssz = (size_t)dk * dv;
+    long maxlen = 0;
+    for (int n = 0; n < nseq; ++n) {
+        const long len = cu ? cu[n + 1] - cu[n] : T;
+        if (len > maxlen) maxlen = len;
+    }
+    const long maxblk = (maxlen + L - 1) / L + 1;
+    memset(dq, 0, (size_t)rows * h_qk * dk * sizeof(double));
+    memset(dkk, 0, (size_t)rows * h_qk * dk * sizeof(double));
+    memset(dvv, 0, (size_t)rows * h_v * dv * sizeof(double));
+    memset(dg, 0, (size_t)rows * h_v * sizeof(double));
+    memset(db, 0, (size_t)rows * h_v * sizeof(double));
+    memset(dqn, 0, (size_t)rows * h_qk * dk * sizeof(double));
+    memset(dkn, 0, (size_t)rows * h_qk * dk * sizeof(double));
+    memset(dvn, 0, (size_t)rows * h_v * dv * sizeof(double));
+    memset(dgn, 0, (size_t)rows * h_v * sizeof(double));
+    memset(dbn, 0, (size_t)rows * h_v * sizeof(double));
+    const grads_t gc = {dq, dkk, dvv, dg, db}, gz = {dqn, dkn, dvn, dgn, dbn};
+    const long nunits = (long)nseq * h_qk;
+    const int group = h_v / h_qk;
+    int err = 0;
+#pragma omp parallel
+    {
+        double *S0 = malloc(ssz * sizeof(double)), *dS = malloc(ssz * sizeof(double));
+        double *ck = malloc(maxblk * ssz * sizeof(double));
+        double *Spre = malloc((size_t)L * ssz * sizeof(double)), *Sst = malloc((size_t)L * ssz * sizeof(double));
+        double *uu = malloc((size_t)L * dv * sizeof(double)), *dSn = malloc(ssz * sizeof(double));
+        double *tmp = malloc((size_t)dv * sizeof(double));
+        const int ok = S0 && dS && ck && Spre && Sst && uu && dSn && tmp;
+        if (!ok) {
+#pragma omp atomic write
+            err = -2;
+        }
+#pragma omp for schedule(dynamic, 1)
+        for (long unit = 0; unit < nunits; ++unit) {
+            if (!ok) continue;
+            const int n = (int)(unit / h_qk), hq = (int)(unit % h_qk);
+            const long r0 = cu ? cu[n] : (long)n * T, r1 = cu ? cu[n + 1] : (long)n * T + T;
+            for (int h = hq * group; h < (hq + 1) * group; ++h) {
+                const size_t so = ((size_t)n * h_v + h) * ssz;
+                if (h0) memcpy(S0, h0 + so, ssz * sizeof(double));
+                else memset(S0, 0, ssz * sizeof(double));
+                if (dht) memcpy(dS, dht + so, ssz * sizeof(double));
+                else memset(dS, 0, ssz * sizeof(double));
+                if (r1 > r0)
+                    two_stream_unit_bwd(&d, L, r0, r1, h, S0, q, k, v, g, beta, qn, kn, vn, gn, betan, do_, don,
+                                        gc, gz, dS, ck, Spre, Sst, uu, dSn, tmp);
+                if (dh0) memcpy(dh0 + so, dS, ssz * sizeof(double));
+            }
+        }
+        free(S0); free(dS); free(ck); free(Spre); free(Sst); free(uu); free(dSn); free(tmp);
     }
     return err;
 }

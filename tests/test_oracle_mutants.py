@@ -75,6 +75,17 @@ MUTANTS = {
     "conv_silu_grad": ("return sg * (1.0 + p * (1.0 - sg));", "return sg;"),
     "conv_dw_misses_noisy": ("                        dw[c * W + i] += gn * xn[src * D + c];",
                              "                        dw[c * W + i] += 0.0 * gn * xn[src * D + c];"),
+    "bwd_drops_prediction_term": ("dk[a] -= acc;", "dk[a] -= 0.0 * acc;"),
+    "bwd_gate_grad_previous_state": ("dgate += dsp * Spre[a * dvv + j];",
+                                     "dgate += dsp * Spre[a * dvv + j] / alpha;"),
+    "bwd_carry_without_gate": ("dS[a * dvv + j] = alpha * dsp;", "dS[a * dvv + j] = dsp;"),
+    "bwd_no_noisy_injection": ("for (size_t e = 0; e < ssz; ++e) dS[e] += dSn[e];", ";"),
+    "bwd_noisy_reads_first_state": ("const double *Send = Sst + (p1 - p0 - 1) * ssz;",
+                                    "const double *Send = Sst;"),
+    "bwd_drops_step_size_grad": ("*db += dbeta;", "*db += 0.0 * dbeta;"),
+    "bwd_write_without_step_size": ("acc += dS[a * dvv + j] * beta * u[j];", "acc += dS[a * dvv + j] * u[j];"),
+    "bwd_seed_of_previous_block": ("const double *seed = ck + b * ssz;",
+                                   "const double *seed = ck + (b > 0 ? b - 1 : 0) * ssz;"),
     "commit_skips_last_token": ("for (long t = (long)r * L; t < (long)r * L + L; ++t) {",
                                 "for (long t = (long)r * L; t < (long)r * L + L - 1; ++t) {"),
 }

@@ -523,3 +523,111 @@ def test_pin_shortconv_backward_is_gradient(act):
             lo[name][idx] -= h
             fd[idx] = (loss(hi["x"], hi["xn"], hi["w"], hi["b"]) - loss(lo["x"], lo["xn"], lo["w"], lo["b"])) / (2 * h)
         np.testing.assert_allclose(grad, fd, rtol=1e-6, atol=1e-7, err_msg=name)
+
+
+# ---------------------------------------------------------------------------
+# Backward of the two-stream forward (appendix "Backward primitives"): the gradient is
+# pinned to central finite differences of the forward oracle (itself pinned above), and
+# to closed forms where the recurrence degenerates.
+# ---------------------------------------------------------------------------
+_BWD_KEYS = ("q", "k", "v", "g", "beta")
+
+
+def _bwd_setup(rng, B, T, hqk, hv, d, L, lengths=None):
+    c, n = _two(rng, B, T, hqk, hv, d, d)
+    for s in (c, n):   # milder gates so that finite differences see every term
+        s["g"] = -np.log1p(np.exp(rng.uniform(-3, 0, s["g"].shape)))
+    nseq = B if lengths is None else len(lengths)
+    h0 = 0.3 * rng.standard_normal((nseq, hv, d, d))
+    do = rng.standard_normal((B, T, hv, d))
+    don = rng.standard_normal((B, T, hv, d))
+    dht = rng.standard_normal((nseq, hv, d, d))
+    cu = None if lengths is None else np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+    return c, n, h0, do, don, dht, cu
+
+
+def _bwd_loss(c, n, L, scale, h0, do, don, dht, cu):
+    o, on, ht = _run(c, n, L, scale, h0=h0, cu_seqlens=cu)
+    return float((o * do).sum() + (on * don).sum() + (ht * dht).sum())
+
+
+@pytest.mark.parametrize("B,T,hqk,hv,d,L,lengths", [
+    (2, 11, 1, 2, 3, 4, None),        # grouped value heads, ragged tail block
+    (1, 13, 2, 2, 3, 4, [8, 5]),      # two packed documents, a partial last block
+    (1, 7, 1, 1, 4, 1, None),         # one-position blocks
+])
+def test_pin_bwd_matches_finite_differences(B, T, hqk, hv, d, L, lengths):
+    rng = np.random.default_rng(40 + T + L)
+    c, n, h0, do, don, dht, cu = _bwd_setup(rng, B, T, hqk, hv, d, L, lengths)
+    scale = 0.7
+    gr = oracle.bwd_train(c["q"], c["k"], c["v"], c["g"], c["beta"], n["q"], n["k"], n["v"], n["g"], n["beta"],
+                          do, don, block=L, scale=scale, h0=h0, dht=dht, cu_seqlens=cu)
+    eps = 1e-6
+    targets = [(c[k_], "d" + k_) for k_ in _BWD_KEYS] + [(n[k_], "d" + k_ + "n") for k_ in _BWD_KEYS]
+    targets.append((h0, "dh0"))
+    for arr, name in targets:
+        fd = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            a0 = arr[idx]
+            arr[idx] = a0 + eps
+            lp = _bwd_loss(c, n, L, scale, h0, do, don, dht, cu)
+            arr[idx] = a0 - eps
+            lm = _bwd_loss(c, n, L, scale, h0, do, don, dht, cu)
+            arr[idx] = a0
+            fd[idx] = (lp - lm) / (2 * eps)
+        np.testing.assert_allclose(gr[name], fd, rtol=1e-6, atol=1e-7, err_msg=name)
+
+
+def test_pin_bwd_frozen_state_closed_form():
+    """beta = 0 in both streams: nothing is written, every state is the decayed h0, so
+    o_t = s e^(G_t) h0^T q_t with G_t the cumulative clean log-gate, and a noisy position of
+    block b reads s e^(G_(b-1) + G~_b) h0^T q~ (G~_b = the noisy block's total log-gate).
+    Then dq_t = s e^(G_t) h0 do_t, dk = dv = 0, and dh0 is the sum of the outer products."""
+    rng = np.random.default_rng(7)
+    B, T, hqk, hv, d, L = 1, 10, 1, 1, 3, 4
+    c, n, h0, do, don, dht, _ = _bwd_setup(rng, B, T, hqk, hv, d, L)
+    c["beta"][:] = 0.0
+    n["beta"][:] = 0.0
+    s = 0.5
+    gr = oracle.bwd_train(c["q"], c["k"], c["v"], c["g"], c["beta"], n["q"], n["k"], n["v"], n["g"], n["beta"],
+                          do, don, block=L, scale=s, h0=h0, dht=None)
+    G = np.cumsum(c["g"][0, :, 0])
+    H = h0[0, 0]
+    dq = np.zeros((T, d))
+    dqn = np.zeros((T, d))
+    dh0 = np.zeros((d, d))
+    for t in range(T):
+        dq[t] = s * np.exp(G[t]) * H @ do[0, t, 0]
+        dh0 += s * np.exp(G[t]) * np.outer(c["q"][0, t, 0], do[0, t, 0])
+    for p0 in range(0, T, L):
+        p1 = min(p0 + L, T)
+        gseed = G[p0 - 1] if p0 > 0 else 0.0
+        gend = gseed + n["g"][0, p0:p1, 0].sum()
+        for l in range(p0, p1):
+            dqn[l] = s * np.exp(gend) * H @ don[0, l, 0]
+            dh0 += s * np.exp(gend) * np.outer(n["q"][0, l, 0], don[0, l, 0])
+    np.testing.assert_allclose(gr["dq"][0, :, 0], dq, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(gr["dqn"][0, :, 0], dqn, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(gr["dh0"][0, 0], dh0, rtol=1e-12, atol=1e-14)
+    for key in ("dk", "dv", "dkn", "dvn"):
+        assert np.abs(gr[key]).max() == 0.0, key
+
+
+def test_pin_bwd_packed_equals_separate_documents():
+    """Packed documents back-propagate exactly as separate sequences (states and their
+    gradients reset at every document start)."""
+    rng = np.random.default_rng(11)
+    L, d = 4, 3
+    lengths = [8, 5]
+    c, n, h0, do, don, dht, cu = _bwd_setup(rng, 1, 13, 1, 1, d, L, lengths)
+    gp = oracle.bwd_train(c["q"], c["k"], c["v"], c["g"], c["beta"], n["q"], n["k"], n["v"], n["g"], n["beta"],
+                          do, don, block=L, scale=1.0, h0=h0, dht=dht, cu_seqlens=cu)
+    for j, (a, e) in enumerate(zip(cu[:-1], cu[1:])):
+        sl = lambda x: x[:, a:e]
+        cs = {k_: sl(v_) for k_, v_ in c.items()}
+        ns = {k_: sl(v_) for k_, v_ in n.items()}
+        gs = oracle.bwd_train(cs["q"], cs["k"], cs["v"], cs["g"], cs["beta"], ns["q"], ns["k"], ns["v"], ns["g"],
+                              ns["beta"], sl(do), sl(don), block=L, scale=1.0, h0=h0[j:j + 1], dht=dht[j:j + 1])
+        for key in ("dq", "dk", "dv", "dg", "dbeta", "dqn", "dkn", "dvn", "dgn", "dbetan"):
+            np.testing.assert_array_equal(gp[key][:, a:e], gs[key], err_msg=key)
+        np.testing.assert_array_equal(gp["dh0"][j], gs["dh0"][0])
