@@ -243,12 +243,12 @@ static void per_step_bwd(const dims_t *d, double *dS, const double *do_, const d
         dk[a] -= acc;
     }
     double dgate = 0.0;
-    const double alpha = exp(g);
+    const double decay = exp(g);
     for (int a = 0; a < dkk; ++a)                    /* dS_pre = dS_t - k du^T; dg = <dS_pre, S_pre> */
         for (int j = 0; j < dvv; ++j) {
             const double dsp = dS[a * dvv + j] - k[a] * ddelta[j];
             dgate += dsp * Spre[a * dvv + j];
-            dS[a * dvv + j] = alpha * dsp;           /* dS_(t-1) = exp(g) dS_pre */
+            dS[a * dvv + j] = decay * dsp;           /* dS_(t-1) = exp(g) dS_pre */
         }
     *dg += dgate;
 }

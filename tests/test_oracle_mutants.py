@@ -77,8 +77,8 @@ MUTANTS = {
                              "                        dw[c * W + i] += 0.0 * gn * xn[src * D + c];"),
     "bwd_drops_prediction_term": ("dk[a] -= acc;", "dk[a] -= 0.0 * acc;"),
     "bwd_gate_grad_previous_state": ("dgate += dsp * Spre[a * dvv + j];",
-                                     "dgate += dsp * Spre[a * dvv + j] / alpha;"),
-    "bwd_carry_without_gate": ("dS[a * dvv + j] = alpha * dsp;", "dS[a * dvv + j] = dsp;"),
+                                     "dgate += dsp * Spre[a * dvv + j] / decay;"),
+    "bwd_carry_without_gate": ("dS[a * dvv + j] = decay * dsp;", "dS[a * dvv + j] = dsp;"),
     "bwd_no_noisy_injection": ("for (size_t e = 0; e < ssz; ++e) dS[e] += dSn[e];", ";"),
     "bwd_noisy_reads_first_state": ("const double *Send = Sst + (p1 - p0 - 1) * ssz;",
                                     "const double *Send = Sst;"),
