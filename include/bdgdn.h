@@ -166,6 +166,43 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc,
                     const float *h0, void *o, void *on, float *ht,
                     void *workspace, size_t workspace_bytes, void *stream);
 
+/* Bytes of device workspace bdgdn_bwd_train needs: the clean seed state of every
+ * (block, v-head) in fp32 plus scratch for the recomputed clean outputs; 0 for a
+ * descriptor it would reject. */
+size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
+
+/*
+ * Backward of bdgdn_fwd_train (Appendix "Backward primitives": the noisy block-end
+ * readout backward, eq. noisy-readout-bwd; the block-level chain rule,
+ * eq. dh-block-recursion; the clean chunk backward): the gradients of
+ *     sum <do, o> + sum <don, on> + <dht, ht>
+ * with respect to every input of the forward, for the same descriptor and inputs
+ * (desc->route is not used; desc->out_dtype is the dtype of do and don).
+ *
+ *   do, don              [B*T][h_v][d_v] upstream gradients of o and on (out_dtype)
+ *   dht                  [B or N][h_v][d_k][d_v] fp32 gradient of ht, or NULL for zero
+ *   dq, dk, dqn, dkn     [B*T][h_qk][d_k] fp32 (summed over the v-heads of a q/k head)
+ *   dv, dvn              [B*T][h_v][d_v] fp32
+ *   dg, dbeta, dgn, dbetan  [B*T][h_v] fp32 (gradients of the log-gates and step sizes)
+ *   dh0                  [B or N][h_v][d_k][d_v] fp32 gradient of h0, or NULL
+ *   workspace            at least bdgdn_bwd_train_workspace(desc) bytes, 256-byte aligned,
+ *                        owned by the call until the stream passes it
+ * Every gradient row is overwritten.  Available for bf16 inputs with d_k = d_v = 128 and
+ * blocks of at most 32 positions (else BDGDN_ERR_UNSUPPORTED).  With grouped value heads
+ * (h_v > h_qk) dq, dk, dqn, dkn are summed with floating-point atomics (summation order
+ * not fixed); otherwise every result is deterministic.
+ */
+int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc,
+                    const void *q, const void *k, const void *v,
+                    const float *g, const float *beta,
+                    const void *qn, const void *kn, const void *vn,
+                    const float *gn, const float *betan,
+                    const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                    const float *h0, const void *do_, const void *don, const float *dht,
+                    float *dq, float *dk, float *dv, float *dg, float *dbeta,
+                    float *dqn, float *dkn, float *dvn, float *dgn, float *dbetan, float *dh0,
+                    void *workspace, size_t workspace_bytes, void *stream);
+
 /*
  * One Diffusion-Trust denoise pass over R blocks (Appendix "Per-block denoise loop",
  * "Differences between the denoise pass and the state-update pass").  Request r's

@@ -24,6 +24,7 @@ __all__ = [
     "bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace", "bdgdn_fwd_train",
     "bdgdn_commit_record", "bdgdn_accept_states", "BDGDN_ACT_NONE", "BDGDN_ACT_SILU",
     "bdgdn_shortconv_fwd", "bdgdn_shortconv_bwd_workspace", "bdgdn_shortconv_bwd",
+    "bdgdn_bwd_train_workspace", "bdgdn_bwd_train",
     "bdgdn_denoise_step", "bdgdn_commit", "library_path", "load_library", "EXPORTED_SYMBOLS",
 ]
 
@@ -48,7 +49,7 @@ BDGDN_ACT_SILU = 1
 EXPORTED_SYMBOLS = ("bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace",
                     "bdgdn_fwd_train", "bdgdn_denoise_step", "bdgdn_commit", "bdgdn_commit_record",
                     "bdgdn_accept_states", "bdgdn_shortconv_fwd", "bdgdn_shortconv_bwd_workspace",
-                    "bdgdn_shortconv_bwd")
+                    "bdgdn_shortconv_bwd", "bdgdn_bwd_train_workspace", "bdgdn_bwd_train")
 
 
 class FwdDesc(ctypes.Structure):
@@ -111,6 +112,10 @@ def load_library():
     lib.bdgdn_commit_record.restype = ctypes.c_int
     lib.bdgdn_accept_states.argtypes = [ctypes.POINTER(ServeDesc), P, P, P, ctypes.c_int32, P, P]
     lib.bdgdn_accept_states.restype = ctypes.c_int
+    lib.bdgdn_bwd_train_workspace.argtypes = [ctypes.POINTER(FwdDesc)]
+    lib.bdgdn_bwd_train_workspace.restype = ctypes.c_size_t
+    lib.bdgdn_bwd_train.argtypes = [ctypes.POINTER(FwdDesc)] + [P] * 28 + [ctypes.c_size_t, P]
+    lib.bdgdn_bwd_train.restype = ctypes.c_int
     lib.bdgdn_shortconv_fwd.argtypes = [ctypes.POINTER(ConvDesc)] + [P] * 9
     lib.bdgdn_shortconv_fwd.restype = ctypes.c_int
     lib.bdgdn_shortconv_bwd_workspace.argtypes = [ctypes.POINTER(ConvDesc)]
@@ -230,6 +235,65 @@ def bdgdn_fwd_train(q, k, v, g, beta, qn, kn, vn, gn, betan, *, block, scale=Non
         _ptr(h0), _ptr(o), _ptr(on), _ptr(ht), _ptr(workspace), ws_size, _stream(stream))
     _check(st, "bdgdn_fwd_train")
     return o, on, ht
+
+
+def bdgdn_bwd_train_workspace(desc: FwdDesc) -> int:
+    return int(load_library().bdgdn_bwd_train_workspace(ctypes.byref(desc)))
+
+
+_BWD_NAMES = ("dq", "dk", "dv", "dg", "dbeta", "dqn", "dkn", "dvn", "dgn", "dbetan")
+
+
+def bdgdn_bwd_train(q, k, v, g, beta, qn, kn, vn, gn, betan, do, don, *, block, scale=None,
+                    cu_seqlens=None, cu_seqlens_host=None, h0=None, dht=None, want_dh0=False,
+                    grads=None, workspace=None, stream=None):
+    """Backward of bdgdn_fwd_train: gradients of sum(do*o) + sum(don*on) + sum(dht*ht).
+    Inputs as for bdgdn_fwd_train; do, don [B,T,h_v,d_v] in the forward's output dtype
+    (fp32 or bf16); dht like ht or None.  Returns a dict of fp32 tensors (dq, dk, dv, dg,
+    dbeta and the noisy dqn, ..., dbetan; dh0 when want_dh0).  ``grads`` may supply the
+    output tensors (same names)."""
+    lib = load_library()
+    dt = q.dtype
+    for name, t in (("q", q), ("k", k), ("v", v), ("qn", qn), ("kn", kn), ("vn", vn)):
+        _dev(t, name, dt)
+    for name, t in (("g", g), ("beta", beta), ("gn", gn), ("betan", betan)):
+        _dev(t, name, torch.float32)
+    _dev(do, "do")
+    _dev(don, "don", do.dtype)
+    num_seqs = 0
+    cu_h = None
+    if cu_seqlens is not None:
+        _dev(cu_seqlens, "cu_seqlens", torch.int32)
+        num_seqs = cu_seqlens.numel() - 1
+        if cu_seqlens_host is None:
+            cu_seqlens_host = cu_seqlens.cpu()
+        cu_h = torch.as_tensor(cu_seqlens_host, dtype=torch.int32).contiguous()
+    desc = make_fwd_desc(q, v, block=block, scale=scale, num_seqs=num_seqs, out_dtype=do.dtype)
+    out = {} if grads is None else dict(grads)
+    like = {"dq": q, "dk": k, "dv": v, "dg": g, "dbeta": beta, "dqn": qn, "dkn": kn, "dvn": vn, "dgn": gn,
+            "dbetan": betan}
+    for name in _BWD_NAMES:
+        if name not in out:
+            out[name] = torch.empty(like[name].shape, dtype=torch.float32, device=q.device)
+        _dev(out[name], name, torch.float32)
+    units = num_seqs if num_seqs else q.shape[0]
+    if want_dh0 and "dh0" not in out:
+        out["dh0"] = torch.empty(units, v.shape[2], q.shape[3], v.shape[3], dtype=torch.float32, device=q.device)
+    _dev(h0, "h0", torch.float32)
+    _dev(dht, "dht", torch.float32)
+    ws_bytes = bdgdn_bwd_train_workspace(desc)
+    if workspace is None and ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    ws_size = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.bdgdn_bwd_train(
+        ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+        _ptr(qn), _ptr(kn), _ptr(vn), _ptr(gn), _ptr(betan),
+        _ptr(cu_seqlens), None if cu_h is None else ctypes.c_void_p(cu_h.data_ptr()),
+        _ptr(h0), _ptr(do), _ptr(don), _ptr(dht),
+        *[_ptr(out[n]) for n in _BWD_NAMES], _ptr(out.get("dh0")),
+        _ptr(workspace), ws_size, _stream(stream))
+    _check(st, "bdgdn_bwd_train")
+    return out
 
 
 def _serve_desc(q, v, scale, out_dtype):

@@ -356,6 +356,100 @@ int bdgdn_accept_states(const bdgdn_serve_desc_t *desc, float *state_pool, const
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
 }
 
+// Backward workspace: the clean seed state of every (block, v-head) (fp32), then scratch
+// for the clean outputs the recomputing scan writes (bf16).
+static bool bwd_shape_ok(const bdgdn_fwd_desc_t *d)
+{
+    return d->dtype == BDGDN_BF16 && d->d_k == 128 && d->d_v == 128 && d->block <= 32;
+}
+
+static size_t bwd_seed_bytes(const bdgdn_fwd_desc_t *d)
+{
+    return ((size_t)total_blocks(d) * d->h_v * d->d_k * d->d_v * sizeof(float) + 255) & ~(size_t)255;
+}
+
+size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc)
+{
+    if (!desc || check_heads(desc->h_qk, desc->h_v, desc->d_k, desc->d_v, desc->block, desc->scale, desc->dtype,
+                             desc->out_dtype) != BDGDN_OK)
+        return 0;
+    if (desc->batch <= 0 || desc->seqlen <= 0 || !bwd_shape_ok(desc)) return 0;
+    const size_t rows = (size_t)desc->batch * desc->seqlen;
+    return bwd_seed_bytes(desc) + rows * desc->h_v * desc->d_v * 2;
+}
+
+int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, const void *v,
+                    const float *g, const float *beta, const void *qn, const void *kn,
+                    const void *vn, const float *gn, const float *betan,
+                    const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host, const float *h0,
+                    const void *dout, const void *doutn, const float *dht,
+                    float *dq, float *dk, float *dv, float *dg, float *dbeta,
+                    float *dqn, float *dkn, float *dvn, float *dgn, float *dbetan, float *dh0,
+                    void *workspace, size_t workspace_bytes, void *stream)
+{
+    int st = check_fwd(desc, cu_seqlens_dev, cu_seqlens_host);
+    if (st != BDGDN_OK) return st;
+    if (!bwd_shape_ok(desc)) return BDGDN_ERR_UNSUPPORTED;
+    if (!q || !k || !v || !g || !beta || !qn || !kn || !vn || !gn || !betan || !dout || !doutn || !dq ||
+        !dk || !dv || !dg || !dbeta || !dqn || !dkn || !dvn || !dgn || !dbetan)
+        return BDGDN_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(qn) || !aligned16(kn) ||
+        !aligned16(vn) || !aligned16(dout) || !aligned16(doutn) || !aligned16(h0) || !aligned16(dht))
+        return BDGDN_ERR_INVALID_ARG;
+    if (desc->seqlen == 0) return BDGDN_OK;
+    const size_t need = bdgdn_bwd_train_workspace(desc);
+    if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0)
+        return BDGDN_ERR_WORKSPACE;
+    const bool packed = desc->num_seqs > 0;
+    const int nseq = packed ? desc->num_seqs : desc->batch;
+    const hipStream_t strm = static_cast<hipStream_t>(stream);
+    unsigned char *ws = static_cast<unsigned char *>(workspace);
+    float *seeds = reinterpret_cast<float *>(ws);
+    // 1. the clean scan from h0, writing the seed state of every block
+    ScanArgs sa = {};
+    sa.q = q; sa.k = k; sa.v = v; sa.qn = qn; sa.kn = kn; sa.vn = vn;
+    sa.g = g; sa.beta = beta; sa.gn = gn; sa.betan = betan;
+    sa.cu = packed ? cu_seqlens_dev : nullptr;
+    sa.h0 = h0; sa.ht = nullptr;
+    sa.o = ws + bwd_seed_bytes(desc); sa.on = nullptr;
+    sa.ws = nullptr;
+    sa.bs = seeds;
+    sa.T = desc->seqlen; sa.L = desc->block; sa.nblk = (desc->seqlen + desc->block - 1) / desc->block;
+    sa.h_qk = desc->h_qk; sa.h_v = desc->h_v; sa.dv = desc->d_v;
+    sa.n_chains = nseq * desc->h_v;
+    sa.n_vt = desc->d_v / scan_tile_v();
+    sa.scale = desc->scale;
+    sa.n_order = 0;
+    if (packed && nseq <= kMaxOrder) {
+        std::vector<int> idx(nseq);
+        std::iota(idx.begin(), idx.end(), 0);
+        std::stable_sort(idx.begin(), idx.end(), [&](int x, int y) {
+            return cu_seqlens_host[x + 1] - cu_seqlens_host[x] > cu_seqlens_host[y + 1] - cu_seqlens_host[y];
+        });
+        for (int i = 0; i < nseq; ++i) sa.order[i] = idx[i];
+        sa.n_order = nseq;
+    }
+    hipError_t e = launch_scan_states(lp_of(desc->block), sa, strm);
+    if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
+    // 2. the reverse walk over the blocks of every (sequence, v-head)
+    BwdArgs a = {};
+    a.q = q; a.k = k; a.v = v; a.qn = qn; a.kn = kn; a.vn = vn;
+    a.g = g; a.beta = beta; a.gn = gn; a.betan = betan;
+    a.dout = dout; a.doutn = doutn;
+    a.seeds = seeds; a.dht = dht;
+    a.dq = dq; a.dk = dk; a.dv = dv; a.dg = dg; a.db = dbeta;
+    a.dqn = dqn; a.dkn = dkn; a.dvn = dvn; a.dgn = dgn; a.dbn = dbetan;
+    a.dh0 = dh0;
+    a.cu = sa.cu;
+    a.T = desc->seqlen; a.nblk = sa.nblk; a.L = desc->block;
+    a.h_qk = desc->h_qk; a.h_v = desc->h_v;
+    a.scale = desc->scale;
+    a.atomic_qk = desc->h_v != desc->h_qk;
+    const long rows = (long)desc->batch * desc->seqlen;
+    e = launch_bwd(desc->out_dtype == BDGDN_BF16, a, nseq * desc->h_v, rows * desc->h_qk * desc->d_k, strm);
+    return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+}
+
 size_t bdgdn_shortconv_bwd_workspace(const bdgdn_conv_desc_t *desc)
 {
     if (!desc || desc->batch <= 0 || desc->seqlen < 0 || desc->channels <= 0 || desc->width < 1 || desc->width > 4)

@@ -96,6 +96,23 @@ static hipError_t launch_split(const ScanArgs &sa, const NoisyArgs &na, hipStrea
     return hipGetLastError();
 }
 
+// The clean scan alone, writing the seed state of every block (the recomputation the
+// backward starts from); the clean outputs go to sa.o.
+hipError_t launch_scan_states(int lp, const ScanArgs &sa, hipStream_t s)
+{
+    if ((lp != 16 && lp != 32) || sa.n_vt * 32 != sa.dv || !sa.bs) return hipErrorInvalidValue;
+    auto run = [&](auto k2, int bytes) {
+        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void *>(k2),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+        if (err != hipSuccess) return err;
+        const int grid = (sa.n_chains + 7) / 8 * 8 * sa.n_vt;
+        hipLaunchKernelGGL(k2, dim3(grid), dim3(768), bytes, s, sa);
+        return hipGetLastError();
+    };
+    return lp == 16 ? run(bdgdn_k2_scan_states_kernel<__bf16, 16>, Fused<__bf16, 128, 16, true>::BYTES)
+                    : run(bdgdn_k2_scan_states_kernel<__bf16, 32>, Fused<__bf16, 128, 32, true>::BYTES);
+}
+
 bool split_supported(Types ty, int dk, int dv, int lp)
 {
     return ty != Types::F32 && dk == 128 && dv == 128 && (lp == 16 || lp == 32);

@@ -250,3 +250,29 @@ def test_shortconv_workspace():
     assert _conv("bwd", ws=None, ws_bytes=0) == bd.BDGDN_ERR_WORKSPACE
     assert _conv("bwd", ws=FAKE, ws_bytes=ws() - 4) == bd.BDGDN_ERR_WORKSPACE
     assert _conv("bwd", ws=ctypes.c_void_p(0x1004), ws_bytes=ws()) == bd.BDGDN_ERR_WORKSPACE   # misaligned
+
+
+def _bwd(desc, ws=None, ws_bytes=0, null_grad=False, **_):
+    lib = bd.load_library()
+    P = FAKE
+    grads = [P] * 10
+    if null_grad:
+        grads[3] = None
+    return lib.bdgdn_bwd_train(ctypes.byref(desc), P, P, P, P, P, P, P, P, P, P, None, None, None, P, P, None,
+                               *grads, None, ws, ws_bytes, None)
+
+
+def test_bwd_train_validation_and_workspace():
+    lib = bd.load_library()
+    ok = _desc()
+    need = lib.bdgdn_bwd_train_workspace(ctypes.byref(ok))
+    # fp32 seed states of every (block, v-head) + bf16 scratch for the clean outputs
+    assert need >= 2 * 4 * 128 * 128 * 4 + 64 * 4 * 128 * 2
+    assert lib.bdgdn_bwd_train_workspace(ctypes.byref(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32))) == 0
+    assert _bwd(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32)) == bd.BDGDN_ERR_UNSUPPORTED
+    assert _bwd(_desc(d_k=64, d_v=64)) == bd.BDGDN_ERR_UNSUPPORTED
+    assert _bwd(_desc(block=64)) == bd.BDGDN_ERR_UNSUPPORTED
+    assert _bwd(_desc(h_v=3)) == bd.BDGDN_ERR_INVALID_ARG
+    assert _bwd(ok, null_grad=True) == bd.BDGDN_ERR_INVALID_ARG
+    assert _bwd(ok, ws=None, ws_bytes=0) == bd.BDGDN_ERR_WORKSPACE
+    assert _bwd(ok, ws=FAKE, ws_bytes=need - 1) == bd.BDGDN_ERR_WORKSPACE

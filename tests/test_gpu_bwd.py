@@ -1,0 +1,95 @@
+"""GPU parity of the two-stream training backward (bdgdn_bwd_train) against the fp64
+oracle's backward, through the C ABI: every gradient tensor (clean and noisy q, k, v,
+log-gates, step sizes, and the initial state) within the bf16 tolerance of max |err| / RMS,
+over ragged tails, grouped value heads (atomically summed q/k gradients), packed documents,
+an initial state with a final-state gradient, and bf16 upstream gradients."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_01774_amd as bd
+from paper_2606_01774_amd import workloads as W
+from parity_utils import TOL, rel_err
+
+pytestmark = pytest.mark.gpu
+
+NAMES = ("dq", "dk", "dv", "dg", "dbeta", "dqn", "dkn", "dvn", "dgn", "dbetan")
+
+
+def _case(B, T, hqk, hv, L, seed, lengths=None, h0=False, dht=False, do_dtype=torch.float32):
+    inp = W.make_custom_train(B, T, hqk, hv, 128, 128, "bf16", seed=seed, lengths=lengths)
+    rng = np.random.default_rng(seed + 1)
+    nseq = B if lengths is None else len(lengths)
+    do = torch.from_numpy(rng.standard_normal((B, T, hv, 128)).astype(np.float32)).to(do_dtype)
+    don = torch.from_numpy(rng.standard_normal((B, T, hv, 128)).astype(np.float32)).to(do_dtype)
+    h0t = torch.from_numpy((0.3 * rng.standard_normal((nseq, hv, 128, 128))).astype(np.float32)) if h0 else None
+    dhtt = torch.from_numpy(rng.standard_normal((nseq, hv, 128, 128)).astype(np.float32)) if dht else None
+    cu = None
+    if lengths is not None:
+        cu = torch.tensor(np.concatenate([[0], np.cumsum(lengths)]), dtype=torch.int32)
+    return inp, do, don, h0t, dhtt, cu
+
+
+def _check(B, T, hqk, hv, L, seed, **kw):
+    inp, do, don, h0, dht, cu = _case(B, T, hqk, hv, L, seed, **kw)
+    print(f"bwd B={B} T={T} hqk={hqk} hv={hv} L={L} {kw}", flush=True)
+    scale = 1.0 / math.sqrt(128)
+    d = {k: v.cuda() for k, v in inp.items()}
+    got = bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
+                             d["betan"], do.cuda(), don.cuda(), block=L, scale=scale,
+                             cu_seqlens=None if cu is None else cu.cuda(), cu_seqlens_host=cu,
+                             h0=None if h0 is None else h0.cuda(), dht=None if dht is None else dht.cuda(),
+                             want_dh0=True)
+    torch.cuda.synchronize()
+    ref = oracle.bwd_train(inp["q"], inp["k"], inp["v"], inp["g"], inp["beta"], inp["qn"], inp["kn"], inp["vn"],
+                           inp["gn"], inp["betan"], do, don, block=L, scale=scale,
+                           cu_seqlens=None if cu is None else cu.numpy(), h0=h0, dht=dht)
+    errs = {}
+    for name in NAMES + ("dh0",):
+        errs[name] = rel_err(got[name], ref[name])
+    print("  " + " ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
+    for name, e in errs.items():
+        assert e <= TOL["bf16"], f"{name}: {e:.3e}"
+
+
+@pytest.mark.parametrize("B,T,hqk,hv,L,kw", [
+    (1, 64, 1, 1, 32, {}),
+    (2, 100, 2, 2, 16, {}),                                  # ragged tail block
+    (1, 96, 1, 2, 32, {}),                                   # grouped value heads
+    (1, 160, 2, 2, 32, {"lengths": [64, 32, 64]}),           # packed documents
+    (1, 80, 1, 1, 32, {"h0": True, "dht": True}),            # initial state, final-state gradient
+    (1, 64, 1, 1, 8, {"do_dtype": torch.bfloat16}),         # bf16 upstream gradients, small blocks
+])
+def test_bwd_matches_oracle(B, T, hqk, hv, L, kw):
+    _check(B, T, hqk, hv, L, 300 + T + L, **kw)
+
+
+def test_bwd_training_workload_sampled_units():
+    """The benchmark's shape (4 x 4096 + 4096 tokens, 16 heads, L = 32), run whole on the
+    GPU; three (sequence, head) units checked against the oracle one by one (the units are
+    independent: no q/k head is shared)."""
+    w = W.TRAIN_4K
+    inp = W.make_train(w)
+    rng = np.random.default_rng(91)
+    shape = (w.batch, w.seqlen, w.h_v, w.d_v)
+    do = torch.from_numpy(rng.standard_normal(shape, dtype=np.float32))
+    don = torch.from_numpy(rng.standard_normal(shape, dtype=np.float32))
+    scale = 1.0 / math.sqrt(w.d_k)
+    d = {k: v.cuda() for k, v in inp.items()}
+    print(f"bwd {w.name}", flush=True)
+    got = bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
+                             d["betan"], do.cuda(), don.cuda(), block=w.block, scale=scale, want_dh0=True)
+    torch.cuda.synchronize()
+    for b, h in ((0, 0), (2, 7), (3, 15)):
+        sl = lambda x: x[b:b + 1, :, h:h + 1]
+        u = {k: sl(v) for k, v in inp.items()}
+        ref = oracle.bwd_train(u["q"], u["k"], u["v"], u["g"], u["beta"], u["qn"], u["kn"], u["vn"], u["gn"],
+                               u["betan"], sl(do), sl(don), block=w.block, scale=scale)
+        errs = {n: rel_err(sl(got[n].cpu()), ref[n]) for n in NAMES}
+        errs["dh0"] = rel_err(got["dh0"][b:b + 1, h:h + 1].cpu(), ref["dh0"])
+        print(f"  unit ({b}, {h}): " + " ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
+        for name, e in errs.items():
+            assert e <= TOL["bf16"], f"unit ({b}, {h}) {name}: {e:.3e}"
