@@ -6,9 +6,9 @@ state and fp32 outputs, inputs resident in HBM.  `value` is tokens/s (clean +
 noisy tokens).  The line also carries the roofline of the fused kernel (HBM
 bytes the algorithm must move per launch over its measured duration), the
 model-FLOP rate against the bf16/fp16 MFMA peak, the denoise_step and commit
-bandwidths of the 64-request serving workload, the two-stream ShortConv forward and
-backward bandwidths at the training token shape, and the fp64 CPU oracle timed on
-the same workload.
+bandwidths of the 64-request serving workload, the training backward's time, the
+two-stream ShortConv forward and backward bandwidths at the training token shape, and
+the fp64 CPU oracle timed on the same workload.
 
   python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
 """
@@ -166,6 +166,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-serve", action="store_true")
     ap.add_argument("--no-conv", action="store_true")
+    ap.add_argument("--no-bwd", action="store_true")
     ap.add_argument("--route", choices=sorted(ROUTES), default="fused",
                     help="schedule of the training forward (fused is the performance mode; split and "
                          "records attribute its parts to separate kernels)")
@@ -296,6 +297,27 @@ def main():
                             "kernel": "bdgdn_k4_commit_record_kernel (7 recorded states, no outputs)",
                             "accept_us_per_call": ams * 1e3,
                             "accept_gb_per_s": abytes_acc / (ams * 1e-3) / 1e9}
+
+    if not args.no_bwd:
+        # the two-stream training backward at the same workload (fp32 upstream gradients)
+        gdo = torch.randn(o.shape, generator=torch.Generator(device=dev).manual_seed(5), device=dev)
+        gdon = torch.randn(o.shape, generator=torch.Generator(device=dev).manual_seed(6), device=dev)
+        bdesc = bd.make_fwd_desc(d["q"], d["v"], block=w.block, scale=scale, out_dtype=torch.float32)
+        bws = torch.empty(bd.bdgdn_bwd_train_workspace(bdesc), dtype=torch.uint8, device=dev)
+        bgrads = bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
+                                    d["betan"], gdo, gdon, block=w.block, scale=scale, workspace=bws)
+
+        def bwstep():
+            bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
+                               d["betan"], gdo, gdon, block=w.block, scale=scale, workspace=bws, grads=bgrads,
+                               stream=stream)
+        bsteps = max(2, args.steps // 4)
+        bms = time_launches(bwstep, bsteps, 2, stream)
+        result["backward"] = {
+            "workload": w.name, "ms_per_call": bms, "tokens_per_s": tokens / (bms * 1e-3), "steps": bsteps,
+            "kernels": "bdgdn_k2_scan_states_kernel (seed states) + bdgdn_bwd_noisy_kernel + "
+                       "bdgdn_bwd_scan_kernel + bdgdn_bwd_clean_kernel",
+            "workspace_bytes": bws.numel()}
 
     if not args.no_conv:
         # the GDN layer's two-stream ShortConv at the same token shape (channels = the q, k

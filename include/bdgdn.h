@@ -166,8 +166,9 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc,
                     const float *h0, void *o, void *on, float *ht,
                     void *workspace, size_t workspace_bytes, void *stream);
 
-/* Bytes of device workspace bdgdn_bwd_train needs: the clean seed state of every
- * (block, v-head) in fp32 plus scratch for the recomputed clean outputs; 0 for a
+/* Bytes of device workspace bdgdn_bwd_train needs: three fp32 states per (block, v-head)
+ * (the recomputed clean seed, the gradient of the noisy block's seed, the clean state
+ * gradient at the block's end) plus scratch for the recomputed clean outputs; 0 for a
  * descriptor it would reject. */
 size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
 

@@ -356,8 +356,9 @@ int bdgdn_accept_states(const bdgdn_serve_desc_t *desc, float *state_pool, const
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
 }
 
-// Backward workspace: the clean seed state of every (block, v-head) (fp32), then scratch
-// for the clean outputs the recomputing scan writes (bf16).
+// Backward workspace: three fp32 states per (block, v-head) -- the clean seed, the gradient
+// of the noisy block's seed, the clean state gradient at the block's end -- then scratch for
+// the clean outputs the recomputing scan writes (bf16).
 static bool bwd_shape_ok(const bdgdn_fwd_desc_t *d)
 {
     return d->dtype == BDGDN_BF16 && d->d_k == 128 && d->d_v == 128 && d->block <= 32;
@@ -375,7 +376,7 @@ size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc)
         return 0;
     if (desc->batch <= 0 || desc->seqlen <= 0 || !bwd_shape_ok(desc)) return 0;
     const size_t rows = (size_t)desc->batch * desc->seqlen;
-    return bwd_seed_bytes(desc) + rows * desc->h_v * desc->d_v * 2;
+    return 3 * bwd_seed_bytes(desc) + rows * desc->h_v * desc->d_v * 2;
 }
 
 int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, const void *v,
@@ -411,7 +412,7 @@ int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     sa.g = g; sa.beta = beta; sa.gn = gn; sa.betan = betan;
     sa.cu = packed ? cu_seqlens_dev : nullptr;
     sa.h0 = h0; sa.ht = nullptr;
-    sa.o = ws + bwd_seed_bytes(desc); sa.on = nullptr;
+    sa.o = ws + 3 * bwd_seed_bytes(desc); sa.on = nullptr;
     sa.ws = nullptr;
     sa.bs = seeds;
     sa.T = desc->seqlen; sa.L = desc->block; sa.nblk = (desc->seqlen + desc->block - 1) / desc->block;
@@ -440,13 +441,17 @@ int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     a.dq = dq; a.dk = dk; a.dv = dv; a.dg = dg; a.db = dbeta;
     a.dqn = dqn; a.dkn = dkn; a.dvn = dvn; a.dgn = dgn; a.dbn = dbetan;
     a.dh0 = dh0;
+    a.dseed = reinterpret_cast<float *>(ws + bwd_seed_bytes(desc));
+    a.dh = reinterpret_cast<float *>(ws + 2 * bwd_seed_bytes(desc));
     a.cu = sa.cu;
+    a.n_docs = packed ? nseq : 0;
     a.T = desc->seqlen; a.nblk = sa.nblk; a.L = desc->block;
     a.h_qk = desc->h_qk; a.h_v = desc->h_v;
     a.scale = desc->scale;
     a.atomic_qk = desc->h_v != desc->h_qk;
     const long rows = (long)desc->batch * desc->seqlen;
-    e = launch_bwd(desc->out_dtype == BDGDN_BF16, a, nseq * desc->h_v, rows * desc->h_qk * desc->d_k, strm);
+    e = launch_bwd(desc->out_dtype == BDGDN_BF16, a, nseq * desc->h_v, total_blocks(desc) * desc->h_v,
+                   rows * desc->h_qk * desc->d_k, strm);
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
 }
 

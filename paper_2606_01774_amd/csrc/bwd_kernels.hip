@@ -23,9 +23,11 @@
 // dh_(b-1) = dS0(clean block b) + dS0(noisy block b), since the noisy block b is seeded with
 // the clean state at the end of block b - 1.
 //
-// One workgroup per (sequence, v-head) walks its blocks in reverse with dh (fp32) in
-// registers; the seed of every block comes from the split schedule's clean scan
-// (launch_scan_states).  Products are 16x16x16 MFMA tiles on fp16 operands read from LDS
+// Three phases after the split schedule's clean scan has written every block's seed
+// (launch_scan_states): every noisy block in parallel (its gradients and its seed's
+// gradient), the reverse scan of the clean state gradient over the blocks of each
+// (sequence, v-head) in 32-column tiles (the columns are independent), and every clean
+// block in parallel from its seed and the gradient at its end.  Products are 16x16x16 MFMA tiles on fp16 operands read from LDS
 // through accessors (any transposition is an index swap), fp32 accumulation; the 32x32
 // triangular solve and the n x n backward terms run in fp32.  Blocks are padded to 32
 // positions with identity steps (k = 0, beta = 0, g = 0), which change nothing.
@@ -108,11 +110,12 @@ struct StreamPtrs {
 
 }  // namespace
 
-// One block's backward.  For the clean stream dS (LDS, f16) and dsn (registers, fp32, the
-// tile layout of the carried state gradient: wave w holds column block w, row blocks 0..7)
-// hold dS_n on entry; for the noisy stream dS_n is formed here from the block-end readout
-// (dsn is not read).  S0 (LDS f16) holds the seed.  Adds dS0 into acc (same layout).
-template <bool CLEAN, typename Od>
+// One block's gradients.  For the clean stream dS (LDS, f16) and dsn (registers, fp32, the
+// tile layout of a state gradient: wave w holds column block w, row blocks 0..7) hold dS_n
+// on entry; for the noisy stream dS_n is formed here from the block-end readout (dsn is not
+// read).  S0 (LDS f16) holds the seed.  With DS0 the seed's gradient dS0 is added into acc
+// (same layout).
+template <bool CLEAN, bool DS0, typename Od>
 __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, const float (&dsn)[8][4],
                           float (&acc)[8][4], int tid)
 {
@@ -132,12 +135,16 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
         sm.dB[tid] = 0.f;
     }
     __syncthreads();
-    if (tid == 0) {   // local cumulative log-gates and their exponentials
-        float c = 0.f;
-        for (int i = 0; i < NP; ++i) {
-            c += sm.G[i];
-            sm.G[i] = c;
-            sm.gam[i] = ex(c);
+    if (wave == 0) {   // local cumulative log-gates (a 32-lane scan) and their exponentials
+        float x = lane < NP ? sm.G[lane] : 0.f;
+#pragma unroll
+        for (int o = 1; o < NP; o <<= 1) {
+            const float y = __shfl_up(x, o);
+            if (lane >= o) x += y;
+        }
+        if (lane < NP) {
+            sm.G[lane] = x;
+            sm.gam[lane] = ex(x);
         }
     }
     __syncthreads();
@@ -149,11 +156,11 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
     // ---- KK = K K^T, P = (Q K^T) o Mc (clean); X = K S0 -> R = V - Gamma X; noisy dS_n = s Q^T dO
     if (wave < 4) {
         const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
-        f32x4 c = mm_tile<DD>(z, m0, n0, hq(sm.K), hqt(sm.K), lane);
+        f32x4 c = tile_mma<_Float16, DD>(z, sm.K + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
 #pragma unroll
         for (int j = 0; j < 4; ++j) sm.KK[(m0 + 4 * g4 + j) * LDF + n0 + rr] = c[j];
         if constexpr (CLEAN) {
-            c = mm_tile<DD>(z, m0, n0, hq(sm.Q), hqt(sm.K), lane);
+            c = tile_mma<_Float16, DD>(z, sm.Q + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int r = m0 + 4 * g4 + j, i = n0 + rr;
@@ -188,7 +195,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
             for (int j = 0; j < 4; ++j) {
                 const int r = 16 * tm + 4 * g4 + j, col = 16 * wave + rr;
                 if constexpr (!CLEAN) sm.dS[r * LDH + col] = (_Float16)c[j];
-                acc[tm][j] += gn * c[j];
+                if constexpr (DS0) acc[tm][j] += gn * c[j];
                 wg += c[j] * (float)sm.S0[r * LDH + col];
             }
         }
@@ -196,20 +203,24 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
         if (lane == 0) lds_add(&sm.dG[NP - 1], gn * wg);
     }
     __syncthreads();
-    // ---- A (fp32, into W), then M = (I + A)^-1 by forward substitution: one wave, lane c
-    // computes column c of M in place (its own earlier entries are re-read from LDS)
+    // ---- A (fp32, into W), then M = (I + A)^-1 by forward substitution (one wave)
     for (int e = tid; e < NP * NP; e += 64 * kWaves) {
         const int r = e / NP, i = e % NP;
         sm.W[r * LDF + i] = i < r ? sm.bet[r] * ex(sm.G[r] - sm.G[i]) * sm.KK[r * LDF + i] : 0.f;
     }
     __syncthreads();
-    if (wave == 0 && lane < NP) {
+    if (wave == 0 && lane < NP) {   // lane c: column c of M in registers (zero above the diagonal)
         const int c = lane;
+        float m[NP];
+#pragma unroll
         for (int r = 0; r < NP; ++r) {
             float v = r == c ? 1.f : 0.f;
-            for (int i = c; i < r; ++i) v = fmaf(-sm.W[r * LDF + i], sm.M[i * LDF + c], v);
-            sm.M[r * LDF + c] = r < c ? 0.f : v;
+#pragma unroll
+            for (int i = 0; i < r; ++i) v = fmaf(-sm.W[r * LDF + i], m[i], v);
+            m[r] = v;
         }
+#pragma unroll
+        for (int r = 0; r < NP; ++r) sm.M[r * LDF + c] = m[r];
     }
     __syncthreads();
     // ---- Delta = T R, T_ri = M_ri beta_i
@@ -224,7 +235,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
     // ---- E = dO Delta^T; dDelta = [clean] s P^T dO + D K dS_n, with the D-term gate gradient
     if (wave < 4) {
         const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
-        const f32x4 c = mm_tile<DD>(z, m0, n0, hq(sm.dO), hqt(sm.Dl), lane);
+        const f32x4 c = tile_mma<_Float16, DD>(z, sm.dO + m0 * LDH, LDH, sm.Dl + n0 * LDH, LDH, lane);
 #pragma unroll
         for (int j = 0; j < 4; ++j) sm.E[(m0 + 4 * g4 + j) * LDF + n0 + rr] = c[j];
     }
@@ -273,7 +284,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
     };
 #pragma unroll 1
     for (int tm = 0; tm < 2; ++tm) {
-        f32x4 c = mm_tile<DD>(z, 16 * tm, 16 * wave, hq(sm.dO), hqt(sm.S0), lane);
+        f32x4 c = tile_mma<_Float16, DD>(z, sm.dO + 16 * tm * LDH, LDH, sm.S0 + 16 * wave * LDH, LDH, lane);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int r = 16 * tm + 4 * g4 + j, col = 16 * wave + rr;
@@ -318,12 +329,12 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
     // ---- dT = dDelta R^T; dS0 into acc
     if (wave < 4) {
         const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
-        const f32x4 c = mm_tile<DD>(z, m0, n0, hq(sm.dDl), hqt(sm.R), lane);
+        const f32x4 c = tile_mma<_Float16, DD>(z, sm.dDl + m0 * LDH, LDH, sm.R + n0 * LDH, LDH, lane);
 #pragma unroll
         for (int j = 0; j < 4; ++j) sm.dT[(m0 + 4 * g4 + j) * LDF + n0 + rr] = c[j];
     }
     // dS0 += [clean] s Q^T Gamma dO - K^T Gamma dR (gamma_n dS_n was added above)
-    {
+    if constexpr (DS0) {
         auto sgdo = [&sm, s](int i, int c) { return (_Float16)(s * sm.gam[i] * (float)sm.dO[i * LDH + c]); };
         auto mgdr = [&sm](int i, int c) { return (_Float16)(-sm.gam[i] * (float)sm.dR[i * LDH + c]); };
 #pragma unroll
@@ -384,8 +395,8 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
     auto Wacc = [&sm](int r, int c) { return (_Float16)sm.W[r * LDF + c]; };
 #pragma unroll 1
     for (int tm = 0; tm < 2; ++tm) {
-        f32x4 c = mm_tile<DD>(z, 16 * tm, 16 * wave, hq(sm.dR), hqt(sm.S0), lane);
-        const f32x4 d2 = mm_tile<DD>(z, 16 * tm, 16 * wave, hq(sm.Dl), hqt(sm.dS), lane);
+        f32x4 c = tile_mma<_Float16, DD>(z, sm.dR + 16 * tm * LDH, LDH, sm.S0 + 16 * wave * LDH, LDH, lane);
+        const f32x4 d2 = tile_mma<_Float16, DD>(z, sm.Dl + 16 * tm * LDH, LDH, sm.dS + 16 * wave * LDH, LDH, lane);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int r = 16 * tm + 4 * g4 + j, col = 16 * wave + rr;
@@ -417,27 +428,161 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
         }
     }
     __syncthreads();
-    if (tid == 0) {
-        float c = 0.f;
-        for (int i = NP - 1; i >= 0; --i) {
-            c += sm.dG[i];
-            if (i < nvalid) {
-                p.dg[(long)i * a.h_v] = c;
-                p.db[(long)i * a.h_v] = sm.dB[i];
-            }
+    if (wave == 0) {   // dg = reverse cumulative sum of dG (a 32-lane scan)
+        float x = lane < NP ? sm.dG[lane] : 0.f;
+#pragma unroll
+        for (int o = 1; o < NP; o <<= 1) {
+            const float y = __shfl_down(x, o);
+            if (lane + o < NP) x += y;
+        }
+        if (lane < nvalid) {
+            p.dg[(long)lane * a.h_v] = x;
+            p.db[(long)lane * a.h_v] = sm.dB[lane];
         }
     }
     __syncthreads();
 }
 
+namespace {
+
+// The (sequence, first row, rows) of global block gblk: packed documents start on block
+// boundaries, so a block lies inside one document.
+__device__ __forceinline__ void block_unit(const BwdArgs &a, long gblk, int &n, long &p0, int &nvalid)
+{
+    if (a.cu) {
+        p0 = gblk * a.L;
+        int lo = 0, hi = a.n_docs;   // the last document with cu[d] <= p0
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (a.cu[mid] <= p0)
+                lo = mid;
+            else
+                hi = mid;
+        }
+        n = lo;
+        const long rem = a.cu[lo + 1] - p0;
+        nvalid = (int)(rem < a.L ? rem : a.L);
+    } else {
+        n = (int)(gblk / a.nblk);
+        const int b = (int)(gblk % a.nblk);
+        p0 = (long)n * a.T + (long)b * a.L;
+        const int rem = a.T - b * a.L;
+        nvalid = rem < a.L ? rem : a.L;
+    }
+}
+
 template <typename Od>
-__global__ void __launch_bounds__(512) bdgdn_bwd_chain_kernel(BwdArgs a)
+__device__ __forceinline__ StreamPtrs stream_ptrs(const BwdArgs &a, bool noisy, long p0, int h, int hq)
+{
+    const long qks = (long)a.h_qk * DD, vs = (long)a.h_v * DD;
+    StreamPtrs p;
+    p.q = static_cast<const __bf16 *>(noisy ? a.qn : a.q) + p0 * qks + hq * DD;
+    p.k = static_cast<const __bf16 *>(noisy ? a.kn : a.k) + p0 * qks + hq * DD;
+    p.v = static_cast<const __bf16 *>(noisy ? a.vn : a.v) + p0 * vs + h * DD;
+    p.g = (noisy ? a.gn : a.g) + p0 * a.h_v + h;
+    p.beta = (noisy ? a.betan : a.beta) + p0 * a.h_v + h;
+    p.dout = static_cast<const Od *>(noisy ? a.doutn : a.dout) + p0 * vs + h * DD;
+    p.dq = (noisy ? a.dqn : a.dq) + p0 * qks + hq * DD;
+    p.dk = (noisy ? a.dkn : a.dk) + p0 * qks + hq * DD;
+    p.dv = (noisy ? a.dvn : a.dv) + p0 * vs + h * DD;
+    p.dg = (noisy ? a.dgn : a.dg) + p0 * a.h_v + h;
+    p.db = (noisy ? a.dbn : a.db) + p0 * a.h_v + h;
+    return p;
+}
+
+// Stage a fp32 state (seed) as f16 into LDS.
+__device__ __forceinline__ void stage_state(_Float16 *dst, const float *src, int tid)
+{
+    for (int e = tid * 4; e < DD * DD; e += 512 * 4) {
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(src + e);
+        const int r = e / DD, c = e % DD;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dst[r * LDH + c + j] = (_Float16)v[j];
+    }
+}
+
+}  // namespace
+
+// Phase 1: every noisy block, in parallel (one workgroup per (global block, v-head)): its
+// gradients, and the gradient of its seed (written to dseed, fp32 [block][h_v][128][128]).
+template <typename Od>
+__global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     Smem &sm = *reinterpret_cast<Smem *>(smem_raw);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15;
-    const int n = blockIdx.x / a.h_v, h = blockIdx.x % a.h_v;
-    const int hq = h / (a.h_v / a.h_qk);
+    const long gblk = blockIdx.x / a.h_v;
+    const int h = blockIdx.x % a.h_v, hq = h / (a.h_v / a.h_qk);
+    int n, nvalid;
+    long p0;
+    block_unit(a, gblk, n, p0, nvalid);
+    const size_t so = ((size_t)gblk * a.h_v + h) * DD * DD;
+    stage_state(sm.S0, a.seeds + so, tid);
+    float acc[8][4];
+#pragma unroll
+    for (int tm = 0; tm < 8; ++tm)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[tm][j] = 0.f;
+    __syncthreads();
+    block_bwd<false, true, Od>(sm, stream_ptrs<Od>(a, true, p0, h, hq), a, nvalid, acc, acc, tid);
+    float *dst = a.dseed + so;
+#pragma unroll
+    for (int tm = 0; tm < 8; ++tm)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dst[(16 * tm + 4 * g4 + j) * DD + 16 * wave + rr] = acc[tm][j];
+}
+
+// Phase 3: every clean block, in parallel, from its seed and the gradient at its end (dh,
+// written by the scan).
+template <typename Od>
+__global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    Smem &sm = *reinterpret_cast<Smem *>(smem_raw);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15;
+    const long gblk = blockIdx.x / a.h_v;
+    const int h = blockIdx.x % a.h_v, hq = h / (a.h_v / a.h_qk);
+    int n, nvalid;
+    long p0;
+    block_unit(a, gblk, n, p0, nvalid);
+    const size_t so = ((size_t)gblk * a.h_v + h) * DD * DD;
+    stage_state(sm.S0, a.seeds + so, tid);
+    float dsn[8][4];
+    const float *dh = a.dh + so;
+#pragma unroll
+    for (int tm = 0; tm < 8; ++tm)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r = 16 * tm + 4 * g4 + j, c = 16 * wave + rr;
+            dsn[tm][j] = dh[r * DD + c];
+            sm.dS[r * LDH + c] = (_Float16)dsn[tm][j];
+        }
+    __syncthreads();
+    block_bwd<true, false, Od>(sm, stream_ptrs<Od>(a, false, p0, h, hq), a, nvalid, dsn, dsn, tid);
+}
+
+// Phase 2: the reverse scan of the clean state gradient over the blocks of a (sequence,
+// v-head), one workgroup per 32 columns (the columns are independent):
+//   dh_(b-1) = gamma_n dh_b + s Q^T Gamma dO - K^T Gamma dR + dseed_b,
+//   dR = T^T (s P^T dO + D K dh_b),
+// writing dh_b (the gradient at the end of block b) for phase 3, and dh0.
+namespace {
+constexpr int LDT = 32 + 8;   // f16 row stride of 32-column tiles
+struct ScanSmem {
+    _Float16 Q[NP * LDH], K[NP * LDH];
+    _Float16 dO[NP * LDT], dH[DD * LDT], dDl[NP * LDT], dR[NP * LDT];
+    float KK[NP * LDF], P[NP * LDF], W[NP * LDF], M[NP * LDF];
+    float G[NP], gam[NP], bet[NP];
+};
+}  // namespace
+
+template <typename Od>
+__global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
+{
+    __shared__ __align__(16) ScanSmem sm;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15;
+    const int chain = blockIdx.x >> 2, v0 = 32 * (blockIdx.x & 3);
+    const int n = chain / a.h_v, h = chain % a.h_v, hq = h / (a.h_v / a.h_qk);
     long r0, r1;
     if (a.cu) {
         r0 = a.cu[n];
@@ -448,70 +593,154 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_chain_kernel(BwdArgs a)
     }
     const int nb = (int)((r1 - r0 + a.L - 1) / a.L);
     const size_t SS = (size_t)DD * DD;
-    float dh[8][4], acc[8][4];
+    const long qks = (long)a.h_qk * DD, vs = (long)a.h_v * DD;
+    const float s = a.scale;
+    // dh tiles: wave w holds rows 32 w .. 32 w + 31 (two row blocks) of the 32 columns
+    float dh[2][2][4];
     const float *dht = a.dht ? a.dht + ((size_t)n * a.h_v + h) * SS : nullptr;
 #pragma unroll
-    for (int tm = 0; tm < 8; ++tm)
+    for (int tl = 0; tl < 2; ++tl)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            dh[tm][j] = dht ? dht[(16 * tm + 4 * g4 + j) * DD + 16 * wave + rr] : 0.f;
-    const long qks = (long)a.h_qk * DD, vs = (long)a.h_v * DD;
+        for (int tn = 0; tn < 2; ++tn)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                dh[tl][tn][j] = dht ? dht[(32 * wave + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] : 0.f;
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    auto hq_ = [](const _Float16 *m, int ld) { return [m, ld](int r, int c) { return m[r * ld + c]; }; };
+    auto hqt_ = [](const _Float16 *m, int ld) { return [m, ld](int r, int c) { return m[c * ld + r]; }; };
     for (int b = nb - 1; b >= 0; --b) {
         const long p0 = r0 + (long)b * a.L;
         const int nvalid = (int)(r1 - p0 < a.L ? r1 - p0 : a.L);
         const long gblk = a.cu ? p0 / a.L : (long)n * a.nblk + b;
-        const float *seed = a.seeds + ((size_t)gblk * a.h_v + h) * SS;
-        // seed (f16) and dS_n = dh (f16 operand copy; fp32 in registers)
-        for (int e = tid * 4; e < DD * DD; e += 512 * 4) {
-            const f32x4 v = *reinterpret_cast<const f32x4 *>(seed + e);
-            const int r = e / DD, c = e % DD;
+        const size_t so = ((size_t)gblk * a.h_v + h) * SS;
+        // publish dh_b; its f16 copy is the operand of K dh
 #pragma unroll
-            for (int j = 0; j < 4; ++j) sm.S0[r * LDH + c + j] = (_Float16)v[j];
+        for (int tl = 0; tl < 2; ++tl)
+#pragma unroll
+            for (int tn = 0; tn < 2; ++tn)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int r = 32 * wave + 16 * tl + 4 * g4 + j, c = 16 * tn + rr;
+                    a.dh[so + (size_t)r * DD + v0 + c] = dh[tl][tn][j];
+                    sm.dH[r * LDT + c] = (_Float16)dh[tl][tn][j];
+                }
+        // stage q, k (all 128 columns), the 32 columns of dO, the gates
+        {
+            const __bf16 *q = static_cast<const __bf16 *>(a.q) + p0 * qks + hq * DD;
+            const __bf16 *k = static_cast<const __bf16 *>(a.k) + p0 * qks + hq * DD;
+            for (int e = tid; e < NP * 16; e += 256) {
+                const int r = e >> 4, c = (e & 15) * 8;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    sm.Q[r * LDH + c + j] = r < nvalid ? (_Float16)to_f(q[r * qks + c + j]) : (_Float16)0.f;
+                    sm.K[r * LDH + c + j] = r < nvalid ? (_Float16)to_f(k[r * qks + c + j]) : (_Float16)0.f;
+                }
+            }
+            const Od *dout = static_cast<const Od *>(a.dout) + p0 * vs + h * DD + v0;
+            for (int e = tid; e < NP * 32; e += 256) {
+                const int r = e >> 5, c = e & 31;
+                sm.dO[r * LDT + c] = r < nvalid ? (_Float16)to_f(dout[r * vs + c]) : (_Float16)0.f;
+            }
+            if (tid < NP) {
+                const bool ok = tid < nvalid;
+                sm.bet[tid] = ok ? a.beta[(p0 + tid) * a.h_v + h] : 0.f;
+                sm.G[tid] = ok ? a.g[(p0 + tid) * a.h_v + h] : 0.f;
+            }
         }
+        __syncthreads();
+        if (wave == 0) {
+            float x = lane < NP ? sm.G[lane] : 0.f;
 #pragma unroll
-        for (int tm = 0; tm < 8; ++tm)
+            for (int o = 1; o < NP; o <<= 1) {
+                const float y = __shfl_up(x, o);
+                if (lane >= o) x += y;
+            }
+            if (lane < NP) {
+                sm.G[lane] = x;
+                sm.gam[lane] = ex(x);
+            }
+        }
+        __syncthreads();
+        const float Gn = sm.G[NP - 1], gn = ex(Gn);
+        {   // KK and P = (Q K^T) o Mc: one 16 x 16 tile per wave
+            const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
+            const f32x4 kk = tile_mma<_Float16, DD>(z, sm.K + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
+            const f32x4 qk = tile_mma<_Float16, DD>(z, sm.Q + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                sm.dS[(16 * tm + 4 * g4 + j) * LDH + 16 * wave + rr] = (_Float16)dh[tm][j];
-                acc[tm][j] = 0.f;
+                const int r = m0 + 4 * g4 + j, i = n0 + rr;
+                sm.KK[r * LDF + i] = kk[j];
+                sm.P[r * LDF + i] = i <= r ? qk[j] * ex(sm.G[r] - sm.G[i]) : 0.f;
             }
+        }
         __syncthreads();
-        StreamPtrs pc, pn;
-        pc.q = static_cast<const __bf16 *>(a.q) + (p0 * a.h_qk + hq) * DD;
-        pc.k = static_cast<const __bf16 *>(a.k) + (p0 * a.h_qk + hq) * DD;
-        pc.v = static_cast<const __bf16 *>(a.v) + (p0 * a.h_v + h) * DD;
-        pc.g = a.g + p0 * a.h_v + h;
-        pc.beta = a.beta + p0 * a.h_v + h;
-        pc.dout = static_cast<const Od *>(a.dout) + p0 * vs + h * DD;
-        pc.dq = a.dq + p0 * qks + hq * DD;
-        pc.dk = a.dk + p0 * qks + hq * DD;
-        pc.dv = a.dv + p0 * vs + h * DD;
-        pc.dg = a.dg + p0 * a.h_v + h;
-        pc.db = a.db + p0 * a.h_v + h;
-        pn.q = static_cast<const __bf16 *>(a.qn) + (p0 * a.h_qk + hq) * DD;
-        pn.k = static_cast<const __bf16 *>(a.kn) + (p0 * a.h_qk + hq) * DD;
-        pn.v = static_cast<const __bf16 *>(a.vn) + (p0 * a.h_v + h) * DD;
-        pn.g = a.gn + p0 * a.h_v + h;
-        pn.beta = a.betan + p0 * a.h_v + h;
-        pn.dout = static_cast<const Od *>(a.doutn) + p0 * vs + h * DD;
-        pn.dq = a.dqn + p0 * qks + hq * DD;
-        pn.dk = a.dkn + p0 * qks + hq * DD;
-        pn.dv = a.dvn + p0 * vs + h * DD;
-        pn.dg = a.dgn + p0 * a.h_v + h;
-        pn.db = a.dbn + p0 * a.h_v + h;
-        block_bwd<true, Od>(sm, pc, a, nvalid, dh, acc, tid);
-        block_bwd<false, Od>(sm, pn, a, nvalid, dh, acc, tid);
+        for (int e = tid; e < NP * NP; e += 256) {
+            const int r = e / NP, i = e % NP;
+            sm.W[r * LDF + i] = i < r ? sm.bet[r] * ex(sm.G[r] - sm.G[i]) * sm.KK[r * LDF + i] : 0.f;
+        }
+        __syncthreads();
+        if (wave == 0 && lane < NP) {
+            const int c = lane;
+            float m[NP];
 #pragma unroll
-        for (int tm = 0; tm < 8; ++tm)
+            for (int r = 0; r < NP; ++r) {
+                float v = r == c ? 1.f : 0.f;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) dh[tm][j] = acc[tm][j];
+                for (int i = 0; i < r; ++i) v = fmaf(-sm.W[r * LDF + i], m[i], v);
+                m[r] = v;
+            }
+#pragma unroll
+            for (int r = 0; r < NP; ++r) sm.M[r * LDF + c] = m[r];
+        }
+        __syncthreads();
+        {   // dDelta = s P^T dO + D K dh: one 16 x 16 tile (rows 16 (w >> 1), columns 16 (w & 1)) per wave
+            const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
+            const f32x4 kdh = mm_tile<DD>(z, m0, n0, hq_(sm.K, LDH), hq_(sm.dH, LDT), lane);
+            auto Pt = [](int r, int i) { return (_Float16)sm.P[i * LDF + r]; };
+            const f32x4 pd = mm_tile<NP>(z, m0, n0, Pt, hq_(sm.dO, LDT), lane);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = m0 + 4 * g4 + j;
+                sm.dDl[r * LDT + n0 + rr] = (_Float16)(s * pd[j] + ex(Gn - sm.G[r]) * kdh[j]);
+            }
+        }
+        __syncthreads();
+        {   // dR = T^T dDelta, T_ri = M_ri beta_i
+            const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
+            auto Tt = [](int i, int r) { return (_Float16)(sm.M[r * LDF + i] * sm.bet[i]); };
+            const f32x4 c = mm_tile<NP>(z, m0, n0, Tt, hq_(sm.dDl, LDT), lane);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) sm.dR[(m0 + 4 * g4 + j) * LDT + n0 + rr] = (_Float16)c[j];
+        }
+        __syncthreads();
+        {   // dh_(b-1) = gamma_n dh + s Q^T Gamma dO - K^T Gamma dR + dseed_b
+            auto sgdo = [s](int i, int c) { return (_Float16)(s * sm.gam[i] * (float)sm.dO[i * LDT + c]); };
+            auto mgdr = [](int i, int c) { return (_Float16)(-sm.gam[i] * (float)sm.dR[i * LDT + c]); };
+#pragma unroll
+            for (int tl = 0; tl < 2; ++tl)
+#pragma unroll
+                for (int tn = 0; tn < 2; ++tn) {
+                    const int m0 = 32 * wave + 16 * tl, n0 = 16 * tn;
+                    f32x4 c = mm_tile<NP>(z, m0, n0, hqt_(sm.K, LDH), mgdr, lane);
+                    c = mm_tile<NP>(c, m0, n0, hqt_(sm.Q, LDH), sgdo, lane);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int r = m0 + 4 * g4 + j;
+                        dh[tl][tn][j] = gn * dh[tl][tn][j] + c[j] + a.dseed[so + (size_t)r * DD + v0 + n0 + rr];
+                    }
+                }
+        }
+        __syncthreads();
     }
     if (a.dh0) {
         float *d0 = a.dh0 + ((size_t)n * a.h_v + h) * SS;
 #pragma unroll
-        for (int tm = 0; tm < 8; ++tm)
+        for (int tl = 0; tl < 2; ++tl)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) d0[(16 * tm + 4 * g4 + j) * DD + 16 * wave + rr] = dh[tm][j];
+            for (int tn = 0; tn < 2; ++tn)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    d0[(32 * wave + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] = dh[tl][tn][j];
     }
 }
 
@@ -520,9 +749,10 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_zero_kernel(float *p, long n)
     for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256) p[i] = 0.f;
 }
 
-size_t bwd_chain_lds() { return sizeof(Smem); }
+size_t bwd_block_lds() { return sizeof(Smem); }
 
-hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, int n_units, long qk_elems, hipStream_t s)
+hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, int n_chains, long n_block_units, long qk_elems,
+                      hipStream_t s)
 {
     if (a.atomic_qk) {
         for (float *p : {a.dq, a.dk, a.dqn, a.dkn}) {
@@ -531,14 +761,27 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, int n_units, long qk_elem
             if (e != hipSuccess) return e;
         }
     }
-    auto run = [&](auto kern) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+    auto run = [&](auto noisy, auto scan, auto clean) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(noisy),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(Smem));
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(kern, dim3(n_units), dim3(512), sizeof(Smem), s, a);
-        return hipGetLastError();
+        e = hipFuncSetAttribute(reinterpret_cast<const void *>(clean), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)sizeof(Smem));
+        if (e != hipSuccess) return e;
+        if (n_block_units > 0) {
+            hipLaunchKernelGGL(noisy, dim3((unsigned)n_block_units), dim3(512), sizeof(Smem), s, a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        hipLaunchKernelGGL(scan, dim3(4 * n_chains), dim3(256), 0, s, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (n_block_units > 0) {
+            hipLaunchKernelGGL(clean, dim3((unsigned)n_block_units), dim3(512), sizeof(Smem), s, a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        return hipSuccess;
     };
-    return bf16_out ? run(bdgdn_bwd_chain_kernel<__bf16>) : run(bdgdn_bwd_chain_kernel<float>);
+    return bf16_out ? run(bdgdn_bwd_noisy_kernel<__bf16>, bdgdn_bwd_scan_kernel<__bf16>, bdgdn_bwd_clean_kernel<__bf16>)
+                    : run(bdgdn_bwd_noisy_kernel<float>, bdgdn_bwd_scan_kernel<float>, bdgdn_bwd_clean_kernel<float>);
 }
 
 }  // namespace bdgdn
