@@ -167,6 +167,7 @@ def main():
     ap.add_argument("--no-serve", action="store_true")
     ap.add_argument("--no-conv", action="store_true")
     ap.add_argument("--no-bwd", action="store_true")
+    ap.add_argument("--no-views", action="store_true")
     ap.add_argument("--route", choices=sorted(ROUTES), default="fused",
                     help="schedule of the training forward (fused is the performance mode; split and "
                          "records attribute its parts to separate kernels)")
@@ -297,6 +298,29 @@ def main():
                             "kernel": "bdgdn_k4_commit_record_kernel (7 recorded states, no outputs)",
                             "accept_us_per_call": ams * 1e3,
                             "accept_gb_per_s": abytes_acc / (ams * 1e-3) / 1e9}
+
+    if not args.no_views:
+        # complementary views: one clean scan seeding two noisy views (the second view drawn
+        # with the same recipe), against two calls of the one-kernel forward
+        v2 = W.make_custom_train(w.batch, w.seqlen, w.h_qk, w.h_v, w.d_k, w.d_v, w.dtype, seed=w.seed + 50)
+        views = [{k_: d[k_ + "n"] for k_ in ("q", "k", "v", "g", "beta")},
+                 {k_: v2[k_ + "n"].to(dev) for k_ in ("q", "k", "v", "g", "beta")}]
+        for vw_ in views:
+            vw_["o"] = torch.empty_like(o)
+        vdesc = bd.make_fwd_desc(d["q"], d["v"], block=w.block, scale=scale, route=bd.BDGDN_ROUTE_SPLIT)
+        vws = torch.empty(bd.bdgdn_fwd_train_views_workspace(vdesc), dtype=torch.uint8, device=dev)
+        vms = {}
+        for rname, rt in (("fused", bd.BDGDN_ROUTE_FUSED), ("split", bd.BDGDN_ROUTE_SPLIT)):
+            def vstep2(rt=rt):
+                bd.bdgdn_fwd_train_views(d["q"], d["k"], d["v"], d["g"], d["beta"], views, block=w.block,
+                                         scale=scale, o=o, route=rt, workspace=vws, stream=stream)
+            vms[rname] = time_launches(vstep2, args.steps, args.warmup, stream)
+        result["views"] = {
+            "workload": w.name + " + a second noisy view", "n_views": 2,
+            "ms_per_call": min(vms.values()), "tokens_per_s": 3 * w.tokens / (min(vms.values()) * 1e-3),
+            "fused_ms": vms["fused"], "split_ms": vms["split"],
+            "schedules": {"fused": "bdgdn_fwd_pipelined_kernel once per view (clean scan recomputed on chip)",
+                          "split": "bdgdn_fwd_pipelined_seeds_kernel (view 0 + seed states) + bdgdn_k3_noisy_kernel"}}
 
     if not args.no_bwd:
         # the two-stream training backward at the same workload (fp32 upstream gradients)

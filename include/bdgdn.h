@@ -166,6 +166,43 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc,
                     const float *h0, void *o, void *on, float *ht,
                     void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * Complementary-view training forward (Sec. 3.3 "Training Objective and Mask Design": each
+ * block is trained under two complementary noisy views, both conditioned on the same clean
+ * context): one clean scan, whose boundary states seed every block of every noisy view.
+ * Each view is a noisy stream of its own (inputs, gates, block-end readout); view i's output
+ * equals the `on` of bdgdn_fwd_train with the same clean stream and view i as the noisy
+ * stream.  desc->route picks the schedule:
+ *   FUSED  one pass of the one-kernel forward per view, the clean scan recomputed with each
+ *          view and every noisy block evaluated from the on-chip boundary state (no
+ *          workspace);
+ *   SPLIT  one pass of the one-kernel forward over the clean stream and view 0 that also
+ *          writes the seed state of every (block, v-head) to the workspace, then the
+ *          noisy-block pass from the seeds for every further view (the clean scan runs once;
+ *          the seeds make a round trip through device memory).
+ * Other routes give BDGDN_ERR_UNSUPPORTED.
+ */
+typedef struct {
+    const void *q, *k, *v;   /* [B*T][h_qk or h_v][d] of desc->dtype, 16-byte aligned */
+    const float *g, *beta;   /* [B*T][h_v] fp32: the view's log-gates and step sizes  */
+    void *o;                 /* [B*T][h_v][d_v] of desc->out_dtype: its readout       */
+} bdgdn_noisy_view_t;
+
+/* Bytes of workspace bdgdn_fwd_train_views needs: the seed states for the SPLIT route, 0
+ * for FUSED or for a descriptor it would reject. */
+size_t bdgdn_fwd_train_views_workspace(const bdgdn_fwd_desc_t *desc);
+
+/* Clean inputs, h0, o, ht and cu_seqlens as for bdgdn_fwd_train (desc->route is not used);
+ * views[0 .. n_views-1], 1 <= n_views <= 16.  bf16 inputs, d_k = d_v = 128 and blocks of
+ * at most 32 positions (else BDGDN_ERR_UNSUPPORTED). */
+int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc,
+                          const void *q, const void *k, const void *v,
+                          const float *g, const float *beta,
+                          const bdgdn_noisy_view_t *views, int32_t n_views,
+                          const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                          const float *h0, void *o, float *ht,
+                          void *workspace, size_t workspace_bytes, void *stream);
+
 /* Bytes of device workspace bdgdn_bwd_train needs: three fp32 states per (block, v-head)
  * (the recomputed clean seed, the gradient of the noisy block's seed, the clean state
  * gradient at the block's end) plus scratch for the recomputed clean outputs; 0 for a

@@ -24,7 +24,7 @@ __all__ = [
     "bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace", "bdgdn_fwd_train",
     "bdgdn_commit_record", "bdgdn_accept_states", "BDGDN_ACT_NONE", "BDGDN_ACT_SILU",
     "bdgdn_shortconv_fwd", "bdgdn_shortconv_bwd_workspace", "bdgdn_shortconv_bwd",
-    "bdgdn_bwd_train_workspace", "bdgdn_bwd_train",
+    "bdgdn_bwd_train_workspace", "bdgdn_bwd_train", "bdgdn_fwd_train_views_workspace", "bdgdn_fwd_train_views",
     "bdgdn_denoise_step", "bdgdn_commit", "library_path", "load_library", "EXPORTED_SYMBOLS",
 ]
 
@@ -49,7 +49,8 @@ BDGDN_ACT_SILU = 1
 EXPORTED_SYMBOLS = ("bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace",
                     "bdgdn_fwd_train", "bdgdn_denoise_step", "bdgdn_commit", "bdgdn_commit_record",
                     "bdgdn_accept_states", "bdgdn_shortconv_fwd", "bdgdn_shortconv_bwd_workspace",
-                    "bdgdn_shortconv_bwd", "bdgdn_bwd_train_workspace", "bdgdn_bwd_train")
+                    "bdgdn_shortconv_bwd", "bdgdn_bwd_train_workspace", "bdgdn_bwd_train",
+                    "bdgdn_fwd_train_views_workspace", "bdgdn_fwd_train_views")
 
 
 class FwdDesc(ctypes.Structure):
@@ -66,6 +67,11 @@ class ServeDesc(ctypes.Structure):
                 ("h_v", ctypes.c_int32), ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32),
                 ("block", ctypes.c_int32), ("scale", ctypes.c_float),
                 ("dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32)]
+
+
+class NoisyView(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("g", ctypes.c_void_p), ("beta", ctypes.c_void_p), ("o", ctypes.c_void_p)]
 
 
 class ConvDesc(ctypes.Structure):
@@ -112,6 +118,11 @@ def load_library():
     lib.bdgdn_commit_record.restype = ctypes.c_int
     lib.bdgdn_accept_states.argtypes = [ctypes.POINTER(ServeDesc), P, P, P, ctypes.c_int32, P, P]
     lib.bdgdn_accept_states.restype = ctypes.c_int
+    lib.bdgdn_fwd_train_views_workspace.argtypes = [ctypes.POINTER(FwdDesc)]
+    lib.bdgdn_fwd_train_views_workspace.restype = ctypes.c_size_t
+    lib.bdgdn_fwd_train_views.argtypes = ([ctypes.POINTER(FwdDesc)] + [P] * 5 + [ctypes.POINTER(NoisyView), ctypes.c_int32]
+                                          + [P] * 6 + [ctypes.c_size_t, P])
+    lib.bdgdn_fwd_train_views.restype = ctypes.c_int
     lib.bdgdn_bwd_train_workspace.argtypes = [ctypes.POINTER(FwdDesc)]
     lib.bdgdn_bwd_train_workspace.restype = ctypes.c_size_t
     lib.bdgdn_bwd_train.argtypes = [ctypes.POINTER(FwdDesc)] + [P] * 28 + [ctypes.c_size_t, P]
@@ -235,6 +246,68 @@ def bdgdn_fwd_train(q, k, v, g, beta, qn, kn, vn, gn, betan, *, block, scale=Non
         _ptr(h0), _ptr(o), _ptr(on), _ptr(ht), _ptr(workspace), ws_size, _stream(stream))
     _check(st, "bdgdn_fwd_train")
     return o, on, ht
+
+
+def bdgdn_fwd_train_views_workspace(desc: FwdDesc) -> int:
+    return int(load_library().bdgdn_fwd_train_views_workspace(ctypes.byref(desc)))
+
+
+def bdgdn_fwd_train_views(q, k, v, g, beta, views, *, block, scale=None, cu_seqlens=None, cu_seqlens_host=None,
+                          h0=None, o=None, ht=None, want_ht=False, out_dtype=torch.float32,
+                          route=BDGDN_ROUTE_FUSED, workspace=None, stream=None):
+    """Complementary-view forward: one clean stream (q, k, v, g, beta, [B,T,h,d]) and
+    ``views``, a list of noisy streams, each a dict with q, k, v, g, beta (and optionally o).
+    route FUSED (a one-kernel pass per view) or SPLIT (one clean pass writing the seeds, then
+    a noisy pass per further view).  Returns (o, [view outputs], ht)."""
+    lib = load_library()
+    dt = q.dtype
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _dev(t, name, dt)
+    for name, t in (("g", g), ("beta", beta)):
+        _dev(t, name, torch.float32)
+    if o is not None:
+        out_dtype = o.dtype
+    num_seqs = 0
+    cu_h = None
+    if cu_seqlens is not None:
+        _dev(cu_seqlens, "cu_seqlens", torch.int32)
+        num_seqs = cu_seqlens.numel() - 1
+        if cu_seqlens_host is None:
+            cu_seqlens_host = cu_seqlens.cpu()
+        cu_h = torch.as_tensor(cu_seqlens_host, dtype=torch.int32).contiguous()
+    desc = make_fwd_desc(q, v, block=block, scale=scale, num_seqs=num_seqs, route=route, out_dtype=out_dtype)
+    if o is None:
+        o = torch.empty(v.shape, dtype=out_dtype, device=v.device)
+    _dev(o, "o", out_dtype)
+    outs = []
+    arr = (NoisyView * max(1, len(views)))()
+    for i, w in enumerate(views):
+        for name in ("q", "k", "v"):
+            _dev(w[name], f"views[{i}].{name}", dt)
+        for name in ("g", "beta"):
+            _dev(w[name], f"views[{i}].{name}", torch.float32)
+        ov = w.get("o")
+        if ov is None:
+            ov = torch.empty(w["v"].shape, dtype=out_dtype, device=v.device)
+        _dev(ov, f"views[{i}].o", out_dtype)
+        outs.append(ov)
+        arr[i] = NoisyView(w["q"].data_ptr(), w["k"].data_ptr(), w["v"].data_ptr(), w["g"].data_ptr(),
+                           w["beta"].data_ptr(), ov.data_ptr())
+    units = num_seqs if num_seqs else q.shape[0]
+    if ht is None and want_ht:
+        ht = torch.empty(units, v.shape[2], q.shape[3], v.shape[3], device=q.device, dtype=torch.float32)
+    _dev(ht, "ht", torch.float32)
+    _dev(h0, "h0", torch.float32)
+    ws_bytes = bdgdn_fwd_train_views_workspace(desc)
+    if workspace is None and ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    ws_size = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.bdgdn_fwd_train_views(
+        ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), arr, len(views),
+        _ptr(cu_seqlens), None if cu_h is None else ctypes.c_void_p(cu_h.data_ptr()),
+        _ptr(h0), _ptr(o), _ptr(ht), _ptr(workspace), ws_size, _stream(stream))
+    _check(st, "bdgdn_fwd_train_views")
+    return o, outs, ht
 
 
 def bdgdn_bwd_train_workspace(desc: FwdDesc) -> int:

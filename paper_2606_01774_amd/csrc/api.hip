@@ -356,6 +356,113 @@ int bdgdn_accept_states(const bdgdn_serve_desc_t *desc, float *state_pool, const
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
 }
 
+static bool views_supported(const bdgdn_fwd_desc_t *d)
+{
+    Types ty;
+    return types_of(d->dtype, d->out_dtype, ty) && split_supported(ty, d->d_k, d->d_v, lp_of(d->block)) &&
+           pipelined_supported(ty, d->d_k, lp_of(d->block));
+}
+
+size_t bdgdn_fwd_train_views_workspace(const bdgdn_fwd_desc_t *desc)
+{
+    if (!desc || check_heads(desc->h_qk, desc->h_v, desc->d_k, desc->d_v, desc->block, desc->scale, desc->dtype,
+                             desc->out_dtype) != BDGDN_OK)
+        return 0;
+    if (desc->batch <= 0 || desc->seqlen <= 0 || !views_supported(desc)) return 0;
+    if (desc->route != BDGDN_ROUTE_SPLIT) return 0;   // the fused schedule needs no workspace
+    // the seeds (needed from the second view on; sized for any number of views)
+    return (size_t)total_blocks(desc) * desc->h_v * desc->d_k * desc->d_v * sizeof(float);
+}
+
+int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, const void *v,
+                          const float *g, const float *beta, const bdgdn_noisy_view_t *views, int32_t n_views,
+                          const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host, const float *h0,
+                          void *o, float *ht, void *workspace, size_t workspace_bytes, void *stream)
+{
+    int st = check_fwd(desc, cu_seqlens_dev, cu_seqlens_host);
+    if (st != BDGDN_OK) return st;
+    if (!views_supported(desc)) return BDGDN_ERR_UNSUPPORTED;
+    if (desc->route != BDGDN_ROUTE_FUSED && desc->route != BDGDN_ROUTE_SPLIT) return BDGDN_ERR_UNSUPPORTED;
+    if (!q || !k || !v || !g || !beta || !o || !views || n_views < 1 || n_views > 16) return BDGDN_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return BDGDN_ERR_INVALID_ARG;
+    for (int i = 0; i < n_views; ++i) {
+        const bdgdn_noisy_view_t &w = views[i];
+        if (!w.q || !w.k || !w.v || !w.g || !w.beta || !w.o) return BDGDN_ERR_INVALID_ARG;
+        if (!aligned16(w.q) || !aligned16(w.k) || !aligned16(w.v) || !aligned16(w.o)) return BDGDN_ERR_INVALID_ARG;
+    }
+    if (desc->seqlen == 0) return BDGDN_OK;
+    const bool split = desc->route == BDGDN_ROUTE_SPLIT && n_views > 1;
+    const size_t need = split ? bdgdn_fwd_train_views_workspace(desc) : 0;
+    if (need > 0 && (workspace_bytes < need || !workspace)) return BDGDN_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return BDGDN_ERR_WORKSPACE;
+    const bool packed = desc->num_seqs > 0;
+    const int nseq = packed ? desc->num_seqs : desc->batch;
+    const hipStream_t strm = static_cast<hipStream_t>(stream);
+    const int lp = lp_of(desc->block);
+    const bool f32_out = desc->out_dtype == BDGDN_F32;
+    ScanArgs sa = {};
+    sa.q = q; sa.k = k; sa.v = v;
+    sa.qn = views[0].q; sa.kn = views[0].k; sa.vn = views[0].v;
+    sa.g = g; sa.beta = beta; sa.gn = views[0].g; sa.betan = views[0].beta;
+    sa.cu = packed ? cu_seqlens_dev : nullptr;
+    sa.h0 = h0; sa.ht = ht; sa.o = o; sa.on = nullptr;
+    sa.ws = nullptr;
+    sa.bs = static_cast<float *>(workspace);
+    sa.T = desc->seqlen; sa.L = desc->block; sa.nblk = (desc->seqlen + desc->block - 1) / desc->block;
+    sa.h_qk = desc->h_qk; sa.h_v = desc->h_v; sa.dv = desc->d_v;
+    sa.n_chains = nseq * desc->h_v;
+    sa.n_vt = desc->d_v / scan_tile_v();
+    sa.scale = desc->scale;
+    sa.n_order = 0;
+    if (packed && nseq <= kMaxOrder) {
+        std::vector<int> idx(nseq);
+        std::iota(idx.begin(), idx.end(), 0);
+        std::stable_sort(idx.begin(), idx.end(), [&](int x, int y) {
+            return cu_seqlens_host[x + 1] - cu_seqlens_host[x] > cu_seqlens_host[y + 1] - cu_seqlens_host[y];
+        });
+        for (int i = 0; i < nseq; ++i) sa.order[i] = idx[i];
+        sa.n_order = nseq;
+    }
+    Types ty;
+    types_of(desc->dtype, desc->out_dtype, ty);
+    hipError_t e;
+    if (!split) {
+        // FUSED: one on-chip pass per view (the clean scan recomputed with each; its outputs
+        // are the same every time)
+        sa.bs = nullptr;
+        for (int i = 0; i < n_views; ++i) {
+            sa.qn = views[i].q; sa.kn = views[i].k; sa.vn = views[i].v;
+            sa.gn = views[i].g; sa.betan = views[i].beta;
+            sa.on = views[i].o;
+            sa.ht = i == 0 ? ht : nullptr;
+            e = launch_fwd_pipelined(ty, desc->d_k, lp, sa, strm);
+            if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
+        }
+        return BDGDN_OK;
+    }
+    // SPLIT: view 0 in the one-kernel forward, which also writes the seed of every
+    // (block, v-head); every further view from the seeds
+    sa.on = views[0].o;
+    e = launch_fwd_pipelined_seeds(ty, lp, sa, strm);
+    if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
+    for (int i = 1; i < n_views; ++i) {
+        NoisyArgs na = {};
+        na.qn = views[i].q; na.kn = views[i].k; na.vn = views[i].v;
+        na.gn = views[i].g; na.betan = views[i].beta;
+        na.bs = sa.bs;
+        na.cu = sa.cu;
+        na.on = views[i].o;
+        na.T = desc->seqlen; na.L = desc->block; na.nblk = sa.nblk;
+        na.n_docs = packed ? nseq : 0;
+        na.total_blocks = total_blocks(desc);
+        na.h_qk = desc->h_qk; na.h_v = desc->h_v;
+        na.scale = desc->scale;
+        e = launch_noisy_blocks(lp, f32_out, na, strm);
+        if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
+    }
+    return BDGDN_OK;
+}
+
 // Backward workspace: three fp32 states per (block, v-head) -- the clean seed, the gradient
 // of the noisy block's seed, the clean state gradient at the block's end -- then scratch for
 // the clean outputs the recomputing scan writes (bf16).
@@ -430,7 +537,7 @@ int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         for (int i = 0; i < nseq; ++i) sa.order[i] = idx[i];
         sa.n_order = nseq;
     }
-    hipError_t e = launch_scan_states(lp_of(desc->block), sa, strm);
+    hipError_t e = launch_scan_states(lp_of(desc->block), false, sa, strm);
     if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
     // 2. the reverse walk over the blocks of every (sequence, v-head)
     BwdArgs a = {};

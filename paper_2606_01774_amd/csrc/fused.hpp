@@ -34,7 +34,7 @@ namespace bdgdn {
 // I"): the noisy waves and the noisy half of the record stand idle, the noisy rows are not
 // staged, and the C waves write each block's seed state (the clean state before the
 // block) to HBM for a separate noisy-block kernel.
-template <typename Out, int DK, int LP, bool SPLIT = false>
+template <typename Out, int DK, int LP, bool SPLIT = false, bool SEEDS = SPLIT>
 struct Fused {
     typedef __bf16 In;
     typedef _Float16 E;
@@ -42,6 +42,7 @@ struct Fused {
     typedef Out OutT;
     static constexpr int DKC = DK;
     static constexpr bool kSplit = SPLIT;
+    static constexpr bool kSeeds = SEEDS;   // write the clean state before every block (the seeds)
     static constexpr int NW = 12, kThreads = 64 * NW;
     static constexpr int BV = 32, NVB = 2;
     static constexpr int NB = LP / 16, DKB = DK / 16;
@@ -159,7 +160,7 @@ struct Fused {
         int qks, vst, gst;           // row strides (elements)
         long len;
         int L;
-        float *bs;     // SPLIT: seed state of the chain's first block (column v0), or null
+        float *bs;     // seed state of the chain's first block (column v0), or null
         long bs_blk;   // per-block advance of bs (elements)
         const float *h0;
         float *ht;
@@ -587,7 +588,7 @@ struct Fused {
             lds_barrier();
             float *bs = c.bs;
             for (int j = 0; j < nb; ++j) {
-                if constexpr (SPLIT) {
+                if constexpr (SEEDS) {
                     // the seed of noisy block j: the clean state before block j
 #pragma unroll
                     for (int kb = 0; kb < DKB; ++kb)
@@ -749,9 +750,9 @@ __device__ __forceinline__ void run_chain(const ScanArgs &a, unsigned char *smem
     c.L = a.L;
     const long state_off = ((long)seq * a.h_v + h) * DK * a.dv + v0;
     c.h0 = a.h0 ? a.h0 + state_off : nullptr;
-    if constexpr (K::kSplit) {
-        // seed states by global block: documents start on block boundaries, sequences
-        // own ceil(T / L) blocks each
+    if constexpr (K::kSeeds) {
+        // seed states by global block: documents start on block boundaries, sequences own
+        // ceil(T / L) blocks each
         const long gblk0 = a.cu ? base / a.L : (long)seq * a.nblk;
         c.bs = a.bs + (gblk0 * a.h_v + h) * DK * a.dv + v0;
         c.bs_blk = (long)a.h_v * DK * a.dv;

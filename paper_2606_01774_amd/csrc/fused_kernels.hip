@@ -32,6 +32,35 @@ static hipError_t launch_one(const ScanArgs &a, hipStream_t s)
     return hipGetLastError();
 }
 
+// The same forward that also writes the seed state of every (block, v-head) to a.bs (the
+// complementary-view schedule's first pass); d_k = 128.
+template <typename Out, int LP>
+__global__ void __launch_bounds__(768) bdgdn_fwd_pipelined_seeds_kernel(ScanArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    run_chain<Fused<Out, 128, LP, false, true>>(a, smem);
+}
+
+template <typename Out, int LP>
+static hipError_t launch_seeds(const ScanArgs &a, hipStream_t s)
+{
+    typedef Fused<Out, 128, LP, false, true> K;
+    auto kern = bdgdn_fwd_pipelined_seeds_kernel<Out, LP>;
+    hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, K::BYTES);
+    if (err != hipSuccess) return err;
+    const int grid = (a.n_chains + 7) / 8 * 8 * a.n_vt;
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(K::kThreads), K::BYTES, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_fwd_pipelined_seeds(Types ty, int lp, const ScanArgs &a, hipStream_t s)
+{
+    if (!pipelined_supported(ty, 128, lp) || a.n_vt * 32 != a.dv || !a.bs) return hipErrorInvalidValue;
+    if (ty == Types::BF16_IN_F32_OUT) return lp == 16 ? launch_seeds<float, 16>(a, s) : launch_seeds<float, 32>(a, s);
+    return lp == 16 ? launch_seeds<__bf16, 16>(a, s) : launch_seeds<__bf16, 32>(a, s);
+}
+
 bool pipelined_supported(Types ty, int dk, int lp)
 {
     return ty != Types::F32 && (dk == 64 || dk == 128) && (lp == 16 || lp == 32);

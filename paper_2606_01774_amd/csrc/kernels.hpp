@@ -99,6 +99,8 @@ hipError_t launch_fwd_scan(Types ty, int dk, int lp, const IntraArgs &ia, const 
 // inputs, blocks of at most 32 positions.
 bool pipelined_supported(Types ty, int dk, int lp);
 hipError_t launch_fwd_pipelined(Types ty, int dk, int lp, const ScanArgs &a, hipStream_t s);
+// The same, also writing the seed state of every (block, v-head) to a.bs (d_k = 128).
+hipError_t launch_fwd_pipelined_seeds(Types ty, int lp, const ScanArgs &a, hipStream_t s);
 // The split schedule (clean scan exposing the seed states, then the noisy-block pass):
 // bf16 inputs, d_k = d_v = 128, blocks of at most 32 positions.
 bool split_supported(Types ty, int dk, int dv, int lp);
@@ -135,7 +137,8 @@ struct BwdArgs {
 size_t bwd_block_lds();
 hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, int n_chains, long n_block_units, long qk_elems,
                       hipStream_t s);
-hipError_t launch_scan_states(int lp, const ScanArgs &sa, hipStream_t s);
+hipError_t launch_scan_states(int lp, bool f32_out, const ScanArgs &sa, hipStream_t s);
+hipError_t launch_noisy_blocks(int lp, bool f32_out, const NoisyArgs &na, hipStream_t s);
 
 // The two-stream ShortConv (conv_kernels.hip).  x, xn, y, yn, dy, dyn are [rows][D] of the
 // conv dtype; w [D][W] and bias [D] fp32; part [row groups][W + 1][D] fp32 partials of the

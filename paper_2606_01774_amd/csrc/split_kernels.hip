@@ -96,11 +96,10 @@ static hipError_t launch_split(const ScanArgs &sa, const NoisyArgs &na, hipStrea
     return hipGetLastError();
 }
 
-// The clean scan alone, writing the seed state of every block (the recomputation the
-// backward starts from); the clean outputs go to sa.o.
-hipError_t launch_scan_states(int lp, const ScanArgs &sa, hipStream_t s)
+// The clean scan alone, writing the seed state of every block (what the backward and the
+// noisy views start from); the clean outputs go to sa.o, of type Out.
+template <typename Out> static hipError_t scan_states(int lp, const ScanArgs &sa, hipStream_t s)
 {
-    if ((lp != 16 && lp != 32) || sa.n_vt * 32 != sa.dv || !sa.bs) return hipErrorInvalidValue;
     auto run = [&](auto k2, int bytes) {
         hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void *>(k2),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
@@ -109,8 +108,30 @@ hipError_t launch_scan_states(int lp, const ScanArgs &sa, hipStream_t s)
         hipLaunchKernelGGL(k2, dim3(grid), dim3(768), bytes, s, sa);
         return hipGetLastError();
     };
-    return lp == 16 ? run(bdgdn_k2_scan_states_kernel<__bf16, 16>, Fused<__bf16, 128, 16, true>::BYTES)
-                    : run(bdgdn_k2_scan_states_kernel<__bf16, 32>, Fused<__bf16, 128, 32, true>::BYTES);
+    return lp == 16 ? run(bdgdn_k2_scan_states_kernel<Out, 16>, Fused<Out, 128, 16, true>::BYTES)
+                    : run(bdgdn_k2_scan_states_kernel<Out, 32>, Fused<Out, 128, 32, true>::BYTES);
+}
+
+hipError_t launch_scan_states(int lp, bool f32_out, const ScanArgs &sa, hipStream_t s)
+{
+    if ((lp != 16 && lp != 32) || sa.n_vt * 32 != sa.dv || !sa.bs) return hipErrorInvalidValue;
+    return f32_out ? scan_states<float>(lp, sa, s) : scan_states<__bf16>(lp, sa, s);
+}
+
+// The noisy-block pass alone (every block of one noisy stream from the seeds in na.bs).
+hipError_t launch_noisy_blocks(int lp, bool f32_out, const NoisyArgs &na, hipStream_t s)
+{
+    if (lp != 16 && lp != 32) return hipErrorInvalidValue;
+    if (na.total_blocks * na.h_v == 0) return hipSuccess;
+    auto run = [&](auto k3, int bytes) {
+        hipLaunchKernelGGL(k3, dim3((unsigned)(na.total_blocks * na.h_v)), dim3(256), bytes, s, na);
+        return hipGetLastError();
+    };
+    if (f32_out)
+        return lp == 16 ? run(bdgdn_k3_noisy_kernel<float, 16>, Serve<float, 128, 16, false, false>::BYTES)
+                        : run(bdgdn_k3_noisy_kernel<float, 32>, Serve<float, 128, 32, false, false>::BYTES);
+    return lp == 16 ? run(bdgdn_k3_noisy_kernel<__bf16, 16>, Serve<__bf16, 128, 16, false, false>::BYTES)
+                    : run(bdgdn_k3_noisy_kernel<__bf16, 32>, Serve<__bf16, 128, 32, false, false>::BYTES);
 }
 
 bool split_supported(Types ty, int dk, int dv, int lp)

@@ -276,3 +276,26 @@ def test_bwd_train_validation_and_workspace():
     assert _bwd(ok, null_grad=True) == bd.BDGDN_ERR_INVALID_ARG
     assert _bwd(ok, ws=None, ws_bytes=0) == bd.BDGDN_ERR_WORKSPACE
     assert _bwd(ok, ws=FAKE, ws_bytes=need - 1) == bd.BDGDN_ERR_WORKSPACE
+
+
+def test_views_validation():
+    lib = bd.load_library()
+    ok = _desc()
+    split = _desc(route=bd.BDGDN_ROUTE_SPLIT)
+    assert lib.bdgdn_fwd_train_views_workspace(ctypes.byref(split)) == 2 * 4 * 128 * 128 * 4   # a seed per (block, head)
+    assert lib.bdgdn_fwd_train_views_workspace(ctypes.byref(ok)) == 0                          # fused: none
+    assert lib.bdgdn_fwd_train_views_workspace(ctypes.byref(_desc(d_k=64, d_v=64))) == 0
+    P = FAKE
+    views = (bd.NoisyView * 2)(bd.NoisyView(0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000),
+                               bd.NoisyView(0x1000, 0x1000, 0x1000, 0x1000, None, 0x1000))
+
+    def call(desc, n, ws=None, ws_bytes=0):
+        return lib.bdgdn_fwd_train_views(ctypes.byref(desc), P, P, P, P, P, views, n, None, None, None, P, None,
+                                         ws, ws_bytes, None)
+    assert call(ok, 0) == bd.BDGDN_ERR_INVALID_ARG
+    assert call(ok, 17) == bd.BDGDN_ERR_INVALID_ARG
+    assert call(ok, 2) == bd.BDGDN_ERR_INVALID_ARG          # view 1 has no beta
+    views[1] = bd.NoisyView(0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000)
+    assert call(split, 2) == bd.BDGDN_ERR_WORKSPACE
+    assert call(_desc(route=bd.BDGDN_ROUTE_RECORDS), 2) == bd.BDGDN_ERR_UNSUPPORTED
+    assert call(_desc(block=64), 1) == bd.BDGDN_ERR_UNSUPPORTED
