@@ -7,6 +7,7 @@
 #include <vector>
 
 #include "bdgdn.h"
+#include "bwd.hpp"
 #include "kernels.hpp"
 
 using namespace bdgdn;

@@ -32,6 +32,7 @@
 // triangular solve and the n x n backward terms run in fp32.  Blocks are padded to 32
 // positions with identity steps (k = 0, beta = 0, g = 0), which change nothing.
 #include "common.hpp"
+#include "bwd.hpp"
 #include "kernels.hpp"
 
 namespace bdgdn {

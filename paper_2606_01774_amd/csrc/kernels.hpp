@@ -113,30 +113,8 @@ int serve_tile_v();
 // Whether the (types, d_k, lp) combination is instantiated and fits in LDS.
 bool fwd_supported(Types ty, int dk, int lp);
 
-// Backward of the two-stream training forward (bwd_kernels.hip): from the seed states of
-// the split schedule's clean scan, the noisy blocks in parallel, a reverse scan of the clean
-// state gradient, the clean blocks in parallel.  Gradients are fp32; dq, dk (per q/k head) are summed with
-// atomics when several v-heads share a q/k head (zeroed first by launch_bwd).
-struct BwdArgs {
-    const void *q, *k, *v, *qn, *kn, *vn;   // bf16 [rows][heads][128]
-    const float *g, *beta, *gn, *betan;      // [rows][h_v]
-    const void *dout, *doutn;                // [rows][h_v][128] of the output type
-    const float *seeds;                      // [global block][h_v][128][128]
-    const float *dht;                        // [seq][h_v][128][128] or null
-    float *dq, *dk, *dv, *dg, *db;
-    float *dqn, *dkn, *dvn, *dgn, *dbn;
-    float *dh0;                              // or null
-    float *dseed;                            // [global block][h_v][128][128]: noisy seed gradients
-    float *dh;                               // [global block][h_v][128][128]: gradient at block ends
-    const int32_t *cu;                       // packed documents, or null
-    int n_docs;
-    int T, nblk, L, h_qk, h_v;
-    float scale;
-    bool atomic_qk;
-};
-size_t bwd_block_lds();
-hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, int n_chains, long n_block_units, long qk_elems,
-                      hipStream_t s);
+// The split schedule's two kernels on their own: the clean scan writing every block's seed
+// state (the backward's recomputation), and the noisy-block pass from the seeds.
 hipError_t launch_scan_states(int lp, bool f32_out, const ScanArgs &sa, hipStream_t s);
 hipError_t launch_noisy_blocks(int lp, bool f32_out, const NoisyArgs &na, hipStream_t s);
 
