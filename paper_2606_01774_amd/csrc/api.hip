@@ -477,6 +477,16 @@ static size_t bwd_seed_bytes(const bdgdn_fwd_desc_t *d)
     return ((size_t)total_blocks(d) * d->h_v * d->d_k * d->d_v * sizeof(float) + 255) & ~(size_t)255;
 }
 
+// U K (32 x d_k, fp16) and gamma_n (fp32) of every clean (block, v-head), for the reverse scan.
+static size_t bwd_uk_bytes(const bdgdn_fwd_desc_t *d)
+{
+    return ((size_t)total_blocks(d) * d->h_v * 32 * d->d_k * 2 + 255) & ~(size_t)255;
+}
+static size_t bwd_gn_bytes(const bdgdn_fwd_desc_t *d)
+{
+    return ((size_t)total_blocks(d) * d->h_v * sizeof(float) + 255) & ~(size_t)255;
+}
+
 size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc)
 {
     if (!desc || check_heads(desc->h_qk, desc->h_v, desc->d_k, desc->d_v, desc->block, desc->scale, desc->dtype,
@@ -484,7 +494,7 @@ size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc)
         return 0;
     if (desc->batch <= 0 || desc->seqlen <= 0 || !bwd_shape_ok(desc)) return 0;
     const size_t rows = (size_t)desc->batch * desc->seqlen;
-    return 3 * bwd_seed_bytes(desc) + rows * desc->h_v * desc->d_v * 2;
+    return 3 * bwd_seed_bytes(desc) + bwd_uk_bytes(desc) + bwd_gn_bytes(desc) + rows * desc->h_v * desc->d_v * 2;
 }
 
 int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, const void *v,
@@ -520,7 +530,7 @@ int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     sa.g = g; sa.beta = beta; sa.gn = gn; sa.betan = betan;
     sa.cu = packed ? cu_seqlens_dev : nullptr;
     sa.h0 = h0; sa.ht = nullptr;
-    sa.o = ws + 3 * bwd_seed_bytes(desc); sa.on = nullptr;
+    sa.o = ws + 3 * bwd_seed_bytes(desc) + bwd_uk_bytes(desc) + bwd_gn_bytes(desc); sa.on = nullptr;
     sa.ws = nullptr;
     sa.bs = seeds;
     sa.T = desc->seqlen; sa.L = desc->block; sa.nblk = (desc->seqlen + desc->block - 1) / desc->block;
@@ -549,8 +559,10 @@ int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     a.dq = dq; a.dk = dk; a.dv = dv; a.dg = dg; a.db = dbeta;
     a.dqn = dqn; a.dkn = dkn; a.dvn = dvn; a.dgn = dgn; a.dbn = dbetan;
     a.dh0 = dh0;
-    a.dseed = reinterpret_cast<float *>(ws + bwd_seed_bytes(desc));
+    a.cterm = reinterpret_cast<float *>(ws + bwd_seed_bytes(desc));
     a.dh = reinterpret_cast<float *>(ws + 2 * bwd_seed_bytes(desc));
+    a.uk = reinterpret_cast<_Float16 *>(ws + 3 * bwd_seed_bytes(desc));
+    a.gnb = reinterpret_cast<float *>(ws + 3 * bwd_seed_bytes(desc) + bwd_uk_bytes(desc));
     a.cu = sa.cu;
     a.n_docs = packed ? nseq : 0;
     a.T = desc->seqlen; a.nblk = sa.nblk; a.L = desc->block;

@@ -8,8 +8,9 @@
 namespace bdgdn {
 
 // Backward of the two-stream training forward (bwd_kernels.hip): from the seed states of
-// the split schedule's clean scan, the noisy blocks in parallel, a reverse scan of the clean
-// state gradient, the clean blocks in parallel.  Gradients are fp32; dq, dk (per q/k head) are summed with
+// the split schedule's clean scan, the noisy blocks (with the state-gradient-independent part
+// of the clean blocks) in parallel, a reverse scan of the clean state gradient, the clean
+// blocks in parallel.  Gradients are fp32; dq, dk (per q/k head) are summed with
 // atomics when several v-heads share a q/k head (zeroed first by launch_bwd).
 struct BwdArgs {
     const void *q, *k, *v, *qn, *kn, *vn;   // bf16 [rows][heads][128]
@@ -20,7 +21,11 @@ struct BwdArgs {
     float *dq, *dk, *dv, *dg, *db;
     float *dqn, *dkn, *dvn, *dgn, *dbn;
     float *dh0;                              // or null
-    float *dseed;                            // [global block][h_v][128][128]: noisy seed gradients
+    float *cterm;                            // [global block][h_v][128][128]: the part of dh_(b-1)
+                                             // that does not depend on dh_b (noisy seed gradient
+                                             // + clean terms)
+    _Float16 *uk;                            // [global block][h_v][32][128]: U K of each clean block
+    float *gnb;                              // [global block][h_v]: gamma_n of each clean block
     float *dh;                               // [global block][h_v][128][128]: gradient at block ends
     const int32_t *cu;                       // packed documents, or null
     int n_docs;

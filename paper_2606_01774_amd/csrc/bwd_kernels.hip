@@ -504,8 +504,126 @@ __device__ __forceinline__ void stage_state(_Float16 *dst, const float *src, int
 
 }  // namespace
 
+// The part of a clean block's contribution to the state gradient at its start that does not
+// depend on the gradient dh at its end.  With dDelta = s P^T dO + D K dh and dR = T^T dDelta,
+//   dS0 = gamma_n dh + s Q^T Gamma dO - K^T Gamma T^T (s P^T dO) - K^T (U K) dh,  U = Gamma T^T D,
+// so acc += s Q^T Gamma dO - K^T Gamma T^T (s P^T dO), and U K (32 x 128, U_ij = T_ji
+// gamma_i gamma_n / gamma_j, upper triangular with |U_ij| <= |T_ji|) goes to uk and gamma_n to
+// *gnb for the reverse scan.
+template <typename Od>
+__device__ void clean_prep(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, float (&acc)[8][4],
+                           _Float16 *uk, float *gnb, int tid)
+{
+    const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15;
+    const float s = a.scale;
+    const long qks = (long)a.h_qk * DD, vs = (long)a.h_v * DD;
+    stage_rows(sm.Q, p.q, qks, nvalid, tid);
+    stage_rows(sm.K, p.k, qks, nvalid, tid);
+    stage_rows(sm.dO, static_cast<const Od *>(p.dout), vs, nvalid, tid);
+    if (tid < NP) {
+        const bool ok = tid < nvalid;
+        sm.bet[tid] = ok ? p.beta[(long)tid * a.h_v] : 0.f;
+        sm.G[tid] = ok ? p.g[(long)tid * a.h_v] : 0.f;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        float x = lane < NP ? sm.G[lane] : 0.f;
+#pragma unroll
+        for (int o = 1; o < NP; o <<= 1) {
+            const float y = __shfl_up(x, o);
+            if (lane >= o) x += y;
+        }
+        if (lane < NP) {
+            sm.G[lane] = x;
+            sm.gam[lane] = ex(x);
+        }
+    }
+    __syncthreads();
+    const float Gn = sm.G[NP - 1];
+    if (tid == 0) *gnb = ex(Gn);
+    auto hq = [](const _Float16 *m) { return [m](int r, int c) { return m[r * LDH + c]; }; };
+    auto hqt = [](const _Float16 *m) { return [m](int r, int c) { return m[c * LDH + r]; }; };
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    if (wave < 4) {   // KK, P = (Q K^T) o Mc
+        const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
+        const f32x4 kk = tile_mma<_Float16, DD>(z, sm.K + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
+        const f32x4 qk = tile_mma<_Float16, DD>(z, sm.Q + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r = m0 + 4 * g4 + j, i = n0 + rr;
+            sm.KK[r * LDF + i] = kk[j];
+            sm.P[r * LDF + i] = i <= r ? qk[j] * ex(sm.G[r] - sm.G[i]) : 0.f;
+        }
+    }
+    __syncthreads();
+    for (int e = tid; e < NP * NP; e += 64 * kWaves) {
+        const int r = e / NP, i = e % NP;
+        sm.W[r * LDF + i] = i < r ? sm.bet[r] * ex(sm.G[r] - sm.G[i]) * sm.KK[r * LDF + i] : 0.f;
+    }
+    __syncthreads();
+    if (wave == 0 && lane < NP) {
+        const int c = lane;
+        float m[NP];
+#pragma unroll
+        for (int r = 0; r < NP; ++r) {
+            float v = r == c ? 1.f : 0.f;
+#pragma unroll
+            for (int i = 0; i < r; ++i) v = fmaf(-sm.W[r * LDF + i], m[i], v);
+            m[r] = v;
+        }
+#pragma unroll
+        for (int r = 0; r < NP; ++r) sm.M[r * LDF + c] = m[r];
+    }
+    __syncthreads();
+    // Y = s P^T dO -> dDl; U -> W (fp32)
+    auto Pt = [&sm](int r, int i) { return (_Float16)sm.P[i * LDF + r]; };
+#pragma unroll 1
+    for (int tm = 0; tm < 2; ++tm) {
+        const f32x4 c = mm_tile<NP>(z, 16 * tm, 16 * wave, Pt, hq(sm.dO), lane);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sm.dDl[(16 * tm + 4 * g4 + j) * LDH + 16 * wave + rr] = (_Float16)(s * c[j]);
+    }
+    for (int e = tid; e < NP * NP; e += 64 * kWaves) {
+        const int i = e / NP, j = e % NP;
+        sm.W[i * LDF + j] = j >= i ? sm.M[j * LDF + i] * sm.bet[i] * ex(sm.G[i] + Gn - sm.G[j]) : 0.f;
+    }
+    __syncthreads();
+    // dR0 = T^T Y, kept as -Gamma dR0 (f16) in dR; dO rescaled in place to s Gamma dO; U K -> uk
+    auto Tt = [&sm](int i, int r) { return (_Float16)(sm.M[r * LDF + i] * sm.bet[i]); };
+    auto Ua = [&sm](int i, int j) { return (_Float16)sm.W[i * LDF + j]; };
+#pragma unroll 1
+    for (int tm = 0; tm < 2; ++tm) {
+        const f32x4 c = mm_tile<NP>(z, 16 * tm, 16 * wave, Tt, hq(sm.dDl), lane);
+        const f32x4 u = mm_tile<NP>(z, 16 * tm, 16 * wave, Ua, hq(sm.K), lane);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r = 16 * tm + 4 * g4 + j, col = 16 * wave + rr;
+            sm.dR[r * LDH + col] = (_Float16)(-sm.gam[r] * c[j]);
+            uk[r * DD + col] = (_Float16)u[j];
+        }
+    }
+    {
+        const int r = tid >> 4, c = (tid & 15) * 8;
+        const float f = s * sm.gam[r];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sm.dO[r * LDH + c + j] = (_Float16)(f * (float)sm.dO[r * LDH + c + j]);
+    }
+    __syncthreads();
+    // acc += K^T (-Gamma dR0) + Q^T (s Gamma dO)
+#pragma unroll
+    for (int tm = 0; tm < 8; ++tm) {
+        f32x4 c = mm_tile<NP>(z, 16 * tm, 16 * wave, hqt(sm.K), hq(sm.dR), lane);
+        c = mm_tile<NP>(c, 16 * tm, 16 * wave, hqt(sm.Q), hq(sm.dO), lane);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[tm][j] += c[j];
+    }
+    __syncthreads();
+}
+
 // Phase 1: every noisy block, in parallel (one workgroup per (global block, v-head)): its
-// gradients, and the gradient of its seed (written to dseed, fp32 [block][h_v][128][128]).
+// gradients and its seed's gradient, plus the dh-independent part of the clean block of the
+// same position (clean_prep); both enter the state gradient at the block's start, whose sum
+// is written to cterm (fp32 [block][h_v][128][128]).
 template <typename Od>
 __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
 {
@@ -517,7 +635,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
     int n, nvalid;
     long p0;
     block_unit(a, gblk, n, p0, nvalid);
-    const size_t so = ((size_t)gblk * a.h_v + h) * DD * DD;
+    const size_t unit = (size_t)gblk * a.h_v + h, so = unit * DD * DD;
     stage_state(sm.S0, a.seeds + so, tid);
     float acc[8][4];
 #pragma unroll
@@ -526,7 +644,9 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
         for (int j = 0; j < 4; ++j) acc[tm][j] = 0.f;
     __syncthreads();
     block_bwd<false, true, Od>(sm, stream_ptrs<Od>(a, true, p0, h, hq), a, nvalid, acc, acc, tid);
-    float *dst = a.dseed + so;
+    clean_prep<Od>(sm, stream_ptrs<Od>(a, false, p0, h, hq), a, nvalid, acc, a.uk + unit * NP * DD, a.gnb + unit,
+                   tid);
+    float *dst = a.cterm + so;
 #pragma unroll
     for (int tm = 0; tm < 8; ++tm)
 #pragma unroll
@@ -563,21 +683,20 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
 }
 
 // Phase 2: the reverse scan of the clean state gradient over the blocks of a (sequence,
-// v-head), one workgroup per 32 columns (the columns are independent):
-//   dh_(b-1) = gamma_n dh_b + s Q^T Gamma dO - K^T Gamma dR + dseed_b,
-//   dR = T^T (s P^T dO + D K dh_b),
-// writing dh_b (the gradient at the end of block b) for phase 3, and dh0.
+// v-head), one workgroup of 4 waves per 32 columns (the columns are independent):
+//   dh_(b-1) = gamma_n dh_b + cterm_b - K^T Z,  Z = (U K) dh_b  (32 x 32),
+// writing dh_b (the gradient at the end of block b) for phase 3, and dh0.  The operands of
+// block b - 1 (U K, K, cterm, gamma_n) are loaded into registers while block b is computed.
 namespace {
-constexpr int LDT = 32 + 8;   // f16 row stride of 32-column tiles
+constexpr int LDK = NP + 8;   // f16 row stride of [*][32] tiles
 struct ScanSmem {
-    _Float16 Q[NP * LDH], K[NP * LDH];
-    _Float16 dO[NP * LDT], dH[DD * LDT], dDl[NP * LDT], dR[NP * LDT];
-    float KK[NP * LDF], P[NP * LDF], W[NP * LDF], M[NP * LDF];
-    float G[NP], gam[NP], bet[NP];
+    _Float16 UK[NP * LDH];       // U K of the block (32 x 128)
+    _Float16 dHt[32 * LDH];      // dh_b transposed: the tile's 32 columns x 128 rows
+    _Float16 Kt[2][DD * LDK];    // K^T (128 x 32), two buffers
+    _Float16 Zt[32 * LDK];       // Z transposed: 32 columns x 32 positions
 };
 }  // namespace
 
-template <typename Od>
 __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
 {
     __shared__ __align__(16) ScanSmem sm;
@@ -594,8 +713,7 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
     }
     const int nb = (int)((r1 - r0 + a.L - 1) / a.L);
     const size_t SS = (size_t)DD * DD;
-    const long qks = (long)a.h_qk * DD, vs = (long)a.h_v * DD;
-    const float s = a.scale;
+    const long qks = (long)a.h_qk * DD;
     // dh tiles: wave w holds rows 32 w .. 32 w + 31 (two row blocks) of the 32 columns
     float dh[2][2][4];
     const float *dht = a.dht ? a.dht + ((size_t)n * a.h_v + h) * SS : nullptr;
@@ -606,132 +724,87 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 dh[tl][tn][j] = dht ? dht[(32 * wave + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] : 0.f;
-    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-    auto hq_ = [](const _Float16 *m, int ld) { return [m, ld](int r, int c) { return m[r * ld + c]; }; };
-    auto hqt_ = [](const _Float16 *m, int ld) { return [m, ld](int r, int c) { return m[c * ld + r]; }; };
-    for (int b = nb - 1; b >= 0; --b) {
+    // staging map of the 32 x 128 operands: row tid / 8, 16 columns from 16 (tid % 8)
+    const int sr = tid >> 3, sc = (tid & 7) * 16;
+    f16x8 ukr[2];
+    bf16x8 kr[2];
+    float cs[2][2][4], gnv = 0.f;
+    auto fetch = [&](int b) {
         const long p0 = r0 + (long)b * a.L;
         const int nvalid = (int)(r1 - p0 < a.L ? r1 - p0 : a.L);
         const long gblk = a.cu ? p0 / a.L : (long)n * a.nblk + b;
-        const size_t so = ((size_t)gblk * a.h_v + h) * SS;
-        // publish dh_b; its f16 copy is the operand of K dh
+        const size_t unit = (size_t)gblk * a.h_v + h;
+        const f16x8 *u = reinterpret_cast<const f16x8 *>(a.uk + unit * NP * DD + sr * DD + sc);
+        ukr[0] = u[0];
+        ukr[1] = u[1];
+        if (sr < nvalid) {
+            const bf16x8 *k = reinterpret_cast<const bf16x8 *>(static_cast<const __bf16 *>(a.k) + (p0 + sr) * qks +
+                                                               hq * DD + sc);
+            kr[0] = k[0];
+            kr[1] = k[1];
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) kr[0][j] = kr[1][j] = (__bf16)0.f;
+        }
+        const float *c = a.cterm + unit * SS;
 #pragma unroll
         for (int tl = 0; tl < 2; ++tl)
 #pragma unroll
             for (int tn = 0; tn < 2; ++tn)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int r = 32 * wave + 16 * tl + 4 * g4 + j, c = 16 * tn + rr;
-                    a.dh[so + (size_t)r * DD + v0 + c] = dh[tl][tn][j];
-                    sm.dH[r * LDT + c] = (_Float16)dh[tl][tn][j];
-                }
-        // stage q, k (all 128 columns), the 32 columns of dO, the gates
-        {
-            const __bf16 *q = static_cast<const __bf16 *>(a.q) + p0 * qks + hq * DD;
-            const __bf16 *k = static_cast<const __bf16 *>(a.k) + p0 * qks + hq * DD;
-            for (int e = tid; e < NP * 16; e += 256) {
-                const int r = e >> 4, c = (e & 15) * 8;
+                for (int j = 0; j < 4; ++j)
+                    cs[tl][tn][j] = c[(32 * wave + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr];
+        gnv = a.gnb[unit];
+    };
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    if (nb > 0) fetch(nb - 1);
+    for (int b = nb - 1; b >= 0; --b) {
+        const int buf = b & 1;
+        const long p0 = r0 + (long)b * a.L;
+        const long gblk = a.cu ? p0 / a.L : (long)n * a.nblk + b;
+        float *dhb = a.dh + ((size_t)gblk * a.h_v + h) * SS;
+        // publish dh_b; stage dh_b^T, U K, K^T of block b
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    sm.Q[r * LDH + c + j] = r < nvalid ? (_Float16)to_f(q[r * qks + c + j]) : (_Float16)0.f;
-                    sm.K[r * LDH + c + j] = r < nvalid ? (_Float16)to_f(k[r * qks + c + j]) : (_Float16)0.f;
-                }
-            }
-            const Od *dout = static_cast<const Od *>(a.dout) + p0 * vs + h * DD + v0;
-            for (int e = tid; e < NP * 32; e += 256) {
-                const int r = e >> 5, c = e & 31;
-                sm.dO[r * LDT + c] = r < nvalid ? (_Float16)to_f(dout[r * vs + c]) : (_Float16)0.f;
-            }
-            if (tid < NP) {
-                const bool ok = tid < nvalid;
-                sm.bet[tid] = ok ? a.beta[(p0 + tid) * a.h_v + h] : 0.f;
-                sm.G[tid] = ok ? a.g[(p0 + tid) * a.h_v + h] : 0.f;
-            }
-        }
-        __syncthreads();
-        if (wave == 0) {
-            float x = lane < NP ? sm.G[lane] : 0.f;
+        for (int tl = 0; tl < 2; ++tl)
 #pragma unroll
-            for (int o = 1; o < NP; o <<= 1) {
-                const float y = __shfl_up(x, o);
-                if (lane >= o) x += y;
+            for (int tn = 0; tn < 2; ++tn) {
+                const int r = 32 * wave + 16 * tl + 4 * g4, c = 16 * tn + rr;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) dhb[(size_t)(r + j) * DD + v0 + c] = dh[tl][tn][j];
+                st4(sm.dHt + c * LDH + r, dh[tl][tn][0], dh[tl][tn][1], dh[tl][tn][2], dh[tl][tn][3]);
             }
-            if (lane < NP) {
-                sm.G[lane] = x;
-                sm.gam[lane] = ex(x);
-            }
+        *reinterpret_cast<f16x8 *>(sm.UK + sr * LDH + sc) = ukr[0];
+        *reinterpret_cast<f16x8 *>(sm.UK + sr * LDH + sc + 8) = ukr[1];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            sm.Kt[buf][(sc + j) * LDK + sr] = (_Float16)(float)kr[0][j];
+            sm.Kt[buf][(sc + 8 + j) * LDK + sr] = (_Float16)(float)kr[1][j];
         }
+        float c0[2][2][4];
+#pragma unroll
+        for (int tl = 0; tl < 2; ++tl)
+#pragma unroll
+            for (int tn = 0; tn < 2; ++tn)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) c0[tl][tn][j] = cs[tl][tn][j];
+        const float gn = gnv;
+        if (b > 0) fetch(b - 1);
         __syncthreads();
-        const float Gn = sm.G[NP - 1], gn = ex(Gn);
-        {   // KK and P = (Q K^T) o Mc: one 16 x 16 tile per wave
+        {   // Z = (U K) dh_b: one 16 x 16 tile per wave, stored transposed
             const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
-            const f32x4 kk = tile_mma<_Float16, DD>(z, sm.K + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
-            const f32x4 qk = tile_mma<_Float16, DD>(z, sm.Q + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
+            const f32x4 c = tile_mma<_Float16, DD>(z, sm.UK + m0 * LDH, LDH, sm.dHt + n0 * LDH, LDH, lane);
+            st4(sm.Zt + (n0 + rr) * LDK + m0 + 4 * g4, c[0], c[1], c[2], c[3]);
+        }
+        __syncthreads();
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int r = m0 + 4 * g4 + j, i = n0 + rr;
-                sm.KK[r * LDF + i] = kk[j];
-                sm.P[r * LDF + i] = i <= r ? qk[j] * ex(sm.G[r] - sm.G[i]) : 0.f;
+        for (int tl = 0; tl < 2; ++tl)
+#pragma unroll
+            for (int tn = 0; tn < 2; ++tn) {
+                const f32x4 c = tile_mma<_Float16, NP>(z, sm.Kt[buf] + (32 * wave + 16 * tl) * LDK, LDK,
+                                                       sm.Zt + 16 * tn * LDK, LDK, lane);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) dh[tl][tn][j] = gn * dh[tl][tn][j] + c0[tl][tn][j] - c[j];
             }
-        }
-        __syncthreads();
-        for (int e = tid; e < NP * NP; e += 256) {
-            const int r = e / NP, i = e % NP;
-            sm.W[r * LDF + i] = i < r ? sm.bet[r] * ex(sm.G[r] - sm.G[i]) * sm.KK[r * LDF + i] : 0.f;
-        }
-        __syncthreads();
-        if (wave == 0 && lane < NP) {
-            const int c = lane;
-            float m[NP];
-#pragma unroll
-            for (int r = 0; r < NP; ++r) {
-                float v = r == c ? 1.f : 0.f;
-#pragma unroll
-                for (int i = 0; i < r; ++i) v = fmaf(-sm.W[r * LDF + i], m[i], v);
-                m[r] = v;
-            }
-#pragma unroll
-            for (int r = 0; r < NP; ++r) sm.M[r * LDF + c] = m[r];
-        }
-        __syncthreads();
-        {   // dDelta = s P^T dO + D K dh: one 16 x 16 tile (rows 16 (w >> 1), columns 16 (w & 1)) per wave
-            const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
-            const f32x4 kdh = mm_tile<DD>(z, m0, n0, hq_(sm.K, LDH), hq_(sm.dH, LDT), lane);
-            auto Pt = [](int r, int i) { return (_Float16)sm.P[i * LDF + r]; };
-            const f32x4 pd = mm_tile<NP>(z, m0, n0, Pt, hq_(sm.dO, LDT), lane);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int r = m0 + 4 * g4 + j;
-                sm.dDl[r * LDT + n0 + rr] = (_Float16)(s * pd[j] + ex(Gn - sm.G[r]) * kdh[j]);
-            }
-        }
-        __syncthreads();
-        {   // dR = T^T dDelta, T_ri = M_ri beta_i
-            const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
-            auto Tt = [](int i, int r) { return (_Float16)(sm.M[r * LDF + i] * sm.bet[i]); };
-            const f32x4 c = mm_tile<NP>(z, m0, n0, Tt, hq_(sm.dDl, LDT), lane);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) sm.dR[(m0 + 4 * g4 + j) * LDT + n0 + rr] = (_Float16)c[j];
-        }
-        __syncthreads();
-        {   // dh_(b-1) = gamma_n dh + s Q^T Gamma dO - K^T Gamma dR + dseed_b
-            auto sgdo = [s](int i, int c) { return (_Float16)(s * sm.gam[i] * (float)sm.dO[i * LDT + c]); };
-            auto mgdr = [](int i, int c) { return (_Float16)(-sm.gam[i] * (float)sm.dR[i * LDT + c]); };
-#pragma unroll
-            for (int tl = 0; tl < 2; ++tl)
-#pragma unroll
-                for (int tn = 0; tn < 2; ++tn) {
-                    const int m0 = 32 * wave + 16 * tl, n0 = 16 * tn;
-                    f32x4 c = mm_tile<NP>(z, m0, n0, hqt_(sm.K, LDH), mgdr, lane);
-                    c = mm_tile<NP>(c, m0, n0, hqt_(sm.Q, LDH), sgdo, lane);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int r = m0 + 4 * g4 + j;
-                        dh[tl][tn][j] = gn * dh[tl][tn][j] + c[j] + a.dseed[so + (size_t)r * DD + v0 + n0 + rr];
-                    }
-                }
-        }
-        __syncthreads();
     }
     if (a.dh0) {
         float *d0 = a.dh0 + ((size_t)n * a.h_v + h) * SS;
@@ -762,7 +835,7 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, int n_chains, long n_bloc
             if (e != hipSuccess) return e;
         }
     }
-    auto run = [&](auto noisy, auto scan, auto clean) {
+    auto run = [&](auto noisy, auto clean) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(noisy),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(Smem));
         if (e != hipSuccess) return e;
@@ -773,7 +846,7 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, int n_chains, long n_bloc
             hipLaunchKernelGGL(noisy, dim3((unsigned)n_block_units), dim3(512), sizeof(Smem), s, a);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
-        hipLaunchKernelGGL(scan, dim3(4 * n_chains), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(bdgdn_bwd_scan_kernel, dim3(4 * n_chains), dim3(256), 0, s, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (n_block_units > 0) {
             hipLaunchKernelGGL(clean, dim3((unsigned)n_block_units), dim3(512), sizeof(Smem), s, a);
@@ -781,8 +854,8 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, int n_chains, long n_bloc
         }
         return hipSuccess;
     };
-    return bf16_out ? run(bdgdn_bwd_noisy_kernel<__bf16>, bdgdn_bwd_scan_kernel<__bf16>, bdgdn_bwd_clean_kernel<__bf16>)
-                    : run(bdgdn_bwd_noisy_kernel<float>, bdgdn_bwd_scan_kernel<float>, bdgdn_bwd_clean_kernel<float>);
+    return bf16_out ? run(bdgdn_bwd_noisy_kernel<__bf16>, bdgdn_bwd_clean_kernel<__bf16>)
+                    : run(bdgdn_bwd_noisy_kernel<float>, bdgdn_bwd_clean_kernel<float>);
 }
 
 }  // namespace bdgdn
