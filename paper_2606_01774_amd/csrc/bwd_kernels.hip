@@ -34,6 +34,7 @@
 #include "common.hpp"
 #include "bwd.hpp"
 #include "kernels.hpp"
+#include "ut.hpp"
 
 namespace bdgdn {
 
@@ -43,34 +44,61 @@ constexpr int NP = 32;           // positions per (padded) block
 constexpr int DD = 128;          // d_k = d_v
 constexpr int LDH = DD + 8;      // f16 row stride of [*][128] LDS matrices
 constexpr int LDF = NP + 1;      // fp32 row stride of [32][32] LDS matrices
+constexpr int LDM = NP + 8;      // f16 row stride of [32][32] LDS matrices
 constexpr int kWaves = 8;
 
 struct Smem {
     _Float16 S0[DD * LDH];       // seed state (d_k x d_v)
-    _Float16 dS[DD * LDH];       // dS_n operand (d_k x d_v)
+    _Float16 dS[DD * LDH];       // dS_n (d_k x d_v)
     _Float16 Q[NP * LDH], K[NP * LDH], R[NP * LDH], dO[NP * LDH];
-    _Float16 Dl[NP * LDH], dDl[NP * LDH], dR[NP * LDH];
-    float KK[NP * LDF], P[NP * LDF], M[NP * LDF], E[NP * LDF], dT[NP * LDF], W[NP * LDF], dA[NP * LDF];
-    float G[NP], gam[NP], bet[NP], dG[NP], dB[NP];
+    _Float16 Dl[NP * LDH], dDl[NP * LDH];
+    _Float16 dR[NP * LDH];       // -Gamma dR
+    _Float16 Mh[NP * LDM];       // M = (I + A)^-1
+    _Float16 Ph[NP * LDM];       // clean: P = (Q K^T) o Mc
+    _Float16 dPh[NP * LDM];      // the gradient of Q K^T: clean s E o Mc, noisy s E_ri D_i
+    _Float16 Wh[NP * LDM];       // dKK + dKK^T (clean_prep: U)
+    float KK[NP * LDF], dT[NP * LDF], W[NP * LDF];
+    float TdA[NP * LDF];         // T (T_ci = M_ci beta_i at [c][i]), later dA
+    float Mt[NP * LDF];          // M^T (fp32)
+    float G[NP], G2[NP], gam[NP], bet[NP], dG[NP], dB[NP];   // G2: cumulative log2-gates
 };
+static_assert(sizeof(Smem) <= 160 * 1024, "one workgroup's LDS");
 
-// acc += A(16 x K) B(K x 16) for the output tile whose first row is m0 and first column n0.
-template <int KD, typename FA, typename FB>
-__device__ __forceinline__ f32x4 mm_tile(f32x4 acc, int m0, int n0, const FA &fa, const FB &fb, int lane)
+typedef __fp16 fp16x4_t __attribute__((__vector_size__(4 * sizeof(__fp16))));
+
+// Operands of v_mfma_f32_16x16x16f16, lane (g, n) = (lane / 16, lane % 16): A row n with
+// k = 4 g .. 4 g + 3, B column n with the same k, C column n with rows 4 g .. 4 g + 3.  A C
+// tile kept in registers is therefore the B operand of a product contracting over its rows.
+//
+// A from a row-major matrix with k contiguous (one 8-byte read).
+__device__ __forceinline__ f16x4 op_row(const _Float16 *X, int ld, int m0, int k0, int lane)
 {
-    const int r = lane & 15, kq = (lane >> 4) * 4;
-#pragma unroll 1
-    for (int k0 = 0; k0 < KD; k0 += 16) {
-        f16x4 av, bv;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            av[j] = fa(m0 + r, k0 + kq + j);
-            bv[j] = fb(k0 + kq + j, n0 + r);
-        }
-        acc = __builtin_amdgcn_mfma_f32_16x16x16f16(av, bv, acc, 0, 0, 0);
-    }
-    return acc;
+    return *reinterpret_cast<const f16x4 *>(X + (m0 + (lane & 15)) * ld + k0 + 4 * (lane >> 4));
 }
+// X[k0 + 4 g + e][c0 + n] of a row-major matrix: the B operand X (k = row) or the A operand
+// X^T, by the LDS transpose load ds_read_b64_tr_b16 (lane L reads the 8 bytes at row
+// k0 + L / 4, columns c0 + 4 (L % 4); each 16-lane group receives the columns of the 4 x 16
+// block its lanes read).
+__device__ __forceinline__ f16x4 op_tr(const _Float16 *X, int ld, int k0, int c0, int lane)
+{
+    const _Float16 *p = X + (k0 + (lane >> 2)) * ld + c0 + 4 * (lane & 3);
+    return __builtin_bit_cast(f16x4, __builtin_amdgcn_ds_read_tr16_b64_v4f16(
+                                         (__attribute__((address_space(3))) fp16x4_t *)(p)));
+}
+__device__ __forceinline__ f32x4 mfma(f16x4 a, f16x4 b, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f16x4 h4(f32x4 v)
+{
+    return f16x4{(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
+}
+__device__ __forceinline__ f16x4 scale4(f16x4 v, f32x4 f)
+{
+    return f16x4{(_Float16)((float)v[0] * f[0]), (_Float16)((float)v[1] * f[1]), (_Float16)((float)v[2] * f[2]),
+                 (_Float16)((float)v[3] * f[3])};
+}
+__device__ __forceinline__ f32x4 ld4(const float *p) { return *reinterpret_cast<const f32x4 *>(p); }
 
 __device__ __forceinline__ float ex(float x) { return __expf(x); }
 
@@ -81,6 +109,21 @@ __device__ __forceinline__ float wave_sum(float v)
 {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+// Sum over the 16 lanes of a lane group (the columns of a C tile row).
+__device__ __forceinline__ float sum16(float v)
+{
+#pragma unroll
+    for (int o = 8; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+// Row sums (over the 32 lanes of each half-wave) of a 32 x 32 fp32 term laid out as row
+// 2 w + lane / 32 (+ 16 it), column lane % 32.
+__device__ __forceinline__ float half_sum(float v)
+{
+#pragma unroll
+    for (int o = 16; o > 0; o >>= 1) v += __shfl_xor(v, o);
     return v;
 }
 
@@ -102,6 +145,49 @@ template <typename In> __device__ __forceinline__ void stage_rows(_Float16 *dst,
     for (int j = 0; j < 8; ++j) dst[r * LDH + c + j] = h[j];
 }
 
+// Block-local cumulative log-gates G (and G2 = G log2 e) and gamma = exp G, by wave 0 (a
+// 32-lane scan of the staged gates in G).
+__device__ __forceinline__ void cum_gates(Smem &sm, int lane)
+{
+    float x = lane < NP ? sm.G[lane] : 0.f;
+#pragma unroll
+    for (int o = 1; o < NP; o <<= 1) {
+        const float y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane < NP) {
+        sm.G[lane] = x;
+        sm.G2[lane] = x * kLog2e;
+        sm.gam[lane] = ex(x);
+    }
+}
+
+// M = (I + A)^-1 of the staged block into sm.Mh, by the register-resident doubling solve of
+// one wave (ut::solve_t) from the keys in sm.K and the gates sm.G2, sm.bet.
+__device__ __forceinline__ void solve_m(Smem &sm, int lane)
+{
+    ut::QE kq[2][DD / 16];
+    const int r = lane & 15, g = lane >> 4;
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int kb = 0; kb < DD / 16; ++kb)
+            kq[rb][kb] = *reinterpret_cast<const f16x4 *>(sm.K + (16 * rb + r) * LDH + 16 * kb + 4 * g);
+    ut::Consts cs;
+    ut::make_consts(cs, lane);
+    ut::solve_t<2, DD / 16, false>(kq, sm.G2, sm.bet, sm.Mh, LDM, cs, lane);
+}
+
+// T^T operand quads of row block tm: A(m = i, k = r) = T_ri = M_ri beta_i for r in 0 .. 31
+// (M^T by the transpose load, scaled by beta of the row i = 16 tm + n).
+__device__ __forceinline__ void tt_ops(const Smem &sm, int tm, int lane, f16x4 &t0, f16x4 &t1)
+{
+    const float b = sm.bet[16 * tm + (lane & 15)];
+    const f32x4 bb = {b, b, b, b};
+    t0 = scale4(op_tr(sm.Mh, LDM, 0, 16 * tm, lane), bb);
+    t1 = scale4(op_tr(sm.Mh, LDM, 16, 16 * tm, lane), bb);
+}
+
 struct StreamPtrs {
     const __bf16 *q, *k, *v;   // first row of the block (q/k head hq, v head h)
     const float *g, *beta;     // first row (head h), stride h_v
@@ -111,18 +197,20 @@ struct StreamPtrs {
 
 }  // namespace
 
-// One block's gradients.  For the clean stream dS (LDS, f16) and dsn (registers, fp32, the
-// tile layout of a state gradient: wave w holds column block w, row blocks 0..7) hold dS_n
-// on entry; for the noisy stream dS_n is formed here from the block-end readout (dsn is not
-// read).  S0 (LDS f16) holds the seed.  With DS0 the seed's gradient dS0 is added into acc
-// (same layout).
-template <bool CLEAN, bool DS0, typename Od>
+// One block's gradients.  S0 (LDS f16) holds the seed.  For the clean stream dS (LDS, f16)
+// and dsn (registers, fp32, the C-tile layout of a state gradient: wave w holds column block
+// w, row blocks 0 .. 7) hold dS_n on entry; for the noisy stream dS_n is formed here from the
+// block-end readout (dsn is not read) and the seed's gradient dS0 is added into acc (same
+// layout).  Wave w computes the 16 columns 16 w .. 16 w + 15 of every 32 x 128 and 128 x 128
+// product.
+template <bool CLEAN, typename Od>
 __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, const float (&dsn)[8][4],
                           float (&acc)[8][4], int tid)
 {
-    const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15;
+    const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
     const float s = a.scale;
     const long qks = (long)a.h_qk * DD, vs = (long)a.h_v * DD;
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
     // ---- stage rows and gates
     stage_rows(sm.Q, p.q, qks, nvalid, tid);
     stage_rows(sm.K, p.k, qks, nvalid, tid);
@@ -136,27 +224,17 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
         sm.dB[tid] = 0.f;
     }
     __syncthreads();
-    if (wave == 0) {   // local cumulative log-gates (a 32-lane scan) and their exponentials
-        float x = lane < NP ? sm.G[lane] : 0.f;
-#pragma unroll
-        for (int o = 1; o < NP; o <<= 1) {
-            const float y = __shfl_up(x, o);
-            if (lane >= o) x += y;
-        }
-        if (lane < NP) {
-            sm.G[lane] = x;
-            sm.gam[lane] = ex(x);
-        }
-    }
+    if (wave == 0) cum_gates(sm, lane);
     __syncthreads();
     const float Gn = sm.G[NP - 1];
     const float gn = ex(Gn);
-    auto hq = [](const _Float16 *m) { return [m](int r, int c) { return m[r * LDH + c]; }; };
-    auto hqt = [](const _Float16 *m) { return [m](int r, int c) { return m[c * LDH + r]; }; };
-    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-    // ---- KK = K K^T, P = (Q K^T) o Mc (clean); X = K S0 -> R = V - Gamma X; noisy dS_n = s Q^T dO
-    if (wave < 4) {
-        const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
+    // ---- M (wave 0); KK = K K^T and P = (Q K^T) o Mc (clean) (waves 1 .. 4); X = K S0 ->
+    // R = V - Gamma X; dS_n (noisy: s Q^T dO) with its share gamma_n dS_n of dS0 and the gate
+    // term dG_last += gamma_n <dS_n, S0>
+    if (wave == 0) {
+        solve_m(sm, lane);
+    } else if (wave <= 4) {
+        const int m0 = 16 * ((wave - 1) >> 1), n0 = 16 * ((wave - 1) & 1);
         f32x4 c = tile_mma<_Float16, DD>(z, sm.K + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
 #pragma unroll
         for (int j = 0; j < 4; ++j) sm.KK[(m0 + 4 * g4 + j) * LDF + n0 + rr] = c[j];
@@ -165,23 +243,31 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int r = m0 + 4 * g4 + j, i = n0 + rr;
-                sm.P[r * LDF + i] = i <= r ? c[j] * ex(sm.G[r] - sm.G[i]) : 0.f;
+                sm.Ph[r * LDM + i] = (_Float16)(i <= r ? c[j] * ex(sm.G[r] - sm.G[i]) : 0.f);
             }
         }
     }
-#pragma unroll 1
-    for (int tm = 0; tm < 2; ++tm) {   // X tiles: rows 16 tm, columns 16 wave
-        const f32x4 x = mm_tile<DD>(z, 16 * tm, 16 * wave, hq(sm.K), hq(sm.S0), lane);
+    f16x4 s0q[8];   // S0 tiles (tm, w): the B operands of K S0 and the layout of dS_n
+#pragma unroll
+    for (int tm = 0; tm < 8; ++tm) s0q[tm] = op_tr(sm.S0, LDH, 16 * tm, c0, lane);
+#pragma unroll
+    for (int tm = 0; tm < 2; ++tm) {
+        f32x4 x = z;
+#pragma unroll
+        for (int kb = 0; kb < 8; ++kb) x = mfma(op_row(sm.K, LDH, 16 * tm, 16 * kb, lane), s0q[kb], x);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int r = 16 * tm + 4 * g4 + j, c = 16 * wave + rr;
-            const float rv = (float)sm.R[r * LDH + c] - sm.gam[r] * x[j];
-            sm.R[r * LDH + c] = (_Float16)rv;
+            const int r = 16 * tm + 4 * g4 + j, c = c0 + rr;
+            sm.R[r * LDH + c] = (_Float16)((float)sm.R[r * LDH + c] - sm.gam[r] * x[j]);
         }
     }
-    // dS_n (clean: given, fp32 in dsn; noisy: s Q^T dO, formed here in the dh tile layout):
-    // its gamma_n dS_n share of dS0 and the gate term dG_last += gamma_n <dS_n, S0>
+    f16x4 dsq[8];   // dS_n tiles (tm, w): the B operands of K dS_n
     {
+        f16x4 dob[2];
+        if constexpr (!CLEAN) {
+            dob[0] = op_tr(sm.dO, LDH, 0, c0, lane);
+            dob[1] = op_tr(sm.dO, LDH, 16, c0, lane);
+        }
         float wg = 0.f;
 #pragma unroll
         for (int tm = 0; tm < 8; ++tm) {
@@ -190,241 +276,251 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
 #pragma unroll
                 for (int j = 0; j < 4; ++j) c[j] = dsn[tm][j];
             } else {
-                c = mm_tile<NP>(z, 16 * tm, 16 * wave, hqt(sm.Q), hq(sm.dO), lane) * s;
+                c = mfma(op_tr(sm.Q, LDH, 16, 16 * tm, lane), dob[1], mfma(op_tr(sm.Q, LDH, 0, 16 * tm, lane), dob[0], z));
+                c *= s;
             }
+            dsq[tm] = h4(c);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int r = 16 * tm + 4 * g4 + j, col = 16 * wave + rr;
-                if constexpr (!CLEAN) sm.dS[r * LDH + col] = (_Float16)c[j];
-                if constexpr (DS0) acc[tm][j] += gn * c[j];
-                wg += c[j] * (float)sm.S0[r * LDH + col];
+                if constexpr (!CLEAN) {
+                    sm.dS[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = dsq[tm][j];
+                    acc[tm][j] += gn * c[j];
+                }
+                wg += c[j] * (float)s0q[tm][j];
             }
         }
         wg = wave_sum(wg);
         if (lane == 0) lds_add(&sm.dG[NP - 1], gn * wg);
     }
     __syncthreads();
-    // ---- A (fp32, into W), then M = (I + A)^-1 by forward substitution (one wave)
+    // ---- Delta = T R (T_ri = M_ri beta_i); fp32 copies of T and M^T for the dA products
+    {
+        const f32x4 b0 = ld4(sm.bet + 4 * g4), b1 = ld4(sm.bet + 16 + 4 * g4);
+        const f16x4 r0 = op_tr(sm.R, LDH, 0, c0, lane), r1 = op_tr(sm.R, LDH, 16, c0, lane);
+#pragma unroll
+        for (int tm = 0; tm < 2; ++tm) {
+            const f16x4 t0 = scale4(op_row(sm.Mh, LDM, 16 * tm, 0, lane), b0);
+            const f16x4 t1 = scale4(op_row(sm.Mh, LDM, 16 * tm, 16, lane), b1);
+            const f32x4 d = mfma(t1, r1, mfma(t0, r0, z));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) sm.Dl[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = (_Float16)d[j];
+        }
+    }
     for (int e = tid; e < NP * NP; e += 64 * kWaves) {
         const int r = e / NP, i = e % NP;
-        sm.W[r * LDF + i] = i < r ? sm.bet[r] * ex(sm.G[r] - sm.G[i]) * sm.KK[r * LDF + i] : 0.f;
+        const float m = (float)sm.Mh[r * LDM + i];
+        sm.TdA[r * LDF + i] = m * sm.bet[i];
+        sm.Mt[i * LDF + r] = m;
     }
     __syncthreads();
-    if (wave == 0 && lane < NP) {   // lane c: column c of M in registers (zero above the diagonal)
-        const int c = lane;
-        float m[NP];
-#pragma unroll
-        for (int r = 0; r < NP; ++r) {
-            float v = r == c ? 1.f : 0.f;
-#pragma unroll
-            for (int i = 0; i < r; ++i) v = fmaf(-sm.W[r * LDF + i], m[i], v);
-            m[r] = v;
-        }
-#pragma unroll
-        for (int r = 0; r < NP; ++r) sm.M[r * LDF + c] = m[r];
-    }
-    __syncthreads();
-    // ---- Delta = T R, T_ri = M_ri beta_i
-    auto Tacc = [&sm](int r, int i) { return (_Float16)(sm.M[r * LDF + i] * sm.bet[i]); };
-#pragma unroll 1
-    for (int tm = 0; tm < 2; ++tm) {
-        const f32x4 c = mm_tile<NP>(z, 16 * tm, 16 * wave, Tacc, hq(sm.R), lane);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) sm.Dl[(16 * tm + 4 * g4 + j) * LDH + 16 * wave + rr] = (_Float16)c[j];
-    }
-    __syncthreads();
-    // ---- E = dO Delta^T; dDelta = [clean] s P^T dO + D K dS_n, with the D-term gate gradient
+    // ---- E = dO Delta^T (waves 0 .. 3), with the gradient of Q K^T into dPh and (clean) the
+    // gates of Mc, W = s E o P: dG_r += sum_i W_ri, dG_i -= sum_r W_ri
     if (wave < 4) {
-        const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
-        const f32x4 c = tile_mma<_Float16, DD>(z, sm.dO + m0 * LDH, LDH, sm.Dl + n0 * LDH, LDH, lane);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) sm.E[(m0 + 4 * g4 + j) * LDF + n0 + rr] = c[j];
-    }
-#pragma unroll 1
-    for (int tm = 0; tm < 2; ++tm) {
-        const f32x4 kds = mm_tile<DD>(z, 16 * tm, 16 * wave, hq(sm.K), hq(sm.dS), lane);
-        f32x4 pd = z;
-        if constexpr (CLEAN) {
-            auto Pt = [&sm](int r, int i) { return (_Float16)sm.P[i * LDF + r]; };
-            pd = mm_tile<NP>(z, 16 * tm, 16 * wave, Pt, hq(sm.dO), lane);
-        }
+        const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1), i = n0 + rr;
+        const f32x4 e4 = tile_mma<_Float16, DD>(z, sm.dO + m0 * LDH, LDH, sm.Dl + n0 * LDH, LDH, lane);
+        float colw = 0.f;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int r = 16 * tm + 4 * g4 + j, c = 16 * wave + rr;
-            const float Dr = ex(Gn - sm.G[r]);
-            sm.dDl[r * LDH + c] = (_Float16)(s * pd[j] + Dr * kds[j]);
-            // D-term of the gates: w_r = D_r sum_j (K dS_n)_rj Delta_rj -> dG_last += w, dG_r -= w
-            float w = Dr * kds[j] * (float)sm.Dl[r * LDH + c];
-            w += __shfl_xor(w, 1);
-            w += __shfl_xor(w, 2);
-            w += __shfl_xor(w, 4);
-            w += __shfl_xor(w, 8);
-            if (rr == 0) {
-                lds_add(&sm.dG[r], -w);
-                lds_add(&sm.dG[NP - 1], w);
-            }
-        }
-    }
-    __syncthreads();
-    // ---- dR = T^T dDelta (= dV); dQ
-    auto Tt = [&sm](int i, int r) { return (_Float16)(sm.M[r * LDF + i] * sm.bet[i]); };
-#pragma unroll 1
-    for (int tm = 0; tm < 2; ++tm) {
-        const f32x4 c = mm_tile<NP>(z, 16 * tm, 16 * wave, Tt, hq(sm.dDl), lane);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int r = 16 * tm + 4 * g4 + j, col = 16 * wave + rr;
-            sm.dR[r * LDH + col] = (_Float16)c[j];
-            if (r < nvalid) p.dv[(long)r * a.h_v * DD + col] = c[j];
-        }
-    }
-    // dQ = [clean] s Gamma (dO S0^T) + (s E o Mc) K;  [noisy] s gamma_n (dO S0^T) + s (E D) K
-    auto dPm = [&sm, s, Gn](int r, int i) {
-        if constexpr (CLEAN) return (_Float16)(i <= r ? s * sm.E[r * LDF + i] * ex(sm.G[r] - sm.G[i]) : 0.f);
-        else return (_Float16)(s * sm.E[r * LDF + i] * ex(Gn - sm.G[i]));
-    };
-#pragma unroll 1
-    for (int tm = 0; tm < 2; ++tm) {
-        f32x4 c = tile_mma<_Float16, DD>(z, sm.dO + 16 * tm * LDH, LDH, sm.S0 + 16 * wave * LDH, LDH, lane);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int r = 16 * tm + 4 * g4 + j, col = 16 * wave + rr;
+            const int r = m0 + 4 * g4 + j;
             if constexpr (CLEAN) {
-                // gate term of Gamma Q S0: dG_r += s gamma_r sum_a Q_ra (dO S0^T)_ra
-                float w = s * sm.gam[r] * c[j] * (float)sm.Q[r * LDH + col];
-                w += __shfl_xor(w, 1);
-                w += __shfl_xor(w, 2);
-                w += __shfl_xor(w, 4);
-                w += __shfl_xor(w, 8);
-                if (rr == 0) lds_add(&sm.dG[r], w);
-                c[j] *= s * sm.gam[r];
+                const float dec = i <= r ? ex(sm.G[r] - sm.G[i]) : 0.f;
+                sm.dPh[r * LDM + i] = (_Float16)(s * e4[j] * dec);
+                const float w = s * e4[j] * (float)sm.Ph[r * LDM + i];
+                const float wr = sum16(w);
+                if (rr == 0) lds_add(&sm.dG[r], wr);
+                colw += w;
             } else {
-                c[j] *= s * gn;
+                sm.dPh[r * LDM + i] = (_Float16)(s * e4[j] * ex(Gn - sm.G[i]));
             }
         }
-        c = mm_tile<NP>(c, 16 * tm, 16 * wave, dPm, hq(sm.K), lane);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int r = 16 * tm + 4 * g4 + j, col = 16 * wave + rr;
-            if (r < nvalid) {
-                float *dst = p.dq + (long)r * a.h_qk * DD + col;
-                if (a.atomic_qk)
-                    atomicAdd(dst, c[j]);
-                else
-                    *dst = c[j];
-            }
+        if constexpr (CLEAN) {
+            colw += __shfl_xor(colw, 16);
+            colw += __shfl_xor(colw, 32);
+            if (g4 == 0) lds_add(&sm.dG[i], -colw);
         }
     }
-    // clean: gates of Mc, W = s E o P: dG_r += sum_i W_ri, dG_i -= sum_r W_ri
-    if constexpr (CLEAN) {
-        for (int e = tid; e < NP * NP; e += 64 * kWaves) {
-            const int r = e / NP, i = e % NP;
-            const float w = s * sm.E[r * LDF + i] * sm.P[r * LDF + i];
-            if (w != 0.f) {
-                lds_add(&sm.dG[r], w);
-                lds_add(&sm.dG[i], -w);
+    // dDelta = [clean] s P^T dO + D K dS_n, with the D-term gate gradient
+    // w_r = D_r sum_c (K dS_n)_rc Delta_rc: dG_last += w, dG_r -= w
+    {
+        f16x4 do0, do1;
+        if constexpr (CLEAN) {
+            do0 = op_tr(sm.dO, LDH, 0, c0, lane);
+            do1 = op_tr(sm.dO, LDH, 16, c0, lane);
+        }
+#pragma unroll
+        for (int tm = 0; tm < 2; ++tm) {
+            f32x4 kds = z;
+#pragma unroll
+            for (int kb = 0; kb < 8; ++kb) kds = mfma(op_row(sm.K, LDH, 16 * tm, 16 * kb, lane), dsq[kb], kds);
+            f32x4 pd = z;
+            if constexpr (CLEAN)
+                pd = mfma(op_tr(sm.Ph, LDM, 16, 16 * tm, lane), do1, mfma(op_tr(sm.Ph, LDM, 0, 16 * tm, lane), do0, z));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = 16 * tm + 4 * g4 + j, c = c0 + rr;
+                const float Dr = ex(Gn - sm.G[r]);
+                sm.dDl[r * LDH + c] = (_Float16)(s * pd[j] + Dr * kds[j]);
+                const float w = sum16(Dr * kds[j] * (float)sm.Dl[r * LDH + c]);
+                if (rr == 0) {
+                    lds_add(&sm.dG[r], -w);
+                    lds_add(&sm.dG[NP - 1], w);
+                }
             }
         }
     }
     __syncthreads();
-    // ---- dT = dDelta R^T; dS0 into acc
-    if (wave < 4) {
-        const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
-        const f32x4 c = tile_mma<_Float16, DD>(z, sm.dDl + m0 * LDH, LDH, sm.R + n0 * LDH, LDH, lane);
+    // ---- dR = T^T dDelta (= dV), kept as -Gamma dR (LDS and, as B operands, registers);
+    // [noisy] dS0 += K^T (-Gamma dR); dQ; dT = dDelta R^T (waves 4 .. 7)
+    f16x4 drq[2];
+    {
+        const f16x4 dd0 = op_tr(sm.dDl, LDH, 0, c0, lane), dd1 = op_tr(sm.dDl, LDH, 16, c0, lane);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) sm.dT[(m0 + 4 * g4 + j) * LDF + n0 + rr] = c[j];
+        for (int tm = 0; tm < 2; ++tm) {
+            f16x4 t0, t1;
+            tt_ops(sm, tm, lane, t0, t1);
+            const f32x4 c = mfma(t1, dd1, mfma(t0, dd0, z));
+            f32x4 ng;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = 16 * tm + 4 * g4 + j, col = c0 + rr;
+                if (r < nvalid) p.dv[(long)r * vs + col] = c[j];
+                ng[j] = -sm.gam[r] * c[j];
+            }
+            drq[tm] = h4(ng);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) sm.dR[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = drq[tm][j];
+        }
     }
-    // dS0 += [clean] s Q^T Gamma dO - K^T Gamma dR (gamma_n dS_n was added above)
-    if constexpr (DS0) {
-        auto sgdo = [&sm, s](int i, int c) { return (_Float16)(s * sm.gam[i] * (float)sm.dO[i * LDH + c]); };
-        auto mgdr = [&sm](int i, int c) { return (_Float16)(-sm.gam[i] * (float)sm.dR[i * LDH + c]); };
+    if constexpr (!CLEAN) {
 #pragma unroll
         for (int tm = 0; tm < 8; ++tm) {
-            f32x4 c = mm_tile<NP>(z, 16 * tm, 16 * wave, hqt(sm.K), mgdr, lane);
-            if constexpr (CLEAN) c = mm_tile<NP>(c, 16 * tm, 16 * wave, hqt(sm.Q), sgdo, lane);
+            const f32x4 c =
+                mfma(op_tr(sm.K, LDH, 16, 16 * tm, lane), drq[1], mfma(op_tr(sm.K, LDH, 0, 16 * tm, lane), drq[0], z));
 #pragma unroll
             for (int j = 0; j < 4; ++j) acc[tm][j] += c[j];
         }
     }
-    __syncthreads();
-    // ---- dbeta, dA = strictly lower part of -M^T (dT diag beta) M^T (fp32)
-    // W = dT diag(beta) M^T  (W_rc = sum_i dT_ri beta_i M_ci)
-    for (int e = tid; e < NP * NP; e += 64 * kWaves) {
-        const int r = e / NP, c = e % NP;
-        float v = 0.f;
-        for (int i = 0; i < NP; ++i) v = fmaf(sm.dT[r * LDF + i] * sm.bet[i], sm.M[c * LDF + i], v);
-        sm.W[r * LDF + c] = v;
+    {   // dQ = [clean] s Gamma (dO S0^T) + dPh K  |  [noisy] s gamma_n (dO S0^T) + dPh K
+        const f16x4 k0q = op_tr(sm.K, LDH, 0, c0, lane), k1q = op_tr(sm.K, LDH, 16, c0, lane);
+#pragma unroll
+        for (int tm = 0; tm < 2; ++tm) {
+            f32x4 c = tile_mma<_Float16, DD>(z, sm.dO + 16 * tm * LDH, LDH, sm.S0 + c0 * LDH, LDH, lane);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = 16 * tm + 4 * g4 + j, col = c0 + rr;
+                if constexpr (CLEAN) {
+                    // gate term of Gamma Q S0: dG_r += s gamma_r sum_a Q_ra (dO S0^T)_ra
+                    const float w = sum16(s * sm.gam[r] * c[j] * (float)sm.Q[r * LDH + col]);
+                    if (rr == 0) lds_add(&sm.dG[r], w);
+                    c[j] *= s * sm.gam[r];
+                } else {
+                    c[j] *= s * gn;
+                }
+            }
+            c = mfma(op_row(sm.dPh, LDM, 16 * tm, 16, lane), k1q, mfma(op_row(sm.dPh, LDM, 16 * tm, 0, lane), k0q, c));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = 16 * tm + 4 * g4 + j, col = c0 + rr;
+                if (r < nvalid) {
+                    float *dst = p.dq + (long)r * a.h_qk * DD + col;
+                    if (a.atomic_qk)
+                        atomicAdd(dst, c[j]);
+                    else
+                        *dst = c[j];
+                }
+            }
+        }
     }
-    if (tid < NP) {   // dbeta_i += sum_r dT_ri M_ri
-        float v = 0.f;
-        for (int r = 0; r < NP; ++r) v = fmaf(sm.dT[r * LDF + tid], sm.M[r * LDF + tid], v);
-        sm.dB[tid] += v;
+    if (wave >= 4) {
+        const int m0 = 16 * ((wave - 4) >> 1), n0 = 16 * ((wave - 4) & 1);
+        const f32x4 c = tile_mma<_Float16, DD>(z, sm.dDl + m0 * LDH, LDH, sm.R + n0 * LDH, LDH, lane);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sm.dT[(m0 + 4 * g4 + j) * LDF + n0 + rr] = c[j];
     }
     __syncthreads();
-    // dA_rc = -sum_i M_ir W_ic (r > c)
-    for (int e = tid; e < NP * NP; e += 64 * kWaves) {
-        const int r = e / NP, c = e % NP;
+    // ---- dbeta, dA = strictly lower part of -M^T (dT diag beta) M^T (fp32 MFMA)
+    // W = dT T^T (W_rc = sum_i dT_ri beta_i M_ci), stored transposed; dbeta_i += sum_r dT_ri M_ri
+    if (wave < 4) {
+        const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
+        const f32x4 c = tile_mma<float, NP>(z, sm.dT + m0 * LDF, LDF, sm.TdA + n0 * LDF, LDF, lane);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sm.W[(n0 + rr) * LDF + m0 + 4 * g4 + j] = c[j];
+    } else if (tid < 256 + NP) {
+        const int i = tid - 256;
         float v = 0.f;
-        if (r > c)
-            for (int i = 0; i < NP; ++i) v = fmaf(-sm.M[i * LDF + r], sm.W[i * LDF + c], v);
-        sm.dA[r * LDF + c] = v;
+        for (int r = 0; r < NP; ++r) v = fmaf(sm.dT[r * LDF + i], sm.Mt[i * LDF + r], v);
+        sm.dB[i] += v;
+    }
+    __syncthreads();
+    // dA_rc = -sum_i M_ir W_ic (r > c), into TdA
+    if (wave < 4) {
+        const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
+        const f32x4 c = tile_mma<float, NP>(z, sm.Mt + m0 * LDF, LDF, sm.W + n0 * LDF, LDF, lane);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r = m0 + 4 * g4 + j, cc = n0 + rr;
+            sm.TdA[r * LDF + cc] = r > cc ? -c[j] : 0.f;
+        }
     }
     __syncthreads();
     // dbeta_r += sum_c dA_rc F_rc; dG from A: WA = dA o A, dG_r += sum_c WA_rc, dG_c -= sum_r WA_rc;
-    // dKK_rc = dA_rc beta_r gamma_r/gamma_c, symmetrised into W
-    for (int e = tid; e < NP * NP; e += 64 * kWaves) {
-        const int r = e / NP, c = e % NP;
-        const float da = sm.dA[r * LDF + c];
-        float sym = 0.f;
+    // dKK_rc = dA_rc beta_r gamma_r/gamma_c, symmetrised into Wh
+#pragma unroll 1
+    for (int it = 0; it < 2; ++it) {
+        const int r = 16 * it + 2 * wave + (lane >> 5), c = lane & 31;
+        float bt = 0.f, wa = 0.f, sym = 0.f;
         if (r > c) {
-            const float f = ex(sm.G[r] - sm.G[c]) * sm.KK[r * LDF + c];
-            lds_add(&sm.dB[r], da * f);
-            const float wa = da * sm.bet[r] * f;
-            if (wa != 0.f) {
-                lds_add(&sm.dG[r], wa);
-                lds_add(&sm.dG[c], -wa);
-            }
-            sym = da * sm.bet[r] * ex(sm.G[r] - sm.G[c]);
+            const float da = sm.TdA[r * LDF + c], e = ex(sm.G[r] - sm.G[c]);
+            const float f = e * sm.KK[r * LDF + c];
+            bt = da * f;
+            wa = da * sm.bet[r] * f;
+            sym = da * sm.bet[r] * e;
         } else if (c > r) {
-            sym = sm.dA[c * LDF + r] * sm.bet[c] * ex(sm.G[c] - sm.G[r]);
+            sym = sm.TdA[c * LDF + r] * sm.bet[c] * ex(sm.G[c] - sm.G[r]);
         }
-        sm.W[r * LDF + c] = sym;
+        sm.Wh[r * LDM + c] = (_Float16)sym;
+        const float wc = wa + __shfl_xor(wa, 32);
+        const float br = half_sum(bt), wr = half_sum(wa);
+        if (c == 0) {
+            lds_add(&sm.dB[r], br);
+            lds_add(&sm.dG[r], wr);
+        }
+        if (lane < 32 && wc != 0.f) lds_add(&sm.dG[c], -wc);
     }
     __syncthreads();
-    // ---- dK = - Gamma dR S0^T + D Delta dS_n^T + [clean] (s E o Mc)^T Q + (dKK + dKK^T) K, with
-    // the R-gate term dG_r -= gamma_r sum_a K_ra (dR S0^T)_ra; then dg, dbeta
-    auto Wacc = [&sm](int r, int c) { return (_Float16)sm.W[r * LDF + c]; };
-#pragma unroll 1
-    for (int tm = 0; tm < 2; ++tm) {
-        f32x4 c = tile_mma<_Float16, DD>(z, sm.dR + 16 * tm * LDH, LDH, sm.S0 + 16 * wave * LDH, LDH, lane);
-        const f32x4 d2 = tile_mma<_Float16, DD>(z, sm.Dl + 16 * tm * LDH, LDH, sm.dS + 16 * wave * LDH, LDH, lane);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int r = 16 * tm + 4 * g4 + j, col = 16 * wave + rr;
-            float w = sm.gam[r] * c[j] * (float)sm.K[r * LDH + col];
-            w += __shfl_xor(w, 1);
-            w += __shfl_xor(w, 2);
-            w += __shfl_xor(w, 4);
-            w += __shfl_xor(w, 8);
-            if (rr == 0) lds_add(&sm.dG[r], -w);
-            c[j] = -sm.gam[r] * c[j] + ex(Gn - sm.G[r]) * d2[j];
-        }
+    // ---- dK = -Gamma dR S0^T + D Delta dS_n^T + [clean] (s E o Mc)^T Q + (dKK + dKK^T) K, with
+    // the R-gate term dG_r -= gamma_r sum_a K_ra (dR S0^T)_ra
+    {
+        const f16x4 k0q = op_tr(sm.K, LDH, 0, c0, lane), k1q = op_tr(sm.K, LDH, 16, c0, lane);
+        f16x4 q0q, q1q;
         if constexpr (CLEAN) {
-            auto dPmT = [&sm, s](int i, int r) {
-                return (_Float16)(i <= r ? s * sm.E[r * LDF + i] * ex(sm.G[r] - sm.G[i]) : 0.f);
-            };
-            c = mm_tile<NP>(c, 16 * tm, 16 * wave, dPmT, hq(sm.Q), lane);
+            q0q = op_tr(sm.Q, LDH, 0, c0, lane);
+            q1q = op_tr(sm.Q, LDH, 16, c0, lane);
         }
-        c = mm_tile<NP>(c, 16 * tm, 16 * wave, Wacc, hq(sm.K), lane);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int r = 16 * tm + 4 * g4 + j, col = 16 * wave + rr;
-            if (r < nvalid) {
-                float *dst = p.dk + (long)r * a.h_qk * DD + col;
-                if (a.atomic_qk)
-                    atomicAdd(dst, c[j]);
-                else
-                    *dst = c[j];
+        for (int tm = 0; tm < 2; ++tm) {
+            f32x4 c = tile_mma<_Float16, DD>(z, sm.dR + 16 * tm * LDH, LDH, sm.S0 + c0 * LDH, LDH, lane);
+            const f32x4 d2 = tile_mma<_Float16, DD>(z, sm.Dl + 16 * tm * LDH, LDH, sm.dS + c0 * LDH, LDH, lane);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = 16 * tm + 4 * g4 + j, col = c0 + rr;
+                const float w = sum16(c[j] * (float)sm.K[r * LDH + col]);
+                if (rr == 0) lds_add(&sm.dG[r], w);
+                c[j] += ex(Gn - sm.G[r]) * d2[j];
+            }
+            if constexpr (CLEAN)
+                c = mfma(op_tr(sm.dPh, LDM, 16, 16 * tm, lane), q1q, mfma(op_tr(sm.dPh, LDM, 0, 16 * tm, lane), q0q, c));
+            c = mfma(op_row(sm.Wh, LDM, 16 * tm, 16, lane), k1q, mfma(op_row(sm.Wh, LDM, 16 * tm, 0, lane), k0q, c));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = 16 * tm + 4 * g4 + j, col = c0 + rr;
+                if (r < nvalid) {
+                    float *dst = p.dk + (long)r * a.h_qk * DD + col;
+                    if (a.atomic_qk)
+                        atomicAdd(dst, c[j]);
+                    else
+                        *dst = c[j];
+                }
             }
         }
     }
@@ -514,9 +610,10 @@ template <typename Od>
 __device__ void clean_prep(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, float (&acc)[8][4],
                            _Float16 *uk, float *gnb, int tid)
 {
-    const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15;
+    const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
     const float s = a.scale;
     const long qks = (long)a.h_qk * DD, vs = (long)a.h_v * DD;
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
     stage_rows(sm.Q, p.q, qks, nvalid, tid);
     stage_rows(sm.K, p.k, qks, nvalid, tid);
     stage_rows(sm.dO, static_cast<const Od *>(p.dout), vs, nvalid, tid);
@@ -526,96 +623,70 @@ __device__ void clean_prep(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int 
         sm.G[tid] = ok ? p.g[(long)tid * a.h_v] : 0.f;
     }
     __syncthreads();
-    if (wave == 0) {
-        float x = lane < NP ? sm.G[lane] : 0.f;
-#pragma unroll
-        for (int o = 1; o < NP; o <<= 1) {
-            const float y = __shfl_up(x, o);
-            if (lane >= o) x += y;
-        }
-        if (lane < NP) {
-            sm.G[lane] = x;
-            sm.gam[lane] = ex(x);
-        }
-    }
+    if (wave == 0) cum_gates(sm, lane);
     __syncthreads();
     const float Gn = sm.G[NP - 1];
     if (tid == 0) *gnb = ex(Gn);
-    auto hq = [](const _Float16 *m) { return [m](int r, int c) { return m[r * LDH + c]; }; };
-    auto hqt = [](const _Float16 *m) { return [m](int r, int c) { return m[c * LDH + r]; }; };
-    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-    if (wave < 4) {   // KK, P = (Q K^T) o Mc
-        const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
-        const f32x4 kk = tile_mma<_Float16, DD>(z, sm.K + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
+    if (wave == 0) {   // M
+        solve_m(sm, lane);
+    } else if (wave >= 4) {   // P = (Q K^T) o Mc
+        const int m0 = 16 * ((wave - 4) >> 1), n0 = 16 * ((wave - 4) & 1);
         const f32x4 qk = tile_mma<_Float16, DD>(z, sm.Q + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int r = m0 + 4 * g4 + j, i = n0 + rr;
-            sm.KK[r * LDF + i] = kk[j];
-            sm.P[r * LDF + i] = i <= r ? qk[j] * ex(sm.G[r] - sm.G[i]) : 0.f;
+            sm.Ph[r * LDM + i] = (_Float16)(i <= r ? qk[j] * ex(sm.G[r] - sm.G[i]) : 0.f);
         }
     }
     __syncthreads();
-    for (int e = tid; e < NP * NP; e += 64 * kWaves) {
-        const int r = e / NP, i = e % NP;
-        sm.W[r * LDF + i] = i < r ? sm.bet[r] * ex(sm.G[r] - sm.G[i]) * sm.KK[r * LDF + i] : 0.f;
-    }
-    __syncthreads();
-    if (wave == 0 && lane < NP) {
-        const int c = lane;
-        float m[NP];
+    {   // Y = s P^T dO -> dDl
+        const f16x4 do0 = op_tr(sm.dO, LDH, 0, c0, lane), do1 = op_tr(sm.dO, LDH, 16, c0, lane);
 #pragma unroll
-        for (int r = 0; r < NP; ++r) {
-            float v = r == c ? 1.f : 0.f;
+        for (int tm = 0; tm < 2; ++tm) {
+            const f32x4 c =
+                mfma(op_tr(sm.Ph, LDM, 16, 16 * tm, lane), do1, mfma(op_tr(sm.Ph, LDM, 0, 16 * tm, lane), do0, z));
 #pragma unroll
-            for (int i = 0; i < r; ++i) v = fmaf(-sm.W[r * LDF + i], m[i], v);
-            m[r] = v;
+            for (int j = 0; j < 4; ++j) sm.dDl[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = (_Float16)(s * c[j]);
         }
-#pragma unroll
-        for (int r = 0; r < NP; ++r) sm.M[r * LDF + c] = m[r];
     }
-    __syncthreads();
-    // Y = s P^T dO -> dDl; U -> W (fp32)
-    auto Pt = [&sm](int r, int i) { return (_Float16)sm.P[i * LDF + r]; };
-#pragma unroll 1
-    for (int tm = 0; tm < 2; ++tm) {
-        const f32x4 c = mm_tile<NP>(z, 16 * tm, 16 * wave, Pt, hq(sm.dO), lane);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) sm.dDl[(16 * tm + 4 * g4 + j) * LDH + 16 * wave + rr] = (_Float16)(s * c[j]);
-    }
-    for (int e = tid; e < NP * NP; e += 64 * kWaves) {
+    for (int e = tid; e < NP * NP; e += 64 * kWaves) {   // U -> Wh
         const int i = e / NP, j = e % NP;
-        sm.W[i * LDF + j] = j >= i ? sm.M[j * LDF + i] * sm.bet[i] * ex(sm.G[i] + Gn - sm.G[j]) : 0.f;
+        sm.Wh[i * LDM + j] =
+            (_Float16)(j >= i ? (float)sm.Mh[j * LDM + i] * sm.bet[i] * ex(sm.G[i] + Gn - sm.G[j]) : 0.f);
     }
     __syncthreads();
-    // dR0 = T^T Y, kept as -Gamma dR0 (f16) in dR; dO rescaled in place to s Gamma dO; U K -> uk
-    auto Tt = [&sm](int i, int r) { return (_Float16)(sm.M[r * LDF + i] * sm.bet[i]); };
-    auto Ua = [&sm](int i, int j) { return (_Float16)sm.W[i * LDF + j]; };
-#pragma unroll 1
-    for (int tm = 0; tm < 2; ++tm) {
-        const f32x4 c = mm_tile<NP>(z, 16 * tm, 16 * wave, Tt, hq(sm.dDl), lane);
-        const f32x4 u = mm_tile<NP>(z, 16 * tm, 16 * wave, Ua, hq(sm.K), lane);
+    // dR0 = T^T Y, as -Gamma dR0 in registers (B operands); acc += K^T (-Gamma dR0) + Q^T (s Gamma dO)
+    f16x4 drq[2], sd[2];
+    {
+        const f16x4 y0 = op_tr(sm.dDl, LDH, 0, c0, lane), y1 = op_tr(sm.dDl, LDH, 16, c0, lane);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int r = 16 * tm + 4 * g4 + j, col = 16 * wave + rr;
-            sm.dR[r * LDH + col] = (_Float16)(-sm.gam[r] * c[j]);
-            uk[r * DD + col] = (_Float16)u[j];
+        for (int tm = 0; tm < 2; ++tm) {
+            f16x4 t0, t1;
+            tt_ops(sm, tm, lane, t0, t1);
+            const f32x4 c = mfma(t1, y1, mfma(t0, y0, z));
+            const f32x4 gm = ld4(sm.gam + 16 * tm + 4 * g4);
+            drq[tm] = h4(-gm * c);
+            // s Gamma dO: the transpose loads of dO scaled by s gamma of their rows
+            sd[tm] = scale4(op_tr(sm.dO, LDH, 16 * tm, c0, lane), s * gm);
         }
     }
-    {
-        const int r = tid >> 4, c = (tid & 15) * 8;
-        const float f = s * sm.gam[r];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) sm.dO[r * LDH + c + j] = (_Float16)(f * (float)sm.dO[r * LDH + c + j]);
-    }
-    __syncthreads();
-    // acc += K^T (-Gamma dR0) + Q^T (s Gamma dO)
 #pragma unroll
     for (int tm = 0; tm < 8; ++tm) {
-        f32x4 c = mm_tile<NP>(z, 16 * tm, 16 * wave, hqt(sm.K), hq(sm.dR), lane);
-        c = mm_tile<NP>(c, 16 * tm, 16 * wave, hqt(sm.Q), hq(sm.dO), lane);
+        f32x4 c = mfma(op_tr(sm.K, LDH, 0, 16 * tm, lane), drq[0], z);
+        c = mfma(op_tr(sm.K, LDH, 16, 16 * tm, lane), drq[1], c);
+        c = mfma(op_tr(sm.Q, LDH, 0, 16 * tm, lane), sd[0], c);
+        c = mfma(op_tr(sm.Q, LDH, 16, 16 * tm, lane), sd[1], c);
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[tm][j] += c[j];
+    }
+    {   // U K -> uk
+        const f16x4 k0q = op_tr(sm.K, LDH, 0, c0, lane), k1q = op_tr(sm.K, LDH, 16, c0, lane);
+#pragma unroll
+        for (int tm = 0; tm < 2; ++tm) {
+            const f32x4 u = mfma(op_row(sm.Wh, LDM, 16 * tm, 16, lane), k1q, mfma(op_row(sm.Wh, LDM, 16 * tm, 0, lane), k0q, z));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) uk[(16 * tm + 4 * g4 + j) * DD + c0 + rr] = (_Float16)u[j];
+        }
     }
     __syncthreads();
 }
@@ -643,7 +714,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[tm][j] = 0.f;
     __syncthreads();
-    block_bwd<false, true, Od>(sm, stream_ptrs<Od>(a, true, p0, h, hq), a, nvalid, acc, acc, tid);
+    block_bwd<false, Od>(sm, stream_ptrs<Od>(a, true, p0, h, hq), a, nvalid, acc, acc, tid);
     clean_prep<Od>(sm, stream_ptrs<Od>(a, false, p0, h, hq), a, nvalid, acc, a.uk + unit * NP * DD, a.gnb + unit,
                    tid);
     float *dst = a.cterm + so;
@@ -679,7 +750,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
             sm.dS[r * LDH + c] = (_Float16)dsn[tm][j];
         }
     __syncthreads();
-    block_bwd<true, false, Od>(sm, stream_ptrs<Od>(a, false, p0, h, hq), a, nvalid, dsn, dsn, tid);
+    block_bwd<true, Od>(sm, stream_ptrs<Od>(a, false, p0, h, hq), a, nvalid, dsn, dsn, tid);
 }
 
 // Phase 2: the reverse scan of the clean state gradient over the blocks of a (sequence,

@@ -104,8 +104,9 @@ __device__ __forceinline__ f16x4 and_mask(f16x4 q, const unsigned (&m)[2])
 // so each lane writes four consecutive entries of a row.  Masked entries are selected, not
 // branched on.  With log-gates g <= 0 the cumulative G is non-increasing, so every decay
 // exponent kept (G_r - G_c, r >= c) is <= 0 and is evaluated as -|G_r - G_c|, which also
-// keeps the discarded entries finite.
-template <int NB, int DKB>
+// keeps the discarded entries finite.  With BETA = false the inverse M = (I + A)^(-1) itself
+// is written instead of T (the backward needs M where a step size is zero).
+template <int NB, int DKB, bool BETA = true>
 __device__ __forceinline__ void solve_t(const QE (&kq)[NB][DKB], const float *Gs, const float *Bs, E *T, int ts,
                                         const Consts &us_, int lane)
 {
@@ -138,7 +139,10 @@ __device__ __forceinline__ void solve_t(const QE (&kq)[NB][DKB], const float *Gs
     // T tile (bi, bj) from the accumulator of its transpose X_(bi, bj)^T (times beta of the
     // columns)
     auto put = [&](int bi, int bj, f32x4 xt) {
-        st_quad(T + (16 * bi + n) * ts + 16 * bj + 4 * g, quad_of<E>(xt * br[bj]));
+        if constexpr (BETA)
+            st_quad(T + (16 * bi + n) * ts + 16 * bj + 4 * g, quad_of<E>(xt * br[bj]));
+        else
+            st_quad(T + (16 * bi + n) * ts + 16 * bj + 4 * g, quad_of<E>(xt));
     };
     // diagonal tiles of A (below the diagonal) and A^T (above): one exponent serves both
     f32x4 D[NB], Dt[NB];
