@@ -230,7 +230,7 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         if (desc->route == BDGDN_ROUTE_SPLIT) {
             NoisyArgs na;
             na.qn = qn; na.kn = kn; na.vn = vn; na.gn = gn; na.betan = betan;
-            na.bs = sa.bs;
+            na.bs = static_cast<const float *>(sa.bs);
             na.cu = sa.cu;
             na.on = on;
             na.T = desc->seqlen; na.L = desc->block; na.nblk = ia.nblk;
@@ -450,7 +450,7 @@ int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc, const void *q, const voi
         NoisyArgs na = {};
         na.qn = views[i].q; na.kn = views[i].k; na.vn = views[i].v;
         na.gn = views[i].g; na.betan = views[i].beta;
-        na.bs = sa.bs;
+        na.bs = static_cast<const float *>(sa.bs);
         na.cu = sa.cu;
         na.on = views[i].o;
         na.T = desc->seqlen; na.L = desc->block; na.nblk = sa.nblk;
@@ -472,19 +472,26 @@ static bool bwd_shape_ok(const bdgdn_fwd_desc_t *d)
     return d->dtype == BDGDN_BF16 && d->d_k == 128 && d->d_v == 128 && d->block <= 32;
 }
 
-static size_t bwd_seed_bytes(const bdgdn_fwd_desc_t *d)
+// Workspace of the backward, per (global block, v-head): the seed state (fp16), the part of
+// the state gradient at the block's start that does not depend on dh (fp32), dh at the
+// block's end (fp32), U K (32 x d_k, fp16), gamma_n (fp32); then the recomputing scan's clean
+// outputs (bf16, not read).  Byte offsets, each aligned to 256.
+struct BwdLayout {
+    size_t seeds, cterm, dh, uk, gnb, o, total;
+};
+static BwdLayout bwd_layout(const bdgdn_fwd_desc_t *d)
 {
-    return ((size_t)total_blocks(d) * d->h_v * d->d_k * d->d_v * sizeof(float) + 255) & ~(size_t)255;
-}
-
-// U K (32 x d_k, fp16) and gamma_n (fp32) of every clean (block, v-head), for the reverse scan.
-static size_t bwd_uk_bytes(const bdgdn_fwd_desc_t *d)
-{
-    return ((size_t)total_blocks(d) * d->h_v * 32 * d->d_k * 2 + 255) & ~(size_t)255;
-}
-static size_t bwd_gn_bytes(const bdgdn_fwd_desc_t *d)
-{
-    return ((size_t)total_blocks(d) * d->h_v * sizeof(float) + 255) & ~(size_t)255;
+    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    const size_t units = (size_t)total_blocks(d) * d->h_v, st = (size_t)d->d_k * d->d_v;
+    BwdLayout l;
+    l.seeds = 0;
+    l.cterm = l.seeds + up(units * st * 2);
+    l.dh = l.cterm + up(units * st * 4);
+    l.uk = l.dh + up(units * st * 4);
+    l.gnb = l.uk + up(units * 32 * d->d_k * 2);
+    l.o = l.gnb + up(units * 4);
+    l.total = l.o + (size_t)d->batch * d->seqlen * d->h_v * d->d_v * 2;
+    return l;
 }
 
 size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc)
@@ -493,8 +500,7 @@ size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc)
                              desc->out_dtype) != BDGDN_OK)
         return 0;
     if (desc->batch <= 0 || desc->seqlen <= 0 || !bwd_shape_ok(desc)) return 0;
-    const size_t rows = (size_t)desc->batch * desc->seqlen;
-    return 3 * bwd_seed_bytes(desc) + bwd_uk_bytes(desc) + bwd_gn_bytes(desc) + rows * desc->h_v * desc->d_v * 2;
+    return bwd_layout(desc).total;
 }
 
 int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, const void *v,
@@ -523,14 +529,16 @@ int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     const int nseq = packed ? desc->num_seqs : desc->batch;
     const hipStream_t strm = static_cast<hipStream_t>(stream);
     unsigned char *ws = static_cast<unsigned char *>(workspace);
-    float *seeds = reinterpret_cast<float *>(ws);
-    // 1. the clean scan from h0, writing the seed state of every block
+    const BwdLayout lay = bwd_layout(desc);
+    _Float16 *seeds = reinterpret_cast<_Float16 *>(ws + lay.seeds);
+    // 1. the clean scan from h0, writing the seed state of every block (fp16: the block
+    // kernels stage it as fp16 MFMA operands)
     ScanArgs sa = {};
     sa.q = q; sa.k = k; sa.v = v; sa.qn = qn; sa.kn = kn; sa.vn = vn;
     sa.g = g; sa.beta = beta; sa.gn = gn; sa.betan = betan;
     sa.cu = packed ? cu_seqlens_dev : nullptr;
     sa.h0 = h0; sa.ht = nullptr;
-    sa.o = ws + 3 * bwd_seed_bytes(desc) + bwd_uk_bytes(desc) + bwd_gn_bytes(desc); sa.on = nullptr;
+    sa.o = ws + lay.o; sa.on = nullptr;
     sa.ws = nullptr;
     sa.bs = seeds;
     sa.T = desc->seqlen; sa.L = desc->block; sa.nblk = (desc->seqlen + desc->block - 1) / desc->block;
@@ -548,7 +556,7 @@ int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         for (int i = 0; i < nseq; ++i) sa.order[i] = idx[i];
         sa.n_order = nseq;
     }
-    hipError_t e = launch_scan_states(lp_of(desc->block), false, sa, strm);
+    hipError_t e = launch_scan_states(lp_of(desc->block), false, true, sa, strm);
     if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
     // 2. the reverse walk over the blocks of every (sequence, v-head)
     BwdArgs a = {};
@@ -559,12 +567,13 @@ int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     a.dq = dq; a.dk = dk; a.dv = dv; a.dg = dg; a.db = dbeta;
     a.dqn = dqn; a.dkn = dkn; a.dvn = dvn; a.dgn = dgn; a.dbn = dbetan;
     a.dh0 = dh0;
-    a.cterm = reinterpret_cast<float *>(ws + bwd_seed_bytes(desc));
-    a.dh = reinterpret_cast<float *>(ws + 2 * bwd_seed_bytes(desc));
-    a.uk = reinterpret_cast<_Float16 *>(ws + 3 * bwd_seed_bytes(desc));
-    a.gnb = reinterpret_cast<float *>(ws + 3 * bwd_seed_bytes(desc) + bwd_uk_bytes(desc));
+    a.cterm = reinterpret_cast<float *>(ws + lay.cterm);
+    a.dh = reinterpret_cast<float *>(ws + lay.dh);
+    a.uk = reinterpret_cast<_Float16 *>(ws + lay.uk);
+    a.gnb = reinterpret_cast<float *>(ws + lay.gnb);
     a.cu = sa.cu;
     a.n_docs = packed ? nseq : 0;
+    a.n_chains = nseq * desc->h_v;
     a.T = desc->seqlen; a.nblk = sa.nblk; a.L = desc->block;
     a.h_qk = desc->h_qk; a.h_v = desc->h_v;
     a.scale = desc->scale;

@@ -16,7 +16,7 @@ struct BwdArgs {
     const void *q, *k, *v, *qn, *kn, *vn;   // bf16 [rows][heads][128]
     const float *g, *beta, *gn, *betan;      // [rows][h_v]
     const void *dout, *doutn;                // [rows][h_v][128] of the output type
-    const float *seeds;                      // [global block][h_v][128][128]
+    const _Float16 *seeds;                   // [global block][h_v][128][128] fp16
     const float *dht;                        // [seq][h_v][128][128] or null
     float *dq, *dk, *dv, *dg, *db;
     float *dqn, *dkn, *dvn, *dgn, *dbn;
@@ -29,6 +29,7 @@ struct BwdArgs {
     float *dh;                               // [global block][h_v][128][128]: gradient at block ends
     const int32_t *cu;                       // packed documents, or null
     int n_docs;
+    int n_chains;                            // sequences x v-heads
     int T, nblk, L, h_qk, h_v;
     float scale;
     bool atomic_qk;

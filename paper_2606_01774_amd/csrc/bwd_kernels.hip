@@ -61,6 +61,7 @@ struct Smem {
     float TdA[NP * LDF];         // T (T_ci = M_ci beta_i at [c][i]), later dA
     float Mt[NP * LDF];          // M^T (fp32)
     float G[NP], G2[NP], gam[NP], bet[NP], dG[NP], dB[NP];   // G2: cumulative log2-gates
+    float part[kWaves][NP];      // per-wave partial sums of the row gate terms
 };
 static_assert(sizeof(Smem) <= 160 * 1024, "one workgroup's LDS");
 
@@ -105,44 +106,103 @@ __device__ __forceinline__ float ex(float x) { return __expf(x); }
 // Workgroup sum of v added to *dst (LDS), from every thread.
 __device__ __forceinline__ void lds_add(float *dst, float v) { atomicAdd(dst, v); }
 
-__device__ __forceinline__ float wave_sum(float v)
+// Sum over the 16 lanes of each lane row (the columns of a C tile row), by DPP row shifts:
+// valid in lane 15 of the row.
+__device__ __forceinline__ float row_total(float v)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    v += ut::dpp<0x111>(v);
+    v += ut::dpp<0x112>(v);
+    v += ut::dpp<0x114>(v);
+    v += ut::dpp<0x118>(v);
     return v;
 }
-// Sum over the 16 lanes of a lane group (the columns of a C tile row).
-__device__ __forceinline__ float sum16(float v)
+// Sums over lanes 0 .. 31 and 32 .. 63, each returned to the lanes of its half.
+__device__ __forceinline__ float half_total(float v, int lane)
 {
-#pragma unroll
-    for (int o = 8; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
+    const float t = row_total(v);
+    const float h0 = ut::lane_value(t, 15) + ut::lane_value(t, 31);
+    const float h1 = ut::lane_value(t, 47) + ut::lane_value(t, 63);
+    return lane < 32 ? h0 : h1;
 }
-// Row sums (over the 32 lanes of each half-wave) of a 32 x 32 fp32 term laid out as row
-// 2 w + lane / 32 (+ 16 it), column lane % 32.
-__device__ __forceinline__ float half_sum(float v)
+__device__ __forceinline__ float wave_total(float v)
 {
-#pragma unroll
-    for (int o = 16; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
+    const float t = row_total(v);
+    return (ut::lane_value(t, 15) + ut::lane_value(t, 31)) + (ut::lane_value(t, 47) + ut::lane_value(t, 63));
 }
 
-template <typename In> __device__ __forceinline__ void stage_rows(_Float16 *dst, const In *src, long stride, int nvalid,
-                                                                 int tid)
-{
-    // 32 rows x 128 values, 8 per thread
-    const int r = tid >> 4, c = (tid & 15) * 8;
-    _Float16 h[8];
-    if (r < nvalid) {
-        const In *p = src + (long)r * stride + c;
+// One thread's share of a 32 x 128 row block (row tid / 16, the 8 values from 8 (tid % 16)),
+// loaded into registers ahead of its store to LDS as fp16, so that all loads of a unit are
+// in flight together.
+template <typename In> struct Row8;
+template <> struct Row8<__bf16> {
+    bf16x8 v;
+    __device__ __forceinline__ void load(const __bf16 *p) { v = *reinterpret_cast<const bf16x8 *>(p); }
+    __device__ __forceinline__ void zero()
+    {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) h[j] = (_Float16)to_f(p[j]);
-    } else {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) h[j] = (_Float16)0.f;
+        for (int j = 0; j < 8; ++j) v[j] = (__bf16)0.f;
     }
+    __device__ __forceinline__ f16x8 h() const
+    {
+        f16x8 r;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) dst[r * LDH + c + j] = h[j];
+        for (int j = 0; j < 8; ++j) r[j] = (_Float16)(float)v[j];
+        return r;
+    }
+};
+template <> struct Row8<float> {
+    f32x4 lo, hi;
+    __device__ __forceinline__ void load(const float *p)
+    {
+        lo = ld4(p);
+        hi = ld4(p + 4);
+    }
+    __device__ __forceinline__ void zero() { lo = hi = f32x4{0.f, 0.f, 0.f, 0.f}; }
+    __device__ __forceinline__ f16x8 h() const
+    {
+        f16x8 r;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            r[j] = (_Float16)lo[j];
+            r[4 + j] = (_Float16)hi[j];
+        }
+        return r;
+    }
+};
+template <typename In> __device__ __forceinline__ Row8<In> load_rows(const In *src, long stride, int nvalid, int tid)
+{
+    const int r = tid >> 4, c = (tid & 15) * 8;
+    Row8<In> x;
+    if (r < nvalid)
+        x.load(src + (long)r * stride + c);
+    else
+        x.zero();
+    return x;
+}
+template <typename In> __device__ __forceinline__ void store_rows(_Float16 *dst, const Row8<In> &x, int tid)
+{
+    const int r = tid >> 4, c = (tid & 15) * 8;
+    *reinterpret_cast<f16x8 *>(dst + r * LDH + c) = x.h();
+}
+
+// The fp16 seed state (128 x 128, 32 KB): four 16-byte pieces per thread.
+struct SeedRegs {
+    f16x8 v[4];
+};
+__device__ __forceinline__ SeedRegs load_seed(const _Float16 *src, int tid)
+{
+    SeedRegs x;
+#pragma unroll
+    for (int it = 0; it < 4; ++it) x.v[it] = *reinterpret_cast<const f16x8 *>(src + (tid + 512 * it) * 8);
+    return x;
+}
+__device__ __forceinline__ void store_seed(_Float16 *dst, const SeedRegs &x, int tid)
+{
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const int e = (tid + 512 * it) * 8;
+        *reinterpret_cast<f16x8 *>(dst + (e / DD) * LDH + e % DD) = x.v[it];
+    }
 }
 
 // Block-local cumulative log-gates G (and G2 = G log2 e) and gamma = exp G, by wave 0 (a
@@ -195,6 +255,28 @@ struct StreamPtrs {
     float *dq, *dk, *dv, *dg, *db;   // first row of the gradients
 };
 
+// A block's inputs in registers (V only with WITH_V); g, b: the gate and step size of
+// position tid (tid < 32).
+template <typename Od, bool WITH_V> struct BlockRows {
+    Row8<__bf16> q, k, v;
+    Row8<Od> dout;
+    float g, b;
+};
+template <typename Od, bool WITH_V>
+__device__ __forceinline__ BlockRows<Od, WITH_V> load_block(const StreamPtrs &p, int h_qk, int h_v, int nvalid, int tid)
+{
+    const long qks = (long)h_qk * DD, vs = (long)h_v * DD;
+    BlockRows<Od, WITH_V> x;
+    x.q = load_rows(p.q, qks, nvalid, tid);
+    x.k = load_rows(p.k, qks, nvalid, tid);
+    if constexpr (WITH_V) x.v = load_rows(p.v, vs, nvalid, tid);
+    x.dout = load_rows(static_cast<const Od *>(p.dout), vs, nvalid, tid);
+    const bool ok = tid < NP && tid < nvalid;
+    x.g = ok ? p.g[(long)tid * h_v] : 0.f;
+    x.b = ok ? p.beta[(long)tid * h_v] : 0.f;
+    return x;
+}
+
 }  // namespace
 
 // One block's gradients.  S0 (LDS f16) holds the seed.  For the clean stream dS (LDS, f16)
@@ -204,22 +286,25 @@ struct StreamPtrs {
 // layout).  Wave w computes the 16 columns 16 w .. 16 w + 15 of every 32 x 128 and 128 x 128
 // product.
 template <bool CLEAN, typename Od>
-__device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, const float (&dsn)[8][4],
-                          float (&acc)[8][4], int tid)
+__device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, const BlockRows<Od, true> &in,
+                          const float (&dsn)[8][4], float (&acc)[8][4], int tid)
 {
     const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
     const float s = a.scale;
-    const long qks = (long)a.h_qk * DD, vs = (long)a.h_v * DD;
+    const long vs = (long)a.h_v * DD;
     const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    // This lane's shares of the gate gradients that are sums over a row of a 32 x 128 product:
+    // rowg[tm][j] for row 16 tm + 4 g + j (this lane's column), dlast for the last position;
+    // reduced once, at the end.
+    float rowg[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}}, dlast = 0.f;
     // ---- stage rows and gates
-    stage_rows(sm.Q, p.q, qks, nvalid, tid);
-    stage_rows(sm.K, p.k, qks, nvalid, tid);
-    stage_rows(sm.R, p.v, vs, nvalid, tid);   // V, becomes R below
-    stage_rows(sm.dO, static_cast<const Od *>(p.dout), vs, nvalid, tid);
+    store_rows(sm.Q, in.q, tid);
+    store_rows(sm.K, in.k, tid);
+    store_rows(sm.R, in.v, tid);   // V, becomes R below
+    store_rows(sm.dO, in.dout, tid);
     if (tid < NP) {
-        const bool ok = tid < nvalid;
-        sm.bet[tid] = ok ? p.beta[(long)tid * a.h_v] : 0.f;
-        sm.G[tid] = ok ? p.g[(long)tid * a.h_v] : 0.f;
+        sm.bet[tid] = in.b;
+        sm.G[tid] = in.g;
         sm.dG[tid] = 0.f;
         sm.dB[tid] = 0.f;
     }
@@ -289,8 +374,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
                 wg += c[j] * (float)s0q[tm][j];
             }
         }
-        wg = wave_sum(wg);
-        if (lane == 0) lds_add(&sm.dG[NP - 1], gn * wg);
+        dlast += gn * wg;
     }
     __syncthreads();
     // ---- Delta = T R (T_ri = M_ri beta_i); fp32 copies of T and M^T for the dA products
@@ -326,8 +410,10 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
                 const float dec = i <= r ? ex(sm.G[r] - sm.G[i]) : 0.f;
                 sm.dPh[r * LDM + i] = (_Float16)(s * e4[j] * dec);
                 const float w = s * e4[j] * (float)sm.Ph[r * LDM + i];
-                const float wr = sum16(w);
-                if (rr == 0) lds_add(&sm.dG[r], wr);
+                if (wave >> 1)
+                    rowg[1][j] += w;
+                else
+                    rowg[0][j] += w;
                 colw += w;
             } else {
                 sm.dPh[r * LDM + i] = (_Float16)(s * e4[j] * ex(Gn - sm.G[i]));
@@ -360,11 +446,9 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
                 const int r = 16 * tm + 4 * g4 + j, c = c0 + rr;
                 const float Dr = ex(Gn - sm.G[r]);
                 sm.dDl[r * LDH + c] = (_Float16)(s * pd[j] + Dr * kds[j]);
-                const float w = sum16(Dr * kds[j] * (float)sm.Dl[r * LDH + c]);
-                if (rr == 0) {
-                    lds_add(&sm.dG[r], -w);
-                    lds_add(&sm.dG[NP - 1], w);
-                }
+                const float w = Dr * kds[j] * (float)sm.Dl[r * LDH + c];
+                rowg[tm][j] -= w;
+                dlast += w;
             }
         }
     }
@@ -410,8 +494,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
                 const int r = 16 * tm + 4 * g4 + j, col = c0 + rr;
                 if constexpr (CLEAN) {
                     // gate term of Gamma Q S0: dG_r += s gamma_r sum_a Q_ra (dO S0^T)_ra
-                    const float w = sum16(s * sm.gam[r] * c[j] * (float)sm.Q[r * LDH + col]);
-                    if (rr == 0) lds_add(&sm.dG[r], w);
+                    rowg[tm][j] += s * sm.gam[r] * c[j] * (float)sm.Q[r * LDH + col];
                     c[j] *= s * sm.gam[r];
                 } else {
                     c[j] *= s * gn;
@@ -480,7 +563,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
         }
         sm.Wh[r * LDM + c] = (_Float16)sym;
         const float wc = wa + __shfl_xor(wa, 32);
-        const float br = half_sum(bt), wr = half_sum(wa);
+        const float br = half_total(bt, lane), wr = half_total(wa, lane);
         if (c == 0) {
             lds_add(&sm.dB[r], br);
             lds_add(&sm.dG[r], wr);
@@ -504,8 +587,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int r = 16 * tm + 4 * g4 + j, col = c0 + rr;
-                const float w = sum16(c[j] * (float)sm.K[r * LDH + col]);
-                if (rr == 0) lds_add(&sm.dG[r], w);
+                rowg[tm][j] += c[j] * (float)sm.K[r * LDH + col];
                 c[j] += ex(Gn - sm.G[r]) * d2[j];
             }
             if constexpr (CLEAN)
@@ -524,9 +606,25 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
             }
         }
     }
+    {   // the row gate terms: this wave's partial sums
+        const float dl = wave_total(dlast);
+#pragma unroll
+        for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = 16 * tm + 4 * g4 + j;
+                const float t = row_total(rowg[tm][j]);
+                if (rr == 15) sm.part[wave][r] = r == NP - 1 ? t + dl : t;
+            }
+    }
     __syncthreads();
     if (wave == 0) {   // dg = reverse cumulative sum of dG (a 32-lane scan)
-        float x = lane < NP ? sm.dG[lane] : 0.f;
+        float x = 0.f;
+        if (lane < NP) {
+            x = sm.dG[lane];
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) x += sm.part[w][lane];
+        }
 #pragma unroll
         for (int o = 1; o < NP; o <<= 1) {
             const float y = __shfl_down(x, o);
@@ -587,17 +685,6 @@ __device__ __forceinline__ StreamPtrs stream_ptrs(const BwdArgs &a, bool noisy, 
     return p;
 }
 
-// Stage a fp32 state (seed) as f16 into LDS.
-__device__ __forceinline__ void stage_state(_Float16 *dst, const float *src, int tid)
-{
-    for (int e = tid * 4; e < DD * DD; e += 512 * 4) {
-        const f32x4 v = *reinterpret_cast<const f32x4 *>(src + e);
-        const int r = e / DD, c = e % DD;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) dst[r * LDH + c + j] = (_Float16)v[j];
-    }
-}
-
 }  // namespace
 
 // The part of a clean block's contribution to the state gradient at its start that does not
@@ -607,20 +694,18 @@ __device__ __forceinline__ void stage_state(_Float16 *dst, const float *src, int
 // gamma_i gamma_n / gamma_j, upper triangular with |U_ij| <= |T_ji|) goes to uk and gamma_n to
 // *gnb for the reverse scan.
 template <typename Od>
-__device__ void clean_prep(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, float (&acc)[8][4],
+__device__ void clean_prep(Smem &sm, const BwdArgs &a, const BlockRows<Od, false> &in, float (&acc)[8][4],
                            _Float16 *uk, float *gnb, int tid)
 {
     const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
     const float s = a.scale;
-    const long qks = (long)a.h_qk * DD, vs = (long)a.h_v * DD;
     const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-    stage_rows(sm.Q, p.q, qks, nvalid, tid);
-    stage_rows(sm.K, p.k, qks, nvalid, tid);
-    stage_rows(sm.dO, static_cast<const Od *>(p.dout), vs, nvalid, tid);
+    store_rows(sm.Q, in.q, tid);
+    store_rows(sm.K, in.k, tid);
+    store_rows(sm.dO, in.dout, tid);
     if (tid < NP) {
-        const bool ok = tid < nvalid;
-        sm.bet[tid] = ok ? p.beta[(long)tid * a.h_v] : 0.f;
-        sm.G[tid] = ok ? p.g[(long)tid * a.h_v] : 0.f;
+        sm.bet[tid] = in.b;
+        sm.G[tid] = in.g;
     }
     __syncthreads();
     if (wave == 0) cum_gates(sm, lane);
@@ -707,16 +792,20 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
     long p0;
     block_unit(a, gblk, n, p0, nvalid);
     const size_t unit = (size_t)gblk * a.h_v + h, so = unit * DD * DD;
-    stage_state(sm.S0, a.seeds + so, tid);
+    const StreamPtrs pc = stream_ptrs<Od>(a, false, p0, h, hq), pn = stream_ptrs<Od>(a, true, p0, h, hq);
+    // every load of the unit in flight together: the clean rows (the clean prep runs first;
+    // it needs no seed), the seed, the noisy rows
+    const BlockRows<Od, false> cin = load_block<Od, false>(pc, a.h_qk, a.h_v, nvalid, tid);
+    const SeedRegs seed = load_seed(a.seeds + so, tid);
+    const BlockRows<Od, true> nin = load_block<Od, true>(pn, a.h_qk, a.h_v, nvalid, tid);
     float acc[8][4];
 #pragma unroll
     for (int tm = 0; tm < 8; ++tm)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[tm][j] = 0.f;
-    __syncthreads();
-    block_bwd<false, Od>(sm, stream_ptrs<Od>(a, true, p0, h, hq), a, nvalid, acc, acc, tid);
-    clean_prep<Od>(sm, stream_ptrs<Od>(a, false, p0, h, hq), a, nvalid, acc, a.uk + unit * NP * DD, a.gnb + unit,
-                   tid);
+    clean_prep<Od>(sm, a, cin, acc, a.uk + unit * NP * DD, a.gnb + unit, tid);
+    store_seed(sm.S0, seed, tid);   // made visible by block_bwd's first barrier
+    block_bwd<false, Od>(sm, pn, a, nvalid, nin, acc, acc, tid);
     float *dst = a.cterm + so;
 #pragma unroll
     for (int tm = 0; tm < 8; ++tm)
@@ -738,23 +827,25 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
     long p0;
     block_unit(a, gblk, n, p0, nvalid);
     const size_t so = ((size_t)gblk * a.h_v + h) * DD * DD;
-    stage_state(sm.S0, a.seeds + so, tid);
+    const StreamPtrs pc = stream_ptrs<Od>(a, false, p0, h, hq);
+    const SeedRegs seed = load_seed(a.seeds + so, tid);
     float dsn[8][4];
     const float *dh = a.dh + so;
 #pragma unroll
     for (int tm = 0; tm < 8; ++tm)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int r = 16 * tm + 4 * g4 + j, c = 16 * wave + rr;
-            dsn[tm][j] = dh[r * DD + c];
-            sm.dS[r * LDH + c] = (_Float16)dsn[tm][j];
-        }
-    __syncthreads();
-    block_bwd<true, Od>(sm, stream_ptrs<Od>(a, false, p0, h, hq), a, nvalid, dsn, dsn, tid);
+        for (int j = 0; j < 4; ++j) dsn[tm][j] = dh[(16 * tm + 4 * g4 + j) * DD + 16 * wave + rr];
+    const BlockRows<Od, true> in = load_block<Od, true>(pc, a.h_qk, a.h_v, nvalid, tid);
+    store_seed(sm.S0, seed, tid);
+#pragma unroll
+    for (int tm = 0; tm < 8; ++tm)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sm.dS[(16 * tm + 4 * g4 + j) * LDH + 16 * wave + rr] = (_Float16)dsn[tm][j];
+    block_bwd<true, Od>(sm, pc, a, nvalid, in, dsn, dsn, tid);   // its first barrier covers S0, dS
 }
 
 // Phase 2: the reverse scan of the clean state gradient over the blocks of a (sequence,
-// v-head), one workgroup of 4 waves per 32 columns (the columns are independent):
+// v-head) (a chain), one workgroup of 4 waves per 32 columns (the columns are independent):
 //   dh_(b-1) = gamma_n dh_b + cterm_b - K^T Z,  Z = (U K) dh_b  (32 x 32),
 // writing dh_b (the gradient at the end of block b) for phase 3, and dh0.  The operands of
 // block b - 1 (U K, K, cterm, gamma_n) are loaded into registers while block b is computed.
@@ -772,7 +863,11 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
 {
     __shared__ __align__(16) ScanSmem sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15;
-    const int chain = blockIdx.x >> 2, v0 = 32 * (blockIdx.x & 3);
+    // the 4 column tiles of a chain on one XCD (workgroups are dealt to the 8 XCDs in turn),
+    // so that they read its U K and K rows through one L2
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int chain = (slot >> 2) * 8 + xcd, v0 = 32 * (slot & 3);
+    if (chain >= a.n_chains) return;
     const int n = chain / a.h_v, h = chain % a.h_v, hq = h / (a.h_v / a.h_qk);
     long r0, r1;
     if (a.cu) {
@@ -797,25 +892,29 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
                 dh[tl][tn][j] = dht ? dht[(32 * wave + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] : 0.f;
     // staging map of the 32 x 128 operands: row tid / 8, 16 columns from 16 (tid % 8)
     const int sr = tid >> 3, sc = (tid & 7) * 16;
-    f16x8 ukr[2];
-    bf16x8 kr[2];
-    float cs[2][2][4], gnv = 0.f;
-    auto fetch = [&](int b) {
+    // one block's operands in registers; two sets alternate so that the loads for block
+    // b - 1 are in flight while block b is computed (and no register copy waits on them)
+    struct Ops {
+        f16x8 uk[2];
+        bf16x8 k[2];
+        float cs[2][2][4], gn;
+    };
+    auto fetch = [&](int b, Ops &o) {
         const long p0 = r0 + (long)b * a.L;
         const int nvalid = (int)(r1 - p0 < a.L ? r1 - p0 : a.L);
         const long gblk = a.cu ? p0 / a.L : (long)n * a.nblk + b;
         const size_t unit = (size_t)gblk * a.h_v + h;
         const f16x8 *u = reinterpret_cast<const f16x8 *>(a.uk + unit * NP * DD + sr * DD + sc);
-        ukr[0] = u[0];
-        ukr[1] = u[1];
+        o.uk[0] = u[0];
+        o.uk[1] = u[1];
         if (sr < nvalid) {
             const bf16x8 *k = reinterpret_cast<const bf16x8 *>(static_cast<const __bf16 *>(a.k) + (p0 + sr) * qks +
                                                                hq * DD + sc);
-            kr[0] = k[0];
-            kr[1] = k[1];
+            o.k[0] = k[0];
+            o.k[1] = k[1];
         } else {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) kr[0][j] = kr[1][j] = (__bf16)0.f;
+            for (int j = 0; j < 8; ++j) o.k[0][j] = o.k[1][j] = (__bf16)0.f;
         }
         const float *c = a.cterm + unit * SS;
 #pragma unroll
@@ -824,16 +923,16 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
             for (int tn = 0; tn < 2; ++tn)
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    cs[tl][tn][j] = c[(32 * wave + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr];
-        gnv = a.gnb[unit];
+                    o.cs[tl][tn][j] = c[(32 * wave + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr];
+        o.gn = a.gnb[unit];
     };
     const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-    if (nb > 0) fetch(nb - 1);
-    for (int b = nb - 1; b >= 0; --b) {
+    auto step = [&](int b, const Ops &cur, Ops &nxt) {
         const int buf = b & 1;
         const long p0 = r0 + (long)b * a.L;
         const long gblk = a.cu ? p0 / a.L : (long)n * a.nblk + b;
         float *dhb = a.dh + ((size_t)gblk * a.h_v + h) * SS;
+        if (b > 0) fetch(b - 1, nxt);
         // publish dh_b; stage dh_b^T, U K, K^T of block b
 #pragma unroll
         for (int tl = 0; tl < 2; ++tl)
@@ -844,22 +943,13 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
                 for (int j = 0; j < 4; ++j) dhb[(size_t)(r + j) * DD + v0 + c] = dh[tl][tn][j];
                 st4(sm.dHt + c * LDH + r, dh[tl][tn][0], dh[tl][tn][1], dh[tl][tn][2], dh[tl][tn][3]);
             }
-        *reinterpret_cast<f16x8 *>(sm.UK + sr * LDH + sc) = ukr[0];
-        *reinterpret_cast<f16x8 *>(sm.UK + sr * LDH + sc + 8) = ukr[1];
+        *reinterpret_cast<f16x8 *>(sm.UK + sr * LDH + sc) = cur.uk[0];
+        *reinterpret_cast<f16x8 *>(sm.UK + sr * LDH + sc + 8) = cur.uk[1];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            sm.Kt[buf][(sc + j) * LDK + sr] = (_Float16)(float)kr[0][j];
-            sm.Kt[buf][(sc + 8 + j) * LDK + sr] = (_Float16)(float)kr[1][j];
+            sm.Kt[buf][(sc + j) * LDK + sr] = (_Float16)(float)cur.k[0][j];
+            sm.Kt[buf][(sc + 8 + j) * LDK + sr] = (_Float16)(float)cur.k[1][j];
         }
-        float c0[2][2][4];
-#pragma unroll
-        for (int tl = 0; tl < 2; ++tl)
-#pragma unroll
-            for (int tn = 0; tn < 2; ++tn)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) c0[tl][tn][j] = cs[tl][tn][j];
-        const float gn = gnv;
-        if (b > 0) fetch(b - 1);
         __syncthreads();
         {   // Z = (U K) dh_b: one 16 x 16 tile per wave, stored transposed
             const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
@@ -874,8 +964,15 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
                 const f32x4 c = tile_mma<_Float16, NP>(z, sm.Kt[buf] + (32 * wave + 16 * tl) * LDK, LDK,
                                                        sm.Zt + 16 * tn * LDK, LDK, lane);
 #pragma unroll
-                for (int j = 0; j < 4; ++j) dh[tl][tn][j] = gn * dh[tl][tn][j] + c0[tl][tn][j] - c[j];
+                for (int j = 0; j < 4; ++j) dh[tl][tn][j] = cur.gn * dh[tl][tn][j] + cur.cs[tl][tn][j] - c[j];
             }
+    };
+    Ops o0, o1;
+    if (nb > 0) fetch(nb - 1, o0);
+    for (int b = nb - 1; b >= 0; b -= 2) {
+        step(b, o0, o1);
+        if (b == 0) break;
+        step(b - 1, o1, o0);
     }
     if (a.dh0) {
         float *d0 = a.dh0 + ((size_t)n * a.h_v + h) * SS;
@@ -917,7 +1014,7 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, int n_chains, long n_bloc
             hipLaunchKernelGGL(noisy, dim3((unsigned)n_block_units), dim3(512), sizeof(Smem), s, a);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
-        hipLaunchKernelGGL(bdgdn_bwd_scan_kernel, dim3(4 * n_chains), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(bdgdn_bwd_scan_kernel, dim3((4 * n_chains + 31) / 32 * 32), dim3(256), 0, s, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (n_block_units > 0) {
             hipLaunchKernelGGL(clean, dim3((unsigned)n_block_units), dim3(512), sizeof(Smem), s, a);

@@ -33,9 +33,10 @@ namespace bdgdn {
 // SPLIT: the clean scan alone (the first kernel of the split schedule, Appendix "Route
 // I"): the noisy waves and the noisy half of the record stand idle, the noisy rows are not
 // staged, and the C waves write each block's seed state (the clean state before the
-// block) to HBM for a separate noisy-block kernel.
-template <typename Out, int DK, int LP, bool SPLIT = false, bool SEEDS = SPLIT>
+// block) to HBM for a separate noisy-block kernel.  SeedT_ is the element type of the seeds.
+template <typename Out, int DK, int LP, bool SPLIT = false, bool SEEDS = SPLIT, typename SeedT_ = float>
 struct Fused {
+    typedef SeedT_ SeedT;
     typedef __bf16 In;
     typedef _Float16 E;
     typedef Quad<E> QE;
@@ -160,7 +161,7 @@ struct Fused {
         int qks, vst, gst;           // row strides (elements)
         long len;
         int L;
-        float *bs;     // seed state of the chain's first block (column v0), or null
+        SeedT *bs;     // seed state of the chain's first block (column v0), or null
         long bs_blk;   // per-block advance of bs (elements)
         const float *h0;
         float *ht;
@@ -586,14 +587,15 @@ struct Fused {
             write_st(0, sq, bc, qo);
             lds_barrier();
             lds_barrier();
-            float *bs = c.bs;
+            SeedT *bs = c.bs;
             for (int j = 0; j < nb; ++j) {
                 if constexpr (SEEDS) {
                     // the seed of noisy block j: the clean state before block j
 #pragma unroll
                     for (int kb = 0; kb < DKB; ++kb)
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) bs[(long)(16 * kb + 4 * g + i) * c.dv + 16 * bc + n] = S[kb][i];
+                        for (int i = 0; i < 4; ++i)
+                            bs[(long)(16 * kb + 4 * g + i) * c.dv + 16 * bc + n] = (SeedT)S[kb][i];
                     bs += c.bs_blk;
                 }
                 c_block(j % 3, j & 1, j & 1, bc, S, sq, qo);
@@ -754,7 +756,7 @@ __device__ __forceinline__ void run_chain(const ScanArgs &a, unsigned char *smem
         // seed states by global block: documents start on block boundaries, sequences own
         // ceil(T / L) blocks each
         const long gblk0 = a.cu ? base / a.L : (long)seq * a.nblk;
-        c.bs = a.bs + (gblk0 * a.h_v + h) * DK * a.dv + v0;
+        c.bs = static_cast<typename K::SeedT *>(a.bs) + (gblk0 * a.h_v + h) * DK * a.dv + v0;
         c.bs_blk = (long)a.h_v * DK * a.dv;
     } else {
         c.bs = nullptr;

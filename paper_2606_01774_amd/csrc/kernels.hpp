@@ -41,7 +41,8 @@ struct ScanArgs {
     float *ht;
     void *o, *on;
     const unsigned char *ws;
-    float *bs;           // split schedule: seed states by (global block, v-head), or null
+    void *bs;            // seed states by (global block, v-head): fp32 (split schedule, views),
+                         // fp16 (the backward's recomputation), or null
     int T, L, nblk, h_qk, h_v, dv;
     int n_chains, n_vt;
     float scale;
@@ -115,7 +116,7 @@ bool fwd_supported(Types ty, int dk, int lp);
 
 // The split schedule's two kernels on their own: the clean scan writing every block's seed
 // state (the backward's recomputation), and the noisy-block pass from the seeds.
-hipError_t launch_scan_states(int lp, bool f32_out, const ScanArgs &sa, hipStream_t s);
+hipError_t launch_scan_states(int lp, bool f32_out, bool f16_seeds, const ScanArgs &sa, hipStream_t s);
 hipError_t launch_noisy_blocks(int lp, bool f32_out, const NoisyArgs &na, hipStream_t s);
 
 // The two-stream ShortConv (conv_kernels.hip).  x, xn, y, yn, dy, dyn are [rows][D] of the
