@@ -337,11 +337,25 @@ def main():
                                stream=stream)
         bsteps = max(2, args.steps // 4)
         bms = time_launches(bwstep, bsteps, 2, stream)
+        # the complementary-view backward: the same clean stream, two noisy views (the second
+        # drawn with the same recipe)
+        v2b = W.make_custom_train(w.batch, w.seqlen, w.h_qk, w.h_v, w.d_k, w.d_v, w.dtype, seed=w.seed + 50)
+        gdon2 = torch.randn(o.shape, generator=torch.Generator(device=dev).manual_seed(7), device=dev)
+        bviews = [dict({k_: d[k_ + "n"] for k_ in ("q", "k", "v", "g", "beta")}, do=gdon),
+                  dict({k_: v2b[k_ + "n"].to(dev) for k_ in ("q", "k", "v", "g", "beta")}, do=gdon2)]
+        bvgrads = bd.bdgdn_bwd_train_views(d["q"], d["k"], d["v"], d["g"], d["beta"], bviews, gdo, block=w.block,
+                                           scale=scale, workspace=bws)
+
+        def bvstep():
+            bd.bdgdn_bwd_train_views(d["q"], d["k"], d["v"], d["g"], d["beta"], bviews, gdo, block=w.block,
+                                     scale=scale, grads=bvgrads, workspace=bws, stream=stream)
+        bvms = time_launches(bvstep, bsteps, 2, stream)
         result["backward"] = {
             "workload": w.name, "ms_per_call": bms, "tokens_per_s": tokens / (bms * 1e-3), "steps": bsteps,
             "kernels": "bdgdn_k2_scan_states_kernel (seed states) + bdgdn_bwd_noisy_kernel + "
                        "bdgdn_bwd_scan_kernel + bdgdn_bwd_clean_kernel",
-            "workspace_bytes": bws.numel()}
+            "workspace_bytes": bws.numel(),
+            "views2_ms_per_call": bvms, "views2_tokens_per_s": 3 * w.tokens / (bvms * 1e-3)}
 
     if not args.no_conv:
         # the GDN layer's two-stream ShortConv at the same token shape (channels = the q, k

@@ -203,10 +203,11 @@ int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc,
                           const float *h0, void *o, float *ht,
                           void *workspace, size_t workspace_bytes, void *stream);
 
-/* Bytes of device workspace bdgdn_bwd_train needs: three fp32 states per (block, v-head)
- * (the recomputed clean seed, the gradient of the noisy block's seed, the clean state
- * gradient at the block's end) plus scratch for the recomputed clean outputs; 0 for a
- * descriptor it would reject. */
+/* Bytes of device workspace bdgdn_bwd_train needs, per (block, v-head): the recomputed
+ * clean seed state (fp16), two fp32 states (the part of the clean state gradient at the
+ * block's start that does not depend on the gradient at its end, and the gradient at its
+ * end), the block's U K (32 x d_k fp16) and gamma_n; plus scratch for the recomputed clean
+ * outputs; 0 for a descriptor it would reject. */
 size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
 
 /*
@@ -240,6 +241,43 @@ int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc,
                     float *dq, float *dk, float *dv, float *dg, float *dbeta,
                     float *dqn, float *dkn, float *dvn, float *dgn, float *dbetan, float *dh0,
                     void *workspace, size_t workspace_bytes, void *stream);
+
+/* One noisy view of the complementary-view backward: its inputs (as bdgdn_noisy_view_t),
+ * the upstream gradient of its readout and its gradients (as dqn .. dbetan of
+ * bdgdn_bwd_train). */
+typedef struct {
+    const void *q, *k, *v;   /* [B*T][h_qk or h_v][d] of desc->dtype, 16-byte aligned      */
+    const float *g, *beta;   /* [B*T][h_v] fp32                                              */
+    const void *do_;         /* [B*T][h_v][d_v] of desc->out_dtype, 16-byte aligned          */
+    float *dq, *dk;          /* [B*T][h_qk][d_k] fp32                                        */
+    float *dv;               /* [B*T][h_v][d_v] fp32                                         */
+    float *dg, *dbeta;       /* [B*T][h_v] fp32                                              */
+} bdgdn_noisy_view_grad_t;
+
+/* Bytes of device workspace bdgdn_bwd_train_views needs (that of bdgdn_bwd_train: the views
+ * share it). */
+size_t bdgdn_bwd_train_views_workspace(const bdgdn_fwd_desc_t *desc);
+
+/*
+ * Backward of bdgdn_fwd_train_views (the complementary-view objective of Sec. 3.3 "Training
+ * Objective and Mask Design": several noisy views, each block seeded from the same clean
+ * state): the gradients of
+ *     sum <do, o> + sum_i sum <views[i].do_, o_i> + <dht, ht>
+ * for 1 <= n_views <= 16.  Every view's noisy block b sends its seed's gradient into the
+ * clean state gradient at the end of clean block b - 1 (eq. dh-block-recursion, summed over
+ * the views).  Clean inputs, h0, do, dht, dq .. dbeta, dh0 and the workspace as for
+ * bdgdn_bwd_train; each view's gradients go to its own arrays.  The same support and
+ * errors as bdgdn_bwd_train; deterministic except for the grouped-head atomics described
+ * there.
+ */
+int bdgdn_bwd_train_views(const bdgdn_fwd_desc_t *desc,
+                          const void *q, const void *k, const void *v,
+                          const float *g, const float *beta,
+                          const bdgdn_noisy_view_grad_t *views, int32_t n_views,
+                          const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                          const float *h0, const void *do_, const float *dht,
+                          float *dq, float *dk, float *dv, float *dg, float *dbeta, float *dh0,
+                          void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * One Diffusion-Trust denoise pass over R blocks (Appendix "Per-block denoise loop",

@@ -20,6 +20,9 @@ to it.  Each entry point follows the paper (FLARE, arXiv 2606.01774):
   "Backward primitives": the per-step backward, eq. per-step-bwd; the noisy
   block-end readout backward, eq. noisy-readout-bwd; the block-level chain rule,
   eq. dh-block-recursion).
+* ``bwd_train_views`` -- gradients of the complementary-view objective (Sec. 3.3 "Training
+  Objective and Mask Design": several noisy views, each block seeded from the same clean
+  state), composed from ``bwd_train`` by linearity.
 """
 from __future__ import annotations
 
@@ -166,6 +169,29 @@ def bwd_train(q, k, v, g, beta, qn, kn, vn, gn, betan, do, don, *, block, scale,
     if rc != 0:
         raise RuntimeError(f"oracle_bwd_train failed: {rc}")
     return out
+
+
+def bwd_train_views(q, k, v, g, beta, views, do, *, block, scale, cu_seqlens=None, h0=None, dht=None):
+    """Gradients of  sum(do * o) + sum_i sum(views[i]["do"] * o_i) + sum(dht * ht)  where o_i
+    is the block-end readout of noisy view i (each view a noisy stream seeded from the same
+    clean states; o and ht are the clean stream's, shared by every view).
+
+    The loss is linear in its upstream gradients, so it is the sum over views of two-stream
+    losses: view 0 carries do and dht, every other view only its own readout term (clean
+    upstream gradient zero).  bwd_train of each gives that view's gradients and its share of
+    the clean gradients; the clean ones add up.  Returns (clean, per_view): ``clean`` a dict
+    dq, dk, dv, dg, dbeta, dh0, ``per_view`` one dict dq, dk, dv, dg, dbeta per view (fp64).
+    """
+    clean, per_view = None, []
+    zero_do = np.zeros(np.shape(do))
+    for i, w in enumerate(views):
+        r = bwd_train(q, k, v, g, beta, w["q"], w["k"], w["v"], w["g"], w["beta"],
+                      do if i == 0 else zero_do, w["do"], block=block, scale=scale,
+                      cu_seqlens=cu_seqlens, h0=h0, dht=dht if i == 0 else None)
+        per_view.append({name: r[name + "n"] for name in ("dq", "dk", "dv", "dg", "dbeta")})
+        part = {name: r[name] for name in ("dq", "dk", "dv", "dg", "dbeta", "dh0")}
+        clean = part if clean is None else {name: clean[name] + part[name] for name in part}
+    return clean, per_view
 
 
 def denoise(pool, q, k, v, g, beta, *, scale, slot=None):

@@ -25,7 +25,7 @@ __all__ = [
     "bdgdn_commit_record", "bdgdn_accept_states", "BDGDN_ACT_NONE", "BDGDN_ACT_SILU",
     "bdgdn_shortconv_fwd", "bdgdn_shortconv_bwd_workspace", "bdgdn_shortconv_bwd",
     "bdgdn_bwd_train_workspace", "bdgdn_bwd_train", "bdgdn_fwd_train_views_workspace", "bdgdn_fwd_train_views",
-    "bdgdn_denoise_step", "bdgdn_commit", "library_path", "load_library", "EXPORTED_SYMBOLS",
+    "bdgdn_bwd_train_views_workspace", "bdgdn_bwd_train_views", "bdgdn_denoise_step", "bdgdn_commit", "library_path", "load_library", "EXPORTED_SYMBOLS",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -50,7 +50,8 @@ EXPORTED_SYMBOLS = ("bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_wor
                     "bdgdn_fwd_train", "bdgdn_denoise_step", "bdgdn_commit", "bdgdn_commit_record",
                     "bdgdn_accept_states", "bdgdn_shortconv_fwd", "bdgdn_shortconv_bwd_workspace",
                     "bdgdn_shortconv_bwd", "bdgdn_bwd_train_workspace", "bdgdn_bwd_train",
-                    "bdgdn_fwd_train_views_workspace", "bdgdn_fwd_train_views")
+                    "bdgdn_fwd_train_views_workspace", "bdgdn_fwd_train_views",
+                    "bdgdn_bwd_train_views_workspace", "bdgdn_bwd_train_views")
 
 
 class FwdDesc(ctypes.Structure):
@@ -72,6 +73,13 @@ class ServeDesc(ctypes.Structure):
 class NoisyView(ctypes.Structure):
     _fields_ = [("q", ctypes.c_void_p), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
                 ("g", ctypes.c_void_p), ("beta", ctypes.c_void_p), ("o", ctypes.c_void_p)]
+
+
+class NoisyViewGrad(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("g", ctypes.c_void_p), ("beta", ctypes.c_void_p), ("do_", ctypes.c_void_p),
+                ("dq", ctypes.c_void_p), ("dk", ctypes.c_void_p), ("dv", ctypes.c_void_p),
+                ("dg", ctypes.c_void_p), ("dbeta", ctypes.c_void_p)]
 
 
 class ConvDesc(ctypes.Structure):
@@ -127,6 +135,12 @@ def load_library():
     lib.bdgdn_bwd_train_workspace.restype = ctypes.c_size_t
     lib.bdgdn_bwd_train.argtypes = [ctypes.POINTER(FwdDesc)] + [P] * 28 + [ctypes.c_size_t, P]
     lib.bdgdn_bwd_train.restype = ctypes.c_int
+    lib.bdgdn_bwd_train_views_workspace.argtypes = [ctypes.POINTER(FwdDesc)]
+    lib.bdgdn_bwd_train_views_workspace.restype = ctypes.c_size_t
+    lib.bdgdn_bwd_train_views.argtypes = ([ctypes.POINTER(FwdDesc)] + [P] * 5
+                                          + [ctypes.POINTER(NoisyViewGrad), ctypes.c_int32] + [P] * 12
+                                          + [ctypes.c_size_t, P])
+    lib.bdgdn_bwd_train_views.restype = ctypes.c_int
     lib.bdgdn_shortconv_fwd.argtypes = [ctypes.POINTER(ConvDesc)] + [P] * 9
     lib.bdgdn_shortconv_fwd.restype = ctypes.c_int
     lib.bdgdn_shortconv_bwd_workspace.argtypes = [ctypes.POINTER(ConvDesc)]
@@ -367,6 +381,76 @@ def bdgdn_bwd_train(q, k, v, g, beta, qn, kn, vn, gn, betan, do, don, *, block, 
         _ptr(workspace), ws_size, _stream(stream))
     _check(st, "bdgdn_bwd_train")
     return out
+
+
+def bdgdn_bwd_train_views_workspace(desc: FwdDesc) -> int:
+    return int(load_library().bdgdn_bwd_train_views_workspace(ctypes.byref(desc)))
+
+
+_VIEW_GRAD_NAMES = ("dq", "dk", "dv", "dg", "dbeta")
+
+
+def bdgdn_bwd_train_views(q, k, v, g, beta, views, do, *, block, scale=None, cu_seqlens=None,
+                          cu_seqlens_host=None, h0=None, dht=None, want_dh0=False, grads=None, workspace=None,
+                          stream=None):
+    """Backward of bdgdn_fwd_train_views: gradients of sum(do*o) + sum_i sum(views[i]["do"]*o_i)
+    + sum(dht*ht).  ``views`` is a list of dicts with the view's q, k, v, g, beta and the
+    upstream gradient "do" of its readout.  Returns (clean, per_view): ``clean`` a dict of
+    fp32 tensors dq, dk, dv, dg, dbeta (and dh0 when want_dh0), ``per_view`` one such dict per
+    view.  ``grads`` may supply them (a previous call's result)."""
+    lib = load_library()
+    dt = q.dtype
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _dev(t, name, dt)
+    _dev(g, "g", torch.float32)
+    _dev(beta, "beta", torch.float32)
+    _dev(do, "do")
+    n = len(views)
+    arr = (NoisyViewGrad * max(n, 1))()
+    per_view = []
+    like = {"dq": q, "dk": k, "dv": v, "dg": g, "dbeta": beta}
+    for i, w in enumerate(views):
+        for name in ("q", "k", "v"):
+            _dev(w[name], f"views[{i}].{name}", dt)
+        for name in ("g", "beta"):
+            _dev(w[name], f"views[{i}].{name}", torch.float32)
+        _dev(w["do"], f"views[{i}].do", do.dtype)
+        gr = grads[1][i] if grads is not None else {
+            name: torch.empty(like[name].shape, dtype=torch.float32, device=q.device) for name in _VIEW_GRAD_NAMES}
+        for name in _VIEW_GRAD_NAMES:
+            _dev(gr[name], f"views[{i}] {name}", torch.float32)
+        per_view.append(gr)
+        arr[i] = NoisyViewGrad(*[_ptr(w[name]) for name in ("q", "k", "v", "g", "beta", "do")],
+                               *[_ptr(gr[name]) for name in _VIEW_GRAD_NAMES])
+    num_seqs = 0
+    cu_h = None
+    if cu_seqlens is not None:
+        _dev(cu_seqlens, "cu_seqlens", torch.int32)
+        num_seqs = cu_seqlens.numel() - 1
+        if cu_seqlens_host is None:
+            cu_seqlens_host = cu_seqlens.cpu()
+        cu_h = torch.as_tensor(cu_seqlens_host, dtype=torch.int32).contiguous()
+    desc = make_fwd_desc(q, v, block=block, scale=scale, num_seqs=num_seqs, out_dtype=do.dtype)
+    clean = dict(grads[0]) if grads is not None else {
+        name: torch.empty(like[name].shape, dtype=torch.float32, device=q.device) for name in _VIEW_GRAD_NAMES}
+    for name in _VIEW_GRAD_NAMES:
+        _dev(clean[name], name, torch.float32)
+    units = num_seqs if num_seqs else q.shape[0]
+    if want_dh0 and "dh0" not in clean:
+        clean["dh0"] = torch.empty(units, v.shape[2], q.shape[3], v.shape[3], dtype=torch.float32, device=q.device)
+    _dev(h0, "h0", torch.float32)
+    _dev(dht, "dht", torch.float32)
+    ws_bytes = bdgdn_bwd_train_views_workspace(desc)
+    if workspace is None and ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    ws_size = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.bdgdn_bwd_train_views(
+        ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), arr, n,
+        _ptr(cu_seqlens), None if cu_h is None else ctypes.c_void_p(cu_h.data_ptr()),
+        _ptr(h0), _ptr(do), _ptr(dht), *[_ptr(clean[name]) for name in _VIEW_GRAD_NAMES], _ptr(clean.get("dh0")),
+        _ptr(workspace), ws_size, _stream(stream))
+    _check(st, "bdgdn_bwd_train_views")
+    return clean, per_view
 
 
 def _serve_desc(q, v, scale, out_dtype):

@@ -503,14 +503,14 @@ size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc)
     return bwd_layout(desc).total;
 }
 
-int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, const void *v,
-                    const float *g, const float *beta, const void *qn, const void *kn,
-                    const void *vn, const float *gn, const float *betan,
-                    const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host, const float *h0,
-                    const void *dout, const void *doutn, const float *dht,
-                    float *dq, float *dk, float *dv, float *dg, float *dbeta,
-                    float *dqn, float *dkn, float *dvn, float *dgn, float *dbetan, float *dh0,
-                    void *workspace, size_t workspace_bytes, void *stream)
+// The backward of the clean stream and noisy view 0 (qn .. dbetan), plus n_more further views.
+static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, const void *v, const float *g,
+                    const float *beta, const void *qn, const void *kn, const void *vn, const float *gn,
+                    const float *betan, const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                    const float *h0, const void *dout, const void *doutn, const float *dht, float *dq, float *dk,
+                    float *dv, float *dg, float *dbeta, float *dqn, float *dkn, float *dvn, float *dgn,
+                    float *dbetan, float *dh0, const BwdView *more, int n_more, void *workspace,
+                    size_t workspace_bytes, void *stream)
 {
     int st = check_fwd(desc, cu_seqlens_dev, cu_seqlens_host);
     if (st != BDGDN_OK) return st;
@@ -521,6 +521,12 @@ int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(qn) || !aligned16(kn) ||
         !aligned16(vn) || !aligned16(dout) || !aligned16(doutn) || !aligned16(h0) || !aligned16(dht))
         return BDGDN_ERR_INVALID_ARG;
+    for (int i = 0; i < n_more; ++i) {
+        const BwdView &w = more[i];
+        if (!w.q || !w.k || !w.v || !w.g || !w.beta || !w.dout || !w.dq || !w.dk || !w.dv || !w.dg || !w.db)
+            return BDGDN_ERR_INVALID_ARG;
+        if (!aligned16(w.q) || !aligned16(w.k) || !aligned16(w.v) || !aligned16(w.dout)) return BDGDN_ERR_INVALID_ARG;
+    }
     if (desc->seqlen == 0) return BDGDN_OK;
     const size_t need = bdgdn_bwd_train_workspace(desc);
     if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0)
@@ -579,9 +585,44 @@ int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     a.scale = desc->scale;
     a.atomic_qk = desc->h_v != desc->h_qk;
     const long rows = (long)desc->batch * desc->seqlen;
-    e = launch_bwd(desc->out_dtype == BDGDN_BF16, a, nseq * desc->h_v, total_blocks(desc) * desc->h_v,
+    e = launch_bwd(desc->out_dtype == BDGDN_BF16, a, more, n_more, nseq * desc->h_v, total_blocks(desc) * desc->h_v,
                    rows * desc->h_qk * desc->d_k, strm);
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+}
+
+int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, const void *v,
+                    const float *g, const float *beta, const void *qn, const void *kn,
+                    const void *vn, const float *gn, const float *betan,
+                    const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host, const float *h0,
+                    const void *dout, const void *doutn, const float *dht,
+                    float *dq, float *dk, float *dv, float *dg, float *dbeta,
+                    float *dqn, float *dkn, float *dvn, float *dgn, float *dbetan, float *dh0,
+                    void *workspace, size_t workspace_bytes, void *stream)
+{
+    return bwd_impl(desc, q, k, v, g, beta, qn, kn, vn, gn, betan, cu_seqlens_dev, cu_seqlens_host, h0, dout,
+                    doutn, dht, dq, dk, dv, dg, dbeta, dqn, dkn, dvn, dgn, dbetan, dh0, nullptr, 0, workspace,
+                    workspace_bytes, stream);
+}
+
+size_t bdgdn_bwd_train_views_workspace(const bdgdn_fwd_desc_t *desc) { return bdgdn_bwd_train_workspace(desc); }
+
+int bdgdn_bwd_train_views(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, const void *v,
+                          const float *g, const float *beta, const bdgdn_noisy_view_grad_t *views, int32_t n_views,
+                          const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host, const float *h0,
+                          const void *dout, const float *dht, float *dq, float *dk, float *dv, float *dg,
+                          float *dbeta, float *dh0, void *workspace, size_t workspace_bytes, void *stream)
+{
+    if (!desc) return BDGDN_ERR_INVALID_ARG;
+    if (!views || n_views < 1 || n_views > 16) return BDGDN_ERR_INVALID_ARG;
+    BwdView more[16];
+    for (int i = 1; i < n_views; ++i) {
+        const bdgdn_noisy_view_grad_t &w = views[i];
+        more[i - 1] = BwdView{w.q, w.k, w.v, w.g, w.beta, w.do_, w.dq, w.dk, w.dv, w.dg, w.dbeta};
+    }
+    const bdgdn_noisy_view_grad_t &w0 = views[0];
+    return bwd_impl(desc, q, k, v, g, beta, w0.q, w0.k, w0.v, w0.g, w0.beta, cu_seqlens_dev, cu_seqlens_host, h0,
+                    dout, w0.do_, dht, dq, dk, dv, dg, dbeta, w0.dq, w0.dk, w0.dv, w0.dg, w0.dbeta, dh0, more,
+                    n_views - 1, workspace, workspace_bytes, stream);
 }
 
 size_t bdgdn_shortconv_bwd_workspace(const bdgdn_conv_desc_t *desc)

@@ -34,8 +34,18 @@ struct BwdArgs {
     float scale;
     bool atomic_qk;
 };
+// A further noisy view (the complementary-view backward): its inputs, the upstream gradient
+// of its readout and its gradients, laid out as the noisy stream of BwdArgs.
+struct BwdView {
+    const void *q, *k, *v;
+    const float *g, *beta;
+    const void *dout;
+    float *dq, *dk, *dv, *dg, *db;
+};
 size_t bwd_block_lds();
-hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, int n_chains, long n_block_units, long qk_elems,
-                      hipStream_t s);
+// The backward of a's two streams, plus n_more further noisy views seeded from the same clean
+// states (their seed gradients summed into the clean state gradient).
+hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int n_more, int n_chains,
+                      long n_block_units, long qk_elems, hipStream_t s);
 
 }  // namespace bdgdn

@@ -60,8 +60,11 @@ struct Smem {
     float KK[NP * LDF], dT[NP * LDF], W[NP * LDF];
     float TdA[NP * LDF];         // T (T_ci = M_ci beta_i at [c][i]), later dA
     float Mt[NP * LDF];          // M^T (fp32)
-    float G[NP], G2[NP], gam[NP], bet[NP], dG[NP], dB[NP];   // G2: cumulative log2-gates
-    float part[kWaves][NP];      // per-wave partial sums of the row gate terms
+    float G[NP], G2[NP], gam[NP], bet[NP], dB[NP];   // G2: cumulative log2-gates
+    // the gradient of the local cumulative gates, as per-wave partial sums: every
+    // contribution goes to the row of the wave that makes it, and the rows are added in a
+    // fixed order at the end (deterministic, unlike float atomics from several waves)
+    float part[kWaves][NP];
 };
 static_assert(sizeof(Smem) <= 160 * 1024, "one workgroup's LDS");
 
@@ -305,9 +308,9 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
     if (tid < NP) {
         sm.bet[tid] = in.b;
         sm.G[tid] = in.g;
-        sm.dG[tid] = 0.f;
         sm.dB[tid] = 0.f;
     }
+    if (tid < kWaves * NP) sm.part[tid / NP][tid % NP] = 0.f;
     __syncthreads();
     if (wave == 0) cum_gates(sm, lane);
     __syncthreads();
@@ -422,7 +425,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
         if constexpr (CLEAN) {
             colw += __shfl_xor(colw, 16);
             colw += __shfl_xor(colw, 32);
-            if (g4 == 0) lds_add(&sm.dG[i], -colw);
+            if (g4 == 0) lds_add(&sm.part[wave][i], -colw);
         }
     }
     // dDelta = [clean] s P^T dO + D K dS_n, with the D-term gate gradient
@@ -566,9 +569,9 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
         const float br = half_total(bt, lane), wr = half_total(wa, lane);
         if (c == 0) {
             lds_add(&sm.dB[r], br);
-            lds_add(&sm.dG[r], wr);
+            lds_add(&sm.part[wave][r], wr);
         }
-        if (lane < 32 && wc != 0.f) lds_add(&sm.dG[c], -wc);
+        if (lane < 32 && wc != 0.f) lds_add(&sm.part[wave][c], -wc);
     }
     __syncthreads();
     // ---- dK = -Gamma dR S0^T + D Delta dS_n^T + [clean] (s E o Mc)^T Q + (dKK + dKK^T) K, with
@@ -614,14 +617,13 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
             for (int j = 0; j < 4; ++j) {
                 const int r = 16 * tm + 4 * g4 + j;
                 const float t = row_total(rowg[tm][j]);
-                if (rr == 15) sm.part[wave][r] = r == NP - 1 ? t + dl : t;
+                if (rr == 15) sm.part[wave][r] += r == NP - 1 ? t + dl : t;
             }
     }
     __syncthreads();
     if (wave == 0) {   // dg = reverse cumulative sum of dG (a 32-lane scan)
         float x = 0.f;
         if (lane < NP) {
-            x = sm.dG[lane];
 #pragma unroll
             for (int w = 0; w < kWaves; ++w) x += sm.part[w][lane];
         }
@@ -777,10 +779,12 @@ __device__ void clean_prep(Smem &sm, const BwdArgs &a, const BlockRows<Od, false
 }
 
 // Phase 1: every noisy block, in parallel (one workgroup per (global block, v-head)): its
-// gradients and its seed's gradient, plus the dh-independent part of the clean block of the
-// same position (clean_prep); both enter the state gradient at the block's start, whose sum
-// is written to cterm (fp32 [block][h_v][128][128]).
-template <typename Od>
+// gradients and its seed's gradient, plus (PREP) the dh-independent part of the clean block
+// of the same position (clean_prep); both enter the state gradient at the block's start,
+// whose sum is written to cterm (fp32 [block][h_v][128][128]).  Without PREP (the further
+// noisy views of the complementary-view backward, each seeded from the same clean state)
+// the seed's gradient is added to cterm.
+template <typename Od, bool PREP>
 __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -795,7 +799,8 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
     const StreamPtrs pc = stream_ptrs<Od>(a, false, p0, h, hq), pn = stream_ptrs<Od>(a, true, p0, h, hq);
     // every load of the unit in flight together: the clean rows (the clean prep runs first;
     // it needs no seed), the seed, the noisy rows
-    const BlockRows<Od, false> cin = load_block<Od, false>(pc, a.h_qk, a.h_v, nvalid, tid);
+    BlockRows<Od, false> cin;
+    if constexpr (PREP) cin = load_block<Od, false>(pc, a.h_qk, a.h_v, nvalid, tid);
     const SeedRegs seed = load_seed(a.seeds + so, tid);
     const BlockRows<Od, true> nin = load_block<Od, true>(pn, a.h_qk, a.h_v, nvalid, tid);
     float acc[8][4];
@@ -803,14 +808,20 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
     for (int tm = 0; tm < 8; ++tm)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[tm][j] = 0.f;
-    clean_prep<Od>(sm, a, cin, acc, a.uk + unit * NP * DD, a.gnb + unit, tid);
+    if constexpr (PREP) clean_prep<Od>(sm, a, cin, acc, a.uk + unit * NP * DD, a.gnb + unit, tid);
     store_seed(sm.S0, seed, tid);   // made visible by block_bwd's first barrier
     block_bwd<false, Od>(sm, pn, a, nvalid, nin, acc, acc, tid);
     float *dst = a.cterm + so;
 #pragma unroll
     for (int tm = 0; tm < 8; ++tm)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) dst[(16 * tm + 4 * g4 + j) * DD + 16 * wave + rr] = acc[tm][j];
+        for (int j = 0; j < 4; ++j) {
+            float *p = dst + (16 * tm + 4 * g4 + j) * DD + 16 * wave + rr;
+            if constexpr (PREP)
+                *p = acc[tm][j];
+            else
+                *p += acc[tm][j];
+        }
 }
 
 // Phase 3: every clean block, in parallel, from its seed and the gradient at its end (dh,
@@ -993,26 +1004,43 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_zero_kernel(float *p, long n)
 
 size_t bwd_block_lds() { return sizeof(Smem); }
 
-hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, int n_chains, long n_block_units, long qk_elems,
-                      hipStream_t s)
+hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int n_more, int n_chains,
+                      long n_block_units, long qk_elems, hipStream_t s)
 {
+    if (n_more < 0 || (n_more > 0 && !more)) return hipErrorInvalidValue;
+    // the noisy stream of a: its pointers replaced by those of view i
+    auto with_view = [&](const BwdView &w) {
+        BwdArgs b = a;
+        b.qn = w.q; b.kn = w.k; b.vn = w.v; b.gn = w.g; b.betan = w.beta; b.doutn = w.dout;
+        b.dqn = w.dq; b.dkn = w.dk; b.dvn = w.dv; b.dgn = w.dg; b.dbn = w.db;
+        return b;
+    };
+    auto zero = [&](float *p) {
+        hipLaunchKernelGGL(bdgdn_bwd_zero_kernel, dim3(1024), dim3(256), 0, s, p, qk_elems);
+        return hipGetLastError();
+    };
     if (a.atomic_qk) {
-        for (float *p : {a.dq, a.dk, a.dqn, a.dkn}) {
-            hipLaunchKernelGGL(bdgdn_bwd_zero_kernel, dim3(1024), dim3(256), 0, s, p, qk_elems);
-            const hipError_t e = hipGetLastError();
+        for (float *p : {a.dq, a.dk, a.dqn, a.dkn})
+            if (hipError_t e = zero(p); e != hipSuccess) return e;
+        for (int i = 0; i < n_more; ++i)
+            for (float *p : {more[i].dq, more[i].dk})
+                if (hipError_t e = zero(p); e != hipSuccess) return e;
+    }
+    auto run = [&](auto noisy, auto noisy_more, auto clean) {
+        for (const void *f : {reinterpret_cast<const void *>(noisy), reinterpret_cast<const void *>(noisy_more),
+                              reinterpret_cast<const void *>(clean)}) {
+            const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(Smem));
             if (e != hipSuccess) return e;
         }
-    }
-    auto run = [&](auto noisy, auto clean) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(noisy),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(Smem));
-        if (e != hipSuccess) return e;
-        e = hipFuncSetAttribute(reinterpret_cast<const void *>(clean), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)sizeof(Smem));
-        if (e != hipSuccess) return e;
+        hipError_t e;
         if (n_block_units > 0) {
             hipLaunchKernelGGL(noisy, dim3((unsigned)n_block_units), dim3(512), sizeof(Smem), s, a);
             if ((e = hipGetLastError()) != hipSuccess) return e;
+            for (int i = 0; i < n_more; ++i) {   // in stream order: each adds its seed gradients
+                hipLaunchKernelGGL(noisy_more, dim3((unsigned)n_block_units), dim3(512), sizeof(Smem), s,
+                                   with_view(more[i]));
+                if ((e = hipGetLastError()) != hipSuccess) return e;
+            }
         }
         hipLaunchKernelGGL(bdgdn_bwd_scan_kernel, dim3((4 * n_chains + 31) / 32 * 32), dim3(256), 0, s, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1022,8 +1050,10 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, int n_chains, long n_bloc
         }
         return hipSuccess;
     };
-    return bf16_out ? run(bdgdn_bwd_noisy_kernel<__bf16>, bdgdn_bwd_clean_kernel<__bf16>)
-                    : run(bdgdn_bwd_noisy_kernel<float>, bdgdn_bwd_clean_kernel<float>);
+    return bf16_out ? run(bdgdn_bwd_noisy_kernel<__bf16, true>, bdgdn_bwd_noisy_kernel<__bf16, false>,
+                          bdgdn_bwd_clean_kernel<__bf16>)
+                    : run(bdgdn_bwd_noisy_kernel<float, true>, bdgdn_bwd_noisy_kernel<float, false>,
+                          bdgdn_bwd_clean_kernel<float>);
 }
 
 }  // namespace bdgdn

@@ -266,8 +266,10 @@ def test_bwd_train_validation_and_workspace():
     lib = bd.load_library()
     ok = _desc()
     need = lib.bdgdn_bwd_train_workspace(ctypes.byref(ok))
-    # fp32 seed states of every (block, v-head) + bf16 scratch for the clean outputs
-    assert need >= 2 * 4 * 128 * 128 * 4 + 64 * 4 * 128 * 2
+    # per (block, v-head): an fp16 seed, two fp32 states, U K (32 x 128 fp16); + bf16 scratch
+    # for the clean outputs
+    units = 2 * 4
+    assert need >= units * 128 * 128 * (2 + 4 + 4) + units * 32 * 128 * 2 + 64 * 4 * 128 * 2
     assert lib.bdgdn_bwd_train_workspace(ctypes.byref(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32))) == 0
     assert _bwd(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32)) == bd.BDGDN_ERR_UNSUPPORTED
     assert _bwd(_desc(d_k=64, d_v=64)) == bd.BDGDN_ERR_UNSUPPORTED
@@ -299,3 +301,28 @@ def test_views_validation():
     assert call(split, 2) == bd.BDGDN_ERR_WORKSPACE
     assert call(_desc(route=bd.BDGDN_ROUTE_RECORDS), 2) == bd.BDGDN_ERR_UNSUPPORTED
     assert call(_desc(block=64), 1) == bd.BDGDN_ERR_UNSUPPORTED
+
+
+def test_bwd_views_validation():
+    lib = bd.load_library()
+    ok = _desc()
+    need = lib.bdgdn_bwd_train_workspace(ctypes.byref(ok))
+    assert lib.bdgdn_bwd_train_views_workspace(ctypes.byref(ok)) == need
+    P = FAKE
+    full = [0x1000] * 11
+    views = (bd.NoisyViewGrad * 2)(bd.NoisyViewGrad(*full), bd.NoisyViewGrad(*full))
+
+    def call(desc, n, ws=None, ws_bytes=0):
+        return lib.bdgdn_bwd_train_views(ctypes.byref(desc), P, P, P, P, P, views, n, None, None, None, P, None,
+                                         P, P, P, P, P, None, ws, ws_bytes, None)
+    assert call(ok, 0) == bd.BDGDN_ERR_INVALID_ARG
+    assert call(ok, 17) == bd.BDGDN_ERR_INVALID_ARG
+    assert call(ok, 2) == bd.BDGDN_ERR_WORKSPACE             # every pointer given: only the workspace lacks
+    assert call(ok, 2, ws=FAKE, ws_bytes=need - 1) == bd.BDGDN_ERR_WORKSPACE
+    views[1] = bd.NoisyViewGrad(*(full[:8] + [None] + full[9:]))   # view 1 without dg
+    assert call(ok, 2) == bd.BDGDN_ERR_INVALID_ARG
+    views[1] = bd.NoisyViewGrad(*(full[:5] + [0x1008] + full[6:]))  # view 1's do not 16-byte aligned
+    assert call(ok, 2) == bd.BDGDN_ERR_INVALID_ARG
+    views[1] = bd.NoisyViewGrad(*full)
+    assert call(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32), 2) == bd.BDGDN_ERR_UNSUPPORTED
+    assert call(_desc(block=64), 2) == bd.BDGDN_ERR_UNSUPPORTED

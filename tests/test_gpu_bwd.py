@@ -93,3 +93,66 @@ def test_bwd_training_workload_sampled_units():
         print(f"  unit ({b}, {h}): " + " ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
         for name, e in errs.items():
             assert e <= TOL["bf16"], f"unit ({b}, {h}) {name}: {e:.3e}"
+
+
+KEYS = ("q", "k", "v", "g", "beta")
+
+
+@pytest.mark.parametrize("B,T,hqk,hv,L,lengths,n_views", [
+    (1, 96, 1, 1, 32, None, 2),
+    (2, 100, 1, 2, 16, None, 3),              # grouped value heads, ragged tail
+    (1, 160, 2, 2, 32, [64, 32, 64], 2),      # packed documents
+])
+def test_bwd_views_match_oracle(B, T, hqk, hv, L, lengths, n_views):
+    """The complementary-view backward (bdgdn_bwd_train_views) against the oracle's
+    composition of two-stream backwards: the clean gradients (summed over the views), dh0,
+    and every view's own gradients."""
+    print(f"bwd views B={B} T={T} hqk={hqk} hv={hv} L={L} n={n_views} lengths={lengths}", flush=True)
+    base = W.make_custom_train(B, T, hqk, hv, 128, 128, "bf16", seed=900 + T, lengths=lengths)
+    clean = {k: base[k] for k in KEYS}
+    rng = np.random.default_rng(950 + T)
+    views = []
+    for i in range(n_views):
+        src = base if i == 0 else W.make_custom_train(B, T, hqk, hv, 128, 128, "bf16", seed=960 + 5 * i + T,
+                                                      lengths=lengths)
+        w = {k: src[k + "n"] for k in KEYS}
+        w["do"] = torch.from_numpy(rng.standard_normal((B, T, hv, 128)).astype(np.float32))
+        views.append(w)
+    do = torch.from_numpy(rng.standard_normal((B, T, hv, 128)).astype(np.float32))
+    nseq = B if lengths is None else len(lengths)
+    h0 = torch.from_numpy((0.3 * rng.standard_normal((nseq, hv, 128, 128))).astype(np.float32))
+    dht = torch.from_numpy(rng.standard_normal((nseq, hv, 128, 128)).astype(np.float32))
+    cu = None if lengths is None else torch.tensor(np.concatenate([[0], np.cumsum(lengths)]), dtype=torch.int32)
+    scale = 1.0 / math.sqrt(128)
+    dc = {k: v.cuda() for k, v in clean.items()}
+    dv = [{k: v.cuda() for k, v in w.items()} for w in views]
+    got_c, got_v = bd.bdgdn_bwd_train_views(dc["q"], dc["k"], dc["v"], dc["g"], dc["beta"], dv, do.cuda(), block=L,
+                                            scale=scale, cu_seqlens=None if cu is None else cu.cuda(),
+                                            cu_seqlens_host=cu, h0=h0.cuda(), dht=dht.cuda(), want_dh0=True)
+    torch.cuda.synchronize()
+    ref_c, ref_v = oracle.bwd_train_views(*[clean[k] for k in KEYS], views, do, block=L, scale=scale,
+                                          cu_seqlens=None if cu is None else cu.numpy(), h0=h0, dht=dht)
+    errs = {"clean " + n: rel_err(got_c[n], ref_c[n]) for n in ("dq", "dk", "dv", "dg", "dbeta", "dh0")}
+    for i in range(n_views):
+        errs.update({f"view{i} {n}": rel_err(got_v[i][n], ref_v[i][n]) for n in ("dq", "dk", "dv", "dg", "dbeta")})
+    print("  " + " ".join(f"{k}={v:.1e}" for k, v in errs.items()), flush=True)
+    for name, e in errs.items():
+        assert e <= TOL["bf16"], f"{name}: {e:.3e}"
+
+
+def test_bwd_one_view_equals_two_stream_backward():
+    """One view through bdgdn_bwd_train_views is bdgdn_bwd_train, bit for bit."""
+    inp, do, don, h0, dht, cu = _case(2, 80, 2, 2, 16, 5, h0=True, dht=True)
+    d = {k: v.cuda() for k, v in inp.items()}
+    print("bwd one view = two-stream", flush=True)
+    ref = bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
+                             d["betan"], do.cuda(), don.cuda(), block=16, h0=h0.cuda(), dht=dht.cuda(), want_dh0=True)
+    view = {k: d[k + "n"] for k in KEYS}
+    view["do"] = don.cuda()
+    got_c, got_v = bd.bdgdn_bwd_train_views(d["q"], d["k"], d["v"], d["g"], d["beta"], [view], do.cuda(), block=16,
+                                            h0=h0.cuda(), dht=dht.cuda(), want_dh0=True)
+    torch.cuda.synchronize()
+    for n in ("dq", "dk", "dv", "dg", "dbeta", "dh0"):
+        assert torch.equal(got_c[n], ref[n]), n
+    for n in ("dq", "dk", "dv", "dg", "dbeta"):
+        assert torch.equal(got_v[0][n], ref[n + "n"]), n

@@ -578,6 +578,61 @@ def test_pin_bwd_matches_finite_differences(B, T, hqk, hv, d, L, lengths):
         np.testing.assert_allclose(gr[name], fd, rtol=1e-6, atol=1e-7, err_msg=name)
 
 
+def test_pin_bwd_views_matches_finite_differences():
+    """The complementary-view backward (several noisy views seeded from the same clean
+    states) equals central finite differences of its loss  <do, o> + sum_i <do_i, o_i> +
+    <dht, ht>, each view's readout o_i taken from the (pinned) two-stream forward with that
+    view as the noisy stream; clean inputs, every view's inputs and h0 are perturbed."""
+    rng = np.random.default_rng(77)
+    B, T, hqk, hv, d, L, nv = 1, 9, 1, 2, 3, 4, 3
+    c, _, h0, do, _, dht, cu = _bwd_setup(rng, B, T, hqk, hv, d, L)
+    views = []
+    for _ in range(nv):
+        _, w, _, _, dw, _, _ = _bwd_setup(rng, B, T, hqk, hv, d, L)
+        w["do"] = dw
+        views.append(w)
+    scale = 0.6
+
+    def loss():
+        tot = float((dht * _run(c, views[0], L, scale, h0=h0)[2]).sum())
+        for i, w in enumerate(views):
+            o, on, _ = _run(c, w, L, scale, h0=h0)
+            tot += float((on * w["do"]).sum()) + (float((o * do).sum()) if i == 0 else 0.0)
+        return tot
+
+    clean, per_view = oracle.bwd_train_views(c["q"], c["k"], c["v"], c["g"], c["beta"], views, do, block=L,
+                                             scale=scale, h0=h0, dht=dht)
+    eps = 1e-6
+    targets = [(c[k_], clean["d" + k_], "clean d" + k_) for k_ in _BWD_KEYS] + [(h0, clean["dh0"], "dh0")]
+    for i, w in enumerate(views):
+        targets += [(w[k_], per_view[i]["d" + k_], f"view {i} d{k_}") for k_ in _BWD_KEYS]
+    for arr, grad, name in targets:
+        fd = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            a0 = arr[idx]
+            arr[idx] = a0 + eps
+            lp = loss()
+            arr[idx] = a0 - eps
+            lm = loss()
+            arr[idx] = a0
+            fd[idx] = (lp - lm) / (2 * eps)
+        np.testing.assert_allclose(grad, fd, rtol=1e-6, atol=1e-7, err_msg=name)
+
+
+def test_pin_bwd_views_one_view_is_two_stream_backward():
+    """With one view the complementary-view backward is the two-stream backward."""
+    rng = np.random.default_rng(78)
+    c, n, h0, do, don, dht, cu = _bwd_setup(rng, 1, 10, 1, 1, 3, 4, [6, 4])
+    ref = oracle.bwd_train(c["q"], c["k"], c["v"], c["g"], c["beta"], n["q"], n["k"], n["v"], n["g"], n["beta"],
+                           do, don, block=4, scale=0.5, h0=h0, dht=dht, cu_seqlens=cu)
+    clean, per_view = oracle.bwd_train_views(c["q"], c["k"], c["v"], c["g"], c["beta"], [dict(n, do=don)], do,
+                                             block=4, scale=0.5, h0=h0, dht=dht, cu_seqlens=cu)
+    for k_ in _BWD_KEYS:
+        assert np.array_equal(clean["d" + k_], ref["d" + k_])
+        assert np.array_equal(per_view[0]["d" + k_], ref["d" + k_ + "n"])
+    assert np.array_equal(clean["dh0"], ref["dh0"])
+
+
 def test_pin_bwd_frozen_state_closed_form():
     """beta = 0 in both streams: nothing is written, every state is the decayed h0, so
     o_t = s e^(G_t) h0^T q_t with G_t the cumulative clean log-gate, and a noisy position of
