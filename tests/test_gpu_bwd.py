@@ -62,6 +62,7 @@ def _check(B, T, hqk, hv, L, seed, **kw):
     (1, 160, 2, 2, 32, {"lengths": [64, 32, 64]}),           # packed documents
     (1, 80, 1, 1, 32, {"h0": True, "dht": True}),            # initial state, final-state gradient
     (1, 64, 1, 1, 8, {"do_dtype": torch.bfloat16}),         # bf16 upstream gradients, small blocks
+    (1, 116, 1, 1, 32, {"lengths": [64, 0, 32, 20], "h0": True}),   # an empty document, a partial last one
 ])
 def test_bwd_matches_oracle(B, T, hqk, hv, L, kw):
     _check(B, T, hqk, hv, L, 300 + T + L, **kw)
@@ -98,12 +99,13 @@ def test_bwd_training_workload_sampled_units():
 KEYS = ("q", "k", "v", "g", "beta")
 
 
-@pytest.mark.parametrize("B,T,hqk,hv,L,lengths,n_views", [
-    (1, 96, 1, 1, 32, None, 2),
-    (2, 100, 1, 2, 16, None, 3),              # grouped value heads, ragged tail
-    (1, 160, 2, 2, 32, [64, 32, 64], 2),      # packed documents
+@pytest.mark.parametrize("B,T,hqk,hv,L,lengths,n_views,do_dtype", [
+    (1, 96, 1, 1, 32, None, 2, torch.float32),
+    (2, 100, 1, 2, 16, None, 3, torch.float32),              # grouped value heads, ragged tail
+    (1, 160, 2, 2, 32, [64, 32, 64], 2, torch.float32),      # packed documents
+    (1, 64, 1, 2, 8, None, 4, torch.bfloat16),               # bf16 upstream gradients, small blocks
 ])
-def test_bwd_views_match_oracle(B, T, hqk, hv, L, lengths, n_views):
+def test_bwd_views_match_oracle(B, T, hqk, hv, L, lengths, n_views, do_dtype):
     """The complementary-view backward (bdgdn_bwd_train_views) against the oracle's
     composition of two-stream backwards: the clean gradients (summed over the views), dh0,
     and every view's own gradients."""
@@ -116,9 +118,9 @@ def test_bwd_views_match_oracle(B, T, hqk, hv, L, lengths, n_views):
         src = base if i == 0 else W.make_custom_train(B, T, hqk, hv, 128, 128, "bf16", seed=960 + 5 * i + T,
                                                       lengths=lengths)
         w = {k: src[k + "n"] for k in KEYS}
-        w["do"] = torch.from_numpy(rng.standard_normal((B, T, hv, 128)).astype(np.float32))
+        w["do"] = torch.from_numpy(rng.standard_normal((B, T, hv, 128)).astype(np.float32)).to(do_dtype)
         views.append(w)
-    do = torch.from_numpy(rng.standard_normal((B, T, hv, 128)).astype(np.float32))
+    do = torch.from_numpy(rng.standard_normal((B, T, hv, 128)).astype(np.float32)).to(do_dtype)
     nseq = B if lengths is None else len(lengths)
     h0 = torch.from_numpy((0.3 * rng.standard_normal((nseq, hv, 128, 128))).astype(np.float32))
     dht = torch.from_numpy(rng.standard_normal((nseq, hv, 128, 128)).astype(np.float32))
