@@ -34,9 +34,14 @@ namespace bdgdn {
 // I"): the noisy waves and the noisy half of the record stand idle, the noisy rows are not
 // staged, and the C waves write each block's seed state (the clean state before the
 // block) to HBM for a separate noisy-block kernel.  SeedT_ is the element type of the seeds.
-template <typename Out, int DK, int LP, bool SPLIT = false, bool SEEDS = SPLIT, typename SeedT_ = float>
+// STATES (with SPLIT, fp16 seeds): the recomputation of the seeds alone, for the backward:
+// no clean outputs (the O waves stand idle too), and the seeds are copied from the state
+// operand in LDS by the otherwise idle N waves, off the C waves' path.
+template <typename Out, int DK, int LP, bool SPLIT = false, bool SEEDS = SPLIT, typename SeedT_ = float,
+          bool STATES = false>
 struct Fused {
     typedef SeedT_ SeedT;
+    static_assert(!STATES || (SPLIT && SEEDS && sizeof(SeedT_) == 2), "STATES: the split scan, fp16 seeds");
     typedef __bf16 In;
     typedef _Float16 E;
     typedef Quad<E> QE;
@@ -589,7 +594,7 @@ struct Fused {
             lds_barrier();
             SeedT *bs = c.bs;
             for (int j = 0; j < nb; ++j) {
-                if constexpr (SEEDS) {
+                if constexpr (SEEDS && !STATES) {
                     // the seed of noisy block j: the clean state before block j
 #pragma unroll
                     for (int kb = 0; kb < DKB; ++kb)
@@ -610,7 +615,27 @@ struct Fused {
                     for (int i = 0; i < 4; ++i) dst[i * c.dv] = S[kb][i];
                 }
             }
-        } else if (SPLIT && (wave < 4 || wave == 7)) {
+        } else if (STATES && wave < 4) {
+            // ---- the seeds: in step j the state operand st(j & 1) holds the clean state
+            // before block j (its fp16 copy, as the C waves would store it); one d_k row per
+            // lane, this workgroup's BV columns as 16-byte stores
+            const int a = 64 * (wave - 2) + lane;
+            SeedT *bs = c.bs;
+            lds_barrier();
+            lds_barrier();
+            for (int j = 0; j < nb; ++j) {
+                const E *sv = st(j & 1);
+#pragma unroll
+                for (int cb = 0; cb < BV / 8; ++cb) {
+                    f16x8 v8;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) v8[e] = sv[rofs(8 * cb + e, a)];
+                    *reinterpret_cast<f16x8 *>(bs + (long)a * c.dv + 8 * cb) = v8;
+                }
+                bs += c.bs_blk;
+                lds_barrier();
+            }
+        } else if (SPLIT && (wave < 4 || wave == 7 || (STATES && wave < 6))) {
             // ---- idle in the split schedule: keep the barrier count
             lds_barrier();
             lds_barrier();

@@ -115,7 +115,8 @@ int serve_tile_v();
 bool fwd_supported(Types ty, int dk, int lp);
 
 // The split schedule's two kernels on their own: the clean scan writing every block's seed
-// state (the backward's recomputation), and the noisy-block pass from the seeds.
+// state (with f16_seeds: the backward's recomputation, fp16 seeds and no clean outputs), and
+// the noisy-block pass from the seeds.
 hipError_t launch_scan_states(int lp, bool f32_out, bool f16_seeds, const ScanArgs &sa, hipStream_t s);
 hipError_t launch_noisy_blocks(int lp, bool f32_out, const NoisyArgs &na, hipStream_t s);
 

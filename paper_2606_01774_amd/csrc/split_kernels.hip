@@ -16,11 +16,11 @@
 
 namespace bdgdn {
 
-template <typename Out, int LP, typename SeedT = float>
+template <typename Out, int LP, typename SeedT = float, bool STATES = false>
 __global__ void __launch_bounds__(768) bdgdn_k2_scan_states_kernel(ScanArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    run_chain<Fused<Out, 128, LP, true, true, SeedT>>(a, smem);
+    run_chain<Fused<Out, 128, LP, true, true, SeedT, STATES>>(a, smem);
 }
 
 template <typename Out, int LP>
@@ -97,8 +97,10 @@ static hipError_t launch_split(const ScanArgs &sa, const NoisyArgs &na, hipStrea
 }
 
 // The clean scan alone, writing the seed state of every block (what the backward and the
-// noisy views start from) as SeedT; the clean outputs go to sa.o, of type Out.
-template <typename Out, typename SeedT> static hipError_t scan_states(int lp, const ScanArgs &sa, hipStream_t s)
+// noisy views start from) as SeedT; the clean outputs go to sa.o, of type Out (not with
+// STATES: the backward's recomputation).
+template <typename Out, typename SeedT, bool STATES = false>
+static hipError_t scan_states(int lp, const ScanArgs &sa, hipStream_t s)
 {
     auto run = [&](auto k2, int bytes) {
         hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void *>(k2),
@@ -108,14 +110,17 @@ template <typename Out, typename SeedT> static hipError_t scan_states(int lp, co
         hipLaunchKernelGGL(k2, dim3(grid), dim3(768), bytes, s, sa);
         return hipGetLastError();
     };
-    return lp == 16 ? run(bdgdn_k2_scan_states_kernel<Out, 16, SeedT>, Fused<Out, 128, 16, true, true, SeedT>::BYTES)
-                    : run(bdgdn_k2_scan_states_kernel<Out, 32, SeedT>, Fused<Out, 128, 32, true, true, SeedT>::BYTES);
+    return lp == 16 ? run(bdgdn_k2_scan_states_kernel<Out, 16, SeedT, STATES>,
+                          Fused<Out, 128, 16, true, true, SeedT, STATES>::BYTES)
+                    : run(bdgdn_k2_scan_states_kernel<Out, 32, SeedT, STATES>,
+                          Fused<Out, 128, 32, true, true, SeedT, STATES>::BYTES);
 }
 
 hipError_t launch_scan_states(int lp, bool f32_out, bool f16_seeds, const ScanArgs &sa, hipStream_t s)
 {
     if ((lp != 16 && lp != 32) || sa.n_vt * 32 != sa.dv || !sa.bs) return hipErrorInvalidValue;
-    if (f16_seeds) return f32_out ? scan_states<float, _Float16>(lp, sa, s) : scan_states<__bf16, _Float16>(lp, sa, s);
+    if (f16_seeds)   // the backward's recomputation: seeds only
+        return f32_out ? scan_states<float, _Float16, true>(lp, sa, s) : scan_states<__bf16, _Float16, true>(lp, sa, s);
     return f32_out ? scan_states<float, float>(lp, sa, s) : scan_states<__bf16, float>(lp, sa, s);
 }
 
