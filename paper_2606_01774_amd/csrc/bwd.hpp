@@ -30,6 +30,7 @@ struct BwdArgs {
     const int32_t *cu;                       // packed documents, or null
     int n_docs;
     int n_chains;                            // sequences x v-heads
+    long n_units;                            // global blocks x v-heads (set by launch_bwd)
     int T, nblk, L, h_qk, h_v;
     float scale;
     bool atomic_qk;

@@ -226,8 +226,8 @@ __device__ __forceinline__ void cum_gates(Smem &sm, int lane)
 }
 
 // M = (I + A)^-1 of the staged block into sm.Mh, by the register-resident doubling solve of
-// one wave (ut::solve_t) from the keys in sm.K and the gates sm.G2, sm.bet.
-__device__ __forceinline__ void solve_m(Smem &sm, int lane)
+// one wave (ut::solve_t) from the keys K (LDS, [32][LDH]) and the gates sm.G2, sm.bet.
+__device__ __forceinline__ void solve_m(Smem &sm, const _Float16 *K, int lane)
 {
     ut::QE kq[2][DD / 16];
     const int r = lane & 15, g = lane >> 4;
@@ -235,7 +235,7 @@ __device__ __forceinline__ void solve_m(Smem &sm, int lane)
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
         for (int kb = 0; kb < DD / 16; ++kb)
-            kq[rb][kb] = *reinterpret_cast<const f16x4 *>(sm.K + (16 * rb + r) * LDH + 16 * kb + 4 * g);
+            kq[rb][kb] = *reinterpret_cast<const f16x4 *>(K + (16 * rb + r) * LDH + 16 * kb + 4 * g);
     ut::Consts cs;
     ut::make_consts(cs, lane);
     ut::solve_t<2, DD / 16, false>(kq, sm.G2, sm.bet, sm.Mh, LDM, cs, lane);
@@ -282,15 +282,17 @@ __device__ __forceinline__ BlockRows<Od, WITH_V> load_block(const StreamPtrs &p,
 
 }  // namespace
 
-// One block's gradients.  S0 (LDS f16) holds the seed.  For the clean stream dS (LDS, f16)
+// One block's gradients.  S0 (LDS f16) holds the seed.  hook1() runs once the arrays R, dDl
+// and dO are dead (after the dR / dQ phase), hook2() two phases later (the next unit's clean
+// rows are loaded in the one and staged into those arrays in the other).  For the clean stream dS (LDS, f16)
 // and dsn (registers, fp32, the C-tile layout of a state gradient: wave w holds column block
 // w, row blocks 0 .. 7) hold dS_n on entry; for the noisy stream dS_n is formed here from the
 // block-end readout (dsn is not read) and the seed's gradient dS0 is added into acc (same
 // layout).  Wave w computes the 16 columns 16 w .. 16 w + 15 of every 32 x 128 and 128 x 128
 // product.
-template <bool CLEAN, typename Od>
+template <bool CLEAN, typename Od, typename H1, typename H2>
 __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, const BlockRows<Od, true> &in,
-                          const float (&dsn)[8][4], float (&acc)[8][4], int tid)
+                          const float (&dsn)[8][4], float (&acc)[8][4], int tid, const H1 &hook1, const H2 &hook2)
 {
     const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
     const float s = a.scale;
@@ -320,7 +322,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
     // R = V - Gamma X; dS_n (noisy: s Q^T dO) with its share gamma_n dS_n of dS0 and the gate
     // term dG_last += gamma_n <dS_n, S0>
     if (wave == 0) {
-        solve_m(sm, lane);
+        solve_m(sm, sm.K, lane);
     } else if (wave <= 4) {
         const int m0 = 16 * ((wave - 1) >> 1), n0 = 16 * ((wave - 1) & 1);
         f32x4 c = tile_mma<_Float16, DD>(z, sm.K + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
@@ -524,6 +526,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
         for (int j = 0; j < 4; ++j) sm.dT[(m0 + 4 * g4 + j) * LDF + n0 + rr] = c[j];
     }
     __syncthreads();
+    hook1();   // R, dDl, dO are dead from here on
     // ---- dbeta, dA = strictly lower part of -M^T (dT diag beta) M^T (fp32 MFMA)
     // W = dT T^T (W_rc = sum_i dT_ri beta_i M_ci), stored transposed; dbeta_i += sum_r dT_ri M_ri
     if (wave < 4) {
@@ -549,6 +552,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
         }
     }
     __syncthreads();
+    hook2();
     // dbeta_r += sum_c dA_rc F_rc; dG from A: WA = dA o A, dG_r += sum_c WA_rc, dG_c -= sum_r WA_rc;
     // dKK_rc = dA_rc beta_r gamma_r/gamma_c, symmetrised into Wh
 #pragma unroll 1
@@ -695,19 +699,19 @@ __device__ __forceinline__ StreamPtrs stream_ptrs(const BwdArgs &a, bool noisy, 
 // so acc += s Q^T Gamma dO - K^T Gamma T^T (s P^T dO), and U K (32 x 128, U_ij = T_ji
 // gamma_i gamma_n / gamma_j, upper triangular with |U_ij| <= |T_ji|) goes to uk and gamma_n to
 // *gnb for the reverse scan.
-template <typename Od>
-__device__ void clean_prep(Smem &sm, const BwdArgs &a, const BlockRows<Od, false> &in, float (&acc)[8][4],
-                           _Float16 *uk, float *gnb, int tid)
+// The clean rows are staged in R (q), dDl (k) and dO (do): the arrays block_bwd leaves dead
+// after its dR / dQ phase, so that a persistent workgroup stages the next unit's rows there
+// while it finishes the current one.  gx, bx: the gate and step size of position tid.
+__device__ void clean_prep(Smem &sm, const BwdArgs &a, float gx, float bx, float (&acc)[8][4], _Float16 *uk,
+                           float *gnb, int tid)
 {
     const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
     const float s = a.scale;
     const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-    store_rows(sm.Q, in.q, tid);
-    store_rows(sm.K, in.k, tid);
-    store_rows(sm.dO, in.dout, tid);
+    const _Float16 *Qs = sm.R, *Ks = sm.dDl;
     if (tid < NP) {
-        sm.bet[tid] = in.b;
-        sm.G[tid] = in.g;
+        sm.bet[tid] = bx;
+        sm.G[tid] = gx;
     }
     __syncthreads();
     if (wave == 0) cum_gates(sm, lane);
@@ -715,10 +719,10 @@ __device__ void clean_prep(Smem &sm, const BwdArgs &a, const BlockRows<Od, false
     const float Gn = sm.G[NP - 1];
     if (tid == 0) *gnb = ex(Gn);
     if (wave == 0) {   // M
-        solve_m(sm, lane);
+        solve_m(sm, Ks, lane);
     } else if (wave >= 4) {   // P = (Q K^T) o Mc
         const int m0 = 16 * ((wave - 4) >> 1), n0 = 16 * ((wave - 4) & 1);
-        const f32x4 qk = tile_mma<_Float16, DD>(z, sm.Q + m0 * LDH, LDH, sm.K + n0 * LDH, LDH, lane);
+        const f32x4 qk = tile_mma<_Float16, DD>(z, Qs + m0 * LDH, LDH, Ks + n0 * LDH, LDH, lane);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int r = m0 + 4 * g4 + j, i = n0 + rr;
@@ -726,14 +730,14 @@ __device__ void clean_prep(Smem &sm, const BwdArgs &a, const BlockRows<Od, false
         }
     }
     __syncthreads();
-    {   // Y = s P^T dO -> dDl
+    {   // Y = s P^T dO -> Dl
         const f16x4 do0 = op_tr(sm.dO, LDH, 0, c0, lane), do1 = op_tr(sm.dO, LDH, 16, c0, lane);
 #pragma unroll
         for (int tm = 0; tm < 2; ++tm) {
             const f32x4 c =
                 mfma(op_tr(sm.Ph, LDM, 16, 16 * tm, lane), do1, mfma(op_tr(sm.Ph, LDM, 0, 16 * tm, lane), do0, z));
 #pragma unroll
-            for (int j = 0; j < 4; ++j) sm.dDl[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = (_Float16)(s * c[j]);
+            for (int j = 0; j < 4; ++j) sm.Dl[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = (_Float16)(s * c[j]);
         }
     }
     for (int e = tid; e < NP * NP; e += 64 * kWaves) {   // U -> Wh
@@ -745,7 +749,7 @@ __device__ void clean_prep(Smem &sm, const BwdArgs &a, const BlockRows<Od, false
     // dR0 = T^T Y, as -Gamma dR0 in registers (B operands); acc += K^T (-Gamma dR0) + Q^T (s Gamma dO)
     f16x4 drq[2], sd[2];
     {
-        const f16x4 y0 = op_tr(sm.dDl, LDH, 0, c0, lane), y1 = op_tr(sm.dDl, LDH, 16, c0, lane);
+        const f16x4 y0 = op_tr(sm.Dl, LDH, 0, c0, lane), y1 = op_tr(sm.Dl, LDH, 16, c0, lane);
 #pragma unroll
         for (int tm = 0; tm < 2; ++tm) {
             f16x4 t0, t1;
@@ -759,15 +763,15 @@ __device__ void clean_prep(Smem &sm, const BwdArgs &a, const BlockRows<Od, false
     }
 #pragma unroll
     for (int tm = 0; tm < 8; ++tm) {
-        f32x4 c = mfma(op_tr(sm.K, LDH, 0, 16 * tm, lane), drq[0], z);
-        c = mfma(op_tr(sm.K, LDH, 16, 16 * tm, lane), drq[1], c);
-        c = mfma(op_tr(sm.Q, LDH, 0, 16 * tm, lane), sd[0], c);
-        c = mfma(op_tr(sm.Q, LDH, 16, 16 * tm, lane), sd[1], c);
+        f32x4 c = mfma(op_tr(Ks, LDH, 0, 16 * tm, lane), drq[0], z);
+        c = mfma(op_tr(Ks, LDH, 16, 16 * tm, lane), drq[1], c);
+        c = mfma(op_tr(Qs, LDH, 0, 16 * tm, lane), sd[0], c);
+        c = mfma(op_tr(Qs, LDH, 16, 16 * tm, lane), sd[1], c);
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[tm][j] += c[j];
     }
     {   // U K -> uk
-        const f16x4 k0q = op_tr(sm.K, LDH, 0, c0, lane), k1q = op_tr(sm.K, LDH, 16, c0, lane);
+        const f16x4 k0q = op_tr(Ks, LDH, 0, c0, lane), k1q = op_tr(Ks, LDH, 16, c0, lane);
 #pragma unroll
         for (int tm = 0; tm < 2; ++tm) {
             const f32x4 u = mfma(op_row(sm.Wh, LDM, 16 * tm, 16, lane), k1q, mfma(op_row(sm.Wh, LDM, 16 * tm, 0, lane), k0q, z));
@@ -778,50 +782,93 @@ __device__ void clean_prep(Smem &sm, const BwdArgs &a, const BlockRows<Od, false
     __syncthreads();
 }
 
-// Phase 1: every noisy block, in parallel (one workgroup per (global block, v-head)): its
-// gradients and its seed's gradient, plus (PREP) the dh-independent part of the clean block
-// of the same position (clean_prep); both enter the state gradient at the block's start,
-// whose sum is written to cterm (fp32 [block][h_v][128][128]).  Without PREP (the further
-// noisy views of the complementary-view backward, each seeded from the same clean state)
-// the seed's gradient is added to cterm.
+// Phase 1: every noisy block: its gradients and its seed's gradient, plus (PREP) the
+// dh-independent part of the clean block of the same position (clean_prep, run first: it
+// needs no seed); both enter the state gradient at the block's start, whose sum is written
+// to cterm (fp32 [block][h_v][128][128]).  Without PREP (the further noisy views of the
+// complementary-view backward, each seeded from the same clean state) the seed's gradient
+// is added to cterm.  Persistent: one 160 KB workgroup per CU walks the units (global block,
+// v-head) u = blockIdx.x, + gridDim.x, ...; the next unit's clean rows are loaded while the
+// current unit finishes and staged into arrays it no longer uses, and each unit's seed and
+// noisy rows are in flight while its clean prep runs.
 template <typename Od, bool PREP>
 __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     Smem &sm = *reinterpret_cast<Smem *>(smem_raw);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15;
-    const long gblk = blockIdx.x / a.h_v;
-    const int h = blockIdx.x % a.h_v, hq = h / (a.h_v / a.h_qk);
-    int n, nvalid;
-    long p0;
-    block_unit(a, gblk, n, p0, nvalid);
-    const size_t unit = (size_t)gblk * a.h_v + h, so = unit * DD * DD;
-    const StreamPtrs pc = stream_ptrs<Od>(a, false, p0, h, hq), pn = stream_ptrs<Od>(a, true, p0, h, hq);
-    // every load of the unit in flight together: the clean rows (the clean prep runs first;
-    // it needs no seed), the seed, the noisy rows
-    BlockRows<Od, false> cin;
-    if constexpr (PREP) cin = load_block<Od, false>(pc, a.h_qk, a.h_v, nvalid, tid);
-    const SeedRegs seed = load_seed(a.seeds + so, tid);
-    const BlockRows<Od, true> nin = load_block<Od, true>(pn, a.h_qk, a.h_v, nvalid, tid);
-    float acc[8][4];
+    long u = blockIdx.x;
+    float cg = 0.f, cb = 0.f;   // the clean gate and step size of position tid of unit u
+    if constexpr (PREP) {
+        const int tid = threadIdx.x;
+        int n, nvalid;
+        long p0;
+        const int h = (int)(u % a.h_v), hq = h / (a.h_v / a.h_qk);
+        block_unit(a, u / a.h_v, n, p0, nvalid);
+        const BlockRows<Od, false> cin =
+            load_block<Od, false>(stream_ptrs<Od>(a, false, p0, h, hq), a.h_qk, a.h_v, nvalid, tid);
+        store_rows(sm.R, cin.q, tid);
+        store_rows(sm.dDl, cin.k, tid);
+        store_rows(sm.dO, cin.dout, tid);
+        cg = cin.g;
+        cb = cin.b;
+    }
+    for (;;) {
+        // the thread index made opaque per unit, so that the body's lane-dependent addresses
+        // are recomputed rather than hoisted out of the loop (where they would stay live)
+        int tid = threadIdx.x;
+        asm volatile("" : "+v"(tid));
+        const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15;
+        const long un = u + gridDim.x;
+        const bool more = un < a.n_units;
+        int n, nvalid;
+        long p0;
+        const int h = (int)(u % a.h_v), hq = h / (a.h_v / a.h_qk);
+        block_unit(a, u / a.h_v, n, p0, nvalid);
+        const StreamPtrs pn = stream_ptrs<Od>(a, true, p0, h, hq);
+        const SeedRegs seed = load_seed(a.seeds + (size_t)u * DD * DD, tid);
+        const BlockRows<Od, true> nin = load_block<Od, true>(pn, a.h_qk, a.h_v, nvalid, tid);
+        float acc[8][4];
 #pragma unroll
-    for (int tm = 0; tm < 8; ++tm)
+        for (int tm = 0; tm < 8; ++tm)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[tm][j] = 0.f;
-    if constexpr (PREP) clean_prep<Od>(sm, a, cin, acc, a.uk + unit * NP * DD, a.gnb + unit, tid);
-    store_seed(sm.S0, seed, tid);   // made visible by block_bwd's first barrier
-    block_bwd<false, Od>(sm, pn, a, nvalid, nin, acc, acc, tid);
-    float *dst = a.cterm + so;
+            for (int j = 0; j < 4; ++j) acc[tm][j] = 0.f;
+        if constexpr (PREP) clean_prep(sm, a, cg, cb, acc, a.uk + u * NP * DD, a.gnb + u, tid);
+        store_seed(sm.S0, seed, tid);   // made visible by block_bwd's first barrier
+        BlockRows<Od, false> nxt;
+        block_bwd<false, Od>(
+            sm, pn, a, nvalid, nin, acc, acc, tid,
+            [&] {
+                if (PREP && more) {
+                    int n2, nv2;
+                    long q0;
+                    const int h2 = (int)(un % a.h_v), hq2 = h2 / (a.h_v / a.h_qk);
+                    block_unit(a, un / a.h_v, n2, q0, nv2);
+                    nxt = load_block<Od, false>(stream_ptrs<Od>(a, false, q0, h2, hq2), a.h_qk, a.h_v, nv2, tid);
+                }
+            },
+            [&] {
+                if (PREP && more) {
+                    store_rows(sm.R, nxt.q, tid);
+                    store_rows(sm.dDl, nxt.k, tid);
+                    store_rows(sm.dO, nxt.dout, tid);
+                    cg = nxt.g;
+                    cb = nxt.b;
+                }
+            });
+        float *dst = a.cterm + (size_t)u * DD * DD;
 #pragma unroll
-    for (int tm = 0; tm < 8; ++tm)
+        for (int tm = 0; tm < 8; ++tm)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            float *p = dst + (16 * tm + 4 * g4 + j) * DD + 16 * wave + rr;
-            if constexpr (PREP)
-                *p = acc[tm][j];
-            else
-                *p += acc[tm][j];
-        }
+            for (int j = 0; j < 4; ++j) {
+                float *p = dst + (16 * tm + 4 * g4 + j) * DD + 16 * wave + rr;
+                if constexpr (PREP)
+                    *p = acc[tm][j];
+                else
+                    *p += acc[tm][j];
+            }
+        if (!more) break;
+        u = un;
+    }
 }
 
 // Phase 3: every clean block, in parallel, from its seed and the gradient at its end (dh,
@@ -852,7 +899,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
     for (int tm = 0; tm < 8; ++tm)
 #pragma unroll
         for (int j = 0; j < 4; ++j) sm.dS[(16 * tm + 4 * g4 + j) * LDH + 16 * wave + rr] = (_Float16)dsn[tm][j];
-    block_bwd<true, Od>(sm, pc, a, nvalid, in, dsn, dsn, tid);   // its first barrier covers S0, dS
+    block_bwd<true, Od>(sm, pc, a, nvalid, in, dsn, dsn, tid, [] {}, [] {});   // its first barrier covers S0, dS
 }
 
 // Phase 2: the reverse scan of the clean state gradient over the blocks of a (sequence,
@@ -1011,6 +1058,7 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int 
     // the noisy stream of a: its pointers replaced by those of view i
     auto with_view = [&](const BwdView &w) {
         BwdArgs b = a;
+        b.n_units = n_block_units;
         b.qn = w.q; b.kn = w.k; b.vn = w.v; b.gn = w.g; b.betan = w.beta; b.doutn = w.dout;
         b.dqn = w.dq; b.dkn = w.dk; b.dvn = w.dv; b.dgn = w.dg; b.dbn = w.db;
         return b;
@@ -1026,6 +1074,14 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int 
             for (float *p : {more[i].dq, more[i].dk})
                 if (hipError_t e = zero(p); e != hipSuccess) return e;
     }
+    // the persistent noisy kernels: one workgroup per CU (their LDS allows no more)
+    int dev = 0, n_cu = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err == hipSuccess) err = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (err != hipSuccess) return err;
+    const unsigned pgrid = (unsigned)(n_block_units < n_cu ? n_block_units : (n_cu > 0 ? n_cu : 1));
+    BwdArgs a2 = a;
+    a2.n_units = n_block_units;
     auto run = [&](auto noisy, auto noisy_more, auto clean) {
         for (const void *f : {reinterpret_cast<const void *>(noisy), reinterpret_cast<const void *>(noisy_more),
                               reinterpret_cast<const void *>(clean)}) {
@@ -1034,11 +1090,10 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int 
         }
         hipError_t e;
         if (n_block_units > 0) {
-            hipLaunchKernelGGL(noisy, dim3((unsigned)n_block_units), dim3(512), sizeof(Smem), s, a);
+            hipLaunchKernelGGL(noisy, dim3(pgrid), dim3(512), sizeof(Smem), s, a2);
             if ((e = hipGetLastError()) != hipSuccess) return e;
             for (int i = 0; i < n_more; ++i) {   // in stream order: each adds its seed gradients
-                hipLaunchKernelGGL(noisy_more, dim3((unsigned)n_block_units), dim3(512), sizeof(Smem), s,
-                                   with_view(more[i]));
+                hipLaunchKernelGGL(noisy_more, dim3(pgrid), dim3(512), sizeof(Smem), s, with_view(more[i]));
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
         }
