@@ -23,14 +23,19 @@
 // dh_(b-1) = dS0(clean block b) + dS0(noisy block b), since the noisy block b is seeded with
 // the clean state at the end of block b - 1.
 //
-// Three phases after the split schedule's clean scan has written every block's seed
-// (launch_scan_states): every noisy block in parallel (its gradients and its seed's
-// gradient), the reverse scan of the clean state gradient over the blocks of each
-// (sequence, v-head) in 32-column tiles (the columns are independent), and every clean
-// block in parallel from its seed and the gradient at its end.  Products are 16x16x16 MFMA tiles on fp16 operands read from LDS
-// through accessors (any transposition is an index swap), fp32 accumulation; the 32x32
-// triangular solve and the n x n backward terms run in fp32.  Blocks are padded to 32
-// positions with identity steps (k = 0, beta = 0, g = 0), which change nothing.
+// Three phases after the clean scan has written every block's seed (launch_scan_states, fp16):
+//  1. every noisy block in parallel: its gradients and its seed's gradient, plus the part of
+//     the clean block at the same position that does not depend on the state gradient dh
+//     (clean_prep); their sum c_b is the dh-independent part of dh_(b-1);
+//  2. the reverse scan of the clean state gradient over the blocks of each (sequence,
+//     v-head), in 32-column tiles (the columns are independent):
+//     dh_(b-1) = gamma_n dh_b + c_b - K^T (U K) dh_b with U = Gamma T^T D from phase 1;
+//  3. every clean block in parallel from its seed and the gradient at its end.
+// Products are MFMA tiles on fp16 operands with fp32 accumulation: k-contiguous operands by
+// 16-byte LDS reads, the others by the LDS transpose load, and results that are the next
+// product's operand kept in registers; M = (I + A)^-1 by the register-resident doubling solve
+// (ut::solve_t), the dA products in fp32 MFMA.  Blocks are padded to 32 positions with
+// identity steps (k = 0, beta = 0, g = 0), which change nothing.
 #include "common.hpp"
 #include "bwd.hpp"
 #include "kernels.hpp"
@@ -106,7 +111,7 @@ __device__ __forceinline__ f32x4 ld4(const float *p) { return *reinterpret_cast<
 
 __device__ __forceinline__ float ex(float x) { return __expf(x); }
 
-// Workgroup sum of v added to *dst (LDS), from every thread.
+// v added to *dst (LDS) atomically.
 __device__ __forceinline__ void lds_add(float *dst, float v) { atomicAdd(dst, v); }
 
 // Sum over the 16 lanes of each lane row (the columns of a C tile row), by DPP row shifts:
@@ -282,14 +287,14 @@ __device__ __forceinline__ BlockRows<Od, WITH_V> load_block(const StreamPtrs &p,
 
 }  // namespace
 
-// One block's gradients.  S0 (LDS f16) holds the seed.  hook1() runs once the arrays R, dDl
-// and dO are dead (after the dR / dQ phase), hook2() two phases later (the next unit's clean
-// rows are loaded in the one and staged into those arrays in the other).  For the clean stream dS (LDS, f16)
+// One block's gradients.  S0 (LDS f16) holds the seed.  For the clean stream dS (LDS, f16)
 // and dsn (registers, fp32, the C-tile layout of a state gradient: wave w holds column block
 // w, row blocks 0 .. 7) hold dS_n on entry; for the noisy stream dS_n is formed here from the
 // block-end readout (dsn is not read) and the seed's gradient dS0 is added into acc (same
 // layout).  Wave w computes the 16 columns 16 w .. 16 w + 15 of every 32 x 128 and 128 x 128
-// product.
+// product.  hook1() runs once the arrays R, dDl and dO are dead (after the dR / dQ phase),
+// hook2() two phases later: a persistent caller loads the next unit's clean rows in the one
+// and stages them into those arrays in the other.
 template <bool CLEAN, typename Od, typename H1, typename H2>
 __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, const BlockRows<Od, true> &in,
                           const float (&dsn)[8][4], float (&acc)[8][4], int tid, const H1 &hook1, const H2 &hook2)
