@@ -474,10 +474,10 @@ static bool bwd_shape_ok(const bdgdn_fwd_desc_t *d)
 
 // Workspace of the backward, per (global block, v-head): the seed state (fp16), the part of
 // the state gradient at the block's start that does not depend on dh (fp32), dh at the
-// block's end (fp32), U K (32 x d_k, fp16), gamma_n (fp32); then the recomputing scan's clean
-// outputs (bf16, not read).  Byte offsets, each aligned to 256.
+// block's end (fp32), U K (32 x d_k, fp16), gamma_n (fp32).  Byte offsets, each aligned to
+// 256.
 struct BwdLayout {
-    size_t seeds, cterm, dh, uk, gnb, o, total;
+    size_t seeds, cterm, dh, uk, gnb, total;
 };
 static BwdLayout bwd_layout(const bdgdn_fwd_desc_t *d)
 {
@@ -489,8 +489,7 @@ static BwdLayout bwd_layout(const bdgdn_fwd_desc_t *d)
     l.dh = l.cterm + up(units * st * 4);
     l.uk = l.dh + up(units * st * 4);
     l.gnb = l.uk + up(units * 32 * d->d_k * 2);
-    l.o = l.gnb + up(units * 4);
-    l.total = l.o + (size_t)d->batch * d->seqlen * d->h_v * d->d_v * 2;
+    l.total = l.gnb + up(units * 4);
     return l;
 }
 
@@ -544,7 +543,7 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     sa.g = g; sa.beta = beta; sa.gn = gn; sa.betan = betan;
     sa.cu = packed ? cu_seqlens_dev : nullptr;
     sa.h0 = h0; sa.ht = nullptr;
-    sa.o = ws + lay.o; sa.on = nullptr;
+    sa.o = ws; sa.on = nullptr;   // never written: the states-only scan has no outputs
     sa.ws = nullptr;
     sa.bs = seeds;
     sa.T = desc->seqlen; sa.L = desc->block; sa.nblk = (desc->seqlen + desc->block - 1) / desc->block;
