@@ -474,7 +474,7 @@ static bool bwd_shape_ok(const bdgdn_fwd_desc_t *d)
 
 // Workspace of the backward, per (global block, v-head): the seed state (fp16), the part of
 // the state gradient at the block's start that does not depend on dh (fp32), dh at the
-// block's end (fp32), U K (32 x d_k, fp16), gamma_n (fp32).  Byte offsets, each aligned to
+// block's end (fp16: the clean block kernel uses it as fp16 operands only), U K (32 x d_k, fp16), gamma_n (fp32).  Byte offsets, each aligned to
 // 256.
 struct BwdLayout {
     size_t seeds, cterm, dh, uk, gnb, total;
@@ -487,7 +487,7 @@ static BwdLayout bwd_layout(const bdgdn_fwd_desc_t *d)
     l.seeds = 0;
     l.cterm = l.seeds + up(units * st * 2);
     l.dh = l.cterm + up(units * st * 4);
-    l.uk = l.dh + up(units * st * 4);
+    l.uk = l.dh + up(units * st * 2);
     l.gnb = l.uk + up(units * 32 * d->d_k * 2);
     l.total = l.gnb + up(units * 4);
     return l;
@@ -573,7 +573,7 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     a.dqn = dqn; a.dkn = dkn; a.dvn = dvn; a.dgn = dgn; a.dbn = dbetan;
     a.dh0 = dh0;
     a.cterm = reinterpret_cast<float *>(ws + lay.cterm);
-    a.dh = reinterpret_cast<float *>(ws + lay.dh);
+    a.dh = reinterpret_cast<_Float16 *>(ws + lay.dh);
     a.uk = reinterpret_cast<_Float16 *>(ws + lay.uk);
     a.gnb = reinterpret_cast<float *>(ws + lay.gnb);
     a.cu = sa.cu;

@@ -26,7 +26,7 @@ struct BwdArgs {
                                              // + clean terms)
     _Float16 *uk;                            // [global block][h_v][32][128]: U K of each clean block
     float *gnb;                              // [global block][h_v]: gamma_n of each clean block
-    float *dh;                               // [global block][h_v][128][128]: gradient at block ends
+    _Float16 *dh;                            // [global block][h_v][128][128]: gradient at block ends (fp16)
     const int32_t *cu;                       // packed documents, or null
     int n_docs;
     int n_chains;                            // sequences x v-heads

@@ -288,16 +288,15 @@ __device__ __forceinline__ BlockRows<Od, WITH_V> load_block(const StreamPtrs &p,
 }  // namespace
 
 // One block's gradients.  S0 (LDS f16) holds the seed.  For the clean stream dS (LDS, f16)
-// and dsn (registers, fp32, the C-tile layout of a state gradient: wave w holds column block
-// w, row blocks 0 .. 7) hold dS_n on entry; for the noisy stream dS_n is formed here from the
-// block-end readout (dsn is not read) and the seed's gradient dS0 is added into acc (same
-// layout).  Wave w computes the 16 columns 16 w .. 16 w + 15 of every 32 x 128 and 128 x 128
+// holds dS_n on entry; for the noisy stream dS_n is formed here from the block-end readout
+// and the seed's gradient dS0 is added into acc (registers, the C-tile layout of a state
+// gradient: wave w holds column block w, row blocks 0 .. 7).  Wave w computes the 16 columns 16 w .. 16 w + 15 of every 32 x 128 and 128 x 128
 // product.  hook1() runs once the arrays R, dDl and dO are dead (after the dR / dQ phase),
 // hook2() two phases later: a persistent caller loads the next unit's clean rows in the one
 // and stages them into those arrays in the other.
 template <bool CLEAN, typename Od, typename H1, typename H2>
 __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, const BlockRows<Od, true> &in,
-                          const float (&dsn)[8][4], float (&acc)[8][4], int tid, const H1 &hook1, const H2 &hook2)
+                          float (&acc)[8][4], int tid, const H1 &hook1, const H2 &hook2)
 {
     const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
     const float s = a.scale;
@@ -367,14 +366,15 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
 #pragma unroll
         for (int tm = 0; tm < 8; ++tm) {
             f32x4 c;
-            if constexpr (CLEAN) {
+            if constexpr (CLEAN) {   // dS_n tile (tm, w) from LDS by the transpose load
+                dsq[tm] = op_tr(sm.dS, LDH, 16 * tm, c0, lane);
 #pragma unroll
-                for (int j = 0; j < 4; ++j) c[j] = dsn[tm][j];
+                for (int j = 0; j < 4; ++j) c[j] = (float)dsq[tm][j];
             } else {
                 c = mfma(op_tr(sm.Q, LDH, 16, 16 * tm, lane), dob[1], mfma(op_tr(sm.Q, LDH, 0, 16 * tm, lane), dob[0], z));
                 c *= s;
+                dsq[tm] = h4(c);
             }
-            dsq[tm] = h4(c);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 if constexpr (!CLEAN) {
@@ -841,7 +841,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
         store_seed(sm.S0, seed, tid);   // made visible by block_bwd's first barrier
         BlockRows<Od, false> nxt;
         block_bwd<false, Od>(
-            sm, pn, a, nvalid, nin, acc, acc, tid,
+            sm, pn, a, nvalid, nin, acc, tid,
             [&] {
                 if (PREP && more) {
                     int n2, nv2;
@@ -883,7 +883,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     Smem &sm = *reinterpret_cast<Smem *>(smem_raw);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15;
+    const int tid = threadIdx.x;
     const long gblk = blockIdx.x / a.h_v;
     const int h = blockIdx.x % a.h_v, hq = h / (a.h_v / a.h_qk);
     int n, nvalid;
@@ -892,25 +892,19 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
     const size_t so = ((size_t)gblk * a.h_v + h) * DD * DD;
     const StreamPtrs pc = stream_ptrs<Od>(a, false, p0, h, hq);
     const SeedRegs seed = load_seed(a.seeds + so, tid);
-    float dsn[8][4];
-    const float *dh = a.dh + so;
-#pragma unroll
-    for (int tm = 0; tm < 8; ++tm)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) dsn[tm][j] = dh[(16 * tm + 4 * g4 + j) * DD + 16 * wave + rr];
+    const SeedRegs dh = load_seed(a.dh + so, tid);   // fp16, the seed's layout
     const BlockRows<Od, true> in = load_block<Od, true>(pc, a.h_qk, a.h_v, nvalid, tid);
     store_seed(sm.S0, seed, tid);
-#pragma unroll
-    for (int tm = 0; tm < 8; ++tm)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) sm.dS[(16 * tm + 4 * g4 + j) * LDH + 16 * wave + rr] = (_Float16)dsn[tm][j];
-    block_bwd<true, Od>(sm, pc, a, nvalid, in, dsn, dsn, tid, [] {}, [] {});   // its first barrier covers S0, dS
+    store_seed(sm.dS, dh, tid);
+    float no_acc[8][4];   // the clean stream forms no dS0
+    block_bwd<true, Od>(sm, pc, a, nvalid, in, no_acc, tid, [] {}, [] {});   // its first barrier covers S0, dS
 }
 
 // Phase 2: the reverse scan of the clean state gradient over the blocks of a (sequence,
 // v-head) (a chain), one workgroup of 4 waves per 32 columns (the columns are independent):
 //   dh_(b-1) = gamma_n dh_b + cterm_b - K^T Z,  Z = (U K) dh_b  (32 x 32),
-// writing dh_b (the gradient at the end of block b) for phase 3, and dh0.  The operands of
+// writing dh_b (the gradient at the end of block b; fp16, the precision phase 3 uses it in)
+// for phase 3, and dh0 (fp32).  The operands of
 // block b - 1 (U K, K, cterm, gamma_n) are loaded into registers while block b is computed.
 namespace {
 constexpr int LDK = NP + 8;   // f16 row stride of [*][32] tiles
@@ -994,7 +988,7 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
         const int buf = b & 1;
         const long p0 = r0 + (long)b * a.L;
         const long gblk = a.cu ? p0 / a.L : (long)n * a.nblk + b;
-        float *dhb = a.dh + ((size_t)gblk * a.h_v + h) * SS;
+        _Float16 *dhb = a.dh + ((size_t)gblk * a.h_v + h) * SS;
         if (b > 0) fetch(b - 1, nxt);
         // publish dh_b; stage dh_b^T, U K, K^T of block b
 #pragma unroll
@@ -1003,7 +997,7 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
             for (int tn = 0; tn < 2; ++tn) {
                 const int r = 32 * wave + 16 * tl + 4 * g4, c = 16 * tn + rr;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) dhb[(size_t)(r + j) * DD + v0 + c] = dh[tl][tn][j];
+                for (int j = 0; j < 4; ++j) dhb[(size_t)(r + j) * DD + v0 + c] = (_Float16)dh[tl][tn][j];
                 st4(sm.dHt + c * LDH + r, dh[tl][tn][0], dh[tl][tn][1], dh[tl][tn][2], dh[tl][tn][3]);
             }
         *reinterpret_cast<f16x8 *>(sm.UK + sr * LDH + sc) = cur.uk[0];
