@@ -158,3 +158,34 @@ def test_bwd_one_view_equals_two_stream_backward():
         assert torch.equal(got_c[n], ref[n]), n
     for n in ("dq", "dk", "dv", "dg", "dbeta"):
         assert torch.equal(got_v[0][n], ref[n + "n"]), n
+
+
+def test_bwd_grouped_heads_long_sequences_sampled_units():
+    """The grouped-value shape (2 x 16384 + 16384 tokens, 16 q/k heads shared by 32 v heads)
+    with blocks of 32, run whole on the GPU; two (sequence, q/k head) units, each with its
+    two v heads, checked against the oracle (dq, dk summed over the two v heads)."""
+    B, T, hqk, hv, L = 2, 16384, 16, 32, 32
+    inp = W.make_custom_train(B, T, hqk, hv, 128, 128, "bf16", seed=1234)
+    rng = np.random.default_rng(93)
+    do = torch.from_numpy(rng.standard_normal((B, T, hv, 128), dtype=np.float32))
+    don = torch.from_numpy(rng.standard_normal((B, T, hv, 128), dtype=np.float32))
+    scale = 1.0 / math.sqrt(128)
+    d = {k: v.cuda() for k, v in inp.items()}
+    print(f"bwd grouped B={B} T={T} hqk={hqk} hv={hv} L={L}", flush=True)
+    got = bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
+                             d["betan"], do.cuda(), don.cuda(), block=L, scale=scale, want_dh0=True)
+    torch.cuda.synchronize()
+    for b, j in ((0, 3), (1, 14)):
+        qk = lambda x: x[b:b + 1, :, j:j + 1]
+        vh = lambda x: x[b:b + 1, :, 2 * j:2 * j + 2]
+        u = {k: (qk(v) if k in ("q", "k", "qn", "kn") else vh(v)) for k, v in inp.items()}
+        ref = oracle.bwd_train(u["q"], u["k"], u["v"], u["g"], u["beta"], u["qn"], u["kn"], u["vn"], u["gn"],
+                               u["betan"], vh(do), vh(don), block=L, scale=scale)
+        errs = {}
+        for n in NAMES:
+            sl = qk if n in ("dq", "dk", "dqn", "dkn") else vh
+            errs[n] = rel_err(sl(got[n]).cpu(), ref[n])
+        errs["dh0"] = rel_err(got["dh0"][b:b + 1, 2 * j:2 * j + 2].cpu(), ref["dh0"])
+        print(f"  unit ({b}, {j}): " + " ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
+        for name, e in errs.items():
+            assert e <= TOL["bf16"], f"unit ({b}, {j}) {name}: {e:.3e}"
