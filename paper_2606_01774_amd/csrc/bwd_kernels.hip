@@ -896,7 +896,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
     const BlockRows<Od, true> in = load_block<Od, true>(pc, a.h_qk, a.h_v, nvalid, tid);
     store_seed(sm.S0, seed, tid);
     store_seed(sm.dS, dh, tid);
-    float no_acc[8][4];   // the clean stream forms no dS0
+    float no_acc[8][4] = {};   // the clean stream forms no dS0
     block_bwd<true, Od>(sm, pc, a, nvalid, in, no_acc, tid, [] {}, [] {});   // its first barrier covers S0, dS
 }
 
