@@ -63,6 +63,8 @@ def _check(B, T, hqk, hv, L, seed, **kw):
     (1, 80, 1, 1, 32, {"h0": True, "dht": True}),            # initial state, final-state gradient
     (1, 64, 1, 1, 8, {"do_dtype": torch.bfloat16}),         # bf16 upstream gradients, small blocks
     (1, 116, 1, 1, 32, {"lengths": [64, 0, 32, 20], "h0": True}),   # an empty document, a partial last one
+    (1, 20, 1, 1, 32, {"dht": True}),                       # a sequence shorter than one block
+    (3, 33, 1, 1, 32, {"h0": True}),                        # a one-position tail block
 ])
 def test_bwd_matches_oracle(B, T, hqk, hv, L, kw):
     _check(B, T, hqk, hv, L, 300 + T + L, **kw)
