@@ -429,14 +429,14 @@ int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc, const void *q, const voi
     hipError_t e;
     if (!split) {
         // FUSED: one on-chip pass per view (the clean scan recomputed with each; its outputs
-        // are the same every time)
+        // and ht written by the first only)
         sa.bs = nullptr;
         for (int i = 0; i < n_views; ++i) {
             sa.qn = views[i].q; sa.kn = views[i].k; sa.vn = views[i].v;
             sa.gn = views[i].g; sa.betan = views[i].beta;
             sa.on = views[i].o;
             sa.ht = i == 0 ? ht : nullptr;
-            e = launch_fwd_pipelined(ty, desc->d_k, lp, sa, strm);
+            e = launch_fwd_pipelined(ty, desc->d_k, lp, sa, strm, i == 0);
             if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
         }
         return BDGDN_OK;

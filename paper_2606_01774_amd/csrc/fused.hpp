@@ -37,8 +37,10 @@ namespace bdgdn {
 // STATES (with SPLIT, fp16 seeds): the recomputation of the seeds alone, for the backward:
 // no clean outputs (the O waves stand idle too), and the seeds are copied from the state
 // operand in LDS by the otherwise idle N waves, off the C waves' path.
+// NO_O: no clean outputs (the O waves stand idle): a further noisy view of the
+// complementary-view forward, whose clean stream an earlier pass has written.
 template <typename Out, int DK, int LP, bool SPLIT = false, bool SEEDS = SPLIT, typename SeedT_ = float,
-          bool STATES = false>
+          bool STATES = false, bool NO_O = false>
 struct Fused {
     typedef SeedT_ SeedT;
     static_assert(!STATES || (SPLIT && SEEDS && sizeof(SeedT_) == 2), "STATES: the split scan, fp16 seeds");
@@ -651,6 +653,11 @@ struct Fused {
                 advance(pc, c);
                 lds_barrier();
             }
+        } else if (NO_O && wave < 6) {
+            // ---- idle: no clean outputs
+            lds_barrier();
+            lds_barrier();
+            for (int j = 0; j < nb; ++j) lds_barrier();
         } else if (wave < 6) {
             // ---- O
             const int bc = wave - 4;

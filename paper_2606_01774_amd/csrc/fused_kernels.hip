@@ -15,11 +15,19 @@ __global__ void __launch_bounds__(768) bdgdn_fwd_pipelined_kernel(ScanArgs a)
     run_chain<Fused<Out, DK, LP>>(a, smem);
 }
 
+// The same without the clean outputs: a further noisy view of the complementary-view forward.
 template <typename Out, int DK, int LP>
+__global__ void __launch_bounds__(768) bdgdn_fwd_pipelined_noisy_kernel(ScanArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    run_chain<Fused<Out, DK, LP, false, false, float, false, true>>(a, smem);
+}
+
+template <typename Out, int DK, int LP, bool NO_O = false>
 static hipError_t launch_one(const ScanArgs &a, hipStream_t s)
 {
-    typedef Fused<Out, DK, LP> K;
-    auto kern = bdgdn_fwd_pipelined_kernel<Out, DK, LP>;
+    typedef Fused<Out, DK, LP, false, false, float, false, NO_O> K;
+    auto kern = NO_O ? bdgdn_fwd_pipelined_noisy_kernel<Out, DK, LP> : bdgdn_fwd_pipelined_kernel<Out, DK, LP>;
     static std::once_flag once;
     static hipError_t err = hipSuccess;
     std::call_once(once, [&] {
@@ -66,11 +74,11 @@ bool pipelined_supported(Types ty, int dk, int lp)
     return ty != Types::F32 && (dk == 64 || dk == 128) && (lp == 16 || lp == 32);
 }
 
-hipError_t launch_fwd_pipelined(Types ty, int dk, int lp, const ScanArgs &a, hipStream_t s)
+hipError_t launch_fwd_pipelined(Types ty, int dk, int lp, const ScanArgs &a, hipStream_t s, bool clean_out)
 {
     if (!pipelined_supported(ty, dk, lp) || a.n_vt * 32 != a.dv) return hipErrorInvalidValue;
 #define BDGDN_CASE(OUT, DK, LP) \
-    if (dk == DK && lp == LP) return launch_one<OUT, DK, LP>(a, s);
+    if (dk == DK && lp == LP) return clean_out ? launch_one<OUT, DK, LP>(a, s) : launch_one<OUT, DK, LP, true>(a, s);
     if (ty == Types::BF16_IN_F32_OUT) {
         BDGDN_CASE(float, 64, 16) BDGDN_CASE(float, 64, 32) BDGDN_CASE(float, 128, 16) BDGDN_CASE(float, 128, 32)
     } else {

@@ -99,7 +99,8 @@ hipError_t launch_fwd_scan(Types ty, int dk, int lp, const IntraArgs &ia, const 
 // The one-kernel pipelined schedule (UT transform inside the scan workgroups): bf16
 // inputs, blocks of at most 32 positions.
 bool pipelined_supported(Types ty, int dk, int lp);
-hipError_t launch_fwd_pipelined(Types ty, int dk, int lp, const ScanArgs &a, hipStream_t s);
+// clean_out = false: no clean outputs (a further noisy view of the complementary-view forward).
+hipError_t launch_fwd_pipelined(Types ty, int dk, int lp, const ScanArgs &a, hipStream_t s, bool clean_out = true);
 // The same, also writing the seed state of every (block, v-head) to a.bs (d_k = 128).
 hipError_t launch_fwd_pipelined_seeds(Types ty, int lp, const ScanArgs &a, hipStream_t s);
 // The split schedule (clean scan exposing the seed states, then the noisy-block pass):
