@@ -271,7 +271,8 @@ struct Fused {
 #pragma unroll
         for (int u = 0; u < OPS; ++u)
 #pragma unroll
-            for (int si = 0; si < NSETS; ++si) f.c[si][u] = bload(r.r[si], o.rg[u]);
+            for (int si = 0; si < NSETS; ++si)
+                if (!(NO_O && si == 1)) f.c[si][u] = bload(r.r[si], o.rg[u]);   // set 1 (clean q): O only
     }
     __device__ __forceinline__ void fetch_v(const Ptrs &P, const Chain &c, int nvalid, int tw, const LOffs &o, VF &f) const
     {
@@ -287,6 +288,7 @@ struct Fused {
         for (int u = 0; u < OPS; ++u)
 #pragma unroll
             for (int si = 0; si < NSETS; ++si) {
+                if (NO_O && si == 1) continue;   // the clean q rows are read by the O waves only
                 st16(smem + slot * RING_B + si * ROWS_B, o.rl[u], to_operand<In, E>(f.c[si][u]));
                 f.c[si][u] = bload(r.r[si], o.rg[u]);
             }
