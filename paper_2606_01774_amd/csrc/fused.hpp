@@ -272,7 +272,7 @@ struct Fused {
         for (int u = 0; u < OPS; ++u)
 #pragma unroll
             for (int si = 0; si < NSETS; ++si)
-                if (!(NO_O && si == 1)) f.c[si][u] = bload(r.r[si], o.rg[u]);   // set 1 (clean q): O only
+                if (!((NO_O || STATES) && si == 1)) f.c[si][u] = bload(r.r[si], o.rg[u]);   // set 1 (clean q): O only
     }
     __device__ __forceinline__ void fetch_v(const Ptrs &P, const Chain &c, int nvalid, int tw, const LOffs &o, VF &f) const
     {
@@ -288,7 +288,7 @@ struct Fused {
         for (int u = 0; u < OPS; ++u)
 #pragma unroll
             for (int si = 0; si < NSETS; ++si) {
-                if (NO_O && si == 1) continue;   // the clean q rows are read by the O waves only
+                if ((NO_O || STATES) && si == 1) continue;   // the clean q rows are read by the O waves only
                 st16(smem + slot * RING_B + si * ROWS_B, o.rl[u], to_operand<In, E>(f.c[si][u]));
                 f.c[si][u] = bload(r.r[si], o.rg[u]);
             }
