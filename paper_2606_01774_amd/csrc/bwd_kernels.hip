@@ -901,29 +901,37 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
 }
 
 // Phase 2: the reverse scan of the clean state gradient over the blocks of a (sequence,
-// v-head) (a chain), one workgroup of 4 waves per 32 columns (the columns are independent):
-//   dh_(b-1) = gamma_n dh_b + cterm_b - K^T Z,  Z = (U K) dh_b  (32 x 32),
+// v-head) (a chain), one workgroup of NW waves per TC = 8 NW columns (the columns are
+// independent):
+//   dh_(b-1) = gamma_n dh_b + cterm_b - K^T Z,  Z = (U K) dh_b  (32 x TC),
 // writing dh_b (the gradient at the end of block b; fp16, the precision phase 3 uses it in)
-// for phase 3, and dh0 (fp32).  The operands of
-// block b - 1 (U K, K, cterm, gamma_n) are loaded into registers while block b is computed.
+// for phase 3, and dh0 (fp32).  The operands of block b - 1 (U K, K, cterm, gamma_n) are
+// loaded into registers while block b is computed.
 namespace {
 constexpr int LDK = NP + 8;   // f16 row stride of [*][32] tiles
-struct ScanSmem {
+constexpr int kScanWaves = 4;   // waves per workgroup (2: 16 columns, two workgroups per CU, was slower)
+template <int TC> struct ScanSmem {
     _Float16 UK[NP * LDH];       // U K of the block (32 x 128)
-    _Float16 dHt[32 * LDH];      // dh_b transposed: the tile's 32 columns x 128 rows
+    _Float16 dHt[TC * LDH];      // dh_b transposed: the tile's TC columns x 128 rows
     _Float16 Kt[2][DD * LDK];    // K^T (128 x 32), two buffers
-    _Float16 Zt[32 * LDK];       // Z transposed: 32 columns x 32 positions
+    _Float16 Zt[TC * LDK];       // Z transposed: TC columns x 32 positions
 };
 }  // namespace
 
-__global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
+template <int NW>
+__global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
 {
-    __shared__ __align__(16) ScanSmem sm;
+    constexpr int TC = 8 * NW;           // columns per workgroup
+    constexpr int NT = DD / TC;          // column tiles per chain
+    constexpr int RT = DD / (16 * NW);   // 16-row tiles of dh per wave
+    constexpr int CT = TC / 16;          // 16-column tiles
+    constexpr int NC = 8 / NW;           // 16-byte chunks of a 32 x 128 operand per thread
+    __shared__ __align__(16) ScanSmem<TC> sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15;
-    // the 4 column tiles of a chain on one XCD (workgroups are dealt to the 8 XCDs in turn),
+    // the NT column tiles of a chain on one XCD (workgroups are dealt to the 8 XCDs in turn),
     // so that they read its U K and K rows through one L2
     const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-    const int chain = (slot >> 2) * 8 + xcd, v0 = 32 * (slot & 3);
+    const int chain = (slot / NT) * 8 + xcd, v0 = TC * (slot % NT);
     if (chain >= a.n_chains) return;
     const int n = chain / a.h_v, h = chain % a.h_v, hq = h / (a.h_v / a.h_qk);
     long r0, r1;
@@ -937,24 +945,25 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
     const int nb = (int)((r1 - r0 + a.L - 1) / a.L);
     const size_t SS = (size_t)DD * DD;
     const long qks = (long)a.h_qk * DD;
-    // dh tiles: wave w holds rows 32 w .. 32 w + 31 (two row blocks) of the 32 columns
-    float dh[2][2][4];
+    // dh tiles: wave w holds rows (128 / NW) w .. + 128 / NW - 1 (RT row tiles) of the TC columns
+    const int rw = (DD / NW) * wave;
+    float dh[RT][CT][4];
     const float *dht = a.dht ? a.dht + ((size_t)n * a.h_v + h) * SS : nullptr;
 #pragma unroll
-    for (int tl = 0; tl < 2; ++tl)
+    for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
-        for (int tn = 0; tn < 2; ++tn)
+        for (int tn = 0; tn < CT; ++tn)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                dh[tl][tn][j] = dht ? dht[(32 * wave + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] : 0.f;
-    // staging map of the 32 x 128 operands: row tid / 8, 16 columns from 16 (tid % 8)
-    const int sr = tid >> 3, sc = (tid & 7) * 16;
+                dh[tl][tn][j] = dht ? dht[(rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] : 0.f;
+    // staging map of the 32 x 128 operands: NC consecutive 16-byte chunks of one row per thread
+    const int sr = (tid * NC) >> 4, sc = ((tid * NC) & 15) * 8;
     // one block's operands in registers; two sets alternate so that the loads for block
     // b - 1 are in flight while block b is computed (and no register copy waits on them)
     struct Ops {
-        f16x8 uk[2];
-        bf16x8 k[2];
-        float cs[2][2][4], gn;
+        f16x8 uk[NC];
+        bf16x8 k[NC];
+        float cs[RT][CT][4], gn;
     };
     auto fetch = [&](int b, Ops &o) {
         const long p0 = r0 + (long)b * a.L;
@@ -962,25 +971,27 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
         const long gblk = a.cu ? p0 / a.L : (long)n * a.nblk + b;
         const size_t unit = (size_t)gblk * a.h_v + h;
         const f16x8 *u = reinterpret_cast<const f16x8 *>(a.uk + unit * NP * DD + sr * DD + sc);
-        o.uk[0] = u[0];
-        o.uk[1] = u[1];
+#pragma unroll
+        for (int i = 0; i < NC; ++i) o.uk[i] = u[i];
         if (sr < nvalid) {
             const bf16x8 *k = reinterpret_cast<const bf16x8 *>(static_cast<const __bf16 *>(a.k) + (p0 + sr) * qks +
                                                                hq * DD + sc);
-            o.k[0] = k[0];
-            o.k[1] = k[1];
+#pragma unroll
+            for (int i = 0; i < NC; ++i) o.k[i] = k[i];
         } else {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) o.k[0][j] = o.k[1][j] = (__bf16)0.f;
+            for (int i = 0; i < NC; ++i)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) o.k[i][j] = (__bf16)0.f;
         }
         const float *c = a.cterm + unit * SS;
 #pragma unroll
-        for (int tl = 0; tl < 2; ++tl)
+        for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
-            for (int tn = 0; tn < 2; ++tn)
+            for (int tn = 0; tn < CT; ++tn)
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    o.cs[tl][tn][j] = c[(32 * wave + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr];
+                    o.cs[tl][tn][j] = c[(rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr];
         o.gn = a.gnb[unit];
     };
     const f32x4 z = {0.f, 0.f, 0.f, 0.f};
@@ -992,33 +1003,32 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
         if (b > 0) fetch(b - 1, nxt);
         // publish dh_b; stage dh_b^T, U K, K^T of block b
 #pragma unroll
-        for (int tl = 0; tl < 2; ++tl)
+        for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
-            for (int tn = 0; tn < 2; ++tn) {
-                const int r = 32 * wave + 16 * tl + 4 * g4, c = 16 * tn + rr;
+            for (int tn = 0; tn < CT; ++tn) {
+                const int r = rw + 16 * tl + 4 * g4, c = 16 * tn + rr;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) dhb[(size_t)(r + j) * DD + v0 + c] = (_Float16)dh[tl][tn][j];
                 st4(sm.dHt + c * LDH + r, dh[tl][tn][0], dh[tl][tn][1], dh[tl][tn][2], dh[tl][tn][3]);
             }
-        *reinterpret_cast<f16x8 *>(sm.UK + sr * LDH + sc) = cur.uk[0];
-        *reinterpret_cast<f16x8 *>(sm.UK + sr * LDH + sc + 8) = cur.uk[1];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            sm.Kt[buf][(sc + j) * LDK + sr] = (_Float16)(float)cur.k[0][j];
-            sm.Kt[buf][(sc + 8 + j) * LDK + sr] = (_Float16)(float)cur.k[1][j];
+        for (int i = 0; i < NC; ++i) {
+            *reinterpret_cast<f16x8 *>(sm.UK + sr * LDH + sc + 8 * i) = cur.uk[i];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) sm.Kt[buf][(sc + 8 * i + j) * LDK + sr] = (_Float16)(float)cur.k[i][j];
         }
         __syncthreads();
-        {   // Z = (U K) dh_b: one 16 x 16 tile per wave, stored transposed
-            const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1);
+        {   // Z = (U K) dh_b: one 16 x 16 tile per wave (2 CT tiles over NW = 2 CT waves), stored transposed
+            const int m0 = 16 * (wave / CT), n0 = 16 * (wave % CT);
             const f32x4 c = tile_mma<_Float16, DD>(z, sm.UK + m0 * LDH, LDH, sm.dHt + n0 * LDH, LDH, lane);
             st4(sm.Zt + (n0 + rr) * LDK + m0 + 4 * g4, c[0], c[1], c[2], c[3]);
         }
         __syncthreads();
 #pragma unroll
-        for (int tl = 0; tl < 2; ++tl)
+        for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
-            for (int tn = 0; tn < 2; ++tn) {
-                const f32x4 c = tile_mma<_Float16, NP>(z, sm.Kt[buf] + (32 * wave + 16 * tl) * LDK, LDK,
+            for (int tn = 0; tn < CT; ++tn) {
+                const f32x4 c = tile_mma<_Float16, NP>(z, sm.Kt[buf] + (rw + 16 * tl) * LDK, LDK,
                                                        sm.Zt + 16 * tn * LDK, LDK, lane);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) dh[tl][tn][j] = cur.gn * dh[tl][tn][j] + cur.cs[tl][tn][j] - c[j];
@@ -1034,12 +1044,12 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_scan_kernel(BwdArgs a)
     if (a.dh0) {
         float *d0 = a.dh0 + ((size_t)n * a.h_v + h) * SS;
 #pragma unroll
-        for (int tl = 0; tl < 2; ++tl)
+        for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
-            for (int tn = 0; tn < 2; ++tn)
+            for (int tn = 0; tn < CT; ++tn)
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    d0[(32 * wave + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] = dh[tl][tn][j];
+                    d0[(rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] = dh[tl][tn][j];
     }
 }
 
@@ -1096,7 +1106,9 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int 
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
         }
-        hipLaunchKernelGGL(bdgdn_bwd_scan_kernel, dim3((4 * n_chains + 31) / 32 * 32), dim3(256), 0, s, a);
+        constexpr int NT = DD / (8 * kScanWaves);   // column tiles per chain
+        hipLaunchKernelGGL(bdgdn_bwd_scan_kernel<kScanWaves>, dim3((NT * n_chains + 8 * NT - 1) / (8 * NT) * 8 * NT),
+                           dim3(64 * kScanWaves), 0, s, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (n_block_units > 0) {
             hipLaunchKernelGGL(clean, dim3((unsigned)n_block_units), dim3(512), sizeof(Smem), s, a);
