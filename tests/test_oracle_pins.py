@@ -686,3 +686,90 @@ def test_pin_bwd_packed_equals_separate_documents():
         for key in ("dq", "dk", "dv", "dg", "dbeta", "dqn", "dkn", "dvn", "dgn", "dbetan"):
             np.testing.assert_array_equal(gp[key][:, a:e], gs[key], err_msg=key)
         np.testing.assert_array_equal(gp["dh0"][j], gs["dh0"][0])
+
+
+# ---------------------------------------------------------------------------
+# Property tests on random tiny shapes: block sizes 1..4 and one larger than the
+# sequence, ragged tails, grouped value heads, packed documents (empty ones
+# included), with and without an initial state.
+# ---------------------------------------------------------------------------
+from hypothesis import HealthCheck, given, settings, strategies as st
+
+_tiny = st.fixed_dictionaries(dict(
+    seed=st.integers(0, 2**31 - 1),
+    L=st.sampled_from([1, 2, 3, 4, 16]),
+    hqk=st.sampled_from([1, 2]), ratio=st.sampled_from([1, 2]),
+    dk=st.integers(1, 4), dv=st.integers(1, 4),
+    lengths=st.one_of(st.none(), st.lists(st.integers(0, 9), min_size=1, max_size=3)),
+    T=st.integers(1, 11), B=st.integers(1, 2),
+    with_h0=st.booleans(), scale=st.floats(0.25, 1.5)))
+_prop = settings(max_examples=80, deadline=None, derandomize=True,
+                 suppress_health_check=[HealthCheck.too_slow])
+
+
+def _tiny_case(p):
+    rng = np.random.default_rng(p["seed"])
+    hv = p["hqk"] * p["ratio"]
+    if p["lengths"] is None:
+        B, T, cu, nseq = p["B"], p["T"], None, p["B"]
+    else:
+        B, T = 1, max(1, sum(p["lengths"]))
+        cu = np.concatenate([[0], np.cumsum(p["lengths"])]).astype(np.int32)
+        nseq = len(p["lengths"])
+    c, n = _two(rng, B, T, p["hqk"], hv, p["dk"], p["dv"])
+    h0 = 0.5 * rng.standard_normal((nseq, hv, p["dk"], p["dv"])) if p["with_h0"] else None
+    return rng, c, n, h0, cu, nseq, hv
+
+
+@given(_tiny)
+@_prop
+def test_property_fwd_matches_unrolled_product(p):
+    """Every document of every shape drawn equals the brute-force unrolled product of
+    eq. gdn-recurrence, with the noisy blocks of eq. noisy-block-fwd aligned to the
+    document's start; positions past the last document stay zero."""
+    rng, c, n, h0, cu, nseq, hv = _tiny_case(p)
+    L, s = p["L"], p["scale"]
+    o, on, ht = _run(c, n, L, scale=s, h0=h0, cu_seqlens=cu)
+    docs = [(b, 0, c["q"].shape[1]) for b in range(nseq)] if cu is None else \
+        [(0, int(a), int(e)) for a, e in zip(cu[:-1], cu[1:])]
+    for d, (b, a, e) in enumerate(docs):
+        for h in range(hv):
+            S0 = np.zeros((p["dk"], p["dv"])) if h0 is None else h0[d, h]
+            if e == a:
+                np.testing.assert_allclose(ht[d, h], S0, rtol=0, atol=0)
+                continue
+            cs = {key: val[b:b + 1, a:e] for key, val in c.items()}
+            ns = {key: val[b:b + 1, a:e] for key, val in n.items()}
+            bo, bon, bS = _brute_two_stream(cs, ns, L, s, 0, h, S0, hv_per_qk=p["ratio"])
+            np.testing.assert_allclose(o[b, a:e, h], bo, rtol=1e-10, atol=1e-11)
+            np.testing.assert_allclose(on[b, a:e, h], bon, rtol=1e-10, atol=1e-11)
+            np.testing.assert_allclose(ht[d, h], bS, rtol=1e-10, atol=1e-11)
+    if cu is not None and int(cu[-1]) < o.shape[1]:
+        assert not o[:, int(cu[-1]):].any() and not on[:, int(cu[-1]):].any()
+
+
+@given(_tiny)
+@_prop
+def test_property_bwd_euler_identities(p):
+    """The loss <do,o> + <don,on> + <dht,ht> is homogeneous of degree one jointly in
+    (v, v~, h0), since every state is linear in them, and jointly in (q, q~), which
+    enter only the readouts; Euler's theorem then ties the gradients of each group to
+    the forward values, with no finite differences."""
+    rng, c, n, h0, cu, nseq, hv = _tiny_case(p)
+    L, s = p["L"], p["scale"]
+    if h0 is None:
+        h0 = np.zeros((nseq, hv, p["dk"], p["dv"]))
+    do = rng.standard_normal(c["v"].shape)
+    don = rng.standard_normal(c["v"].shape)
+    dht = rng.standard_normal(h0.shape)
+    o, on, ht = _run(c, n, L, scale=s, h0=h0, cu_seqlens=cu)
+    r = oracle.bwd_train(c["q"], c["k"], c["v"], c["g"], c["beta"],
+                         n["q"], n["k"], n["v"], n["g"], n["beta"],
+                         do, don, block=L, scale=s, h0=h0, dht=dht, cu_seqlens=cu)
+    readout = float((o * do).sum() + (on * don).sum())
+    loss = readout + float((ht * dht).sum())
+    lin_v = float((r["dv"] * c["v"]).sum() + (r["dvn"] * n["v"]).sum() + (r["dh0"] * h0).sum())
+    lin_q = float((r["dq"] * c["q"]).sum() + (r["dqn"] * n["q"]).sum())
+    tol = 1e-9 * (1.0 + np.abs(o).sum() + np.abs(on).sum() + np.abs(ht).sum()) * 4
+    assert abs(lin_v - loss) <= tol, (lin_v, loss)
+    assert abs(lin_q - readout) <= tol, (lin_q, readout)
