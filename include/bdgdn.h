@@ -205,7 +205,7 @@ int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc,
 
 /* Bytes of device workspace bdgdn_bwd_train needs, per (block, v-head): the recomputed
  * clean seed state (fp16), the part of the clean state gradient at the block's start that
- * does not depend on the gradient at its end (fp32), the gradient at its end (fp16), the
+ * does not depend on the gradient at its end (fp16), the gradient at its end (fp16), the
  * block's U K (32 x d_k fp16) and gamma_n; 0 for a descriptor it would reject. */
 size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
 

@@ -486,7 +486,7 @@ static BwdLayout bwd_layout(const bdgdn_fwd_desc_t *d)
     BwdLayout l;
     l.seeds = 0;
     l.cterm = l.seeds + up(units * st * 2);
-    l.dh = l.cterm + up(units * st * 4);
+    l.dh = l.cterm + up(units * st * 2);
     l.uk = l.dh + up(units * st * 2);
     l.gnb = l.uk + up(units * 32 * d->d_k * 2);
     l.total = l.gnb + up(units * 4);
@@ -572,7 +572,7 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     a.dq = dq; a.dk = dk; a.dv = dv; a.dg = dg; a.db = dbeta;
     a.dqn = dqn; a.dkn = dkn; a.dvn = dvn; a.dgn = dgn; a.dbn = dbetan;
     a.dh0 = dh0;
-    a.cterm = reinterpret_cast<float *>(ws + lay.cterm);
+    a.cterm = reinterpret_cast<_Float16 *>(ws + lay.cterm);
     a.dh = reinterpret_cast<_Float16 *>(ws + lay.dh);
     a.uk = reinterpret_cast<_Float16 *>(ws + lay.uk);
     a.gnb = reinterpret_cast<float *>(ws + lay.gnb);

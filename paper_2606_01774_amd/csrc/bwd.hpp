@@ -21,12 +21,13 @@ struct BwdArgs {
     float *dq, *dk, *dv, *dg, *db;
     float *dqn, *dkn, *dvn, *dgn, *dbn;
     float *dh0;                              // or null
-    float *cterm;                            // [global block][h_v][128][128]: the part of dh_(b-1)
+    _Float16 *cterm;                         // [global block][h_v][64 tiles][64 lanes][4]: the part of dh_(b-1)
                                              // that does not depend on dh_b (noisy seed gradient
-                                             // + clean terms)
+                                             // + clean terms), fp16 like dh
     _Float16 *uk;                            // [global block][h_v][32][128]: U K of each clean block
     float *gnb;                              // [global block][h_v]: gamma_n of each clean block
-    _Float16 *dh;                            // [global block][h_v][128][128]: gradient at block ends (fp16)
+    _Float16 *dh;                            // [global block][h_v][64 tiles][64 lanes][4]: gradient at
+                                             // block ends (fp16, tile-native like cterm)
     const int32_t *cu;                       // packed documents, or null
     int n_docs;
     int n_chains;                            // sequences x v-heads

@@ -212,6 +212,22 @@ __device__ __forceinline__ void store_seed(_Float16 *dst, const SeedRegs &x, int
         *reinterpret_cast<f16x8 *>(dst + (e / DD) * LDH + e % DD) = x.v[it];
     }
 }
+// The same 128 x 128 fp16 state stored tile-native (64 tiles of 16 x 16 in row-major tile
+// order, each lane-major in the MFMA result layout: lane 16 g + r holds rows 4 g .. 4 g + 3
+// of column r), loaded by load_seed as 16-byte chunks (two lanes of one tile each), into
+// the row-major LDS copy.
+__device__ __forceinline__ void store_tiles(_Float16 *dst, const SeedRegs &x, int tid)
+{
+#pragma unroll
+    for (int it = 0; it < 4; ++it)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+            const int vec = 2 * (tid + 512 * it) + hh, tile = vec >> 6, ln = vec & 63;
+            _Float16 *d = dst + (16 * (tile >> 3) + 4 * (ln >> 4)) * LDH + 16 * (tile & 7) + (ln & 15);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) d[j * LDH] = x.v[it][4 * hh + j];
+        }
+}
 
 // Block-local cumulative log-gates G (and G2 = G log2 e) and gamma = exp G, by wave 0 (a
 // 32-lane scan of the staged gates in G).
@@ -790,9 +806,12 @@ __device__ void clean_prep(Smem &sm, const BwdArgs &a, float gx, float bx, float
 // Phase 1: every noisy block: its gradients and its seed's gradient, plus (PREP) the
 // dh-independent part of the clean block of the same position (clean_prep, run first: it
 // needs no seed); both enter the state gradient at the block's start, whose sum is written
-// to cterm (fp32 [block][h_v][128][128]).  Without PREP (the further noisy views of the
-// complementary-view backward, each seeded from the same clean state) the seed's gradient
-// is added to cterm.  Persistent: one 160 KB workgroup per CU walks the units (global block,
+// to cterm (fp16, the precision of the dh it joins; per (block, v-head) 64 tiles of 16 x 16
+// in row-major tile order, each tile stored lane-major in the MFMA result layout: lane
+// 16 g + r holds rows 4 g .. 4 g + 3 of column r as one 8-byte vector, the layout both
+// this kernel and the scan hold it in registers).  Without PREP (the further noisy views of
+// the complementary-view backward, each seeded from the same clean state) the seed's
+// gradient is added to cterm.  Persistent: one 160 KB workgroup per CU walks the units (global block,
 // v-head) u = blockIdx.x, + gridDim.x, ...; the next unit's clean rows are loaded while the
 // current unit finishes and staged into arrays it no longer uses, and each unit's seed and
 // noisy rows are in flight while its clean prep runs.
@@ -860,17 +879,16 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
                     cb = nxt.b;
                 }
             });
-        float *dst = a.cterm + (size_t)u * DD * DD;
+        f16x4 *dst = reinterpret_cast<f16x4 *>(a.cterm + (size_t)u * DD * DD) + wave * 64 + lane;
 #pragma unroll
-        for (int tm = 0; tm < 8; ++tm)
+        for (int tm = 0; tm < 8; ++tm) {
+            f16x4 *p = dst + tm * 8 * 64;   // tile (tm, wave)
+            f16x4 v;
+            if constexpr (!PREP) v = *p;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                float *p = dst + (16 * tm + 4 * g4 + j) * DD + 16 * wave + rr;
-                if constexpr (PREP)
-                    *p = acc[tm][j];
-                else
-                    *p += acc[tm][j];
-            }
+            for (int j = 0; j < 4; ++j) v[j] = (_Float16)(PREP ? acc[tm][j] : (float)v[j] + acc[tm][j]);
+            *p = v;
+        }
         if (!more) break;
         u = un;
     }
@@ -892,10 +910,10 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
     const size_t so = ((size_t)gblk * a.h_v + h) * DD * DD;
     const StreamPtrs pc = stream_ptrs<Od>(a, false, p0, h, hq);
     const SeedRegs seed = load_seed(a.seeds + so, tid);
-    const SeedRegs dh = load_seed(a.dh + so, tid);   // fp16, the seed's layout
+    const SeedRegs dh = load_seed(a.dh + so, tid);   // fp16, tile-native
     const BlockRows<Od, true> in = load_block<Od, true>(pc, a.h_qk, a.h_v, nvalid, tid);
     store_seed(sm.S0, seed, tid);
-    store_seed(sm.dS, dh, tid);
+    store_tiles(sm.dS, dh, tid);
     float no_acc[8][4] = {};   // the clean stream forms no dS0
     block_bwd<true, Od>(sm, pc, a, nvalid, in, no_acc, tid, [] {}, [] {});   // its first barrier covers S0, dS
 }
@@ -904,8 +922,8 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
 // v-head) (a chain), one workgroup of NW waves per TC = 8 NW columns (the columns are
 // independent):
 //   dh_(b-1) = gamma_n dh_b + cterm_b - K^T Z,  Z = (U K) dh_b  (32 x TC),
-// writing dh_b (the gradient at the end of block b; fp16, the precision phase 3 uses it in)
-// for phase 3, and dh0 (fp32).  The operands of block b - 1 (U K, K, cterm, gamma_n) are
+// writing dh_b (the gradient at the end of block b; fp16, the precision phase 3 uses it in,
+// tile-native like cterm) for phase 3, and dh0 (fp32).  The operands of block b - 2 (U K, K, cterm, gamma_n) are
 // loaded into registers while block b is computed.
 namespace {
 constexpr int LDK = NP + 8;   // f16 row stride of [*][32] tiles
@@ -943,6 +961,9 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
         r1 = r0 + a.T;
     }
     const int nb = (int)((r1 - r0 + a.L - 1) / a.L);
+    // global index of the chain's first block (documents start on block boundaries), so that
+    // block b is gb0 + b with no division in the loop
+    const long gb0 = a.cu ? r0 / a.L : (long)n * a.nblk;
     const size_t SS = (size_t)DD * DD;
     const long qks = (long)a.h_qk * DD;
     // dh tiles: wave w holds rows (128 / NW) w .. + 128 / NW - 1 (RT row tiles) of the TC columns
@@ -956,20 +977,28 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 dh[tl][tn][j] = dht ? dht[(rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] : 0.f;
+    // wait for these loads here, once: left pending into the loop, they would make every
+    // step wait for all outstanding loads (the prefetch of the next blocks included)
+#pragma unroll
+    for (int tl = 0; tl < RT; ++tl)
+#pragma unroll
+        for (int tn = 0; tn < CT; ++tn)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(dh[tl][tn][j]));
     // staging map of the 32 x 128 operands: NC consecutive 16-byte chunks of one row per thread
     const int sr = (tid * NC) >> 4, sc = ((tid * NC) & 15) * 8;
-    // one block's operands in registers; two sets alternate so that the loads for block
-    // b - 1 are in flight while block b is computed (and no register copy waits on them)
+    // one block's operands in registers; three sets rotate so that the loads for blocks
+    // b - 1 and b - 2 are in flight while block b is computed (no register copy waits on them)
     struct Ops {
         f16x8 uk[NC];
         bf16x8 k[NC];
-        float cs[RT][CT][4], gn;
+        f16x4 cs[RT][CT];
+        float gn;
     };
     auto fetch = [&](int b, Ops &o) {
         const long p0 = r0 + (long)b * a.L;
         const int nvalid = (int)(r1 - p0 < a.L ? r1 - p0 : a.L);
-        const long gblk = a.cu ? p0 / a.L : (long)n * a.nblk + b;
-        const size_t unit = (size_t)gblk * a.h_v + h;
+        const size_t unit = (size_t)(gb0 + b) * a.h_v + h;
         const f16x8 *u = reinterpret_cast<const f16x8 *>(a.uk + unit * NP * DD + sr * DD + sc);
 #pragma unroll
         for (int i = 0; i < NC; ++i) o.uk[i] = u[i];
@@ -984,31 +1013,32 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
 #pragma unroll
                 for (int j = 0; j < 8; ++j) o.k[i][j] = (__bf16)0.f;
         }
-        const float *c = a.cterm + unit * SS;
+        // cterm tiles (rows rw / 16 + tl, columns v0 / 16 + tn), lane-major like the dh tiles
+        const f16x4 *c = reinterpret_cast<const f16x4 *>(a.cterm + unit * SS) + lane;
 #pragma unroll
         for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
-            for (int tn = 0; tn < CT; ++tn)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    o.cs[tl][tn][j] = c[(rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr];
-        o.gn = a.gnb[unit];
+            for (int tn = 0; tn < CT; ++tn) o.cs[tl][tn] = c[((rw / 16 + tl) * 8 + v0 / 16 + tn) * 64];
+        // a vector load (the index made lane-opaque): a scalar load would be counted with the
+        // LDS operations, and the wait before the next barrier would wait for it
+        int z;
+        asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+        o.gn = a.gnb[unit + z];
     };
     const f32x4 z = {0.f, 0.f, 0.f, 0.f};
     auto step = [&](int b, const Ops &cur, Ops &nxt) {
         const int buf = b & 1;
-        const long p0 = r0 + (long)b * a.L;
-        const long gblk = a.cu ? p0 / a.L : (long)n * a.nblk + b;
-        _Float16 *dhb = a.dh + ((size_t)gblk * a.h_v + h) * SS;
-        if (b > 0) fetch(b - 1, nxt);
-        // publish dh_b; stage dh_b^T, U K, K^T of block b
+        _Float16 *dhb = a.dh + ((size_t)(gb0 + b) * a.h_v + h) * SS;
+        // publish dh_b; stage dh_b^T, U K, K^T of block b; every use of cur comes before the
+        // loads of block b - 2 are issued, so that no wait for cur can also wait for those
 #pragma unroll
         for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
             for (int tn = 0; tn < CT; ++tn) {
                 const int r = rw + 16 * tl + 4 * g4, c = 16 * tn + rr;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) dhb[(size_t)(r + j) * DD + v0 + c] = (_Float16)dh[tl][tn][j];
+                const f16x4 hv = {(_Float16)dh[tl][tn][0], (_Float16)dh[tl][tn][1], (_Float16)dh[tl][tn][2],
+                                  (_Float16)dh[tl][tn][3]};
+                reinterpret_cast<f16x4 *>(dhb)[((rw / 16 + tl) * 8 + v0 / 16 + tn) * 64 + lane] = hv;   // tile-native
                 st4(sm.dHt + c * LDH + r, dh[tl][tn][0], dh[tl][tn][1], dh[tl][tn][2], dh[tl][tn][3]);
             }
 #pragma unroll
@@ -1017,6 +1047,14 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
 #pragma unroll
             for (int j = 0; j < 8; ++j) sm.Kt[buf][(sc + 8 * i + j) * LDK + sr] = (_Float16)(float)cur.k[i][j];
         }
+        // dh_b is in LDS now: keep gamma_n dh_b + cterm_b in its registers
+#pragma unroll
+        for (int tl = 0; tl < RT; ++tl)
+#pragma unroll
+            for (int tn = 0; tn < CT; ++tn)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) dh[tl][tn][j] = cur.gn * dh[tl][tn][j] + (float)cur.cs[tl][tn][j];
+        if (b > 1) fetch(b - 2, nxt);
         __syncthreads();
         {   // Z = (U K) dh_b: one 16 x 16 tile per wave (2 CT tiles over NW = 2 CT waves), stored transposed
             const int m0 = 16 * (wave / CT), n0 = 16 * (wave % CT);
@@ -1031,15 +1069,19 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
                 const f32x4 c = tile_mma<_Float16, NP>(z, sm.Kt[buf] + (rw + 16 * tl) * LDK, LDK,
                                                        sm.Zt + 16 * tn * LDK, LDK, lane);
 #pragma unroll
-                for (int j = 0; j < 4; ++j) dh[tl][tn][j] = cur.gn * dh[tl][tn][j] + cur.cs[tl][tn][j] - c[j];
+                for (int j = 0; j < 4; ++j) dh[tl][tn][j] -= c[j];
             }
     };
-    Ops o0, o1;
+    // three sets: block b's operands were loaded two steps earlier
+    Ops o0, o1, o2;
     if (nb > 0) fetch(nb - 1, o0);
-    for (int b = nb - 1; b >= 0; b -= 2) {
-        step(b, o0, o1);
+    if (nb > 1) fetch(nb - 2, o1);
+    for (int b = nb - 1; b >= 0; b -= 3) {
+        step(b, o0, o2);
         if (b == 0) break;
         step(b - 1, o1, o0);
+        if (b == 1) break;
+        step(b - 2, o2, o1);
     }
     if (a.dh0) {
         float *d0 = a.dh0 + ((size_t)n * a.h_v + h) * SS;

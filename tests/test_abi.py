@@ -266,9 +266,9 @@ def test_bwd_train_validation_and_workspace():
     lib = bd.load_library()
     ok = _desc()
     need = lib.bdgdn_bwd_train_workspace(ctypes.byref(ok))
-    # per (block, v-head): an fp16 seed, an fp32 and an fp16 state, U K (32 x 128 fp16)
+    # per (block, v-head): an fp16 seed, two fp16 states, U K (32 x 128 fp16)
     units = 2 * 4
-    assert need >= units * 128 * 128 * (2 + 4 + 2) + units * 32 * 128 * 2
+    assert need >= units * 128 * 128 * (2 + 2 + 2) + units * 32 * 128 * 2
     assert lib.bdgdn_bwd_train_workspace(ctypes.byref(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32))) == 0
     assert _bwd(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32)) == bd.BDGDN_ERR_UNSUPPORTED
     assert _bwd(_desc(d_k=64, d_v=64)) == bd.BDGDN_ERR_UNSUPPORTED
