@@ -229,6 +229,11 @@ size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
  * blocks of at most 32 positions (else BDGDN_ERR_UNSUPPORTED).  With grouped value heads
  * (h_v > h_qk) dq, dk, dqn, dkn are summed with floating-point atomics (summation order
  * not fixed); otherwise every result is deterministic.
+ * Range: do, don and the state gradients enter the products as fp16 operands, so entries
+ * below 2^-14 in magnitude lose relative precision (below ~6e-8 they flush to zero) and
+ * entries above 65504 overflow.  Every result is linear in do, don and dht: a caller whose
+ * upstream gradients are that small (a loss averaged over many tokens) scales them by a
+ * power of two into range and divides the results by it (loss scaling), which is exact.
  */
 int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc,
                     const void *q, const void *k, const void *v,
