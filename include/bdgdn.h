@@ -233,7 +233,8 @@ size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
  * below 2^-14 in magnitude lose relative precision (below ~6e-8 they flush to zero) and
  * entries above 65504 overflow.  Every result is linear in do, don and dht: a caller whose
  * upstream gradients are that small (a loss averaged over many tokens) scales them by a
- * power of two into range and divides the results by it (loss scaling), which is exact.
+ * power of two into range and divides the results by it (loss scaling); that changes no
+ * rounding except of the entries it moves across 2^-14.
  */
 int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc,
                     const void *q, const void *k, const void *v,
