@@ -12,7 +12,7 @@ import torch
 import oracle
 import paper_2606_01774_amd as bd
 from paper_2606_01774_amd import workloads as W
-from parity_utils import TOL, rel_err
+from parity_utils import TOL, rel_err, unit_errors
 
 pytestmark = pytest.mark.gpu
 
@@ -70,32 +70,50 @@ def test_bwd_matches_oracle(B, T, hqk, hv, L, kw):
     _check(B, T, hqk, hv, L, 300 + T + L, **kw)
 
 
-def test_bwd_training_workload_sampled_units():
-    """The benchmark's shape (4 x 4096 + 4096 tokens, 16 heads, L = 32), run whole on the
-    GPU; three (sequence, head) units checked against the oracle one by one (the units are
-    independent: no q/k head is shared)."""
-    w = W.TRAIN_4K
-    inp = W.make_train(w)
-    rng = np.random.default_rng(91)
-    shape = (w.batch, w.seqlen, w.h_v, w.d_v)
+def _all_units(got, ref, B):
+    """Worst per-unit max |err| / RMS of every gradient, over all (sequence, head) units."""
+    worst = {}
+    for name in NAMES + ("dh0",):
+        kind = None if name == "dh0" else (name in ("dg", "dbeta", "dgn", "dbetan"))
+        e, where, n = unit_errors(got[name], ref[name], per_token=kind)
+        worst[name] = e
+        print(f"  {name}: worst unit {where} {e:.2e} over {n} units", flush=True)
+    for name, e in worst.items():
+        assert e <= TOL["bf16"], f"{name}: {e:.3e}"
+
+
+def _full_size_bwd(B, T, hqk, hv, L, inp, seed):
+    rng = np.random.default_rng(seed)
+    shape = (B, T, hv, 128)
     do = torch.from_numpy(rng.standard_normal(shape, dtype=np.float32))
     don = torch.from_numpy(rng.standard_normal(shape, dtype=np.float32))
-    scale = 1.0 / math.sqrt(w.d_k)
+    scale = 1.0 / math.sqrt(128)
     d = {k: v.cuda() for k, v in inp.items()}
-    print(f"bwd {w.name}", flush=True)
+    print(f"bwd B={B} T={T} hqk={hqk} hv={hv} L={L}: GPU", flush=True)
     got = bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
-                             d["betan"], do.cuda(), don.cuda(), block=w.block, scale=scale, want_dh0=True)
+                             d["betan"], do.cuda(), don.cuda(), block=L, scale=scale, want_dh0=True)
     torch.cuda.synchronize()
-    for b, h in ((0, 0), (2, 7), (3, 15)):
-        sl = lambda x: x[b:b + 1, :, h:h + 1]
-        u = {k: sl(v) for k, v in inp.items()}
-        ref = oracle.bwd_train(u["q"], u["k"], u["v"], u["g"], u["beta"], u["qn"], u["kn"], u["vn"], u["gn"],
-                               u["betan"], sl(do), sl(don), block=w.block, scale=scale)
-        errs = {n: rel_err(sl(got[n].cpu()), ref[n]) for n in NAMES}
-        errs["dh0"] = rel_err(got["dh0"][b:b + 1, h:h + 1].cpu(), ref["dh0"])
-        print(f"  unit ({b}, {h}): " + " ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
-        for name, e in errs.items():
-            assert e <= TOL["bf16"], f"unit ({b}, {h}) {name}: {e:.3e}"
+    got = {k: v.cpu() for k, v in got.items()}
+    del d
+    print("  oracle", flush=True)
+    ref = oracle.bwd_train(inp["q"], inp["k"], inp["v"], inp["g"], inp["beta"], inp["qn"], inp["kn"], inp["vn"],
+                           inp["gn"], inp["betan"], do, don, block=L, scale=scale)
+    _all_units(got, ref, B)
+
+
+def test_bwd_training_workload_all_units():
+    """The benchmark's shape (4 x 4096 + 4096 tokens, 16 heads, L = 32), run whole on the
+    GPU; every (sequence, head) unit of every gradient compared with one oracle call."""
+    w = W.TRAIN_4K
+    _full_size_bwd(w.batch, w.seqlen, w.h_qk, w.h_v, w.block, W.make_train(w), 91)
+
+
+def test_bwd_grouped_heads_long_sequences_all_units():
+    """The grouped-value shape (2 x 16384 + 16384 tokens, 16 q/k heads shared by 32 v heads),
+    with blocks of 32, run whole on the GPU; every unit compared (dq, dk of a q/k head summed
+    over its two v heads)."""
+    B, T, hqk, hv, L = 2, 16384, 16, 32, 32
+    _full_size_bwd(B, T, hqk, hv, L, W.make_custom_train(B, T, hqk, hv, 128, 128, "bf16", seed=1234), 93)
 
 
 KEYS = ("q", "k", "v", "g", "beta")
@@ -160,37 +178,6 @@ def test_bwd_one_view_equals_two_stream_backward():
         assert torch.equal(got_c[n], ref[n]), n
     for n in ("dq", "dk", "dv", "dg", "dbeta"):
         assert torch.equal(got_v[0][n], ref[n + "n"]), n
-
-
-def test_bwd_grouped_heads_long_sequences_sampled_units():
-    """The grouped-value shape (2 x 16384 + 16384 tokens, 16 q/k heads shared by 32 v heads)
-    with blocks of 32, run whole on the GPU; two (sequence, q/k head) units, each with its
-    two v heads, checked against the oracle (dq, dk summed over the two v heads)."""
-    B, T, hqk, hv, L = 2, 16384, 16, 32, 32
-    inp = W.make_custom_train(B, T, hqk, hv, 128, 128, "bf16", seed=1234)
-    rng = np.random.default_rng(93)
-    do = torch.from_numpy(rng.standard_normal((B, T, hv, 128), dtype=np.float32))
-    don = torch.from_numpy(rng.standard_normal((B, T, hv, 128), dtype=np.float32))
-    scale = 1.0 / math.sqrt(128)
-    d = {k: v.cuda() for k, v in inp.items()}
-    print(f"bwd grouped B={B} T={T} hqk={hqk} hv={hv} L={L}", flush=True)
-    got = bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
-                             d["betan"], do.cuda(), don.cuda(), block=L, scale=scale, want_dh0=True)
-    torch.cuda.synchronize()
-    for b, j in ((0, 3), (1, 14)):
-        qk = lambda x: x[b:b + 1, :, j:j + 1]
-        vh = lambda x: x[b:b + 1, :, 2 * j:2 * j + 2]
-        u = {k: (qk(v) if k in ("q", "k", "qn", "kn") else vh(v)) for k, v in inp.items()}
-        ref = oracle.bwd_train(u["q"], u["k"], u["v"], u["g"], u["beta"], u["qn"], u["kn"], u["vn"], u["gn"],
-                               u["betan"], vh(do), vh(don), block=L, scale=scale)
-        errs = {}
-        for n in NAMES:
-            sl = qk if n in ("dq", "dk", "dqn", "dkn") else vh
-            errs[n] = rel_err(sl(got[n]).cpu(), ref[n])
-        errs["dh0"] = rel_err(got["dh0"][b:b + 1, 2 * j:2 * j + 2].cpu(), ref["dh0"])
-        print(f"  unit ({b}, {j}): " + " ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
-        for name, e in errs.items():
-            assert e <= TOL["bf16"], f"unit ({b}, {j}) {name}: {e:.3e}"
 
 
 @pytest.mark.gpu

@@ -9,7 +9,7 @@ import torch
 
 import paper_2606_01774_amd as bd
 from paper_2606_01774_amd import workloads as W
-from parity_utils import TOL, oracle_full, oracle_unit, rel_err, to_dev
+from parity_utils import TOL, oracle_full, rel_err, to_dev, unit_errors
 
 pytestmark = pytest.mark.gpu
 
@@ -149,51 +149,45 @@ def test_determinism_and_isolation():
     assert not torch.equal(on3[:, mask], on1[:, mask])
 
 
-def _sampled_units(w, inp, units, o, on, ht, cu=None):
-    scale = 1.0 / math.sqrt(w.d_k)
-    ratio = w.h_v // w.h_qk
-    worst = [0.0, 0.0, 0.0]
-    for (b, h) in units:
-        if cu is None:
-            ro, ron, rht = oracle_unit(inp, b, h, ratio, w.block, scale)
-            go, gon, ght = o[b, :, h], on[b, :, h], ht[b, h]
-        else:
-            a, e = int(cu[b]), int(cu[b + 1])
-            ro, ron, rht = oracle_unit(inp, 0, h, ratio, w.block, scale, rows=(a, e))
-            go, gon, ght = o[0, a:e, h], on[0, a:e, h], ht[b, h]
-        errs = (rel_err(go, ro), rel_err(gon, ron), rel_err(ght, rht))
-        print(f"unit (seq {b}, head {h}): err o={errs[0]:.3e} on={errs[1]:.3e} ht={errs[2]:.3e}")
-        worst = [max(x, y) for x, y in zip(worst, errs)]
-    tol = TOL[w.dtype]
-    assert max(worst) <= tol, worst
-
-
-def _full_size(w, units_fn):
+def _full_size(w):
+    """The whole workload on the GPU in the benchmark's launch configuration, every
+    (sequence or document, v-head) unit compared with one multi-threaded oracle call:
+    the worst per-unit max |err| / RMS of o, on and ht must meet the tolerance."""
     inp = W.make_train(w)
     d = to_dev(inp)
-    if "cu_seqlens" in inp:
-        d["cu_host"] = inp["cu_seqlens"]
-    o, on, ht = _run_gpu(d, w.block, 1.0 / math.sqrt(w.d_k))
+    cu = inp.get("cu_seqlens")
+    if cu is not None:
+        d["cu_host"] = cu
+    scale = 1.0 / math.sqrt(w.d_k)
+    print(f"{w.name}: GPU", flush=True)
+    o, on, ht = _run_gpu(d, w.block, scale)
     assert torch.isfinite(o.float()).all() and torch.isfinite(on.float()).all()
     o, on, ht = o.cpu(), on.cpu(), ht.cpu()
-    _sampled_units(w, inp, units_fn(inp), o, on, ht, cu=inp.get("cu_seqlens"))
+    del d
+    print(f"{w.name}: oracle", flush=True)
+    ro, ron, rht = oracle_full(inp, w.block, scale, cu=cu)
+    tol = TOL[w.dtype]
+    worst = {}
+    for name, gpu, ref, kind in (("o", o, ro, False), ("on", on, ron, False), ("ht", ht, rht, None)):
+        e, where, n = unit_errors(gpu, ref, cu=None if cu is None else cu.numpy(), per_token=kind)
+        print(f"  {name}: worst unit {where} max|err|/rms = {e:.3e} over {n} units; "
+              f"whole tensor {rel_err(gpu, ref):.3e}", flush=True)
+        worst[name] = e
+    expected = (len(cu) - 1 if cu is not None else w.batch) * w.h_v
+    assert n == expected - (0 if cu is None else int((np.diff(cu.numpy()) == 0).sum()) * w.h_v)
+    assert max(worst.values()) <= tol, worst
 
 
-def test_full_train_4k_sampled():
-    _full_size(W.TRAIN_4K, lambda inp: [(0, 0), (1, 7), (2, 12), (3, 15)])
+def test_full_train_4k_all_units():
+    _full_size(W.TRAIN_4K)
 
 
-def test_full_gva_16k_sampled():
-    _full_size(W.GVA_16K, lambda inp: [(0, 0), (1, 31)])
+def test_full_gva_16k_all_units():
+    _full_size(W.GVA_16K)
 
 
-def test_full_varlen_128k_sampled():
-    def units(inp):
-        lengths = inp["lengths"]
-        longest = int(np.argmax(lengths))
-        shortest = int(np.argmin(lengths))
-        return [(longest, 3), (shortest, 9), (5, 15)]
-    _full_size(W.VARLEN_128K, units)
+def test_full_varlen_128k_all_units():
+    _full_size(W.VARLEN_128K)
 
 
 def test_bf16_outputs():
