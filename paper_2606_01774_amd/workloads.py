@@ -227,3 +227,15 @@ def draw_conv(rng, batch, seqlen, channels, width, dtype, bias=True):
 def make_conv(w: ConvWorkload, seed: int | None = None):
     rng = np.random.default_rng(w.seed if seed is None else seed)
     return draw_conv(rng, w.batch, w.seqlen, w.channels, w.width, w.dtype)
+
+
+# Serving pools: each request's cached state is the clean state after a seeded prefix of
+# SERVE_PREFIX_BLOCKS blocks of the workload's block length (256 tokens at L = 32).
+SERVE_PREFIX_BLOCKS = 8
+
+
+def make_serve_prefix_block(w: ServeWorkload, pool: int, block: int):
+    """Prefix block ``block`` of state pool ``pool`` (seed (seed*1000 + 500 + 16*pool + block)),
+    drawn with the same recipe as the serving blocks."""
+    rng = np.random.default_rng(w.seed * 1000 + 500 + 16 * pool + block)
+    return draw_stream(rng, (w.requests, w.block), w.h_qk, w.h_v, w.d_k, w.d_v, w.dtype)
