@@ -72,6 +72,8 @@ extern "C" {
                                     of block (Appendix "Document-packed training") */
 #define BDGDN_ERR_WORKSPACE   -4 /* workspace smaller than bdgdn_fwd_train_workspace() */
 #define BDGDN_ERR_LAUNCH      -5 /* the HIP runtime reported an error for a launch */
+#define BDGDN_ERR_SCRATCH     -6 /* the input needs more than the fixed scratch of a
+                                    no-allocation entry point (nothing is launched) */
 
 typedef enum { BDGDN_BF16 = 0, BDGDN_F32 = 1 } bdgdn_dtype_t;
 
@@ -403,6 +405,27 @@ int bdgdn_shortconv_bwd(const bdgdn_conv_desc_t *desc, const void *x, const void
                         const float *bias, const void *dy, const void *dyn, const int32_t *cu_seqlens_dev,
                         const int32_t *cu_seqlens_host, void *dx, void *dxn, float *dw, float *dbias,
                         void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * bdgdn_shortconv_bwd without a workspace argument, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving or training loops, harnesses that
+ * forbid allocation).  It computes exactly what bdgdn_shortconv_bwd computes, with the same
+ * kernels and the same summation order (bit-identical results), and calls no allocating
+ * routine: its dw / dbias partials live in a scratch array of BDGDN_NOALLOC_SCRATCH_BYTES
+ * that the library holds on each GPU it runs on until the process ends (looked up on the
+ * first call on a device; the stream's device, or the current device for a NULL stream).
+ * Inputs needing more than that (bdgdn_shortconv_bwd_workspace(desc) bytes: 4 (width + 1)
+ * channels bytes per started group of 256 rows, e.g. 7.5 MiB for 16384 rows of 6144
+ * channels at width 4) return BDGDN_ERR_SCRATCH before anything is launched.  Every call on one GPU
+ * shares that GPU's scratch: calls whose execution overlaps on one GPU (different streams,
+ * or threads launching concurrently) race and give undefined dw / dbias; serialise them
+ * on one stream.  The caller still owns every input and output buffer.
+ */
+#define BDGDN_NOALLOC_SCRATCH_BYTES (32u << 20)
+int bdgdn_shortconv_bwd_noalloc(const bdgdn_conv_desc_t *desc, const void *x, const void *xn, const float *w,
+                                const float *bias, const void *dy, const void *dyn,
+                                const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host, void *dx,
+                                void *dxn, float *dw, float *dbias, void *stream);
 
 #ifdef __cplusplus
 }

@@ -37,6 +37,8 @@ BDGDN_ERR_UNSUPPORTED = -2
 BDGDN_ERR_UNALIGNED = -3
 BDGDN_ERR_WORKSPACE = -4
 BDGDN_ERR_LAUNCH = -5
+BDGDN_ERR_SCRATCH = -6
+BDGDN_NOALLOC_SCRATCH_BYTES = 32 << 20
 BDGDN_BF16 = 0
 BDGDN_F32 = 1
 BDGDN_ROUTE_FUSED = 0
@@ -51,7 +53,8 @@ EXPORTED_SYMBOLS = ("bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_wor
                     "bdgdn_accept_states", "bdgdn_shortconv_fwd", "bdgdn_shortconv_bwd_workspace",
                     "bdgdn_shortconv_bwd", "bdgdn_bwd_train_workspace", "bdgdn_bwd_train",
                     "bdgdn_fwd_train_views_workspace", "bdgdn_fwd_train_views",
-                    "bdgdn_bwd_train_views_workspace", "bdgdn_bwd_train_views")
+                    "bdgdn_bwd_train_views_workspace", "bdgdn_bwd_train_views",
+                    "bdgdn_shortconv_bwd_noalloc")
 
 
 class FwdDesc(ctypes.Structure):
@@ -147,6 +150,8 @@ def load_library():
     lib.bdgdn_shortconv_bwd_workspace.restype = ctypes.c_size_t
     lib.bdgdn_shortconv_bwd.argtypes = [ctypes.POINTER(ConvDesc)] + [P] * 13 + [ctypes.c_size_t, P]
     lib.bdgdn_shortconv_bwd.restype = ctypes.c_int
+    lib.bdgdn_shortconv_bwd_noalloc.argtypes = [ctypes.POINTER(ConvDesc)] + [P] * 13
+    lib.bdgdn_shortconv_bwd_noalloc.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -642,4 +647,35 @@ def bdgdn_shortconv_bwd(x, xn, w, bias, dy, dyn, *, block, activation=BDGDN_ACT_
                                  _ptr(dx), _ptr(dxn), _ptr(dw), _ptr(dbias), _ptr(workspace), ws_size,
                                  _stream(stream))
     _check(st, "bdgdn_shortconv_bwd")
+    return dx, dxn, dw, dbias
+
+
+def bdgdn_shortconv_bwd_noalloc(x, xn, w, bias, dy, dyn, *, block, activation=BDGDN_ACT_SILU, cu_seqlens=None,
+                                cu_seqlens_host=None, dx=None, dxn=None, dw=None, dbias=None, stream=None):
+    """bdgdn_shortconv_bwd through the entry point that allocates nothing: its partial sums
+    live in the library's fixed per-GPU scratch (BDGDN_NOALLOC_SCRATCH_BYTES).  Pass every
+    output to keep the call free of allocation here too.  Returns (dx, dxn, dw, dbias)."""
+    lib = load_library()
+    _dev(x, "x")
+    for name, t in (("xn", xn), ("dy", dy), ("dyn", dyn)):
+        _dev(t, name, x.dtype)
+        if t.shape != x.shape:
+            raise ValueError(f"{name} must match x")
+    _dev(w, "w", torch.float32)
+    _dev(bias, "bias", torch.float32)
+    n, cu_h = _conv_packing(x, cu_seqlens, cu_seqlens_host)
+    desc = make_conv_desc(x, w, block=block, activation=activation, num_seqs=n)
+    dx = torch.empty_like(x) if dx is None else dx
+    dxn = torch.empty_like(x) if dxn is None else dxn
+    dw = torch.empty_like(w) if dw is None else dw
+    if dbias is None and bias is not None:
+        dbias = torch.empty_like(bias)
+    for name, t, dt in (("dx", dx, x.dtype), ("dxn", dxn, x.dtype), ("dw", dw, torch.float32),
+                        ("dbias", dbias, torch.float32)):
+        _dev(t, name, dt)
+    st = lib.bdgdn_shortconv_bwd_noalloc(ctypes.byref(desc), _ptr(x), _ptr(xn), _ptr(w), _ptr(bias), _ptr(dy),
+                                         _ptr(dyn), _ptr(cu_seqlens),
+                                         None if cu_h is None else ctypes.c_void_p(cu_h.data_ptr()),
+                                         _ptr(dx), _ptr(dxn), _ptr(dw), _ptr(dbias), _stream(stream))
+    _check(st, "bdgdn_shortconv_bwd_noalloc")
     return dx, dxn, dw, dbias

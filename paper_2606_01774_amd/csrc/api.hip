@@ -125,6 +125,7 @@ const char *bdgdn_status_string(int status)
     case BDGDN_ERR_UNALIGNED: return "document start not aligned to the diffusion block";
     case BDGDN_ERR_WORKSPACE: return "workspace too small";
     case BDGDN_ERR_LAUNCH: return "kernel launch failed";
+    case BDGDN_ERR_SCRATCH: return "input larger than the fixed scratch of the no-allocation entry point";
     default: return "unknown status";
     }
 }
@@ -645,10 +646,10 @@ int bdgdn_shortconv_fwd(const bdgdn_conv_desc_t *desc, const void *x, const void
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
 }
 
-int bdgdn_shortconv_bwd(const bdgdn_conv_desc_t *desc, const void *x, const void *xn, const float *w,
-                        const float *bias, const void *dy, const void *dyn, const int32_t *cu_seqlens_dev,
-                        const int32_t *cu_seqlens_host, void *dx, void *dxn, float *dw, float *dbias,
-                        void *workspace, size_t workspace_bytes, void *stream)
+// Validation shared by the two ShortConv backward entry points.
+static int check_conv_bwd(const bdgdn_conv_desc_t *desc, const void *x, const void *xn, const float *w,
+                          const void *dy, const void *dyn, const int32_t *cu_seqlens_dev,
+                          const int32_t *cu_seqlens_host, void *dx, void *dxn, float *dw)
 {
     int st = check_conv(desc, cu_seqlens_dev, cu_seqlens_host);
     if (st != BDGDN_OK) return st;
@@ -656,16 +657,50 @@ int bdgdn_shortconv_bwd(const bdgdn_conv_desc_t *desc, const void *x, const void
     if (!w || !dw || (any && (!x || !xn || !dy || !dyn || !dx || !dxn))) return BDGDN_ERR_INVALID_ARG;
     if (!aligned8(x) || !aligned8(xn) || !aligned8(dy) || !aligned8(dyn) || !aligned8(dx) || !aligned8(dxn))
         return BDGDN_ERR_INVALID_ARG;
+    return BDGDN_OK;
+}
+
+static int conv_bwd_launch(const bdgdn_conv_desc_t *desc, const void *x, const void *xn, const float *w,
+                           const float *bias, const void *dy, const void *dyn, const int32_t *cu_seqlens_dev,
+                           void *dx, void *dxn, float *dw, float *dbias, float *part, hipStream_t stream)
+{
+    ConvArgs a = conv_args(desc, cu_seqlens_dev, x, xn, w, bias, dx, dxn);
+    a.dy = dy; a.dyn = dyn;
+    a.part = part;
+    a.dw = dw;
+    a.dbias = dbias;
+    hipError_t e = launch_shortconv_bwd(desc->dtype == BDGDN_BF16, desc->width, a, stream);
+    return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+}
+
+int bdgdn_shortconv_bwd(const bdgdn_conv_desc_t *desc, const void *x, const void *xn, const float *w,
+                        const float *bias, const void *dy, const void *dyn, const int32_t *cu_seqlens_dev,
+                        const int32_t *cu_seqlens_host, void *dx, void *dxn, float *dw, float *dbias,
+                        void *workspace, size_t workspace_bytes, void *stream)
+{
+    int st = check_conv_bwd(desc, x, xn, w, dy, dyn, cu_seqlens_dev, cu_seqlens_host, dx, dxn, dw);
+    if (st != BDGDN_OK) return st;
     const size_t need = bdgdn_shortconv_bwd_workspace(desc);
     if (need > 0 && (workspace_bytes < need || !workspace)) return BDGDN_ERR_WORKSPACE;
     if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return BDGDN_ERR_WORKSPACE;
-    ConvArgs a = conv_args(desc, cu_seqlens_dev, x, xn, w, bias, dx, dxn);
-    a.dy = dy; a.dyn = dyn;
-    a.part = static_cast<float *>(workspace);
-    a.dw = dw;
-    a.dbias = dbias;
-    hipError_t e = launch_shortconv_bwd(desc->dtype == BDGDN_BF16, desc->width, a, static_cast<hipStream_t>(stream));
-    return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+    return conv_bwd_launch(desc, x, xn, w, bias, dy, dyn, cu_seqlens_dev, dx, dxn, dw, dbias,
+                           static_cast<float *>(workspace), static_cast<hipStream_t>(stream));
+}
+
+static_assert(BDGDN_NOALLOC_SCRATCH_BYTES == kConvScratchBytes, "the header states the scratch size");
+
+int bdgdn_shortconv_bwd_noalloc(const bdgdn_conv_desc_t *desc, const void *x, const void *xn, const float *w,
+                                const float *bias, const void *dy, const void *dyn, const int32_t *cu_seqlens_dev,
+                                const int32_t *cu_seqlens_host, void *dx, void *dxn, float *dw, float *dbias,
+                                void *stream)
+{
+    int st = check_conv_bwd(desc, x, xn, w, dy, dyn, cu_seqlens_dev, cu_seqlens_host, dx, dxn, dw);
+    if (st != BDGDN_OK) return st;
+    if (bdgdn_shortconv_bwd_workspace(desc) > kConvScratchBytes) return BDGDN_ERR_SCRATCH;
+    float *part = nullptr;
+    if (conv_noalloc_scratch(static_cast<hipStream_t>(stream), &part) != hipSuccess) return BDGDN_ERR_LAUNCH;
+    return conv_bwd_launch(desc, x, xn, w, bias, dy, dyn, cu_seqlens_dev, dx, dxn, dw, dbias, part,
+                           static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -28,6 +28,8 @@
 // in a fixed order (deterministic results).
 #include <math.h>
 
+#include <mutex>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -545,5 +547,44 @@ hipError_t launch_shortconv_bwd(bool bf16, int width, const ConvArgs &a, hipStre
 }
 
 #undef BDGDN_CONV_WIDTHS
+
+// The fixed scratch of the no-allocation backward: the per-workgroup dw / dbias partials,
+// in device memory the library holds for the life of the process (each GPU it runs on has
+// its own copy at its own address).  Every partial slot a launch reads is written by that
+// launch first, so nothing needs clearing between calls.  On the host this name is only a
+// stand-in for the device symbol: host code uses the address conv_noalloc_scratch returns.
+static __device__ __align__(256) float scratch[kConvScratchBytes / sizeof(float)];
+
+hipError_t conv_noalloc_scratch(hipStream_t stream, float **ptr)
+{
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static float *addr[kMaxDevices] = {};
+    int cur = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    int dev = cur;
+    if (stream) {
+        e = hipStreamGetDevice(stream, &dev);
+        if (e != hipSuccess) return e;
+    }
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        // the symbol's address on `dev`, looked up once with that device current
+        if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return e;
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (dev != cur) {
+            const hipError_t r = hipSetDevice(cur);
+            if (e == hipSuccess) e = r;
+        }
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[dev] = static_cast<float *>(p);
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
 
 }  // namespace bdgdn

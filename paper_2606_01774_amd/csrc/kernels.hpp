@@ -134,6 +134,10 @@ struct ConvArgs {
     int D, L, act, n_docs, seqlen, n_rg;
 };
 size_t conv_part_floats(long rows, int D, int width);
+// The no-allocation backward's fixed scratch: its size, and its device address on the
+// device of `stream` (the current device for a NULL stream), looked up once per device.
+constexpr size_t kConvScratchBytes = 32u << 20;
+hipError_t conv_noalloc_scratch(hipStream_t stream, float **ptr);
 hipError_t launch_shortconv_fwd(bool bf16, int width, const ConvArgs &a, hipStream_t s);
 hipError_t launch_shortconv_bwd(bool bf16, int width, const ConvArgs &a, hipStream_t s);
 

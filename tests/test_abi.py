@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_status_strings():
     assert bd.bdgdn_version() >= 1
-    for st in (0, -1, -2, -3, -4, -5):
+    for st in (0, -1, -2, -3, -4, -5, -6):
         assert bd.bdgdn_status_string(st)
     assert bd.bdgdn_status_string(-99) == "unknown status"
 
@@ -250,6 +250,37 @@ def test_shortconv_workspace():
     assert _conv("bwd", ws=None, ws_bytes=0) == bd.BDGDN_ERR_WORKSPACE
     assert _conv("bwd", ws=FAKE, ws_bytes=ws() - 4) == bd.BDGDN_ERR_WORKSPACE
     assert _conv("bwd", ws=ctypes.c_void_p(0x1004), ws_bytes=ws()) == bd.BDGDN_ERR_WORKSPACE   # misaligned
+
+
+def test_shortconv_noalloc_validation_and_limit():
+    """The no-allocation backward validates like bdgdn_shortconv_bwd and rejects, before any
+    HIP call, inputs whose partials exceed the fixed scratch."""
+    lib = bd.load_library()
+    P = FAKE
+
+    def call(null_x=False, **kw):
+        d = dict(batch=2, seqlen=64, num_seqs=0, channels=256, width=4, block=8, activation=bd.BDGDN_ACT_SILU,
+                 dtype=bd.BDGDN_BF16)
+        d.update(kw)
+        desc = bd.ConvDesc(**d)
+        return lib.bdgdn_shortconv_bwd_noalloc(ctypes.byref(desc), None if null_x else P, P, P, None, P, P,
+                                               None, None, P, P, P, None, None)
+
+    assert call(width=5) == bd.BDGDN_ERR_UNSUPPORTED
+    assert call(channels=0) == bd.BDGDN_ERR_INVALID_ARG
+    assert call(null_x=True) == bd.BDGDN_ERR_INVALID_ARG
+    assert call(activation=3) == bd.BDGDN_ERR_INVALID_ARG
+    # partials: (width + 1) x channels fp32 per started group of 256 rows
+    per_group = 5 * 6144 * 4
+    groups = bd.BDGDN_NOALLOC_SCRATCH_BYTES // per_group
+    fits = dict(batch=1, seqlen=256 * groups, channels=6144)
+    over = dict(batch=1, seqlen=256 * groups + 1, channels=6144)
+    ws = lambda kw: lib.bdgdn_shortconv_bwd_workspace(ctypes.byref(bd.ConvDesc(
+        **dict(dict(batch=2, seqlen=64, num_seqs=0, channels=256, width=4, block=8, activation=1, dtype=0), **kw))))
+    assert ws(fits) <= bd.BDGDN_NOALLOC_SCRATCH_BYTES < ws(over)
+    assert call(**over) == bd.BDGDN_ERR_SCRATCH
+    assert call(batch=4, seqlen=1 << 20, channels=512, width=2) == bd.BDGDN_ERR_SCRATCH
+    assert "scratch" in bd.bdgdn_status_string(bd.BDGDN_ERR_SCRATCH)
 
 
 def _bwd(desc, ws=None, ws_bytes=0, null_grad=False, **_):
