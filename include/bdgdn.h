@@ -84,7 +84,9 @@ typedef enum { BDGDN_BF16 = 0, BDGDN_F32 = 1 } bdgdn_dtype_t;
  *           on chip and evaluates each noisy block from the in-register boundary state.
  *           With bf16 inputs and blocks of at most 32 positions this is one kernel whose
  *           workgroups also compute each block's UT transform and masked Q K^T a block
- *           ahead (no workspace); otherwise it is the RECORDS schedule.
+ *           ahead (no workspace); blocks of an even 34 .. 64 positions run the same kernel
+ *           on sub-blocks of half the block, each noisy block carrying its state across
+ *           its two halves (no workspace); otherwise it is the RECORDS schedule.
  *  SPLIT:   boundary states through HBM and a separate noisy-block kernel (Appendix
  *           "Route I"): the clean scan writes the clean state before every block (the
  *           seed of that noisy block) into the workspace, fp32 [block][h_v][d_k][d_v]
@@ -194,9 +196,10 @@ typedef struct {
  * for FUSED or for a descriptor it would reject. */
 size_t bdgdn_fwd_train_views_workspace(const bdgdn_fwd_desc_t *desc);
 
-/* Clean inputs, h0, o, ht and cu_seqlens as for bdgdn_fwd_train (desc->route is not used);
- * views[0 .. n_views-1], 1 <= n_views <= 16.  bf16 inputs, d_k = d_v = 128 and blocks of
- * at most 32 positions (else BDGDN_ERR_UNSUPPORTED). */
+/* Clean inputs, h0, o, ht and cu_seqlens as for bdgdn_fwd_train; views[0 .. n_views-1],
+ * 1 <= n_views <= 16.  bf16 inputs; FUSED takes the blocks the one-kernel forward takes (at
+ * most 32 positions, or an even 34 .. 64), SPLIT needs d_k = d_v = 128 and blocks of at most
+ * 32 positions (else BDGDN_ERR_UNSUPPORTED). */
 int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc,
                           const void *q, const void *k, const void *v,
                           const float *g, const float *beta,

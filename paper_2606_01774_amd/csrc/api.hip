@@ -138,10 +138,29 @@ static long total_blocks(const bdgdn_fwd_desc_t *d)
     return d->num_seqs > 0 ? nblk : nblk * d->batch;
 }
 
+// Blocks of 34 .. 64 positions (even) run the one-kernel forward on two sub-blocks of half
+// the block each.
+static bool pair_blocks(const bdgdn_fwd_desc_t *d, Types ty)
+{
+    return !pipelined_supported(ty, d->d_k, lp_of(d->block)) && pair_supported(ty, d->d_k, d->block);
+}
+
 // The fused route runs as one kernel where it can, else through the UT records.
 static bool one_kernel(const bdgdn_fwd_desc_t *d, Types ty)
 {
-    return d->route == BDGDN_ROUTE_FUSED && pipelined_supported(ty, d->d_k, lp_of(d->block));
+    return d->route == BDGDN_ROUTE_FUSED &&
+           (pipelined_supported(ty, d->d_k, lp_of(d->block)) || pair_blocks(d, ty));
+}
+
+// The one-kernel forward on a descriptor's chains: the sub-block is the block, or half of
+// it for pairs.
+static hipError_t launch_one_kernel(const bdgdn_fwd_desc_t *d, Types ty, ScanArgs sa, hipStream_t s,
+                                    bool clean_out = true)
+{
+    if (!pair_blocks(d, ty)) return launch_fwd_pipelined(ty, d->d_k, lp_of(d->block), sa, s, clean_out);
+    sa.L = d->block / 2;
+    sa.nblk = (d->seqlen + sa.L - 1) / sa.L;
+    return launch_fwd_pipelined_pair(ty, d->d_k, sa, s, clean_out);
 }
 
 static size_t workspace_bytes_of(const bdgdn_fwd_desc_t *d)
@@ -241,7 +260,7 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
             na.scale = desc->scale;
             e = launch_fwd_split(ty, lp, sa, na, strm);
         } else {
-            e = one_kernel(desc, ty) ? launch_fwd_pipelined(ty, desc->d_k, lp, sa, strm)
+            e = one_kernel(desc, ty) ? launch_one_kernel(desc, ty, sa, strm)
                                      : launch_fwd_scan(ty, desc->d_k, lp, ia, sa, strm);
         }
     } else {
@@ -358,11 +377,15 @@ int bdgdn_accept_states(const bdgdn_serve_desc_t *desc, float *state_pool, const
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
 }
 
+// The views forward: FUSED runs the one-kernel forward once per view (any block it takes);
+// SPLIT writes the seeds in the one-kernel forward and needs blocks of at most 32.
 static bool views_supported(const bdgdn_fwd_desc_t *d)
 {
     Types ty;
-    return types_of(d->dtype, d->out_dtype, ty) && split_supported(ty, d->d_k, d->d_v, lp_of(d->block)) &&
-           pipelined_supported(ty, d->d_k, lp_of(d->block));
+    if (!types_of(d->dtype, d->out_dtype, ty)) return false;
+    if (d->route == BDGDN_ROUTE_SPLIT)
+        return split_supported(ty, d->d_k, d->d_v, lp_of(d->block)) && pipelined_supported(ty, d->d_k, lp_of(d->block));
+    return pipelined_supported(ty, d->d_k, lp_of(d->block)) || pair_blocks(d, ty);
 }
 
 size_t bdgdn_fwd_train_views_workspace(const bdgdn_fwd_desc_t *desc)
@@ -437,7 +460,7 @@ int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc, const void *q, const voi
             sa.gn = views[i].g; sa.betan = views[i].beta;
             sa.on = views[i].o;
             sa.ht = i == 0 ? ht : nullptr;
-            e = launch_fwd_pipelined(ty, desc->d_k, lp, sa, strm, i == 0);
+            e = launch_one_kernel(desc, ty, sa, strm, i == 0);
             if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
         }
         return BDGDN_OK;

@@ -39,8 +39,12 @@ namespace bdgdn {
 // operand in LDS by the otherwise idle N waves, off the C waves' path.
 // NO_O: no clean outputs (the O waves stand idle): a further noisy view of the
 // complementary-view forward, whose clean stream an earlier pass has written.
+// PAIR: the noisy block is two consecutive sub-blocks of the chain (blocks of 2 x the chain's
+// sub-block, e.g. 64 positions as two halves of 32): the N waves carry the noisy state
+// across the pair and the first half's rows also read the state at the end of the second
+// (see n_block_pair).  The clean stream does not care how it is cut into blocks.
 template <typename Out, int DK, int LP, bool SPLIT = false, bool SEEDS = SPLIT, typename SeedT_ = float,
-          bool STATES = false, bool NO_O = false>
+          bool STATES = false, bool NO_O = false, bool PAIR = false>
 struct Fused {
     typedef SeedT_ SeedT;
     static_assert(!STATES || (SPLIT && SEEDS && sizeof(SeedT_) == 2), "STATES: the split scan, fp16 seeds");
@@ -77,7 +81,14 @@ struct Fused {
     static constexpr int OFF_DT = OFF_ST + 2 * ST_B;
     static constexpr int OFF_US = OFF_DT + 2 * DT_B;
     static constexpr int OFF_SINK = OFF_US + 2 * US_B;
-    static constexpr int BYTES = OFF_SINK + 64 * 16;
+    // PAIR: the noisy state after the first half (fp16 operand, laid out like the state
+    // operand), the first half's readout accumulators Y1 (fp32, per N wave and lane) and the
+    // cross Gram tile R12 (fp16 A-operand quads [bi][bj][lane])
+    static_assert(!PAIR || (LP == 32 && !SPLIT), "pairs of 32-position sub-blocks, noisy waves active");
+    static constexpr int OFF_NS = OFF_SINK + 64 * 16;
+    static constexpr int OFF_Y1 = OFF_NS + (PAIR ? ST_B : 0);
+    static constexpr int OFF_R12 = OFF_Y1 + (PAIR ? 2 * NB * 64 * 16 : 0);
+    static constexpr int BYTES = OFF_R12 + (PAIR ? NB * NB * 64 * 8 : 0);
     static_assert(BYTES <= 160 * 1024, "LDS budget");
     // staging team
     static constexpr int TT = 256;
@@ -122,6 +133,15 @@ struct Fused {
     __device__ __forceinline__ E *st(int b) const { return reinterpret_cast<E *>(smem + OFF_ST + b * ST_B); }
     __device__ __forceinline__ E *dt(int b) const { return reinterpret_cast<E *>(smem + OFF_DT + b * DT_B); }
     __device__ __forceinline__ float *us(int u) const { return reinterpret_cast<float *>(smem + OFF_US + u * US_B); }
+    __device__ __forceinline__ E *ns() const { return reinterpret_cast<E *>(smem + OFF_NS); }
+    __device__ __forceinline__ f32x4 *y1(int bc) const
+    {
+        return reinterpret_cast<f32x4 *>(smem + OFF_Y1) + bc * NB * 64;
+    }
+    __device__ __forceinline__ QE *r12(int bi, int bj) const
+    {
+        return reinterpret_cast<QE *>(smem + OFF_R12) + (bi * NB + bj) * 64;
+    }
 
     // Element offset of (row, k) in a swizzled [rows][DK] matrix: chunk k/8 of a row is
     // stored at chunk (k/8) ^ (row / RPB mod CPR).
@@ -483,6 +503,103 @@ struct Fused {
         for (int rb = 0; rb < NB; ++rb) o[rb] = mma_q<E, NB>(x4[rb], rq[rb], nq);
         store_out(on, stride, nvalid, bc, o, scale);
     }
+    // PAIR: one half of a noisy block of two sub-blocks.  First half (half 0), from the
+    // clean seed S0: Delta~1, the readout Y1 = Q~1 S~1 of the half-end noisy state S~1 (kept
+    // in LDS), S~1 itself (the second half's seed, an fp16 operand in LDS) and the unscaled
+    // cross Gram tile R12 = Q~1 K~2^T with the second half's keys, which sit in the next ring
+    // slot already (each N wave builds one 16-row block of it).  Second half, from S~1: its
+    // own rows as in n_block, and the first half's rows, which read the block-end state too:
+    //     O~1 = gamma~2 Y1 + R12 diag(2^(G~2_n - G~2_i)) Delta~2.
+    // A block whose second half holds no rows stores Y1 directly.
+    __device__ __forceinline__ void n_block_pair(int slot, int slot_next, int p, int sb, int bc, int half,
+                                                 bool has_next, Out *on, Out *on_prev, int stride, int nvalid,
+                                                 int nvalid_prev, float scale, const QOffs &qo) const
+    {
+        const int g = lane >> 4;
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        const f32x4 zs[NB] = {};
+        const E *seed = (half ? ns() : st(sb)) + 16 * bc * DK;
+        f32x4 o[NB];
+        QE uq[NB];   // Delta~ rows times the decay to the half end
+        float gn_end;
+        {
+            QE sq[DKB];
+            ld_q<DKB>(sq, seed, qo.q);
+            QE kq[NB][DKB];
+            f32x4 x3[NB], x4[NB];
+            QE rq[NB][NB];
+#pragma unroll
+            for (int rb = 0; rb < NB; ++rb) {
+                ld_q<DKB>(kq[rb], rows(slot, 2) + 16 * rb * DK, qo.q);
+                x3[rb] = mma_q<E, DKB>(z, kq[rb], sq);
+            }
+            gn_end = fac(p, 2)[LP - 1];
+#pragma unroll
+            for (int bi = 0; bi < NB; ++bi) {
+                QE qq[DKB];
+                ld_q<DKB>(qq, rows(slot, 3) + 16 * bi * DK, qo.q);
+                x4[bi] = mma_q<E, DKB>(z, qq, sq) * gn_end;
+#pragma unroll
+                for (int bj = 0; bj < NB; ++bj)
+                    rq[bi][bj] = quad_of<E>(mma_q<E, DKB>(z, kq[bj], qq) * ld4f(fac(p, 4) + 16 * bj + 4 * g));
+            }
+            QE dq[NB];
+            d_quads(dq, x3, vs(p, 1), fac(p, 2), bc);
+            f32x4 dn[NB];
+            m_times(dn, tm(p, 1), dq, zs);
+            QE nq[NB];
+#pragma unroll
+            for (int rb = 0; rb < NB; ++rb) {
+                nq[rb] = quad_of<E>(dn[rb]);
+                uq[rb] = quad_of<E>(dn[rb] * ld4f(fac(p, 4) + 16 * rb + 4 * g));
+            }
+#pragma unroll
+            for (int rb = 0; rb < NB; ++rb) o[rb] = mma_q<E, NB>(x4[rb], rq[rb], nq);
+        }
+        if (half == 0) {
+            if (!has_next) {
+                store_out(on, stride, nvalid, bc, o, scale);
+                return;
+            }
+#pragma unroll
+            for (int rb = 0; rb < NB; ++rb) y1(bc)[rb * 64 + lane] = o[rb];
+            // S~1 = gamma~ S0 + K~1^T diag(dG~) Delta~1, this wave's 16 columns
+            const E *K = rows(slot, 2);
+            // this wave's columns of the seed buffer; the offset is made opaque so that the
+            // eight store addresses are formed here, not held in registers across the loop
+            unsigned ofs = (unsigned)(OFF_NS + 32 * bc * DK);
+            asm volatile("" : "+s"(ofs));
+            E *dst = reinterpret_cast<E *>(smem + ofs);
+#pragma unroll
+            for (int kb = 0; kb < DKB; ++kb) {
+                QE a[NB];
+                kt_quads(a, K, kb, qo);
+                typedef const __attribute__((address_space(3))) volatile QE *LQ;
+                const f32x4 s0 = __builtin_convertvector(*(LQ)(seed + qo.q[kb]), f32x4) * gn_end;
+                st_quad(dst + qo.q[kb], quad_of<E>(mma_q<E, NB>(s0, a, uq)));
+            }
+            // R12, row block bc
+            QE qq[DKB];
+            ld_q<DKB>(qq, rows(slot, 3) + 16 * bc * DK, qo.q);
+#pragma unroll
+            for (int bj = 0; bj < NB; ++bj) {
+                QE k2[DKB];
+                ld_q<DKB>(k2, rows(slot_next, 2) + 16 * bj * DK, qo.q);
+                r12(bc, bj)[lane] = quad_of<E>(mma_q<E, DKB>(z, k2, qq));
+            }
+        } else {
+            store_out(on, stride, nvalid, bc, o, scale);
+            f32x4 o1[NB];
+#pragma unroll
+            for (int bi = 0; bi < NB; ++bi) {
+                QE a[NB];
+#pragma unroll
+                for (int bj = 0; bj < NB; ++bj) a[bj] = r12(bi, bj)[lane];
+                o1[bi] = mma_q<E, NB>(y1(bc)[bi * 64 + lane] * gn_end, a, uq);
+            }
+            store_out(on_prev, stride, nvalid_prev, bc, o1, scale);
+        }
+    }
     // O, first half: X2 = diag(eG) Q S0 and P_rc = 2^(G_r - G_c) (q_r . k_c), c <= r, of
     // block j in registers (P in the A-operand layout, as for R above).
     __device__ __forceinline__ void o_begin(int slot, int p, int sb, int bc, f32x4 (&x2)[NB], QE (&pq)[NB][NB],
@@ -650,8 +767,17 @@ struct Fused {
             Ptrs pc = c.p0;
             lds_barrier();
             lds_barrier();
+            Out *on_prev = pc.on;
             for (int j = 0; j < nb; ++j) {
-                n_block(j % 3, j & 1, j & 1, bc, pc.on, c.vst, nv(j), c.scale, qo);
+                if constexpr (PAIR) {
+                    // chains start on block boundaries, so even sub-blocks open a block
+                    const int half = j & 1;
+                    n_block_pair(j % 3, (j + 1) % 3, half, half, bc, half, half == 0 && nv(j + 1) > 0, pc.on,
+                                 on_prev, c.vst, nv(j), nv(j - 1), c.scale, qo);
+                    on_prev = pc.on;
+                } else {
+                    n_block(j % 3, j & 1, j & 1, bc, pc.on, c.vst, nv(j), c.scale, qo);
+                }
                 advance(pc, c);
                 lds_barrier();
             }
@@ -732,9 +858,20 @@ struct Fused {
     }
 };
 
-// One workgroup's chain: (sequence or document, v-head, d_v tile) from the block id.  Ids
-// i, i+8, i+16, ... of a group carry the d_v tiles of one chain, so they land on one XCD
-// and share its L2 for the q/k rows and gates.
+// Workgroups of the chain kernels: the r = h_v / h_qk v-heads of a q/k head times the d_v
+// tiles form one group of r * n_vt workgroups per (sequence, q/k head), and eight such
+// groups interleave, so that the ids of one group are i, i + 8, i + 16, ...: workgroup ids
+// are dealt to the eight XCDs in turn, so a group runs on one XCD and reads its q/k rows
+// (shared by its v-heads and tiles) through one L2.
+__host__ __device__ __forceinline__ int chain_grid(const ScanArgs &a)
+{
+    const int r = a.h_v / a.h_qk;
+    const int n_qk = a.n_chains / r;
+    return (n_qk + 7) / 8 * 8 * r * a.n_vt;
+}
+
+// One workgroup's chain: (sequence or document, v-head, d_v tile) from the block id, as
+// chain_grid lays them out.
 template <typename K>
 __device__ __forceinline__ void run_chain(const ScanArgs &a, unsigned char *smem)
 {
@@ -743,12 +880,14 @@ __device__ __forceinline__ void run_chain(const ScanArgs &a, unsigned char *smem
     typedef typename K::OutT Out;
     constexpr int DK = K::DKC;
     const int id = blockIdx.x;
-    const int per = 8 * a.n_vt;
-    const int chain = (id / per) * 8 + (id % 8);
-    const int vt = (id % per) / 8;
-    if (chain >= a.n_chains) return;
-    int seq = chain / a.h_v;
-    const int h = chain % a.h_v;
+    const int r = a.h_v / a.h_qk;
+    const int per = 8 * r * a.n_vt;
+    const int qc = (id / per) * 8 + (id % 8);   // (sequence, q/k head)
+    const int wk = (id % per) / 8;             // (v-head of the group, d_v tile)
+    const int vt = wk % a.n_vt;
+    if (qc >= a.n_chains / r) return;
+    int seq = qc / a.h_qk;
+    const int h = (qc % a.h_qk) * r + wk / a.n_vt;
     if (a.n_order > 0) seq = a.order[seq];
     long base, len;
     if (a.cu) {

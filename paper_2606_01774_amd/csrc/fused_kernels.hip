@@ -23,11 +23,24 @@ __global__ void __launch_bounds__(768) bdgdn_fwd_pipelined_noisy_kernel(ScanArgs
     run_chain<Fused<Out, DK, LP, false, false, float, false, true>>(a, smem);
 }
 
-template <typename Out, int DK, int LP, bool NO_O = false>
-static hipError_t launch_one(const ScanArgs &a, hipStream_t s)
+// Noisy blocks of two 32-position sub-blocks (blocks of 34 to 64 positions, even), with and
+// without the clean outputs.
+template <typename Out, int DK>
+__global__ void __launch_bounds__(768) bdgdn_fwd_pipelined_pair_kernel(ScanArgs a)
 {
-    typedef Fused<Out, DK, LP, false, false, float, false, NO_O> K;
-    auto kern = NO_O ? bdgdn_fwd_pipelined_noisy_kernel<Out, DK, LP> : bdgdn_fwd_pipelined_kernel<Out, DK, LP>;
+    extern __shared__ __align__(16) unsigned char smem[];
+    run_chain<Fused<Out, DK, 32, false, false, float, false, false, true>>(a, smem);
+}
+template <typename Out, int DK>
+__global__ void __launch_bounds__(768) bdgdn_fwd_pipelined_pair_noisy_kernel(ScanArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    run_chain<Fused<Out, DK, 32, false, false, float, false, true, true>>(a, smem);
+}
+
+template <typename K>
+static hipError_t launch_kernel(void (*kern)(ScanArgs), const ScanArgs &a, hipStream_t s)
+{
     static std::once_flag once;
     static hipError_t err = hipSuccess;
     std::call_once(once, [&] {
@@ -35,9 +48,24 @@ static hipError_t launch_one(const ScanArgs &a, hipStream_t s)
                                   K::BYTES);
     });
     if (err != hipSuccess) return err;
-    const int grid = (a.n_chains + 7) / 8 * 8 * a.n_vt;
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(K::kThreads), K::BYTES, s, a);
+    hipLaunchKernelGGL(kern, dim3(chain_grid(a)), dim3(K::kThreads), K::BYTES, s, a);
     return hipGetLastError();
+}
+
+template <typename Out, int DK, int LP, bool NO_O = false>
+static hipError_t launch_one(const ScanArgs &a, hipStream_t s)
+{
+    typedef Fused<Out, DK, LP, false, false, float, false, NO_O> K;
+    return launch_kernel<K>(NO_O ? bdgdn_fwd_pipelined_noisy_kernel<Out, DK, LP> : bdgdn_fwd_pipelined_kernel<Out, DK, LP>,
+                            a, s);
+}
+
+template <typename Out, int DK, bool NO_O = false>
+static hipError_t launch_pair(const ScanArgs &a, hipStream_t s)
+{
+    typedef Fused<Out, DK, 32, false, false, float, false, NO_O, true> K;
+    return launch_kernel<K>(NO_O ? bdgdn_fwd_pipelined_pair_noisy_kernel<Out, DK> : bdgdn_fwd_pipelined_pair_kernel<Out, DK>,
+                            a, s);
 }
 
 // The same forward that also writes the seed state of every (block, v-head) to a.bs (the
@@ -57,8 +85,7 @@ static hipError_t launch_seeds(const ScanArgs &a, hipStream_t s)
     hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                          hipFuncAttributeMaxDynamicSharedMemorySize, K::BYTES);
     if (err != hipSuccess) return err;
-    const int grid = (a.n_chains + 7) / 8 * 8 * a.n_vt;
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(K::kThreads), K::BYTES, s, a);
+    hipLaunchKernelGGL(kern, dim3(chain_grid(a)), dim3(K::kThreads), K::BYTES, s, a);
     return hipGetLastError();
 }
 
@@ -83,6 +110,25 @@ hipError_t launch_fwd_pipelined(Types ty, int dk, int lp, const ScanArgs &a, hip
         BDGDN_CASE(float, 64, 16) BDGDN_CASE(float, 64, 32) BDGDN_CASE(float, 128, 16) BDGDN_CASE(float, 128, 32)
     } else {
         BDGDN_CASE(__bf16, 64, 16) BDGDN_CASE(__bf16, 64, 32) BDGDN_CASE(__bf16, 128, 16) BDGDN_CASE(__bf16, 128, 32)
+    }
+#undef BDGDN_CASE
+    return hipErrorInvalidValue;
+}
+
+bool pair_supported(Types ty, int dk, int L)
+{
+    return ty != Types::F32 && (dk == 64 || dk == 128) && L > 32 && L <= 64 && L % 2 == 0;
+}
+
+hipError_t launch_fwd_pipelined_pair(Types ty, int dk, const ScanArgs &a, hipStream_t s, bool clean_out)
+{
+    if (!pair_supported(ty, dk, 2 * a.L) || a.n_vt * 32 != a.dv) return hipErrorInvalidValue;
+#define BDGDN_CASE(OUT, DK) \
+    if (dk == DK) return clean_out ? launch_pair<OUT, DK>(a, s) : launch_pair<OUT, DK, true>(a, s);
+    if (ty == Types::BF16_IN_F32_OUT) {
+        BDGDN_CASE(float, 64) BDGDN_CASE(float, 128)
+    } else {
+        BDGDN_CASE(__bf16, 64) BDGDN_CASE(__bf16, 128)
     }
 #undef BDGDN_CASE
     return hipErrorInvalidValue;

@@ -101,6 +101,10 @@ hipError_t launch_fwd_scan(Types ty, int dk, int lp, const IntraArgs &ia, const 
 bool pipelined_supported(Types ty, int dk, int lp);
 // clean_out = false: no clean outputs (a further noisy view of the complementary-view forward).
 hipError_t launch_fwd_pipelined(Types ty, int dk, int lp, const ScanArgs &a, hipStream_t s, bool clean_out = true);
+// Blocks of L = 2 a.L positions (L even, 34 .. 64) in the same kernel: the chain runs on
+// sub-blocks of a.L positions and each noisy block spans two of them.
+bool pair_supported(Types ty, int dk, int L);
+hipError_t launch_fwd_pipelined_pair(Types ty, int dk, const ScanArgs &a, hipStream_t s, bool clean_out = true);
 // The same, also writing the seed state of every (block, v-head) to a.bs (d_k = 128).
 hipError_t launch_fwd_pipelined_seeds(Types ty, int lp, const ScanArgs &a, hipStream_t s);
 // The split schedule (clean scan exposing the seed states, then the noisy-block pass):

@@ -88,7 +88,7 @@ static hipError_t launch_split(const ScanArgs &sa, const NoisyArgs &na, hipStrea
                                   K2::BYTES);
     });
     if (err != hipSuccess) return err;
-    const int grid = (sa.n_chains + 7) / 8 * 8 * sa.n_vt;
+    const int grid = chain_grid(sa);
     hipLaunchKernelGGL(k2, dim3(grid), dim3(K2::kThreads), K2::BYTES, s, sa);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -106,7 +106,7 @@ static hipError_t scan_states(int lp, const ScanArgs &sa, hipStream_t s)
         hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void *>(k2),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
         if (err != hipSuccess) return err;
-        const int grid = (sa.n_chains + 7) / 8 * 8 * sa.n_vt;
+        const int grid = chain_grid(sa);
         hipLaunchKernelGGL(k2, dim3(grid), dim3(768), bytes, s, sa);
         return hipGetLastError();
     };

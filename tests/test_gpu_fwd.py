@@ -64,6 +64,24 @@ def test_small_shapes(B, T, hqk, hv, d, L, dtype, route):
     _check_full(inp, L, dtype, h0=h0, route=route)
 
 
+@pytest.mark.parametrize("B,T,hqk,hv,d,L,lengths", [
+    (2, 64 * 3 + 20, 2, 4, 128, 64, None),    # last block: a partial first half, no second half
+    (1, 64 * 2 + 45, 1, 2, 128, 64, None),    # last block: a full first half, a partial second half
+    (1, 64 * 2 + 32, 1, 1, 128, 64, None),    # last block: exactly its first half
+    (1, 200, 2, 2, 64, 64, None),             # d = 64
+    (1, 150, 1, 1, 128, 48, None),            # halves of 24 positions
+    (1, 136, 1, 1, 128, 34, None),            # halves of 17
+    (1, 64 + 128 + 0 + 50, 2, 2, 128, 64, [64, 128, 0, 50]),   # packed: an empty and a partial document
+])
+def test_pair_blocks(B, T, hqk, hv, d, L, lengths):
+    """Blocks of 34 to 64 positions in the one-kernel forward: each noisy block spans two
+    sub-blocks of half the block, its state carried across them, and the first half's rows
+    read the state at the block's end."""
+    inp = W.make_custom_train(B, T, hqk, hv, d, d, "bf16", seed=2000 + T + L, lengths=lengths)
+    h0 = None if lengths else torch.randn(B, hv, d, d, generator=torch.Generator().manual_seed(T + 1)) * 0.3
+    _check_full(inp, L, "bf16", h0=h0)
+
+
 @pytest.mark.parametrize("route", ROUTES)
 def test_packed_documents_small(route):
     lengths = [64, 96, 32, 0, 64, 128, 17]   # an empty doc and a ragged last doc

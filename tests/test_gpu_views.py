@@ -55,6 +55,16 @@ def test_views_match_oracle(B, T, hqk, hv, L, lengths, n_views, route):
             assert rel_err(ht, rht) <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("B,T,hqk,hv,L,lengths,n_views", [
+    (1, 200, 1, 2, 64, None, 2),                 # blocks of 64 (two halves), ragged tail
+    (1, 256, 2, 2, 64, [128, 64, 64], 3),        # packed documents
+])
+def test_views_pair_blocks_match_oracle(B, T, hqk, hv, L, lengths, n_views):
+    """Blocks of more than 32 positions: the fused route runs the one-kernel forward on
+    half-block sub-blocks once per view."""
+    test_views_match_oracle(B, T, hqk, hv, L, lengths, n_views, bd.BDGDN_ROUTE_FUSED)
+
+
 def test_one_view_equals_fused_forward_and_views_equal_split_route():
     """One view is the one-kernel forward; a second view's readout is the split route's noisy
     pass from the same seeds (bit for bit)."""
