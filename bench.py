@@ -140,12 +140,19 @@ class Flusher:
         self.buf.sum()
 
 
-def time_protocol(fn, stream, flush, warmup=5, iters=20, repeats=3, trim=2):
+PROTOCOL = {"iters": 20, "repeats": 3}
+
+
+def time_protocol(fn, stream, flush, warmup=5, iters=None, repeats=None, trim=2):
     """The per-config protocol: `warmup` launches, then `repeats` x `iters` launches, each
     after a scratch flush and bracketed by its own HIP events on the launch stream; the
     `trim` fastest and slowest of each repeat dropped, the rest averaged.  Returns ms
     (mean over repeats) and the per-repeat trimmed means."""
     import torch
+    iters = PROTOCOL["iters"] if iters is None else min(iters, PROTOCOL["iters"])
+    repeats = PROTOCOL["repeats"] if repeats is None else min(repeats, PROTOCOL["repeats"])
+    trim = min(trim, (iters - 1) // 2)
+    warmup = min(warmup, iters)
     for _ in range(warmup):
         flush()
         fn()
@@ -285,7 +292,11 @@ def main():
                          "records attribute its parts to separate kernels)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run only a 256 MiB device copy (byte-counter calibration)")
+    ap.add_argument("--protocol-iters", type=int, default=20,
+                    help="launches per repeat of the per-config protocol (fewer for counter runs)")
+    ap.add_argument("--protocol-repeats", type=int, default=3)
     args = ap.parse_args()
+    PROTOCOL["iters"], PROTOCOL["repeats"] = max(1, args.protocol_iters), max(1, args.protocol_repeats)
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not part of it "
                                    "(--gpus must be 1)", "n_gpus": args.gpus}))
@@ -382,7 +393,8 @@ def main():
         train_config("c1_bf16_out", W.TRAIN_4K, out_dtype=torch.bfloat16,
                      note="bdgdn_fwd_pipelined_kernel, bf16 outputs")
     if "c2" in only:
-        train_config("c2", W.GVA_16K, note="blocks of 64: bdgdn_k1_intra_kernel (UT records) + bdgdn_k2_scan_kernel")
+        train_config("c2", W.GVA_16K, note="bdgdn_fwd_pipelined_pair_kernel (one kernel; each noisy block of 64 "
+                                           "spans two 32-position sub-blocks)")
     if "c4" in only:
         train_config("c4", W.VARLEN_128K, note="bdgdn_fwd_pipelined_kernel (one kernel), longest documents first")
 
