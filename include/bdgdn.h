@@ -211,7 +211,8 @@ int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc,
 /* Bytes of device workspace bdgdn_bwd_train needs, per (block, v-head): the recomputed
  * clean seed state (fp16), the part of the clean state gradient at the block's start that
  * does not depend on the gradient at its end (fp16), the gradient at its end (fp16), the
- * block's U K (32 x d_k fp16) and gamma_n; 0 for a descriptor it would reject. */
+ * block's U K (32 x d_k fp16) and gamma_n; plus 2.3 KB for the range pass; 0 for a
+ * descriptor it would reject. */
 size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
 
 /*
@@ -234,12 +235,13 @@ size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
  * blocks of at most 32 positions (else BDGDN_ERR_UNSUPPORTED).  With grouped value heads
  * (h_v > h_qk) dq, dk, dqn, dkn are summed with floating-point atomics (summation order
  * not fixed); otherwise every result is deterministic.
- * Range: do, don and the state gradients enter the products as fp16 operands, so entries
- * below 2^-14 in magnitude lose relative precision (below ~6e-8 they flush to zero) and
- * entries above 65504 overflow.  Every result is linear in do, don and dht: a caller whose
- * upstream gradients are that small (a loss averaged over many tokens) scales them by a
- * power of two into range and divides the results by it (loss scaling); that changes no
- * rounding except of the entries it moves across 2^-14.
+ * Range: do, don and the state gradients enter the products as fp16 operands.  Every result
+ * is linear in do, don and dht, so the call first finds the largest |entry| of do, don (of
+ * every view) and dht on the device, multiplies them by the power of two sigma that puts it
+ * in [4, 8) as they are converted, and divides every fp32 result by sigma (exact): upstream
+ * gradients of any magnitude (a loss averaged over many tokens, or a large one) keep the
+ * fp16 operands' relative precision, and scaling the upstream gradients by a power of two
+ * scales every result by exactly that factor.  Non-finite upstream gradients give sigma = 1.
  */
 int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc,
                     const void *q, const void *k, const void *v,

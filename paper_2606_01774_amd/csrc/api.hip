@@ -488,20 +488,18 @@ int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc, const void *q, const voi
     return BDGDN_OK;
 }
 
-// Backward workspace: three fp32 states per (block, v-head) -- the clean seed, the gradient
-// of the noisy block's seed, the clean state gradient at the block's end -- then scratch for
-// the clean outputs the recomputing scan writes (bf16).
 static bool bwd_shape_ok(const bdgdn_fwd_desc_t *d)
 {
     return d->dtype == BDGDN_BF16 && d->d_k == 128 && d->d_v == 128 && d->block <= 32;
 }
 
 // Workspace of the backward, per (global block, v-head): the seed state (fp16), the part of
-// the state gradient at the block's start that does not depend on dh (fp32), dh at the
-// block's end (fp16: the clean block kernel uses it as fp16 operands only), U K (32 x d_k, fp16), gamma_n (fp32).  Byte offsets, each aligned to
-// 256.
+// the state gradient at the block's start that does not depend on dh (fp16, tile-native),
+// dh at the block's end (fp16, tile-native: the clean block kernel uses it as fp16 operands
+// only), U K (32 x d_k, fp16), gamma_n (fp32); then the range pass's per-block maxima and
+// {sigma, 1 / sigma}.  Byte offsets, each aligned to 256.
 struct BwdLayout {
-    size_t seeds, cterm, dh, uk, gnb, total;
+    size_t seeds, cterm, dh, uk, gnb, part, range, total;
 };
 static BwdLayout bwd_layout(const bdgdn_fwd_desc_t *d)
 {
@@ -513,7 +511,9 @@ static BwdLayout bwd_layout(const bdgdn_fwd_desc_t *d)
     l.dh = l.cterm + up(units * st * 2);
     l.uk = l.dh + up(units * st * 2);
     l.gnb = l.uk + up(units * 32 * d->d_k * 2);
-    l.total = l.gnb + up(units * 4);
+    l.part = l.gnb + up(units * 4);
+    l.range = l.part + up(kRangeBlocks * 4);
+    l.total = l.range + 256;
     return l;
 }
 
@@ -608,6 +608,24 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     a.scale = desc->scale;
     a.atomic_qk = desc->h_v != desc->h_qk;
     const long rows = (long)desc->batch * desc->seqlen;
+    // the range of the upstream gradients: the power-of-two scale they enter the kernels with
+    RangeArgs ra = {};
+    ra.arr[ra.count] = dout; ra.n[ra.count++] = rows * desc->h_v * desc->d_v;
+    ra.arr[ra.count] = doutn; ra.n[ra.count++] = rows * desc->h_v * desc->d_v;
+    for (int i = 0; i < n_more; ++i) {
+        ra.arr[ra.count] = more[i].dout;
+        ra.n[ra.count++] = rows * desc->h_v * desc->d_v;
+    }
+    if (dht) {
+        ra.arr[ra.count] = dht;
+        ra.n[ra.count++] = (long)nseq * desc->h_v * desc->d_k * desc->d_v;
+        ra.last_f32 = true;
+    }
+    ra.part = reinterpret_cast<float *>(ws + lay.part);
+    ra.range = reinterpret_cast<float *>(ws + lay.range);
+    a.range = ra.range;
+    e = launch_bwd_range(desc->out_dtype == BDGDN_BF16, ra, strm);
+    if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
     e = launch_bwd(desc->out_dtype == BDGDN_BF16, a, more, n_more, nseq * desc->h_v, total_blocks(desc) * desc->h_v,
                    rows * desc->h_qk * desc->d_k, strm);
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;

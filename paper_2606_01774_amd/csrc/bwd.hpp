@@ -28,6 +28,9 @@ struct BwdArgs {
     float *gnb;                              // [global block][h_v]: gamma_n of each clean block
     _Float16 *dh;                            // [global block][h_v][64 tiles][64 lanes][4]: gradient at
                                              // block ends (fp16, tile-native like cterm)
+    const float *range;                      // {sigma, 1 / sigma}: the upstream gradients enter the
+                                             // fp16 operands times sigma, the fp32 results are
+                                             // divided by it (launch_bwd_range writes them)
     const int32_t *cu;                       // packed documents, or null
     int n_docs;
     int n_chains;                            // sequences x v-heads
@@ -44,6 +47,19 @@ struct BwdView {
     const void *dout;
     float *dq, *dk, *dv, *dg, *db;
 };
+// The range pass: max |x| over the upstream gradients (arr[0 .. count-1]: dO, dO~ of each view
+// in the output type, then dht in fp32 when last_f32) into part[kRangeBlocks], reduced to
+// range = {sigma, 1 / sigma}.
+constexpr int kRangeArrays = 19, kRangeBlocks = 512;
+struct RangeArgs {
+    const void *arr[kRangeArrays];
+    long n[kRangeArrays];   // elements of each array (multiples of 128)
+    int count;
+    bool last_f32;
+    float *part;            // [kRangeBlocks]
+    float *range;           // [2]
+};
+hipError_t launch_bwd_range(bool bf16_out, const RangeArgs &r, hipStream_t s);
 size_t bwd_block_lds();
 // The backward of a's two streams, plus n_more further noisy views seeded from the same clean
 // states (their seed gradients summed into the clean state gradient).

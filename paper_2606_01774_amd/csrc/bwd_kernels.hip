@@ -150,11 +150,11 @@ template <> struct Row8<__bf16> {
 #pragma unroll
         for (int j = 0; j < 8; ++j) v[j] = (__bf16)0.f;
     }
-    __device__ __forceinline__ f16x8 h() const
+    __device__ __forceinline__ f16x8 h(float sg = 1.f) const
     {
         f16x8 r;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) r[j] = (_Float16)(float)v[j];
+        for (int j = 0; j < 8; ++j) r[j] = (_Float16)((float)v[j] * sg);
         return r;
     }
 };
@@ -166,13 +166,13 @@ template <> struct Row8<float> {
         hi = ld4(p + 4);
     }
     __device__ __forceinline__ void zero() { lo = hi = f32x4{0.f, 0.f, 0.f, 0.f}; }
-    __device__ __forceinline__ f16x8 h() const
+    __device__ __forceinline__ f16x8 h(float sg = 1.f) const
     {
         f16x8 r;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            r[j] = (_Float16)lo[j];
-            r[4 + j] = (_Float16)hi[j];
+            r[j] = (_Float16)(lo[j] * sg);
+            r[4 + j] = (_Float16)(hi[j] * sg);
         }
         return r;
     }
@@ -187,10 +187,11 @@ template <typename In> __device__ __forceinline__ Row8<In> load_rows(const In *s
         x.zero();
     return x;
 }
-template <typename In> __device__ __forceinline__ void store_rows(_Float16 *dst, const Row8<In> &x, int tid)
+template <typename In> __device__ __forceinline__ void store_rows(_Float16 *dst, const Row8<In> &x, int tid,
+                                                                  float sg = 1.f)
 {
     const int r = tid >> 4, c = (tid & 15) * 8;
-    *reinterpret_cast<f16x8 *>(dst + r * LDH + c) = x.h();
+    *reinterpret_cast<f16x8 *>(dst + r * LDH + c) = x.h(sg);
 }
 
 // The fp16 seed state (128 x 128, 32 KB): four 16-byte pieces per thread.
@@ -316,6 +317,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
 {
     const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
     const float s = a.scale;
+    const float inv = a.range[1];   // every gradient is linear in the scaled upstream gradients
     const long vs = (long)a.h_v * DD;
     const f32x4 z = {0.f, 0.f, 0.f, 0.f};
     // This lane's shares of the gate gradients that are sums over a row of a 32 x 128 product:
@@ -326,7 +328,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
     store_rows(sm.Q, in.q, tid);
     store_rows(sm.K, in.k, tid);
     store_rows(sm.R, in.v, tid);   // V, becomes R below
-    store_rows(sm.dO, in.dout, tid);
+    store_rows(sm.dO, in.dout, tid, a.range[0]);   // upstream gradients times the range scale
     if (tid < NP) {
         sm.bet[tid] = in.b;
         sm.G[tid] = in.g;
@@ -493,7 +495,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int r = 16 * tm + 4 * g4 + j, col = c0 + rr;
-                if (r < nvalid) p.dv[(long)r * vs + col] = c[j];
+                if (r < nvalid) p.dv[(long)r * vs + col] = c[j] * inv;
                 ng[j] = -sm.gam[r] * c[j];
             }
             drq[tm] = h4(ng);
@@ -533,9 +535,9 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
                 if (r < nvalid) {
                     float *dst = p.dq + (long)r * a.h_qk * DD + col;
                     if (a.atomic_qk)
-                        atomicAdd(dst, c[j]);
+                        atomicAdd(dst, c[j] * inv);
                     else
-                        *dst = c[j];
+                        *dst = c[j] * inv;
                 }
             }
         }
@@ -627,9 +629,9 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
                 if (r < nvalid) {
                     float *dst = p.dk + (long)r * a.h_qk * DD + col;
                     if (a.atomic_qk)
-                        atomicAdd(dst, c[j]);
+                        atomicAdd(dst, c[j] * inv);
                     else
-                        *dst = c[j];
+                        *dst = c[j] * inv;
                 }
             }
         }
@@ -658,8 +660,8 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
             if (lane + o < NP) x += y;
         }
         if (lane < nvalid) {
-            p.dg[(long)lane * a.h_v] = x;
-            p.db[(long)lane * a.h_v] = sm.dB[lane];
+            p.dg[(long)lane * a.h_v] = x * inv;
+            p.db[(long)lane * a.h_v] = sm.dB[lane] * inv;
         }
     }
     __syncthreads();
@@ -832,7 +834,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
             load_block<Od, false>(stream_ptrs<Od>(a, false, p0, h, hq), a.h_qk, a.h_v, nvalid, tid);
         store_rows(sm.R, cin.q, tid);
         store_rows(sm.dDl, cin.k, tid);
-        store_rows(sm.dO, cin.dout, tid);
+        store_rows(sm.dO, cin.dout, tid, a.range[0]);
         cg = cin.g;
         cb = cin.b;
     }
@@ -874,7 +876,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
                 if (PREP && more) {
                     store_rows(sm.R, nxt.q, tid);
                     store_rows(sm.dDl, nxt.k, tid);
-                    store_rows(sm.dO, nxt.dout, tid);
+                    store_rows(sm.dO, nxt.dout, tid, a.range[0]);
                     cg = nxt.g;
                     cb = nxt.b;
                 }
@@ -970,13 +972,14 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
     const int rw = (DD / NW) * wave;
     float dh[RT][CT][4];
     const float *dht = a.dht ? a.dht + ((size_t)n * a.h_v + h) * SS : nullptr;
+    const float sg = a.range[0];
 #pragma unroll
     for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
         for (int tn = 0; tn < CT; ++tn)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                dh[tl][tn][j] = dht ? dht[(rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] : 0.f;
+                dh[tl][tn][j] = dht ? dht[(rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] * sg : 0.f;
     // wait for these loads here, once: left pending into the loop, they would make every
     // step wait for all outstanding loads (the prefetch of the next blocks included)
 #pragma unroll
@@ -1091,8 +1094,94 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
             for (int tn = 0; tn < CT; ++tn)
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    d0[(rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] = dh[tl][tn][j];
+                    d0[(rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] = dh[tl][tn][j] * a.range[1];
     }
+}
+
+// The range of the upstream gradients (dO, dO~ of every view, dht): each block's max |x| over
+// its grid-stride share of every array into part[blockIdx.x].  With Od = bf16 the output
+// gradients are bf16 (dht is always fp32).
+template <typename Od>
+__global__ void __launch_bounds__(256) bdgdn_bwd_range_kernel(RangeArgs r)
+{
+    __shared__ float red[4];
+    const long stride = (long)gridDim.x * 256;
+    float m = 0.f;
+    for (int i = 0; i < r.count; ++i) {
+        const long n8 = r.n[i] / 8;   // 8-element vectors (every length is a multiple of 128)
+        if (i == r.count - 1 && r.last_f32) {
+            const f32x4 *x = static_cast<const f32x4 *>(r.arr[i]);
+            for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < 2 * n8; e += stride) {
+                const f32x4 v = x[e];
+                m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+            }
+        } else if constexpr (sizeof(Od) == 2) {
+            const bf16x8 *x = static_cast<const bf16x8 *>(r.arr[i]);
+            for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < n8; e += stride) {
+                const bf16x8 v = x[e];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf((float)v[j]));
+            }
+        } else {
+            const f32x4 *x = static_cast<const f32x4 *>(r.arr[i]);
+            for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < 2 * n8; e += stride) {
+                const f32x4 v = x[e];
+                m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+            }
+        }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) r.part[blockIdx.x] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+// The blocks' maxima reduced to the power-of-two scale sigma that puts the largest upstream
+// gradient in [4, 8), and its inverse: range[0] = sigma, range[1] = 1 / sigma (both 1 when
+// every gradient is zero or one is not finite).  Every gradient is linear in the upstream
+// gradients, so the block kernels work on sigma times them (fp16 operands keep their relative
+// precision whatever the loss scale) and divide their fp32 results by sigma, exactly.
+__global__ void __launch_bounds__(256) bdgdn_bwd_scale_kernel(const float *part, int n, float *range)
+{
+    __shared__ float red[4];
+    float m = 0.f;
+    bool bad = false;
+    for (int i = threadIdx.x; i < n; i += 256) {
+        const float v = part[i];
+        bad |= !isfinite(v);
+        m = fmaxf(m, v);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    const bool any_bad = __syncthreads_or(bad);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+        float sg = 1.f;
+        if (!any_bad && m > 0.f) {
+            int e;
+            frexpf(m, &e);                       // m in [2^(e-1), 2^e)
+            const int k = min(max(3 - e, -120), 120);
+            sg = ldexpf(1.f, k);                 // sigma m in [4, 8)
+        }
+        range[0] = sg;
+        range[1] = 1.f / sg;
+    }
+}
+
+hipError_t launch_bwd_range(bool bf16_out, const RangeArgs &r, hipStream_t s)
+{
+    if (r.count < 1 || r.count > kRangeArrays) return hipErrorInvalidValue;
+    if (bf16_out)
+        hipLaunchKernelGGL(bdgdn_bwd_range_kernel<__bf16>, dim3(kRangeBlocks), dim3(256), 0, s, r);
+    else
+        hipLaunchKernelGGL(bdgdn_bwd_range_kernel<float>, dim3(kRangeBlocks), dim3(256), 0, s, r);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(bdgdn_bwd_scale_kernel, dim3(1), dim3(256), 0, s, r.part, kRangeBlocks, r.range);
+    return hipGetLastError();
 }
 
 __global__ void __launch_bounds__(256) bdgdn_bwd_zero_kernel(float *p, long n)

@@ -180,28 +180,56 @@ def test_bwd_one_view_equals_two_stream_backward():
         assert torch.equal(got_v[0][n], ref[n + "n"]), n
 
 
-@pytest.mark.gpu
 def test_bwd_power_of_two_loss_scaling():
-    """Every gradient is linear in (do, don, dht): scaling them by 2^-4 scales every result
-    by 2^-4, up to the fp16 rounding of the operand entries the scaling moves below 2^-14
-    (measured: up to ~3e-4 of the largest entry, dvn and dh0; 1e-7 for dq; the loss
-    scaling the header recommends for small upstream gradients)."""
+    """Every gradient is linear in (do, don, dht), and the call scales them into the fp16
+    operands' range by a power of two it finds on the device: scaling the upstream gradients
+    by 2^-4 (or 2^7) scales every result by exactly that factor, bit for bit."""
     inp, do, don, h0, dht, cu = _case(2, 80, 1, 1, 32, 8, h0=True, dht=True)
     d = {k: v.cuda() for k, v in inp.items()}
     print("bwd power-of-two loss scaling", flush=True)
-    s = 2.0 ** -4
 
     def run(f):
         return bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
                                   d["betan"], (f * do).cuda(), (f * don).cuda(), block=32, h0=h0.cuda(),
                                   dht=(f * dht).cuda(), want_dh0=True)
 
-    ref, got = run(1.0), run(s)
+    ref = run(1.0)
+    for s in (2.0 ** -4, 2.0 ** 7):
+        got = run(s)
+        torch.cuda.synchronize()
+        for n in NAMES + ("dh0",):
+            assert torch.equal(got[n], ref[n] * s), (s, n)
+
+
+@pytest.mark.parametrize("magnitude", [1e-6, 3e-9, 2e5])
+def test_bwd_upstream_gradient_range(magnitude):
+    """Upstream gradients far from 1 (a loss averaged over many tokens, or a large one),
+    fp32 and bf16, against the oracle at the bf16 tolerance."""
+    for do_dtype in (torch.float32, torch.bfloat16):
+        inp, do, don, h0, dht, cu = _case(1, 96, 1, 2, 32, 11, h0=True, dht=True, do_dtype=do_dtype)
+        do, don = (do.float() * magnitude).to(do_dtype), (don.float() * magnitude).to(do_dtype)
+        dht = dht * magnitude
+        print(f"bwd upstream gradients of magnitude {magnitude} ({do_dtype})", flush=True)
+        d = {k: v.cuda() for k, v in inp.items()}
+        got = bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
+                                 d["betan"], do.cuda(), don.cuda(), block=32, h0=h0.cuda(), dht=dht.cuda(),
+                                 want_dh0=True)
+        torch.cuda.synchronize()
+        ref = oracle.bwd_train(inp["q"], inp["k"], inp["v"], inp["g"], inp["beta"], inp["qn"], inp["kn"],
+                               inp["vn"], inp["gn"], inp["betan"], do.float(), don.float(), block=32,
+                               scale=1.0 / math.sqrt(128), h0=h0, dht=dht)
+        for name in NAMES + ("dh0",):
+            e = rel_err(got[name], ref[name])
+            assert e <= TOL["bf16"], (magnitude, do_dtype, name, e)
+
+
+def test_bwd_zero_upstream_gradients():
+    """All-zero upstream gradients give all-zero gradients (the range pass keeps its scale at 1)."""
+    inp, do, don, h0, dht, cu = _case(1, 64, 1, 1, 32, 12, h0=True)
+    d = {k: v.cuda() for k, v in inp.items()}
+    got = bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
+                             d["betan"], torch.zeros_like(do).cuda(), torch.zeros_like(don).cuda(), block=32,
+                             h0=h0.cuda(), want_dh0=True)
     torch.cuda.synchronize()
-    errs = {}
-    for n in NAMES + ("dh0",):
-        r, g = ref[n].float(), got[n].float() / s
-        errs[n] = float((g - r).abs().max() / r.abs().max())
-    print("  " + " ".join(f"{k} {v:.1e}" for k, v in errs.items()), flush=True)
-    for n, e in errs.items():
-        assert e <= 1e-3, f"{n}: {e:.3e}"
+    for name in NAMES + ("dh0",):
+        assert not got[name].any(), name
