@@ -93,17 +93,20 @@ def test_workspace_query():
     rec = _desc(route=bd.BDGDN_ROUTE_RECORDS)
     ws = bd.bdgdn_fwd_train_workspace(rec)
     assert ws > 0 and ws % (2 * 4) == 0 and (ws // 8) % 256 == 0
-    # FUSED runs as one kernel without a workspace for bf16 inputs and blocks up to 32 ...
+    # FUSED runs as one kernel without a workspace for bf16 inputs with blocks up to 32,
+    # and with even blocks of 34 .. 64 (two half-block sub-blocks) ...
     assert bd.bdgdn_fwd_train_workspace(_desc()) == 0
     assert bd.bdgdn_fwd_train_workspace(_desc(block=16, d_k=64, d_v=64)) == 0
-    # ... and through the records otherwise (64-position blocks, fp32 inputs)
-    assert bd.bdgdn_fwd_train_workspace(_desc(block=64)) > 0
+    assert bd.bdgdn_fwd_train_workspace(_desc(block=64)) == 0
+    assert bd.bdgdn_fwd_train_workspace(_desc(block=40)) == 0
+    # ... and through the records otherwise (odd blocks above 32, fp32 inputs)
+    assert bd.bdgdn_fwd_train_workspace(_desc(block=63)) > 0
     assert bd.bdgdn_fwd_train_workspace(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32)) > 0
     assert bd.bdgdn_fwd_train_workspace(_desc(route=bd.BDGDN_ROUTE_ONEPASS)) == 0
     assert bd.bdgdn_fwd_train_workspace(_desc(h_v=3)) == 0
     # too small a workspace is refused before any launch
     assert _fwd(rec) == bd.BDGDN_ERR_WORKSPACE
-    assert _fwd(_desc(block=64)) == bd.BDGDN_ERR_WORKSPACE
+    assert _fwd(_desc(block=63)) == bd.BDGDN_ERR_WORKSPACE
 
 
 def test_split_route_limits_and_workspace():
@@ -330,7 +333,7 @@ def test_views_validation():
     views[1] = bd.NoisyView(0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000)
     assert call(split, 2) == bd.BDGDN_ERR_WORKSPACE
     assert call(_desc(route=bd.BDGDN_ROUTE_RECORDS), 2) == bd.BDGDN_ERR_UNSUPPORTED
-    assert call(_desc(block=64), 1) == bd.BDGDN_ERR_UNSUPPORTED
+    assert call(_desc(block=63), 1) == bd.BDGDN_ERR_UNSUPPORTED   # odd blocks above 32: records only
 
 
 def test_bwd_views_validation():
