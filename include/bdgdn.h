@@ -98,12 +98,24 @@ typedef enum { BDGDN_BF16 = 0, BDGDN_F32 = 1 } bdgdn_dtype_t;
  *           transform of each block itself, without overlap.  No workspace.
  *  RECORDS: two kernels: the UT transform and masked Q K^T of every (block, v-head)
  *           in parallel into the workspace, then the scan of FUSED reading them.
- *           Needs a workspace (bdgdn_fwd_train_workspace). */
+ *           Needs a workspace (bdgdn_fwd_train_workspace).
+ *  CHUNKED: the chunk-parallel schedule (Appendix "Route II" with the chunk-state pass
+ *           of eq. chunk-state): every (sequence or document, v-head) chain is cut into
+ *           segments of G blocks, G a power of two >= 16 chosen from the descriptor so
+ *           that the (chain, segment) pairs cover the GPU's compute units; a state pass
+ *           computes the clean state at every later segment start (with the blocks'
+ *           clean UT transforms computed in parallel before it), then one workgroup per
+ *           (chain, segment) evaluates the segment's blocks for all d_v columns at once.
+ *           Needs a workspace (bdgdn_fwd_train_workspace): a clean UT record per
+ *           (block, v-head) and an fp32 state per (later segment start, v-head).  bf16
+ *           inputs, d_k = d_v in {64, 128}, blocks of at most 32 positions, at most 512
+ *           packed documents (else BDGDN_ERR_UNSUPPORTED). */
 typedef enum {
     BDGDN_ROUTE_FUSED = 0,
     BDGDN_ROUTE_SPLIT = 1,
     BDGDN_ROUTE_ONEPASS = 2,
-    BDGDN_ROUTE_RECORDS = 3
+    BDGDN_ROUTE_RECORDS = 3,
+    BDGDN_ROUTE_CHUNKED = 4
 } bdgdn_route_t;
 
 typedef struct {

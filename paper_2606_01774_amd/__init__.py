@@ -20,7 +20,7 @@ import torch
 
 __all__ = [
     "BdgdnError", "BDGDN_BF16", "BDGDN_F32", "BDGDN_ROUTE_FUSED", "BDGDN_ROUTE_SPLIT",
-    "BDGDN_ROUTE_ONEPASS", "BDGDN_ROUTE_RECORDS",
+    "BDGDN_ROUTE_ONEPASS", "BDGDN_ROUTE_RECORDS", "BDGDN_ROUTE_CHUNKED",
     "bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace", "bdgdn_fwd_train",
     "bdgdn_commit_record", "bdgdn_accept_states", "BDGDN_ACT_NONE", "BDGDN_ACT_SILU",
     "bdgdn_shortconv_fwd", "bdgdn_shortconv_bwd_workspace", "bdgdn_shortconv_bwd",
@@ -45,6 +45,7 @@ BDGDN_ROUTE_FUSED = 0
 BDGDN_ROUTE_SPLIT = 1
 BDGDN_ROUTE_ONEPASS = 2
 BDGDN_ROUTE_RECORDS = 3
+BDGDN_ROUTE_CHUNKED = 4
 BDGDN_ACT_NONE = 0
 BDGDN_ACT_SILU = 1
 

@@ -52,7 +52,7 @@ int check_fwd(const bdgdn_fwd_desc_t *d, const int32_t *cu_dev, const int32_t *c
     if (st != BDGDN_OK) return st;
     if (d->batch <= 0 || d->seqlen < 0 || d->num_seqs < 0) return BDGDN_ERR_INVALID_ARG;
     if (d->route != BDGDN_ROUTE_FUSED && d->route != BDGDN_ROUTE_SPLIT && d->route != BDGDN_ROUTE_ONEPASS &&
-        d->route != BDGDN_ROUTE_RECORDS)
+        d->route != BDGDN_ROUTE_RECORDS && d->route != BDGDN_ROUTE_CHUNKED)
         return BDGDN_ERR_INVALID_ARG;
     if ((long)d->batch * d->seqlen > 0x7fffffffL) return BDGDN_ERR_UNSUPPORTED;
     const bool packed = d->num_seqs > 0;
@@ -69,6 +69,12 @@ int check_fwd(const bdgdn_fwd_desc_t *d, const int32_t *cu_dev, const int32_t *c
         Types ty;
         types_of(d->dtype, d->out_dtype, ty);
         if (!split_supported(ty, d->d_k, d->d_v, lp_of(d->block))) return BDGDN_ERR_UNSUPPORTED;
+    }
+    if (d->route == BDGDN_ROUTE_CHUNKED) {
+        Types ty;
+        types_of(d->dtype, d->out_dtype, ty);
+        if (!chunked_supported(ty, d->d_k, d->d_v, lp_of(d->block)) || d->num_seqs > kMaxOrder)
+            return BDGDN_ERR_UNSUPPORTED;
     }
     return BDGDN_OK;
 }
@@ -163,10 +169,42 @@ static hipError_t launch_one_kernel(const bdgdn_fwd_desc_t *d, Types ty, ScanArg
     return launch_fwd_pipelined_pair(ty, d->d_k, sa, s, clean_out);
 }
 
+// The chunk-parallel schedule cuts every chain into segments of G blocks: the largest
+// power of two (at least 16) that still gives every compute unit of the GPU a (chain,
+// segment) of its own; with more chains than compute units a chain is one segment.
+constexpr int kComputeUnits = 256;
+static int chunk_segment(const bdgdn_fwd_desc_t *d)
+{
+    const long work = total_blocks(d) * d->h_v;   // (block, v-head) pairs
+    long G = 16;
+    while (G * 2 * kComputeUnits <= work && G < (1 << 20)) G *= 2;
+    return (int)G;
+}
+// Workspace of the chunk-parallel schedule: a clean UT record per (block, v-head) and a
+// state per (segment start after the first, v-head), both bounded by the descriptor alone
+// (a chain of nb blocks has ceil(nb / G) - 1 <= nb / G later segment starts).
+struct ChunkLayout {
+    size_t rec, ckpt, total;
+};
+static ChunkLayout chunk_layout(const bdgdn_fwd_desc_t *d)
+{
+    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    const size_t blocks = (size_t)total_blocks(d);
+    ChunkLayout l;
+    l.rec = 0;
+    l.ckpt = up(blocks * d->h_v * chunk_rec_bytes(lp_of(d->block)));
+    l.total = l.ckpt + up((blocks / chunk_segment(d)) * d->h_v * (size_t)d->d_k * d->d_v * 4);
+    return l;
+}
+
 static size_t workspace_bytes_of(const bdgdn_fwd_desc_t *d)
 {
     Types ty;
     types_of(d->dtype, d->out_dtype, ty);
+    if (d->route == BDGDN_ROUTE_CHUNKED) {
+        if (!chunked_supported(ty, d->d_k, d->d_v, lp_of(d->block))) return 0;
+        return chunk_layout(d).total;
+    }
     if (d->route == BDGDN_ROUTE_SPLIT) {
         if (!split_supported(ty, d->d_k, d->d_v, lp_of(d->block))) return 0;
         return (size_t)total_blocks(d) * d->h_v * d->d_k * d->d_v * sizeof(float);   // seed states
@@ -224,6 +262,51 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         n_order = nseq;
     }
     hipError_t e;
+    if (desc->route == BDGDN_ROUTE_CHUNKED) {
+        ChunkArgs ca = {};
+        ca.q = q; ca.k = k; ca.v = v; ca.qn = qn; ca.kn = kn; ca.vn = vn;
+        ca.g = g; ca.beta = beta; ca.gn = gn; ca.betan = betan;
+        ca.cu = packed ? cu_seqlens_dev : nullptr;
+        ca.h0 = h0; ca.ht = ht; ca.o = o; ca.on = on;
+        const ChunkLayout lay = chunk_layout(desc);
+        ca.rec = static_cast<unsigned char *>(workspace) + lay.rec;
+        ca.ckpt = reinterpret_cast<float *>(static_cast<unsigned char *>(workspace) + lay.ckpt);
+        ca.T = desc->seqlen; ca.L = desc->block; ca.nblk = (desc->seqlen + desc->block - 1) / desc->block;
+        ca.h_qk = desc->h_qk; ca.h_v = desc->h_v; ca.dv = desc->d_v;
+        const int G = chunk_segment(desc);
+        ca.G = G;
+        auto nseg = [&](long len) {   // an empty document is one segment without blocks (it writes ht)
+            const long nb = (len + desc->block - 1) / desc->block;
+            return nb <= 0 ? 1 : (int)((nb + G - 1) / G);
+        };
+        long segs = 0;
+        int n1 = 0, max_seg = 1;
+        if (packed) {
+            for (int i = 0; i < nseq; ++i) {
+                const int doc = order[i];
+                const int ns = nseg(cu_seqlens_host[doc + 1] - cu_seqlens_host[doc]);
+                if (segs >= (1L << 21)) return BDGDN_ERR_UNSUPPORTED;
+                ca.order[i] = doc | (int)(segs << 10);
+                segs += ns;
+                if (ns >= 2) ++n1;
+                max_seg = std::max(max_seg, ns);
+            }
+            ca.n_order = nseq;
+        } else {
+            const int ns = nseg(desc->seqlen);
+            segs = (long)ns * nseq;
+            n1 = ns >= 2 ? nseq : 0;
+            max_seg = ns;
+            ca.n_order = 0;
+        }
+        ca.n1 = n1;
+        ca.J_max = (max_seg - 1) * G;
+        ca.n_units = (int)(segs * desc->h_v);
+        ca.n_vt = desc->d_v / 32;
+        ca.scale = desc->scale;
+        e = launch_fwd_chunked(ty, desc->d_k, lp, ca, strm);
+        return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+    }
     if (desc->route != BDGDN_ROUTE_ONEPASS) {
         IntraArgs ia;
         ia.q = q; ia.k = k; ia.qn = qn; ia.kn = kn;

@@ -50,6 +50,31 @@ struct ScanArgs {
     int order[kMaxOrder];
 };
 
+// The chunk-parallel forward (chunked.hpp): a clean UT-record kernel and a state pass
+// over the blocks before each chain's last segment, then one workgroup per (chain,
+// segment) for the outputs.  Chains are (sequence or document, v-head); a chain of nb
+// blocks has nseg = ceil(nb / G) segments of G blocks.
+struct ChunkArgs {
+    const void *q, *k, *v, *qn, *kn, *vn;
+    const float *g, *beta, *gn, *betan;
+    const int32_t *cu;      // packed documents (device), or null
+    const float *h0;
+    float *ht;
+    void *o, *on;
+    unsigned char *rec;     // clean UT records of the state pass
+    float *ckpt;            // clean state at every segment start after the first
+    int T, L, nblk, h_qk, h_v, dv;
+    int G;                  // blocks per segment
+    int n1;                 // chains' sequences / documents with two or more segments (the
+                            // first n1 in processing order)
+    int J_max;              // blocks of the longest state pass: (max nseg - 1) * G
+    int n_units;            // workgroups of the out kernel
+    int n_vt;               // 32-column tiles of the state pass
+    float scale;
+    int n_order;            // packed: documents listed in order[]
+    int order[kMaxOrder];   // packed, longest first: doc | (segments of the documents before it) << 10
+};
+
 // Noisy-block pass of the split schedule (one workgroup per (global block, v-head)).
 struct NoisyArgs {
     const void *qn, *kn, *vn;
@@ -124,6 +149,11 @@ bool fwd_supported(Types ty, int dk, int lp);
 // the noisy-block pass from the seeds.
 hipError_t launch_scan_states(int lp, bool f32_out, bool f16_seeds, const ScanArgs &sa, hipStream_t s);
 hipError_t launch_noisy_blocks(int lp, bool f32_out, const NoisyArgs &na, hipStream_t s);
+
+// The chunk-parallel forward: bf16 inputs, d_k = d_v in {64, 128}, blocks of at most 32.
+bool chunked_supported(Types ty, int dk, int dv, int lp);
+hipError_t launch_fwd_chunked(Types ty, int dk, int lp, const ChunkArgs &a, hipStream_t s);
+size_t chunk_rec_bytes(int lp);
 
 // The two-stream ShortConv (conv_kernels.hip).  x, xn, y, yn, dy, dyn are [rows][D] of the
 // conv dtype; w [D][W] and bias [D] fp32; part [row groups][W + 1][D] fp32 partials of the

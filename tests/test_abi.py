@@ -109,6 +109,26 @@ def test_workspace_query():
     assert _fwd(_desc(block=63)) == bd.BDGDN_ERR_WORKSPACE
 
 
+def test_chunked_route_limits_and_workspace():
+    """The chunk-parallel schedule: bf16 inputs, d_k = d_v, blocks of at most 32; its
+    workspace holds a clean UT record per (block, v-head) and a state per later segment
+    start (segments of at least 16 blocks)."""
+    ch = dict(route=bd.BDGDN_ROUTE_CHUNKED)
+    for kw in (dict(d_k=64, d_v=128), dict(block=64), dict(block=33),
+               dict(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32)):
+        assert _fwd(_desc(**ch, **kw)) == bd.BDGDN_ERR_UNSUPPORTED, kw
+        assert bd.bdgdn_fwd_train_workspace(_desc(**ch, **kw)) == 0
+    # 64 tokens in blocks of 32: 2 blocks x 4 v-heads of 2304-byte records, no later segment
+    assert bd.bdgdn_fwd_train_workspace(_desc(**ch)) == 2 * 4 * 2304
+    # 4 x 4096 tokens, 16 heads: 512 blocks, segments of 32 -> 16 later-start states per head
+    big = _desc(**ch, batch=4, seqlen=4096, h_qk=16, h_v=16)
+    assert bd.bdgdn_fwd_train_workspace(big) == 512 * 16 * 2304 + 16 * 16 * 128 * 128 * 4
+    assert _fwd(_desc(**ch)) == bd.BDGDN_ERR_WORKSPACE
+    # more packed documents than the schedule orders
+    cu = (ctypes.c_int32 * 514)(*[32 * i for i in range(514)])
+    assert _fwd(_desc(**ch, seqlen=32 * 513, num_seqs=513), cu, cu) == bd.BDGDN_ERR_UNSUPPORTED
+
+
 def test_split_route_limits_and_workspace():
     """The split schedule runs bf16 inputs with d_k = d_v = 128 and blocks up to 32; its
     workspace holds one fp32 seed state per (block, v-head)."""

@@ -128,6 +128,28 @@ def test_split_route(B, T, hqk, hv, L, lengths):
     assert e <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("B,T,hqk,hv,d,L,lengths", [
+    (2, 1100, 2, 2, 128, 32, None),     # 35 blocks: three segments of 16, a ragged tail
+    (1, 600, 2, 4, 128, 16, None),      # grouped value heads, L = 16: 38 blocks
+    (1, 300, 1, 2, 64, 5, None),        # d = 64, L = 5 (padded to 16): 60 blocks, 4 segments
+    (1, 520, 1, 1, 128, 32, None),      # 17 blocks: a last segment of one partial block
+    (1, 1024 + 64 + 544 + 640 + 17, 2, 2, 128, 32, [1024, 64, 0, 544, 640, 17]),   # packed
+])
+def test_chunked_route(B, T, hqk, hv, d, L, lengths):
+    """The chunk-parallel schedule (state pass over the segment starts, then one workgroup
+    per (chain, segment)) against the oracle, and bit for bit against the fused schedule:
+    it carries out the same block arithmetic, the state of each segment start coming from
+    the state pass instead of the previous segment."""
+    inp = W.make_custom_train(B, T, hqk, hv, d, d, "bf16", seed=3000 + T + L, lengths=lengths)
+    h0 = None if lengths else torch.randn(B, hv, d, d, generator=torch.Generator().manual_seed(T + 7)) * 0.3
+    o, on, ht = _check_full(inp, L, "bf16", h0=h0, route=bd.BDGDN_ROUTE_CHUNKED)
+    dd = to_dev(inp)
+    if lengths:
+        dd["cu_host"] = inp["cu_seqlens"]
+    fo, fon, fht = _run_gpu(dd, L, 1.0 / math.sqrt(d), h0=None if h0 is None else h0.cuda())
+    assert torch.equal(o, fo) and torch.equal(on, fon) and torch.equal(ht, fht)
+
+
 def test_packed_equals_separate_bitwise():
     """Packing reproduces per-document results exactly (Appendix, packing contract)."""
     lengths = [96, 64, 40]
@@ -167,7 +189,7 @@ def test_determinism_and_isolation():
     assert not torch.equal(on3[:, mask], on1[:, mask])
 
 
-def _full_size(w):
+def _full_size(w, route=bd.BDGDN_ROUTE_FUSED):
     """The whole workload on the GPU in the benchmark's launch configuration, every
     (sequence or document, v-head) unit compared with one multi-threaded oracle call:
     the worst per-unit max |err| / RMS of o, on and ht must meet the tolerance."""
@@ -177,8 +199,8 @@ def _full_size(w):
     if cu is not None:
         d["cu_host"] = cu
     scale = 1.0 / math.sqrt(w.d_k)
-    print(f"{w.name}: GPU", flush=True)
-    o, on, ht = _run_gpu(d, w.block, scale)
+    print(f"{w.name}: GPU (route {route})", flush=True)
+    o, on, ht = _run_gpu(d, w.block, scale, route=route)
     assert torch.isfinite(o.float()).all() and torch.isfinite(on.float()).all()
     o, on, ht = o.cpu(), on.cpu(), ht.cpu()
     del d
@@ -198,6 +220,14 @@ def _full_size(w):
 
 def test_full_train_4k_all_units():
     _full_size(W.TRAIN_4K)
+
+
+def test_full_train_4k_all_units_chunked():
+    _full_size(W.TRAIN_4K, route=bd.BDGDN_ROUTE_CHUNKED)
+
+
+def test_full_varlen_128k_all_units_chunked():
+    _full_size(W.VARLEN_128K, route=bd.BDGDN_ROUTE_CHUNKED)
 
 
 def test_full_gva_16k_all_units():
