@@ -84,9 +84,12 @@ typedef enum { BDGDN_BF16 = 0, BDGDN_F32 = 1 } bdgdn_dtype_t;
  *           on chip and evaluates each noisy block from the in-register boundary state.
  *           With bf16 inputs and blocks of at most 32 positions this is one kernel whose
  *           workgroups also compute each block's UT transform and masked Q K^T a block
- *           ahead (no workspace); blocks of an even 34 .. 64 positions run the same kernel
- *           on sub-blocks of half the block, each noisy block carrying its state across
- *           its two halves (no workspace); otherwise it is the RECORDS schedule.
+ *           ahead (no workspace); when (sequences or documents) x v-heads reach the
+ *           GPU's 256 compute units and d_k = d_v, one workgroup per (sequence, v-head)
+ *           covers all d_v columns instead (CHUNKED's output pass with one segment per
+ *           chain; no workspace).  Blocks of an even 34 .. 64 positions run the one
+ *           kernel on sub-blocks of half the block, each noisy block carrying its state
+ *           across its two halves (no workspace); otherwise it is the RECORDS schedule.
  *  SPLIT:   boundary states through HBM and a separate noisy-block kernel (Appendix
  *           "Route I"): the clean scan writes the clean state before every block (the
  *           seed of that noisy block) into the workspace, fp32 [block][h_v][d_k][d_v]

@@ -169,16 +169,38 @@ static hipError_t launch_one_kernel(const bdgdn_fwd_desc_t *d, Types ty, ScanArg
     return launch_fwd_pipelined_pair(ty, d->d_k, sa, s, clean_out);
 }
 
-// The chunk-parallel schedule cuts every chain into segments of G blocks: the largest
-// power of two (at least 16) that still gives every compute unit of the GPU a (chain,
-// segment) of its own; with more chains than compute units a chain is one segment.
+// The chunk-parallel schedule's plan: each chain (sequence or document, v-head) is cut
+// into d_v tiles (one, or 32-column tiles when there are fewer chains than compute units)
+// and into segments of G blocks, G the largest power of two (at least 16) that still
+// gives every compute unit of the GPU a (chain, tile, segment) of its own; with enough
+// chains and tiles a chain is one segment and there is no state pass.
 constexpr int kComputeUnits = 256;
-static int chunk_segment(const bdgdn_fwd_desc_t *d)
+struct ChunkPlan {
+    int tiles, G;
+};
+static ChunkPlan chunk_plan(const bdgdn_fwd_desc_t *d)
 {
-    const long work = total_blocks(d) * d->h_v;   // (block, v-head) pairs
+    const long chains = (long)(d->num_seqs > 0 ? d->num_seqs : d->batch) * d->h_v;
+    ChunkPlan p;
+    p.tiles = chains >= kComputeUnits ? 1 : d->d_v / 32;
+    const long work = total_blocks(d) * d->h_v * p.tiles;   // (block, v-head, tile) triples
+    const long nblk = (d->seqlen + d->block - 1) / d->block;
     long G = 16;
-    while (G * 2 * kComputeUnits <= work && G < (1 << 20)) G *= 2;
-    return (int)G;
+    while (G * 2 * kComputeUnits <= work && G < nblk) G *= 2;
+    p.G = (int)G;
+    return p;
+}
+static int chunk_segment(const bdgdn_fwd_desc_t *d) { return chunk_plan(d).G; }
+
+// The fused route with at least as many chains as compute units: one workgroup per chain
+// covering all d_v columns (the chunk-parallel schedule's output pass with one segment per
+// chain, so no state pass and no workspace) instead of one per (chain, 32-column tile),
+// which would repeat the d_v-independent work of every block once per tile.
+static bool fused_uses_wide_pass(const bdgdn_fwd_desc_t *d, Types ty)
+{
+    const long chains = (long)(d->num_seqs > 0 ? d->num_seqs : d->batch) * d->h_v;
+    return chunked_supported(ty, d->d_k, d->d_v, lp_of(d->block)) && d->num_seqs <= kMaxOrder &&
+           chains >= kComputeUnits;
 }
 // Workspace of the chunk-parallel schedule: a clean UT record per (block, v-head) and a
 // state per (segment start after the first, v-head), both bounded by the descriptor alone
@@ -203,6 +225,8 @@ static size_t workspace_bytes_of(const bdgdn_fwd_desc_t *d)
     types_of(d->dtype, d->out_dtype, ty);
     if (d->route == BDGDN_ROUTE_CHUNKED) {
         if (!chunked_supported(ty, d->d_k, d->d_v, lp_of(d->block))) return 0;
+        // every chain (at most nblk blocks) one segment: no state pass, no workspace
+        if (chunk_segment(d) >= (d->seqlen + d->block - 1) / d->block) return 0;
         return chunk_layout(d).total;
     }
     if (d->route == BDGDN_ROUTE_SPLIT) {
@@ -262,7 +286,8 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         n_order = nseq;
     }
     hipError_t e;
-    if (desc->route == BDGDN_ROUTE_CHUNKED) {
+    const bool wide = desc->route == BDGDN_ROUTE_FUSED && fused_uses_wide_pass(desc, ty);
+    if (desc->route == BDGDN_ROUTE_CHUNKED || wide) {
         ChunkArgs ca = {};
         ca.q = q; ca.k = k; ca.v = v; ca.qn = qn; ca.kn = kn; ca.vn = vn;
         ca.g = g; ca.beta = beta; ca.gn = gn; ca.betan = betan;
@@ -273,8 +298,11 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         ca.ckpt = reinterpret_cast<float *>(static_cast<unsigned char *>(workspace) + lay.ckpt);
         ca.T = desc->seqlen; ca.L = desc->block; ca.nblk = (desc->seqlen + desc->block - 1) / desc->block;
         ca.h_qk = desc->h_qk; ca.h_v = desc->h_v; ca.dv = desc->d_v;
-        const int G = chunk_segment(desc);
+        // the fused route's wide pass: every chain one segment, all d_v columns together
+        const ChunkPlan plan = wide ? ChunkPlan{1, std::max(16, ca.nblk)} : chunk_plan(desc);
+        const int G = plan.G;
         ca.G = G;
+        ca.n_ot = plan.tiles;
         auto nseg = [&](long len) {   // an empty document is one segment without blocks (it writes ht)
             const long nb = (len + desc->block - 1) / desc->block;
             return nb <= 0 ? 1 : (int)((nb + G - 1) / G);
@@ -301,7 +329,7 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         }
         ca.n1 = n1;
         ca.J_max = (max_seg - 1) * G;
-        ca.n_units = (int)(segs * desc->h_v);
+        ca.n_groups = (int)(segs * desc->h_qk);
         ca.n_vt = desc->d_v / 32;
         ca.scale = desc->scale;
         e = launch_fwd_chunked(ty, desc->d_k, lp, ca, strm);

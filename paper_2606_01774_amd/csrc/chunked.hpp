@@ -50,10 +50,10 @@ __device__ __forceinline__ u32x4 bload(__amdgpu_buffer_rsrc_t r, unsigned off)
 }
 __device__ __forceinline__ f32x4 ld4f(const float *p) { return *reinterpret_cast<const f32x4 *>(p); }
 
-// Byte layout of one clean UT record of the state pass: T (fp16, LP x LP row-major), eG,
-// dG (fp32, LP each).
+// Byte layout of one clean record of the state pass: T and N = K_(j+1) K_j^T (fp16, LP x LP
+// row-major each; N is zero for the chain's last scanned block), eG, dG (fp32, LP each).
 template <int LP> struct CRec {
-    static constexpr int OFF_T = 0, OFF_EG = LP * LP * 2, OFF_DG = OFF_EG + LP * 4;
+    static constexpr int OFF_T = 0, OFF_N = LP * LP * 2, OFF_EG = 2 * LP * LP * 2, OFF_DG = OFF_EG + LP * 4;
     static constexpr int BYTES = al256(OFF_DG + LP * 4);
 };
 
@@ -105,6 +105,12 @@ __device__ __forceinline__ long rec_index(const ChunkArgs &a, int pos, int h, in
 {
     return ckpt_base(a, pos, h, nseg) * a.G + j;
 }
+
+// Workgroup ids are dealt to the GPU's eight XCDs in turn, each with its own L2.  The state
+// pass's chains are padded to a multiple of 8 and laid out so that every workgroup of chain
+// c (its record groups, its d_v tiles) has an id congruent to c mod 8: a chain's key rows
+// and records are read through one L2.
+__device__ __forceinline__ int chains_padded(const ChunkArgs &a) { return (a.n1 * a.h_v + 7) & ~7; }
 
 // Element offset of (row, k) in a swizzled [rows][DK] fp16 matrix: chunk k/8 of a row is
 // stored at chunk (k/8) ^ (row / RPB mod CPR).
@@ -171,31 +177,61 @@ __device__ __forceinline__ void store_out(Out *dst, int stride, int nvalid, int 
 }
 
 // ====================================================================== rec
-// One wave per (state-pass chain, block): the clean record of the block.
+// One workgroup per (state-pass chain, group of four blocks): the key rows of the four
+// blocks and of the block after them are staged once (fp16, swizzled), then wave w writes
+// the record of block j0 + w: its gate factors, T and N = K_(j+1) K_j^T.
 template <int DK, int LP>
 struct RecKernel {
     static constexpr int NB = LP / 16, DKB = DK / 16;
     typedef CRec<LP> R;
-    static constexpr int kWaves = 4;
-    static constexpr int BYTES = kWaves * 2 * 64 * 4;   // per wave: cumulative gates, beta
+    typedef Swz<DK> SW;
+    static constexpr int kWaves = 4, kThreads = 64 * kWaves;
+    static constexpr int NR = (kWaves + 1) * LP;             // staged rows
+    static constexpr int ROWS_B = NR * DK * 2;
+    static constexpr int OFF_G = ROWS_B;                      // per wave: cumulative gates, beta
+    static constexpr int BYTES = OFF_G + kWaves * 2 * 64 * 4;
+    static constexpr int CH = NR * DK / 8;                    // 16-byte chunks of the rows
+    static constexpr int PER = (CH + kThreads - 1) / kThreads;
 
     __device__ static void run(const ChunkArgs &a, unsigned char *smem)
     {
-        const int lane = threadIdx.x & 63, wave = wave_id();
-        const long unit = (long)blockIdx.x * kWaves + wave;
-        const int c = (int)(unit / a.J_max), j = (int)(unit % a.J_max);
+        const int lane = threadIdx.x & 63, wave = wave_id(), tid = threadIdx.x;
+        const int np = chains_padded(a);
+        const int c = blockIdx.x % np, j0 = (blockIdx.x / np) * kWaves;
         if (c >= a.n1 * a.h_v) return;
         const int pos = c / a.h_v, h = c % a.h_v;
         const Geo geo = geo_of(a, pos);
-        if (j >= (geo.nseg - 1) * a.G) return;
+        const int J = (geo.nseg - 1) * a.G;   // blocks scanned by the state pass (all full)
+        if (j0 >= J) return;
         const int hq = h / (a.h_v / a.h_qk);
-        const long r0 = geo.base + (long)j * a.L;
-        const long rem = geo.len - (long)j * a.L;
-        const int nvalid = rem < a.L ? (int)rem : a.L;
-        float *Gs = reinterpret_cast<float *>(smem) + wave * 128, *Bs = Gs + 64;
+        const int qks = a.h_qk * DK;
+        // rows j0 L .. (j0 + 5) L - 1 of the chain, those of blocks < J only
+        const int nrows = (J - j0 >= kWaves + 1 ? kWaves + 1 : J - j0) * a.L;
+        const In *kp = static_cast<const In *>(a.k) + ((geo.base + (long)j0 * a.L) * a.h_qk + hq) * DK;
+        const __amdgpu_buffer_rsrc_t rk = rsrc(kp, (unsigned)(nrows * qks * 2));
+        E *Ks = reinterpret_cast<E *>(smem);
+        u32x4 f[PER];
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int ch = tid + kThreads * u, t = ch / (DK / 8), cc = ch % (DK / 8);
+            // rows of the LP-padded blocks: row t of the staging is position t % LP of block t / LP
+            const int gr = (t / LP) * a.L + (t % LP);
+            const bool ok = ch < CH && (t % LP) < a.L;
+            f[u] = bload(rk, ok ? (unsigned)(gr * qks * 2 + cc * 16) : 0x80000000u);
+        }
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int ch = tid + kThreads * u, t = ch / (DK / 8), cc = ch % (DK / 8);
+            if (ch < CH) *reinterpret_cast<u32x4 *>(Ks + SW::rofs(t, 8 * cc)) = to_operand<In, E>(f[u]);
+        }
+        __syncthreads();
+        const int j = j0 + wave;
+        if (j >= J) return;
+        float *Gs = reinterpret_cast<float *>(smem + OFF_G) + wave * 128, *Bs = Gs + 64;
         unsigned char *rec = a.rec + rec_index(a, pos, h, geo.nseg, j) * R::BYTES;
+        const long r0 = geo.base + (long)j * a.L;
         float gv = 0.f, bv = 0.f;
-        if (lane < nvalid) {
+        if (lane < a.L) {
             gv = a.g[(r0 + lane) * a.h_v + h];
             bv = a.beta[(r0 + lane) * a.h_v + h];
         }
@@ -207,33 +243,48 @@ struct RecKernel {
             reinterpret_cast<float *>(rec + R::OFF_EG)[lane] = fexp2(x);
             reinterpret_cast<float *>(rec + R::OFF_DG)[lane] = fexp2(gl - x);
         }
-        // key quads: lane (g, r) row 16 rb + r, columns 16 kb + 4 g .. + 3, fp16
-        const int g4 = lane >> 4, r = lane & 15;
-        QE kq[NB][DKB];
-        const In *kp = static_cast<const In *>(a.k) + (r0 * a.h_qk + hq) * DK;
-#pragma unroll
-        for (int rb = 0; rb < NB; ++rb) {
-            const int row = 16 * rb + r;
-#pragma unroll
-            for (int kb = 0; kb < DKB; ++kb) {
-                QE v = {0, 0, 0, 0};
-                if (row < nvalid) {
-                    const bf16x4 b = *reinterpret_cast<const bf16x4 *>(kp + (long)row * a.h_qk * DK + 16 * kb + 4 * g4);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] = (E)(float)b[e];
-                }
-                kq[rb][kb] = v;
-            }
-        }
+        QOffs<DK> qo;
+        qo.make(lane);
+        const E *K = Ks + wave * LP * DK;
         ut::Consts us;
         ut::make_consts(us, lane);
-        ut::solve_t<NB, DKB>(kq, Gs, Bs, reinterpret_cast<E *>(rec + R::OFF_T), LP, us, lane);
+        {
+            QE kq[NB][DKB];
+#pragma unroll
+            for (int rb = 0; rb < NB; ++rb) ld_q<DKB, DK>(kq[rb], K + 16 * rb * DK, qo.q);
+            ut::solve_t<NB, DKB>(kq, Gs, Bs, reinterpret_cast<E *>(rec + R::OFF_T), LP, us, lane);
+        }
+        // N = K_(j+1) K_j^T from the transposed tiles K_j K_(j+1)^T: lane (g, n) holds entry
+        // (16 br + n, 16 bc + 4g + i), four consecutive entries of one row
+        E *N = reinterpret_cast<E *>(rec + R::OFF_N);
+        const int g = lane >> 4, n = lane & 15;
+        const bool last = j + 1 >= J;
+#pragma unroll
+        for (int br = 0; br < NB; ++br) {
+            QE kn[DKB];
+            ld_q<DKB, DK>(kn, K + (LP + 16 * br) * DK, qo.q);
+#pragma unroll
+            for (int bc = 0; bc < NB; ++bc) {
+                QE kc[DKB];
+                ld_q<DKB, DK>(kc, K + 16 * bc * DK, qo.q);
+                f32x4 v = mma_q<E, DKB>(f32x4{0.f, 0.f, 0.f, 0.f}, kc, kn);
+                if (last) v = f32x4{0.f, 0.f, 0.f, 0.f};
+                st_quad(N + (16 * br + n) * LP + 16 * bc + 4 * g, quad_of<E>(v));
+            }
+        }
     }
 };
 
 // ====================================================================== states
 // One workgroup per (state-pass chain, 32-column tile): waves 0, 1 scan 16 columns each,
-// waves 2, 3 stage every block's key rows (fp16), V tile, T and factors three blocks ahead.
+// waves 2, 3 stage every block's key rows (fp16), V tile and record three blocks ahead
+// into a four-slot ring.
+//
+// The scan carries X_j = K_j S_j, the keys times the state at the block start, and uses
+//     X_(j+1) = K_(j+1) S_(j+1) = gamma_n K_(j+1) S_j + (K_(j+1) K_j^T) diag(dG) Delta_j,
+// so that per block only Delta_j = T (V - diag(eG) X_j) and the short product with N_j stand
+// between one block and the next; the state update S_(j+1) = gamma_n S_j + K_j^T diag(dG)
+// Delta_j and Y_(j+2) = K_(j+2) S_(j+1) are off that path.
 template <int DK, int LP>
 struct StatesKernel {
     static constexpr int NB = LP / 16, DKB = DK / 16, BV = 32;
@@ -243,26 +294,26 @@ struct StatesKernel {
     static constexpr int TS = LP + 8, VS = BV + 8;
     static constexpr int ROWS_B = LP * DK * 2;
     static constexpr int V_B = al16(LP * VS * 2);
-    static constexpr int T_B = al16(LP * TS * 2);
-    static constexpr int OFF_V = ROWS_B, OFF_T = OFF_V + V_B, OFF_F = OFF_T + T_B;
+    static constexpr int M_B = al16(LP * TS * 2);
+    static constexpr int OFF_V = ROWS_B, OFF_T = OFF_V + V_B, OFF_N = OFF_T + M_B, OFF_F = OFF_N + M_B;
     static constexpr int SLOT_B = al16(OFF_F + 2 * LP * 4);
-    static constexpr int NS = 3;                   // LDS slots
+    static constexpr int NS = 4;                   // LDS slots: blocks j .. j + 2 in use, j + 3 staged
     static constexpr int OFF_SINK = NS * SLOT_B;
     static constexpr int BYTES = OFF_SINK + 16 * 128;
     // staging: chunks of 16 bytes per block
     static constexpr int TT = 128;
     static constexpr int KCH = LP * DK / 8;        // key rows
     static constexpr int VCH = LP * BV / 8;        // V tile
-    static constexpr int TCH = LP * LP / 8;        // T
+    static constexpr int MCH = LP * LP / 8;        // T or N
     static constexpr int FCH = 2 * LP / 4;         // eG, dG
-    static constexpr int NCH = KCH + VCH + TCH + FCH;
+    static constexpr int NCH = KCH + VCH + 2 * MCH + FCH;
     static constexpr int PER = (NCH + TT - 1) / TT;
     static constexpr int NREG = 3;                 // blocks of loads in flight per L lane
     static_assert(KCH % 64 == 0 && VCH % 64 == 0, "wave-uniform staging sources");
 
     struct Slots {
-        unsigned g[PER];   // byte offset in its source (rows, V, or the record)
-        unsigned l[PER];   // LDS byte offset in a slot (or the sink)
+        unsigned g[PER];          // byte offset in its source (rows, V, or the record)
+        unsigned l[PER];          // LDS byte offset in a slot (or the sink)
         unsigned char src[PER];   // 0 rows, 1 V, 2 record
     };
     struct Regs {
@@ -272,7 +323,8 @@ struct StatesKernel {
     __device__ static void run(const ChunkArgs &a, unsigned char *smem)
     {
         const int lane = threadIdx.x & 63, wave = wave_id();
-        const int c = blockIdx.x / a.n_vt, vt = blockIdx.x % a.n_vt;
+        const int per = 8 * a.n_vt, rem = blockIdx.x % per;
+        const int c = (blockIdx.x / per) * 8 + rem % 8, vt = rem / 8;
         if (c >= a.n1 * a.h_v) return;
         const int pos = c / a.h_v, h = c % a.h_v;
         const Geo geo = geo_of(a, pos);
@@ -305,39 +357,60 @@ struct StatesKernel {
             }
             lds_barrier();
             lds_barrier();
-            for (int j = 0; j < J; ++j) {
-                if (j > 0 && j % a.G == 0) write_ckpt(a, pos, h, geo.nseg, j / a.G, c0, S, lane);
-                const unsigned char *sl = smem + (j % NS) * SLOT_B;
-                const E *K = reinterpret_cast<const E *>(sl);
-                const In *V = reinterpret_cast<const In *>(sl + OFF_V);
-                const E *Tm = reinterpret_cast<const E *>(sl + OFF_T);
-                const float *eG = reinterpret_cast<const float *>(sl + OFF_F), *dG = eG + LP;
-                f32x4 x[NB];
+            const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+            auto slot_of = [&](int jj) { return smem + (jj % NS) * SLOT_B; };
+            auto krows = [&](f32x4 (&y)[NB], int jj) {   // y = K_jj S (state operand sq)
 #pragma unroll
                 for (int rb = 0; rb < NB; ++rb) {
                     QE kq[DKB];
-                    ld_q<DKB, DK>(kq, K + 16 * rb * DK, qo.q);
-                    x[rb] = mma_q<E, DKB>(f32x4{0.f, 0.f, 0.f, 0.f}, kq, sq);
+                    ld_q<DKB, DK>(kq, reinterpret_cast<const E *>(slot_of(jj)) + 16 * rb * DK, qo.q);
+                    y[rb] = mma_q<E, DKB>(z, kq, sq);
                 }
-                QE dq[NB];
+            };
+            // the operands of the serial path of block jj, read from LDS a step ahead
+            struct Ops {
+                f32x4 v[NB];           // V tile, this wave's column
+                f32x4 eg[NB], dg[NB];  // gate factors of rows 16 rb + 4g + i
+                QE t[NB][NB], nm[NB][NB];
+                float decay;
+            };
+            auto load_ops = [&](Ops &op, int jj) {
+                const unsigned char *sl = slot_of(jj);
+                const In *V = reinterpret_cast<const In *>(sl + OFF_V);
+                const float *eG = reinterpret_cast<const float *>(sl + OFF_F), *dG = eG + LP;
 #pragma unroll
                 for (int rb = 0; rb < NB; ++rb) {
                     const int rr = 16 * rb + 4 * g;
-                    const f32x4 gq = ld4f(eG + rr);
-                    f32x4 d;
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) d[i] = to_f(V[(rr + i) * VS + 16 * wave + n]) - gq[i] * x[rb][i];
-                    dq[rb] = quad_of<E>(d);
+                    for (int i = 0; i < 4; ++i) op.v[rb][i] = to_f(V[(rr + i) * VS + 16 * wave + n]);
+                    op.eg[rb] = ld4f(eG + rr);
+                    op.dg[rb] = ld4f(dG + rr);
+                    ld_quads<E, NB>(op.t[rb], reinterpret_cast<const E *>(sl + OFF_T) + 16 * rb * TS, TS, lane);
+                    ld_quads<E, NB>(op.nm[rb], reinterpret_cast<const E *>(sl + OFF_N) + 16 * rb * TS, TS, lane);
                 }
+                op.decay = eG[LP - 1];
+            };
+            f32x4 x[NB], y[NB];
+            krows(x, 0);   // X_0 = K_0 S_0
+            krows(y, 1);   // Y_1 = K_1 S_0
+            Ops op;
+            load_ops(op, 0);
+            int s_next = a.G;
+            for (int j = 0; j < J; ++j) {
+                const E *K = reinterpret_cast<const E *>(slot_of(j));
+                // serial path: Delta_j = T (V - diag(eG) X_j), uq = diag(dG) Delta_j,
+                // X_(j+1) = gamma_n Y_(j+1) + N_j uq
+                QE dq[NB];
+#pragma unroll
+                for (int rb = 0; rb < NB; ++rb) dq[rb] = quad_of<E>(op.v[rb] - op.eg[rb] * x[rb]);
                 QE uq[NB];
 #pragma unroll
-                for (int rb = 0; rb < NB; ++rb) {
-                    QE tq[NB];
-                    ld_quads<E, NB>(tq, Tm + 16 * rb * TS, TS, lane);
-                    const f32x4 dl = mma_q<E, NB>(f32x4{0.f, 0.f, 0.f, 0.f}, tq, dq);
-                    uq[rb] = quad_of<E>(dl * ld4f(dG + 16 * rb + 4 * g));
-                }
-                const float decay = eG[LP - 1];
+                for (int rb = 0; rb < NB; ++rb) uq[rb] = quad_of<E>(mma_q<E, NB>(z, op.t[rb], dq) * op.dg[rb]);
+                const float decay = op.decay;
+#pragma unroll
+                for (int rb = 0; rb < NB; ++rb) x[rb] = mma_q<E, NB>(y[rb] * decay, op.nm[rb], uq);
+                load_ops(op, j + 1);
+                // S_(j+1) = gamma_n S_j + K_j^T diag(dG) Delta_j
 #pragma unroll
                 for (int kb = 0; kb < DKB; ++kb) {
                     QE kt[NB];
@@ -345,18 +418,23 @@ struct StatesKernel {
                     S[kb] = mma_q<E, NB>(S[kb] * decay, kt, uq);
                     sq[kb] = quad_of<E>(S[kb]);
                 }
+                // Y_(j+2) = K_(j+2) S_(j+1)
+                krows(y, j + 2);
+                if (j + 1 == s_next) {
+                    write_ckpt(a, pos, h, geo.nseg, s_next / a.G, c0, S, lane);
+                    s_next += a.G;
+                }
                 lds_barrier();
             }
-            write_ckpt(a, pos, h, geo.nseg, J / a.G, c0, S, lane);
         } else {
-            // ---- L: step j stores the loads of block j + 2 and loads block j + 2 + NREG
+            // ---- L: step j stores the loads of block j + 3 and loads block j + 3 + NREG
             const int lt = 64 * (wave - 2) + lane;
             Slots sl;
 #pragma unroll
             for (int u = 0; u < PER; ++u) {
                 int ch = lt + TT * u;
                 unsigned gsrc = 0, lds = (unsigned)(OFF_SINK + 16 * lt);
-                unsigned char src = 0;
+                int src = 2;   // past the chunks: reload the record's first chunk into the sink
                 if (ch < KCH) {
                     const int t = ch / (DK / 8), cc = ch % (DK / 8);
                     gsrc = (unsigned)(t * qks * 2 + cc * 16);
@@ -367,17 +445,13 @@ struct StatesKernel {
                     gsrc = (unsigned)(t * vst * 2 + cc * 16);
                     lds = (unsigned)(OFF_V + (t * VS + 8 * cc) * 2);
                     src = 1;
-                } else if ((ch -= VCH) < TCH) {
-                    const int t = ch / (LP / 8), cc = ch % (LP / 8);
-                    gsrc = (unsigned)(R::OFF_T + (t * LP + 8 * cc) * 2);
-                    lds = (unsigned)(OFF_T + (t * TS + 8 * cc) * 2);
-                    src = 2;
-                } else if ((ch -= TCH) < FCH) {
+                } else if ((ch -= VCH) < 2 * MCH) {
+                    const int m = ch / MCH, cm = ch % MCH, t = cm / (LP / 8), cc = cm % (LP / 8);
+                    gsrc = (unsigned)((m ? R::OFF_N : R::OFF_T) + (t * LP + 8 * cc) * 2);
+                    lds = (unsigned)((m ? OFF_N : OFF_T) + (t * TS + 8 * cc) * 2);
+                } else if ((ch -= 2 * MCH) < FCH) {
                     gsrc = (unsigned)(R::OFF_EG + 16 * ch);
                     lds = (unsigned)(OFF_F + 16 * ch);
-                    src = 2;
-                } else {
-                    src = 2;   // past the chunks: reload the record's first chunk into the sink
                 }
                 sl.g[u] = gsrc;
                 sl.l[u] = lds;
@@ -386,7 +460,7 @@ struct StatesKernel {
                 sl.src[u] = (unsigned char)__builtin_amdgcn_readfirstlane(src);
             }
             auto fetch = [&](int jj, Regs &rg) {
-                // blocks past J (never stored into a slot that is read) load the record of block 0
+                // blocks past J (never stored into a slot that is read) load block 0 again
                 const int jc = jj < J ? jj : 0;
                 const unsigned rb = (unsigned)(a.L * qks * 2), vb = (unsigned)(a.L * vst * 2);
                 const __amdgpu_buffer_rsrc_t rr = rsrc(kp + (long)jc * a.L * qks, rb);
@@ -410,21 +484,22 @@ struct StatesKernel {
             Regs r[NREG];
 #pragma unroll
             for (int i = 0; i < NREG; ++i) fetch(i, r[i]);
-            // blocks 0 and 1 before the loop
+            // blocks 0, 1 and 2 before the loop
             store(0, r[0]);
             fetch(NREG, r[0]);
             store(1, r[1]);
             fetch(NREG + 1, r[1]);
+            store(2, r[2]);
+            fetch(NREG + 2, r[2]);
             lds_barrier();
             lds_barrier();
-            // step j stores block j + 2 (held in r[(j + 2) % NREG]) and refills it with
-            // block j + 2 + NREG
+            // step j stores block j + 3 (held in r[j % NREG]) and refills it with block j + 3 + NREG
             int j = 0;
             for (; j + NREG <= J; j += NREG) {
 #pragma unroll
                 for (int u = 0; u < NREG; ++u) {
-                    store(j + u + 2, r[(u + 2) % NREG]);
-                    fetch(j + u + 2 + NREG, r[(u + 2) % NREG]);
+                    store(j + u + 3, r[u]);
+                    fetch(j + u + 3 + NREG, r[u]);
                     lds_barrier();
                 }
             }
@@ -444,11 +519,11 @@ struct StatesKernel {
 };
 
 // ====================================================================== out
-// One workgroup per (chain, segment), all d_v columns.  Waves: 0 .. NC-1 C (16 columns
-// each), NC U0 (clean record), NC + 1 U1 (noisy record), then NL staging waves.
-template <typename Out, int DK, int LP, int NL>
+// One workgroup per (chain, segment, tile of DV columns of d_v).  Waves: 0 .. NC-1 C (16
+// columns each), NC U0 (clean record), NC + 1 U1 (noisy record), then NL staging waves.
+template <typename Out, int DK, int DV_, int LP, int NL>
 struct OutKernel {
-    static constexpr int DV = DK, DK_ = DK;
+    static constexpr int DV = DV_, DK_ = DK;   // DV: the d_v columns of one workgroup
     typedef Out OutT;
     static constexpr int NB = LP / 16, DKB = DK / 16, NC = DV / 16;
     static constexpr int NW = NC + 2 + NL, kThreads = 64 * NW;
@@ -920,35 +995,40 @@ __device__ __forceinline__ void run_segment(const ChunkArgs &a, unsigned char *s
     typedef typename K::Seg Seg;
     typedef typename K::Ptrs Ptrs;
     constexpr int DK = K::DK_;
-    const int u = blockIdx.x;
-    if (u >= a.n_units) return;
-    // (position in order, segment, v-head)
-    int pos, s, h;
+    // Workgroups come in groups of (position in order, segment, q/k head); a group's members
+    // are its v-heads times the d_v tiles, all reading the same q/k rows.  Eight groups
+    // interleave, so that the members of a group have ids congruent mod 8 and run on one
+    // XCD (workgroup ids are dealt to the eight XCDs in turn).
+    const int r_v = a.h_v / a.h_qk, M = r_v * a.n_ot;
+    const int u = blockIdx.x, blk = u / (8 * M), rem = u % (8 * M);
+    const int grp = blk * 8 + rem % 8, mem = rem / 8;
+    if (grp >= a.n_groups) return;
+    int pos, s, hq;
     if (a.cu) {
-        // binary search for the last position whose segments-before * h_v <= u
+        // binary search for the last position whose segments-before * h_qk <= grp
         int lo = 0, hi = a.n_order - 1;
         while (lo < hi) {
             const int mid = (lo + hi + 1) >> 1;
-            if ((long)segs_before(a, mid) * a.h_v <= u) lo = mid; else hi = mid - 1;
+            if ((long)segs_before(a, mid) * a.h_qk <= grp) lo = mid; else hi = mid - 1;
         }
         pos = lo;
-        const int r = u - segs_before(a, pos) * a.h_v;
-        s = r / a.h_v;
-        h = r % a.h_v;
+        const int r = grp - segs_before(a, pos) * a.h_qk;
+        s = r / a.h_qk;
+        hq = r % a.h_qk;
     } else {
-        const int per = nseg_of(a.nblk, a.G) * a.h_v;
-        pos = u / per;
-        const int r = u % per;
-        s = r / a.h_v;
-        h = r % a.h_v;
+        const int per = nseg_of(a.nblk, a.G) * a.h_qk;
+        pos = grp / per;
+        const int r = grp % per;
+        s = r / a.h_qk;
+        hq = r % a.h_qk;
     }
+    const int h = hq * r_v + mem / a.n_ot, v0 = (mem % a.n_ot) * K::DV;
     const Geo geo = geo_of(a, pos);
     if (s >= geo.nseg) return;
-    const int hq = h / (a.h_v / a.h_qk);
     const long row0 = geo.base + (long)s * a.G * a.L;
     Seg c;
     const long qk_off = (row0 * a.h_qk + hq) * DK;
-    const long v_off = (row0 * a.h_v + h) * a.dv;
+    const long v_off = (row0 * a.h_v + h) * a.dv + v0;
     const long g_off = row0 * a.h_v + h;
     c.p0.k = static_cast<const In *>(a.k) + qk_off;
     c.p0.q = static_cast<const In *>(a.q) + qk_off;
@@ -972,11 +1052,11 @@ __device__ __forceinline__ void run_segment(const ChunkArgs &a, unsigned char *s
     const int left = geo.nb - s * a.G;
     c.nb = left < a.G ? left : a.G;
     c.L = a.L;
-    const long st_off = ((long)geo.doc * a.h_v + h) * DK * a.dv;
+    const long st_off = ((long)geo.doc * a.h_v + h) * DK * a.dv + v0;
     if (s == 0)
         c.s0 = a.h0 ? a.h0 + st_off : nullptr;
     else
-        c.s0 = a.ckpt + ckpt_index(a, pos, h, geo.nseg, s) * DK * a.dv;
+        c.s0 = a.ckpt + ckpt_index(a, pos, h, geo.nseg, s) * DK * a.dv + v0;
     c.ht = (a.ht && s == geo.nseg - 1) ? a.ht + st_off : nullptr;
     c.dv = a.dv;
     c.scale = a.scale;

@@ -68,7 +68,8 @@ struct ChunkArgs {
     int n1;                 // chains' sequences / documents with two or more segments (the
                             // first n1 in processing order)
     int J_max;              // blocks of the longest state pass: (max nseg - 1) * G
-    int n_units;            // workgroups of the out kernel
+    int n_groups;           // (position in order, segment, q/k head) groups of the out kernel
+    int n_ot;               // d_v tiles of the out kernel
     int n_vt;               // 32-column tiles of the state pass
     float scale;
     int n_order;            // packed: documents listed in order[]
@@ -153,6 +154,8 @@ hipError_t launch_noisy_blocks(int lp, bool f32_out, const NoisyArgs &na, hipStr
 // The chunk-parallel forward: bf16 inputs, d_k = d_v in {64, 128}, blocks of at most 32.
 bool chunked_supported(Types ty, int dk, int dv, int lp);
 hipError_t launch_fwd_chunked(Types ty, int dk, int lp, const ChunkArgs &a, hipStream_t s);
+// Columns of one workgroup of the out kernel: d_v (one tile) or 32.
+bool chunk_tile_supported(int dk, int tile);
 size_t chunk_rec_bytes(int lp);
 
 // The two-stream ShortConv (conv_kernels.hip).  x, xn, y, yn, dy, dyn are [rows][D] of the

@@ -118,12 +118,14 @@ def test_chunked_route_limits_and_workspace():
                dict(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32)):
         assert _fwd(_desc(**ch, **kw)) == bd.BDGDN_ERR_UNSUPPORTED, kw
         assert bd.bdgdn_fwd_train_workspace(_desc(**ch, **kw)) == 0
-    # 64 tokens in blocks of 32: 2 blocks x 4 v-heads of 2304-byte records, no later segment
-    assert bd.bdgdn_fwd_train_workspace(_desc(**ch)) == 2 * 4 * 2304
-    # 4 x 4096 tokens, 16 heads: 512 blocks, segments of 32 -> 16 later-start states per head
-    big = _desc(**ch, batch=4, seqlen=4096, h_qk=16, h_v=16)
-    assert bd.bdgdn_fwd_train_workspace(big) == 512 * 16 * 2304 + 16 * 16 * 128 * 128 * 4
-    assert _fwd(_desc(**ch)) == bd.BDGDN_ERR_WORKSPACE
+    # every chain one segment (no state pass): no workspace
+    assert bd.bdgdn_fwd_train_workspace(_desc(**ch)) == 0
+    assert bd.bdgdn_fwd_train_workspace(_desc(**ch, batch=4, seqlen=4096, h_qk=16, h_v=16)) == 0
+    # 2 x 1100 tokens, 2 heads, blocks of 32: 70 blocks in 32-column tiles -> segments of 16;
+    # records of 4352 bytes per (block, head), a state per (later segment start, head)
+    mid = _desc(**ch, batch=2, seqlen=1100, h_qk=2, h_v=2)
+    assert bd.bdgdn_fwd_train_workspace(mid) == 70 * 2 * 4352 + (70 // 16) * 2 * 128 * 128 * 4
+    assert _fwd(mid) == bd.BDGDN_ERR_WORKSPACE
     # more packed documents than the schedule orders
     cu = (ctypes.c_int32 * 514)(*[32 * i for i in range(514)])
     assert _fwd(_desc(**ch, seqlen=32 * 513, num_seqs=513), cu, cu) == bd.BDGDN_ERR_UNSUPPORTED
