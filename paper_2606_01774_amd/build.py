@@ -16,7 +16,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libbdgdn.so")
 SOURCES = ["api.hip", "fwd_kernels.hip", "fwd_scan_kernels.hip", "fused_kernels.hip", "serve_kernels.hip",
-           "split_kernels.hip", "conv_kernels.hip", "bwd_kernels.hip", "chunked_kernels.hip"]
+           "split_kernels.hip", "conv_kernels.hip", "bwd_kernels.hip", "chunked_kernels.hip",
+           "bwd_generic.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-I" + INCLUDE, "-I" + CSRC,
          # no packed-fp32 instructions in the device code

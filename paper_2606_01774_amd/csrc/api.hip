@@ -628,13 +628,26 @@ static BwdLayout bwd_layout(const bdgdn_fwd_desc_t *d)
     return l;
 }
 
+// Shapes outside the block-form kernels run the per-step fp32 backward (bwd_generic.hip).
+static bool bwd_generic_ok(const bdgdn_fwd_desc_t *d, int n_views)
+{
+    return !bwd_shape_ok(d) && d->num_seqs <= kMaxOrder &&
+           bwd_generic_supported(d->dtype == BDGDN_F32, d->d_k, d->d_v, d->block, n_views);
+}
+static size_t bwd_generic_bytes(const bdgdn_fwd_desc_t *d)
+{
+    const int nseq = d->num_seqs > 0 ? d->num_seqs : d->batch;
+    return bwd_generic_workspace(nseq, total_blocks(d), d->h_v, d->d_k, d->d_v);
+}
+
 size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc)
 {
     if (!desc || check_heads(desc->h_qk, desc->h_v, desc->d_k, desc->d_v, desc->block, desc->scale, desc->dtype,
                              desc->out_dtype) != BDGDN_OK)
         return 0;
-    if (desc->batch <= 0 || desc->seqlen <= 0 || !bwd_shape_ok(desc)) return 0;
-    return bwd_layout(desc).total;
+    if (desc->batch <= 0 || desc->seqlen <= 0) return 0;
+    if (bwd_shape_ok(desc)) return bwd_layout(desc).total;
+    return bwd_generic_ok(desc, 1) ? bwd_generic_bytes(desc) : 0;
 }
 
 // The backward of the clean stream and noisy view 0 (qn .. dbetan), plus n_more further views.
@@ -648,7 +661,8 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
 {
     int st = check_fwd(desc, cu_seqlens_dev, cu_seqlens_host);
     if (st != BDGDN_OK) return st;
-    if (!bwd_shape_ok(desc)) return BDGDN_ERR_UNSUPPORTED;
+    const bool generic = !bwd_shape_ok(desc);
+    if (generic && !bwd_generic_ok(desc, 1 + n_more)) return BDGDN_ERR_UNSUPPORTED;
     if (!q || !k || !v || !g || !beta || !qn || !kn || !vn || !gn || !betan || !dout || !doutn || !dq ||
         !dk || !dv || !dg || !dbeta || !dqn || !dkn || !dvn || !dgn || !dbetan)
         return BDGDN_ERR_INVALID_ARG;
@@ -668,6 +682,26 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     const bool packed = desc->num_seqs > 0;
     const int nseq = packed ? desc->num_seqs : desc->batch;
     const hipStream_t strm = static_cast<hipStream_t>(stream);
+    if (generic) {
+        GenBwdCall c = {};
+        c.q = q; c.k = k; c.v = v; c.g = g; c.beta = beta; c.dout = dout;
+        c.dq = dq; c.dk = dk; c.dv = dv; c.dg = dg; c.db = dbeta;
+        c.qn = qn; c.kn = kn; c.vn = vn; c.gn = gn; c.betan = betan; c.doutn = doutn;
+        c.dqn = dqn; c.dkn = dkn; c.dvn = dvn; c.dgn = dgn; c.dbn = dbetan;
+        c.more = more; c.n_more = n_more;
+        c.cu = packed ? cu_seqlens_dev : nullptr;
+        c.cu_host = packed ? cu_seqlens_host : nullptr;
+        c.n_seq = nseq;
+        c.rows = (long)desc->batch * desc->seqlen;
+        c.total_blocks = total_blocks(desc);
+        c.h0 = h0; c.dht = dht; c.dh0 = dh0;
+        c.T = desc->seqlen; c.L = desc->block; c.h_qk = desc->h_qk; c.h_v = desc->h_v;
+        c.d_k = desc->d_k; c.d_v = desc->d_v;
+        c.scale = desc->scale;
+        c.workspace = workspace;
+        const hipError_t e = launch_bwd_generic(desc->dtype == BDGDN_F32, desc->out_dtype == BDGDN_F32, c, strm);
+        return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+    }
     unsigned char *ws = static_cast<unsigned char *>(workspace);
     const BwdLayout lay = bwd_layout(desc);
     _Float16 *seeds = reinterpret_cast<_Float16 *>(ws + lay.seeds);

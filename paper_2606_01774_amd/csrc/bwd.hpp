@@ -60,6 +60,32 @@ struct RangeArgs {
     float *range;           // [2]
 };
 hipError_t launch_bwd_range(bool bf16_out, const RangeArgs &r, hipStream_t s);
+
+// The per-step fp32 backward (bwd_generic.hip) for the shapes outside the block-form
+// kernels: one call's arguments.
+struct GenBwdCall {
+    const void *q, *k, *v;
+    const float *g, *beta;
+    const void *dout;
+    float *dq, *dk, *dv, *dg, *db;
+    const void *qn, *kn, *vn;
+    const float *gn, *betan;
+    const void *doutn;
+    float *dqn, *dkn, *dvn, *dgn, *dbn;
+    const BwdView *more;
+    int n_more;
+    const int32_t *cu, *cu_host;   // packed documents (device, host), or null
+    int n_seq;                     // sequences or documents
+    long rows, total_blocks;       // token rows; blocks of all chains' sequences
+    const float *h0, *dht;
+    float *dh0;
+    int T, L, h_qk, h_v, d_k, d_v;
+    float scale;
+    void *workspace;
+};
+size_t bwd_generic_workspace(int n_seq, long total_blocks, int h_v, int dk, int dv);
+bool bwd_generic_supported(bool f32_in, int dk, int dv, int L, int n_views);
+hipError_t launch_bwd_generic(bool f32_in, bool f32_out, const GenBwdCall &c, hipStream_t s);
 size_t bwd_block_lds();
 // The backward of a's two streams, plus n_more further noisy views seeded from the same clean
 // states (their seed gradients summed into the clean state gradient).

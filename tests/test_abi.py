@@ -325,10 +325,17 @@ def test_bwd_train_validation_and_workspace():
     # per (block, v-head): an fp16 seed, two fp16 states, U K (32 x 128 fp16)
     units = 2 * 4
     assert need >= units * 128 * 128 * (2 + 2 + 2) + units * 32 * 128 * 2
-    assert lib.bdgdn_bwd_train_workspace(ctypes.byref(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32))) == 0
-    assert _bwd(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32)) == bd.BDGDN_ERR_UNSUPPORTED
-    assert _bwd(_desc(d_k=64, d_v=64)) == bd.BDGDN_ERR_UNSUPPORTED
-    assert _bwd(_desc(block=64)) == bd.BDGDN_ERR_UNSUPPORTED
+    # the other shapes run the per-step backward: a clean state per eighth block start and
+    # per chain (sequence, v-head), and per (chain, 16-column tile) eight block-start states
+    f32 = _desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32)
+    groups = 2 // 8 + 1
+    gen_need = groups * 4 * 128 * 128 * 4 + 4 * 8 * 8 * 128 * 16 * 4
+    assert lib.bdgdn_bwd_train_workspace(ctypes.byref(f32)) == gen_need
+    for kw in (dict(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32), dict(d_k=64, d_v=64), dict(block=64),
+               dict(d_k=64), dict(block=48, out_dtype=bd.BDGDN_BF16)):
+        d = _desc(**kw)
+        assert lib.bdgdn_bwd_train_workspace(ctypes.byref(d)) > 0, kw
+        assert _bwd(d) == bd.BDGDN_ERR_WORKSPACE, kw   # every check passes but the workspace
     assert _bwd(_desc(h_v=3)) == bd.BDGDN_ERR_INVALID_ARG
     assert _bwd(ok, null_grad=True) == bd.BDGDN_ERR_INVALID_ARG
     assert _bwd(ok, ws=None, ws_bytes=0) == bd.BDGDN_ERR_WORKSPACE
@@ -379,5 +386,12 @@ def test_bwd_views_validation():
     views[1] = bd.NoisyViewGrad(*(full[:5] + [0x1008] + full[6:]))  # view 1's do not 16-byte aligned
     assert call(ok, 2) == bd.BDGDN_ERR_INVALID_ARG
     views[1] = bd.NoisyViewGrad(*full)
-    assert call(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32), 2) == bd.BDGDN_ERR_UNSUPPORTED
-    assert call(_desc(block=64), 2) == bd.BDGDN_ERR_UNSUPPORTED
+    # the per-step backward takes up to four views
+    assert call(_desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32), 2) == bd.BDGDN_ERR_WORKSPACE
+    many = (bd.NoisyViewGrad * 5)(*[bd.NoisyViewGrad(*full) for _ in range(5)])
+
+    def call_many(desc, n):
+        return lib.bdgdn_bwd_train_views(ctypes.byref(desc), P, P, P, P, P, many, n, None, None, None, P, None,
+                                         P, P, P, P, P, None, None, 0, None)
+    assert call_many(_desc(block=64), 4) == bd.BDGDN_ERR_WORKSPACE
+    assert call_many(_desc(block=64), 5) == bd.BDGDN_ERR_UNSUPPORTED
