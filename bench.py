@@ -549,6 +549,30 @@ def main():
             "views2_ms_per_call": bvms, "views2_tokens_per_s": 3 * w.tokens / (bvms * 1e-3)}
         del bws, bgrads, bvgrads, bviews
         torch.cuda.empty_cache()
+        # the per-step fp32 backward of the shapes outside the block-form kernels: the tiny
+        # fp32 workload and the grouped-value workload with its blocks of 64 positions
+        per_step = {}
+        for key, pw in (("c0", W.TINY_F32), ("c2", W.GVA_16K)):
+            pin = {k_: v_.to(dev) for k_, v_ in W.make_train(pw).items()}
+            pshape = (pw.batch, pw.seqlen, pw.h_v, pw.d_v)
+            pdo = torch.randn(pshape, generator=torch.Generator(device=dev).manual_seed(8), device=dev)
+            pdon = torch.randn(pshape, generator=torch.Generator(device=dev).manual_seed(9), device=dev)
+            pdesc = bd.make_fwd_desc(pin["q"], pin["v"], block=pw.block, out_dtype=torch.float32)
+            pws = torch.empty(bd.bdgdn_bwd_train_workspace(pdesc), dtype=torch.uint8, device=dev)
+            pscale = 1.0 / math.sqrt(pw.d_k)
+            pargs = [pin[k_] for k_ in ("q", "k", "v", "g", "beta", "qn", "kn", "vn", "gn", "betan")]
+            pgrads = bd.bdgdn_bwd_train(*pargs, pdo, pdon, block=pw.block, scale=pscale, workspace=pws)
+
+            def pstep():
+                bd.bdgdn_bwd_train(*pargs, pdo, pdon, block=pw.block, scale=pscale, workspace=pws, grads=pgrads,
+                                   stream=stream)
+            pms = time_protocol(pstep, stream, flush, warmup=1, iters=3, repeats=1, trim=0)[0]
+            per_step[key] = {"workload": pw.name, "ms_per_call": pms, "tokens_per_s": pw.tokens / (pms * 1e-3),
+                             "workspace_bytes": pws.numel(),
+                             "kernels": "bdgdn_bwd_gen_ckpt_kernel + bdgdn_bwd_gen_walk_kernel (fp32, per step)"}
+            del pin, pws, pgrads
+            torch.cuda.empty_cache()
+        result["backward"]["per_step"] = per_step
 
     if "shortconv" in only:
         # the GDN layer's two-stream ShortConv at the same token shape (channels = the q, k
