@@ -29,6 +29,7 @@
 #include <math.h>
 
 #include <mutex>
+#include <type_traits>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -283,17 +284,20 @@ __global__ void __launch_bounds__(256) bdgdn_shortconv_fwd_kernel(ConvArgs a)
     }
 }
 
-// Backward over a thread's TR rows [t0, t1), streamed in chunks of U rows: the loads of the
-// next chunk (x, xn, dy, dyn) are issued before the current chunk is computed, and the
-// last W rows of x, xn (the lag window) and the pending dx, dxn of the last W rows travel
-// from row to row in registers.  Reader rows run to t1 + W - 2 (the W - 1 rows after the
-// range read its last rows); rows before t0 are the previous range's, so what this thread
+// Backward over a thread's TR rows [t0, t1), streamed in chunks of UW rows (the smallest
+// multiple of W that is at least U): the loads of the next chunk (x, xn, dy, dyn) are issued
+// before the current chunk is computed.  The last W rows of x, xn (the lag window) and the
+// pending dx, dxn of the last W rows stay in registers in circular slots: row s lives in
+// slot (s - t0) mod W, which is a constant inside the unrolled chunk (UW is a multiple of W),
+// so rows never move between registers.  Reader rows run to t1 + W - 2 (the W - 1 rows after
+// the range read its last rows); rows before t0 are the previous range's, so what this thread
 // gathers for them is dropped.
 template <typename In, int W, int TR, int U, int VB>
 __global__ void __launch_bounds__(256) bdgdn_shortconv_bwd_kernel(ConvArgs a)
 {
     constexpr int N = VB / (int)sizeof(In);
     constexpr int P = N * (W + 1);   // filter + bias gradients per thread
+    constexpr int UW = (U + W - 1) / W * W;
     typedef typename Lane<VB>::T T;
     __shared__ float red[3][P][64];
     const int lane = threadIdx.x & 63, wave = wave_id();
@@ -321,25 +325,25 @@ __global__ void __launch_bounds__(256) bdgdn_shortconv_bwd_kernel(ConvArgs a)
         const Rows<VB> gdx(a.y, t0, rows, rb), gdxn(a.yn, t0, rows, rb);
         float w[N][W], b[N];
         load_filter<W, N>(a, c0, w, b);
-        // lag window: wx[k], wn[k] hold rows s - k (clamped rows before 0 are masked as
-        // lying before the document)
+        // lag window: slot (s - t0) mod W holds row s of x, xn (clamped rows before 0 are
+        // masked as lying before the document)
         float wx[W][N], wn[W][N];
 #pragma unroll
         for (int k = 1; k < W; ++k) {
             const int src = t0 - k < b0 ? b0 : t0 - k;
-            unpack<In>(gx.ld(voff, (src - b0) * rb), wx[k]);
-            unpack<In>(gxn.ld(voff, (src - b0) * rb), wn[k]);
+            unpack<In>(gx.ld(voff, (src - b0) * rb), wx[W - k]);
+            unpack<In>(gxn.ld(voff, (src - b0) * rb), wn[W - k]);
         }
-        // pending input gradients: ac[k], an[k] of row s - k
+        // pending input gradients of the last W rows, in the same slots
         float ac[W][N], an[W][N];
 #pragma unroll
         for (int k = 0; k < W; ++k)
 #pragma unroll
             for (int j = 0; j < N; ++j) ac[k][j] = an[k][j] = 0.f;
-        T cx[U], cn[U], cy[U], cyn[U];
-        auto load_chunk = [&](int s0, T (&lx)[U], T (&ln)[U], T (&ly)[U], T (&lyn)[U]) {
+        T cx[UW], cn[UW], cy[UW], cyn[UW];
+        auto load_chunk = [&](int s0, T (&lx)[UW], T (&ln)[UW], T (&ly)[UW], T (&lyn)[UW]) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
+            for (int u = 0; u < UW; ++u) {
                 const int s = s0 + u < rows ? s0 + u : rows - 1;   // rows past the end are never used
                 lx[u] = gx.ld(voff, (s - b0) * rb);
                 ln[u] = gxn.ld(voff, (s - b0) * rb);
@@ -350,18 +354,31 @@ __global__ void __launch_bounds__(256) bdgdn_shortconv_bwd_kernel(ConvArgs a)
         load_chunk(t0, cx, cn, cy, cyn);
         Cursor cur;
         cur.start(a, t0);
-        for (int s0 = t0; s0 < s_end; s0 += U) {
-            T nx[U], nn[U], ny[U], nyn[U];
-            load_chunk(s0 + U, nx, nn, ny, nyn);
+        // one chunk of UW rows from s0; TAIL: rows past the range (reader rows of its last
+        // rows, which count for no filter gradient) and the end of the readers
+        auto chunk = [&](int s0, auto tail) {
+            constexpr bool TAIL = decltype(tail)::value;
+            T nx[UW], nn[UW], ny[UW], nyn[UW];
+            load_chunk(s0 + UW, nx, nn, ny, nyn);
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
+            for (int u = 0; u < UW; ++u) {
                 const int s = s0 + u;
-                if (s >= s_end) break;
-                unpack<In>(cx[u], wx[0]);
-                unpack<In>(cn[u], wn[0]);
+                if (TAIL && s >= s_end) break;
+                const int sl = u % W;                       // slot of row s
+                unpack<In>(cx[u], wx[sl]);
+                unpack<In>(cn[u], wn[sl]);
                 if (s > t0) cur.step(a, s);
+                // lag i of row s sits in slot (u - i) mod W
+                float lx[W][N], ln[W][N];
+#pragma unroll
+                for (int i = 0; i < W; ++i)
+#pragma unroll
+                    for (int j = 0; j < N; ++j) {
+                        lx[i][j] = wx[(u - i + W * UW) % W][j];
+                        ln[i][j] = wn[(u - i + W * UW) % W][j];
+                    }
                 float pc[N], pn[N], gc[N], gn[N];
-                pre_of<W, N>(s, cur, wx, wn, w, b, pc, pn);
+                pre_of<W, N>(s, cur, lx, ln, w, b, pc, pn);
                 unpack<In>(cy[u], gc);
                 unpack<In>(cyn[u], gn);
 #pragma unroll
@@ -369,78 +386,81 @@ __global__ void __launch_bounds__(256) bdgdn_shortconv_bwd_kernel(ConvArgs a)
                     gc[j] *= act_grad(pc[j], a.act);
                     gn[j] *= act_grad(pn[j], a.act);
                 }
-                const bool own = s < t1;   // this range's output: counts for the filter and bias
+                const bool own = !TAIL || s < t1;   // this range's output: counts for the filter and bias
                 if (s - (W - 1) >= cur.bs) {   // every lag in s's block
 #pragma unroll
                     for (int i = 0; i < W; ++i) {
+                        const int li = (u - i + W * UW) % W;
 #pragma unroll
                         for (int j = 0; j < N; ++j) {
-                            ac[i][j] = fmaf(w[j][i], gc[j], ac[i][j]);
-                            an[i][j] = fmaf(w[j][i], gn[j], an[i][j]);
+                            ac[li][j] = fmaf(w[j][i], gc[j], ac[li][j]);
+                            an[li][j] = fmaf(w[j][i], gn[j], an[li][j]);
                         }
                         if (own)
 #pragma unroll
                             for (int j = 0; j < N; ++j)
-                                gw[j][i] = fmaf(gn[j], wn[i][j], fmaf(gc[j], wx[i][j], gw[j][i]));
+                                gw[j][i] = fmaf(gn[j], ln[i][j], fmaf(gc[j], lx[i][j], gw[j][i]));
                     }
                 } else {
 #pragma unroll
                     for (int i = 0; i < W; ++i) {
                         if (s - i < cur.ds) break;   // before the document: nothing read
+                        const int li = (u - i + W * UW) % W;
                         const bool in_blk = s - i >= cur.bs;
                         if (in_blk) {
 #pragma unroll
                             for (int j = 0; j < N; ++j) {
-                                ac[i][j] = fmaf(w[j][i], gc[j], ac[i][j]);
-                                an[i][j] = fmaf(w[j][i], gn[j], an[i][j]);
+                                ac[li][j] = fmaf(w[j][i], gc[j], ac[li][j]);
+                                an[li][j] = fmaf(w[j][i], gn[j], an[li][j]);
                             }
                         } else {
 #pragma unroll
-                            for (int j = 0; j < N; ++j) ac[i][j] = fmaf(w[j][i], gc[j] + gn[j], ac[i][j]);
+                            for (int j = 0; j < N; ++j) ac[li][j] = fmaf(w[j][i], gc[j] + gn[j], ac[li][j]);
                         }
                         if (own)
 #pragma unroll
                             for (int j = 0; j < N; ++j)
-                                gw[j][i] = fmaf(gn[j], in_blk ? wn[i][j] : wx[i][j], fmaf(gc[j], wx[i][j], gw[j][i]));
+                                gw[j][i] = fmaf(gn[j], in_blk ? ln[i][j] : lx[i][j], fmaf(gc[j], lx[i][j], gw[j][i]));
                     }
                 }
                 if (own)
 #pragma unroll
                     for (int j = 0; j < N; ++j) gb[j] += gc[j] + gn[j];
-                // row s - (W - 1) has seen its last reader
+                // row s - (W - 1) (slot (u + 1) mod W) has seen its last reader; its slot
+                // becomes row s + 1's
                 const int done = s - (W - 1);
+                const int ds = (u + 1) % W;
                 if (done >= t0) {
-                    gdx.st(pack<In, N, T>(ac[W - 1]), voff, (done - t0) * rb);
-                    gdxn.st(pack<In, N, T>(an[W - 1]), voff, (done - t0) * rb);
+                    gdx.st(pack<In, N, T>(ac[ds]), voff, (done - t0) * rb);
+                    gdxn.st(pack<In, N, T>(an[ds]), voff, (done - t0) * rb);
                 }
 #pragma unroll
-                for (int k = W - 1; k > 0; --k)
-#pragma unroll
-                    for (int j = 0; j < N; ++j) {
-                        wx[k][j] = wx[k - 1][j];
-                        wn[k][j] = wn[k - 1][j];
-                        ac[k][j] = ac[k - 1][j];
-                        an[k][j] = an[k - 1][j];
-                    }
-#pragma unroll
-                for (int j = 0; j < N; ++j) ac[0][j] = an[0][j] = 0.f;
+                for (int j = 0; j < N; ++j) ac[ds][j] = an[ds][j] = 0.f;
             }
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
+            for (int u = 0; u < UW; ++u) {
                 cx[u] = nx[u];
                 cn[u] = nn[u];
                 cy[u] = ny[u];
                 cyn[u] = nyn[u];
             }
-        }
-        // rows of the range whose readers ran past the end of the tensor: after the last
-        // shift, row s_end - k sits in slot k
+        };
+        int s0 = t0;
+        for (; s0 + UW <= t1; s0 += UW) chunk(s0, std::false_type());
+        for (; s0 < s_end; s0 += UW) chunk(s0, std::true_type());
+        // rows of the range whose readers ran past the end of the tensor: rows s_end - k,
+        // k = 1 .. W - 1, in slots (s_end - k - t0) mod W
 #pragma unroll
         for (int k = 1; k < W; ++k) {
             const int d = s_end - k;
             if (d >= t0 && d < t1) {
-                gdx.st(pack<In, N, T>(ac[k]), voff, (d - t0) * rb);
-                gdxn.st(pack<In, N, T>(an[k]), voff, (d - t0) * rb);
+                const int sl = (d - t0) % W;
+#pragma unroll
+                for (int q = 0; q < W; ++q)
+                    if (q == sl) {
+                        gdx.st(pack<In, N, T>(ac[q]), voff, (d - t0) * rb);
+                        gdxn.st(pack<In, N, T>(an[q]), voff, (d - t0) * rb);
+                    }
             }
         }
     }
