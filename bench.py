@@ -33,7 +33,8 @@ sys.path.insert(0, ROOT)
 
 ROUTES = {"fused": "fused (one kernel: per-block UT transform inside the state scan)",
           "split": "split (clean scan writing fp32 seed states, then the noisy-block kernel)",
-          "records": "records (UT-transform kernel, then the scan)"}
+          "records": "records (UT-transform kernel, then the scan)",
+          "chunked": "chunked (state pass over the segment starts, then one workgroup per (chain, segment, tile))"}
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, GB/s
 MFMA16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16/bf16 MFMA, TFLOP/s
 FLUSH_BYTES = 512 * 1024 * 1024
@@ -79,10 +80,10 @@ def algorithmic_bytes_denoise(w, out_bytes=None):
     return _state_bytes(w) + _block_bytes(w, o=True, out_bytes=out_bytes)
 
 
-def algorithmic_bytes_commit(w, with_outputs):
+def algorithmic_bytes_commit(w, with_outputs, out_bytes=None):
     """The state read and written back and the block's k, v, g, beta read; with outputs
     also q read and the causal o written."""
-    return 2 * _state_bytes(w) + _block_bytes(w, q=with_outputs, o=with_outputs)
+    return 2 * _state_bytes(w) + _block_bytes(w, q=with_outputs, o=with_outputs, out_bytes=out_bytes)
 
 
 def model_flops_denoise(w):
@@ -191,6 +192,7 @@ def rates(ms, abytes, flops, tokens):
 # The sources each measured kernel is built from (translation unit and headers).
 KERNEL_SOURCES = {
     "fused": ("common.hpp", "fused.hpp", "fused_kernels.hip", "intra.hpp", "kernels.hpp", "ut.hpp"),
+    "chunked": ("common.hpp", "chunked.hpp", "chunked_kernels.hip", "intra.hpp", "kernels.hpp", "ut.hpp"),
     "records": ("common.hpp", "intra.hpp", "scan.hpp", "fwd_scan_kernels.hip", "kernels.hpp", "ut.hpp"),
     "serve": ("common.hpp", "serve.hpp", "serve_kernels.hip", "kernels.hpp", "ut.hpp"),
 }
@@ -221,6 +223,98 @@ def recorded_traffic(key):
     if rec.get("source_hash") != kernel_source_hash(rec.get("sources", "fused")):
         return None
     return rec.get("bytes_per_launch")
+
+
+# The configurations whose HBM traffic is recorded: bench section, kernel (a substring of
+# the rocprofv3 kernel name), source group, algorithmic bytes (byte model; with fp32
+# outputs where the kernel writes them).
+def traffic_targets():
+    from paper_2606_01774_amd import workloads as W
+    sw = W.SERVE_64
+    return {
+        "c1": ("c1", "bdgdn_fwd_pipelined_kernel<float, 128, 32>", "fused", W.TRAIN_4K),
+        "c2": ("c2", "bdgdn_fwd_pipelined_pair_kernel<float, 128>", "fused", W.GVA_16K),
+        "c4": ("c4", "bdgdn_chunk_out_kernel<float, 128, 128, 32>", "chunked", W.VARLEN_128K),
+        "c3_denoise": ("c3", "bdgdn_k4_denoise_kernel<float, 32>", "serve", sw),
+        "c3_commit": ("c3", "bdgdn_k4_commit_kernel<float, 32, true>", "serve", sw),
+        "c3_commit_state_only": ("c3", "bdgdn_k4_commit_kernel<float, 32, false>", "serve", sw),
+    }
+
+
+def _counter_medians(run_dir, counter):
+    """Median per kernel name of one counter over the dispatches of a rocprofv3 --pmc run
+    (its *counter_collection.csv files under run_dir)."""
+    import csv
+    import glob
+    vals = {}
+    for path in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for row in csv.DictReader(f):
+                if row.get("Counter_Name") == counter:
+                    vals.setdefault(row["Kernel_Name"], []).append(float(row["Counter_Value"]))
+    return {k: sorted(v)[len(v) // 2] for k, v in vals.items()}
+
+
+def record_traffic(root):
+    """Write profiles/traffic.json and traffic.md from the FETCH_SIZE / WRITE_SIZE counter runs
+    under `root`: copy_fetch/, copy_write/ (bench.py --copy-probe) and <section>_fetch/,
+    <section>_write/ (bench.py --only <section>).  The counters are scaled by what they read
+    for the 256 MiB copy (its true traffic 256 MiB read and 256 MiB written)."""
+    copy_bytes = 256 * 1024 * 1024
+    cf = max(_counter_medians(os.path.join(root, "copy_fetch"), "FETCH_SIZE").values())
+    cw = max(_counter_medians(os.path.join(root, "copy_write"), "WRITE_SIZE").values())
+    ff, wf = copy_bytes / 1024 / cf, copy_bytes / 1024 / cw
+    out = {"calibration": {"copy_bytes": copy_bytes, "fetch_kib_raw": cf, "write_kib_raw": cw,
+                           "fetch_factor": ff, "write_factor": wf}, "configs": {}}
+    rows = []
+    for key, (section, kernel, group, wl) in traffic_targets().items():
+        fm = _counter_medians(os.path.join(root, f"{section}_fetch"), "FETCH_SIZE")
+        wm = _counter_medians(os.path.join(root, f"{section}_write"), "WRITE_SIZE")
+        fk = [v for k, v in fm.items() if kernel in k]
+        wk = [v for k, v in wm.items() if kernel in k]
+        if not fk or not wk:
+            continue
+        rd, wr = fk[0] * 1024 * ff, wk[0] * 1024 * wf
+        out["configs"][key] = {"workload": wl.name, "kernel": kernel, "sources": group,
+                               "source_hash": kernel_source_hash(group), "fetch_kib_raw": fk[0],
+                               "write_kib_raw": wk[0], "read_bytes": rd, "write_bytes": wr,
+                               "bytes_per_launch": int(rd + wr)}
+        if key.startswith("c3"):
+            alg = {"c3_denoise": algorithmic_bytes_denoise(wl, 4),
+                   "c3_commit": algorithmic_bytes_commit(wl, True, 4),
+                   "c3_commit_state_only": algorithmic_bytes_commit(wl, False)}[key]
+            model = f"{alg / 1e6:.1f} (fp32 o)"
+        else:
+            alg = algorithmic_bytes_train(wl, 4)
+            model = f"{algorithmic_bytes_train(wl) / 1e6:.1f} / {alg / 1e6:.1f}"
+        rows.append(f"| `{kernel}` | {wl.name} | {fk[0]:.0f} | {wk[0]:.0f} | {rd / 1e6:.1f} | {wr / 1e6:.1f} | "
+                    f"{(rd + wr) / 1e6:.1f} | {model} | {100 * (rd + wr) / alg:.1f} % |")
+    with open(os.path.join(ROOT, "profiles", "traffic.json"), "w") as f:
+        json.dump(out, f, indent=1)
+    md = ["# HBM traffic per launch, every measured configuration", "",
+          "Counters per dispatch (median over the dispatches of the run) from two `rocprofv3 --pmc` runs per",
+          "configuration, one counter each, scaled by what the same counter reads for a plain 256 MiB device",
+          f"copy (`bench.py --copy-probe`): FETCH_SIZE reads {cf:.0f} KiB for the copy's 262144 KiB of reads",
+          f"(factor {ff:.4f}), WRITE_SIZE {cw:.0f} KiB (factor {wf:.4f}).", "",
+          "Commands (repository root on the MI355X box, `TMPDIR=/tmp`; `<section>` is c1, c2, c4 or c3):", "",
+          "    cd /tmp && rocprofv3 --pmc FETCH_SIZE --output-format csv -d <root>/<section>_fetch -o run -- \\",
+          "        python3 <repo>/bench.py --no-cpu-baseline --only <section> --protocol-iters 3 --protocol-repeats 1",
+          "    cd /tmp && rocprofv3 --pmc WRITE_SIZE --output-format csv -d <root>/<section>_write -o run -- \\",
+          "        python3 <repo>/bench.py --no-cpu-baseline --only <section> --protocol-iters 3 --protocol-repeats 1",
+          "    (and the same two with `bench.py --copy-probe --steps 3` into <root>/copy_fetch, <root>/copy_write)",
+          "    python3 <repo>/bench.py --record-traffic <root>", "",
+          "| kernel | workload | FETCH_SIZE (KiB) | WRITE_SIZE (KiB) | read (MB) | written (MB) | total (MB) | "
+          "algorithmic (MB): byte model / with fp32 o | total / algorithmic with fp32 o |",
+          "|---|---|---|---|---|---|---|---|---|", *rows, "",
+          "The training byte model counts bf16 q, k, v, o and fp32 g, beta once (1032 B per (token, head, stream));",
+          "the kernels write fp32 o, so the bytes they must move are the second figure, which the last column",
+          "compares with.  Serving: the state read (and written back by commit) once, the block's q, k, v, g, beta",
+          "read and o written (fp32).", "",
+          "Recorded in `traffic.json` with the hashes of the kernels' sources; bench.py reports a configuration's",
+          "figure as its traffic while those sources are unchanged."]
+    with open(os.path.join(ROOT, "profiles", "traffic.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
+    print(json.dumps(out["configs"], indent=1))
 
 
 def copy_probe(steps):
@@ -295,12 +389,17 @@ def main():
     ap.add_argument("--protocol-iters", type=int, default=20,
                     help="launches per repeat of the per-config protocol (fewer for counter runs)")
     ap.add_argument("--protocol-repeats", type=int, default=3)
+    ap.add_argument("--record-traffic", metavar="DIR", default=None,
+                    help="write profiles/traffic.json and traffic.md from the counter runs under DIR (no GPU)")
     args = ap.parse_args()
     PROTOCOL["iters"], PROTOCOL["repeats"] = max(1, args.protocol_iters), max(1, args.protocol_repeats)
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not part of it "
                                    "(--gpus must be 1)", "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.record_traffic:
+        record_traffic(args.record_traffic)
+        return
     if args.copy_probe:
         copy_probe(args.steps)
         return
@@ -328,7 +427,7 @@ def main():
     # ---------------- headline: the training shape, K back-to-back steps
     w = W.TRAIN_4K
     route = {"fused": bd.BDGDN_ROUTE_FUSED, "split": bd.BDGDN_ROUTE_SPLIT,
-             "records": bd.BDGDN_ROUTE_RECORDS}[args.route]
+             "records": bd.BDGDN_ROUTE_RECORDS, "chunked": bd.BDGDN_ROUTE_CHUNKED}[args.route]
     inp = None
     if "headline" in only or "c1" in only or "cpu" in only:
         inp, d, step, o = train_setup(w, dev, route, torch.float32)
@@ -396,7 +495,8 @@ def main():
         train_config("c2", W.GVA_16K, note="bdgdn_fwd_pipelined_pair_kernel (one kernel; each noisy block of 64 "
                                            "spans two 32-position sub-blocks)")
     if "c4" in only:
-        train_config("c4", W.VARLEN_128K, note="bdgdn_fwd_pipelined_kernel (one kernel), longest documents first")
+        train_config("c4", W.VARLEN_128K, note="bdgdn_chunk_out_kernel (one workgroup per (document, v-head) over "
+                                               "all d_v columns: 512 chains cover the 256 CUs), longest documents first")
 
     # ---------------- c3: serving
     if "c3" in only:
