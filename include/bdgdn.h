@@ -223,11 +223,14 @@ int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc,
                           const float *h0, void *o, float *ht,
                           void *workspace, size_t workspace_bytes, void *stream);
 
-/* Bytes of device workspace bdgdn_bwd_train needs, per (block, v-head): the recomputed
+/* Bytes of device workspace bdgdn_bwd_train needs.  Block-form shapes (bf16 inputs,
+ * d_k = d_v = 128, blocks of at most 32 positions), per (block, v-head): the recomputed
  * clean seed state (fp16), the part of the clean state gradient at the block's start that
- * does not depend on the gradient at its end (fp16), the gradient at its end (fp16), the
- * block's U K (32 x d_k fp16) and gamma_n; plus 2.3 KB for the range pass; 0 for a
- * descriptor it would reject. */
+ * does not depend on the gradient at its end (fp16; overwritten by the gradient at the
+ * block's end once the reverse scan has read it), the block's U K (32 x d_k fp16) and
+ * gamma_n; plus 2.3 KB for the range pass.  Per-step shapes: the clean state before every
+ * eighth block of every chain (fp32) and eight block-start states per (chain, 16-column
+ * tile) (fp32).  0 for a descriptor it would reject. */
 size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
 
 /*
@@ -246,10 +249,15 @@ size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
  *   dh0                  [B or N][h_v][d_k][d_v] fp32 gradient of h0, or NULL
  *   workspace            at least bdgdn_bwd_train_workspace(desc) bytes, 256-byte aligned,
  *                        owned by the call until the stream passes it
- * Every gradient row is overwritten.  Available for bf16 inputs with d_k = d_v = 128 and
- * blocks of at most 32 positions (else BDGDN_ERR_UNSUPPORTED).  With grouped value heads
- * (h_v > h_qk) dq, dk, dqn, dkn are summed with floating-point atomics (summation order
- * not fixed); otherwise every result is deterministic.
+ * Every gradient row is overwritten.  bf16 inputs with d_k = d_v = 128 and blocks of at
+ * most 32 positions run the block-form kernels; fp32 inputs (blocks of at most 32), d_k or
+ * d_v of 64, and bf16 blocks of 33 .. 64 positions run the per-step fp32 backward (one
+ * wave per (chain, 16-column tile) walking the steps backwards from strided clean
+ * checkpoints; at most 512 packed documents and four views); anything else is
+ * BDGDN_ERR_UNSUPPORTED.  With grouped value heads (h_v > h_qk) dq, dk, dqn, dkn of the
+ * block-form kernels are summed with floating-point atomics (summation order not fixed);
+ * otherwise their results are deterministic.  The per-step backward sums dq, dk, dg and
+ * dbeta over its column tiles with floating-point atomics (summation order not fixed).
  * Range: do, don and the state gradients enter the products as fp16 operands.  Every result
  * is linear in do, don and dht, so the call first finds the largest |entry| of do, don (of
  * every view) and dht on the device, multiplies them by the power of two sigma that puts it

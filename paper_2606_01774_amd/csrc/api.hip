@@ -605,12 +605,12 @@ static bool bwd_shape_ok(const bdgdn_fwd_desc_t *d)
 }
 
 // Workspace of the backward, per (global block, v-head): the seed state (fp16), the part of
-// the state gradient at the block's start that does not depend on dh (fp16, tile-native),
-// dh at the block's end (fp16, tile-native: the clean block kernel uses it as fp16 operands
-// only), U K (32 x d_k, fp16), gamma_n (fp32); then the range pass's per-block maxima and
-// {sigma, 1 / sigma}.  Byte offsets, each aligned to 256.
+// the state gradient at the block's start that does not depend on dh (fp16, tile-native;
+// the reverse scan overwrites it with dh at the block's end, which the clean block kernel
+// uses as fp16 operands only), U K (32 x d_k, fp16), gamma_n (fp32); then the range pass's
+// per-block maxima and {sigma, 1 / sigma}.  Byte offsets, each aligned to 256.
 struct BwdLayout {
-    size_t seeds, cterm, dh, uk, gnb, part, range, total;
+    size_t seeds, cterm, uk, gnb, part, range, total;
 };
 static BwdLayout bwd_layout(const bdgdn_fwd_desc_t *d)
 {
@@ -619,8 +619,7 @@ static BwdLayout bwd_layout(const bdgdn_fwd_desc_t *d)
     BwdLayout l;
     l.seeds = 0;
     l.cterm = l.seeds + up(units * st * 2);
-    l.dh = l.cterm + up(units * st * 2);
-    l.uk = l.dh + up(units * st * 2);
+    l.uk = l.cterm + up(units * st * 2);
     l.gnb = l.uk + up(units * 32 * d->d_k * 2);
     l.part = l.gnb + up(units * 4);
     l.range = l.part + up(kRangeBlocks * 4);
@@ -742,7 +741,7 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     a.dqn = dqn; a.dkn = dkn; a.dvn = dvn; a.dgn = dgn; a.dbn = dbetan;
     a.dh0 = dh0;
     a.cterm = reinterpret_cast<_Float16 *>(ws + lay.cterm);
-    a.dh = reinterpret_cast<_Float16 *>(ws + lay.dh);
+    a.dh = a.cterm;   // the scan writes dh_b over cterm_b once it has read it
     a.uk = reinterpret_cast<_Float16 *>(ws + lay.uk);
     a.gnb = reinterpret_cast<float *>(ws + lay.gnb);
     a.cu = sa.cu;

@@ -27,7 +27,8 @@ struct BwdArgs {
     _Float16 *uk;                            // [global block][h_v][32][128]: U K of each clean block
     float *gnb;                              // [global block][h_v]: gamma_n of each clean block
     _Float16 *dh;                            // [global block][h_v][64 tiles][64 lanes][4]: gradient at
-                                             // block ends (fp16, tile-native like cterm)
+                                             // block ends (fp16, tile-native like cterm; may be cterm
+                                             // itself: the scan reads cterm_b before writing dh_b)
     const float *range;                      // {sigma, 1 / sigma}: the upstream gradients enter the
                                              // fp16 operands times sigma, the fp32 results are
                                              // divided by it (launch_bwd_range writes them)

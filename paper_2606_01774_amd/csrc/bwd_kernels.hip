@@ -925,7 +925,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
 // independent):
 //   dh_(b-1) = gamma_n dh_b + cterm_b - K^T Z,  Z = (U K) dh_b  (32 x TC),
 // writing dh_b (the gradient at the end of block b; fp16, the precision phase 3 uses it in,
-// tile-native like cterm) for phase 3, and dh0 (fp32).  The operands of block b - 2 (U K, K, cterm, gamma_n) are
+// tile-native) over cterm_b, which only this scan reads, for phase 3, and dh0 (fp32).  The operands of block b - 2 (U K, K, cterm, gamma_n) are
 // loaded into registers while block b is computed.
 namespace {
 constexpr int LDK = NP + 8;   // f16 row stride of [*][32] tiles
@@ -1031,17 +1031,19 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
     const f32x4 z = {0.f, 0.f, 0.f, 0.f};
     auto step = [&](int b, const Ops &cur, Ops &nxt) {
         const int buf = b & 1;
-        _Float16 *dhb = a.dh + ((size_t)(gb0 + b) * a.h_v + h) * SS;
-        // publish dh_b; stage dh_b^T, U K, K^T of block b; every use of cur comes before the
-        // loads of block b - 2 are issued, so that no wait for cur can also wait for those
+        // dh_b goes to block b's cterm slot (tile-native, fp16), which this lane read two
+        // steps earlier: the store is issued after that value's use below
+        f16x4 *dhb = reinterpret_cast<f16x4 *>(a.dh + ((size_t)(gb0 + b) * a.h_v + h) * SS) + lane;
+        f16x4 hv[RT][CT];
+        // stage dh_b^T, U K, K^T of block b; every use of cur comes before the loads of block
+        // b - 2 are issued, so that no wait for cur can also wait for those
 #pragma unroll
         for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
             for (int tn = 0; tn < CT; ++tn) {
                 const int r = rw + 16 * tl + 4 * g4, c = 16 * tn + rr;
-                const f16x4 hv = {(_Float16)dh[tl][tn][0], (_Float16)dh[tl][tn][1], (_Float16)dh[tl][tn][2],
-                                  (_Float16)dh[tl][tn][3]};
-                reinterpret_cast<f16x4 *>(dhb)[((rw / 16 + tl) * 8 + v0 / 16 + tn) * 64 + lane] = hv;   // tile-native
+                hv[tl][tn] = f16x4{(_Float16)dh[tl][tn][0], (_Float16)dh[tl][tn][1], (_Float16)dh[tl][tn][2],
+                                   (_Float16)dh[tl][tn][3]};
                 st4(sm.dHt + c * LDH + r, dh[tl][tn][0], dh[tl][tn][1], dh[tl][tn][2], dh[tl][tn][3]);
             }
 #pragma unroll
@@ -1057,6 +1059,10 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
             for (int tn = 0; tn < CT; ++tn)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) dh[tl][tn][j] = cur.gn * dh[tl][tn][j] + (float)cur.cs[tl][tn][j];
+#pragma unroll
+        for (int tl = 0; tl < RT; ++tl)
+#pragma unroll
+            for (int tn = 0; tn < CT; ++tn) dhb[((rw / 16 + tl) * 8 + v0 / 16 + tn) * 64] = hv[tl][tn];
         if (b > 1) fetch(b - 2, nxt);
         __syncthreads();
         {   // Z = (U K) dh_b: one 16 x 16 tile per wave (2 CT tiles over NW = 2 CT waves), stored transposed
