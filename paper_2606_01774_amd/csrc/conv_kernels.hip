@@ -490,14 +490,23 @@ __global__ void __launch_bounds__(256) bdgdn_shortconv_bwd_kernel(ConvArgs a)
     }
 }
 
-// dw, dbias: the workgroups' partials summed in group order; one thread per (slot, channel).
+// dw, dbias: the workgroups' partials summed in a fixed order (eight interleaved running
+// sums, so that eight loads are in flight, then added pairwise); one thread per (slot,
+// channel).
 template <int W>
 __global__ void __launch_bounds__(256) bdgdn_shortconv_reduce_kernel(ConvArgs a)
 {
     const int e = blockIdx.x * 256 + threadIdx.x;
     if (e >= (W + 1) * a.D) return;
-    float acc = 0.f;
-    for (int g = 0; g < a.n_rg; ++g) acc += a.part[(long)g * (W + 1) * a.D + e];
+    const long stride = (long)(W + 1) * a.D;
+    const float *p = a.part + e;
+    float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    int g = 0;
+    for (; g + 8 <= a.n_rg; g += 8)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s[u] += p[(g + u) * stride];
+    for (int u = 0; g < a.n_rg; ++g, ++u) s[u] += p[g * stride];
+    const float acc = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
     const int i = e / a.D, c = e % a.D;
     if (i < W)
         a.dw[c * W + i] = acc;
