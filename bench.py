@@ -649,9 +649,12 @@ def main():
             "views2_ms_per_call": bvms, "views2_tokens_per_s": 3 * w.tokens / (bvms * 1e-3)}
         del bws, bgrads, bvgrads, bviews
         torch.cuda.empty_cache()
-        # the per-step fp32 backward of the shapes outside the block-form kernels: the tiny
-        # fp32 workload and the grouped-value workload with its blocks of 64 positions
+        # the other training workloads: the tiny fp32 one (the per-step fp32 backward) and the
+        # grouped-value one (blocks of 64: the block form with noisy blocks of two sub-blocks)
         per_step = {}
+        paths = {"c0": ("bdgdn_bwd_gen_ckpt_kernel + bdgdn_bwd_gen_walk_kernel (fp32, per step)", 1, 3, 1),
+                 "c2": ("bdgdn_k2_scan_states_kernel (seed states per 32-position sub-block) + "
+                        "bdgdn_bwd_pair_kernel + bdgdn_bwd_scan_kernel + bdgdn_bwd_clean_kernel", 3, 10, 3)}
         for key, pw in (("c0", W.TINY_F32), ("c2", W.GVA_16K)):
             pin = {k_: v_.to(dev) for k_, v_ in W.make_train(pw).items()}
             pshape = (pw.batch, pw.seqlen, pw.h_v, pw.d_v)
@@ -666,13 +669,14 @@ def main():
             def pstep():
                 bd.bdgdn_bwd_train(*pargs, pdo, pdon, block=pw.block, scale=pscale, workspace=pws, grads=pgrads,
                                    stream=stream)
-            pms = time_protocol(pstep, stream, flush, warmup=1, iters=3, repeats=1, trim=0)[0]
+            kern, pwarm, piters, prep = paths[key]
+            pms = time_protocol(pstep, stream, flush, warmup=pwarm, iters=piters, repeats=prep,
+                                trim=1 if piters >= 10 else 0)[0]
             per_step[key] = {"workload": pw.name, "ms_per_call": pms, "tokens_per_s": pw.tokens / (pms * 1e-3),
-                             "workspace_bytes": pws.numel(),
-                             "kernels": "bdgdn_bwd_gen_ckpt_kernel + bdgdn_bwd_gen_walk_kernel (fp32, per step)"}
+                             "workspace_bytes": pws.numel(), "kernels": kern}
             del pin, pws, pgrads
             torch.cuda.empty_cache()
-        result["backward"]["per_step"] = per_step
+        result["backward"]["other_workloads"] = per_step
 
     if "shortconv" in only:
         # the GDN layer's two-stream ShortConv at the same token shape (channels = the q, k

@@ -599,9 +599,21 @@ int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc, const void *q, const voi
     return BDGDN_OK;
 }
 
+// The block-form backward: bf16 inputs, d_k = d_v = 128, blocks of at most 32 positions, or
+// of an even 34 .. 64 (noisy blocks of two sub-blocks, the clean stream in sub-blocks of half
+// the block).
 static bool bwd_shape_ok(const bdgdn_fwd_desc_t *d)
 {
-    return d->dtype == BDGDN_BF16 && d->d_k == 128 && d->d_v == 128 && d->block <= 32;
+    return d->dtype == BDGDN_BF16 && d->d_k == 128 && d->d_v == 128 &&
+           (d->block <= 32 || (d->block <= 64 && d->block % 2 == 0));
+}
+static bool bwd_pairs(const bdgdn_fwd_desc_t *d) { return d->block > 32; }
+// The clean block of the block-form backward: the block, or half of it for pairs.
+static bdgdn_fwd_desc_t bwd_sub(const bdgdn_fwd_desc_t *d)
+{
+    bdgdn_fwd_desc_t s = *d;
+    if (bwd_pairs(d)) s.block = d->block / 2;
+    return s;
 }
 
 // Workspace of the backward, per (global block, v-head): the seed state (fp16), the part of
@@ -615,7 +627,8 @@ struct BwdLayout {
 static BwdLayout bwd_layout(const bdgdn_fwd_desc_t *d)
 {
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    const size_t units = (size_t)total_blocks(d) * d->h_v, st = (size_t)d->d_k * d->d_v;
+    const bdgdn_fwd_desc_t sub = bwd_sub(d);
+    const size_t units = (size_t)total_blocks(&sub) * d->h_v, st = (size_t)d->d_k * d->d_v;
     BwdLayout l;
     l.seeds = 0;
     l.cterm = l.seeds + up(units * st * 2);
@@ -704,6 +717,8 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     unsigned char *ws = static_cast<unsigned char *>(workspace);
     const BwdLayout lay = bwd_layout(desc);
     _Float16 *seeds = reinterpret_cast<_Float16 *>(ws + lay.seeds);
+    const bdgdn_fwd_desc_t sub = bwd_sub(desc);   // the clean blocks
+    const int Lc = sub.block;
     // 1. the clean scan from h0, writing the seed state of every block (fp16: the block
     // kernels stage it as fp16 MFMA operands)
     ScanArgs sa = {};
@@ -714,7 +729,7 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     sa.o = ws; sa.on = nullptr;   // never written: the states-only scan has no outputs
     sa.ws = nullptr;
     sa.bs = seeds;
-    sa.T = desc->seqlen; sa.L = desc->block; sa.nblk = (desc->seqlen + desc->block - 1) / desc->block;
+    sa.T = desc->seqlen; sa.L = Lc; sa.nblk = (desc->seqlen + Lc - 1) / Lc;
     sa.h_qk = desc->h_qk; sa.h_v = desc->h_v; sa.dv = desc->d_v;
     sa.n_chains = nseq * desc->h_v;
     sa.n_vt = desc->d_v / scan_tile_v();
@@ -729,7 +744,7 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         for (int i = 0; i < nseq; ++i) sa.order[i] = idx[i];
         sa.n_order = nseq;
     }
-    hipError_t e = launch_scan_states(lp_of(desc->block), false, true, sa, strm);
+    hipError_t e = launch_scan_states(lp_of(Lc), false, true, sa, strm);
     if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
     // 2. the reverse walk over the blocks of every (sequence, v-head)
     BwdArgs a = {};
@@ -747,7 +762,7 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     a.cu = sa.cu;
     a.n_docs = packed ? nseq : 0;
     a.n_chains = nseq * desc->h_v;
-    a.T = desc->seqlen; a.nblk = sa.nblk; a.L = desc->block;
+    a.T = desc->seqlen; a.nblk = sa.nblk; a.L = Lc;
     a.h_qk = desc->h_qk; a.h_v = desc->h_v;
     a.scale = desc->scale;
     a.atomic_qk = desc->h_v != desc->h_qk;
@@ -770,8 +785,8 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     a.range = ra.range;
     e = launch_bwd_range(desc->out_dtype == BDGDN_BF16, ra, strm);
     if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
-    e = launch_bwd(desc->out_dtype == BDGDN_BF16, a, more, n_more, nseq * desc->h_v, total_blocks(desc) * desc->h_v,
-                   rows * desc->h_qk * desc->d_k, strm);
+    e = launch_bwd(desc->out_dtype == BDGDN_BF16, a, more, n_more, nseq * desc->h_v, total_blocks(&sub) * desc->h_v,
+                   bwd_pairs(desc) ? total_blocks(desc) * desc->h_v : 0, rows * desc->h_qk * desc->d_k, strm);
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
 }
 

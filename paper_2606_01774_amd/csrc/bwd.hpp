@@ -89,8 +89,10 @@ bool bwd_generic_supported(bool f32_in, int dk, int dv, int L, int n_views);
 hipError_t launch_bwd_generic(bool f32_in, bool f32_out, const GenBwdCall &c, hipStream_t s);
 size_t bwd_block_lds();
 // The backward of a's two streams, plus n_more further noisy views seeded from the same clean
-// states (their seed gradients summed into the clean state gradient).
+// states (their seed gradients summed into the clean state gradient).  a.L is the clean
+// block; with n_pair_units > 0 every noisy block spans two clean blocks (n_pair_units =
+// noisy blocks x v-heads).
 hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int n_more, int n_chains,
-                      long n_block_units, long qk_elems, hipStream_t s);
+                      long n_block_units, long n_pair_units, long qk_elems, hipStream_t s);
 
 }  // namespace bdgdn

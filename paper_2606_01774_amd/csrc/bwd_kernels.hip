@@ -304,17 +304,27 @@ __device__ __forceinline__ BlockRows<Od, WITH_V> load_block(const StreamPtrs &p,
 
 }  // namespace
 
-// One block's gradients.  S0 (LDS f16) holds the seed.  For the clean stream dS (LDS, f16)
-// holds dS_n on entry; for the noisy stream dS_n is formed here from the block-end readout
-// and the seed's gradient dS0 is added into acc (registers, the C-tile layout of a state
+// What block_bwd differentiates: a clean block (per-position outputs, dS_n given), a noisy
+// block (every position reads the block-end state, dS_n = s Q^T dO formed here), or a block
+// with no outputs of its own whose dS_n is given (the sub-blocks of a noisy block of two,
+// whose readout gradient the caller has formed).
+enum class Mode { Clean, Noisy, Given };
+
+// One block's gradients.  S0 (LDS f16) holds the seed.  For Clean and Given dS (LDS, f16)
+// holds dS_n on entry; for Noisy dS_n is formed here from the block-end readout.  Noisy and
+// Given add the seed's gradient dS0 into acc (registers, the C-tile layout of a state
 // gradient: wave w holds column block w, row blocks 0 .. 7).  Wave w computes the 16 columns 16 w .. 16 w + 15 of every 32 x 128 and 128 x 128
 // product.  hook1() runs once the arrays R, dDl and dO are dead (after the dR / dQ phase),
 // hook2() two phases later: a persistent caller loads the next unit's clean rows in the one
 // and stages them into those arrays in the other.
-template <bool CLEAN, typename Od, typename H1, typename H2>
+template <Mode MODE, typename Od, typename H1, typename H2>
 __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, const BlockRows<Od, true> &in,
                           float (&acc)[8][4], int tid, const H1 &hook1, const H2 &hook2)
 {
+    constexpr bool CLEAN = MODE == Mode::Clean;     // per-position outputs
+    constexpr bool READOUT = MODE == Mode::Noisy;   // dS_n from the block-end readout
+    constexpr bool SEED = MODE != Mode::Clean;      // the seed's gradient into acc
+    constexpr bool DQ = MODE != Mode::Given;        // q gradients of the block's rows
     const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
     const float s = a.scale;
     const float inv = a.range[1];   // every gradient is linear in the scaled upstream gradients
@@ -376,7 +386,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
     f16x4 dsq[8];   // dS_n tiles (tm, w): the B operands of K dS_n
     {
         f16x4 dob[2];
-        if constexpr (!CLEAN) {
+        if constexpr (READOUT) {
             dob[0] = op_tr(sm.dO, LDH, 0, c0, lane);
             dob[1] = op_tr(sm.dO, LDH, 16, c0, lane);
         }
@@ -384,7 +394,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
 #pragma unroll
         for (int tm = 0; tm < 8; ++tm) {
             f32x4 c;
-            if constexpr (CLEAN) {   // dS_n tile (tm, w) from LDS by the transpose load
+            if constexpr (!READOUT) {   // dS_n tile (tm, w) from LDS by the transpose load
                 dsq[tm] = op_tr(sm.dS, LDH, 16 * tm, c0, lane);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) c[j] = (float)dsq[tm][j];
@@ -395,10 +405,8 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                if constexpr (!CLEAN) {
-                    sm.dS[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = dsq[tm][j];
-                    acc[tm][j] += gn * c[j];
-                }
+                if constexpr (READOUT) sm.dS[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = dsq[tm][j];
+                if constexpr (SEED) acc[tm][j] += gn * c[j];
                 wg += c[j] * (float)s0q[tm][j];
             }
         }
@@ -427,7 +435,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
     __syncthreads();
     // ---- E = dO Delta^T (waves 0 .. 3), with the gradient of Q K^T into dPh and (clean) the
     // gates of Mc, W = s E o P: dG_r += sum_i W_ri, dG_i -= sum_r W_ri
-    if (wave < 4) {
+    if (DQ && wave < 4) {
         const int m0 = 16 * (wave >> 1), n0 = 16 * (wave & 1), i = n0 + rr;
         const f32x4 e4 = tile_mma<_Float16, DD>(z, sm.dO + m0 * LDH, LDH, sm.Dl + n0 * LDH, LDH, lane);
         float colw = 0.f;
@@ -482,7 +490,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
     }
     __syncthreads();
     // ---- dR = T^T dDelta (= dV), kept as -Gamma dR (LDS and, as B operands, registers);
-    // [noisy] dS0 += K^T (-Gamma dR); dQ; dT = dDelta R^T (waves 4 .. 7)
+    // [noisy, given] dS0 += K^T (-Gamma dR); dQ; dT = dDelta R^T (waves 4 .. 7)
     f16x4 drq[2];
     {
         const f16x4 dd0 = op_tr(sm.dDl, LDH, 0, c0, lane), dd1 = op_tr(sm.dDl, LDH, 16, c0, lane);
@@ -503,7 +511,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
             for (int j = 0; j < 4; ++j) sm.dR[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = drq[tm][j];
         }
     }
-    if constexpr (!CLEAN) {
+    if constexpr (SEED) {
 #pragma unroll
         for (int tm = 0; tm < 8; ++tm) {
             const f32x4 c =
@@ -512,7 +520,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
             for (int j = 0; j < 4; ++j) acc[tm][j] += c[j];
         }
     }
-    {   // dQ = [clean] s Gamma (dO S0^T) + dPh K  |  [noisy] s gamma_n (dO S0^T) + dPh K
+    if constexpr (DQ) {   // dQ = [clean] s Gamma (dO S0^T) + dPh K  |  [noisy] s gamma_n (dO S0^T) + dPh K
         const f16x4 k0q = op_tr(sm.K, LDH, 0, c0, lane), k1q = op_tr(sm.K, LDH, 16, c0, lane);
 #pragma unroll
         for (int tm = 0; tm < 2; ++tm) {
@@ -662,6 +670,80 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
         if (lane < nvalid) {
             p.dg[(long)lane * a.h_v] = x * inv;
             p.db[(long)lane * a.h_v] = sm.dB[lane] * inv;
+        }
+    }
+    __syncthreads();
+}
+
+// The state after one block of nvalid positions (padded to 32) from the seed in S0 (LDS
+// f16): S_n = gamma_n S0 + K^T D Delta, Delta = T (V - Gamma K S0), into out (fp32, the C-tile
+// layout of a state: wave w holds column block w, row blocks 0 .. 7).  Stages K in K, V in R,
+// M in Mh, Delta in Dl and the gates; S0's writer must have passed a barrier before the call's
+// first one, and the call ends with a barrier, after which S0 may be rewritten.
+__device__ void block_fwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, float (&out)[8][4], int tid)
+{
+    const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    {
+        const Row8<__bf16> k = load_rows(p.k, (long)a.h_qk * DD, nvalid, tid);
+        const Row8<__bf16> v = load_rows(p.v, (long)a.h_v * DD, nvalid, tid);
+        const bool ok = tid < NP && tid < nvalid;
+        const float gx = ok ? p.g[(long)tid * a.h_v] : 0.f, bx = ok ? p.beta[(long)tid * a.h_v] : 0.f;
+        store_rows(sm.K, k, tid);
+        store_rows(sm.R, v, tid);
+        if (tid < NP) {
+            sm.bet[tid] = bx;
+            sm.G[tid] = gx;
+        }
+    }
+    __syncthreads();
+    if (wave == 0) cum_gates(sm, lane);
+    __syncthreads();
+    const float Gn = sm.G[NP - 1], gn = ex(Gn);
+    if (wave == 0) solve_m(sm, sm.K, lane);
+    f16x4 s0q[8];
+#pragma unroll
+    for (int tm = 0; tm < 8; ++tm) s0q[tm] = op_tr(sm.S0, LDH, 16 * tm, c0, lane);
+#pragma unroll
+    for (int tm = 0; tm < 2; ++tm) {   // R = V - Gamma K S0
+        f32x4 x = z;
+#pragma unroll
+        for (int kb = 0; kb < 8; ++kb) x = mfma(op_row(sm.K, LDH, 16 * tm, 16 * kb, lane), s0q[kb], x);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r = 16 * tm + 4 * g4 + j, c = c0 + rr;
+            sm.R[r * LDH + c] = (_Float16)((float)sm.R[r * LDH + c] - sm.gam[r] * x[j]);
+        }
+    }
+    __syncthreads();
+    {   // Delta = T R (T_ri = M_ri beta_i)
+        const f32x4 b0 = ld4(sm.bet + 4 * g4), b1 = ld4(sm.bet + 16 + 4 * g4);
+        const f16x4 r0 = op_tr(sm.R, LDH, 0, c0, lane), r1 = op_tr(sm.R, LDH, 16, c0, lane);
+#pragma unroll
+        for (int tm = 0; tm < 2; ++tm) {
+            const f16x4 t0 = scale4(op_row(sm.Mh, LDM, 16 * tm, 0, lane), b0);
+            const f16x4 t1 = scale4(op_row(sm.Mh, LDM, 16 * tm, 16, lane), b1);
+            const f32x4 d = mfma(t1, r1, mfma(t0, r0, z));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) sm.Dl[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = (_Float16)d[j];
+        }
+    }
+    __syncthreads();
+    {   // S_n = gamma_n S0 + K^T (D o Delta), the B operands D o Delta scaled per position
+        f32x4 d0, d1;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            d0[e] = ex(Gn - sm.G[4 * g4 + e]);
+            d1[e] = ex(Gn - sm.G[16 + 4 * g4 + e]);
+        }
+        const f16x4 b0 = scale4(op_tr(sm.Dl, LDH, 0, c0, lane), d0);
+        const f16x4 b1 = scale4(op_tr(sm.Dl, LDH, 16, c0, lane), d1);
+#pragma unroll
+        for (int tm = 0; tm < 8; ++tm) {
+            const f32x4 c =
+                mfma(op_tr(sm.K, LDH, 16, 16 * tm, lane), b1, mfma(op_tr(sm.K, LDH, 0, 16 * tm, lane), b0, z));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) out[tm][j] = gn * (float)s0q[tm][j] + c[j];
         }
     }
     __syncthreads();
@@ -861,7 +943,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
         if constexpr (PREP) clean_prep(sm, a, cg, cb, acc, a.uk + u * NP * DD, a.gnb + u, tid);
         store_seed(sm.S0, seed, tid);   // made visible by block_bwd's first barrier
         BlockRows<Od, false> nxt;
-        block_bwd<false, Od>(
+        block_bwd<Mode::Noisy, Od>(
             sm, pn, a, nvalid, nin, acc, tid,
             [&] {
                 if (PREP && more) {
@@ -896,6 +978,175 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
     }
 }
 
+// Phase 1 for noisy blocks of two sub-blocks (blocks of 2 L positions, L = a.L <= 32, the
+// clean stream cut into sub-blocks of L): one workgroup per (block, v-head).  The noisy block
+// runs from the clean seed S0 of its first sub-block a through its two halves,
+// S~1 = f_a(S0) and S~2 = f_b(S~1), and every position of both halves reads S~2, so that
+//   dQ = s dO S~2^T (both halves' rows),  dS~2 = s (Q_a^T dO_a + Q_b^T dO_b);
+// half b is then differentiated from S~1 with dS_n = dS~2 (Mode::Given: it has no outputs of
+// its own), which gives its gradients and dS~1, and half a from S0 with dS_n = dS~1, which
+// gives its gradients and the seed's gradient dS0.  With PREP, dS0 and the dh-independent
+// term of clean sub-block a (clean_prep) are written together to cterm of a, and clean
+// sub-block b's term to cterm of b; without PREP (a further view) dS0 is added to cterm of a.
+template <typename Od, bool PREP>
+__global__ void __launch_bounds__(512) bdgdn_bwd_pair_kernel(BwdArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    Smem &sm = *reinterpret_cast<Smem *>(smem_raw);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
+    const int h = (int)(blockIdx.x % a.h_v), hq = h / (a.h_v / a.h_qk);
+    const long m = blockIdx.x / a.h_v;   // the block of 2 L positions
+    const int L2 = 2 * a.L;
+    long p0, ga;   // its first row; the global index of its first sub-block
+    int nv;        // its rows
+    if (a.cu) {
+        p0 = m * L2;   // documents start on block boundaries
+        int lo = 0, hi = a.n_docs;   // the last document with cu[d] <= p0
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (a.cu[mid] <= p0)
+                lo = mid;
+            else
+                hi = mid;
+        }
+        const long rem = a.cu[lo + 1] - p0;
+        nv = (int)(rem < L2 ? rem : L2);
+        ga = p0 / a.L;
+    } else {
+        const long nb2 = (a.T + L2 - 1) / L2;
+        const int n = (int)(m / nb2), b = (int)(m % nb2);
+        p0 = (long)n * a.T + (long)b * L2;
+        const int rem = a.T - b * L2;
+        nv = rem < L2 ? rem : L2;
+        ga = (long)n * a.nblk + 2 * b;
+    }
+    const int nva = nv < a.L ? nv : a.L, nvb = nv - nva;   // rows of the halves (nvb may be 0)
+    const long ua = ga * a.h_v + h, ub = ua + a.h_v;
+    const StreamPtrs pa = stream_ptrs<Od>(a, true, p0, h, hq), pb = stream_ptrs<Od>(a, true, p0 + a.L, h, hq);
+    const long qks = (long)a.h_qk * DD, vs = (long)a.h_v * DD;
+    const float s = a.scale, inv = a.range[1];
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    float st[8][4];   // a state in the C-tile layout
+    // S~1 = f_a(S0) into S0; S~2 = f_b(S~1) into dS
+    store_seed(sm.S0, load_seed(a.seeds + (size_t)ua * DD * DD, tid), tid);
+    __syncthreads();
+    block_fwd(sm, pa, a, nva, st, tid);
+#pragma unroll
+    for (int tm = 0; tm < 8; ++tm)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sm.S0[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = (_Float16)st[tm][j];
+    __syncthreads();
+    block_fwd(sm, pb, a, nvb, st, tid);
+#pragma unroll
+    for (int tm = 0; tm < 8; ++tm)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sm.dS[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = (_Float16)st[tm][j];
+    // the halves' q and do rows: Q_a in Q, dO_a in dO, Q_b in dR, dO_b in dDl
+    store_rows(sm.Q, load_rows(pa.q, qks, nva, tid), tid);
+    store_rows(sm.dO, load_rows(static_cast<const Od *>(pa.dout), vs, nva, tid), tid, a.range[0]);
+    store_rows(sm.dR, load_rows(pb.q, qks, nvb, tid), tid);
+    store_rows(sm.dDl, load_rows(static_cast<const Od *>(pb.dout), vs, nvb, tid), tid, a.range[0]);
+    __syncthreads();
+    // dQ = s dO S~2^T for the rows of both halves
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+        const _Float16 *dOx = x ? sm.dDl : sm.dO;
+        const StreamPtrs &px = x ? pb : pa;
+        const int nvx = x ? nvb : nva;
+#pragma unroll
+        for (int tm = 0; tm < 2; ++tm) {
+            const f32x4 c = tile_mma<_Float16, DD>(z, dOx + 16 * tm * LDH, LDH, sm.dS + c0 * LDH, LDH, lane);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = 16 * tm + 4 * g4 + j;
+                if (r < nvx) {
+                    float *dst = px.dq + (long)r * qks + c0 + rr;
+                    if (a.atomic_qk)
+                        atomicAdd(dst, s * c[j] * inv);
+                    else
+                        *dst = s * c[j] * inv;
+                }
+            }
+        }
+    }
+    // dS~2 = s (Q_a^T dO_a + Q_b^T dO_b), written over S~2 once every read of it is done
+    f16x4 ds[8];
+    {
+        const f16x4 da0 = op_tr(sm.dO, LDH, 0, c0, lane), da1 = op_tr(sm.dO, LDH, 16, c0, lane);
+        const f16x4 db0 = op_tr(sm.dDl, LDH, 0, c0, lane), db1 = op_tr(sm.dDl, LDH, 16, c0, lane);
+#pragma unroll
+        for (int tm = 0; tm < 8; ++tm) {
+            f32x4 c = mfma(op_tr(sm.Q, LDH, 0, 16 * tm, lane), da0, z);
+            c = mfma(op_tr(sm.Q, LDH, 16, 16 * tm, lane), da1, c);
+            c = mfma(op_tr(sm.dR, LDH, 0, 16 * tm, lane), db0, c);
+            c = mfma(op_tr(sm.dR, LDH, 16, 16 * tm, lane), db1, c);
+            ds[tm] = h4(c * s);
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int tm = 0; tm < 8; ++tm)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sm.dS[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = ds[tm][j];
+    // half b from S~1 (S0) with dS_n = dS~2 (dS): its gradients, and dS~1 into acc
+    float acc[8][4];
+#pragma unroll
+    for (int tm = 0; tm < 8; ++tm)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[tm][j] = 0.f;
+    block_bwd<Mode::Given, Od>(sm, pb, a, nvb, load_block<Od, true>(pb, a.h_qk, a.h_v, nvb, tid), acc, tid, [] {},
+                               [] {});
+    // half a from the clean seed with dS_n = dS~1: its gradients, and dS0 into acc
+#pragma unroll
+    for (int tm = 0; tm < 8; ++tm)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            sm.dS[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = (_Float16)acc[tm][j];
+            acc[tm][j] = 0.f;
+        }
+    store_seed(sm.S0, load_seed(a.seeds + (size_t)ua * DD * DD, tid), tid);
+    block_bwd<Mode::Given, Od>(sm, pa, a, nva, load_block<Od, true>(pa, a.h_qk, a.h_v, nva, tid), acc, tid, [] {},
+                               [] {});
+    if constexpr (PREP) {
+        // clean sub-blocks a and b: their dh-independent terms (a's together with dS0)
+#pragma unroll 1
+        for (int x = 0; x < 2; ++x) {
+            if (x == 1 && nvb <= 0) break;   // a partial last block without a second sub-block
+            const long ux = x ? ub : ua;
+            const int nvx = x ? nvb : nva;
+            const BlockRows<Od, false> cin = load_block<Od, false>(stream_ptrs<Od>(a, false, p0 + x * a.L, h, hq),
+                                                                   a.h_qk, a.h_v, nvx, tid);
+            store_rows(sm.R, cin.q, tid);
+            store_rows(sm.dDl, cin.k, tid);
+            store_rows(sm.dO, cin.dout, tid, a.range[0]);
+            if (x == 1) {
+#pragma unroll
+                for (int tm = 0; tm < 8; ++tm)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[tm][j] = 0.f;
+            }
+            clean_prep(sm, a, cin.g, cin.b, acc, a.uk + ux * NP * DD, a.gnb + ux, tid);
+            f16x4 *dst = reinterpret_cast<f16x4 *>(a.cterm + (size_t)ux * DD * DD) + wave * 64 + lane;
+#pragma unroll
+            for (int tm = 0; tm < 8; ++tm) {
+                f16x4 v;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) v[j] = (_Float16)acc[tm][j];
+                dst[tm * 8 * 64] = v;
+            }
+        }
+    } else {
+        f16x4 *dst = reinterpret_cast<f16x4 *>(a.cterm + (size_t)ua * DD * DD) + wave * 64 + lane;
+#pragma unroll
+        for (int tm = 0; tm < 8; ++tm) {
+            f16x4 v = dst[tm * 8 * 64];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = (_Float16)((float)v[j] + acc[tm][j]);
+            dst[tm * 8 * 64] = v;
+        }
+    }
+}
+
 // Phase 3: every clean block, in parallel, from its seed and the gradient at its end (dh,
 // written by the scan).
 template <typename Od>
@@ -917,7 +1168,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
     store_seed(sm.S0, seed, tid);
     store_tiles(sm.dS, dh, tid);
     float no_acc[8][4] = {};   // the clean stream forms no dS0
-    block_bwd<true, Od>(sm, pc, a, nvalid, in, no_acc, tid, [] {}, [] {});   // its first barrier covers S0, dS
+    block_bwd<Mode::Clean, Od>(sm, pc, a, nvalid, in, no_acc, tid, [] {}, [] {});   // its first barrier covers S0, dS
 }
 
 // Phase 2: the reverse scan of the clean state gradient over the blocks of a (sequence,
@@ -1198,7 +1449,7 @@ __global__ void __launch_bounds__(256) bdgdn_bwd_zero_kernel(float *p, long n)
 size_t bwd_block_lds() { return sizeof(Smem); }
 
 hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int n_more, int n_chains,
-                      long n_block_units, long qk_elems, hipStream_t s)
+                      long n_block_units, long n_pair_units, long qk_elems, hipStream_t s)
 {
     if (n_more < 0 || (n_more > 0 && !more)) return hipErrorInvalidValue;
     // the noisy stream of a: its pointers replaced by those of view i
@@ -1228,14 +1479,23 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int 
     const unsigned pgrid = (unsigned)(n_block_units < n_cu ? n_block_units : (n_cu > 0 ? n_cu : 1));
     BwdArgs a2 = a;
     a2.n_units = n_block_units;
-    auto run = [&](auto noisy, auto noisy_more, auto clean) {
+    auto run = [&](auto noisy, auto noisy_more, auto pair, auto pair_more, auto clean) {
         for (const void *f : {reinterpret_cast<const void *>(noisy), reinterpret_cast<const void *>(noisy_more),
+                              reinterpret_cast<const void *>(pair), reinterpret_cast<const void *>(pair_more),
                               reinterpret_cast<const void *>(clean)}) {
             const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(Smem));
             if (e != hipSuccess) return e;
         }
         hipError_t e;
-        if (n_block_units > 0) {
+        if (n_pair_units > 0) {   // noisy blocks of two sub-blocks: one workgroup per (block, v-head)
+            hipLaunchKernelGGL(pair, dim3((unsigned)n_pair_units), dim3(512), sizeof(Smem), s, a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            for (int i = 0; i < n_more; ++i) {   // in stream order: each adds its seed gradients
+                hipLaunchKernelGGL(pair_more, dim3((unsigned)n_pair_units), dim3(512), sizeof(Smem), s,
+                                   with_view(more[i]));
+                if ((e = hipGetLastError()) != hipSuccess) return e;
+            }
+        } else if (n_block_units > 0) {
             hipLaunchKernelGGL(noisy, dim3(pgrid), dim3(512), sizeof(Smem), s, a2);
             if ((e = hipGetLastError()) != hipSuccess) return e;
             for (int i = 0; i < n_more; ++i) {   // in stream order: each adds its seed gradients
@@ -1254,8 +1514,10 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int 
         return hipSuccess;
     };
     return bf16_out ? run(bdgdn_bwd_noisy_kernel<__bf16, true>, bdgdn_bwd_noisy_kernel<__bf16, false>,
+                          bdgdn_bwd_pair_kernel<__bf16, true>, bdgdn_bwd_pair_kernel<__bf16, false>,
                           bdgdn_bwd_clean_kernel<__bf16>)
                     : run(bdgdn_bwd_noisy_kernel<float, true>, bdgdn_bwd_noisy_kernel<float, false>,
+                          bdgdn_bwd_pair_kernel<float, true>, bdgdn_bwd_pair_kernel<float, false>,
                           bdgdn_bwd_clean_kernel<float>);
 }
 

@@ -327,6 +327,12 @@ def test_bwd_train_validation_and_workspace():
     units = 2 * 4
     body = units * 128 * 128 * (2 + 2) + units * 32 * 128 * 2
     assert body <= need < body + 8 * 1024
+    # even blocks of 34 .. 64 positions: noisy blocks of two sub-blocks, the clean stream and
+    # the workspace in sub-blocks of half the block (here the same units as blocks of 32)
+    assert lib.bdgdn_bwd_train_workspace(ctypes.byref(_desc(block=64))) == need
+    need48 = lib.bdgdn_bwd_train_workspace(ctypes.byref(_desc(block=48)))   # 3 sub-blocks of 24
+    body48 = 3 * 4 * (128 * 128 * (2 + 2) + 32 * 128 * 2)
+    assert body48 <= need48 < body48 + 8 * 1024
     # the other shapes run the per-step backward: a clean state per eighth block start and
     # per chain (sequence, v-head), and per (chain, 16-column tile) eight block-start states
     f32 = _desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32)
@@ -334,7 +340,7 @@ def test_bwd_train_validation_and_workspace():
     gen_need = groups * 4 * 128 * 128 * 4 + 4 * 8 * 8 * 128 * 16 * 4
     assert lib.bdgdn_bwd_train_workspace(ctypes.byref(f32)) == gen_need
     for kw in (dict(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32), dict(d_k=64, d_v=64), dict(block=64),
-               dict(d_k=64), dict(block=48, out_dtype=bd.BDGDN_BF16)):
+               dict(d_k=64), dict(block=48, out_dtype=bd.BDGDN_BF16), dict(block=63)):
         d = _desc(**kw)
         assert lib.bdgdn_bwd_train_workspace(ctypes.byref(d)) > 0, kw
         assert _bwd(d) == bd.BDGDN_ERR_WORKSPACE, kw   # every check passes but the workspace
@@ -395,5 +401,6 @@ def test_bwd_views_validation():
     def call_many(desc, n):
         return lib.bdgdn_bwd_train_views(ctypes.byref(desc), P, P, P, P, P, many, n, None, None, None, P, None,
                                          P, P, P, P, P, None, None, 0, None)
-    assert call_many(_desc(block=64), 4) == bd.BDGDN_ERR_WORKSPACE
-    assert call_many(_desc(block=64), 5) == bd.BDGDN_ERR_UNSUPPORTED
+    assert call_many(_desc(block=63), 4) == bd.BDGDN_ERR_WORKSPACE
+    assert call_many(_desc(block=63), 5) == bd.BDGDN_ERR_UNSUPPORTED
+    assert call_many(_desc(block=64), 5) == bd.BDGDN_ERR_WORKSPACE   # block form: up to 16 views

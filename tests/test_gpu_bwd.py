@@ -61,15 +61,29 @@ def _check(B, T, hqk, hv, L, seed, **kw):
     (1, 96, 1, 1, 16, {"dtype": "f32", "d": 64}),                         # fp32 inputs
     (2, 100, 1, 2, 32, {"dtype": "f32", "d": 128, "h0": True, "dht": True}),
     (1, 70, 2, 2, 5, {"dtype": "f32", "d": 64, "lengths": [20, 0, 50]}),  # packed, an empty document
-    (1, 200, 1, 1, 64, {}),                                               # blocks of 64
-    (2, 150, 1, 2, 48, {"h0": True, "dht": True}),                        # blocks of 48, grouped heads
-    (1, 300, 2, 2, 64, {"lengths": [128, 64, 108]}),                      # packed, blocks of 64
+    (1, 200, 1, 1, 63, {}),                                               # odd blocks above 32
+    (2, 150, 1, 2, 33, {"h0": True, "dht": True}),                        # grouped heads
+    (1, 300, 2, 2, 63, {"lengths": [126, 63, 111]}),                      # packed, blocks of 63
     (1, 130, 1, 1, 32, {"d": 64, "do_dtype": torch.bfloat16}),            # d = 64, bf16 upstream gradients
 ])
 def test_bwd_per_step_path_matches_oracle(B, T, hqk, hv, L, kw):
-    """Shapes outside the block-form kernels (fp32 inputs, d = 64, blocks above 32 positions)
-    run the per-step fp32 backward; same contract and tolerance (fp32: 1e-4)."""
+    """Shapes outside the block-form kernels (fp32 inputs, d = 64, odd blocks above 32
+    positions) run the per-step fp32 backward; same contract and tolerance (fp32: 1e-4)."""
     _check(B, T, hqk, hv, L, 700 + T + L, **kw)
+
+
+@pytest.mark.parametrize("B,T,hqk,hv,L,kw", [
+    (1, 200, 1, 1, 64, {}),                                    # the last block without a second half
+    (2, 150, 1, 2, 48, {"h0": True, "dht": True}),             # blocks of 48, grouped heads
+    (1, 300, 2, 2, 64, {"lengths": [128, 64, 108]}),           # packed, a partial second half
+    (2, 100, 1, 1, 64, {"do_dtype": torch.bfloat16}),          # bf16 upstream gradients
+    (1, 262, 1, 1, 64, {"lengths": [64, 0, 128, 70], "h0": True, "dht": True}),   # an empty document
+    (1, 70, 1, 1, 40, {"dht": True}),                          # blocks of 40: halves of 20 and 10 rows
+])
+def test_bwd_pair_blocks_match_oracle(B, T, hqk, hv, L, kw):
+    """Even blocks of 34 .. 64 positions: the block-form backward with every noisy block as two
+    sub-blocks (the clean stream in sub-blocks of half the block)."""
+    _check(B, T, hqk, hv, L, 800 + T + L, **kw)
 
 
 def test_bwd_tiny_f32_full_config():
@@ -154,7 +168,7 @@ def test_bwd_grouped_heads_long_sequences_all_units():
 
 def test_bwd_grouped_value_workload_blocks_of_64_all_units():
     """The grouped-value workload as specified (2 x 16384 + 16384 tokens, 16 q/k heads shared
-    by 32 v heads, blocks of 64 positions), through the per-step backward; every unit of every
+    by 32 v heads, blocks of 64 positions: noisy blocks of two sub-blocks); every unit of every
     gradient compared with one oracle call."""
     w = W.GVA_16K
     _full_size_bwd(w.batch, w.seqlen, w.h_qk, w.h_v, w.block, W.make_train(w), 97)
@@ -168,6 +182,8 @@ KEYS = ("q", "k", "v", "g", "beta")
     (2, 100, 1, 2, 16, None, 3, torch.float32),              # grouped value heads, ragged tail
     (1, 160, 2, 2, 32, [64, 32, 64], 2, torch.float32),      # packed documents
     (1, 64, 1, 2, 8, None, 4, torch.bfloat16),               # bf16 upstream gradients, small blocks
+    (1, 200, 1, 2, 64, None, 2, torch.float32),              # blocks of 64: noisy blocks of two halves
+    (1, 256, 2, 2, 64, [128, 64, 64], 3, torch.float32),     # packed, blocks of 64
 ])
 def test_bwd_views_match_oracle(B, T, hqk, hv, L, lengths, n_views, do_dtype):
     """The complementary-view backward (bdgdn_bwd_train_views) against the oracle's
