@@ -41,7 +41,7 @@ namespace {
 // Tile shapes: rows per wave tile (forward), rows per thread and rows per prefetched chunk
 // (backward), bytes of channels per lane.
 constexpr int kFwdTN = 8, kFwdVB = 8;
-constexpr int kBwdTR = 64, kBwdU = 4, kBwdVB = 4;
+constexpr int kBwdTR = 128, kBwdU = 4, kBwdVB = 4;
 
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
@@ -344,7 +344,9 @@ __global__ void __launch_bounds__(256) bdgdn_shortconv_bwd_kernel(ConvArgs a)
         auto load_chunk = [&](int s0, T (&lx)[UW], T (&ln)[UW], T (&ly)[UW], T (&lyn)[UW]) {
 #pragma unroll
             for (int u = 0; u < UW; ++u) {
-                const int s = s0 + u < rows ? s0 + u : rows - 1;   // rows past the end are never used
+                // rows from the last reader on are never used: they re-read the last one (a
+                // cache hit) rather than fetch a row of the next range
+                const int s = s0 + u < s_end ? s0 + u : s_end - 1;
                 lx[u] = gx.ld(voff, (s - b0) * rb);
                 ln[u] = gxn.ld(voff, (s - b0) * rb);
                 ly[u] = gdy.ld(voff, (s - t0) * rb);
@@ -359,7 +361,9 @@ __global__ void __launch_bounds__(256) bdgdn_shortconv_bwd_kernel(ConvArgs a)
         auto chunk = [&](int s0, auto tail) {
             constexpr bool TAIL = decltype(tail)::value;
             T nx[UW], nn[UW], ny[UW], nyn[UW];
-            load_chunk(s0 + UW, nx, nn, ny, nyn);
+            // the next chunk, unless this is the last one (a tail chunk can be)
+            const bool next = !TAIL || s0 + UW < s_end;
+            if (next) load_chunk(s0 + UW, nx, nn, ny, nyn);
 #pragma unroll
             for (int u = 0; u < UW; ++u) {
                 const int s = s0 + u;
@@ -437,13 +441,14 @@ __global__ void __launch_bounds__(256) bdgdn_shortconv_bwd_kernel(ConvArgs a)
 #pragma unroll
                 for (int j = 0; j < N; ++j) ac[ds][j] = an[ds][j] = 0.f;
             }
+            if (next)
 #pragma unroll
-            for (int u = 0; u < UW; ++u) {
-                cx[u] = nx[u];
-                cn[u] = nn[u];
-                cy[u] = ny[u];
-                cyn[u] = nyn[u];
-            }
+                for (int u = 0; u < UW; ++u) {
+                    cx[u] = nx[u];
+                    cn[u] = nn[u];
+                    cy[u] = ny[u];
+                    cyn[u] = nyn[u];
+                }
         };
         int s0 = t0;
         for (; s0 + UW <= t1; s0 += UW) chunk(s0, std::false_type());
