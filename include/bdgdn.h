@@ -254,10 +254,10 @@ size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
  * d_v of 64, and bf16 blocks of 33 .. 64 positions run the per-step fp32 backward (one
  * wave per (chain, 16-column tile) walking the steps backwards from strided clean
  * checkpoints; at most 512 packed documents and four views); anything else is
- * BDGDN_ERR_UNSUPPORTED.  With grouped value heads (h_v > h_qk) dq, dk, dqn, dkn of the
- * block-form kernels are summed with floating-point atomics (summation order not fixed);
- * otherwise their results are deterministic.  The per-step backward sums dq, dk, dg and
- * dbeta over its column tiles with floating-point atomics (summation order not fixed).
+ * BDGDN_ERR_UNSUPPORTED.  The block-form kernels are deterministic, grouped value heads
+ * included (dq, dk of a q/k head summed over its v-heads in a fixed order).  The per-step
+ * backward sums dq, dk, dg and dbeta over its column tiles with floating-point atomics
+ * (summation order not fixed).
  * Range: do, don and the state gradients enter the products as fp16 operands.  Every result
  * is linear in do, don and dht, so the call first finds the largest |entry| of do, don (of
  * every view) and dht on the device, multiplies them by the power of two sigma that puts it

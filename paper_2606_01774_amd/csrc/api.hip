@@ -765,7 +765,6 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     a.T = desc->seqlen; a.nblk = sa.nblk; a.L = Lc;
     a.h_qk = desc->h_qk; a.h_v = desc->h_v;
     a.scale = desc->scale;
-    a.atomic_qk = desc->h_v != desc->h_qk;
     const long rows = (long)desc->batch * desc->seqlen;
     // the range of the upstream gradients: the power-of-two scale they enter the kernels with
     RangeArgs ra = {};
@@ -786,7 +785,7 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     e = launch_bwd_range(desc->out_dtype == BDGDN_BF16, ra, strm);
     if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
     e = launch_bwd(desc->out_dtype == BDGDN_BF16, a, more, n_more, nseq * desc->h_v, total_blocks(&sub) * desc->h_v,
-                   bwd_pairs(desc) ? total_blocks(desc) * desc->h_v : 0, rows * desc->h_qk * desc->d_k, strm);
+                   bwd_pairs(desc) ? total_blocks(desc) * desc->h_v : 0, strm);
     return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
 }
 

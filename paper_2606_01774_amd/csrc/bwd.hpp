@@ -10,8 +10,8 @@ namespace bdgdn {
 // Backward of the two-stream training forward (bwd_kernels.hip): from the seed states of
 // the split schedule's clean scan, the noisy blocks (with the state-gradient-independent part
 // of the clean blocks) in parallel, a reverse scan of the clean state gradient, the clean
-// blocks in parallel.  Gradients are fp32; dq, dk (per q/k head) are summed with
-// atomics when several v-heads share a q/k head (zeroed first by launch_bwd).
+// blocks in parallel.  Gradients are fp32; a workgroup runs the v-heads of a (block, q/k
+// head) in turn, storing dq, dk for the first and adding for the others (deterministic).
 struct BwdArgs {
     const void *q, *k, *v, *qn, *kn, *vn;   // bf16 [rows][heads][128]
     const float *g, *beta, *gn, *betan;      // [rows][h_v]
@@ -38,7 +38,6 @@ struct BwdArgs {
     long n_units;                            // global blocks x v-heads (set by launch_bwd)
     int T, nblk, L, h_qk, h_v;
     float scale;
-    bool atomic_qk;
 };
 // A further noisy view (the complementary-view backward): its inputs, the upstream gradient
 // of its readout and its gradients, laid out as the noisy stream of BwdArgs.
@@ -93,6 +92,6 @@ size_t bwd_block_lds();
 // block; with n_pair_units > 0 every noisy block spans two clean blocks (n_pair_units =
 // noisy blocks x v-heads).
 hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int n_more, int n_chains,
-                      long n_block_units, long n_pair_units, long qk_elems, hipStream_t s);
+                      long n_block_units, long n_pair_units, hipStream_t s);
 
 }  // namespace bdgdn

@@ -304,6 +304,17 @@ __device__ __forceinline__ BlockRows<Od, WITH_V> load_block(const StreamPtrs &p,
 
 }  // namespace
 
+// q/k gradient x into *dst: stored for the first v-head of a q/k head, added for the others
+// (a workgroup runs the v-heads of a q/k head one after the other, and the same thread
+// writes the same element for each, so the sum has a fixed order; see unit_of).
+__device__ __forceinline__ void put_qk(bool add, float *dst, float x)
+{
+    if (add)
+        *dst += x;
+    else
+        *dst = x;
+}
+
 // What block_bwd differentiates: a clean block (per-position outputs, dS_n given), a noisy
 // block (every position reads the block-end state, dS_n = s Q^T dO formed here), or a block
 // with no outputs of its own whose dS_n is given (the sub-blocks of a noisy block of two,
@@ -318,8 +329,8 @@ enum class Mode { Clean, Noisy, Given };
 // hook2() two phases later: a persistent caller loads the next unit's clean rows in the one
 // and stages them into those arrays in the other.
 template <Mode MODE, typename Od, typename H1, typename H2>
-__device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, const BlockRows<Od, true> &in,
-                          float (&acc)[8][4], int tid, const H1 &hook1, const H2 &hook2)
+__device__ __forceinline__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, const BlockRows<Od, true> &in,
+                          float (&acc)[8][4], int tid, bool add_qk, const H1 &hook1, const H2 &hook2)
 {
     constexpr bool CLEAN = MODE == Mode::Clean;     // per-position outputs
     constexpr bool READOUT = MODE == Mode::Noisy;   // dS_n from the block-end readout
@@ -540,13 +551,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int r = 16 * tm + 4 * g4 + j, col = c0 + rr;
-                if (r < nvalid) {
-                    float *dst = p.dq + (long)r * a.h_qk * DD + col;
-                    if (a.atomic_qk)
-                        atomicAdd(dst, c[j] * inv);
-                    else
-                        *dst = c[j] * inv;
-                }
+                if (r < nvalid) put_qk(add_qk, p.dq + (long)r * a.h_qk * DD + col, c[j] * inv);
             }
         }
     }
@@ -634,13 +639,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int r = 16 * tm + 4 * g4 + j, col = c0 + rr;
-                if (r < nvalid) {
-                    float *dst = p.dk + (long)r * a.h_qk * DD + col;
-                    if (a.atomic_qk)
-                        atomicAdd(dst, c[j] * inv);
-                    else
-                        *dst = c[j] * inv;
-                }
+                if (r < nvalid) put_qk(add_qk, p.dk + (long)r * a.h_qk * DD + col, c[j] * inv);
             }
         }
     }
@@ -680,7 +679,7 @@ __device__ void block_bwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
 // layout of a state: wave w holds column block w, row blocks 0 .. 7).  Stages K in K, V in R,
 // M in Mh, Delta in Dl and the gates; S0's writer must have passed a barrier before the call's
 // first one, and the call ends with a barrier, after which S0 may be rewritten.
-__device__ void block_fwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, float (&out)[8][4], int tid)
+__device__ __forceinline__ void block_fwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int nvalid, float (&out)[8][4], int tid)
 {
     const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
     const f32x4 z = {0.f, 0.f, 0.f, 0.f};
@@ -751,6 +750,22 @@ __device__ void block_fwd(Smem &sm, const StreamPtrs &p, const BwdArgs &a, int n
 
 namespace {
 
+// Unit t of the (block, v-head) units ordered so that the r = h_v / h_qk v-heads of a q/k
+// head (consecutive v-heads) are consecutive: t = ((gblk h_qk) + hq) r + i, v-head h = hq r + i.
+// Each workgroup runs the units of a (block, q/k head) one after the other, so that its dq, dk
+// rows are stored by the first (i = 0) and added to by the others: a fixed summation order,
+// no atomics, nothing to clear.  Returns the unit's index in the per-(block, v-head) arrays.
+__device__ __forceinline__ long unit_of(const BwdArgs &a, long t, long &gblk, int &h, int &hq, int &i)
+{
+    const int r = a.h_v / a.h_qk;
+    const long gi = t / r;
+    i = (int)(t % r);
+    gblk = gi / a.h_qk;
+    hq = (int)(gi % a.h_qk);
+    h = hq * r + i;
+    return gblk * a.h_v + h;
+}
+
 // The (sequence, first row, rows) of global block gblk: packed documents start on block
 // boundaries, so a block lies inside one document.
 __device__ __forceinline__ void block_unit(const BwdArgs &a, long gblk, int &n, long &p0, int &nvalid)
@@ -807,7 +822,7 @@ __device__ __forceinline__ StreamPtrs stream_ptrs(const BwdArgs &a, bool noisy, 
 // The clean rows are staged in R (q), dDl (k) and dO (do): the arrays block_bwd leaves dead
 // after its dR / dQ phase, so that a persistent workgroup stages the next unit's rows there
 // while it finishes the current one.  gx, bx: the gate and step size of position tid.
-__device__ void clean_prep(Smem &sm, const BwdArgs &a, float gx, float bx, float (&acc)[8][4], _Float16 *uk,
+__device__ __forceinline__ void clean_prep(Smem &sm, const BwdArgs &a, float gx, float bx, float (&acc)[8][4], _Float16 *uk,
                            float *gnb, int tid)
 {
     const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
@@ -904,14 +919,20 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     Smem &sm = *reinterpret_cast<Smem *>(smem_raw);
-    long u = blockIdx.x;
+    // workgroup w takes the (block, q/k head) groups w, w + gridDim.x, ..., each as its r
+    // consecutive units (unit_of)
+    const int r = a.h_v / a.h_qk;
+    long u = (long)blockIdx.x * r;
+    auto next_unit = [&](long t) { return (t + 1) % r ? t + 1 : t + 1 + (long)(gridDim.x - 1) * r; };
     float cg = 0.f, cb = 0.f;   // the clean gate and step size of position tid of unit u
     if constexpr (PREP) {
         const int tid = threadIdx.x;
         int n, nvalid;
         long p0;
-        const int h = (int)(u % a.h_v), hq = h / (a.h_v / a.h_qk);
-        block_unit(a, u / a.h_v, n, p0, nvalid);
+        long gb;
+        int h, hq, vi;
+        unit_of(a, u, gb, h, hq, vi);
+        block_unit(a, gb, n, p0, nvalid);
         const BlockRows<Od, false> cin =
             load_block<Od, false>(stream_ptrs<Od>(a, false, p0, h, hq), a.h_qk, a.h_v, nvalid, tid);
         store_rows(sm.R, cin.q, tid);
@@ -926,31 +947,35 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
         int tid = threadIdx.x;
         asm volatile("" : "+v"(tid));
         const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15;
-        const long un = u + gridDim.x;
+        const long un = next_unit(u);
         const bool more = un < a.n_units;
         int n, nvalid;
         long p0;
-        const int h = (int)(u % a.h_v), hq = h / (a.h_v / a.h_qk);
-        block_unit(a, u / a.h_v, n, p0, nvalid);
+        long gb;
+        int h, hq, vi;
+        const long uw = unit_of(a, u, gb, h, hq, vi);   // the unit's workspace index
+        block_unit(a, gb, n, p0, nvalid);
         const StreamPtrs pn = stream_ptrs<Od>(a, true, p0, h, hq);
-        const SeedRegs seed = load_seed(a.seeds + (size_t)u * DD * DD, tid);
+        const SeedRegs seed = load_seed(a.seeds + (size_t)uw * DD * DD, tid);
         const BlockRows<Od, true> nin = load_block<Od, true>(pn, a.h_qk, a.h_v, nvalid, tid);
         float acc[8][4];
 #pragma unroll
         for (int tm = 0; tm < 8; ++tm)
 #pragma unroll
             for (int j = 0; j < 4; ++j) acc[tm][j] = 0.f;
-        if constexpr (PREP) clean_prep(sm, a, cg, cb, acc, a.uk + u * NP * DD, a.gnb + u, tid);
+        if constexpr (PREP) clean_prep(sm, a, cg, cb, acc, a.uk + uw * NP * DD, a.gnb + uw, tid);
         store_seed(sm.S0, seed, tid);   // made visible by block_bwd's first barrier
         BlockRows<Od, false> nxt;
         block_bwd<Mode::Noisy, Od>(
-            sm, pn, a, nvalid, nin, acc, tid,
+            sm, pn, a, nvalid, nin, acc, tid, vi > 0,
             [&] {
                 if (PREP && more) {
                     int n2, nv2;
                     long q0;
-                    const int h2 = (int)(un % a.h_v), hq2 = h2 / (a.h_v / a.h_qk);
-                    block_unit(a, un / a.h_v, n2, q0, nv2);
+                    long gb2;
+                    int h2, hq2, vi2;
+                    unit_of(a, un, gb2, h2, hq2, vi2);
+                    block_unit(a, gb2, n2, q0, nv2);
                     nxt = load_block<Od, false>(stream_ptrs<Od>(a, false, q0, h2, hq2), a.h_qk, a.h_v, nv2, tid);
                 }
             },
@@ -963,7 +988,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
                     cb = nxt.b;
                 }
             });
-        f16x4 *dst = reinterpret_cast<f16x4 *>(a.cterm + (size_t)u * DD * DD) + wave * 64 + lane;
+        f16x4 *dst = reinterpret_cast<f16x4 *>(a.cterm + (size_t)uw * DD * DD) + wave * 64 + lane;
 #pragma unroll
         for (int tm = 0; tm < 8; ++tm) {
             f16x4 *p = dst + tm * 8 * 64;   // tile (tm, wave)
@@ -989,13 +1014,13 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_noisy_kernel(BwdArgs a)
 // term of clean sub-block a (clean_prep) are written together to cterm of a, and clean
 // sub-block b's term to cterm of b; without PREP (a further view) dS0 is added to cterm of a.
 template <typename Od, bool PREP>
-__global__ void __launch_bounds__(512) bdgdn_bwd_pair_kernel(BwdArgs a)
+__device__ __forceinline__ void pair_unit(Smem &sm, const BwdArgs &a, long t, int tid)
 {
-    extern __shared__ __align__(16) unsigned char smem_raw[];
-    Smem &sm = *reinterpret_cast<Smem *>(smem_raw);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
-    const int h = (int)(blockIdx.x % a.h_v), hq = h / (a.h_v / a.h_qk);
-    const long m = blockIdx.x / a.h_v;   // the block of 2 L positions
+    const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, rr = lane & 15, c0 = 16 * wave;
+    long m;   // the block of 2 L positions
+    int h, hq, vi;
+    unit_of(a, t, m, h, hq, vi);
+    const bool add_qk = vi > 0;
     const int L2 = 2 * a.L;
     long p0, ga;   // its first row; the global index of its first sub-block
     int nv;        // its rows
@@ -1036,6 +1061,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_pair_kernel(BwdArgs a)
 #pragma unroll
         for (int j = 0; j < 4; ++j) sm.S0[(16 * tm + 4 * g4 + j) * LDH + c0 + rr] = (_Float16)st[tm][j];
     __syncthreads();
+    asm volatile("" : "+v"(tid));   // lane-dependent addresses recomputed per phase, not kept live
     block_fwd(sm, pb, a, nvb, st, tid);
 #pragma unroll
     for (int tm = 0; tm < 8; ++tm)
@@ -1059,13 +1085,7 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_pair_kernel(BwdArgs a)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int r = 16 * tm + 4 * g4 + j;
-                if (r < nvx) {
-                    float *dst = px.dq + (long)r * qks + c0 + rr;
-                    if (a.atomic_qk)
-                        atomicAdd(dst, s * c[j] * inv);
-                    else
-                        *dst = s * c[j] * inv;
-                }
+                if (r < nvx) put_qk(add_qk, px.dq + (long)r * qks + c0 + rr, s * c[j] * inv);
             }
         }
     }
@@ -1094,7 +1114,8 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_pair_kernel(BwdArgs a)
     for (int tm = 0; tm < 8; ++tm)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[tm][j] = 0.f;
-    block_bwd<Mode::Given, Od>(sm, pb, a, nvb, load_block<Od, true>(pb, a.h_qk, a.h_v, nvb, tid), acc, tid, [] {},
+    asm volatile("" : "+v"(tid));
+    block_bwd<Mode::Given, Od>(sm, pb, a, nvb, load_block<Od, true>(pb, a.h_qk, a.h_v, nvb, tid), acc, tid, add_qk, [] {},
                                [] {});
     // half a from the clean seed with dS_n = dS~1: its gradients, and dS0 into acc
 #pragma unroll
@@ -1105,7 +1126,8 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_pair_kernel(BwdArgs a)
             acc[tm][j] = 0.f;
         }
     store_seed(sm.S0, load_seed(a.seeds + (size_t)ua * DD * DD, tid), tid);
-    block_bwd<Mode::Given, Od>(sm, pa, a, nva, load_block<Od, true>(pa, a.h_qk, a.h_v, nva, tid), acc, tid, [] {},
+    asm volatile("" : "+v"(tid));
+    block_bwd<Mode::Given, Od>(sm, pa, a, nva, load_block<Od, true>(pa, a.h_qk, a.h_v, nva, tid), acc, tid, add_qk, [] {},
                                [] {});
     if constexpr (PREP) {
         // clean sub-blocks a and b: their dh-independent terms (a's together with dS0)
@@ -1147,28 +1169,50 @@ __global__ void __launch_bounds__(512) bdgdn_bwd_pair_kernel(BwdArgs a)
     }
 }
 
+// One workgroup per (block, q/k head): the pair units of its v-heads in turn.
+template <typename Od, bool PREP>
+__global__ void __launch_bounds__(512) bdgdn_bwd_pair_kernel(BwdArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    Smem &sm = *reinterpret_cast<Smem *>(smem_raw);
+    const int r = a.h_v / a.h_qk;
+    for (int i = 0; i < r; ++i) {
+        // the thread index made opaque per unit, so that lane-dependent addresses are
+        // recomputed rather than hoisted out of the loop (where they would stay live)
+        int tid = threadIdx.x;
+        asm volatile("" : "+v"(tid));
+        pair_unit<Od, PREP>(sm, a, (long)blockIdx.x * r + i, tid);
+    }
+}
+
 // Phase 3: every clean block, in parallel, from its seed and the gradient at its end (dh,
-// written by the scan).
+// written by the scan); one workgroup per (block, q/k head).
 template <typename Od>
 __global__ void __launch_bounds__(512) bdgdn_bwd_clean_kernel(BwdArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     Smem &sm = *reinterpret_cast<Smem *>(smem_raw);
-    const int tid = threadIdx.x;
-    const long gblk = blockIdx.x / a.h_v;
-    const int h = blockIdx.x % a.h_v, hq = h / (a.h_v / a.h_qk);
-    int n, nvalid;
-    long p0;
-    block_unit(a, gblk, n, p0, nvalid);
-    const size_t so = ((size_t)gblk * a.h_v + h) * DD * DD;
-    const StreamPtrs pc = stream_ptrs<Od>(a, false, p0, h, hq);
-    const SeedRegs seed = load_seed(a.seeds + so, tid);
-    const SeedRegs dh = load_seed(a.dh + so, tid);   // fp16, tile-native
-    const BlockRows<Od, true> in = load_block<Od, true>(pc, a.h_qk, a.h_v, nvalid, tid);
-    store_seed(sm.S0, seed, tid);
-    store_tiles(sm.dS, dh, tid);
-    float no_acc[8][4] = {};   // the clean stream forms no dS0
-    block_bwd<Mode::Clean, Od>(sm, pc, a, nvalid, in, no_acc, tid, [] {}, [] {});   // its first barrier covers S0, dS
+    const int r = a.h_v / a.h_qk;
+    for (int i = 0; i < r; ++i) {   // the v-heads of this (block, q/k head) in turn
+        int tid = threadIdx.x;       // opaque per unit, as in the noisy kernel
+        asm volatile("" : "+v"(tid));
+        long gblk;
+        int h, hq, vi;
+        unit_of(a, (long)blockIdx.x * r + i, gblk, h, hq, vi);
+        int n, nvalid;
+        long p0;
+        block_unit(a, gblk, n, p0, nvalid);
+        const size_t so = ((size_t)gblk * a.h_v + h) * DD * DD;
+        const StreamPtrs pc = stream_ptrs<Od>(a, false, p0, h, hq);
+        const SeedRegs seed = load_seed(a.seeds + so, tid);
+        const SeedRegs dh = load_seed(a.dh + so, tid);   // fp16, tile-native
+        const BlockRows<Od, true> in = load_block<Od, true>(pc, a.h_qk, a.h_v, nvalid, tid);
+        store_seed(sm.S0, seed, tid);
+        store_tiles(sm.dS, dh, tid);
+        float no_acc[8][4] = {};   // the clean stream forms no dS0
+        // its first barrier covers S0, dS; its last one the next v-head's stores
+        block_bwd<Mode::Clean, Od>(sm, pc, a, nvalid, in, no_acc, tid, vi > 0, [] {}, [] {});
+    }
 }
 
 // Phase 2: the reverse scan of the clean state gradient over the blocks of a (sequence,
@@ -1441,44 +1485,30 @@ hipError_t launch_bwd_range(bool bf16_out, const RangeArgs &r, hipStream_t s)
     return hipGetLastError();
 }
 
-__global__ void __launch_bounds__(256) bdgdn_bwd_zero_kernel(float *p, long n)
-{
-    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256) p[i] = 0.f;
-}
-
 size_t bwd_block_lds() { return sizeof(Smem); }
 
 hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int n_more, int n_chains,
-                      long n_block_units, long n_pair_units, long qk_elems, hipStream_t s)
+                      long n_block_units, long n_pair_units, hipStream_t s)
 {
     if (n_more < 0 || (n_more > 0 && !more)) return hipErrorInvalidValue;
+    // one workgroup per (block, q/k head), running its r v-heads in turn (unit_of)
+    const int r = a.h_v / a.h_qk;
+    const long groups = n_block_units / r, pair_groups = n_pair_units / r;
+    BwdArgs a2 = a;
+    a2.n_units = n_block_units;
     // the noisy stream of a: its pointers replaced by those of view i
     auto with_view = [&](const BwdView &w) {
-        BwdArgs b = a;
-        b.n_units = n_block_units;
+        BwdArgs b = a2;
         b.qn = w.q; b.kn = w.k; b.vn = w.v; b.gn = w.g; b.betan = w.beta; b.doutn = w.dout;
         b.dqn = w.dq; b.dkn = w.dk; b.dvn = w.dv; b.dgn = w.dg; b.dbn = w.db;
         return b;
     };
-    auto zero = [&](float *p) {
-        hipLaunchKernelGGL(bdgdn_bwd_zero_kernel, dim3(1024), dim3(256), 0, s, p, qk_elems);
-        return hipGetLastError();
-    };
-    if (a.atomic_qk) {
-        for (float *p : {a.dq, a.dk, a.dqn, a.dkn})
-            if (hipError_t e = zero(p); e != hipSuccess) return e;
-        for (int i = 0; i < n_more; ++i)
-            for (float *p : {more[i].dq, more[i].dk})
-                if (hipError_t e = zero(p); e != hipSuccess) return e;
-    }
     // the persistent noisy kernels: one workgroup per CU (their LDS allows no more)
     int dev = 0, n_cu = 0;
     hipError_t err = hipGetDevice(&dev);
     if (err == hipSuccess) err = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
     if (err != hipSuccess) return err;
-    const unsigned pgrid = (unsigned)(n_block_units < n_cu ? n_block_units : (n_cu > 0 ? n_cu : 1));
-    BwdArgs a2 = a;
-    a2.n_units = n_block_units;
+    const unsigned pgrid = (unsigned)(groups < n_cu ? groups : (n_cu > 0 ? n_cu : 1));
     auto run = [&](auto noisy, auto noisy_more, auto pair, auto pair_more, auto clean) {
         for (const void *f : {reinterpret_cast<const void *>(noisy), reinterpret_cast<const void *>(noisy_more),
                               reinterpret_cast<const void *>(pair), reinterpret_cast<const void *>(pair_more),
@@ -1487,15 +1517,15 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int 
             if (e != hipSuccess) return e;
         }
         hipError_t e;
-        if (n_pair_units > 0) {   // noisy blocks of two sub-blocks: one workgroup per (block, v-head)
-            hipLaunchKernelGGL(pair, dim3((unsigned)n_pair_units), dim3(512), sizeof(Smem), s, a);
+        if (pair_groups > 0) {   // noisy blocks of two sub-blocks
+            hipLaunchKernelGGL(pair, dim3((unsigned)pair_groups), dim3(512), sizeof(Smem), s, a2);
             if ((e = hipGetLastError()) != hipSuccess) return e;
             for (int i = 0; i < n_more; ++i) {   // in stream order: each adds its seed gradients
-                hipLaunchKernelGGL(pair_more, dim3((unsigned)n_pair_units), dim3(512), sizeof(Smem), s,
+                hipLaunchKernelGGL(pair_more, dim3((unsigned)pair_groups), dim3(512), sizeof(Smem), s,
                                    with_view(more[i]));
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
-        } else if (n_block_units > 0) {
+        } else if (groups > 0) {
             hipLaunchKernelGGL(noisy, dim3(pgrid), dim3(512), sizeof(Smem), s, a2);
             if ((e = hipGetLastError()) != hipSuccess) return e;
             for (int i = 0; i < n_more; ++i) {   // in stream order: each adds its seed gradients
@@ -1507,8 +1537,8 @@ hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int 
         hipLaunchKernelGGL(bdgdn_bwd_scan_kernel<kScanWaves>, dim3((NT * n_chains + 8 * NT - 1) / (8 * NT) * 8 * NT),
                            dim3(64 * kScanWaves), 0, s, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        if (n_block_units > 0) {
-            hipLaunchKernelGGL(clean, dim3((unsigned)n_block_units), dim3(512), sizeof(Smem), s, a);
+        if (groups > 0) {
+            hipLaunchKernelGGL(clean, dim3((unsigned)groups), dim3(512), sizeof(Smem), s, a2);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
         return hipSuccess;

@@ -240,6 +240,21 @@ def test_bwd_one_view_equals_two_stream_backward():
         assert torch.equal(got_v[0][n], ref[n + "n"]), n
 
 
+@pytest.mark.parametrize("L", [32, 64])
+def test_bwd_grouped_heads_deterministic(L):
+    """Grouped value heads (four v heads per q/k head): the q/k gradients are summed over the
+    v heads in a fixed order, so two calls give the same bits."""
+    inp, do, don, h0, dht, cu = _case(1, 300, 2, 8, L, 11, h0=True, dht=True)
+    d = {k: v.cuda() for k, v in inp.items()}
+    print(f"bwd grouped heads twice, L={L}", flush=True)
+    args = [d[k] for k in ("q", "k", "v", "g", "beta", "qn", "kn", "vn", "gn", "betan")]
+    runs = [bd.bdgdn_bwd_train(*args, do.cuda(), don.cuda(), block=L, h0=h0.cuda(), dht=dht.cuda(), want_dh0=True)
+            for _ in range(2)]
+    torch.cuda.synchronize()
+    for n in NAMES + ("dh0",):
+        assert torch.equal(runs[0][n], runs[1][n]), n
+
+
 def test_bwd_power_of_two_loss_scaling():
     """Every gradient is linear in (do, don, dht), and the call scales them into the fp16
     operands' range by a power of two it finds on the device: scaling the upstream gradients
