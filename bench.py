@@ -38,7 +38,7 @@ ROUTES = {"fused": "fused (one kernel: per-block UT transform inside the state s
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, GB/s
 MFMA16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16/bf16 MFMA, TFLOP/s
 FLUSH_BYTES = 512 * 1024 * 1024
-SECTIONS = ("headline", "c0", "c1", "c1_bf16_out", "c2", "c3", "c4", "c4_bf16_out", "verify", "views", "backward",
+SECTIONS = ("headline", "tiny_f32", "train_4k", "train_4k_bf16_out", "gva_16k", "serve", "varlen_128k", "varlen_128k_bf16_out", "verify", "views", "backward",
             "shortconv", "cpu")
 
 
@@ -232,12 +232,12 @@ def traffic_targets():
     from paper_2606_01774_amd import workloads as W
     sw = W.SERVE_64
     return {
-        "c1": ("c1", "bdgdn_fwd_pipelined_kernel<float, 128, 32>", "fused", W.TRAIN_4K),
-        "c2": ("c2", "bdgdn_fwd_pipelined_pair_kernel<float, 128>", "fused", W.GVA_16K),
-        "c4": ("c4", "bdgdn_chunk_out_kernel<float, 128, 128, 32>", "chunked", W.VARLEN_128K),
-        "c3_denoise": ("c3", "bdgdn_k4_denoise_kernel<float, 32>", "serve", sw),
-        "c3_commit": ("c3", "bdgdn_k4_commit_kernel<float, 32, true>", "serve", sw),
-        "c3_commit_state_only": ("c3", "bdgdn_k4_commit_kernel<float, 32, false>", "serve", sw),
+        "train_4k": ("train_4k", "bdgdn_fwd_pipelined_kernel<float, 128, 32>", "fused", W.TRAIN_4K),
+        "gva_16k": ("gva_16k", "bdgdn_fwd_pipelined_pair_kernel<float, 128>", "fused", W.GVA_16K),
+        "varlen_128k": ("varlen_128k", "bdgdn_chunk_out_kernel<float, 128, 128, 32>", "chunked", W.VARLEN_128K),
+        "serve_denoise": ("serve", "bdgdn_k4_denoise_kernel<float, 32>", "serve", sw),
+        "serve_commit": ("serve", "bdgdn_k4_commit_kernel<float, 32, true>", "serve", sw),
+        "serve_commit_state_only": ("serve", "bdgdn_k4_commit_kernel<float, 32, false>", "serve", sw),
     }
 
 
@@ -279,10 +279,10 @@ def record_traffic(root):
                                "source_hash": kernel_source_hash(group), "fetch_kib_raw": fk[0],
                                "write_kib_raw": wk[0], "read_bytes": rd, "write_bytes": wr,
                                "bytes_per_launch": int(rd + wr)}
-        if key.startswith("c3"):
-            alg = {"c3_denoise": algorithmic_bytes_denoise(wl, 4),
-                   "c3_commit": algorithmic_bytes_commit(wl, True, 4),
-                   "c3_commit_state_only": algorithmic_bytes_commit(wl, False)}[key]
+        if key.startswith("serve"):
+            alg = {"serve_denoise": algorithmic_bytes_denoise(wl, 4),
+                   "serve_commit": algorithmic_bytes_commit(wl, True, 4),
+                   "serve_commit_state_only": algorithmic_bytes_commit(wl, False)}[key]
             model = f"{alg / 1e6:.1f} (fp32 o)"
         else:
             alg = algorithmic_bytes_train(wl, 4)
@@ -296,7 +296,7 @@ def record_traffic(root):
           "configuration, one counter each, scaled by what the same counter reads for a plain 256 MiB device",
           f"copy (`bench.py --copy-probe`): FETCH_SIZE reads {cf:.0f} KiB for the copy's 262144 KiB of reads",
           f"(factor {ff:.4f}), WRITE_SIZE {cw:.0f} KiB (factor {wf:.4f}).", "",
-          "Commands (repository root on the MI355X box, `TMPDIR=/tmp`; `<section>` is c1, c2, c4 or c3):", "",
+          "Commands (repository root on the MI355X box, `TMPDIR=/tmp`; `<section>` is train_4k, gva_16k, varlen_128k or serve):", "",
           "    cd /tmp && rocprofv3 --pmc FETCH_SIZE --output-format csv -d <root>/<section>_fetch -o run -- \\",
           "        python3 <repo>/bench.py --no-cpu-baseline --only <section> --protocol-iters 3 --protocol-repeats 1",
           "    cd /tmp && rocprofv3 --pmc WRITE_SIZE --output-format csv -d <root>/<section>_write -o run -- \\",
@@ -410,7 +410,7 @@ def main():
     if args.no_cpu_baseline:
         only.discard("cpu")
     if "verify" in only:
-        only.add("c3")   # the verify pass runs on the serving pools
+        only.add("serve")   # the verify pass runs on the serving pools
 
     import torch
 
@@ -429,7 +429,7 @@ def main():
     route = {"fused": bd.BDGDN_ROUTE_FUSED, "split": bd.BDGDN_ROUTE_SPLIT,
              "records": bd.BDGDN_ROUTE_RECORDS, "chunked": bd.BDGDN_ROUTE_CHUNKED}[args.route]
     inp = None
-    if "headline" in only or "c1" in only or "cpu" in only:
+    if "headline" in only or "train_4k" in only or "cpu" in only:
         inp, d, step, o = train_setup(w, dev, route, torch.float32)
     if "headline" in only:
         ms = time_launches(step, args.steps, args.warmup, stream)
@@ -450,7 +450,7 @@ def main():
                        "route": ROUTES[args.route], "parallelism": "none (1 GPU)"},
             "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": achieved / HBM_PEAK_GBS,
-                         "traffic": recorded_traffic("c1") if args.route == "fused" else None,
+                         "traffic": recorded_traffic("train_4k") if args.route == "fused" else None,
                          "kernel": ("bdgdn_fwd_pipelined_kernel (the whole bdgdn_fwd_train step)"
                                     if args.route == "fused" else f"the {args.route} schedule (all of its kernels)"),
                          "algorithmic_bytes": abytes,
@@ -483,27 +483,27 @@ def main():
         del dd
         torch.cuda.empty_cache()
 
-    if "c0" in only:
-        train_config("c0", W.TINY_F32, note="records route (fp32 inputs): UT-transform kernel + scan")
-    if "c1" in only:
-        train_config("c1", W.TRAIN_4K, note="bdgdn_fwd_pipelined_kernel (one kernel)",
+    if "tiny_f32" in only:
+        train_config("tiny_f32", W.TINY_F32, note="records route (fp32 inputs): UT-transform kernel + scan")
+    if "train_4k" in only:
+        train_config("train_4k", W.TRAIN_4K, note="bdgdn_fwd_pipelined_kernel (one kernel)",
                      stp=step if route == bd.BDGDN_ROUTE_FUSED else None)
-    if "c1_bf16_out" in only:
-        train_config("c1_bf16_out", W.TRAIN_4K, out_dtype=torch.bfloat16,
+    if "train_4k_bf16_out" in only:
+        train_config("train_4k_bf16_out", W.TRAIN_4K, out_dtype=torch.bfloat16,
                      note="bdgdn_fwd_pipelined_kernel, bf16 outputs")
-    if "c2" in only:
-        train_config("c2", W.GVA_16K, note="bdgdn_fwd_pipelined_pair_kernel (one kernel; each noisy block of 64 "
+    if "gva_16k" in only:
+        train_config("gva_16k", W.GVA_16K, note="bdgdn_fwd_pipelined_pair_kernel (one kernel; each noisy block of 64 "
                                            "spans two 32-position sub-blocks)")
-    if "c4" in only:
-        train_config("c4", W.VARLEN_128K, note="bdgdn_chunk_out_kernel (one workgroup per (document, v-head) over "
+    if "varlen_128k" in only:
+        train_config("varlen_128k", W.VARLEN_128K, note="bdgdn_chunk_out_kernel (one workgroup per (document, v-head) over "
                                                "all d_v columns: 512 chains cover the 256 CUs), longest documents first")
-    if "c4_bf16_out" in only:
+    if "varlen_128k_bf16_out" in only:
         # the same kernel writing bf16 outputs: the bytes it moves are then those of the byte model
-        train_config("c4_bf16_out", W.VARLEN_128K, out_dtype=torch.bfloat16,
+        train_config("varlen_128k_bf16_out", W.VARLEN_128K, out_dtype=torch.bfloat16,
                      note="bdgdn_chunk_out_kernel, bf16 outputs")
 
-    # ---------------- c3: serving
-    if "c3" in only:
+    # ---------------- serving
+    if "serve" in only:
         sw = W.SERVE_64
         pools = prefix_pools(sw, dev, 3, stream)   # 3 x 128 MiB > the 256 MB MALL
         blk = {k: v.to(dev) for k, v in W.make_serve_block(sw, 0).items()}
@@ -518,8 +518,8 @@ def main():
         ms, reps = time_protocol(dstep, stream, flush)
         r = rates(ms, algorithmic_bytes_denoise(sw), model_flops_denoise(sw), sw.requests * sw.block)
         r.update({"workload": sw.name, "repeats_ms": reps, "kernel": "bdgdn_k4_denoise_kernel",
-                  "pools": "3 prefix-state pools rotated (384 MiB)", "traffic_bytes": recorded_traffic("c3_denoise")})
-        configs["c3_denoise"] = r
+                  "pools": "3 prefix-state pools rotated (384 MiB)", "traffic_bytes": recorded_traffic("serve_denoise")})
+        configs["serve_denoise"] = r
         # warm: one pool, no flush (its 128 MiB state can stay in the MALL between calls)
         it[0] = 0
         one = pools[:1]
@@ -529,9 +529,9 @@ def main():
         wms, wreps = time_protocol(wstep, stream, lambda: None)
         rw = rates(wms, algorithmic_bytes_denoise(sw), model_flops_denoise(sw), sw.requests * sw.block)
         rw.update({"workload": sw.name, "repeats_ms": wreps, "pools": "one pool, no flush (warm)"})
-        configs["c3_denoise_warm"] = rw
+        configs["serve_denoise_warm"] = rw
         oc = torch.empty_like(od)
-        for key, want in (("c3_commit", True), ("c3_commit_state_only", False)):
+        for key, want in (("serve_commit", True), ("serve_commit_state_only", False)):
             def cstep(want=want):
                 pool = pools[it[0] % len(pools)]
                 it[0] += 1
@@ -542,16 +542,16 @@ def main():
             rc.update({"workload": sw.name, "repeats_ms": creps, "traffic_bytes": recorded_traffic(key),
                        "kernel": "bdgdn_k4_commit_kernel (" + ("causal outputs" if want else "no outputs") + ")"})
             configs[key] = rc
-        print(f"c3 denoise {ms * 1e3:.1f} us", file=sys.stderr, flush=True)
+        print(f"serve denoise {ms * 1e3:.1f} us", file=sys.stderr, flush=True)
         result["denoise_step"] = {"workload": sw.name, "us_per_call": ms * 1e3, "gb_per_s": r["gb_per_s"],
                                   "frac_hbm": r["frac_hbm"], "algorithmic_bytes": r["algorithmic_bytes"],
                                   "tokens_per_s": r["tokens_per_s"], "kernel": "bdgdn_k4_denoise_kernel",
                                   "warm_single_pool_us": wms * 1e3, "traffic_bytes": r["traffic_bytes"]}
-        result["commit"] = {"workload": sw.name, "us_per_call": configs["c3_commit"]["ms"] * 1e3,
-                            "gb_per_s": configs["c3_commit"]["gb_per_s"],
-                            "frac_hbm": configs["c3_commit"]["frac_hbm"],
-                            "state_only_us_per_call": configs["c3_commit_state_only"]["ms"] * 1e3,
-                            "state_only_frac_hbm": configs["c3_commit_state_only"]["frac_hbm"]}
+        result["commit"] = {"workload": sw.name, "us_per_call": configs["serve_commit"]["ms"] * 1e3,
+                            "gb_per_s": configs["serve_commit"]["gb_per_s"],
+                            "frac_hbm": configs["serve_commit"]["frac_hbm"],
+                            "state_only_us_per_call": configs["serve_commit_state_only"]["ms"] * 1e3,
+                            "state_only_frac_hbm": configs["serve_commit_state_only"]["frac_hbm"]}
 
         if "verify" in only:
             # AR-Trust verify round: the verify pass keeping the states before the draft
@@ -656,10 +656,10 @@ def main():
         # the other training workloads: the tiny fp32 one (the per-step fp32 backward) and the
         # grouped-value one (blocks of 64: the block form with noisy blocks of two sub-blocks)
         per_step = {}
-        paths = {"c0": ("bdgdn_bwd_gen_ckpt_kernel + bdgdn_bwd_gen_walk_kernel (fp32, per step)", 1, 3, 1),
-                 "c2": ("bdgdn_k2_scan_states_kernel (seed states per 32-position sub-block) + "
+        paths = {"tiny_f32": ("bdgdn_bwd_gen_ckpt_kernel + bdgdn_bwd_gen_walk_kernel (fp32, per step)", 1, 3, 1),
+                 "gva_16k": ("bdgdn_k2_scan_states_kernel (seed states per 32-position sub-block) + "
                         "bdgdn_bwd_pair_kernel + bdgdn_bwd_scan_kernel + bdgdn_bwd_clean_kernel", 3, 10, 3)}
-        for key, pw in (("c0", W.TINY_F32), ("c2", W.GVA_16K)):
+        for key, pw in (("tiny_f32", W.TINY_F32), ("gva_16k", W.GVA_16K)):
             pin = {k_: v_.to(dev) for k_, v_ in W.make_train(pw).items()}
             pshape = (pw.batch, pw.seqlen, pw.h_v, pw.d_v)
             pdo = torch.randn(pshape, generator=torch.Generator(device=dev).manual_seed(8), device=dev)
