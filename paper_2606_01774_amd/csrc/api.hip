@@ -185,8 +185,10 @@ static ChunkPlan chunk_plan(const bdgdn_fwd_desc_t *d)
     p.tiles = chains >= kComputeUnits ? 1 : d->d_v / 32;
     const long work = total_blocks(d) * d->h_v * p.tiles;   // (block, v-head, tile) triples
     const long nblk = (d->seqlen + d->block - 1) / d->block;
+    // G: the largest power of two from 16 on with at least two (chain, segment, tile)
+    // workgroups per compute unit and fewer blocks than a chain
     long G = 16;
-    while (G * 2 * kComputeUnits <= work && G < nblk) G *= 2;
+    while (2 * G * 2 * kComputeUnits <= work && 2 * G < nblk) G *= 2;
     p.G = (int)G;
     return p;
 }

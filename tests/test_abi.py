@@ -120,7 +120,10 @@ def test_chunked_route_limits_and_workspace():
         assert bd.bdgdn_fwd_train_workspace(_desc(**ch, **kw)) == 0
     # every chain one segment (no state pass): no workspace
     assert bd.bdgdn_fwd_train_workspace(_desc(**ch)) == 0
-    assert bd.bdgdn_fwd_train_workspace(_desc(**ch, batch=4, seqlen=4096, h_qk=16, h_v=16)) == 0
+    # 4 x 4096 tokens, 16 heads: 64 chains x 4 tiles, 128 blocks each -> segments of 64 (two
+    # workgroups per compute unit)
+    big = _desc(**ch, batch=4, seqlen=4096, h_qk=16, h_v=16)
+    assert bd.bdgdn_fwd_train_workspace(big) == 512 * 16 * 4352 + (512 // 64) * 16 * 128 * 128 * 4
     # 2 x 1100 tokens, 2 heads, blocks of 32: 70 blocks in 32-column tiles -> segments of 16;
     # records of 4352 bytes per (block, head), a state per (later segment start, head)
     mid = _desc(**ch, batch=2, seqlen=1100, h_qk=2, h_v=2)
