@@ -151,6 +151,10 @@ static bool pair_blocks(const bdgdn_fwd_desc_t *d, Types ty)
     return !pipelined_supported(ty, d->d_k, lp_of(d->block)) && pair_supported(ty, d->d_k, d->block);
 }
 
+// Blocks of 1, 2, 4 or 8 positions run the one-kernel forward on 32-position clean chunks
+// that hold several noisy blocks each (the noisy seeds inside a chunk are formed on chip).
+static bool small_blocks(const bdgdn_fwd_desc_t *d, Types ty) { return small_supported(ty, d->d_k, d->block); }
+
 // The fused route runs as one kernel where it can, else through the UT records.
 static bool one_kernel(const bdgdn_fwd_desc_t *d, Types ty)
 {
@@ -159,10 +163,17 @@ static bool one_kernel(const bdgdn_fwd_desc_t *d, Types ty)
 }
 
 // The one-kernel forward on a descriptor's chains: the sub-block is the block, or half of
-// it for pairs.
+// it for pairs, or a 32-position chunk of small blocks (with the clean outputs only: a
+// further noisy view keeps one block per step).
 static hipError_t launch_one_kernel(const bdgdn_fwd_desc_t *d, Types ty, ScanArgs sa, hipStream_t s,
                                     bool clean_out = true)
 {
+    if (clean_out && small_blocks(d, ty)) {
+        sa.nl = d->block;
+        sa.L = 32;
+        sa.nblk = (d->seqlen + 31) / 32;
+        return launch_fwd_pipelined_small(ty, d->d_k, sa, s);
+    }
     if (!pair_blocks(d, ty)) return launch_fwd_pipelined(ty, d->d_k, lp_of(d->block), sa, s, clean_out);
     sa.L = d->block / 2;
     sa.nblk = (d->seqlen + sa.L - 1) / sa.L;
@@ -202,7 +213,7 @@ static bool fused_uses_wide_pass(const bdgdn_fwd_desc_t *d, Types ty)
 {
     const long chains = (long)(d->num_seqs > 0 ? d->num_seqs : d->batch) * d->h_v;
     return chunked_supported(ty, d->d_k, d->d_v, lp_of(d->block)) && d->num_seqs <= kMaxOrder &&
-           chains >= kComputeUnits;
+           chains >= kComputeUnits && !small_blocks(d, ty);
 }
 // Workspace of the chunk-parallel schedule: a clean UT record per (block, v-head) and a
 // state per (segment start after the first, v-head), both bounded by the descriptor alone

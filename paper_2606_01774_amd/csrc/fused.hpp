@@ -43,8 +43,12 @@ namespace bdgdn {
 // sub-block, e.g. 64 positions as two halves of 32): the N waves carry the noisy state
 // across the pair and the first half's rows also read the state at the end of the second
 // (see n_block_pair).  The clean stream does not care how it is cut into blocks.
+// SMALL: noisy blocks of nl positions (nl a power of two below LP, the chain's nl): the chain
+// runs on LP-position clean chunks, each holding LP / nl noisy blocks whose seeds (the clean
+// state at each block start inside the chunk) the N waves form from the chunk-start state
+// and the chunk's clean Delta (see n_block_small).
 template <typename Out, int DK, int LP, bool SPLIT = false, bool SEEDS = SPLIT, typename SeedT_ = float,
-          bool STATES = false, bool NO_O = false, bool PAIR = false>
+          bool STATES = false, bool NO_O = false, bool PAIR = false, bool SMALL = false>
 struct Fused {
     typedef SeedT_ SeedT;
     static_assert(!STATES || (SPLIT && SEEDS && sizeof(SeedT_) == 2), "STATES: the split scan, fp16 seeds");
@@ -71,7 +75,10 @@ struct Fused {
     static constexpr int TM_B = al16(LP * TS * 2);
     static constexpr int OFF_TM = 2 * V_B;
     static constexpr int OFF_FAC = OFF_TM + 2 * TM_B;
-    static constexpr int NFAC = 5;
+    // factors per position: 0 2^G, 1 2^(G_n - G), 3 G (clean, log2); 2 2^G~, 4 2^(G~_n - G~)
+    // (noisy); SMALL: 5 2^(G~ at the end of the position's noisy block), 6 the clean G
+    // before the position's noisy block starts (log2), G~ restarting at every noisy block
+    static constexpr int NFAC = SMALL ? 7 : 5;
     static constexpr int SET_B = OFF_FAC + NFAC * 64 * 4;
     static constexpr int ST_B = BV * DK * 2;     // state operand [v][d_k], swizzled like rows
     static constexpr int DT_B = al16(BV * TS * 2);
@@ -85,6 +92,7 @@ struct Fused {
     // operand), the first half's readout accumulators Y1 (fp32, per N wave and lane) and the
     // cross Gram tile R12 (fp16 A-operand quads [bi][bj][lane])
     static_assert(!PAIR || (LP == 32 && !SPLIT), "pairs of 32-position sub-blocks, noisy waves active");
+    static_assert(!SMALL || (LP == 32 && !SPLIT && !PAIR && !NO_O), "small noisy blocks in 32-position chunks");
     static constexpr int OFF_NS = OFF_SINK + 64 * 16;
     static constexpr int OFF_Y1 = OFF_NS + (PAIR ? ST_B : 0);
     static constexpr int OFF_R12 = OFF_Y1 + (PAIR ? 2 * NB * 64 * 16 : 0);
@@ -188,6 +196,7 @@ struct Fused {
         int qks, vst, gst;           // row strides (elements)
         long len;
         int L;
+        int nl;        // SMALL: positions per noisy block
         SeedT *bs;     // seed state of the chain's first block (column v0), or null
         long bs_blk;   // per-block advance of bs (elements)
         const float *h0;
@@ -332,14 +341,37 @@ struct Fused {
     // solve itself is ut::solve_t.
     template <int STREAM>
     __device__ __forceinline__ void u_record(int slot, int p, float gv, float bv, const QOffs &qo,
-                                             const ut::Consts &us_) const
+                                             const ut::Consts &us_, int nl) const
     {
         float *Gs = us(STREAM), *Bs = Gs + 64;   // cumulative log2-gates, beta
         const float x = ut::scan32(lane < LP ? gv * kLog2e : 0.f, lane);
         const float gl = ut::lane_value(x, LP - 1);
         Gs[lane] = x;
         Bs[lane] = bv;
-        if (lane < LP) {
+        if constexpr (SMALL) {
+            // xb: the cumulative gate before the start of this position's noisy block (the
+            // lane exchanges run on every lane; the selects follow them)
+            const int pb = lane & (LP - 1) & ~(nl - 1);
+            const float xp = __shfl(x, pb > 0 ? pb - 1 : 0, 64);
+            const float xb = pb > 0 ? xp : 0.f;
+            if (STREAM == 0) {
+                if (lane < LP) {
+                    fac(p, 0)[lane] = fexp2(x);
+                    fac(p, 1)[lane] = fexp2(gl - x);
+                    fac(p, 3)[lane] = x;
+                    fac(p, 6)[lane] = xb;
+                }
+            } else {
+                // noisy gates from the start of each noisy block; xe at its last position
+                const float xs = x - xb;
+                const float xe = __shfl(xs, pb + nl - 1, 64);
+                if (lane < LP) {
+                    fac(p, 2)[lane] = fexp2(xs);
+                    fac(p, 4)[lane] = fexp2(xe - xs);
+                    fac(p, 5)[lane] = fexp2(xe);
+                }
+            }
+        } else if (lane < LP) {
             if (STREAM == 0) {
                 fac(p, 0)[lane] = fexp2(x);
                 fac(p, 1)[lane] = fexp2(gl - x);
@@ -353,7 +385,10 @@ struct Fused {
         QE kq[NB][DKB];
 #pragma unroll
         for (int rb = 0; rb < NB; ++rb) ld_q<DKB>(kq[rb], K + 16 * rb * DK, qo.q);
-        ut::solve_t<NB, DKB>(kq, Gs, Bs, tm(p, STREAM == 0 ? 0 : 1), TS, us_, lane);
+        if constexpr (SMALL && STREAM == 1)
+            ut::solve_t<NB, DKB, true, true>(kq, Gs, Bs, tm(p, 1), TS, us_, lane, nl);
+        else
+            ut::solve_t<NB, DKB>(kq, Gs, Bs, tm(p, STREAM == 0 ? 0 : 1), TS, us_, lane);
     }
 
     // ------------------------------------------------------------------ scan helpers
@@ -501,6 +536,117 @@ struct Fused {
         f32x4 o[NB];
 #pragma unroll
         for (int rb = 0; rb < NB; ++rb) o[rb] = mma_q<E, NB>(x4[rb], rq[rb], nq);
+        store_out(on, stride, nvalid, bc, o, scale);
+    }
+    // SMALL: the noisy blocks of nl positions inside one clean chunk.  Noisy block j (rows
+    // p_j .. p_j + nl - 1) is seeded with the clean state before position p_j,
+    //     S_(p_j) = 2^(c_j) S0 + sum_(i < p_j) 2^(c_j - G_i) k_i Delta_i^T,   c_j = G_(p_j - 1),
+    // so with the chunk's clean Delta (recomputed here from its record and rows) every noisy
+    // row r of block j reads
+    //     X~ = diag(2^c) K~ S0 + (K~ K^T o M) Delta,   M_ri = 2^(c_r - G_i) [i < p_(j(r))],
+    //     O~ = diag(gamma~_end) [diag(2^c) Q~ S0 + (Q~ K^T o M) Delta] + (R o B) Delta~,
+    // with Delta~ = T~ (V~ - Gamma~ X~), the noisy gates restarting at each noisy block
+    // (Gamma~, gamma~_end at the block's last position, R_rc = 2^(G~_end - G~_c) q~_r . k~_c)
+    // and B, T~ block diagonal over the noisy blocks.  The Gram tiles K~ K^T, Q~ K^T and R are
+    // formed in the A-operand layout (lane (g, n): row 16 bi + n, column 16 bj + 4 g + i).
+    // Row quads are read from LDS where each product uses them (the quad loads are not
+    // merged), which keeps the register footprint within three waves per SIMD.
+    __device__ __forceinline__ void n_block_small(int slot, int p, int sb, int bc, Out *on, int stride, int nvalid,
+                                                  float scale, int nl, const QOffs &qo) const
+    {
+        const int g = lane >> 4, n = lane & 15;
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        const f32x4 zs[NB] = {};
+        const f16x4 zq = {};
+        QE sq[DKB];
+        ld_q<DKB>(sq, st(sb) + 16 * bc * DK, qo.q);
+        const E *Kc = rows(slot, 0), *Kn = rows(slot, 2), *Qn = rows(slot, 3);
+        // the chunk's clean Delta for this wave's 16 columns, as B-operand quads
+        QE dcq[NB];
+        {
+            f32x4 x1[NB];
+#pragma unroll
+            for (int rb = 0; rb < NB; ++rb) {
+                QE kc[DKB];
+                ld_q<DKB>(kc, Kc + 16 * rb * DK, qo.q);
+                x1[rb] = mma_q<E, DKB>(z, kc, sq);
+            }
+            QE dq[NB];
+            d_quads(dq, x1, vs(p, 0), fac(p, 0), bc);
+            f32x4 dl[NB];
+            m_times(dl, tm(p, 0), dq, zs);
+#pragma unroll
+            for (int rb = 0; rb < NB; ++rb) dcq[rb] = quad_of<E>(dl[rb]);
+        }
+        const float *Gc = fac(p, 3), *Cb = fac(p, 6);
+        // M of tile (bi, bj) applied to a Gram accumulator in the A-operand layout
+        auto masked = [&](f32x4 t, int bi, int bj) {
+            const int r = 16 * bi + n, pj = r & ~(nl - 1);
+            const float cr = Cb[r];
+            const f32x4 gi = ld4f(Gc + 16 * bj + 4 * g);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) t[i] = 16 * bj + 4 * g + i < pj ? fexp2(-fabsf(cr - gi[i])) * t[i] : 0.f;
+            return quad_of<E>(t);
+        };
+        // 2^c of the rows 16 rb + 4 g + i (accumulator layout)
+        f32x4 ec[NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) {
+            const f32x4 cb = ld4f(Cb + 16 * rb + 4 * g);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) ec[rb][i] = fexp2(cb[i]);
+        }
+        // clean-key tile bj against the rows x (A-operand layout of x K^T), masked
+        auto cross = [&](const QE (&x)[DKB], int bi, int bj) {
+            if (bj > bi) return zq;
+            QE kc[DKB];
+            ld_q<DKB>(kc, Kc + 16 * bj * DK, qo.q);
+            return masked(mma_q<E, DKB>(z, kc, x), bi, bj);
+        };
+        // X~ and Delta~
+        f32x4 x3[NB];
+#pragma unroll
+        for (int bi = 0; bi < NB; ++bi) {
+            QE kq[DKB];
+            ld_q<DKB>(kq, Kn + 16 * bi * DK, qo.q);
+            QE mk[NB];
+#pragma unroll
+            for (int bj = 0; bj < NB; ++bj) mk[bj] = cross(kq, bi, bj);
+            x3[bi] = mma_q<E, NB>(mma_q<E, DKB>(z, kq, sq) * ec[bi], mk, dcq);
+        }
+        QE dq[NB];
+        d_quads(dq, x3, vs(p, 1), fac(p, 2), bc);
+        f32x4 dn[NB];
+        m_times(dn, tm(p, 1), dq, zs);
+        QE nq[NB];
+#pragma unroll
+        for (int rb = 0; rb < NB; ++rb) nq[rb] = quad_of<E>(dn[rb]);
+        // readout
+        f32x4 o[NB];
+#pragma unroll
+        for (int bi = 0; bi < NB; ++bi) {
+            QE qq[DKB];
+            ld_q<DKB>(qq, Qn + 16 * bi * DK, qo.q);
+            QE mq[NB], rq[NB];
+#pragma unroll
+            for (int bj = 0; bj < NB; ++bj) {
+                mq[bj] = cross(qq, bi, bj);
+                if (bj == bi) {
+                    // same noisy block: (r ^ c) < nl, within this 16 x 16 tile since nl <= 16
+                    QE kq[DKB];
+                    ld_q<DKB>(kq, Kn + 16 * bj * DK, qo.q);
+                    f32x4 t = mma_q<E, DKB>(z, kq, qq);
+                    const f32x4 fc = ld4f(fac(p, 4) + 16 * bj + 4 * g);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) t[i] = ((n ^ (4 * g + i)) < nl) ? t[i] * fc[i] : 0.f;
+                    rq[bj] = quad_of<E>(t);
+                } else {
+                    rq[bj] = zq;
+                }
+            }
+            const f32x4 y = mma_q<E, NB>(mma_q<E, DKB>(z, qq, sq) * ec[bi], mq, dcq);
+            o[bi] = mma_q<E, NB>(y * ld4f(fac(p, 5) + 16 * bi + 4 * g), rq, nq);
+        }
         store_out(on, stride, nvalid, bc, o, scale);
     }
     // PAIR: one half of a noisy block of two sub-blocks.  First half (half 0), from the
@@ -672,11 +818,11 @@ struct Fused {
         load_gates(0, gx, bx);
         load_gates(1, gy, by);
         lds_barrier();
-        u_record<STREAM>(0, 0, lane < LP ? gx : 0.f, lane < LP ? bx : 0.f, qo, usv);
+        u_record<STREAM>(0, 0, lane < LP ? gx : 0.f, lane < LP ? bx : 0.f, qo, usv, c.nl);
         lds_barrier();
         for (int j = 0; j < nb; ++j) {
             load_gates(j + 2, gx, bx);
-            u_record<STREAM>((j + 1) % 3, (j + 1) & 1, lane < LP ? gy : 0.f, lane < LP ? by : 0.f, qo, usv);
+            u_record<STREAM>((j + 1) % 3, (j + 1) & 1, lane < LP ? gy : 0.f, lane < LP ? by : 0.f, qo, usv, c.nl);
             gy = gx;
             by = bx;
             lds_barrier();
@@ -775,6 +921,8 @@ struct Fused {
                     n_block_pair(j % 3, (j + 1) % 3, half, half, bc, half, half == 0 && nv(j + 1) > 0, pc.on,
                                  on_prev, c.vst, nv(j), nv(j - 1), c.scale, qo);
                     on_prev = pc.on;
+                } else if constexpr (SMALL) {
+                    n_block_small(j % 3, j & 1, j & 1, bc, pc.on, c.vst, nv(j), c.scale, c.nl, qo);
                 } else {
                     n_block(j % 3, j & 1, j & 1, bc, pc.on, c.vst, nv(j), c.scale, qo);
                 }
@@ -923,6 +1071,7 @@ __device__ __forceinline__ void run_chain(const ScanArgs &a, unsigned char *smem
     c.g_blk = (long)a.L * c.gst;
     c.len = len;
     c.L = a.L;
+    c.nl = a.nl;
     const long state_off = ((long)seq * a.h_v + h) * DK * a.dv + v0;
     c.h0 = a.h0 ? a.h0 + state_off : nullptr;
     if constexpr (K::kSeeds) {

@@ -38,6 +38,14 @@ __global__ void __launch_bounds__(768) bdgdn_fwd_pipelined_pair_noisy_kernel(Sca
     run_chain<Fused<Out, DK, 32, false, false, float, false, true, true>>(a, smem);
 }
 
+// Noisy blocks of 1 .. 8 positions inside 32-position clean chunks.
+template <typename Out, int DK>
+__global__ void __launch_bounds__(768) bdgdn_fwd_pipelined_small_kernel(ScanArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    run_chain<Fused<Out, DK, 32, false, false, float, false, false, false, true>>(a, smem);
+}
+
 template <typename K>
 static hipError_t launch_kernel(void (*kern)(ScanArgs), const ScanArgs &a, hipStream_t s)
 {
@@ -110,6 +118,28 @@ hipError_t launch_fwd_pipelined(Types ty, int dk, int lp, const ScanArgs &a, hip
         BDGDN_CASE(float, 64, 16) BDGDN_CASE(float, 64, 32) BDGDN_CASE(float, 128, 16) BDGDN_CASE(float, 128, 32)
     } else {
         BDGDN_CASE(__bf16, 64, 16) BDGDN_CASE(__bf16, 64, 32) BDGDN_CASE(__bf16, 128, 16) BDGDN_CASE(__bf16, 128, 32)
+    }
+#undef BDGDN_CASE
+    return hipErrorInvalidValue;
+}
+
+bool small_supported(Types ty, int dk, int L)
+{
+    return ty != Types::F32 && (dk == 64 || dk == 128) && L >= 1 && L <= 8 && (L & (L - 1)) == 0;
+}
+
+hipError_t launch_fwd_pipelined_small(Types ty, int dk, const ScanArgs &a, hipStream_t s)
+{
+    if (!small_supported(ty, dk, a.nl) || a.L != 32 || a.n_vt * 32 != a.dv) return hipErrorInvalidValue;
+#define BDGDN_CASE(OUT, DK)                                                                      \
+    if (dk == DK) {                                                                              \
+        typedef Fused<OUT, DK, 32, false, false, float, false, false, false, true> K;            \
+        return launch_kernel<K>(bdgdn_fwd_pipelined_small_kernel<OUT, DK>, a, s);                \
+    }
+    if (ty == Types::BF16_IN_F32_OUT) {
+        BDGDN_CASE(float, 64) BDGDN_CASE(float, 128)
+    } else {
+        BDGDN_CASE(__bf16, 64) BDGDN_CASE(__bf16, 128)
     }
 #undef BDGDN_CASE
     return hipErrorInvalidValue;

@@ -44,6 +44,7 @@ struct ScanArgs {
     void *bs;            // seed states by (global block, v-head): fp32 (split schedule, views),
                          // fp16 (the backward's recomputation), or null
     int T, L, nblk, h_qk, h_v, dv;
+    int nl;              // noisy block of the small-block one-kernel forward (L is its clean chunk)
     int n_chains, n_vt;
     float scale;
     int n_order;
@@ -131,6 +132,10 @@ hipError_t launch_fwd_pipelined(Types ty, int dk, int lp, const ScanArgs &a, hip
 // sub-blocks of a.L positions and each noisy block spans two of them.
 bool pair_supported(Types ty, int dk, int L);
 hipError_t launch_fwd_pipelined_pair(Types ty, int dk, const ScanArgs &a, hipStream_t s, bool clean_out = true);
+// Noisy blocks of a.nl = 1, 2, 4 or 8 positions in the same kernel: the chain runs on clean
+// chunks of a.L = 32 positions, each holding 32 / a.nl noisy blocks.
+bool small_supported(Types ty, int dk, int L);
+hipError_t launch_fwd_pipelined_small(Types ty, int dk, const ScanArgs &a, hipStream_t s);
 // The same, also writing the seed state of every (block, v-head) to a.bs (d_k = 128).
 hipError_t launch_fwd_pipelined_seeds(Types ty, int lp, const ScanArgs &a, hipStream_t s);
 // The split schedule (clean scan exposing the seed states, then the noisy-block pass):

@@ -105,10 +105,13 @@ __device__ __forceinline__ f16x4 and_mask(f16x4 q, const unsigned (&m)[2])
 // branched on.  With log-gates g <= 0 the cumulative G is non-increasing, so every decay
 // exponent kept (G_r - G_c, r >= c) is <= 0 and is evaluated as -|G_r - G_c|, which also
 // keeps the discarded entries finite.  With BETA = false the inverse M = (I + A)^(-1) itself
-// is written instead of T (the backward needs M where a step size is zero).
-template <int NB, int DKB, bool BETA = true>
+// is written instead of T (the backward needs M where a step size is zero).  With BLKDIAG
+// the positions form consecutive groups of nl (a power of two) with no coupling between
+// groups: A_ri is kept only where r and i lie in the same group, so T is block diagonal
+// (the transform of each group on its own).
+template <int NB, int DKB, bool BETA = true, bool BLKDIAG = false>
 __device__ __forceinline__ void solve_t(const QE (&kq)[NB][DKB], const float *Gs, const float *Bs, E *T, int ts,
-                                        const Consts &us_, int lane)
+                                        const Consts &us_, int lane, int nl = 0)
 {
     static_assert(NB == 1 || NB == 2 || NB == 4, "blocks of 16, 32 or 64 positions");
     const int g = lane >> 4, n = lane & 15;
@@ -118,7 +121,15 @@ __device__ __forceinline__ void solve_t(const QE (&kq)[NB][DKB], const float *Gs
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi)
 #pragma unroll
-        for (int bj = bi; bj < NB; ++bj) kk[bi][bj] = mma_q<E, DKB>(z, kq[bi], kq[bj]);
+        for (int bj = bi; bj < NB; ++bj) {
+            kk[bi][bj] = mma_q<E, DKB>(z, kq[bi], kq[bj]);
+            if constexpr (BLKDIAG) {
+                // positions r, i share a group of nl iff (r ^ i) < nl
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (((16 * bi + 4 * g + i) ^ (16 * bj + n)) >= nl) kk[bi][bj][i] = 0.f;
+            }
+        }
     // per-lane gates: rows 4g + i and column n of each 16-block
     f32x4 gr[NB], br[NB];
     float gc[NB], bc[NB];

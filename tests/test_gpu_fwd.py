@@ -82,6 +82,53 @@ def test_pair_blocks(B, T, hqk, hv, d, L, lengths):
     _check_full(inp, L, "bf16", h0=h0)
 
 
+@pytest.mark.parametrize("B,T,hqk,hv,d,L,lengths", [
+    (2, 200, 2, 2, 128, 8, None),        # 200 = 6 * 32 + 8: the last chunk holds one noisy block
+    (1, 150, 1, 2, 128, 4, None),        # 150 = 4 * 32 + 22: the last chunk ends inside a noisy block
+    (1, 97, 2, 2, 64, 2, None),          # d = 64
+    (1, 70, 1, 1, 128, 1, None),         # every noisy block one step
+    (1, 256, 2, 4, 128, 8, None),        # grouped value heads
+    (1, 8 + 40 + 0 + 96 + 23, 2, 2, 128, 8, [8, 40, 0, 96, 23]),   # packed: documents starting inside a chunk
+])
+def test_small_blocks(B, T, hqk, hv, d, L, lengths):
+    """Noisy blocks of 1, 2, 4 or 8 positions in the one-kernel forward: the chain runs on
+    32-position clean chunks and each chunk's noisy blocks are seeded with the clean state at
+    their own start, formed on chip.  Against the oracle, and against the records route
+    (one padded block per step)."""
+    inp = W.make_custom_train(B, T, hqk, hv, d, d, "bf16", seed=7000 + T + L, lengths=lengths)
+    h0 = None if lengths else torch.randn(B, hv, d, d, generator=torch.Generator().manual_seed(T + 3)) * 0.3
+    o, on, ht = _check_full(inp, L, "bf16", h0=h0)
+    d_ = to_dev(inp)
+    if lengths:
+        d_["cu_host"] = inp["cu_seqlens"]
+    b = _run_gpu(d_, L, 1.0 / math.sqrt(d), h0=None if h0 is None else h0.cuda(), route=bd.BDGDN_ROUTE_RECORDS)
+    for x, y in zip((o, on, ht), b):
+        e = rel_err(x, y.double().cpu().numpy())
+        print(f"small-block kernel vs records route {e:.3e}")
+        assert e <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("L", [1, 8])
+def test_full_small_blocks_all_units(L):
+    """The block-size sweep's shape (1 x 4096 clean + 4096 noisy tokens, 16 heads, d = 128)
+    at noisy blocks of 1 and 8 positions: every (sequence, head) unit against the oracle."""
+    inp = W.make_custom_train(1, 4096, 16, 16, 128, 128, "bf16", seed=8000 + L)
+    d = to_dev(inp)
+    scale = 1.0 / math.sqrt(128)
+    print(f"small blocks L={L}: GPU", flush=True)
+    o, on, ht = _run_gpu(d, L, scale)
+    o, on, ht = o.cpu(), on.cpu(), ht.cpu()
+    print(f"small blocks L={L}: oracle", flush=True)
+    ro, ron, rht = oracle_full(inp, L, scale)
+    worst = {}
+    for name, gpu, ref, kind in (("o", o, ro, False), ("on", on, ron, False), ("ht", ht, rht, None)):
+        e, where, n = unit_errors(gpu, ref, per_token=kind)
+        print(f"  {name}: worst unit {where} max|err|/rms = {e:.3e} over {n} units", flush=True)
+        worst[name] = e
+        assert n == 16
+    assert max(worst.values()) <= TOL["bf16"], worst
+
+
 @pytest.mark.parametrize("route", ROUTES)
 def test_packed_documents_small(route):
     lengths = [64, 96, 32, 0, 64, 128, 17]   # an empty doc and a ragged last doc
