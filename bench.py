@@ -39,7 +39,8 @@ HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, GB/s
 MFMA16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16/bf16 MFMA, TFLOP/s
 FLUSH_BYTES = 512 * 1024 * 1024
 SECTIONS = ("headline", "tiny_f32", "train_4k", "train_4k_bf16_out", "gva_16k", "serve", "varlen_128k", "varlen_128k_bf16_out", "verify", "views", "backward",
-            "shortconv", "cpu")
+            "blocks", "shortconv", "cpu")
+SWEEP_BLOCKS = (1, 2, 4, 8, 16, 32)   # the diffusion-block sweep of the route comparison
 
 
 # ---------------------------------------------------------------- work models
@@ -681,6 +682,41 @@ def main():
             del pin, pws, pgrads
             torch.cuda.empty_cache()
         result["backward"]["other_workloads"] = per_step
+
+    if "blocks" in only:
+        # forward and backward across diffusion-block sizes at one sequence of 4096 clean +
+        # 4096 noisy tokens, 16 heads, d = 128 (the shape of the paper's route comparison)
+        sin = {k_: v_.to(dev) for k_, v_ in W.make_custom_train(1, 4096, 16, 16, 128, 128, "bf16", seed=91).items()}
+        sargs = [sin[k_] for k_ in ("q", "k", "v", "g", "beta", "qn", "kn", "vn", "gn", "betan")]
+        sshape = (1, 4096, 16, 128)
+        sdo = torch.randn(sshape, generator=torch.Generator(device=dev).manual_seed(10), device=dev)
+        sdon = torch.randn(sshape, generator=torch.Generator(device=dev).manual_seed(11), device=dev)
+        so, son = torch.empty(sshape, device=dev), torch.empty(sshape, device=dev)
+        sweep = {}
+        for L in SWEEP_BLOCKS:
+            sdesc = bd.make_fwd_desc(sin["q"], sin["v"], block=L, out_dtype=torch.float32)
+            fws = bd.bdgdn_fwd_train_workspace(sdesc)
+            bws = torch.empty(max(256, bd.bdgdn_bwd_train_workspace(sdesc)), dtype=torch.uint8, device=dev)
+            sgrads = bd.bdgdn_bwd_train(*sargs, sdo, sdon, block=L, workspace=bws)
+
+            def sfstep(L=L):
+                bd.bdgdn_fwd_train(*sargs, block=L, o=so, on=son, stream=stream)
+
+            def sbstep(L=L):
+                bd.bdgdn_bwd_train(*sargs, sdo, sdon, block=L, workspace=bws, grads=sgrads, stream=stream)
+            sfms = time_protocol(sfstep, stream, flush)[0]
+            sbms = time_protocol(sbstep, stream, flush, iters=5 if L < 8 else 10, repeats=3, trim=1)[0]
+            sweep[str(L)] = {
+                "fwd_ms": sfms, "bwd_ms": sbms, "fwd_workspace_bytes": fws, "bwd_workspace_bytes": bws.numel(),
+                "fwd_schedule": ("bdgdn_fwd_pipelined_small_kernel (32-position clean chunks, %d noisy blocks each)"
+                                 % (32 // L)) if L <= 8 else "bdgdn_fwd_pipelined_kernel (one block per step)"}
+            del bws, sgrads
+            torch.cuda.empty_cache()
+            print(f"blocks L={L}: fwd {sfms:.3f} ms, bwd {sbms:.3f} ms", file=sys.stderr, flush=True)
+        result["blocks"] = {"workload": "sweep_bf16_b1_t4096_h16_d128 (fp32 outputs, fp32 upstream gradients)",
+                            "by_block": sweep}
+        del sin, sargs, sdo, sdon, so, son
+        torch.cuda.empty_cache()
 
     if "shortconv" in only:
         # the GDN layer's two-stream ShortConv at the same token shape (channels = the q, k

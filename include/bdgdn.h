@@ -89,7 +89,10 @@ typedef enum { BDGDN_BF16 = 0, BDGDN_F32 = 1 } bdgdn_dtype_t;
  *           covers all d_v columns instead (CHUNKED's output pass with one segment per
  *           chain; no workspace).  Blocks of an even 34 .. 64 positions run the one
  *           kernel on sub-blocks of half the block, each noisy block carrying its state
- *           across its two halves (no workspace); otherwise it is the RECORDS schedule.
+ *           across its two halves (no workspace).  Blocks of 1, 2, 4 or 8 positions run
+ *           it on 32-position clean chunks that hold 32 / block noisy blocks each, every
+ *           noisy block seeded on chip with the clean state at its own start (no
+ *           workspace).  Otherwise it is the RECORDS schedule.
  *  SPLIT:   boundary states through HBM and a separate noisy-block kernel (Appendix
  *           "Route I"): the clean scan writes the clean state before every block (the
  *           seed of that noisy block) into the workspace, fp32 [block][h_v][d_k][d_v]
