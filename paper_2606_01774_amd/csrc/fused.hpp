@@ -96,7 +96,13 @@ struct Fused {
     static constexpr int OFF_NS = OFF_SINK + 64 * 16;
     static constexpr int OFF_Y1 = OFF_NS + (PAIR ? ST_B : 0);
     static constexpr int OFF_R12 = OFF_Y1 + (PAIR ? 2 * NB * 64 * 16 : 0);
-    static constexpr int BYTES = OFF_R12 + (PAIR ? NB * NB * 64 * 8 : 0);
+    // SMALL: per record set, the raw Gram tiles of the block formed by the noisy U wave (fp32
+    // accumulators in the A-operand layout): K~ K^T and Q~ K^T (tiles bj <= bi), then the
+    // diagonal tiles of Q~ K~^T
+    static constexpr int XT = NB * (NB + 1) / 2;
+    static constexpr int XG_B = (2 * XT + NB) * 64 * 16;
+    static constexpr int OFF_XG = OFF_R12 + (PAIR ? NB * NB * 64 * 8 : 0);
+    static constexpr int BYTES = OFF_XG + (SMALL ? 2 * XG_B : 0);
     static_assert(BYTES <= 160 * 1024, "LDS budget");
     // staging team
     static constexpr int TT = 256;
@@ -145,6 +151,14 @@ struct Fused {
     __device__ __forceinline__ f32x4 *y1(int bc) const
     {
         return reinterpret_cast<f32x4 *>(smem + OFF_Y1) + bc * NB * 64;
+    }
+    __device__ __forceinline__ f32x4 *xg(int p, int which, int bi, int bj) const
+    {
+        return reinterpret_cast<f32x4 *>(smem + OFF_XG + p * XG_B) + (which * XT + bi * (bi + 1) / 2 + bj) * 64;
+    }
+    __device__ __forceinline__ f32x4 *xr(int p, int b) const
+    {
+        return reinterpret_cast<f32x4 *>(smem + OFF_XG + p * XG_B) + (2 * XT + b) * 64;
     }
     __device__ __forceinline__ QE *r12(int bi, int bj) const
     {
@@ -385,10 +399,27 @@ struct Fused {
         QE kq[NB][DKB];
 #pragma unroll
         for (int rb = 0; rb < NB; ++rb) ld_q<DKB>(kq[rb], K + 16 * rb * DK, qo.q);
-        if constexpr (SMALL && STREAM == 1)
+        if constexpr (SMALL && STREAM == 1) {
             ut::solve_t<NB, DKB, true, true>(kq, Gs, Bs, tm(p, 1), TS, us_, lane, nl);
-        else
+            // the raw cross Gram tiles of the noisy rows with the clean keys (for the N waves a
+            // step later; the clean keys sit in the same ring slot)
+            const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int bj = 0; bj < NB; ++bj) {
+                QE kc[DKB];
+                ld_q<DKB>(kc, rows(slot, 0) + 16 * bj * DK, qo.q);
+#pragma unroll
+                for (int bi = bj; bi < NB; ++bi) {
+                    xg(p, 0, bi, bj)[lane] = mma_q<E, DKB>(z, kc, kq[bi]);
+                    QE qq[DKB];
+                    ld_q<DKB>(qq, rows(slot, 3) + 16 * bi * DK, qo.q);
+                    xg(p, 1, bi, bj)[lane] = mma_q<E, DKB>(z, kc, qq);
+                    if (bi == bj) xr(p, bi)[lane] = mma_q<E, DKB>(z, kq[bi], qq);   // Q~ K~^T, tile (bi, bi)
+                }
+            }
+        } else {
             ut::solve_t<NB, DKB>(kq, Gs, Bs, tm(p, STREAM == 0 ? 0 : 1), TS, us_, lane);
+        }
     }
 
     // ------------------------------------------------------------------ scan helpers
@@ -548,8 +579,9 @@ struct Fused {
     // with Delta~ = T~ (V~ - Gamma~ X~), the noisy gates restarting at each noisy block
     // (Gamma~, gamma~_end at the block's last position, R_rc = 2^(G~_end - G~_c) q~_r . k~_c)
     // and B, T~ block diagonal over the noisy blocks.  The Gram tiles K~ K^T, Q~ K^T and R are
-    // formed in the A-operand layout (lane (g, n): row 16 bi + n, column 16 bj + 4 g + i).
-    // Row quads are read from LDS where each product uses them (the quad loads are not
+    // in the A-operand layout (lane (g, n): row 16 bi + n, column 16 bj + 4 g + i); the noisy
+    // U wave formed the first two a step earlier (raw, fp32 in LDS) and they are masked here.
+    // Noisy row quads are read from LDS where each product uses them (the quad loads are not
     // merged), which keeps the register footprint within three waves per SIMD.
     __device__ __forceinline__ void n_block_small(int slot, int p, int sb, int bc, Out *on, int stride, int nvalid,
                                                   float scale, int nl, const QOffs &qo) const
@@ -597,12 +629,8 @@ struct Fused {
             for (int i = 0; i < 4; ++i) ec[rb][i] = fexp2(cb[i]);
         }
         // clean-key tile bj against the rows x (A-operand layout of x K^T), masked
-        auto cross = [&](const QE (&x)[DKB], int bi, int bj) {
-            if (bj > bi) return zq;
-            QE kc[DKB];
-            ld_q<DKB>(kc, Kc + 16 * bj * DK, qo.q);
-            return masked(mma_q<E, DKB>(z, kc, x), bi, bj);
-        };
+        // the cross Gram tile (which: 0 K~ K^T, 1 Q~ K^T), masked
+        auto cross = [&](int which, int bi, int bj) { return bj > bi ? zq : masked(xg(p, which, bi, bj)[lane], bi, bj); };
         // X~ and Delta~
         f32x4 x3[NB];
 #pragma unroll
@@ -611,7 +639,7 @@ struct Fused {
             ld_q<DKB>(kq, Kn + 16 * bi * DK, qo.q);
             QE mk[NB];
 #pragma unroll
-            for (int bj = 0; bj < NB; ++bj) mk[bj] = cross(kq, bi, bj);
+            for (int bj = 0; bj < NB; ++bj) mk[bj] = cross(0, bi, bj);
             x3[bi] = mma_q<E, NB>(mma_q<E, DKB>(z, kq, sq) * ec[bi], mk, dcq);
         }
         QE dq[NB];
@@ -630,12 +658,10 @@ struct Fused {
             QE mq[NB], rq[NB];
 #pragma unroll
             for (int bj = 0; bj < NB; ++bj) {
-                mq[bj] = cross(qq, bi, bj);
+                mq[bj] = cross(1, bi, bj);
                 if (bj == bi) {
                     // same noisy block: (r ^ c) < nl, within this 16 x 16 tile since nl <= 16
-                    QE kq[DKB];
-                    ld_q<DKB>(kq, Kn + 16 * bj * DK, qo.q);
-                    f32x4 t = mma_q<E, DKB>(z, kq, qq);
+                    f32x4 t = xr(p, bi)[lane];
                     const f32x4 fc = ld4f(fac(p, 4) + 16 * bj + 4 * g);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) t[i] = ((n ^ (4 * g + i)) < nl) ? t[i] * fc[i] : 0.f;
