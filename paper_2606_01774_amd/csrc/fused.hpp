@@ -93,7 +93,10 @@ struct Fused {
     // cross Gram tile R12 (fp16 A-operand quads [bi][bj][lane])
     static_assert(!PAIR || (LP == 32 && !SPLIT), "pairs of 32-position sub-blocks, noisy waves active");
     static_assert(!SMALL || (LP == 32 && !SPLIT && !PAIR && !NO_O), "small noisy blocks in 32-position chunks");
-    static constexpr int OFF_NS = OFF_SINK + 64 * 16;
+    // the staging team's per-lane sink for unassigned slots (none at 32-position blocks)
+    static constexpr bool SINK_USED = (((LP * (DK / 8) + 255) / 256) * 256 != LP * (DK / 8)) ||
+                                      ((((SPLIT ? 1 : 2) * LP * (BV / 8) + 255) / 256) * 256 != (SPLIT ? 1 : 2) * LP * (BV / 8));
+    static constexpr int OFF_NS = OFF_SINK + (SINK_USED ? 64 * 16 : 0);
     static constexpr int OFF_Y1 = OFF_NS + (PAIR ? ST_B : 0);
     static constexpr int OFF_R12 = OFF_Y1 + (PAIR ? 2 * NB * 64 * 16 : 0);
     // SMALL: per record set, the raw Gram tiles of the block formed by the noisy U wave (fp32
@@ -102,7 +105,11 @@ struct Fused {
     static constexpr int XT = NB * (NB + 1) / 2;
     static constexpr int XG_B = (2 * XT + NB) * 64 * 16;
     static constexpr int OFF_XG = OFF_R12 + (PAIR ? NB * NB * 64 * 8 : 0);
-    static constexpr int BYTES = OFF_XG + (SMALL ? 2 * XG_B : 0);
+    // PAIR: per record set, the raw Gram tiles Q~ K~^T of the sub-block (fp16 A-operand quads),
+    // formed by the noisy U wave
+    static constexpr int RR_B = NB * NB * 64 * 8;
+    static constexpr int OFF_RR = OFF_XG + (SMALL ? 2 * XG_B : 0);
+    static constexpr int BYTES = OFF_RR + (PAIR ? 2 * RR_B : 0);
     static_assert(BYTES <= 160 * 1024, "LDS budget");
     // staging team
     static constexpr int TT = 256;
@@ -112,6 +119,7 @@ struct Fused {
     static constexpr int VCPR = BV / 8, VPS = LP * VCPR;  // V chunks per stream
     static constexpr int VPL = (2 * VPS + TT - 1) / TT;
     static_assert(VPS % 64 == 0, "a wave's V slot lies in one stream");
+    static_assert(SINK_USED == (OPS * TT != OCH || VPL * TT != (SPLIT ? 1 : 2) * VPS), "sink sizing");
 
     unsigned char *smem;
     int tid, lane, wave;
@@ -159,6 +167,10 @@ struct Fused {
     __device__ __forceinline__ f32x4 *xr(int p, int b) const
     {
         return reinterpret_cast<f32x4 *>(smem + OFF_XG + p * XG_B) + (2 * XT + b) * 64;
+    }
+    __device__ __forceinline__ QE *rr(int p, int bi, int bj) const
+    {
+        return reinterpret_cast<QE *>(smem + OFF_RR + p * RR_B) + (bi * NB + bj) * 64;
     }
     __device__ __forceinline__ QE *r12(int bi, int bj) const
     {
@@ -420,6 +432,29 @@ struct Fused {
         } else {
             ut::solve_t<NB, DKB>(kq, Gs, Bs, tm(p, STREAM == 0 ? 0 : 1), TS, us_, lane);
         }
+        if constexpr (PAIR && STREAM == 1) {
+            // for the N waves a step later: the raw Gram tiles Q~ K~^T of this sub-block and, when
+            // it is the second half of a noisy block (odd record sets), the cross tiles
+            // R12 = Q~1 K~2^T with the first half's query rows (their ring slot is still intact)
+            const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int bi = 0; bi < NB; ++bi) {
+                QE qq[DKB];
+                ld_q<DKB>(qq, rows(slot, 3) + 16 * bi * DK, qo.q);
+#pragma unroll
+                for (int bj = 0; bj < NB; ++bj) rr(p, bi, bj)[lane] = quad_of<E>(mma_q<E, DKB>(z, kq[bj], qq));
+            }
+            if (p == 1) {
+                const int prev = slot == 0 ? 2 : slot - 1;
+#pragma unroll
+                for (int bi = 0; bi < NB; ++bi) {
+                    QE qq[DKB];
+                    ld_q<DKB>(qq, rows(prev, 3) + 16 * bi * DK, qo.q);
+#pragma unroll
+                    for (int bj = 0; bj < NB; ++bj) r12(bi, bj)[lane] = quad_of<E>(mma_q<E, DKB>(z, kq[bj], qq));
+                }
+            }
+        }
     }
 
     // ------------------------------------------------------------------ scan helpers
@@ -677,13 +712,14 @@ struct Fused {
     }
     // PAIR: one half of a noisy block of two sub-blocks.  First half (half 0), from the
     // clean seed S0: Delta~1, the readout Y1 = Q~1 S~1 of the half-end noisy state S~1 (kept
-    // in LDS), S~1 itself (the second half's seed, an fp16 operand in LDS) and the unscaled
-    // cross Gram tile R12 = Q~1 K~2^T with the second half's keys, which sit in the next ring
-    // slot already (each N wave builds one 16-row block of it).  Second half, from S~1: its
-    // own rows as in n_block, and the first half's rows, which read the block-end state too:
-    //     O~1 = gamma~2 Y1 + R12 diag(2^(G~2_n - G~2_i)) Delta~2.
-    // A block whose second half holds no rows stores Y1 directly.
-    __device__ __forceinline__ void n_block_pair(int slot, int slot_next, int p, int sb, int bc, int half,
+    // in LDS) and S~1 itself (the second half's seed, an fp16 operand in LDS).  Second half,
+    // from S~1: its own rows as in n_block, and the first half's rows, which read the
+    // block-end state too:
+    //     O~1 = gamma~2 Y1 + R12 diag(2^(G~2_n - G~2_i)) Delta~2,
+    // with the unscaled cross Gram tile R12 = Q~1 K~2^T, which the noisy U wave formed with
+    // the second half's record.  Both halves take their R from the raw tiles Q~ K~^T of that
+    // wave.  A block whose second half holds no rows stores Y1 directly.
+    __device__ __forceinline__ void n_block_pair(int slot, int p, int sb, int bc, int half,
                                                  bool has_next, Out *on, Out *on_prev, int stride, int nvalid,
                                                  int nvalid_prev, float scale, const QOffs &qo) const
     {
@@ -711,9 +747,11 @@ struct Fused {
                 QE qq[DKB];
                 ld_q<DKB>(qq, rows(slot, 3) + 16 * bi * DK, qo.q);
                 x4[bi] = mma_q<E, DKB>(z, qq, sq) * gn_end;
+                // R from the raw tiles the noisy U wave formed a step earlier
 #pragma unroll
                 for (int bj = 0; bj < NB; ++bj)
-                    rq[bi][bj] = quad_of<E>(mma_q<E, DKB>(z, kq[bj], qq) * ld4f(fac(p, 4) + 16 * bj + 4 * g));
+                    rq[bi][bj] = quad_of<E>(__builtin_convertvector(rr(p, bi, bj)[lane], f32x4) *
+                                            ld4f(fac(p, 4) + 16 * bj + 4 * g));
             }
             QE dq[NB];
             d_quads(dq, x3, vs(p, 1), fac(p, 2), bc);
@@ -749,15 +787,6 @@ struct Fused {
                 typedef const __attribute__((address_space(3))) volatile QE *LQ;
                 const f32x4 s0 = __builtin_convertvector(*(LQ)(seed + qo.q[kb]), f32x4) * gn_end;
                 st_quad(dst + qo.q[kb], quad_of<E>(mma_q<E, NB>(s0, a, uq)));
-            }
-            // R12, row block bc
-            QE qq[DKB];
-            ld_q<DKB>(qq, rows(slot, 3) + 16 * bc * DK, qo.q);
-#pragma unroll
-            for (int bj = 0; bj < NB; ++bj) {
-                QE k2[DKB];
-                ld_q<DKB>(k2, rows(slot_next, 2) + 16 * bj * DK, qo.q);
-                r12(bc, bj)[lane] = quad_of<E>(mma_q<E, DKB>(z, k2, qq));
             }
         } else {
             store_out(on, stride, nvalid, bc, o, scale);
@@ -944,7 +973,7 @@ struct Fused {
                 if constexpr (PAIR) {
                     // chains start on block boundaries, so even sub-blocks open a block
                     const int half = j & 1;
-                    n_block_pair(j % 3, (j + 1) % 3, half, half, bc, half, half == 0 && nv(j + 1) > 0, pc.on,
+                    n_block_pair(j % 3, half, half, bc, half, half == 0 && nv(j + 1) > 0, pc.on,
                                  on_prev, c.vst, nv(j), nv(j - 1), c.scale, qo);
                     on_prev = pc.on;
                 } else if constexpr (SMALL) {
