@@ -28,6 +28,7 @@ def _view(B, T, hqk, hv, seed, lengths=None):
     (2, 96, 2, 2, 32, None, 2),
     (1, 130, 1, 2, 16, None, 3),                 # grouped heads, ragged tail
     (1, 160, 2, 2, 32, [64, 32, 64], 2),         # packed documents
+    (1, 150, 1, 2, 4, None, 3),                  # small blocks: the first pass on 32-position chunks
 ])
 def test_views_match_oracle(B, T, hqk, hv, L, lengths, n_views, route):
     print(f"views B={B} T={T} hqk={hqk} hv={hv} L={L} n={n_views} lengths={lengths} route={route}", flush=True)
