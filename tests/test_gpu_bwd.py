@@ -112,6 +112,8 @@ def test_bwd_tiny_f32_full_config():
     (1, 160, 2, 2, 32, {"lengths": [64, 32, 64]}),           # packed documents
     (1, 80, 1, 1, 32, {"h0": True, "dht": True}),            # initial state, final-state gradient
     (1, 64, 1, 1, 8, {"do_dtype": torch.bfloat16}),         # bf16 upstream gradients, small blocks
+    (1, 37, 1, 2, 1, {"dht": True}),                        # blocks of one position
+    (1, 76, 1, 1, 4, {"lengths": [32, 0, 44], "h0": True}), # blocks of four, packed
     (1, 116, 1, 1, 32, {"lengths": [64, 0, 32, 20], "h0": True}),   # an empty document, a partial last one
     (1, 20, 1, 1, 32, {"dht": True}),                       # a sequence shorter than one block
     (3, 33, 1, 1, 32, {"h0": True}),                        # a one-position tail block
