@@ -108,6 +108,20 @@ def test_small_blocks(B, T, hqk, hv, d, L, lengths):
         assert e <= TOL["bf16"]
 
 
+def test_small_blocks_bf16_outputs():
+    """The small-block kernel with bf16 outputs: the fp32-output kernel's results rounded, bit
+    for bit, and the same final state."""
+    inp = W.make_custom_train(2, 150, 2, 2, 128, 128, "bf16", seed=23)
+    d = to_dev(inp)
+    o16, on16, ht16 = bd.bdgdn_fwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"],
+                                         d["qn"], d["kn"], d["vn"], d["gn"], d["betan"],
+                                         block=4, scale=0.0884, want_ht=True, out_dtype=torch.bfloat16)
+    o32, on32, ht32 = _run_gpu(d, 4, 0.0884)
+    assert o16.dtype == torch.bfloat16 and on16.dtype == torch.bfloat16
+    assert torch.equal(o32.to(torch.bfloat16), o16) and torch.equal(on32.to(torch.bfloat16), on16)
+    assert torch.equal(ht32, ht16)
+
+
 @pytest.mark.parametrize("L", [1, 8])
 def test_full_small_blocks_all_units(L):
     """The block-size sweep's shape (1 x 4096 clean + 4096 noisy tokens, 16 heads, d = 128)
