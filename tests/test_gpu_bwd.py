@@ -122,12 +122,13 @@ def test_bwd_matches_oracle(B, T, hqk, hv, L, kw):
     _check(B, T, hqk, hv, L, 300 + T + L, **kw)
 
 
-def _all_units(got, ref, B, tol=TOL["bf16"]):
-    """Worst per-unit max |err| / RMS of every gradient, over all (sequence, head) units."""
+def _all_units(got, ref, B, tol=TOL["bf16"], cu=None):
+    """Worst per-unit max |err| / RMS of every gradient, over all (sequence or document, head)
+    units."""
     worst = {}
     for name in NAMES + ("dh0",):
         kind = None if name == "dh0" else (name in ("dg", "dbeta", "dgn", "dbetan"))
-        e, where, n = unit_errors(got[name], ref[name], per_token=kind)
+        e, where, n = unit_errors(got[name], ref[name], cu=None if kind is None else cu, per_token=kind)
         worst[name] = e
         print(f"  {name}: worst unit {where} {e:.2e} over {n} units", flush=True)
     for name, e in worst.items():
@@ -140,17 +141,21 @@ def _full_size_bwd(B, T, hqk, hv, L, inp, seed):
     do = torch.from_numpy(rng.standard_normal(shape, dtype=np.float32))
     don = torch.from_numpy(rng.standard_normal(shape, dtype=np.float32))
     scale = 1.0 / math.sqrt(128)
-    d = {k: v.cuda() for k, v in inp.items()}
-    print(f"bwd B={B} T={T} hqk={hqk} hv={hv} L={L}: GPU", flush=True)
+    cu = inp.get("cu_seqlens")
+    d = {k: v.cuda() for k, v in inp.items() if isinstance(v, torch.Tensor)}
+    print(f"bwd B={B} T={T} hqk={hqk} hv={hv} L={L} documents={None if cu is None else len(cu) - 1}: GPU",
+          flush=True)
     got = bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
-                             d["betan"], do.cuda(), don.cuda(), block=L, scale=scale, want_dh0=True)
+                             d["betan"], do.cuda(), don.cuda(), block=L, scale=scale, want_dh0=True,
+                             cu_seqlens=d.get("cu_seqlens"), cu_seqlens_host=cu)
     torch.cuda.synchronize()
     got = {k: v.cpu() for k, v in got.items()}
     del d
     print("  oracle", flush=True)
     ref = oracle.bwd_train(inp["q"], inp["k"], inp["v"], inp["g"], inp["beta"], inp["qn"], inp["kn"], inp["vn"],
-                           inp["gn"], inp["betan"], do, don, block=L, scale=scale)
-    _all_units(got, ref, B)
+                           inp["gn"], inp["betan"], do, don, block=L, scale=scale,
+                           cu_seqlens=None if cu is None else cu.numpy())
+    _all_units(got, ref, B, cu=None if cu is None else cu.numpy())
 
 
 def test_bwd_training_workload_all_units():
@@ -166,6 +171,13 @@ def test_bwd_grouped_heads_long_sequences_all_units():
     over its two v heads)."""
     B, T, hqk, hv, L = 2, 16384, 16, 32, 32
     _full_size_bwd(B, T, hqk, hv, L, W.make_custom_train(B, T, hqk, hv, 128, 128, "bf16", seed=1234), 93)
+
+
+def test_bwd_packed_workload_all_units():
+    """The packed workload (32 documents, 131072 + 131072 tokens, 16 heads, L = 32), run whole
+    on the GPU; every (document, head) unit of every gradient compared with one oracle call."""
+    w = W.VARLEN_128K
+    _full_size_bwd(w.batch, w.seqlen, w.h_qk, w.h_v, w.block, W.make_train(w), 95)
 
 
 def test_bwd_grouped_value_workload_blocks_of_64_all_units():
