@@ -654,30 +654,38 @@ def main():
             "views2_ms_per_call": bvms, "views2_tokens_per_s": 3 * w.tokens / (bvms * 1e-3)}
         del bws, bgrads, bvgrads, bviews
         torch.cuda.empty_cache()
-        # the other training workloads: the tiny fp32 one (the per-step fp32 backward) and the
+        # the other training workloads: the tiny fp32 one (the per-step fp32 backward), the
         # grouped-value one (blocks of 64: the block form with noisy blocks of two sub-blocks)
+        # and the packed 128k one (32 documents)
         per_step = {}
+        block_form = ("bdgdn_k2_scan_states_kernel (seed states) + bdgdn_bwd_noisy_kernel + "
+                      "bdgdn_bwd_scan_kernel + bdgdn_bwd_clean_kernel")
         paths = {"tiny_f32": ("bdgdn_bwd_gen_ckpt_kernel + bdgdn_bwd_gen_walk_kernel (fp32, per step)", 1, 3, 1),
                  "gva_16k": ("bdgdn_k2_scan_states_kernel (seed states per 32-position sub-block) + "
-                        "bdgdn_bwd_pair_kernel + bdgdn_bwd_scan_kernel + bdgdn_bwd_clean_kernel", 3, 10, 3)}
-        for key, pw in (("tiny_f32", W.TINY_F32), ("gva_16k", W.GVA_16K)):
-            pin = {k_: v_.to(dev) for k_, v_ in W.make_train(pw).items()}
+                        "bdgdn_bwd_pair_kernel + bdgdn_bwd_scan_kernel + bdgdn_bwd_clean_kernel", 3, 10, 3),
+                 "varlen_128k": (block_form, 3, 10, 3)}
+        for key, pw in (("tiny_f32", W.TINY_F32), ("gva_16k", W.GVA_16K), ("varlen_128k", W.VARLEN_128K)):
+            praw = W.make_train(pw)
+            pin = {k_: v_.to(dev) for k_, v_ in praw.items() if isinstance(v_, torch.Tensor)}
+            pcu = praw.get("cu_seqlens")
+            pkw = {} if pcu is None else {"cu_seqlens": pin["cu_seqlens"], "cu_seqlens_host": pcu}
             pshape = (pw.batch, pw.seqlen, pw.h_v, pw.d_v)
             pdo = torch.randn(pshape, generator=torch.Generator(device=dev).manual_seed(8), device=dev)
             pdon = torch.randn(pshape, generator=torch.Generator(device=dev).manual_seed(9), device=dev)
-            pdesc = bd.make_fwd_desc(pin["q"], pin["v"], block=pw.block, out_dtype=torch.float32)
+            pdesc = bd.make_fwd_desc(pin["q"], pin["v"], block=pw.block, out_dtype=torch.float32,
+                                     num_seqs=0 if pcu is None else len(pcu) - 1)
             pws = torch.empty(bd.bdgdn_bwd_train_workspace(pdesc), dtype=torch.uint8, device=dev)
             pscale = 1.0 / math.sqrt(pw.d_k)
             pargs = [pin[k_] for k_ in ("q", "k", "v", "g", "beta", "qn", "kn", "vn", "gn", "betan")]
-            pgrads = bd.bdgdn_bwd_train(*pargs, pdo, pdon, block=pw.block, scale=pscale, workspace=pws)
+            pgrads = bd.bdgdn_bwd_train(*pargs, pdo, pdon, block=pw.block, scale=pscale, workspace=pws, **pkw)
 
             def pstep():
                 bd.bdgdn_bwd_train(*pargs, pdo, pdon, block=pw.block, scale=pscale, workspace=pws, grads=pgrads,
-                                   stream=stream)
+                                   stream=stream, **pkw)
             kern, pwarm, piters, prep = paths[key]
             pms = time_protocol(pstep, stream, flush, warmup=pwarm, iters=piters, repeats=prep,
                                 trim=1 if piters >= 10 else 0)[0]
-            per_step[key] = {"workload": pw.name, "ms_per_call": pms, "tokens_per_s": pw.tokens / (pms * 1e-3),
+            per_step[key] = {"workload": pw.name, "ms_per_call": pms, "tokens_per_s": 2 * pw.tokens / (pms * 1e-3),
                              "workspace_bytes": pws.numel(), "kernels": kern}
             del pin, pws, pgrads
             torch.cuda.empty_cache()
