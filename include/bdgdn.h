@@ -446,7 +446,7 @@ int bdgdn_shortconv_bwd(const bdgdn_conv_desc_t *desc, const void *x, const void
  * that the library holds on each GPU it runs on until the process ends (looked up on the
  * first call on a device; the stream's device, or the current device for a NULL stream).
  * Inputs needing more than that (bdgdn_shortconv_bwd_workspace(desc) bytes: 4 (width + 1)
- * channels bytes per started group of 512 rows, e.g. 3.75 MiB for 16384 rows of 6144
+ * channels bytes per started group of 1024 rows, e.g. 1.9 MiB for 16384 rows of 6144
  * channels at width 4) return BDGDN_ERR_SCRATCH before anything is launched.  Every call on one GPU
  * shares that GPU's scratch: calls whose execution overlaps on one GPU (different streams,
  * or threads launching concurrently) race and give undefined dw / dbias; serialise them

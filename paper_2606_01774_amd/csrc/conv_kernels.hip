@@ -41,7 +41,7 @@ namespace {
 // Tile shapes: rows per wave tile (forward), rows per thread and rows per prefetched chunk
 // (backward), bytes of channels per lane.
 constexpr int kFwdTN = 8, kFwdVB = 8;
-constexpr int kBwdTR = 128, kBwdU = 4, kBwdVB = 4;
+constexpr int kBwdTR = 256, kBwdU = 4, kBwdVB = 4;
 
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 

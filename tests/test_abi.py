@@ -298,16 +298,16 @@ def test_shortconv_noalloc_validation_and_limit():
     assert call(channels=0) == bd.BDGDN_ERR_INVALID_ARG
     assert call(null_x=True) == bd.BDGDN_ERR_INVALID_ARG
     assert call(activation=3) == bd.BDGDN_ERR_INVALID_ARG
-    # partials: (width + 1) x channels fp32 per started group of 512 rows
+    # partials: (width + 1) x channels fp32 per started group of 1024 rows
     per_group = 5 * 6144 * 4
     groups = bd.BDGDN_NOALLOC_SCRATCH_BYTES // per_group
-    fits = dict(batch=1, seqlen=512 * groups, channels=6144)
-    over = dict(batch=1, seqlen=512 * groups + 1, channels=6144)
+    fits = dict(batch=1, seqlen=1024 * groups, channels=6144)
+    over = dict(batch=1, seqlen=1024 * groups + 1, channels=6144)
     ws = lambda kw: lib.bdgdn_shortconv_bwd_workspace(ctypes.byref(bd.ConvDesc(
         **dict(dict(batch=2, seqlen=64, num_seqs=0, channels=256, width=4, block=8, activation=1, dtype=0), **kw))))
     assert ws(fits) <= bd.BDGDN_NOALLOC_SCRATCH_BYTES < ws(over)
     assert call(**over) == bd.BDGDN_ERR_SCRATCH
-    assert call(batch=4, seqlen=1 << 20, channels=512, width=2) == bd.BDGDN_ERR_SCRATCH
+    assert call(batch=8, seqlen=1 << 20, channels=512, width=2) == bd.BDGDN_ERR_SCRATCH
     assert "scratch" in bd.bdgdn_status_string(bd.BDGDN_ERR_SCRATCH)
 
 

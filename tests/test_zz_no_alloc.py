@@ -51,7 +51,7 @@ def test_noalloc_matches_workspace_entry_point_twice():
 
 def test_noalloc_rejects_inputs_beyond_the_scratch():
     per_group = 5 * 6144 * 4
-    rows = 512 * (bd.BDGDN_NOALLOC_SCRATCH_BYTES // per_group) + 1
+    rows = 1024 * (bd.BDGDN_NOALLOC_SCRATCH_BYTES // per_group) + 1
     print(f"noalloc: {rows} rows x 6144 channels (beyond the scratch)", flush=True)
     x = torch.zeros(1, rows, 6144, dtype=torch.bfloat16, device="cuda")
     w = torch.zeros(6144, 4, device="cuda")
