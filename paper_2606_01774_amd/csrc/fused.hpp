@@ -613,11 +613,12 @@ struct Fused {
     //     O~ = diag(gamma~_end) [diag(2^c) Q~ S0 + (Q~ K^T o M) Delta] + (R o B) Delta~,
     // with Delta~ = T~ (V~ - Gamma~ X~), the noisy gates restarting at each noisy block
     // (Gamma~, gamma~_end at the block's last position, R_rc = 2^(G~_end - G~_c) q~_r . k~_c)
-    // and B, T~ block diagonal over the noisy blocks.  The Gram tiles K~ K^T, Q~ K^T and R are
-    // in the A-operand layout (lane (g, n): row 16 bi + n, column 16 bj + 4 g + i); the noisy
-    // U wave formed the first two a step earlier (raw, fp32 in LDS) and they are masked here.
-    // Noisy row quads are read from LDS where each product uses them (the quad loads are not
-    // merged), which keeps the register footprint within three waves per SIMD.
+    // and B, T~ block diagonal over the noisy blocks.  The Gram tiles K~ K^T, Q~ K^T (tiles
+    // bj <= bi) and the diagonal tiles of R are in the A-operand layout (lane (g, n): row
+    // 16 bi + n, column 16 bj + 4 g + i); the noisy U wave formed them a step earlier (raw, fp32
+    // in LDS) and they are masked here.  Row quads are read from LDS where each product uses
+    // them (the quad loads are not merged), which keeps the register footprint within three
+    // waves per SIMD.
     __device__ __forceinline__ void n_block_small(int slot, int p, int sb, int bc, Out *on, int stride, int nvalid,
                                                   float scale, int nl, const QOffs &qo) const
     {
@@ -663,7 +664,6 @@ struct Fused {
 #pragma unroll
             for (int i = 0; i < 4; ++i) ec[rb][i] = fexp2(cb[i]);
         }
-        // clean-key tile bj against the rows x (A-operand layout of x K^T), masked
         // the cross Gram tile (which: 0 K~ K^T, 1 Q~ K^T), masked
         auto cross = [&](int which, int bi, int bj) { return bj > bi ? zq : masked(xg(p, which, bi, bj)[lane], bi, bj); };
         // X~ and Delta~
