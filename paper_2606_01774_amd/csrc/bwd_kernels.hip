@@ -1402,34 +1402,46 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
 // The range of the upstream gradients (dO, dO~ of every view, dht): each block's max |x| over
 // its grid-stride share of every array into part[blockIdx.x].  With Od = bf16 the output
 // gradients are bf16 (dht is always fp32).
+__device__ __forceinline__ float absmax4(f32x4 v)
+{
+    return fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3])));
+}
+__device__ __forceinline__ float absmax8(bf16x8 v)
+{
+    float m = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf((float)v[j]));
+    return m;
+}
+// max |x| over this block's contiguous segment of x[0 .. n), eight 16-byte loads in flight
+// per thread
+template <typename V, typename F>
+__device__ __forceinline__ float range_max(const V *x, long n, float m, const F &absmax)
+{
+    const long seg = (n + gridDim.x - 1) / gridDim.x;
+    const long end = min(n, seg * (blockIdx.x + 1));
+    long e = seg * blockIdx.x + threadIdx.x;
+    for (; e + 7 * 256 < end; e += 8 * 256) {
+        V v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = x[e + u * 256];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) m = fmaxf(m, absmax(v[u]));
+    }
+    for (; e < end; e += 256) m = fmaxf(m, absmax(x[e]));
+    return m;
+}
 template <typename Od>
 __global__ void __launch_bounds__(256) bdgdn_bwd_range_kernel(RangeArgs r)
 {
     __shared__ float red[4];
-    const long stride = (long)gridDim.x * 256;
     float m = 0.f;
     for (int i = 0; i < r.count; ++i) {
         const long n8 = r.n[i] / 8;   // 8-element vectors (every length is a multiple of 128)
-        if (i == r.count - 1 && r.last_f32) {
-            const f32x4 *x = static_cast<const f32x4 *>(r.arr[i]);
-            for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < 2 * n8; e += stride) {
-                const f32x4 v = x[e];
-                m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
-            }
-        } else if constexpr (sizeof(Od) == 2) {
-            const bf16x8 *x = static_cast<const bf16x8 *>(r.arr[i]);
-            for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < n8; e += stride) {
-                const bf16x8 v = x[e];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf((float)v[j]));
-            }
-        } else {
-            const f32x4 *x = static_cast<const f32x4 *>(r.arr[i]);
-            for (long e = (long)blockIdx.x * 256 + threadIdx.x; e < 2 * n8; e += stride) {
-                const f32x4 v = x[e];
-                m = fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
-            }
-        }
+        if (sizeof(Od) == 2 && !(i == r.count - 1 && r.last_f32))
+            m = range_max(static_cast<const bf16x8 *>(r.arr[i]), n8, m, absmax8);
+        else
+            m = range_max(static_cast<const f32x4 *>(r.arr[i]), 2 * n8, m, absmax4);
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
