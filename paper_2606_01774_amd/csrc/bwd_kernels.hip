@@ -1228,7 +1228,7 @@ constexpr int kScanWaves = 4;   // waves per workgroup (2: 16 columns, two workg
 template <int TC> struct ScanSmem {
     _Float16 UK[NP * LDH];       // U K of the block (32 x 128)
     _Float16 dHt[TC * LDH];      // dh_b transposed: the tile's TC columns x 128 rows
-    _Float16 Kt[2][DD * LDK];    // K^T (128 x 32), two buffers
+    _Float16 Kr[2][NP * LDH];    // K (32 x 128, row-major; its transpose is read by transpose loads), two buffers
     _Float16 Zt[TC * LDK];       // Z transposed: TC columns x 32 positions
 };
 }  // namespace
@@ -1344,8 +1344,10 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
 #pragma unroll
         for (int i = 0; i < NC; ++i) {
             *reinterpret_cast<f16x8 *>(sm.UK + sr * LDH + sc + 8 * i) = cur.uk[i];
+            f16x8 kh;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) sm.Kt[buf][(sc + 8 * i + j) * LDK + sr] = (_Float16)(float)cur.k[i][j];
+            for (int j = 0; j < 8; ++j) kh[j] = (_Float16)(float)cur.k[i][j];
+            *reinterpret_cast<f16x8 *>(sm.Kr[buf] + sr * LDH + sc + 8 * i) = kh;
         }
         // dh_b is in LDS now: keep gamma_n dh_b + cterm_b in its registers
 #pragma unroll
@@ -1370,8 +1372,11 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
         for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
             for (int tn = 0; tn < CT; ++tn) {
-                const f32x4 c = tile_mma<_Float16, NP>(z, sm.Kt[buf] + (rw + 16 * tl) * LDK, LDK,
-                                                       sm.Zt + 16 * tn * LDK, LDK, lane);
+                // K^T Z: the A operand K^T by transpose loads of the row-major K, positions in two
+                // 16-halves (the same k order as the Zt operand's)
+                const int m0 = rw + 16 * tl;
+                const f32x4 c = mfma(op_tr(sm.Kr[buf], LDH, 16, m0, lane), op_row(sm.Zt, LDK, 16 * tn, 16, lane),
+                                     mfma(op_tr(sm.Kr[buf], LDH, 0, m0, lane), op_row(sm.Zt, LDK, 16 * tn, 0, lane), z));
 #pragma unroll
                 for (int j = 0; j < 4; ++j) dh[tl][tn][j] -= c[j];
             }
