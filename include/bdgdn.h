@@ -236,6 +236,24 @@ int bdgdn_fwd_train_views(const bdgdn_fwd_desc_t *desc,
  * tile) (fp32).  0 for a descriptor it would reject. */
 size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
 
+/* Bytes of device workspace bdgdn_bwd_train (and bdgdn_bwd_train_views) needs when run in
+ * `segments` time segments (Appendix "Backward primitives": the strided clean-state
+ * checkpoints of the checkpoint build, with the stride chosen as in "Choosing the stride"):
+ * every chain's clean blocks (sub-blocks of half the block for blocks of 34 .. 64) are cut
+ * into segments of ceil(longest chain's blocks / segments) (even for sub-blocks), the clean
+ * state at each segment start after the first is kept (fp32, one per (sequence, v-head)),
+ * and the segments run last first, each recomputing its own seeds from its checkpoint, so
+ * that the per-block workspace above holds the first segment's blocks only (for every
+ * sequence, min(its blocks, the segment length)), plus the checkpoints, one fp32
+ * state-gradient carry per (sequence, v-head) and the segment tables.
+ *   cu_seqlens_host   [N+1] document offsets when desc->num_seqs > 0, else NULL
+ *   segments          >= 1; 1 gives bdgdn_bwd_train_workspace(desc); more than the longest
+ *                     chain's blocks count as that many
+ * Per-step shapes need no more than bdgdn_bwd_train_workspace(desc) and are never segmented
+ * (that value for any segments).  0 for a descriptor it would reject or missing packing. */
+size_t bdgdn_bwd_train_workspace_segmented(const bdgdn_fwd_desc_t *desc, const int32_t *cu_seqlens_host,
+                                           int segments);
+
 /*
  * Backward of bdgdn_fwd_train (Appendix "Backward primitives": the noisy block-end
  * readout backward, eq. noisy-readout-bwd; the block-level chain rule,
@@ -250,8 +268,15 @@ size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc);
  *   dv, dvn              [B*T][h_v][d_v] fp32
  *   dg, dbeta, dgn, dbetan  [B*T][h_v] fp32 (gradients of the log-gates and step sizes)
  *   dh0                  [B or N][h_v][d_k][d_v] fp32 gradient of h0, or NULL
- *   workspace            at least bdgdn_bwd_train_workspace(desc) bytes, 256-byte aligned,
- *                        owned by the call until the stream passes it
+ *   workspace            256-byte aligned, owned by the call until the stream passes it;
+ *                        at least bdgdn_bwd_train_workspace(desc) bytes runs the blocks of
+ *                        every chain at once.  A smaller one runs the block-form shapes in
+ *                        the fewest time segments s >= 2 with
+ *                        bdgdn_bwd_train_workspace_segmented(desc, cu_seqlens_host, s) <=
+ *                        workspace_bytes (the same results bit for bit: the checkpoints
+ *                        and the carry are the fp32 values the one-pass call keeps on
+ *                        chip; one more clean-scan pass over all but the last segment and
+ *                        more, smaller launches); BDGDN_ERR_WORKSPACE if none fits
  * Every gradient row is overwritten.  bf16 inputs with d_k = d_v = 128 and blocks of at
  * most 32 positions run the block-form kernels; fp32 inputs (blocks of at most 32), d_k or
  * d_v of 64, and bf16 blocks of 33 .. 64 positions run the per-step fp32 backward (one

@@ -24,7 +24,8 @@ __all__ = [
     "bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_workspace", "bdgdn_fwd_train",
     "bdgdn_commit_record", "bdgdn_accept_states", "BDGDN_ACT_NONE", "BDGDN_ACT_SILU",
     "bdgdn_shortconv_fwd", "bdgdn_shortconv_bwd_workspace", "bdgdn_shortconv_bwd",
-    "bdgdn_bwd_train_workspace", "bdgdn_bwd_train", "bdgdn_fwd_train_views_workspace", "bdgdn_fwd_train_views",
+    "bdgdn_bwd_train_workspace", "bdgdn_bwd_train_workspace_segmented", "bdgdn_bwd_train",
+    "bdgdn_fwd_train_views_workspace", "bdgdn_fwd_train_views",
     "bdgdn_bwd_train_views_workspace", "bdgdn_bwd_train_views", "bdgdn_denoise_step", "bdgdn_commit", "library_path", "load_library", "EXPORTED_SYMBOLS",
 ]
 
@@ -55,7 +56,7 @@ EXPORTED_SYMBOLS = ("bdgdn_version", "bdgdn_status_string", "bdgdn_fwd_train_wor
                     "bdgdn_shortconv_bwd", "bdgdn_bwd_train_workspace", "bdgdn_bwd_train",
                     "bdgdn_fwd_train_views_workspace", "bdgdn_fwd_train_views",
                     "bdgdn_bwd_train_views_workspace", "bdgdn_bwd_train_views",
-                    "bdgdn_shortconv_bwd_noalloc")
+                    "bdgdn_shortconv_bwd_noalloc", "bdgdn_bwd_train_workspace_segmented")
 
 
 class FwdDesc(ctypes.Structure):
@@ -137,6 +138,8 @@ def load_library():
     lib.bdgdn_fwd_train_views.restype = ctypes.c_int
     lib.bdgdn_bwd_train_workspace.argtypes = [ctypes.POINTER(FwdDesc)]
     lib.bdgdn_bwd_train_workspace.restype = ctypes.c_size_t
+    lib.bdgdn_bwd_train_workspace_segmented.argtypes = [ctypes.POINTER(FwdDesc), P, ctypes.c_int32]
+    lib.bdgdn_bwd_train_workspace_segmented.restype = ctypes.c_size_t
     lib.bdgdn_bwd_train.argtypes = [ctypes.POINTER(FwdDesc)] + [P] * 28 + [ctypes.c_size_t, P]
     lib.bdgdn_bwd_train.restype = ctypes.c_int
     lib.bdgdn_bwd_train_views_workspace.argtypes = [ctypes.POINTER(FwdDesc)]
@@ -334,17 +337,33 @@ def bdgdn_bwd_train_workspace(desc: FwdDesc) -> int:
     return int(load_library().bdgdn_bwd_train_workspace(ctypes.byref(desc)))
 
 
+def bdgdn_bwd_train_workspace_segmented(desc: FwdDesc, cu_seqlens_host, segments: int) -> int:
+    """Workspace of the backward run in ``segments`` time segments (cu_seqlens_host: the
+    packing as an int32 CPU tensor, or None)."""
+    cu_h = None if cu_seqlens_host is None else torch.as_tensor(cu_seqlens_host, dtype=torch.int32).contiguous()
+    return int(load_library().bdgdn_bwd_train_workspace_segmented(
+        ctypes.byref(desc), None if cu_h is None else ctypes.c_void_p(cu_h.data_ptr()), int(segments)))
+
+
+def _bwd_workspace(desc, cu_h, segments, full, device):
+    """The backward's workspace: the full size, or that of ``segments`` time segments."""
+    ws_bytes = full if segments is None else bdgdn_bwd_train_workspace_segmented(desc, cu_h, segments)
+    return torch.empty(ws_bytes, dtype=torch.uint8, device=device) if ws_bytes else None
+
+
 _BWD_NAMES = ("dq", "dk", "dv", "dg", "dbeta", "dqn", "dkn", "dvn", "dgn", "dbetan")
 
 
 def bdgdn_bwd_train(q, k, v, g, beta, qn, kn, vn, gn, betan, do, don, *, block, scale=None,
                     cu_seqlens=None, cu_seqlens_host=None, h0=None, dht=None, want_dh0=False,
-                    grads=None, workspace=None, stream=None):
+                    grads=None, workspace=None, segments=None, stream=None):
     """Backward of bdgdn_fwd_train: gradients of sum(do*o) + sum(don*on) + sum(dht*ht).
     Inputs as for bdgdn_fwd_train; do, don [B,T,h_v,d_v] in the forward's output dtype
     (fp32 or bf16); dht like ht or None.  Returns a dict of fp32 tensors (dq, dk, dv, dg,
     dbeta and the noisy dqn, ..., dbetan; dh0 when want_dh0).  ``grads`` may supply the
-    output tensors (same names)."""
+    output tensors (same names).  Without ``workspace``, one of the full size is allocated,
+    or with ``segments`` that of that many time segments (the library then runs the
+    segmented schedule)."""
     lib = load_library()
     dt = q.dtype
     for name, t in (("q", q), ("k", k), ("v", v), ("qn", qn), ("kn", kn), ("vn", vn)):
@@ -374,9 +393,8 @@ def bdgdn_bwd_train(q, k, v, g, beta, qn, kn, vn, gn, betan, do, don, *, block, 
         out["dh0"] = torch.empty(units, v.shape[2], q.shape[3], v.shape[3], dtype=torch.float32, device=q.device)
     _dev(h0, "h0", torch.float32)
     _dev(dht, "dht", torch.float32)
-    ws_bytes = bdgdn_bwd_train_workspace(desc)
-    if workspace is None and ws_bytes:
-        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    if workspace is None:
+        workspace = _bwd_workspace(desc, cu_h, segments, bdgdn_bwd_train_workspace(desc), q.device)
     ws_size = 0 if workspace is None else workspace.numel() * workspace.element_size()
     st = lib.bdgdn_bwd_train(
         ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
@@ -398,12 +416,13 @@ _VIEW_GRAD_NAMES = ("dq", "dk", "dv", "dg", "dbeta")
 
 def bdgdn_bwd_train_views(q, k, v, g, beta, views, do, *, block, scale=None, cu_seqlens=None,
                           cu_seqlens_host=None, h0=None, dht=None, want_dh0=False, grads=None, workspace=None,
-                          stream=None):
+                          segments=None, stream=None):
     """Backward of bdgdn_fwd_train_views: gradients of sum(do*o) + sum_i sum(views[i]["do"]*o_i)
     + sum(dht*ht).  ``views`` is a list of dicts with the view's q, k, v, g, beta and the
     upstream gradient "do" of its readout.  Returns (clean, per_view): ``clean`` a dict of
     fp32 tensors dq, dk, dv, dg, dbeta (and dh0 when want_dh0), ``per_view`` one such dict per
-    view.  ``grads`` may supply them (a previous call's result)."""
+    view.  ``grads`` may supply them (a previous call's result).  ``workspace`` and
+    ``segments`` as for bdgdn_bwd_train."""
     lib = load_library()
     dt = q.dtype
     for name, t in (("q", q), ("k", k), ("v", v)):
@@ -446,9 +465,8 @@ def bdgdn_bwd_train_views(q, k, v, g, beta, views, do, *, block, scale=None, cu_
         clean["dh0"] = torch.empty(units, v.shape[2], q.shape[3], v.shape[3], dtype=torch.float32, device=q.device)
     _dev(h0, "h0", torch.float32)
     _dev(dht, "dht", torch.float32)
-    ws_bytes = bdgdn_bwd_train_views_workspace(desc)
-    if workspace is None and ws_bytes:
-        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    if workspace is None:
+        workspace = _bwd_workspace(desc, cu_h, segments, bdgdn_bwd_train_views_workspace(desc), q.device)
     ws_size = 0 if workspace is None else workspace.numel() * workspace.element_size()
     st = lib.bdgdn_bwd_train_views(
         ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), arr, n,

@@ -357,7 +357,7 @@ int bdgdn_fwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         ia.nblk = (desc->seqlen + desc->block - 1) / desc->block;
         ia.total_blocks = total_blocks(desc);
         ia.h_qk = desc->h_qk; ia.h_v = desc->h_v;
-        ScanArgs sa;
+        ScanArgs sa = {};
         sa.q = q; sa.k = k; sa.v = v; sa.qn = qn; sa.kn = kn; sa.vn = vn;
         sa.g = g; sa.beta = beta; sa.gn = gn; sa.betan = betan;
         sa.cu = packed ? cu_seqlens_dev : nullptr;
@@ -637,19 +637,95 @@ static bdgdn_fwd_desc_t bwd_sub(const bdgdn_fwd_desc_t *d)
 struct BwdLayout {
     size_t seeds, cterm, uk, gnb, part, range, total;
 };
+static size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
+static BwdLayout bwd_layout_units(size_t units, const bdgdn_fwd_desc_t *d, size_t base)
+{
+    const size_t st = (size_t)d->d_k * d->d_v;
+    BwdLayout l;
+    l.seeds = base;
+    l.cterm = l.seeds + up256(units * st * 2);
+    l.uk = l.cterm + up256(units * st * 2);
+    l.gnb = l.uk + up256(units * 32 * d->d_k * 2);
+    l.part = l.gnb + up256(units * 4);
+    l.range = l.part + up256(kRangeBlocks * 4);
+    l.total = l.range + 256;
+    return l;
+}
 static BwdLayout bwd_layout(const bdgdn_fwd_desc_t *d)
 {
-    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
     const bdgdn_fwd_desc_t sub = bwd_sub(d);
-    const size_t units = (size_t)total_blocks(&sub) * d->h_v, st = (size_t)d->d_k * d->d_v;
-    BwdLayout l;
-    l.seeds = 0;
-    l.cterm = l.seeds + up(units * st * 2);
-    l.uk = l.cterm + up(units * st * 2);
-    l.gnb = l.uk + up(units * 32 * d->d_k * 2);
-    l.part = l.gnb + up(units * 4);
-    l.range = l.part + up(kRangeBlocks * 4);
-    l.total = l.range + 256;
+    return bwd_layout_units((size_t)total_blocks(&sub) * d->h_v, d, 0);
+}
+
+// The time-segmented block-form backward (Appendix "Backward primitives", the strided clean
+// checkpoints of the checkpoint build and "Choosing the stride"): every chain's clean blocks
+// (sub-blocks for noisy blocks of two) cut into segments of seg_len, the clean state kept
+// at each segment start after the first (fp32, one per chain), the segments then run last
+// first, each recomputing its own seeds from its checkpoint, so that the per-block
+// workspace holds one segment.  Segment 0 holds the most blocks: every chain contributes
+// min(its blocks, seg_len) to it.
+struct SegPlan {
+    int n_seg = 1, seg_len = 0;
+    long max_units = 0;               // clean (sub-)blocks of segment 0, all sequences
+    std::vector<long> units, pairs;   // per segment: clean (sub-)blocks, noisy blocks of two
+};
+static long chain_blocks(const bdgdn_fwd_desc_t *d, const int32_t *cu_host, int n, int Lc)
+{
+    const long len = d->num_seqs > 0 ? (long)cu_host[n + 1] - cu_host[n] : d->seqlen;
+    return (len + Lc - 1) / Lc;
+}
+// The plan for `segments` segments (fewer when the chains are short); false when packed
+// lengths are missing or invalid.  With counts = false only n_seg, seg_len and max_units.
+static bool seg_plan(const bdgdn_fwd_desc_t *d, const int32_t *cu_host, int segments, bool counts, SegPlan &p)
+{
+    const bool packed = d->num_seqs > 0;
+    const int nseq = packed ? d->num_seqs : d->batch;
+    if (segments < 1 || (packed && !cu_host)) return false;
+    if (packed && (cu_host[0] != 0 || cu_host[nseq] != d->seqlen)) return false;
+    const int Lc = bwd_sub(d).block;
+    long maxnb = 0;
+    for (int n = 0; n < nseq; ++n) {
+        if (packed && cu_host[n + 1] < cu_host[n]) return false;
+        maxnb = std::max(maxnb, chain_blocks(d, cu_host, n, Lc));
+    }
+    if (maxnb == 0) return false;
+    long S = (maxnb + segments - 1) / segments;
+    if (bwd_pairs(d)) S += S & 1;   // segments start on noisy-block boundaries
+    p.seg_len = (int)S;
+    p.n_seg = (int)((maxnb + S - 1) / S);
+    p.max_units = 0;
+    for (int n = 0; n < nseq; ++n) p.max_units += std::min(chain_blocks(d, cu_host, n, Lc), S);
+    if (counts) {
+        p.units.assign(p.n_seg, 0);
+        p.pairs.assign(p.n_seg, 0);
+        for (int n = 0; n < nseq; ++n) {
+            const long nb = chain_blocks(d, cu_host, n, Lc);
+            for (int k = 0; k < p.n_seg; ++k) {
+                const long c = std::max(0L, std::min(nb - (long)k * S, S));
+                p.units[k] += c;
+                p.pairs[k] += (c + 1) / 2;
+            }
+        }
+    }
+    return true;
+}
+// Workspace of the segmented backward: the checkpoints at segment starts 1 .. n_seg - 1, the
+// state-gradient carry (fp32 [seq][h_v][d_k][d_v] each), the segment tables, then the
+// per-block layout for segment 0's blocks.
+struct SegLayout {
+    size_t ckpt, carry, tab;
+    BwdLayout body;
+};
+static SegLayout seg_layout(const bdgdn_fwd_desc_t *d, const SegPlan &p)
+{
+    const int nseq = d->num_seqs > 0 ? d->num_seqs : d->batch;
+    const size_t state = (size_t)nseq * d->h_v * d->d_k * d->d_v * sizeof(float);
+    SegLayout l;
+    l.ckpt = 0;
+    l.carry = l.ckpt + up256((size_t)(p.n_seg - 1) * state);
+    l.tab = l.carry + up256(state);
+    const size_t tab_bytes = 2 * (size_t)p.n_seg * (nseq + 1) * sizeof(int);
+    l.body = bwd_layout_units((size_t)p.max_units * d->h_v, d, l.tab + up256(tab_bytes));
     return l;
 }
 
@@ -673,6 +749,17 @@ size_t bdgdn_bwd_train_workspace(const bdgdn_fwd_desc_t *desc)
     if (desc->batch <= 0 || desc->seqlen <= 0) return 0;
     if (bwd_shape_ok(desc)) return bwd_layout(desc).total;
     return bwd_generic_ok(desc, 1) ? bwd_generic_bytes(desc) : 0;
+}
+
+size_t bdgdn_bwd_train_workspace_segmented(const bdgdn_fwd_desc_t *desc, const int32_t *cu_seqlens_host,
+                                           int segments)
+{
+    const size_t full = bdgdn_bwd_train_workspace(desc);
+    if (full == 0 || segments < 1) return 0;
+    if (!bwd_shape_ok(desc) || segments == 1) return full;
+    SegPlan p;
+    if (!seg_plan(desc, cu_seqlens_host, segments, false, p)) return 0;
+    return p.n_seg > 1 ? seg_layout(desc, p).body.total : full;
 }
 
 // The backward of the clean stream and noisy view 0 (qn .. dbetan), plus n_more further views.
@@ -702,8 +789,22 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     }
     if (desc->seqlen == 0) return BDGDN_OK;
     const size_t need = bdgdn_bwd_train_workspace(desc);
-    if (workspace_bytes < need || !workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0)
-        return BDGDN_ERR_WORKSPACE;
+    if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return BDGDN_ERR_WORKSPACE;
+    // below the full workspace, the block-form backward runs in the fewest time segments
+    // whose workspace fits
+    SegPlan plan;
+    bool segmented = false;
+    if (workspace_bytes < need) {
+        if (generic) return BDGDN_ERR_WORKSPACE;
+        int K = 2;
+        for (;; ++K) {
+            if (!seg_plan(desc, cu_seqlens_host, K, false, plan)) return BDGDN_ERR_WORKSPACE;
+            if (plan.n_seg > 1 && seg_layout(desc, plan).body.total <= workspace_bytes) break;
+            if (plan.seg_len <= (bwd_pairs(desc) ? 2 : 1)) return BDGDN_ERR_WORKSPACE;   // no finer segments
+        }
+        seg_plan(desc, cu_seqlens_host, K, true, plan);
+        segmented = true;
+    }
     const bool packed = desc->num_seqs > 0;
     const int nseq = packed ? desc->num_seqs : desc->batch;
     const hipStream_t strm = static_cast<hipStream_t>(stream);
@@ -728,7 +829,8 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
     }
     unsigned char *ws = static_cast<unsigned char *>(workspace);
-    const BwdLayout lay = bwd_layout(desc);
+    const SegLayout sl = segmented ? seg_layout(desc, plan) : SegLayout{};
+    const BwdLayout lay = segmented ? sl.body : bwd_layout(desc);
     _Float16 *seeds = reinterpret_cast<_Float16 *>(ws + lay.seeds);
     const bdgdn_fwd_desc_t sub = bwd_sub(desc);   // the clean blocks
     const int Lc = sub.block;
@@ -757,8 +859,11 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
         for (int i = 0; i < nseq; ++i) sa.order[i] = idx[i];
         sa.n_order = nseq;
     }
-    hipError_t e = launch_scan_states(lp_of(Lc), false, true, sa, strm);
-    if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
+    hipError_t e = hipSuccess;
+    if (!segmented) {
+        e = launch_scan_states(lp_of(Lc), false, true, sa, strm);
+        if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
+    }
     // 2. the reverse walk over the blocks of every (sequence, v-head)
     BwdArgs a = {};
     a.q = q; a.k = k; a.v = v; a.qn = qn; a.kn = kn; a.vn = vn;
@@ -797,9 +902,41 @@ static int bwd_impl(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, 
     a.range = ra.range;
     e = launch_bwd_range(desc->out_dtype == BDGDN_BF16, ra, strm);
     if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
-    e = launch_bwd(desc->out_dtype == BDGDN_BF16, a, more, n_more, nseq * desc->h_v, total_blocks(&sub) * desc->h_v,
-                   bwd_pairs(desc) ? total_blocks(desc) * desc->h_v : 0, strm);
-    return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+    if (!segmented) {
+        e = launch_bwd(desc->out_dtype == BDGDN_BF16, a, more, n_more, nseq * desc->h_v,
+                       total_blocks(&sub) * desc->h_v, bwd_pairs(desc) ? total_blocks(desc) * desc->h_v : 0, strm);
+        return e == hipSuccess ? BDGDN_OK : BDGDN_ERR_LAUNCH;
+    }
+    // time segments: the tables, the checkpoints by a forward pass over segments 0 ..
+    // n_seg - 2, then each segment last first: its seeds from its checkpoint, its blocks
+    const size_t state = (size_t)nseq * desc->h_v * desc->d_k * desc->d_v;
+    float *ckpt = reinterpret_cast<float *>(ws + sl.ckpt);   // segment k's start state at ckpt + (k - 1) state
+    int *tab = reinterpret_cast<int *>(ws + sl.tab), *tabp = tab + (size_t)plan.n_seg * (nseq + 1);
+    e = launch_bwd_seg_plan(packed ? cu_seqlens_dev : nullptr, nseq, desc->seqlen, Lc, plan.seg_len, plan.n_seg, tab,
+                            tabp, strm);
+    if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
+    auto seg_states = [&](int k, bool checkpoint) {
+        sa.seg = tab + (size_t)k * (nseq + 1);
+        sa.blk0 = k * plan.seg_len;
+        sa.seg_len = plan.seg_len;
+        sa.h0 = k > 0 ? ckpt + (size_t)(k - 1) * state : h0;
+        sa.ht = checkpoint ? ckpt + (size_t)k * state : nullptr;
+        return launch_scan_states(lp_of(Lc), false, true, sa, strm);
+    };
+    for (int k = 0; k + 1 < plan.n_seg; ++k)
+        if (seg_states(k, true) != hipSuccess) return BDGDN_ERR_LAUNCH;
+    a.carry = reinterpret_cast<float *>(ws + sl.carry);
+    a.seg_len = plan.seg_len;
+    for (int k = plan.n_seg - 1; k >= 0; --k) {
+        if (seg_states(k, false) != hipSuccess) return BDGDN_ERR_LAUNCH;
+        a.seg = tab + (size_t)k * (nseq + 1);
+        a.segp = tabp + (size_t)k * (nseq + 1);
+        a.blk0 = k * plan.seg_len;
+        e = launch_bwd(desc->out_dtype == BDGDN_BF16, a, more, n_more, nseq * desc->h_v, plan.units[k] * desc->h_v,
+                       bwd_pairs(desc) ? plan.pairs[k] * desc->h_v : 0, strm);
+        if (e != hipSuccess) return BDGDN_ERR_LAUNCH;
+    }
+    return BDGDN_OK;
 }
 
 int bdgdn_bwd_train(const bdgdn_fwd_desc_t *desc, const void *q, const void *k, const void *v,

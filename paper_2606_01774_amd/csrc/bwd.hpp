@@ -33,6 +33,14 @@ struct BwdArgs {
                                              // fp16 operands times sigma, the fp32 results are
                                              // divided by it (launch_bwd_range writes them)
     const int32_t *cu;                       // packed documents, or null
+    // one time segment of every chain (strided checkpoints): per sequence or document the
+    // blocks blk0 .. blk0 + seg_len - 1, with workspace units numbered from seg[n] (clean
+    // blocks) and noisy blocks of two sub-blocks from segp[n] (tables of sequences + 1
+    // entries); carry [seq][h_v][128][128] fp32 hands the state gradient at the segment's
+    // start to the segment before it; seg null: all blocks, units by global block
+    const int *seg, *segp;
+    float *carry;
+    int blk0, seg_len;
     int n_docs;
     int n_chains;                            // sequences x v-heads
     long n_units;                            // global blocks x v-heads (set by launch_bwd)
@@ -93,5 +101,11 @@ size_t bwd_block_lds();
 // noisy blocks x v-heads).
 hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int n_more, int n_chains,
                       long n_block_units, long n_pair_units, hipStream_t s);
+// The segment tables of a segmented backward: for segments k = 0 .. n_seg - 1 of seg_len
+// blocks of L positions, seg[k][n] = the blocks of sequences 0 .. n - 1 inside segment k and
+// segp[k][n] = their noisy blocks of two sub-blocks (n = 0 .. n_seq); lengths from cu
+// (packed) or T.
+hipError_t launch_bwd_seg_plan(const int32_t *cu, int n_seq, int T, int L, int seg_len, int n_seg, int *seg,
+                               int *segp, hipStream_t s);
 
 }  // namespace bdgdn

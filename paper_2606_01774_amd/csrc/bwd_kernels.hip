@@ -770,7 +770,23 @@ __device__ __forceinline__ long unit_of(const BwdArgs &a, long t, long &gblk, in
 // boundaries, so a block lies inside one document.
 __device__ __forceinline__ void block_unit(const BwdArgs &a, long gblk, int &n, long &p0, int &nvalid)
 {
-    if (a.cu) {
+    if (a.seg) {
+        // a segment's unit: the last sequence n with seg[n] <= gblk (one with no blocks in
+        // the segment has seg[n] == seg[n + 1] and is passed over), block blk0 + gblk - seg[n]
+        int lo = 0, hi = a.n_chains / a.h_v;
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (a.seg[mid] <= gblk)
+                lo = mid;
+            else
+                hi = mid;
+        }
+        n = lo;
+        const long r0 = a.cu ? a.cu[n] : (long)n * a.T, r1 = a.cu ? a.cu[n + 1] : r0 + a.T;
+        p0 = r0 + (a.blk0 + gblk - a.seg[n]) * a.L;
+        const long rem = r1 - p0;
+        nvalid = rem < 0 ? 0 : (rem < a.L ? (int)rem : a.L);
+    } else if (a.cu) {
         p0 = gblk * a.L;
         int lo = 0, hi = a.n_docs;   // the last document with cu[d] <= p0
         while (hi - lo > 1) {
@@ -1024,7 +1040,24 @@ __device__ __forceinline__ void pair_unit(Smem &sm, const BwdArgs &a, long t, in
     const int L2 = 2 * a.L;
     long p0, ga;   // its first row; the global index of its first sub-block
     int nv;        // its rows
-    if (a.cu) {
+    if (a.seg) {
+        // a segment's noisy block: the last sequence n with segp[n] <= m, its noisy block
+        // (blk0 / 2) + m - segp[n] (blk0 and the segment length are even)
+        int lo = 0, hi = a.n_chains / a.h_v;
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (a.segp[mid] <= m)
+                lo = mid;
+            else
+                hi = mid;
+        }
+        const long lm = m - a.segp[lo];
+        const long r0 = a.cu ? a.cu[lo] : (long)lo * a.T, r1 = a.cu ? a.cu[lo + 1] : r0 + a.T;
+        p0 = r0 + (a.blk0 + 2 * lm) * a.L;
+        const long rem = r1 - p0;
+        nv = rem < 0 ? 0 : (rem < L2 ? (int)rem : L2);
+        ga = a.seg[lo] + 2 * lm;
+    } else if (a.cu) {
         p0 = m * L2;   // documents start on block boundaries
         int lo = 0, hi = a.n_docs;   // the last document with cu[d] <= p0
         while (hi - lo > 1) {
@@ -1258,23 +1291,42 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
         r1 = r0 + a.T;
     }
     const int nb = (int)((r1 - r0 + a.L - 1) / a.L);
-    // global index of the chain's first block (documents start on block boundaries), so that
-    // block b is gb0 + b with no division in the loop
-    const long gb0 = a.cu ? r0 / a.L : (long)n * a.nblk;
+    // the blocks walked, blo .. bhi - 1, and the workspace unit of block b, gb0 + b: all the
+    // chain's blocks by global index (documents start on block boundaries), or those of one
+    // time segment numbered from seg[n]; the walk starts from dht where the chain ends in it,
+    // else from the gradient the next segment left in carry, and ends in dh0 at the chain's
+    // start, else in carry
+    int blo = 0, bhi = nb;
+    long gb0 = a.cu ? r0 / a.L : (long)n * a.nblk;
+    bool from_dht = true, to_dh0 = true;
+    if (a.seg) {
+        blo = a.blk0;
+        bhi = nb < a.blk0 + a.seg_len ? nb : a.blk0 + a.seg_len;
+        // no blocks of this chain in the segment: nothing to do, but for an empty chain,
+        // whose dh0 is dht, in the first segment
+        if (bhi <= blo && !(nb == 0 && a.blk0 == 0)) return;
+        gb0 = a.seg[n] - blo;
+        from_dht = nb <= a.blk0 + a.seg_len;
+        to_dh0 = a.blk0 == 0;
+    }
     const size_t SS = (size_t)DD * DD;
     const long qks = (long)a.h_qk * DD;
     // dh tiles: wave w holds rows (128 / NW) w .. + 128 / NW - 1 (RT row tiles) of the TC columns
     const int rw = (DD / NW) * wave;
     float dh[RT][CT][4];
     const float *dht = a.dht ? a.dht + ((size_t)n * a.h_v + h) * SS : nullptr;
+    float *carry = a.seg ? a.carry + ((size_t)n * a.h_v + h) * SS : nullptr;
     const float sg = a.range[0];
 #pragma unroll
     for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
         for (int tn = 0; tn < CT; ++tn)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                dh[tl][tn][j] = dht ? dht[(rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] * sg : 0.f;
+            for (int j = 0; j < 4; ++j) {
+                const int e = (rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr;
+                // the carry holds dh as the walk keeps it (times sigma)
+                dh[tl][tn][j] = !from_dht ? carry[e] : (dht ? dht[e] * sg : 0.f);
+            }
     // wait for these loads here, once: left pending into the loop, they would make every
     // step wait for all outstanding loads (the prefetch of the next blocks included)
 #pragma unroll
@@ -1360,7 +1412,7 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
         for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
             for (int tn = 0; tn < CT; ++tn) dhb[((rw / 16 + tl) * 8 + v0 / 16 + tn) * 64] = hv[tl][tn];
-        if (b > 1) fetch(b - 2, nxt);
+        if (b - 2 >= blo) fetch(b - 2, nxt);
         __syncthreads();
         {   // Z = (U K) dh_b: one 16 x 16 tile per wave (2 CT tiles over NW = 2 CT waves), stored transposed
             const int m0 = 16 * (wave / CT), n0 = 16 * (wave % CT);
@@ -1383,24 +1435,25 @@ __global__ void __launch_bounds__(64 * NW) bdgdn_bwd_scan_kernel(BwdArgs a)
     };
     // three sets: block b's operands were loaded two steps earlier
     Ops o0, o1, o2;
-    if (nb > 0) fetch(nb - 1, o0);
-    if (nb > 1) fetch(nb - 2, o1);
-    for (int b = nb - 1; b >= 0; b -= 3) {
+    if (bhi - blo > 0) fetch(bhi - 1, o0);
+    if (bhi - blo > 1) fetch(bhi - 2, o1);
+    for (int b = bhi - 1; b >= blo; b -= 3) {
         step(b, o0, o2);
-        if (b == 0) break;
+        if (b == blo) break;
         step(b - 1, o1, o0);
-        if (b == 1) break;
+        if (b == blo + 1) break;
         step(b - 2, o2, o1);
     }
-    if (a.dh0) {
-        float *d0 = a.dh0 + ((size_t)n * a.h_v + h) * SS;
+    float *d0 = !to_dh0 ? carry : (a.dh0 ? a.dh0 + ((size_t)n * a.h_v + h) * SS : nullptr);
+    if (d0) {
+        const float f = to_dh0 ? a.range[1] : 1.f;
 #pragma unroll
         for (int tl = 0; tl < RT; ++tl)
 #pragma unroll
             for (int tn = 0; tn < CT; ++tn)
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    d0[(rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] = dh[tl][tn][j] * a.range[1];
+                    d0[(rw + 16 * tl + 4 * g4 + j) * DD + v0 + 16 * tn + rr] = dh[tl][tn][j] * f;
     }
 }
 
@@ -1503,6 +1556,37 @@ hipError_t launch_bwd_range(bool bf16_out, const RangeArgs &r, hipStream_t s)
 }
 
 size_t bwd_block_lds() { return sizeof(Smem); }
+
+// The segment tables: thread k walks the sequences, counting the blocks of each inside
+// segment k (and its noisy blocks of two sub-blocks, the last one possibly half).
+__global__ void __launch_bounds__(64) bdgdn_bwd_seg_plan_kernel(const int32_t *cu, int n_seq, int T, int L,
+                                                                int seg_len, int n_seg, int *seg, int *segp)
+{
+    const int k = blockIdx.x * 64 + threadIdx.x;
+    if (k >= n_seg) return;
+    int *o = seg + (long)k * (n_seq + 1), *op = segp + (long)k * (n_seq + 1);
+    int acc = 0, accp = 0;
+    for (int n = 0; n < n_seq; ++n) {
+        o[n] = acc;
+        op[n] = accp;
+        const long len = cu ? (long)cu[n + 1] - cu[n] : T;
+        const long nb = (len + L - 1) / L, rest = nb - (long)k * seg_len;
+        const int cnt = rest <= 0 ? 0 : (rest < seg_len ? (int)rest : seg_len);
+        acc += cnt;
+        accp += (cnt + 1) / 2;
+    }
+    o[n_seq] = acc;
+    op[n_seq] = accp;
+}
+
+hipError_t launch_bwd_seg_plan(const int32_t *cu, int n_seq, int T, int L, int seg_len, int n_seg, int *seg,
+                               int *segp, hipStream_t s)
+{
+    if (n_seg <= 0 || n_seq <= 0 || L <= 0 || seg_len <= 0) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(bdgdn_bwd_seg_plan_kernel, dim3((n_seg + 63) / 64), dim3(64), 0, s, cu, n_seq, T, L, seg_len,
+                       n_seg, seg, segp);
+    return hipGetLastError();
+}
 
 hipError_t launch_bwd(bool bf16_out, const BwdArgs &a, const BwdView *more, int n_more, int n_chains,
                       long n_block_units, long n_pair_units, hipStream_t s)

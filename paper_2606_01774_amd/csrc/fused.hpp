@@ -1100,6 +1100,17 @@ __device__ __forceinline__ void run_chain(const ScanArgs &a, unsigned char *smem
         base = (long)seq * a.T;
         len = a.T;
     }
+    // seed states by global block: documents start on block boundaries, sequences own
+    // ceil(T / L) blocks each
+    long gblk0 = a.cu ? base / a.L : (long)seq * a.nblk;
+    if constexpr (K::kSeeds) {
+        if (a.seg) {   // one time segment of the chain, its seeds indexed from seg[seq]
+            const long off = (long)a.blk0 * a.L, cap = (long)a.seg_len * a.L;
+            len = len > off ? (len - off < cap ? len - off : cap) : 0;
+            base += off;
+            gblk0 = a.seg[seq];
+        }
+    }
     const int hq = h / (a.h_v / a.h_qk);
     const int v0 = vt * K::BV;
     typename K::Chain c;
@@ -1130,9 +1141,6 @@ __device__ __forceinline__ void run_chain(const ScanArgs &a, unsigned char *smem
     const long state_off = ((long)seq * a.h_v + h) * DK * a.dv + v0;
     c.h0 = a.h0 ? a.h0 + state_off : nullptr;
     if constexpr (K::kSeeds) {
-        // seed states by global block: documents start on block boundaries, sequences own
-        // ceil(T / L) blocks each
-        const long gblk0 = a.cu ? base / a.L : (long)seq * a.nblk;
         c.bs = static_cast<typename K::SeedT *>(a.bs) + (gblk0 * a.h_v + h) * DK * a.dv + v0;
         c.bs_blk = (long)a.h_v * DK * a.dv;
     } else {

@@ -45,6 +45,11 @@ struct ScanArgs {
                          // fp16 (the backward's recomputation), or null
     int T, L, nblk, h_qk, h_v, dv;
     int nl;              // noisy block of the small-block one-kernel forward (L is its clean chunk)
+    // one time segment of every chain (the backward's strided checkpoints; seeds kernels
+    // only): blocks blk0 .. blk0 + seg_len - 1 of each sequence or document, whose seeds are
+    // indexed from seg[sequence]; seg null: all blocks, indexed by global block
+    const int *seg;
+    int blk0, seg_len;
     int n_chains, n_vt;
     float scale;
     int n_order;

@@ -353,6 +353,53 @@ def test_bwd_train_validation_and_workspace():
     assert _bwd(ok, ws=FAKE, ws_bytes=need - 1) == bd.BDGDN_ERR_WORKSPACE
 
 
+def _seg(desc, cu, k):
+    lib = bd.load_library()
+    cu_h = None if cu is None else (ctypes.c_int32 * len(cu))(*cu)
+    return lib.bdgdn_bwd_train_workspace_segmented(ctypes.byref(desc), cu_h, k)
+
+
+def test_bwd_segmented_workspace():
+    """The time-segmented backward's workspace: checkpoints at the segment starts after the
+    first and the state-gradient carry (one fp32 state per (sequence, v-head) each), two
+    segment tables, then the per-block layout for the first segment's blocks."""
+    lib = bd.load_library()
+    state = 128 * 128 * 4
+    unit = 128 * 128 * (2 + 2) + 32 * 128 * 2 + 4   # per (block, v-head), as in one pass
+    d = _desc(batch=2, seqlen=4096)                    # 128 blocks per sequence, 4 v-heads
+    full = lib.bdgdn_bwd_train_workspace(ctypes.byref(d))
+    assert _seg(d, None, 1) == full
+    for k in (2, 3, 4, 8, 100, 128, 1000):
+        S = -(-128 // k)
+        n_seg = -(-128 // S)
+        body = (n_seg - 1) * 2 * 4 * state + 2 * 4 * state + 2 * n_seg * 3 * 4 + 2 * min(128, S) * 4 * unit
+        got = _seg(d, None, k)
+        assert body <= got < body + 8 * 1024, k
+    assert _seg(d, None, 4) < full // 3     # 32 of 128 blocks per sequence
+    assert _seg(d, None, 0) == 0
+    # packed: segments of ceil(the longest document's blocks / k); a document contributes
+    # min(its blocks, the segment) to the first segment
+    cu = [0, 64, 64, 64 + 4096, 64 + 4096 + 1000]      # blocks 2, 0, 128, 32
+    p = _desc(seqlen=cu[-1], num_seqs=4)
+    S = 32
+    body = 3 * 4 * 4 * state + 4 * 4 * state + 2 * 4 * 5 * 4 + (2 + 0 + 32 + 32) * 4 * unit
+    assert body <= _seg(p, cu, 4) < body + 8 * 1024
+    assert _seg(p, None, 4) == 0                       # packing needed
+    assert _seg(p, [0, 64, 64, 4160, 5000], 4) == 0    # offsets must end at seqlen
+    # blocks of 64: sub-blocks of 32, segments of an even number of them
+    d64 = _desc(seqlen=4096, block=64)                 # 128 sub-blocks
+    S = 44                                             # ceil(128 / 3) = 43, made even
+    body = 2 * 4 * state + 4 * state + 2 * 3 * 2 * 4 + S * 4 * unit
+    assert body <= _seg(d64, None, 3) < body + 8 * 1024
+    # the per-step shapes are never segmented
+    f32 = _desc(dtype=bd.BDGDN_F32, out_dtype=bd.BDGDN_F32, seqlen=4096)
+    assert _seg(f32, None, 4) == lib.bdgdn_bwd_train_workspace(ctypes.byref(f32))
+    # below every segmented size (and the full one) the call is refused before any launch
+    smallest = min(_seg(d, None, k) for k in range(2, 129))
+    assert smallest < full
+    assert _bwd(d, ws=FAKE, ws_bytes=smallest - 1) == bd.BDGDN_ERR_WORKSPACE
+
+
 def test_views_validation():
     lib = bd.load_library()
     ok = _desc()
