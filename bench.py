@@ -646,13 +646,24 @@ def main():
             bd.bdgdn_bwd_train_views(d["q"], d["k"], d["v"], d["g"], d["beta"], bviews, gdo, block=w.block,
                                      grads=bvgrads, workspace=bws, stream=stream)
         bvms = time_protocol(bvstep, stream, flush, iters=10, repeats=3, trim=1)[0]
+        # the same backward in four time segments (strided clean checkpoints): the workspace
+        # the library needs for them, the same gradients bit for bit
+        sseg = 4
+        sws = torch.empty(bd.bdgdn_bwd_train_workspace_segmented(bdesc, None, sseg), dtype=torch.uint8, device=dev)
+
+        def bsstep():
+            bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
+                               d["betan"], gdo, gdon, block=w.block, workspace=sws, grads=bgrads, stream=stream)
+        bsms = time_protocol(bsstep, stream, flush, iters=10, repeats=3, trim=1)[0]
         result["backward"] = {
             "workload": w.name, "ms_per_call": bms, "tokens_per_s": tokens / (bms * 1e-3),
             "kernels": "bdgdn_k2_scan_states_kernel (seed states) + bdgdn_bwd_noisy_kernel + "
                        "bdgdn_bwd_scan_kernel + bdgdn_bwd_clean_kernel",
             "workspace_bytes": bws.numel(),
-            "views2_ms_per_call": bvms, "views2_tokens_per_s": 3 * w.tokens / (bvms * 1e-3)}
-        del bws, bgrads, bvgrads, bviews
+            "views2_ms_per_call": bvms, "views2_tokens_per_s": 3 * w.tokens / (bvms * 1e-3),
+            "segmented": {"segments": sseg, "workspace_bytes": sws.numel(), "ms_per_call": bsms,
+                          "tokens_per_s": tokens / (bsms * 1e-3)}}
+        del bws, sws, bgrads, bvgrads, bviews
         torch.cuda.empty_cache()
         # the other training workloads: the tiny fp32 one (the per-step fp32 backward), the
         # grouped-value one (blocks of 64: the block form with noisy blocks of two sub-blocks)
@@ -687,6 +698,14 @@ def main():
                                 trim=1 if piters >= 10 else 0)[0]
             per_step[key] = {"workload": pw.name, "ms_per_call": pms, "tokens_per_s": 2 * pw.tokens / (pms * 1e-3),
                              "workspace_bytes": pws.numel(), "kernels": kern}
+            if key != "tiny_f32":   # the block form in eight time segments
+                del pws
+                pws = torch.empty(bd.bdgdn_bwd_train_workspace_segmented(pdesc, pcu, 8), dtype=torch.uint8,
+                                  device=dev)
+                psms = time_protocol(pstep, stream, flush, warmup=pwarm, iters=piters, repeats=prep,
+                                     trim=1 if piters >= 10 else 0)[0]
+                per_step[key]["segmented"] = {"segments": 8, "workspace_bytes": pws.numel(), "ms_per_call": psms,
+                                              "tokens_per_s": 2 * pw.tokens / (psms * 1e-3)}
             del pin, pws, pgrads
             torch.cuda.empty_cache()
         result["backward"]["other_workloads"] = per_step
