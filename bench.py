@@ -54,6 +54,17 @@ def algorithmic_bytes_train(w, out_bytes=None):
     return 2 * w.tokens * per_row
 
 
+def algorithmic_bytes_bwd(w, up_bytes=4):
+    """Bytes the two-stream backward must move once: every forward input read (q, k per q/k
+    head, v, g, beta per v head), the upstream gradients of o and o~ read (up_bytes each),
+    and the fp32 gradients of every input written, for both streams; the seeds, state
+    gradients and any workspace traffic are the schedule's, not counted."""
+    in_b = 2 if w.dtype == "bf16" else 4
+    read = 2 * w.h_qk * w.d_k * in_b + w.h_v * w.d_v * in_b + 2 * w.h_v * 4 + w.h_v * w.d_v * up_bytes
+    written = 4 * (2 * w.h_qk * w.d_k + w.h_v * w.d_v + 2 * w.h_v)
+    return 2 * w.tokens * (read + written)
+
+
 def model_flops_train(w, chunk=64):
     """Work model: clean 6d^2 + 10Cd per (token, v-head) with C = 64, noisy
     2d^2 + 12Ld; the Gram terms (4Cd + 4Ld) once per q/k head; the triangular solve
@@ -655,8 +666,11 @@ def main():
             bd.bdgdn_bwd_train(d["q"], d["k"], d["v"], d["g"], d["beta"], d["qn"], d["kn"], d["vn"], d["gn"],
                                d["betan"], gdo, gdon, block=w.block, workspace=sws, grads=bgrads, stream=stream)
         bsms = time_protocol(bsstep, stream, flush, iters=10, repeats=3, trim=1)[0]
+        bab = algorithmic_bytes_bwd(w)
         result["backward"] = {
             "workload": w.name, "ms_per_call": bms, "tokens_per_s": tokens / (bms * 1e-3),
+            "algorithmic_bytes": bab, "frac_hbm": bab / (bms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "byte_model": "inputs and fp32 upstream gradients read, fp32 gradients written, once",
             "kernels": "bdgdn_k2_scan_states_kernel (seed states) + bdgdn_bwd_noisy_kernel + "
                        "bdgdn_bwd_scan_kernel + bdgdn_bwd_clean_kernel",
             "workspace_bytes": bws.numel(),
@@ -696,7 +710,9 @@ def main():
             kern, pwarm, piters, prep = paths[key]
             pms = time_protocol(pstep, stream, flush, warmup=pwarm, iters=piters, repeats=prep,
                                 trim=1 if piters >= 10 else 0)[0]
+            pab = algorithmic_bytes_bwd(pw)
             per_step[key] = {"workload": pw.name, "ms_per_call": pms, "tokens_per_s": 2 * pw.tokens / (pms * 1e-3),
+                             "algorithmic_bytes": pab, "frac_hbm": pab / (pms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                              "workspace_bytes": pws.numel(), "kernels": kern}
             if key != "tiny_f32":   # the block form in eight time segments
                 del pws
