@@ -31,6 +31,11 @@
 //     v-head), in 32-column tiles (the columns are independent):
 //     dh_(b-1) = gamma_n dh_b + c_b - K^T (U K) dh_b with U = Gamma T^T D from phase 1;
 //  3. every clean block in parallel from its seed and the gradient at its end.
+// In time segments (BwdArgs::seg; the strided clean checkpoints of the checkpoint build) the
+// same three phases run over one segment of every chain at a time, last segment first: the
+// seeds come from the segment's checkpoint, the scan starts from the gradient the later
+// segment left in the carry and leaves its own there, and the units are numbered inside the
+// segment by the segment tables (bdgdn_bwd_seg_plan_kernel).
 // Products are MFMA tiles on fp16 operands with fp32 accumulation: k-contiguous operands by
 // 16-byte LDS reads, the others by the LDS transpose load, and results that are the next
 // product's operand kept in registers; M = (I + A)^-1 by the register-resident doubling solve
