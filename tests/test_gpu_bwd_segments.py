@@ -4,8 +4,8 @@ fewest time segments that fit, and every gradient (and dh0) equals the one-pass 
 for bit, over ragged tails, packed documents (an empty one among them), grouped value
 heads, blocks of 16, 20, 32 and 64 (noisy blocks of two sub-blocks), an initial state with
 a final-state gradient, bf16 upstream gradients and two noisy views; then the 4 x 4096
-training shape in four segments, under 256 MiB of workspace, whole."""
-import ctypes
+training shape in four segments, under 256 MiB of workspace, and the grouped-value and packed
+128k workloads in eight, whole."""
 import math
 
 import numpy as np
@@ -156,3 +156,28 @@ def test_segmented_training_workload_under_256_mib():
     torch.cuda.synchronize()
     for name in NAMES:
         assert torch.equal(got[name].cpu(), ref[name]), name
+
+
+@pytest.mark.parametrize("name", ["GVA_16K", "VARLEN_128K"])
+def test_segmented_full_workloads_equal_one_pass(name):
+    """The grouped-value workload (blocks of 64: the pair kernel) and the packed 128k workload
+    (32 documents) in eight segments, whole: every gradient equal to the one-pass call's."""
+    w = getattr(W, name)
+    raw = W.make_train(w)
+    d = {k: v.cuda() for k, v in raw.items() if isinstance(v, torch.Tensor)}
+    cu = raw.get("cu_seqlens")
+    rng = np.random.default_rng(7)
+    shape = (w.batch, w.seqlen, w.h_v, w.d_v)
+    do = torch.from_numpy(rng.standard_normal(shape, dtype=np.float32)).cuda()
+    don = torch.from_numpy(rng.standard_normal(shape, dtype=np.float32)).cuda()
+    desc = _desc(d["q"], d["v"], w.block, cu, torch.float32)
+    budget = bd.bdgdn_bwd_train_workspace_segmented(desc, cu, 8)
+    print(f"segmented {w.name}: {budget} of {bd.bdgdn_bwd_train_workspace(desc)} bytes, "
+          f"{_segments_run(desc, cu, budget)} segments", flush=True)
+    ref = _bwd(d, do, don, w.block, cu, None, None)
+    ref = {k: v.cpu() for k, v in ref.items()}
+    torch.cuda.empty_cache()
+    got = _bwd(d, do, don, w.block, cu, None, None, workspace=torch.empty(budget, dtype=torch.uint8, device="cuda"))
+    torch.cuda.synchronize()
+    for n in NAMES:
+        assert torch.equal(got[n].cpu(), ref[n]), n
